@@ -1,0 +1,414 @@
+"""numpy front door to the CPU oracle (test infrastructure only).
+
+Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may
+import this module.  It loads oracle/libhqoracle.so (built from hq_oracle.c by
+oracle/build.py) and never touches the HIP library.  Every function mirrors
+one step of the paper's pipeline; see hq_oracle.c for the passages.
+"""
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+from . import build as _build
+
+E8, D4, A2, Z = 0, 1, 2, 3
+LATTICES = {"E8": E8, "D4": D4, "A2": A2, "Z": Z}
+DIM = {E8: 8, D4: 4, A2: 2, Z: 1}
+
+OK, ERR_ARG, ERR_CAPACITY, ERR_OVERFLOW, ERR_CORRUPT = 0, -1, -3, -4, -6
+
+_lib = None
+
+
+class _Params(C.Structure):
+    _fields_ = [
+        ("tile", C.c_int32),
+        ("lattice", C.c_int32),
+        ("substream", C.c_int32),
+        ("rice_k", C.c_int32),
+        ("alpha", C.c_float),
+        ("norm_fp16", C.c_int32),
+        ("rht_seed", C.c_uint64),
+        ("rotation", C.c_int32),
+        ("dither", C.c_int32),
+        ("rot_seed", C.c_uint64),
+        ("dither_seed", C.c_uint64),
+    ]
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        path = _build.LIB
+        if not os.path.exists(path) or os.path.getmtime(path) < os.path.getmtime(_build.SRC):
+            _build.build(force=True)
+        L = C.CDLL(path)
+        p = C.c_void_p
+        i64 = C.c_int64
+        L.hqo_alpha.restype = C.c_float
+        L.hqo_alpha.argtypes = [C.c_int, C.c_double]
+        L.hqo_alpha64.restype = C.c_double
+        L.hqo_alpha64.argtypes = [C.c_int, C.c_double]
+        L.hqo_nsm.restype = C.c_double
+        L.hqo_nsm.argtypes = [C.c_int]
+        L.hqo_covolume.restype = C.c_double
+        L.hqo_covolume.argtypes = [C.c_int]
+        L.hqo_splitmix64.restype = C.c_uint64
+        L.hqo_splitmix64.argtypes = [C.c_uint64, C.c_uint64]
+        L.hqo_sign.restype = C.c_int
+        L.hqo_sign.argtypes = [C.c_uint64, i64]
+        L.hqo_philox4x32_10.argtypes = [p, p, p]
+        L.hqo_fwht_f32.argtypes = [p, C.c_int]
+        L.hqo_fwht_f64.argtypes = [p, C.c_int]
+        L.hqo_fwht_i64.argtypes = [p, C.c_int]
+        L.hqo_f32_to_f16.restype = C.c_uint16
+        L.hqo_f32_to_f16.argtypes = [C.c_float]
+        L.hqo_f16_to_f32.restype = C.c_float
+        L.hqo_f16_to_f32.argtypes = [C.c_uint16]
+        L.hqo_quantize.argtypes = [C.c_int, p, i64, p]
+        L.hqo_margins.argtypes = [C.c_int, p, p, i64, p]
+        L.hqo_strip.argtypes = [C.c_int, p, i64, p]
+        L.hqo_unstrip.argtypes = [C.c_int, p, i64, p]
+        L.hqo_zigzag.restype = C.c_uint32
+        L.hqo_zigzag.argtypes = [C.c_int32]
+        L.hqo_unzigzag.restype = C.c_int32
+        L.hqo_unzigzag.argtypes = [C.c_uint32]
+        L.hqo_rice_kstar.restype = C.c_int
+        L.hqo_rice_kstar.argtypes = [C.c_double]
+        L.hqo_rice_k_auto.restype = C.c_int
+        L.hqo_rice_k_auto.argtypes = [i64, i64]
+        L.hqo_rice_length.restype = i64
+        L.hqo_rice_length.argtypes = [C.c_uint32, C.c_int]
+        L.hqo_rice_put_substream.restype = i64
+        L.hqo_rice_put_substream.argtypes = [p, p, C.c_int, p, p]
+        L.hqo_rice_get_substream.restype = i64
+        L.hqo_rice_get_substream.argtypes = [p, p, i64, C.c_int, p, p]
+        L.hqo_dither_block.argtypes = [C.c_int, C.c_uint64, i64, i64, p]
+        L.hqo_frontend.restype = C.c_int
+        L.hqo_frontend.argtypes = [p, p, i64, i64, i64, i64, p, p, p]
+        L.hqo_pack.restype = C.c_int
+        L.hqo_pack.argtypes = [p, p, i64, i64, i64, p, i64, i64, p, p, p]
+        L.hqo_unpack.restype = C.c_int
+        L.hqo_unpack.argtypes = [p, p, p, p, i64, i64, i64, p]
+        L.hqo_backend.restype = C.c_int
+        L.hqo_backend.argtypes = [p, p, p, i64, i64, i64, p]
+        L.hqo_encode.restype = C.c_int
+        L.hqo_encode.argtypes = [p, p, i64, i64, i64, i64, p, i64, i64, p, p, p, p]
+        L.hqo_decode.restype = C.c_int
+        L.hqo_decode.argtypes = [p, p, p, p, p, i64, i64, i64, p]
+        L.hqo_weight_factors.argtypes = [p, p, i64, i64, p]
+        L.hqo_act_prep.argtypes = [p, i64, i64, C.c_int, C.c_uint64, p, p]
+        L.hqo_gemm_blockscaled.argtypes = [p, p, p, p, i64, i64, i64, C.c_int, p]
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return a.ctypes.data_as(C.c_void_p) if a is not None else None
+
+
+@dataclass
+class Params:
+    """Codec parameters, the knobs of the paper's parameter table (Sec. 4.9)."""
+    tile: int = 128
+    lattice: int = E8
+    alpha: float = 1.0
+    substream: int = 512
+    rice_k: int = -1
+    norm_fp16: bool = False
+    rht_seed: int = 0
+    rotation: int = 0
+    dither: bool = False
+    rot_seed: int = 0
+    dither_seed: int = 0
+
+    def c(self):
+        return _Params(self.tile, self.lattice, self.substream, self.rice_k, np.float32(self.alpha),
+                       int(self.norm_fp16), self.rht_seed & (2**64 - 1), self.rotation,
+                       int(self.dither), self.rot_seed & (2**64 - 1), self.dither_seed & (2**64 - 1))
+
+
+# ---------------------------------------------------------------- constants
+
+def nsm(lat):
+    return lib().hqo_nsm(lat)
+
+
+def covolume(lat):
+    return lib().hqo_covolume(lat)
+
+
+def alpha(lat, snr_db):
+    """fp32 alpha of App. B eq. alpha-calib."""
+    return np.float32(lib().hqo_alpha(lat, float(snr_db)))
+
+
+def alpha64(lat, snr_db):
+    return lib().hqo_alpha64(lat, float(snr_db))
+
+
+def sigma2_vor(lat):
+    """Per-coordinate Voronoi second moment G * V^(2/m) of the realization."""
+    return nsm(lat) * covolume(lat) ** (2.0 / DIM[lat])
+
+
+# ---------------------------------------------------------------- generators
+
+def splitmix64(seed, j):
+    return lib().hqo_splitmix64(seed & (2**64 - 1), j)
+
+
+def signs(seed, n, start=0):
+    L = lib()
+    return np.array([L.hqo_sign(seed & (2**64 - 1), start + j) for j in range(n)], dtype=np.int8)
+
+
+def philox(ctr, key):
+    c = np.asarray(ctr, dtype=np.uint32)
+    k = np.asarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    lib().hqo_philox4x32_10(_ptr(c), _ptr(k), _ptr(out))
+    return out
+
+
+def dither_block(lat, seed, row, col0):
+    u = np.zeros(8, dtype=np.float32)
+    lib().hqo_dither_block(lat, seed & (2**64 - 1), row, col0, _ptr(u))
+    return u[:DIM[lat]].copy()
+
+
+# ---------------------------------------------------------------- transforms
+
+def fwht(v):
+    """Unnormalized Sylvester FWHT of the last axis (stages h = 1 .. n/2)."""
+    v = np.array(v, copy=True)
+    n = v.shape[-1]
+    flat = v.reshape(-1, n)
+    fn = {np.dtype(np.float32): lib().hqo_fwht_f32, np.dtype(np.float64): lib().hqo_fwht_f64,
+          np.dtype(np.int64): lib().hqo_fwht_i64}[flat.dtype]
+    flat = np.ascontiguousarray(flat)
+    for r in range(flat.shape[0]):
+        row = flat[r]
+        fn(row.ctypes.data_as(C.c_void_p), n)
+    return flat.reshape(v.shape)
+
+
+def f32_to_f16_bits(x):
+    L = lib()
+    return np.array([L.hqo_f32_to_f16(float(v)) for v in np.ravel(x)], dtype=np.uint16)
+
+
+def f16_bits_to_f32(h):
+    L = lib()
+    return np.array([L.hqo_f16_to_f32(int(v)) for v in np.ravel(h)], dtype=np.float32)
+
+
+# ---------------------------------------------------------------- lattices
+
+def quantize(lat, z):
+    z = np.ascontiguousarray(z, dtype=np.float32)
+    m = DIM[lat]
+    assert z.size % m == 0
+    c = np.zeros(z.shape, dtype=np.int32)
+    lib().hqo_quantize(lat, _ptr(z), z.size // m, _ptr(c))
+    return c
+
+
+def margins(lat, z, c):
+    z = np.ascontiguousarray(z, dtype=np.float32)
+    c = np.ascontiguousarray(c, dtype=np.int32)
+    m = DIM[lat]
+    out = np.zeros(z.size // m, dtype=np.float64)
+    lib().hqo_margins(lat, _ptr(z), _ptr(c), z.size // m, _ptr(out))
+    return out
+
+
+def lattice_points(lat, c):
+    """Integer codes -> points of R^m (fp64)."""
+    p = np.asarray(c, dtype=np.float64).copy()
+    if lat == A2:
+        p[..., 0::2] *= np.sqrt(3.0)
+    return p
+
+
+def strip(lat, c):
+    c = np.ascontiguousarray(c, dtype=np.int32)
+    s = np.zeros(c.shape, dtype=np.uint32)
+    lib().hqo_strip(lat, _ptr(c), c.size // DIM[lat], _ptr(s))
+    return s
+
+
+def unstrip(lat, s):
+    s = np.ascontiguousarray(s, dtype=np.uint32)
+    c = np.zeros(s.shape, dtype=np.int32)
+    lib().hqo_unstrip(lat, _ptr(s), s.size // DIM[lat], _ptr(c))
+    return c
+
+
+def zigzag(v):
+    return lib().hqo_zigzag(int(v))
+
+
+def unzigzag(m):
+    return lib().hqo_unzigzag(int(m))
+
+
+# ---------------------------------------------------------------- Rice
+
+def rice_kstar(p):
+    return lib().hqo_rice_kstar(float(p))
+
+
+def rice_k_auto(count, total):
+    return lib().hqo_rice_k_auto(int(count), int(total))
+
+
+def rice_length(m, k):
+    return lib().hqo_rice_length(int(m), int(k))
+
+
+def rice_put(params: Params, sym, k0, k1=None):
+    sym = np.ascontiguousarray(sym, dtype=np.uint32)
+    k = np.array([k0, k0 if k1 is None else k1], dtype=np.int32)
+    words = np.zeros(int(sym.size * (2 + 32)) + 64, dtype=np.uint32)
+    P = params.c()
+    nbits = lib().hqo_rice_put_substream(C.byref(P), _ptr(sym), sym.size, _ptr(k), _ptr(words))
+    return words[: (nbits + 31) // 32].copy(), nbits
+
+
+def rice_get(params: Params, words, S, k0, k1=None):
+    words = np.ascontiguousarray(words, dtype=np.uint32)
+    k = np.array([k0, k0 if k1 is None else k1], dtype=np.int32)
+    sym = np.zeros(S, dtype=np.uint32)
+    P = params.c()
+    used = lib().hqo_rice_get_substream(C.byref(P), _ptr(words), words.size, S, _ptr(k), _ptr(sym))
+    return sym, used
+
+
+# ---------------------------------------------------------------- codec
+
+@dataclass
+class Stream:
+    """A whole encoded tensor: payload words, sub-stream word offsets, k bytes, norms."""
+    payload: np.ndarray
+    offsets: np.ndarray
+    kparam: np.ndarray
+    norms: np.ndarray
+    rows: int
+    cols: int
+    payload_bits: int
+
+    @property
+    def end(self):
+        return int(self.offsets[-1])
+
+
+def capacity_words(params: Params, rows, cols):
+    """A generous capacity for the oracle (it grows nothing on the fly)."""
+    return int(rows * cols * 2 + 64)
+
+
+def frontend(params: Params, x, row0=0, want_z=False):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    rows, cols = x.shape
+    codes = np.zeros((rows, cols), dtype=np.int32)
+    tpr = cols // params.tile
+    norms = np.zeros((rows, tpr), dtype=np.uint16 if params.norm_fp16 else np.float32)
+    zin = np.zeros((rows, cols), dtype=np.float32) if want_z else None
+    P = params.c()
+    rc = lib().hqo_frontend(C.byref(P), _ptr(x), rows, cols, cols, row0, _ptr(codes), _ptr(norms),
+                            _ptr(zin))
+    if rc not in (OK, ERR_OVERFLOW):
+        raise ValueError(f"hqo_frontend failed: {rc}")
+    return codes, norms, zin, rc
+
+
+def pack(params: Params, codes, row0=0, word0=0, payload=None, offsets=None, kparam=None,
+         total_rows=None):
+    codes = np.ascontiguousarray(codes, dtype=np.int32)
+    rows, cols = codes.shape
+    total_rows = total_rows or (row0 + rows)
+    spr = cols // params.substream
+    if payload is None:
+        payload = np.zeros(capacity_words(params, total_rows, cols), dtype=np.uint32)
+    if offsets is None:
+        offsets = np.zeros(total_rows * spr + 1, dtype=np.uint32)
+    if kparam is None:
+        kparam = np.zeros(total_rows * spr, dtype=np.uint8)
+    bits = C.c_int64(0)
+    P = params.c()
+    rc = lib().hqo_pack(C.byref(P), _ptr(codes), rows, cols, row0, _ptr(payload), payload.size,
+                        word0, _ptr(offsets), _ptr(kparam), C.byref(bits))
+    if rc != OK:
+        raise ValueError(f"hqo_pack failed: {rc}")
+    return payload, offsets, kparam, bits.value
+
+
+def unpack(params: Params, payload, offsets, kparam, rows, cols, row0=0):
+    codes = np.zeros((rows, cols), dtype=np.int32)
+    P = params.c()
+    rc = lib().hqo_unpack(C.byref(P), _ptr(np.ascontiguousarray(payload, dtype=np.uint32)),
+                          _ptr(np.ascontiguousarray(offsets, dtype=np.uint32)),
+                          _ptr(np.ascontiguousarray(kparam, dtype=np.uint8)), rows, cols, row0,
+                          _ptr(codes))
+    return codes, rc
+
+
+def backend(params: Params, codes, norms, row0=0):
+    codes = np.ascontiguousarray(codes, dtype=np.int32)
+    rows, cols = codes.shape
+    y = np.zeros((rows, cols), dtype=np.float32)
+    norms = np.ascontiguousarray(norms)
+    P = params.c()
+    rc = lib().hqo_backend(C.byref(P), _ptr(codes), _ptr(norms), rows, cols, row0, _ptr(y))
+    if rc != OK:
+        raise ValueError(f"hqo_backend failed: {rc}")
+    return y
+
+
+def encode(params: Params, x, row0=0, want_codes=False, want_z=False):
+    """Front end + pack of a whole rows x cols matrix into a fresh stream."""
+    codes, norms, zin, rc = frontend(params, x, row0=row0, want_z=want_z)
+    payload, offsets, kparam, bits = pack(params, codes, row0=row0)
+    end = int(offsets[-1])
+    st = Stream(payload[:end].copy(), offsets, kparam, norms, x.shape[0], x.shape[1], bits)
+    if want_codes or want_z:
+        return st, codes, zin
+    return st
+
+
+def decode(params: Params, st: Stream):
+    codes, rc = unpack(params, st.payload, st.offsets, st.kparam, st.rows, st.cols)
+    if rc != OK:
+        raise ValueError(f"hqo_unpack failed: {rc}")
+    return backend(params, codes, st.norms)
+
+
+def weight_factors(params: Params, norms, rows, cols):
+    g = np.zeros((rows, cols // params.tile), dtype=np.float32)
+    P = params.c()
+    lib().hqo_weight_factors(C.byref(P), _ptr(np.ascontiguousarray(norms)), rows, cols, _ptr(g))
+    return g
+
+
+def act_prep(a, tile, rht_seed):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    M, K = a.shape
+    xq = np.zeros((M, K), dtype=np.int8)
+    sx = np.zeros(M, dtype=np.float32)
+    lib().hqo_act_prep(_ptr(a), M, K, tile, rht_seed & (2**64 - 1), _ptr(xq), _ptr(sx))
+    return xq, sx
+
+
+def gemm_blockscaled(codes, g, xq, sx, tile):
+    codes = np.ascontiguousarray(codes, dtype=np.int32)
+    N, K = codes.shape
+    M = xq.shape[0]
+    out = np.zeros((M, N), dtype=np.float64)
+    lib().hqo_gemm_blockscaled(_ptr(codes), _ptr(np.ascontiguousarray(g, dtype=np.float32)),
+                               _ptr(np.ascontiguousarray(xq, dtype=np.int8)),
+                               _ptr(np.ascontiguousarray(sx, dtype=np.float32)), M, N, K, tile,
+                               _ptr(out))
+    return out

@@ -1,0 +1,299 @@
+"""Pins of the oracle's whole codec against the paper's printed numbers and
+closed forms (CPU only): realized rates at 21 dB, stripping savings, marginal
+entropy vs the lattice ideal, realized SNR vs target, the int8 code budget,
+the capacity bound, subtractive-dither unbiasedness (App. A), KV storage,
+and the block-scaled GEMM against a dense fp64 product."""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+
+LATS = [O.E8, O.D4, O.A2, O.Z]
+NAMES = {O.E8: "E8", O.D4: "D4", O.A2: "A2", O.Z: "Z"}
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def gauss(n_tiles=4096, seed=42):
+    rng = np.random.default_rng(seed)
+    return rng.standard_normal((n_tiles * 128 // 512, 512)).astype(np.float32)
+
+
+def op_point(name, bps):
+    pts = json.load(open(os.path.join(GOLDEN, "operating_points.json")))["points"]
+    for p in pts:
+        if p["lattice"] == name and abs(p["bps"] - bps) < 1e-9:
+            return p["snr_db"]
+    raise KeyError((name, bps))
+
+
+def snr_db(x, y):
+    x = x.astype(np.float64)
+    return 10 * np.log10((x ** 2).sum() / ((x - y.astype(np.float64)) ** 2).sum())
+
+
+@pytest.mark.parametrize("lat,paper", [(O.E8, 3.74), (O.D4, 3.77), (O.A2, 3.81), (O.Z, 3.84)])
+def test_rate_at_21db_matches_paper(lat, paper):
+    # Sec. 4.6 "Effect on the achievable bit-rate": empirical Rice rates at
+    # 21 dB on Gaussian input.
+    x = gauss()
+    P = O.Params(lattice=lat, alpha=O.alpha(lat, 21.0))
+    st = O.encode(P, x)
+    assert abs(st.payload_bits / x.size - paper) < 0.03
+
+
+def best_k_rate(sym_rows, nclass=1):
+    """Rice bits with the per-sub-stream best k (brute force) for each of the
+    nclass interleaved symbol classes, per scalar."""
+    total = 0
+    for s in sym_rows:
+        s = s.astype(np.int64)
+        for c in range(nclass):
+            sc = s[c::nclass]
+            total += min(int(((sc >> k) + 1 + k).sum()) for k in range(16))
+    return total / sym_rows.size
+
+
+@pytest.mark.parametrize("lat,saving", [(O.E8, 1.0), (O.A2, 0.5)])
+def test_stripping_saves_paper_bits(lat, saving):
+    # Sec. 4.6: removing the strip raises the E8 rate by 1.0 bps and A2 by 0.5.
+    x = gauss(1024)
+    P = O.Params(lattice=lat, alpha=O.alpha(lat, 21.0))
+    codes, _, _, _ = O.frontend(P, x)
+    raw = np.vectorize(O.zigzag, otypes=[np.uint32])(codes.reshape(-1)).reshape(-1, 512)
+    st = O.encode(P, x)
+    stripped = st.payload_bits / x.size
+    unstripped = best_k_rate(raw, 2 if lat == O.A2 else 1)
+    assert abs((unstripped - stripped) - saving) < 0.06
+
+
+def entropy_bits(v):
+    _, c = np.unique(v, return_counts=True)
+    p = c / c.sum()
+    return -(p * np.log2(p)).sum()
+
+
+@pytest.mark.parametrize("lat", LATS)
+@pytest.mark.parametrize("snr", [21.0, 27.0])
+def test_marginal_entropy_meets_lattice_ideal(lat, snr):
+    # App. B (strip optimality): the per-scalar sum of marginal entropies of
+    # the stripped symbols is R_D + 1/2 log2(2 pi e G) to ~1e-2 bps, and the
+    # Rice rate sits ~0.1 bps above it.
+    x = gauss(8192)
+    P = O.Params(lattice=lat, alpha=O.alpha(lat, snr))
+    codes, _, _, _ = O.frontend(P, x)
+    m = O.DIM[lat]
+    sym = O.strip(lat, codes.reshape(-1)).reshape(-1, m)
+    h = sum(entropy_bits(sym[:, i]) for i in range(m)) / m
+    r_ideal = 0.5 * math.log2(10 ** (snr / 10)) + 0.5 * math.log2(2 * math.pi * math.e * O.nsm(lat))
+    assert abs(h - r_ideal) < 0.03
+    st = O.encode(P, x)
+    gap = st.payload_bits / x.size - r_ideal
+    assert 0.03 < gap < 0.2
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2])
+def test_realized_snr_tracks_target(lat):
+    # App. B: realized SNR within ~0.1 dB of the target across 20-30 dB (the
+    # empirical Voronoi second moment is within 5% of MSE_vor).
+    x = gauss(2048)
+    for target in (20.0, 25.0, 30.0):
+        P = O.Params(lattice=lat, alpha=O.alpha(lat, target))
+        y = O.decode(P, O.encode(P, x))
+        assert abs(snr_db(x, y) - target) < 0.1
+
+
+def test_realized_snr_z_within_20pct():
+    x = gauss(2048)
+    for target in (20.0, 25.0, 30.0):
+        P = O.Params(lattice=O.Z, alpha=O.alpha(O.Z, target))
+        y = O.decode(P, O.encode(P, x))
+        assert abs(snr_db(x, y) - target) < 10 * math.log10(1.2)
+
+
+def test_int8_code_budget():
+    # App. B int8 budget: |c_i| <= |z_i| + rho <= alpha sqrt(n) + 2 for 2E8,
+    # which stays <= 127 up to alpha = 11.05 (about 4.6 bps); the codes track
+    # N(0, alpha^2) and the largest seen is a few sigma.
+    x = gauss(8192)
+    alpha_max = (127 - 2) / math.sqrt(128)
+    for snr in (20.0, 23.0, 26.0):
+        a = O.alpha(O.E8, snr)
+        P = O.Params(lattice=O.E8, alpha=a)
+        codes, _, _, _ = O.frontend(P, x)
+        assert np.abs(codes).max() <= a * math.sqrt(128) + 2
+        assert abs(codes.std() / a - 1.0) < 0.02
+        assert 3.0 < np.abs(codes).max() / a < 6.0
+    assert O.alpha(O.E8, 26.25) <= alpha_max < O.alpha(O.E8, 26.35)
+
+
+def capacity_bits_per_tile(lat, alpha, n, k, dither=False):
+    """Worst-case Rice bits of one tile (n symbols) at parameter k: every
+    symbol costs 1 + k bits plus floor(m / 2^k) unary zeros, and the symbols
+    sum to at most 2 sum|c| + (extra per block): zz(s) <= 2|s| <= |c| + 1 and
+    comb <= |c7| + 3 for E8; sum|c| <= sqrt(n) |c| <= sqrt(n) (|z| + rho sqrt(n/m))."""
+    m = O.DIM[lat]
+    rho = {O.E8: 2.0, O.D4: 1.0, O.A2: 2 / math.sqrt(3), O.Z: 0.5}[lat]
+    cn = alpha * math.sqrt(n) + rho * math.sqrt(n / m) * (2 if dither else 1)
+    sum_abs = math.sqrt(n) * cn
+    extra = {O.E8: 8 + 3, O.D4: 4 + 1, O.A2: 2 + 1, O.Z: 1}[lat] * (n // m)
+    return n * (1 + k) + (2 * sum_abs + extra) / 2 ** k
+
+
+def test_capacity_bound_holds():
+    # The bound used to size payload buffers (P8b) is never exceeded, here on
+    # Gaussian tiles and on the adversarial one-hot tile.
+    for lat in LATS:
+        for snr in (10.0, 22.0, 30.0):
+            a = O.alpha(lat, snr)
+            x = gauss(512)
+            x[0, :128] = 0
+            x[0, 5] = 1.0  # all energy on one coordinate
+            P = O.Params(lattice=lat, alpha=a)
+            st = O.encode(P, x)
+            words = np.diff(st.offsets.astype(np.int64))
+            for s in range(words.size):
+                k = st.kparam[s] & 15
+                bound = 4 * max(capacity_bits_per_tile(lat, a, 128, kk) for kk in range(k, k + 1))
+                assert words[s] * 32 <= bound + 31
+
+
+def test_zero_tile_and_overflow():
+    x = gauss(64)
+    x[3, 128:256] = 0.0
+    P = O.Params(lattice=O.E8, alpha=O.alpha(O.E8, 22.0))
+    st = O.encode(P, x)
+    y = O.decode(P, st)
+    assert np.all(y[3, 128:256] == 0.0)
+    assert st.norms[3, 1] == 0.0
+    Pf = O.Params(lattice=O.E8, alpha=O.alpha(O.E8, 22.0), norm_fp16=True)
+    big = gauss(64) * 1e5
+    _, _, _, rc = O.frontend(Pf, big)
+    assert rc == O.ERR_OVERFLOW
+
+
+def test_append_equals_one_shot():
+    # KV quantize-on-append: encoding rows in chunks continues the stream
+    # exactly where a one-shot encode of all rows would be.
+    x = gauss(256)
+    P = O.Params(lattice=O.E8, alpha=O.alpha(O.E8, 10.0), rotation=1, rot_seed=9, dither=True,
+                 dither_seed=77, norm_fp16=True)
+    codes, norms, _, _ = O.frontend(P, x)
+    payload, offsets, kparam, bits = O.pack(P, codes)
+    rows = x.shape[0]
+    pay2 = np.zeros_like(payload)
+    off2 = np.zeros_like(offsets)
+    kp2 = np.zeros_like(kparam)
+    word = 0
+    for r0 in range(0, rows, 16):
+        c_chunk, n_chunk, _, _ = O.frontend(P, x[r0:r0 + 16], row0=r0)
+        assert np.array_equal(c_chunk, codes[r0:r0 + 16])
+        assert np.array_equal(n_chunk, norms[r0:r0 + 16])
+        O.pack(P, c_chunk, row0=r0, word0=word, payload=pay2, offsets=off2, kparam=kp2,
+               total_rows=rows)
+        word = int(off2[(r0 + 16) * 1])
+    assert np.array_equal(off2, offsets) and np.array_equal(kp2, kparam)
+    assert np.array_equal(pay2[:offsets[-1]], payload[:offsets[-1]])
+
+
+def test_kv_storage_bytes_per_scalar():
+    # Sec. 6.6: E8 at 4 bps with a float16 norm per 128-vector is ~0.516 B/scalar.
+    x = gauss(2048)
+    P = O.Params(lattice=O.E8, alpha=O.alpha(O.E8, op_point("E8", 4.0)), norm_fp16=True)
+    st = O.encode(P, x)
+    b = (st.payload_bits / 8 + 2 * st.norms.size) / x.size
+    assert abs(b - 0.516) < 0.004
+
+
+def dither_draws(lat, xrow, R, rotation=1, snr=10.0):
+    """R reconstructions of one 512-wide row under independent dither seeds."""
+    outs = []
+    for r in range(R):
+        P = O.Params(lattice=lat, alpha=O.alpha(lat, snr), rotation=rotation, rot_seed=5,
+                     dither=True, dither_seed=1000 + r, norm_fp16=True)
+        outs.append(O.decode(P, O.encode(P, xrow[None, :]))[0])
+    return np.array(outs, dtype=np.float64)
+
+
+@pytest.mark.parametrize("lat", LATS)
+def test_dither_error_uniform_zero_mean(lat):
+    # Thm. schuchman / Cor. variance: the error is uniform on the Voronoi cell,
+    # independent of x: zero mean and per-coordinate variance sigma^2_Vor in
+    # lattice units, so Var <q, x_hat> = sigma^2_Vor |q|^2 (r / (alpha sqrt n))^2.
+    rng = np.random.default_rng(8)
+    x = rng.standard_normal(512).astype(np.float32)
+    x[:4] *= 10
+    R = 400
+    y = dither_draws(lat, x, R)
+    a = float(O.alpha(lat, 10.0))
+    r = np.array([np.float32(np.linalg.norm(x[t * 128:(t + 1) * 128].astype(np.float32)))
+                  for t in range(4)])
+    r = O.f16_bits_to_f32(O.f32_to_f16_bits(r)).astype(np.float64)
+    unit = np.repeat(r / (a * math.sqrt(128)), 128)  # lattice unit per coordinate
+    e = (y - x.astype(np.float64)) / unit  # error in lattice units
+    s2 = O.sigma2_vor(lat)
+    assert abs(e.var() / s2 - 1) < 0.03
+    t = e.mean(axis=0) / (e.std(axis=0) / math.sqrt(R))
+    assert np.mean(np.abs(t) > 3.5) < 0.01
+    # isotropy: off-diagonal covariance small against the variance
+    cov = np.cov(e[:, :16].T)
+    off = cov - np.diag(np.diag(cov))
+    assert np.abs(off).max() < 0.25 * s2
+    # <q, x_hat> unbiased with the closed-form variance
+    q = rng.standard_normal((64, 512))
+    ip = y @ q.T  # R x 64
+    ip0 = q @ x.astype(np.float64)
+    var_th = s2 * ((q * unit) ** 2).sum(axis=1)
+    tt = (ip.mean(axis=0) - ip0) / np.sqrt(var_th / R)
+    assert np.mean(np.abs(tt) > 3.5) < 0.05
+    assert np.all(np.abs(ip.var(axis=0) / var_th - 1) < 0.35)
+
+
+def test_no_dither_is_biased_per_vector():
+    # Prop. qjl: without dither the reconstruction of a fixed vector is
+    # deterministic, so its error (the per-vector bias) is non-zero.
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal(512).astype(np.float32)
+    P = O.Params(lattice=O.E8, alpha=O.alpha(O.E8, 10.0), rotation=1, rot_seed=5)
+    y1 = O.decode(P, O.encode(P, x[None]))[0]
+    y2 = O.decode(P, O.encode(P, x[None]))[0]
+    assert np.array_equal(y1, y2)
+    assert np.abs(y1 - x).max() > 0
+
+
+def test_gemm_blockscaled_equals_dense_fp64():
+    # Sec. 4.1 / Fig. 1: the RHT cancels against the activations' RHT, so
+    # sum_t g c . (H D a) equals the dense product of the decoded weights with
+    # the decoded (int8, then inverse-RHT) activations.
+    rng = np.random.default_rng(10)
+    N, K, M, n = 48, 512, 24, 128
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    a = rng.standard_normal((M, K)).astype(np.float32)
+    a[:, 7] *= 30
+    P = O.Params(lattice=O.E8, alpha=O.alpha(O.E8, op_point("E8", 4.0)), rht_seed=33)
+    codes, norms, _, _ = O.frontend(P, w)
+    g = O.weight_factors(P, norms, N, K)
+    xq, sx = O.act_prep(a, n, 33)
+    out = O.gemm_blockscaled(codes, g, xq, sx, n)
+    # dense reference in fp64
+    d = O.signs(33, K).astype(np.float64)
+    w_hat = np.zeros((N, K))
+    for t in range(K // n):
+        w_hat[:, t * n:(t + 1) * n] = O.fwht(codes[:, t * n:(t + 1) * n].astype(np.float64)) \
+            * g[:, t:t + 1].astype(np.float64)
+    w_hat *= d
+    a_hat = xq.astype(np.float64) * sx[:, None].astype(np.float64)
+    for t in range(K // n):
+        a_hat[:, t * n:(t + 1) * n] = O.fwht(a_hat[:, t * n:(t + 1) * n]) / n
+    a_hat *= d
+    ref = a_hat @ w_hat.T
+    assert np.abs(out - ref).max() <= 1e-9 * np.abs(ref).max()
+    # and both approximate the unquantized product
+    exact = a.astype(np.float64) @ w.astype(np.float64).T
+    assert np.linalg.norm(out - exact) / np.linalg.norm(exact) < 0.1
+    # the decoded weights equal the oracle's decoder output
+    st = O.encode(P, w)
+    assert np.allclose(O.decode(P, st), w_hat, rtol=0, atol=1e-6 * np.abs(w_hat).max())
