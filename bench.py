@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Headline benchmark of the HyperQuant codec on one MI355X.
+
+Metric: encode + decode GB/s of bf16 input (E8 lattice, 4 bits per scalar)
+and its fraction of HBM peak.  Workload: the whole Llama-3.1-8B-shaped linear
+stack (32 layers x {q, k, v, o, gate, up, down}, 6.98e9 bf16 weights,
+N(0, 0.02^2) with log-uniform per-output-channel scales, seeded synthetic
+data).  One step = encode all 224 matrices (RHT, normalize, E8, strip, Rice,
+offset scan) and then decode all of them back to bf16 (Rice decode, unstrip,
+inverse RHT, denormalize), every input resident in HBM.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Prints one JSON line.  The CPU oracle is timed on a bounded sample of the
+same workload beside it (cpu_baseline).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, vendor figure
+INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA, vendor figure
+
+
+def parse_args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--bps", type=float, default=4.0)
+    ap.add_argument("--snr", type=float, default=None,
+                    help="plan at this SNR instead of the library's bps calibration")
+    ap.add_argument("--layers", type=int, default=32)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm", action="store_true")
+    return ap.parse_args()
+
+
+def build_workload(H, W, layers, bps, dev, snr=None):
+    """Plans, resident bf16 inputs, encoded-stream buffers and decode outputs."""
+    mats = []
+    for layer in range(layers):
+        for idx, (name, out_f, in_f) in enumerate(W.LLAMA_LINEARS):
+            seed = W.llama_linear_seed(layer, idx)
+            plan = H.hq_plan(128, H.HQ_E8, bps, seed, -1, in_f, snr_db=snr)
+            x = W.llama_linear(layer, idx, device=dev)
+            s = H.EncodedStream(plan, out_f, device=dev)
+            y = torch.empty_like(x)
+            mats.append({"name": name, "layer": layer, "plan": plan, "x": x, "s": s, "y": y})
+    return mats
+
+
+def encode_all(H, mats):
+    for m in mats:
+        H.hq_encode(m["plan"], m["x"], m["s"])
+
+
+def decode_all(H, mats):
+    for m in mats:
+        H.hq_decode(m["plan"], m["s"], out=m["y"])
+
+
+def cpu_baseline(mats, seconds):
+    """The oracle as it stands, single-threaded, on row slices of layer 0's
+    seven matrices, repeated until `seconds` of CPU work.  Its alpha is the
+    oracle's own E8 at 4 bps operating point."""
+    from oracle import oracle as O
+    from paper_2606_23406_amd import workloads as W
+    pts = json.load(open(os.path.join(ROOT, "tests", "golden", "operating_points.json")))["points"]
+    snr = [p["snr_db"] for p in pts if p["lattice"] == "E8" and p["bps"] == 4.0][0]
+    names = [n for n, _, _ in W.LLAMA_LINEARS]
+    rows_per = {"q": 256, "k": 128, "v": 128, "o": 256, "gate": 512, "up": 512, "down": 256}
+    sample = []
+    for m in mats[:7]:
+        x = m["x"][:rows_per[m["name"]]].float().cpu().numpy()
+        seed = W.llama_linear_seed(m["layer"], names.index(m["name"]))
+        sample.append((O.Params(tile=128, lattice=O.E8, alpha=O.alpha(O.E8, snr), rht_seed=seed), x))
+    n_scalars = 0
+    t_enc = t_dec = 0.0
+    t_start = time.time()
+    while time.time() - t_start < seconds:
+        for P, x in sample:
+            t0 = time.perf_counter()
+            st = O.encode(P, x)
+            t1 = time.perf_counter()
+            O.decode(P, st)
+            t2 = time.perf_counter()
+            t_enc += t1 - t0
+            t_dec += t2 - t1
+            n_scalars += x.size
+    gbs = 2.0 * n_scalars / (t_enc + t_dec) / 1e9
+    desc = ("oracle encode+decode, 1 thread, on row slices of layer 0 "
+            "(q 256, k 128, v 128, o 256, gate 512, up 512, down 256 rows), "
+            f"{n_scalars / 1e6:.1f}M scalars in {t_enc + t_dec:.1f}s")
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle", "sample": desc,
+            "encode_GBs": round(2.0 * n_scalars / t_enc / 1e9, 4),
+            "decode_GBs": round(2.0 * n_scalars / t_dec / 1e9, 4)}
+
+
+def gemm_extra(H, W, mats, dev):
+    """Dequant-fused int8 GEMM: gate-shaped E8@4 weights x 4096 bf16 tokens."""
+    gate = [m for m in mats if m["name"] == "gate"][0]
+    plan, s = gate["plan"], gate["s"]
+    a = W.activations(device=dev)
+    M, N, K = a.shape[0], s.rows, plan.cols
+    ws = torch.empty(H.hq_gemm_workspace_bytes(plan, M, N), dtype=torch.uint8, device=dev)
+    out = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    xq, sx = H.hq_act_prep(plan, a)
+    codes, g = H.hq_decode_int8(plan, s)
+    for _ in range(3):
+        H.hq_dequant_gemm_int8(plan, s, a, workspace=ws, out=out)
+        H.hq_gemm_int8_blockscaled(plan, xq, sx, codes, g, out=out)
+    torch.cuda.synchronize()
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    reps = 10
+    e0.record()
+    for _ in range(reps):
+        H.hq_gemm_int8_blockscaled(plan, xq, sx, codes, g, out=out)
+    e1.record()
+    for _ in range(reps):
+        H.hq_dequant_gemm_int8(plan, s, a, workspace=ws, out=out)
+    e2.record()
+    torch.cuda.synchronize()
+    t_gemm = e0.elapsed_time(e1) / reps * 1e-3
+    t_e2e = e1.elapsed_time(e2) / reps * 1e-3
+    ops = 2.0 * M * N * K
+    return {"workload": f"W {N}x{K} E8@4 Rice stream, A {M}x{K} bf16 (1% outlier channels x30)",
+            "gemm_ms": round(t_gemm * 1e3, 4), "gemm_TOPS": round(ops / t_gemm / 1e12, 2),
+            "gemm_frac_int8_peak": round(ops / t_gemm / 1e12 / INT8_PEAK_TOPS, 4),
+            "end_to_end_ms": round(t_e2e * 1e3, 4),
+            "end_to_end_TOPS": round(ops / t_e2e / 1e12, 2)}
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the codec needs no collective and this build runs on a "
+              f"single MI355X (asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+    from paper_2606_23406_amd import hq as H
+    from paper_2606_23406_amd import workloads as W
+    H.lib()
+    dev = "cuda"
+    torch.cuda.set_device(0)
+
+    mats = build_workload(H, W, args.layers, args.bps, dev, args.snr)
+    n_scalars = sum(m["x"].numel() for m in mats)
+    n_tiles = n_scalars // 128
+    n_subs = n_scalars // 512
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        encode_all(H, mats)
+        decode_all(H, mats)
+    for m in mats:
+        m["s"].reset_stats()
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        a, b, c = ev[k]
+        a.record(stream)
+        encode_all(H, mats)
+        b.record(stream)
+        decode_all(H, mats)
+        c.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    t_enc = sum(a.elapsed_time(b) for a, b, _ in ev) * 1e-3 / args.steps
+    t_dec = sum(b.elapsed_time(c) for _, b, c in ev) * 1e-3 / args.steps
+    t_step = t_enc + t_dec
+
+    # realized rate: stats accumulated over the timed steps
+    payload_bits = sum(m["s"].read_stats()["payload_bits"] for m in mats) / args.steps
+    status = [m["s"].read_stats()["status"] for m in mats]
+    bps = payload_bits / n_scalars
+    stream_bytes = payload_bits / 8 + 4 * n_tiles + 5 * n_subs  # payload + fp32 norms + offset/k
+    enc_bytes = 2 * n_scalars + stream_bytes
+    dec_bytes = stream_bytes + 2 * n_scalars
+    value = 2.0 * n_scalars / t_step / 1e9
+    enc_gbs = enc_bytes / t_enc / 1e9
+    dec_gbs = dec_bytes / t_dec / 1e9
+
+    out = {
+        "metric": "encode+decode GB/s of bf16 input (E8, 4 bps) and % of HBM peak, 1 GPU",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(t_step * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "Llama-3.1-8B-shaped linear stack, 32 layers x {q,k,v,o,gate,up,down}, "
+                               "6.98e9 bf16 weights, E8 lattice at 4 bps, RHT tile 128, encode then "
+                               "decode per step",
+                   "scalars": n_scalars, "matrices": len(mats), "bps_target": args.bps,
+                   "bps_realized": round(bps, 4)},
+        "pct_hbm_peak": round(100.0 * (enc_bytes + dec_bytes) / t_step / 1e9 / HBM_PEAK_GBS, 2),
+        "roofline": {"bound": "hbm", "kernel": "hq_encode_kernel (E8, bf16 in)",
+                     "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(enc_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes_per_scalar": round(enc_bytes / n_scalars, 4)},
+        "decode_roofline": {"bound": "hbm", "kernel": "hq_decode_kernel (E8, bf16 out)",
+                            "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                            "algorithmic_bytes_per_scalar": round(dec_bytes / n_scalars, 4)},
+        "encode_ms": round(t_enc * 1e3, 4),
+        "decode_ms": round(t_dec * 1e3, 4),
+        "encode_GBs_bf16_in": round(2.0 * n_scalars / t_enc / 1e9, 1),
+        "decode_GBs_bf16_out": round(2.0 * n_scalars / t_dec / 1e9, 1),
+        "wall_s_timed": round(wall, 3),
+        "device_status_ok": all(s == 0 for s in status),
+    }
+    if not args.no_gemm:
+        out["gemm_int8"] = gemm_extra(H, W, mats, dev)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(mats, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

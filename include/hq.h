@@ -1,0 +1,228 @@
+/*
+ * hq.h -- C ABI of the MI355X (gfx950) HyperQuant codec library, libhq.so.
+ *
+ * HyperQuant ("HyperQuant: A Rate-Distortion-Optimal Quantization Pipeline
+ * for Large Language and Diffusion Models") encodes every tile of n_tile
+ * consecutive scalars along a row as:
+ *   RHT (eq. rht, Sec. 3.1 / 4.1) -> [signs rotation, Sec. 4.2] ->
+ *   Normalize (Sec. 4.3) -> [subtractive dither, Sec. 4.4 / App. A] ->
+ *   nearest point of the E8 / D4 / A2 / Z integer realization (Sec. 4.5) ->
+ *   Strip + zig-zag (Sec. 4.6) -> Rice code (Sec. 3.3 / 4.7) in
+ *   offset-indexed sub-streams (Sec. 5.3),
+ * and decodes by the exact inverse.  The int8 GEMM path (Sec. 4.8, 6.3)
+ * multiplies post-RHT lattice codes with per-token int8 activations.
+ *
+ * Conventions for every entry point:
+ *  - Every call returns hq_status; 0 is success, negative values are errors.
+ *    No C++ exception crosses this boundary.
+ *  - Pointers named d_* or documented as "device" are device memory of the
+ *    current HIP device, allocated and owned by the caller.  The library
+ *    allocates device memory only inside hq_plan (small constants: sign
+ *    bitmasks), released by hq_plan_destroy.
+ *  - `stream` is a hipStream_t passed as void*.  All device work is enqueued
+ *    on it asynchronously; no call synchronizes the device.  Errors found on
+ *    the device (capacity, fp16 norm overflow, corrupt sub-stream) are
+ *    reported in the optional hq_stats block and become visible when the
+ *    caller synchronizes.
+ *  - Matrices are row-major; tiles run along a row (the input/contraction
+ *    dimension of a weight, the head dimension of a KV vector).
+ */
+#ifndef HQ_H
+#define HQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HQ_OK = 0,
+  HQ_ERR_INVALID_ARG = -1,   /* bad shape, null pointer, out-of-range knob */
+  HQ_ERR_UNSUPPORTED = -2,   /* valid for the method, not built for gfx950 here */
+  HQ_ERR_CAPACITY = -3,      /* caller buffers too small */
+  HQ_ERR_OVERFLOW = -4,      /* fp16 norm overflow or a non-finite input tile */
+  HQ_ERR_HIP = -5,           /* a HIP runtime call failed */
+  HQ_ERR_CORRUPT = -6,       /* a sub-stream does not decode within its words */
+  HQ_ERR_NO_CALIBRATION = -7 /* no SNR <-> bps table for this lattice / k */
+} hq_status;
+
+typedef enum { HQ_E8 = 0, HQ_D4 = 1, HQ_A2 = 2, HQ_Z = 3 } hq_lattice;
+typedef enum { HQ_BF16 = 0, HQ_FP32 = 1, HQ_FP16 = 2, HQ_INT8 = 3 } hq_dtype;
+typedef enum { HQ_ROT_NONE = 0, HQ_ROT_SIGNS = 1 } hq_rotation;
+
+/* Options beyond the five knobs of hq_plan; all-zero means the weight-path
+   defaults (no rotation, no dither, fp32 norms, 512-symbol sub-streams, SNR
+   from the calibration table). */
+typedef struct {
+  int32_t rotation;     /* hq_rotation: the KV pre-rotation of Sec. 4.2 */
+  int32_t dither;       /* 1 = subtractive dither (Sec. 4.4), KV only */
+  uint64_t rot_seed;    /* seed of the +-1 rotation diagonal S */
+  uint64_t dither_seed; /* key of the dither generator; change per forward call */
+  int32_t norm_dtype;   /* HQ_FP32 (default) or HQ_FP16 (KV, Sec. 6.6) */
+  int32_t substream;    /* symbols per sub-stream S (Sec. 5.3); 0 = 512 */
+  int32_t use_snr;      /* 1 = take snr_db below instead of the table lookup */
+  int32_t reserved0;
+  double snr_db;        /* quantization SNR in dB (App. B) when use_snr = 1 */
+} hq_options;
+
+typedef struct hq_plan_s* hq_plan_t;
+
+/* Host-side values derived by hq_plan. */
+typedef struct {
+  float alpha;                 /* App. B eq. alpha-calib, rounded to fp32 */
+  float snr_db;                /* the SNR realizing the target bps */
+  int32_t tile, lattice, substream, rice_k;
+  int64_t cols, tiles_per_row, subs_per_row;
+  int64_t max_words_per_substream; /* deterministic capacity bound */
+  int64_t max_words_per_row;       /* = subs_per_row * max_words_per_substream */
+} hq_plan_info;
+
+/* hq_plan -- validate the knobs of the paper's problem statement (Sec. 4.9,
+ * Tab. params) and derive the codec constants.
+ *   tile      n_tile, a power of two; this build runs 128 (Sec. 4.1 default).
+ *   lattice   hq_lattice (Sec. 4.5).
+ *   bps       target payload bits per scalar (App. B); mapped to an SNR by the
+ *             library's calibration table unless opt->use_snr is set.
+ *   rht_seed  seed of the RHT sign diagonal D of eq. rht: d_j = -1 iff the top
+ *             bit of the j-th SplitMix64 output for this seed is set, for the
+ *             global column j.
+ *   rice_k    >= 0: fixed Rice parameter for every sub-stream (D4 codes its
+ *             halved symbol at max(k-1, 0), A2 both classes at k); -1: per
+ *             sub-stream, the better of the geometric optimum k* of Sec. 3.3
+ *             and k* + 1 on the sub-stream's own symbols.
+ *   cols      row length of every matrix encoded with this plan; a multiple of
+ *             the tile and of the sub-stream length.
+ *   opt       nullable hq_options.
+ * On success *out receives a plan (owned by the caller, free with
+ * hq_plan_destroy) and *info (nullable) its derived values.  Plans are
+ * immutable and may be shared by concurrent calls on different streams.
+ * Errors: HQ_ERR_INVALID_ARG, HQ_ERR_UNSUPPORTED, HQ_ERR_NO_CALIBRATION,
+ * HQ_ERR_HIP. */
+hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, int32_t rice_k,
+                  int64_t cols, const hq_options* opt, hq_plan_t* out, hq_plan_info* info);
+hq_status hq_plan_destroy(hq_plan_t plan);
+hq_status hq_plan_get_info(hq_plan_t plan, hq_plan_info* info);
+
+/* Device-side counters of an encode or decode (all fields device memory of
+ * one hq_stats block; the caller zeroes it when it wants fresh counts). */
+typedef struct {
+  unsigned long long payload_bits;  /* unpadded Rice bits written */
+  unsigned long long pad_bits;      /* padding bits to 32-bit word boundaries */
+  uint32_t status;                  /* first device error (hq_status, as uint) */
+  uint32_t overflow_tiles;          /* fp16 norm overflow / non-finite tiles */
+  uint32_t corrupt_substreams;      /* decode: sub-streams that failed to parse */
+  uint32_t clamps;                  /* int8 decode: codes clamped to +-127 */
+} hq_stats;
+
+/* An encoded matrix (Sec. 5.1 / 5.2): Rice payload plus the per-sub-stream
+ * table of Sec. 5.3 (32-bit start offsets and k) and per-tile norms.  All
+ * array members are caller-owned device memory; the scalar members are host
+ * values the library reads and advances.
+ *   payload       capacity_words 32-bit words; sub-streams are word aligned,
+ *                 bits LSB-first.  capacity_words >= rows_capacity *
+ *                 info.max_words_per_row makes HQ_ERR_CAPACITY impossible.
+ *   offsets       rows_capacity * subs_per_row + 1 absolute word offsets:
+ *                 sub-stream i occupies [offsets[i], offsets[i+1]).
+ *   kparam        rows_capacity * subs_per_row Rice parameter bytes (A2: low
+ *                 nibble k of t_y, high nibble k of n_x).
+ *   norms         rows_capacity * tiles_per_row stored tile norms (fp32, or
+ *                 fp16 bits when the plan's norm_dtype is HQ_FP16).
+ *   rows          rows encoded so far; hq_encode sets or advances it.
+ *   scan          device scratch (8-byte aligned) of scan_bytes >=
+ *                 hq_scan_bytes(plan, rows) bytes for the encoder's
+ *                 single-pass cross-workgroup prefix scan.  Zero it once before
+ *                 first use; afterwards the kernels keep it consistent
+ *                 themselves (an encode can be captured in a HIP graph and
+ *                 replayed).  Encodes that run concurrently need their own.
+ *   stats         nullable device hq_stats. */
+typedef struct {
+  uint32_t* payload;
+  int64_t capacity_words;
+  uint32_t* offsets;
+  uint8_t* kparam;
+  void* norms;
+  int64_t rows_capacity;
+  int64_t rows;
+  void* scan;
+  int64_t scan_bytes;
+  hq_stats* stats;
+} hq_stream;
+
+/* Bytes of encoder scan scratch needed to encode up to `rows` rows per call. */
+size_t hq_scan_bytes(hq_plan_t plan, int64_t rows);
+
+/* hq_encode -- the encode path of Fig. 1 on `rows` rows of x.
+ *   x       device, rows x plan.cols, element type xt (HQ_BF16 or HQ_FP32),
+ *           row stride ld elements (ld >= cols).
+ *   append  0: the rows become rows 0 .. rows-1 of s (s->rows = rows);
+ *           1: the rows continue the stream after s->rows (KV
+ *           quantize-on-append, Sec. 5.2); their dither keys use the global
+ *           row index, and the payload continues at offsets[first sub-stream]
+ *           as written by the previous encode on the same stream.
+ * Errors (synchronous): HQ_ERR_INVALID_ARG, HQ_ERR_CAPACITY (rows_capacity),
+ * HQ_ERR_HIP.  Device-side: payload capacity and fp16 overflow in s->stats. */
+hq_status hq_encode(hq_plan_t plan, const void* x, int32_t xt, int64_t rows, int64_t ld,
+                    hq_stream* s, int32_t append, void* stream);
+
+/* hq_decode -- the decode path of Fig. 1, including the explicit inverse RHT,
+ * for rows row0 .. row0+rows-1 of s into y (device, element type yt =
+ * HQ_BF16 or HQ_FP32, row stride ld).  A sub-stream whose offsets or bits are
+ * inconsistent is decoded as zeros and counted in s->stats (never read out of
+ * bounds).  Errors: HQ_ERR_INVALID_ARG, HQ_ERR_HIP. */
+hq_status hq_decode(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows, void* y,
+                    int32_t yt, int64_t ld, void* stream);
+
+/* hq_decode_int8 -- Rice decode and unstrip without the inverse RHT (Sec. 4.8
+ * Cast): the int8 lattice codes c (device, rows x cols, row stride ldc) and
+ * the per-tile factors g = r / (alpha n) (device fp32, rows x tiles_per_row),
+ * so that a decoded weight row is D H c g.  Codes beyond +-127 are clamped
+ * and counted.  E8, D4 and Z only (A2 has a sqrt3 axis): HQ_ERR_UNSUPPORTED
+ * otherwise; dithered streams are HQ_ERR_UNSUPPORTED too. */
+hq_status hq_decode_int8(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows,
+                         int8_t* codes, int64_t ldc, float* g, void* stream);
+
+/* hq_act_prep -- activation side of the GEMM: per K-tile y = H D a with the
+ * weight plan's signs (so the two rotations cancel), then per token
+ * symmetric int8 over the whole row: x_q = clamp(rint(y * 127 / amax), +-127),
+ * s_x = amax / 127.  a: device bf16 M x cols (row stride lda); xq: device
+ * int8 M x cols; sx: device fp32 [M]. */
+hq_status hq_act_prep(hq_plan_t plan, const void* a, int64_t M, int64_t lda, int8_t* xq,
+                      float* sx, void* stream);
+
+/* hq_gemm_int8_blockscaled -- out[i, r] = s_x[i] * sum_t g[r, t] *
+ * sum_{j in tile t} c[r, j] * x_q[i, j] with exact int32 tile sums on the
+ * int8 matrix cores and fp32 accumulation (N = weight rows, K = plan.cols).
+ * out: device M x N, HQ_BF16 or HQ_FP32. */
+hq_status hq_gemm_int8_blockscaled(hq_plan_t plan, const int8_t* xq, const float* sx, int64_t M,
+                                   const int8_t* codes, const float* g, int64_t N, void* out,
+                                   int32_t ot, void* stream);
+
+/* Workspace bytes for hq_dequant_gemm_int8 with M tokens and N weight rows. */
+size_t hq_gemm_workspace_bytes(hq_plan_t plan, int64_t M, int64_t N);
+
+/* hq_dequant_gemm_int8 -- Y = A W^T from a Rice-coded weight stream w (N rows
+ * of plan.cols) and bf16 activations a (device M x cols, unrotated): act
+ * prep, decode to int8, then the block-scaled int8 GEMM (Sec. 6.3).
+ * workspace: device, >= hq_gemm_workspace_bytes(plan, M, N) bytes.
+ * Errors as the three stages. */
+hq_status hq_dequant_gemm_int8(hq_plan_t plan, const hq_stream* w, int64_t N, const void* a,
+                               int64_t M, void* out, int32_t ot, void* workspace,
+                               size_t ws_bytes, void* stream);
+
+/* The library's automatic Rice-k rule for `count` symbols summing to `sum`
+ * (the geometric optimum k* of Sec. 3.3), as the kernels evaluate it. */
+int32_t hq_rice_kstar(int64_t count, int64_t sum);
+
+/* Calibration lookup (App. B): the SNR whose realized payload rate is `bps`
+ * for this lattice and Rice setting; HQ_ERR_NO_CALIBRATION if no table. */
+hq_status hq_calibrated_snr(int32_t lattice, int32_t rice_k, float bps, double* snr_db);
+
+const char* hq_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HQ_H */

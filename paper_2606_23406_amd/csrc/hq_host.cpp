@@ -1,0 +1,533 @@
+// Host side of libhq.so: plan construction, argument validation and the
+// C ABI declared in include/hq.h.  All codec arithmetic runs in the gfx950
+// kernels of hq_kernels.hip; this file derives constants and launches.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "hq_internal.h"
+
+namespace {
+
+#include "calib_table.inc"
+
+// Lattice dimension, normalized second moment G (the closed forms behind the
+// four-digit values of the paper's lattice-constant table) and covolume of
+// the integer realization (Sec. 4.5).
+int lattice_dim(int lat) { return lat == HQ_E8 ? 8 : lat == HQ_D4 ? 4 : lat == HQ_A2 ? 2 : 1; }
+
+double lattice_nsm(int lat) {
+  switch (lat) {
+    case HQ_E8: return 929.0 / 12960.0;
+    case HQ_D4: return 13.0 / (120.0 * std::sqrt(2.0));
+    case HQ_A2: return 5.0 / (36.0 * std::sqrt(3.0));
+    default: return 1.0 / 12.0;
+  }
+}
+
+double lattice_covolume(int lat) {
+  switch (lat) {
+    case HQ_E8: return 256.0;
+    case HQ_D4: return 2.0;
+    case HQ_A2: return 2.0 * std::sqrt(3.0);
+    default: return 1.0;
+  }
+}
+
+// Covering radius of the integer realization: how far the nearest point can
+// be from any input.
+double lattice_rho(int lat) {
+  switch (lat) {
+    case HQ_E8: return 2.0;
+    case HQ_D4: return 1.0;
+    case HQ_A2: return 2.0 / std::sqrt(3.0);
+    default: return 0.5;
+  }
+}
+
+// App. B, eq. alpha-calib: alpha = sqrt(SNR_lin G V^(2/N)).
+double alpha_for_snr(int lat, double snr_db) {
+  const double snr_lin = std::pow(10.0, snr_db / 10.0);
+  return std::sqrt(snr_lin * lattice_nsm(lat) *
+                   std::pow(lattice_covolume(lat), 2.0 / (double)lattice_dim(lat)));
+}
+
+// The sign of column j: -1 iff the top bit of SplitMix64's j-th output is set
+// (SplitMix64: Steele, Lea and Flood, 2014).
+bool splitmix_negative(uint64_t seed, uint64_t j) {
+  uint64_t z = seed + (j + 1) * 0x9E3779B97F4A7C15ULL;
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ULL;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBULL;
+  z ^= z >> 31;
+  return (z >> 63) != 0;
+}
+
+// Sec. 3.3: optimal Rice parameter of a geometric source, with the
+// parameter estimated from `count` symbols summing to `sum`.
+int kstar_formula(int64_t count, int64_t sum) {
+  if (count <= 0) return 0;
+  const double p = (double)count / ((double)count + (double)sum);
+  if (p >= 1.0) return 0;
+  const double ratio = -std::log(2.0 - p) / std::log(1.0 - p);
+  const double c = std::ceil(ratio);
+  if (!(c >= 1.0)) return 0;
+  if (c > 9.0e15) return HQ_KMAX;
+  const int k = 63 - __builtin_clzll((unsigned long long)(int64_t)c);
+  return std::min(k, HQ_KMAX);
+}
+
+// thr[t] = smallest sum with kstar_formula(count, sum) >= t (k* is
+// non-decreasing in the sum); 0xFFFFFFFF when no 32-bit sum reaches t.
+void kstar_thresholds(int64_t count, uint32_t* thr) {
+  thr[0] = 0;
+  for (int t = 1; t <= HQ_KMAX; ++t) {
+    int64_t lo = 0, hi = 0xFFFFFFFFLL;
+    if (kstar_formula(count, hi) < t) {
+      thr[t] = 0xFFFFFFFFu;
+      continue;
+    }
+    while (lo < hi) {
+      const int64_t mid = lo + (hi - lo) / 2;
+      if (kstar_formula(count, mid) >= t) hi = mid; else lo = mid + 1;
+    }
+    thr[t] = (uint32_t)lo;
+  }
+}
+
+int kstar_from_thresholds(const uint32_t* thr, int64_t sum) {
+  int k = 0;
+  for (int t = 1; t <= HQ_KMAX; ++t) k += (sum >= (int64_t)thr[t]) ? 1 : 0;
+  return k;
+}
+
+// Class sizes of one sub-stream (Rice class 0 and 1).
+void class_counts(int lat, int S, int64_t* n0, int64_t* n1) {
+  if (lat == HQ_D4) {
+    *n0 = 3 * S / 4;
+    *n1 = S / 4;
+  } else if (lat == HQ_A2) {
+    *n0 = S / 2;
+    *n1 = S / 2;
+  } else {
+    *n0 = S;
+    *n1 = 0;
+  }
+}
+
+// Deterministic bound on the words of one sub-stream.  Per tile the lattice
+// code satisfies |c| <= |z| + rho sqrt(n/m) (plus rho sqrt(n/m) again with
+// dither), |z| = alpha sqrt(n) r / r_s (r_s the stored norm; fp16 can round a
+// tiny norm down by up to a third); each stripped symbol is at most
+// 2 |coordinate| + 2, so a class sums to M <= T (2 sqrt(n) |c| + 2 n).  A
+// class with parameter k costs count (1 + k) + sum / 2^k bits, and the
+// encoder's k never costs more than the geometric k* of that sum.
+int64_t substream_word_bound(const hq_plan_s& p) {
+  const int n = p.tile, m = p.dim, S = p.substream;
+  const double T = (double)S / n;
+  const double fac = p.norm_fp16 ? 1.5 : 1.0;
+  const double cn = fac * (double)p.alpha * std::sqrt((double)n) * 1.001 +
+                    lattice_rho(p.lattice) * std::sqrt((double)n / m) * (p.dither ? 2.0 : 1.0);
+  const double M = T * (2.0 * std::sqrt((double)n) * cn + 2.0 * n);
+  const int64_t Mi = (int64_t)std::ceil(M) + 1;
+  int64_t n0, n1;
+  class_counts(p.lattice, S, &n0, &n1);
+  auto cost = [&](int64_t count, int k, int64_t sum) -> double {
+    return (double)count * (1 + k) + std::ldexp((double)sum, -k);
+  };
+  double worst = 0.0;
+  if (p.rice_k >= 0) {
+    const int k0 = p.rice_k;
+    const int k1 = (p.lattice == HQ_D4) ? std::max(k0 - 1, 0) : k0;
+    worst = cost(n0, k0, Mi) + (n1 ? cost(n1, k1, Mi) : 0.0);
+  } else {
+    // worst case over every class sum up to M, at the k the sum selects
+    double w0 = 0.0, w1 = 0.0;
+    const int64_t step = std::max<int64_t>(1, Mi / 200000);
+    for (int64_t s = 0; s <= Mi; s += step) {
+      const int64_t ss = std::min(Mi, s + step - 1);  // the sum is at most this in the bin
+      const int k0 = kstar_from_thresholds(p.thr[0], s);
+      w0 = std::max(w0, cost(n0, k0, ss));
+      if (p.lattice == HQ_D4) {
+        w1 = std::max(w1, cost(n1, std::max(k0 - 1, 0), ss));
+      } else if (p.lattice == HQ_A2) {
+        const int k1 = kstar_from_thresholds(p.thr[1], s);
+        w1 = std::max(w1, cost(n1, k1, ss));
+      }
+    }
+    if (p.lattice == HQ_D4) {
+      // the class-1 sum can be large while class 0 selects k = 0
+      w1 = std::max(w1, cost(n1, 0, Mi));
+    }
+    worst = w0 + w1;
+  }
+  return (int64_t)std::ceil(worst * 1.02 / 32.0) + 2;
+}
+
+bool lookup_calibration(int lat, int rice_k, double bps, double* snr) {
+  for (const hq_calib_curve& c : kCalib) {
+    if (c.lattice != lat || c.rice_k != rice_k || c.n < 2) continue;
+    for (int i = 0; i + 1 < c.n; ++i) {
+      const double b0 = c.bps[i], b1 = c.bps[i + 1];
+      if (b0 <= bps && bps <= b1 && b1 > b0) {
+        const double f = (bps - b0) / (b1 - b0);
+        *snr = c.snr0 + c.step * (i + f);
+        return true;
+      }
+    }
+    return false;
+  }
+  return false;
+}
+
+bool has_calibration(int lat, int rice_k) {
+  for (const hq_calib_curve& c : kCalib)
+    if (c.lattice == lat && c.rice_k == rice_k && c.n >= 2) return true;
+  return false;
+}
+
+hq_status hip_status(int e) { return e == 0 ? HQ_OK : HQ_ERR_HIP; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace
+
+extern "C" {
+
+const char* hq_status_string(int32_t status) {
+  switch (status) {
+    case HQ_OK: return "ok";
+    case HQ_ERR_INVALID_ARG: return "invalid argument";
+    case HQ_ERR_UNSUPPORTED: return "unsupported configuration";
+    case HQ_ERR_CAPACITY: return "buffer capacity exceeded";
+    case HQ_ERR_OVERFLOW: return "norm overflow or non-finite input";
+    case HQ_ERR_HIP: return "HIP runtime error";
+    case HQ_ERR_CORRUPT: return "corrupt sub-stream";
+    case HQ_ERR_NO_CALIBRATION: return "no calibration table for this lattice / Rice setting";
+  }
+  return "unknown status";
+}
+
+int32_t hq_rice_kstar(int64_t count, int64_t sum) {
+  uint32_t thr[HQ_KMAX + 1];
+  kstar_thresholds(count, thr);
+  return kstar_from_thresholds(thr, sum);
+}
+
+hq_status hq_calibrated_snr(int32_t lattice, int32_t rice_k, float bps, double* snr_db) {
+  if (!snr_db || lattice < HQ_E8 || lattice > HQ_Z) return HQ_ERR_INVALID_ARG;
+  if (!has_calibration(lattice, rice_k)) return HQ_ERR_NO_CALIBRATION;
+  if (!lookup_calibration(lattice, rice_k, (double)bps, snr_db)) return HQ_ERR_INVALID_ARG;
+  return HQ_OK;
+}
+
+hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, int32_t rice_k,
+                  int64_t cols, const hq_options* opt, hq_plan_t* out, hq_plan_info* info) {
+  if (!out) return HQ_ERR_INVALID_ARG;
+  *out = nullptr;
+  hq_options o;
+  std::memset(&o, 0, sizeof(o));
+  if (opt) o = *opt;
+  if (lattice < HQ_E8 || lattice > HQ_Z) return HQ_ERR_INVALID_ARG;
+  const int m = lattice_dim(lattice);
+  if (tile < m || tile <= 0 || (tile & (tile - 1)) != 0) return HQ_ERR_INVALID_ARG;
+  const int S = o.substream ? o.substream : HQ_SUB;
+  if (S <= 0 || S % tile != 0 || cols <= 0 || cols % tile != 0 || cols % S != 0)
+    return HQ_ERR_INVALID_ARG;
+  if (rice_k < -1 || rice_k > HQ_KMAX) return HQ_ERR_INVALID_ARG;
+  if (o.rotation != HQ_ROT_NONE && o.rotation != HQ_ROT_SIGNS) return HQ_ERR_INVALID_ARG;
+  if (o.norm_dtype != 0 && o.norm_dtype != HQ_FP32 && o.norm_dtype != HQ_FP16)
+    return HQ_ERR_INVALID_ARG;
+  if (tile != HQ_TILE || S != HQ_SUB) return HQ_ERR_UNSUPPORTED;
+  if (cols > (int64_t)1 << 31) return HQ_ERR_UNSUPPORTED;
+
+  double snr;
+  if (o.use_snr) {
+    snr = o.snr_db;
+    if (!std::isfinite(snr) || snr < -30.0 || snr > 80.0) return HQ_ERR_INVALID_ARG;
+  } else {
+    if (!(bps > 0.0f) || !std::isfinite(bps)) return HQ_ERR_INVALID_ARG;
+    if (!has_calibration(lattice, rice_k)) return HQ_ERR_NO_CALIBRATION;
+    if (!lookup_calibration(lattice, rice_k, (double)bps, &snr)) return HQ_ERR_INVALID_ARG;
+  }
+
+  hq_plan_s* p = new (std::nothrow) hq_plan_s();
+  if (!p) return HQ_ERR_INVALID_ARG;
+  p->tile = tile;
+  p->lattice = lattice;
+  p->dim = m;
+  p->substream = S;
+  p->rice_k = rice_k;
+  p->cols = cols;
+  p->tpr = cols / tile;
+  p->spr = cols / S;
+  p->snr_db = snr;
+  p->alpha = (float)alpha_for_snr(lattice, snr);
+  p->rotation = o.rotation;
+  p->dither = o.dither ? 1 : 0;
+  p->norm_fp16 = (o.norm_dtype == HQ_FP16) ? 1 : 0;
+  p->rht_seed = rht_seed;
+  p->rot_seed = o.rot_seed;
+  p->dither_seed = o.dither_seed;
+  int64_t n0, n1;
+  class_counts(lattice, S, &n0, &n1);
+  kstar_thresholds(n0, p->thr[0]);
+  if (n1) kstar_thresholds(n1, p->thr[1]); else kstar_thresholds(1, p->thr[1]);
+  p->max_words_sub = substream_word_bound(*p);
+  if (p->max_words_sub > 8192) {
+    delete p;
+    return HQ_ERR_UNSUPPORTED;
+  }
+  hipGetDevice(&p->device);
+
+  // sign bitmasks: bit j set means the sign is -1
+  const int64_t nw = (cols + 31) / 32;
+  std::vector<uint32_t> dm((size_t)nw, 0u), sm(4, 0u);
+  for (int64_t j = 0; j < cols; ++j)
+    if (splitmix_negative(rht_seed, (uint64_t)j)) dm[(size_t)(j >> 5)] |= 1u << (j & 31);
+  for (int j = 0; j < tile; ++j)
+    if (splitmix_negative(o.rot_seed, (uint64_t)j)) sm[(size_t)(j >> 5)] |= 1u << (j & 31);
+  if (hipMalloc((void**)&p->d_dmask, sizeof(uint32_t) * (size_t)nw) != hipSuccess ||
+      hipMalloc((void**)&p->d_smask, sizeof(uint32_t) * 4) != hipSuccess) {
+    if (p->d_dmask) hipFree(p->d_dmask);
+    delete p;
+    return HQ_ERR_HIP;
+  }
+  if (hipMemcpy(p->d_dmask, dm.data(), sizeof(uint32_t) * (size_t)nw, hipMemcpyHostToDevice) !=
+          hipSuccess ||
+      hipMemcpy(p->d_smask, sm.data(), sizeof(uint32_t) * 4, hipMemcpyHostToDevice) !=
+          hipSuccess) {
+    hipFree(p->d_dmask);
+    hipFree(p->d_smask);
+    delete p;
+    return HQ_ERR_HIP;
+  }
+  *out = p;
+  if (info) hq_plan_get_info(p, info);
+  return HQ_OK;
+}
+
+hq_status hq_plan_get_info(hq_plan_t p, hq_plan_info* info) {
+  if (!p || !info) return HQ_ERR_INVALID_ARG;
+  std::memset(info, 0, sizeof(*info));
+  info->alpha = p->alpha;
+  info->snr_db = (float)p->snr_db;
+  info->tile = p->tile;
+  info->lattice = p->lattice;
+  info->substream = p->substream;
+  info->rice_k = p->rice_k;
+  info->cols = p->cols;
+  info->tiles_per_row = p->tpr;
+  info->subs_per_row = p->spr;
+  info->max_words_per_substream = p->max_words_sub;
+  info->max_words_per_row = p->max_words_sub * p->spr;
+  return HQ_OK;
+}
+
+hq_status hq_plan_destroy(hq_plan_t p) {
+  if (!p) return HQ_ERR_INVALID_ARG;
+  hipFree(p->d_dmask);
+  hipFree(p->d_smask);
+  delete p;
+  return HQ_OK;
+}
+
+size_t hq_scan_bytes(hq_plan_t p, int64_t rows) {
+  if (!p || rows < 0) return 0;
+  const int64_t nwg = (rows * p->spr + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG;
+  return (size_t)HQ_SCAN_STATUS_OFFSET + sizeof(unsigned long long) * (size_t)std::max<int64_t>(nwg, 1);
+}
+
+hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_t ld,
+                    hq_stream* s, int32_t append, void* stream) {
+  if (!p || !s || rows < 0) return HQ_ERR_INVALID_ARG;
+  if (xt != HQ_BF16 && xt != HQ_FP32) return HQ_ERR_INVALID_ARG;
+  if (!s->payload || !s->offsets || !s->kparam || !s->norms || !s->scan) return HQ_ERR_INVALID_ARG;
+  if (((uintptr_t)s->scan & 7u) != 0) return HQ_ERR_INVALID_ARG;
+  const int64_t row0 = append ? s->rows : 0;
+  if (row0 < 0 || row0 + rows > s->rows_capacity) return HQ_ERR_CAPACITY;
+  if (rows > 0) {
+    if (!x || ld < p->cols) return HQ_ERR_INVALID_ARG;
+    const int64_t esz = (xt == HQ_BF16) ? 2 : 4;
+    if (!aligned16(x) || (ld * esz) % 16 != 0) return HQ_ERR_INVALID_ARG;
+  }
+  const int64_t nsub = rows * p->spr;
+  const int64_t first_sub = row0 * p->spr;
+  if (first_sub + nsub > (int64_t)0xFFFFFFFF) return HQ_ERR_UNSUPPORTED;
+  if (rows == 0) {
+    if (!append) {
+      s->rows = 0;
+      return hip_status(hq_launch_zero(s->offsets, sizeof(uint32_t), stream));
+    }
+    return HQ_OK;
+  }
+  const int64_t nwg = (nsub + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG;
+  if (nwg > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
+  if ((size_t)s->scan_bytes < hq_scan_bytes(p, rows)) return HQ_ERR_CAPACITY;
+
+  hq_encode_args a;
+  std::memset(&a, 0, sizeof(a));
+  a.x = x;
+  a.ld = ld;
+  a.first_row = row0;
+  a.first_sub = first_sub;
+  a.nsub = nsub;
+  a.spr = p->spr;
+  a.tpr = p->tpr;
+  a.payload = s->payload;
+  a.cap_words = s->capacity_words;
+  a.offsets = s->offsets;
+  a.kparam = s->kparam;
+  a.norms = s->norms;
+  a.dmask = p->d_dmask;
+  a.smask = p->d_smask;
+  a.stats = s->stats;
+  a.ticket = (unsigned long long*)s->scan;
+  a.status = (unsigned long long*)((char*)s->scan + HQ_SCAN_STATUS_OFFSET);
+  a.nwg = (uint32_t)nwg;
+  a.append = append ? 1 : 0;
+  a.rice_k = p->rice_k;
+  a.rotation = p->rotation;
+  a.dither = p->dither;
+  a.norm_fp16 = p->norm_fp16;
+  a.lds_words = (uint32_t)p->max_words_sub;
+  a.dither_seed = p->dither_seed;
+  a.alpha = p->alpha;
+  std::memcpy(a.thr0, p->thr[0], sizeof(a.thr0));
+  std::memcpy(a.thr1, p->thr[1], sizeof(a.thr1));
+  const int e = hq_launch_encode(p, a, xt, stream);
+  if (e) return HQ_ERR_HIP;
+  s->rows = row0 + rows;
+  return HQ_OK;
+}
+
+static void fill_decode_args(const hq_plan_s* p, const hq_stream* s, int64_t row0, int64_t rows,
+                             hq_decode_args* a) {
+  std::memset(a, 0, sizeof(*a));
+  a->payload = s->payload;
+  a->cap_words = s->capacity_words;
+  a->offsets = s->offsets;
+  a->kparam = s->kparam;
+  a->norms = s->norms;
+  a->first_row = row0;
+  a->first_sub = row0 * p->spr;
+  a->nsub = rows * p->spr;
+  a->spr = p->spr;
+  a->tpr = p->tpr;
+  a->dmask = p->d_dmask;
+  a->smask = p->d_smask;
+  a->stats = s->stats;
+  a->rotation = p->rotation;
+  a->dither = p->dither;
+  a->norm_fp16 = p->norm_fp16;
+  a->lds_words = (uint32_t)p->max_words_sub;
+  a->dither_seed = p->dither_seed;
+  a->alpha = p->alpha;
+  a->alpha_n = p->alpha * (float)p->tile;
+}
+
+hq_status hq_decode(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows, void* y,
+                    int32_t yt, int64_t ld, void* stream) {
+  if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
+  if (yt != HQ_BF16 && yt != HQ_FP32) return HQ_ERR_INVALID_ARG;
+  if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
+  if (rows == 0) return HQ_OK;
+  if (!y || ld < p->cols || !s->payload || !s->offsets || !s->kparam || !s->norms)
+    return HQ_ERR_INVALID_ARG;
+  const int64_t esz = (yt == HQ_BF16) ? 2 : 4;
+  if (!aligned16(y) || (ld * esz) % 16 != 0) return HQ_ERR_INVALID_ARG;
+  hq_decode_args a;
+  fill_decode_args(p, s, row0, rows, &a);
+  a.y = y;
+  a.ld = ld;
+  return hip_status(hq_launch_decode(p, a, yt, stream));
+}
+
+hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
+                         int8_t* codes, int64_t ldc, float* g, void* stream) {
+  if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
+  if (p->lattice == HQ_A2 || p->dither) return HQ_ERR_UNSUPPORTED;
+  if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
+  if (rows == 0) return HQ_OK;
+  if (!codes || !g || ldc < p->cols || ldc % 8 != 0 || ((uintptr_t)codes & 7u) != 0)
+    return HQ_ERR_INVALID_ARG;
+  hq_decode_args a;
+  fill_decode_args(p, s, row0, rows, &a);
+  a.y = codes;
+  a.ld = ldc;
+  a.g = g;
+  return hip_status(hq_launch_decode_int8(p, a, stream));
+}
+
+hq_status hq_act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t* xq, float* sx,
+                      void* stream) {
+  if (!p || M < 0) return HQ_ERR_INVALID_ARG;
+  if (M == 0) return HQ_OK;
+  if (!a || !xq || !sx || lda < p->cols || !aligned16(a) || (lda * 2) % 16 != 0 ||
+      ((uintptr_t)xq & 3u) != 0)
+    return HQ_ERR_INVALID_ARG;
+  if (p->cols > 16384 || M > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
+  hq_actprep_args args;
+  args.a = a;
+  args.lda = lda;
+  args.M = M;
+  args.K = p->cols;
+  args.xq = xq;
+  args.sx = sx;
+  args.dmask = p->d_dmask;
+  return hip_status(hq_launch_act_prep(args, stream));
+}
+
+hq_status hq_gemm_int8_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx, int64_t M,
+                                   const int8_t* codes, const float* g, int64_t N, void* out,
+                                   int32_t ot, void* stream) {
+  if (!p || M < 0 || N < 0) return HQ_ERR_INVALID_ARG;
+  if (ot != HQ_BF16 && ot != HQ_FP32) return HQ_ERR_INVALID_ARG;
+  if (M == 0 || N == 0) return HQ_OK;
+  if (!xq || !sx || !codes || !g || !out) return HQ_ERR_INVALID_ARG;
+  if (!aligned16(xq) || !aligned16(codes) || !aligned16(out)) return HQ_ERR_INVALID_ARG;
+  hq_gemm_args a;
+  a.xq = xq;
+  a.sx = sx;
+  a.w = codes;
+  a.g = g;
+  a.out = out;
+  a.M = M;
+  a.N = N;
+  a.K = p->cols;
+  a.out_bf16 = (ot == HQ_BF16) ? 1 : 0;
+  const int e = hq_launch_gemm(a, stream);
+  if (e == -1) return HQ_ERR_UNSUPPORTED;
+  return hip_status(e);
+}
+
+size_t hq_gemm_workspace_bytes(hq_plan_t p, int64_t M, int64_t N) {
+  if (!p || M < 0 || N < 0) return 0;
+  const size_t K = (size_t)p->cols;
+  const auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+  return up((size_t)M * K) + up((size_t)M * 4) + up((size_t)N * K) + up((size_t)N * (K / 128) * 4);
+}
+
+hq_status hq_dequant_gemm_int8(hq_plan_t p, const hq_stream* w, int64_t N, const void* a,
+                               int64_t M, void* out, int32_t ot, void* workspace,
+                               size_t ws_bytes, void* stream) {
+  if (!p || !w || !a || !out || M < 0 || N < 0) return HQ_ERR_INVALID_ARG;
+  if (ws_bytes < hq_gemm_workspace_bytes(p, M, N) || !workspace) return HQ_ERR_CAPACITY;
+  const size_t K = (size_t)p->cols;
+  const auto up = [](size_t v) { return (v + 255) & ~(size_t)255; };
+  char* ws = (char*)workspace;
+  int8_t* xq = (int8_t*)ws;
+  float* sx = (float*)(ws + up((size_t)M * K));
+  int8_t* codes = (int8_t*)(ws + up((size_t)M * K) + up((size_t)M * 4));
+  float* g = (float*)(ws + up((size_t)M * K) + up((size_t)M * 4) + up((size_t)N * K));
+  hq_status st = hq_act_prep(p, a, M, (int64_t)K, xq, sx, stream);
+  if (st != HQ_OK) return st;
+  st = hq_decode_int8(p, w, 0, N, codes, (int64_t)K, g, stream);
+  if (st != HQ_OK) return st;
+  return hq_gemm_int8_blockscaled(p, xq, sx, M, codes, g, N, out, ot, stream);
+}
+
+}  // extern "C"

@@ -1,0 +1,111 @@
+// Internal declarations shared by the host plan (hq_host.cpp) and the gfx950
+// kernels (hq_kernels.hip) of libhq.so.  Not part of the public ABI.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/hq.h"
+
+#define HQ_KMAX 15
+#define HQ_TILE 128              // tile length the kernels are built for
+#define HQ_SUB 512               // symbols per sub-stream the kernels are built for
+#define HQ_WAVES_PER_WG 4        // one sub-stream per wave, four per workgroup
+#define HQ_SCAN_STATUS_OFFSET 128  // bytes before the look-back status array
+
+// Plan: immutable after hq_plan returns.
+struct hq_plan_s {
+  int32_t tile, lattice, dim, substream, rice_k;
+  int64_t cols, tpr, spr;
+  float alpha;
+  double snr_db;
+  int32_t rotation, dither, norm_fp16;
+  uint64_t rht_seed, rot_seed, dither_seed;
+  // Automatic Rice k of a class with `count` symbols summing to `sum`:
+  // k0 = #{t in 1..KMAX : sum >= thr[c][t]} (thr[c][0] unused).
+  uint32_t thr[2][HQ_KMAX + 1];
+  int64_t max_words_sub;   // capacity bound of one sub-stream, in 32-bit words
+  uint32_t* d_dmask;       // device: RHT sign bit per global column (1 = -1)
+  uint32_t* d_smask;       // device: rotation sign bit per tile coordinate
+  int device;
+};
+
+// Arguments of the encode kernel (passed by value).
+struct hq_encode_args {
+  const void* x;
+  int64_t ld;
+  int64_t first_row;      // global row of x's first row
+  int64_t first_sub;      // global sub-stream index of x's first sub-stream
+  int64_t nsub;           // sub-streams in this call
+  int64_t spr;            // sub-streams per row
+  int64_t tpr;            // tiles per row
+  uint32_t* payload;
+  int64_t cap_words;
+  uint32_t* offsets;
+  uint8_t* kparam;
+  void* norms;
+  const uint32_t* dmask;
+  const uint32_t* smask;
+  hq_stats* stats;
+  unsigned long long* ticket;  // scan scratch: (epoch << 32 | next ticket)
+  unsigned long long* status;  // scan scratch: one word per workgroup
+  uint32_t nwg;
+  int32_t append;
+  int32_t rice_k;
+  int32_t rotation, dither, norm_fp16;
+  uint32_t lds_words;     // per-wave assembly buffer, in words
+  uint64_t dither_seed;
+  float alpha;
+  uint32_t thr0[HQ_KMAX + 1];
+  uint32_t thr1[HQ_KMAX + 1];
+};
+
+struct hq_decode_args {
+  const uint32_t* payload;
+  int64_t cap_words;
+  const uint32_t* offsets;
+  const uint8_t* kparam;
+  const void* norms;
+  int64_t first_row;
+  int64_t first_sub;
+  int64_t nsub;
+  int64_t spr, tpr;
+  void* y;                 // decode: output rows; decode_int8: int8 codes
+  int64_t ld;
+  float* g;                // decode_int8: per-tile factors (rows x tpr)
+  const uint32_t* dmask;
+  const uint32_t* smask;
+  hq_stats* stats;
+  int32_t rotation, dither, norm_fp16;
+  uint32_t lds_words;
+  uint64_t dither_seed;
+  float alpha;
+  float alpha_n;           // alpha * tile, exact
+};
+
+struct hq_actprep_args {
+  const void* a;
+  int64_t lda;
+  int64_t M, K;
+  int8_t* xq;
+  float* sx;
+  const uint32_t* dmask;
+};
+
+struct hq_gemm_args {
+  const int8_t* xq;   // M x K
+  const float* sx;    // M
+  const int8_t* w;    // N x K
+  const float* g;     // N x (K / 128)
+  void* out;          // M x N
+  int64_t M, N, K;
+  int32_t out_bf16;
+};
+
+// Kernel launchers (hq_kernels.hip); return a hipError_t as int.
+int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, int xt, void* stream);
+int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream);
+int hq_launch_decode_int8(const hq_plan_s* p, const hq_decode_args& a, void* stream);
+int hq_launch_act_prep(const hq_actprep_args& a, void* stream);
+int hq_launch_gemm(const hq_gemm_args& a, void* stream);
+int hq_launch_zero(void* ptr, size_t bytes, void* stream);

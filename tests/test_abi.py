@@ -1,0 +1,80 @@
+"""CPU-side checks of the C ABI (no GPU compute): libhq.so loads, exports
+every function include/hq.h declares, validates arguments before touching the
+device, and its host Rice-k rule equals the oracle's formula."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hq.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hq_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def hq():
+    from paper_2606_23406_amd import build, hq as H
+    if not os.path.exists(build.LIB):
+        build.build()
+    return H
+
+
+def test_library_exports_every_declared_symbol(hq):
+    L = hq.lib()
+    names = declared_functions()
+    assert "hq_plan" in names and "hq_encode" in names and "hq_dequant_gemm_int8" in names
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(hq.EXPORTED) <= set(names)
+
+
+def test_status_strings(hq):
+    L = hq.lib()
+    assert L.hq_status_string(0) == b"ok"
+    assert L.hq_status_string(-7).startswith(b"no calibration")
+
+
+def test_plan_argument_errors_are_synchronous(hq):
+    L = hq.lib()
+    h = C.c_void_p()
+    info = hq.PlanInfo()
+    o = hq.Options(0, 0, 0, 0, 0, 0, 1, 0, 20.0)
+    # tile not a power of two / smaller than the lattice / cols not divisible
+    assert L.hq_plan(96, 0, 4.0, 0, -1, 4096, C.byref(o), C.byref(h), C.byref(info)) == -1
+    assert L.hq_plan(4, 0, 4.0, 0, -1, 4096, C.byref(o), C.byref(h), C.byref(info)) == -1
+    assert L.hq_plan(128, 0, 4.0, 0, -1, 4000, C.byref(o), C.byref(h), C.byref(info)) == -1
+    assert L.hq_plan(128, 7, 4.0, 0, -1, 4096, C.byref(o), C.byref(h), C.byref(info)) == -1
+    assert L.hq_plan(128, 0, 4.0, 0, 16, 4096, C.byref(o), C.byref(h), C.byref(info)) == -1
+    # valid for the method, not built here: other tile sizes / sub-stream lengths
+    assert L.hq_plan(256, 0, 4.0, 0, -1, 4096, C.byref(o), C.byref(h), C.byref(info)) == -2
+    o2 = hq.Options(0, 0, 0, 0, 0, 1024, 1, 0, 20.0)
+    assert L.hq_plan(128, 0, 4.0, 0, -1, 4096, C.byref(o2), C.byref(h), C.byref(info)) == -2
+    # null output handle
+    assert L.hq_plan(128, 0, 4.0, 0, -1, 4096, C.byref(o), None, None) == -1
+
+
+def test_encode_decode_argument_errors(hq):
+    L = hq.lib()
+    s = hq.StreamStruct()
+    assert L.hq_encode(None, None, 0, 0, 0, C.byref(s), 0, None) == -1
+    assert L.hq_decode(None, C.byref(s), 0, 0, None, 0, 0, None) == -1
+    assert L.hq_dequant_gemm_int8(None, None, 0, None, 0, None, 0, None, 0, None) == -1
+
+
+@pytest.mark.parametrize("count", [512, 384, 256, 128, 1])
+def test_host_rice_kstar_equals_oracle(hq, count):
+    # the kernels evaluate k* through integer thresholds precomputed on the
+    # host; they must agree with the paper's formula at every sum.
+    L = hq.lib()
+    sums = list(range(0, 70000)) + list(np.unique(np.geomspace(70000, 2**31, 3000).astype(np.int64)))
+    for s in sums:
+        assert L.hq_rice_kstar(count, int(s)) == O.rice_k_auto(count, int(s)), (count, s)

@@ -1,0 +1,221 @@
+"""GPU parity of the HIP codec (through the C ABI) against the oracle.
+
+Bar: lattice indices and Rice bitstreams bit-exact per sub-stream, except
+blocks whose oracle Voronoi margin is below 1e-6 (counted, and their
+sub-stream must be exactly the oracle's Rice code of the GPU's symbols);
+reconstruction within 1e-5 of the tile's lattice unit in fp32 (bit-exact in
+practice); GEMM within 1e-3 relative to max(|ref|, rms(ref)).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from tests import parity as PT
+
+pytestmark = pytest.mark.gpu
+
+LAT_NAMES = {O.E8: "E8", O.D4: "D4", O.A2: "A2", O.Z: "Z"}
+
+
+@pytest.fixture(scope="module")
+def hq():
+    from paper_2606_23406_amd import hq as H
+    H.lib()
+    assert torch.cuda.is_available()
+    return H
+
+
+def encode_gpu(hq, P, snr, x, rows_capacity=None, append_chunks=None):
+    rows, cols = x.shape
+    plan = PT.gpu_plan(hq, P, snr, cols)
+    s = hq.EncodedStream(plan, rows_capacity or rows)
+    xd = x.cuda()
+    if append_chunks:
+        for r0 in range(0, rows, append_chunks):
+            hq.hq_encode(plan, xd[r0:r0 + append_chunks], s, append=r0 > 0)
+    else:
+        hq.hq_encode(plan, xd, s)
+    torch.cuda.synchronize()
+    return plan, s
+
+
+def check_roundtrip(hq, P, snr, x, label, append_chunks=None):
+    print(f"[parity] {label} shape={tuple(x.shape)} dtype={x.dtype}", flush=True)
+    plan, s = encode_gpu(hq, P, snr, x, append_chunks=append_chunks)
+    rows = x.shape[0]
+    st = s.read_stats()
+    assert st["status"] == 0, st
+    gpu = PT.gpu_stream_arrays(s, rows)
+    x_np = x.float().numpy()
+    res = PT.compare_streams(P, x_np, gpu)
+    assert res["exempt_blocks"] <= max(2, res["substreams"] // 1000), res["exempt_blocks"]
+    assert st["payload_bits"] == res["payload_bits"] or res["exempt_substreams"] > 0
+    # decode: fp32 against the oracle's fp32 reconstruction, bf16 = bf16(that)
+    y32 = hq.hq_decode(plan, s, out_dtype=torch.float32)
+    y16 = hq.hq_decode(plan, s, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    st2 = s.read_stats()
+    assert st2["corrupt_substreams"] == 0
+    ref = O.backend(P, res["codes"], res["norms"], row0=0)
+    g = y32.cpu().numpy()
+    skip = PT.tiles_with_code_diffs(res["codes"], res["gpu_codes"]).reshape(rows, -1)
+    unit = PT.lattice_unit(P, res["norms"]).reshape(rows, -1)
+    err = np.abs(g.astype(np.float64) - ref).reshape(rows, -1, 128).max(axis=2)
+    assert np.all(err[~skip] <= 1e-5 * unit[~skip]), err.max()
+    exact = np.mean(g.reshape(rows, -1, 128)[~skip] == ref.reshape(rows, -1, 128)[~skip])
+    ref16 = torch.from_numpy(ref).to(torch.bfloat16)
+    b16 = (y16.cpu().view(torch.int16) == ref16.view(torch.int16)).numpy().reshape(rows, -1, 128)
+    assert b16[~skip].all()
+    print(f"[parity] {label}: {res['substreams']} sub-streams, exempt blocks "
+          f"{res['exempt_blocks']}, fp32 bit-exact fraction {exact:.6f}", flush=True)
+    return plan, s, res
+
+
+def gauss(rows, cols, seed, scale=1.0, dtype=torch.float32):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn((rows, cols), generator=g) * scale).to(dtype)
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2, O.Z])
+def test_weights_roundtrip_bf16(hq, lat):
+    # 63 rows x 1024: 126 sub-streams, so the last workgroup is ragged
+    snr = {O.E8: PT.op_snr("E8", 4.0), O.D4: PT.op_snr("D4", 3.0), O.A2: PT.op_snr("A2", 4.0),
+           O.Z: PT.op_snr("Z", 4.0)}[lat]
+    P = PT.oracle_params(lat, snr, rht_seed=11)
+    x = gauss(63, 1024, 100 + lat, 0.02, torch.bfloat16)
+    check_roundtrip(hq, P, snr, x, f"weights {LAT_NAMES[lat]}")
+
+
+def test_single_matrix_fp32_e8(hq):
+    from paper_2606_23406_amd import workloads
+    x = torch.from_numpy(workloads.single_matrix_fp32())
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=0)
+    check_roundtrip(hq, P, snr, x, "512x512 fp32 E8@4")
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2, O.Z])
+@pytest.mark.parametrize("rice_k", [0, 2, 5])
+def test_fixed_rice_k(hq, lat, rice_k):
+    snr = 15.0
+    P = PT.oracle_params(lat, snr, rht_seed=5, rice_k=rice_k)
+    x = gauss(16, 2048, 7 + lat, 1.0)
+    check_roundtrip(hq, P, snr, x, f"fixed k={rice_k} {LAT_NAMES[lat]}")
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2, O.Z])
+def test_kv_rotation_dither_fp16_append(hq, lat):
+    # KV path: signs rotation + subtractive dither + fp16 norms, appended in
+    # chunks of 16 rows; the oracle encodes all rows at once.
+    snr = {O.E8: PT.op_snr("E8", 2.0), O.D4: 12.0, O.A2: PT.op_snr("A2", 1.7),
+           O.Z: PT.op_snr("Z", 1.7)}[lat]
+    P = PT.oracle_params(lat, snr, rht_seed=3, rotation=1, rot_seed=99, dither=True,
+                         dither_seed=1234 + lat, norm_fp16=True)
+    x = gauss(48, 1024, 50 + lat, 1.0, torch.bfloat16)
+    x[:, 5::128] *= 10  # outlier channels
+    check_roundtrip(hq, P, snr, x, f"kv {LAT_NAMES[lat]}", append_chunks=16)
+
+
+def test_zero_tiles_and_tiny_norms(hq):
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=2)
+    x = gauss(8, 1024, 3, 0.02)
+    x[1] = 0.0
+    x[2, 128:256] = 0.0
+    x[3, :128] = 1e-30
+    plan, s, res = check_roundtrip(hq, P, snr, x, "zero tiles")
+    y = hq.hq_decode(plan, s, out_dtype=torch.float32).cpu()
+    assert torch.all(y[1] == 0) and torch.all(y[2, 128:256] == 0)
+
+
+def test_fp16_norm_overflow_is_reported(hq):
+    P = PT.oracle_params(O.E8, 20.0, norm_fp16=True)
+    x = gauss(4, 512, 1, 1e5)
+    plan = PT.gpu_plan(hq, P, 20.0, 512)
+    s = hq.EncodedStream(plan, 4)
+    hq.hq_encode(plan, x.cuda(), s)
+    torch.cuda.synchronize()
+    st = s.read_stats()
+    assert st["status"] == (-4 & 0xFFFFFFFF) and st["overflow_tiles"] == 16
+
+
+def test_empty_and_capacity_errors(hq):
+    P = PT.oracle_params(O.E8, 20.0)
+    plan = PT.gpu_plan(hq, P, 20.0, 1024)
+    s = hq.EncodedStream(plan, 4)
+    hq.hq_encode(plan, torch.zeros((0, 1024), device="cuda"), s)
+    assert s.rows == 0
+    with pytest.raises(hq.HQError):
+        hq.hq_encode(plan, torch.zeros((5, 1024), device="cuda"), s)
+
+
+def test_deterministic_bitstream(hq):
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=8)
+    x = gauss(256, 4096, 9, 0.02, torch.bfloat16).cuda()
+    plan = PT.gpu_plan(hq, P, snr, 4096)
+    a = hq.EncodedStream(plan, 256)
+    b = hq.EncodedStream(plan, 256)
+    hq.hq_encode(plan, x, a)
+    hq.hq_encode(plan, x, b)
+    hq.hq_encode(plan, x, b)  # re-encode over the same buffers (new scan epoch)
+    torch.cuda.synchronize()
+    n = a.end_words()
+    assert n == b.end_words()
+    assert torch.equal(a.payload[:n], b.payload[:n]) and torch.equal(a.offsets, b.offsets)
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.Z])
+def test_decode_int8_codes_and_factors(hq, lat):
+    snr = PT.op_snr("E8", 4.0) if lat == O.E8 else 16.0
+    P = PT.oracle_params(lat, snr, rht_seed=21)
+    x = gauss(40, 1024, 31, 0.02, torch.bfloat16)
+    print(f"[parity] decode_int8 {LAT_NAMES[lat]}", flush=True)
+    plan, s = encode_gpu(hq, P, snr, x)
+    codes, g = hq.hq_decode_int8(plan, s)
+    torch.cuda.synchronize()
+    oc, norms, _, _ = O.frontend(P, x.float().numpy())
+    og = O.weight_factors(P, norms, 40, 1024)
+    assert np.array_equal(codes.cpu().numpy().astype(np.int32), np.clip(oc, -127, 127))
+    assert np.array_equal(g.cpu().numpy(), og)
+
+
+def test_act_prep(hq):
+    from paper_2606_23406_amd import workloads
+    a = workloads.activations(tokens=64, features=1024)
+    P = PT.oracle_params(O.E8, 20.0, rht_seed=41)
+    plan = PT.gpu_plan(hq, P, 20.0, 1024)
+    print("[parity] act_prep 64x1024", flush=True)
+    xq, sx = hq.hq_act_prep(plan, a.cuda())
+    torch.cuda.synchronize()
+    oxq, osx = O.act_prep(a.float().numpy(), 128, 41)
+    assert np.array_equal(sx.cpu().numpy(), osx)
+    assert np.array_equal(xq.cpu().numpy(), oxq)
+
+
+@pytest.mark.parametrize("M,N", [(128, 256), (200, 384), (64, 96)])
+def test_gemm_int8_blockscaled(hq, M, N):
+    from paper_2606_23406_amd import workloads
+    K = 1024
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=51)
+    w = gauss(N, K, 61, 0.02, torch.bfloat16)
+    a = workloads.activations(tokens=M, features=K)
+    print(f"[parity] gemm M={M} N={N} K={K}", flush=True)
+    plan, s = encode_gpu(hq, P, snr, w)
+    out32 = hq.hq_dequant_gemm_int8(plan, s, a.cuda(), out_dtype=torch.float32)
+    out16 = hq.hq_dequant_gemm_int8(plan, s, a.cuda(), out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    codes, norms, _, _ = O.frontend(P, w.float().numpy())
+    g = O.weight_factors(P, norms, N, K)
+    xq, sx = O.act_prep(a.float().numpy(), 128, 51)
+    ref = O.gemm_blockscaled(codes, g, xq, sx, 128)
+    got = out32.cpu().numpy().astype(np.float64)
+    denom = np.maximum(np.abs(ref), np.sqrt((ref ** 2).mean()))
+    assert np.max(np.abs(got - ref) / denom) <= 1e-3
+    ref16 = torch.from_numpy(ref.astype(np.float32)).to(torch.bfloat16).float().numpy()
+    got16 = out16.cpu().float().numpy()
+    # one bf16 ulp of the reference, or fp32 accumulation noise near zero
+    tol = np.maximum(np.abs(ref16) * 2.0 ** -7, 1e-5 * np.sqrt((ref ** 2).mean()))
+    assert np.all(np.abs(got16 - ref16) <= tol)
