@@ -647,7 +647,7 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   const uint32_t U = readfirst(__shfl(uincl, 63, 64));
   const uint32_t uoff = uincl - ulen;
   uint32_t W = (R + U + 31) >> 5;
-  bool overflow = W > A.lds_words;
+  const bool overflow = active && W > A.lds_words;
   if (!active) W = 0;
 
   // A sub-stream that does not fit the plan's bound (only non-finite or
@@ -657,44 +657,12 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   if (lane == 0) s_words[wave] = W;
   __syncthreads();
 
-  // ---- workgroup aggregate and look-back for the absolute word offset
-  if (tid == 0) {
-    uint32_t agg = 0;
-    for (int w = 0; w < HQ_WAVES_PER_WG; ++w) agg += s_words[w];
-    uint32_t prefix = 0;
-    bool timed_out = false;
-    if (wg > 0) {
-      store_status(&A.status[wg], pack_status(epoch, 1u, agg));
-      int64_t j = (int64_t)wg - 1;
-      for (;;) {
-        unsigned long long st = load_status(&A.status[j]);
-        uint32_t spins = 0;
-        while ((uint32_t)(st >> 34) != epoch || ((st >> 32) & 3u) == 0u) {
-          if (++spins > kSpinLimit) {
-            timed_out = true;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(2);
-          st = load_status(&A.status[j]);
-        }
-        if (timed_out) break;
-        prefix += (uint32_t)st;
-        if (((st >> 32) & 3u) == 2u || j == 0) break;
-        --j;
-      }
-    }
-    store_status(&A.status[wg], pack_status(epoch, 2u, prefix + agg));
-    if (timed_out && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
-    const unsigned long long base = A.append ? (unsigned long long)A.offsets[A.first_sub] : 0ull;
-    s_base = base + prefix;
-  }
-  __syncthreads();
+  // ---- publish this workgroup's aggregate at once, so successors can pass it
+  uint32_t agg = 0;
+  for (int w = 0; w < HQ_WAVES_PER_WG; ++w) agg += s_words[w];
+  if (tid == 0 && wg > 0) store_status(&A.status[wg], pack_status(epoch, 1u, agg));
 
-  uint32_t before = 0;
-  for (int w = 0; w < wave; ++w) before += s_words[w];
-  const unsigned long long start = s_base + before;
-
-  // ---- assemble the sub-stream in LDS
+  // ---- assemble the sub-stream in LDS (needs no global offset)
   uint32_t* buf = smem + wave * A.lds_words;
   for (uint32_t w = lane; w < W; w += 64) buf[w] = 0u;
   __syncthreads();
@@ -716,7 +684,52 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   } else if (active && overflow) {
     for (uint32_t w = lane; w < W; w += 64) buf[w] = 0xFFFFFFFFu;
   }
+
+  // ---- look-back by wave 0: 64 predecessors per round trip
+  if (wave == 0) {
+    uint32_t prefix = 0;
+    bool timed_out = false;
+    int64_t hi = (int64_t)wg - 1;
+    while (hi >= 0) {
+      const int64_t idx = hi - lane;
+      unsigned long long st = 0;
+      bool ready = idx < 0;
+      uint32_t spins = 0;
+      // wait until every predecessor in this window has published something
+      for (;;) {
+        if (!ready) {
+          st = load_status(&A.status[idx]);
+          ready = (uint32_t)(st >> 34) == epoch && ((st >> 32) & 3u) != 0u;
+        }
+        if (__all(ready)) break;
+        if (++spins > kSpinLimit) {
+          timed_out = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      if (timed_out) break;
+      const bool incl = idx >= 0 && ((st >> 32) & 3u) == 2u;
+      const unsigned long long pmask = __ballot(incl);
+      const int stop = pmask ? __builtin_ctzll(pmask) : 64;  // nearest inclusive prefix
+      uint32_t v = (idx >= 0 && lane <= stop) ? (uint32_t)st : 0u;
+      v = wave_sum_u32(v);
+      prefix += v;
+      if (pmask) break;
+      hi -= 64;
+    }
+    if (lane == 0) {
+      store_status(&A.status[wg], pack_status(epoch, 2u, prefix + agg));
+      if (timed_out && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
+      const unsigned long long base = A.append ? (unsigned long long)A.offsets[A.first_sub] : 0ull;
+      s_base = base + prefix;
+    }
+  }
   __syncthreads();
+
+  uint32_t before = 0;
+  for (int w = 0; w < wave; ++w) before += s_words[w];
+  const unsigned long long start = s_base + before;
 
   // ---- write payload, offsets, k
   if (active) {
@@ -897,13 +910,14 @@ __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
     float y[8];
     const bool exact = !A.dither && LAT != kA2;
     const uint32_t sbits = A.rotation ? sign_bits8(A.smask, q * 8) : 0u;
+    const uint32_t dbits = sign_bits8(A.dmask, col);
     if (exact) {
       int32_t v[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = ((sbits >> j) & 1u) ? -c[j] : c[j];
       fwht128_i(v, lane);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = (float)v[j];
+      for (int j = 0; j < 8; ++j) y[j] = (float)(((dbits >> j) & 1u) ? -v[j] : v[j]) * g;
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) y[j] = code_coord<LAT>(c[j], j);
@@ -916,10 +930,9 @@ __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) y[j] = flip(y[j], sbits, j);
       fwht128(y, lane);
-    }
-    const uint32_t dbits = sign_bits8(A.dmask, col);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) y[j] = flip(y[j], dbits, j) * g;
+      for (int j = 0; j < 8; ++j) y[j] = flip(y[j], dbits, j) * g;
+    }
     if (!active) return;
     if constexpr (MODE == 0) {
       float4* out = (float4*)((float*)A.y + lrow * A.ld + col);

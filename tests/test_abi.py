@@ -78,3 +78,19 @@ def test_host_rice_kstar_equals_oracle(hq, count):
     sums = list(range(0, 70000)) + list(np.unique(np.geomspace(70000, 2**31, 3000).astype(np.int64)))
     for s in sums:
         assert L.hq_rice_kstar(count, int(s)) == O.rice_k_auto(count, int(s)), (count, s)
+
+
+def test_library_calibration_matches_oracle_operating_points(hq):
+    # App. B: both sides invert a realized-rate curve measured on iid Gaussian
+    # tiles; the library's table (its own encoder, torch samples) and the
+    # oracle's bisection (its own encoder, numpy samples) must agree.
+    import json
+    pts = json.load(open(os.path.join(ROOT, "tests", "golden", "operating_points.json")))["points"]
+    for p in pts:
+        lat = hq.LATTICES[p["lattice"]]
+        snr = hq.hq_calibrated_snr(lat, -1, p["bps"])
+        assert abs(snr - p["snr_db"]) < 0.05, (p, snr)
+    # fixed-k curves exist too, and bps below their 1 + k floor is rejected
+    assert hq.hq_calibrated_snr(hq.HQ_E8, 2, 4.0) > 0
+    with pytest.raises(hq.HQError):
+        hq.hq_calibrated_snr(hq.HQ_E8, 3, 2.0)
