@@ -337,8 +337,10 @@ hq_status hq_plan_destroy(hq_plan_t p) {
 
 size_t hq_scan_bytes(hq_plan_t p, int64_t rows) {
   if (!p || rows < 0) return 0;
-  const int64_t nwg = (rows * p->spr + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG;
-  return (size_t)HQ_SCAN_STATUS_OFFSET + sizeof(unsigned long long) * (size_t)std::max<int64_t>(nwg, 1);
+  const int64_t nwg = (rows * p->spr + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
+  // the epoch word, then a look-back status word and a stats word per workgroup
+  return (size_t)HQ_SCAN_STATUS_OFFSET +
+         2 * sizeof(unsigned long long) * (size_t)std::max<int64_t>(nwg, 1);
 }
 
 hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_t ld,
@@ -364,7 +366,7 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
     }
     return HQ_OK;
   }
-  const int64_t nwg = (nsub + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG;
+  const int64_t nwg = (nsub + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
   if (nwg > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
   if ((size_t)s->scan_bytes < hq_scan_bytes(p, rows)) return HQ_ERR_CAPACITY;
 
@@ -385,8 +387,9 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
   a.dmask = p->d_dmask;
   a.smask = p->d_smask;
   a.stats = s->stats;
-  a.ticket = (unsigned long long*)s->scan;
+  a.epoch = (unsigned long long*)s->scan;
   a.status = (unsigned long long*)((char*)s->scan + HQ_SCAN_STATUS_OFFSET);
+  a.wgstat = a.status + nwg;
   a.nwg = (uint32_t)nwg;
   a.append = append ? 1 : 0;
   a.rice_k = p->rice_k;

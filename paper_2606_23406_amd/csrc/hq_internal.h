@@ -10,7 +10,9 @@
 #define HQ_KMAX 15
 #define HQ_TILE 128              // tile length the kernels are built for
 #define HQ_SUB 512               // symbols per sub-stream the kernels are built for
-#define HQ_WAVES_PER_WG 4        // one sub-stream per wave, four per workgroup
+#define HQ_WAVES_PER_WG 4        // wave64s per workgroup
+#define HQ_ENC_SUBS_PER_WAVE 4   // encode: sub-streams per wave, one after another
+#define HQ_ENC_SUBS_PER_WG (HQ_WAVES_PER_WG * HQ_ENC_SUBS_PER_WAVE)
 #define HQ_SCAN_STATUS_OFFSET 128  // bytes before the look-back status array
 
 // Plan: immutable after hq_plan returns.
@@ -47,8 +49,9 @@ struct hq_encode_args {
   const uint32_t* dmask;
   const uint32_t* smask;
   hq_stats* stats;
-  unsigned long long* ticket;  // scan scratch: (epoch << 32 | next ticket)
-  unsigned long long* status;  // scan scratch: one word per workgroup
+  unsigned long long* epoch;   // scan scratch: the launch epoch
+  unsigned long long* status;  // scan scratch: one look-back word per workgroup
+  unsigned long long* wgstat;  // scan scratch: one stats word per workgroup
   uint32_t nwg;
   int32_t append;
   int32_t rice_k;

@@ -30,20 +30,55 @@ __device__ __forceinline__ uint32_t readfirst(uint32_t v) {
   return __builtin_amdgcn_readfirstlane(v);
 }
 
-__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
-#pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v += __shfl_xor(v, m, 64);
-  return v;
+// DPP lane moves (data-parallel primitives of the gfx9 VALU): dst lane l reads
+// src lane f(l) inside its 16-lane row; lanes whose row/bank is masked off
+// keep `old`, lanes with no source read 0 when BC is set.
+template <int CTRL, int RM = 0xF, int BM = 0xF, bool BC = false>
+__device__ __forceinline__ uint32_t dpp(uint32_t old, uint32_t src) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)src, CTRL, RM, BM, BC);
 }
 
-// Inclusive prefix sum over the 64 lanes.
-__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v, int lane) {
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    uint32_t o = __shfl_up(v, d, 64);
-    if (lane >= d) v += o;
+constexpr int kDppQuadXor1 = 0xB1;  // quad_perm [1,0,3,2]
+constexpr int kDppQuadXor2 = 0x4E;  // quad_perm [2,3,0,1]
+constexpr int kDppRowShl4 = 0x104;  // lane l reads l + 4
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppRowRor8 = 0x128;  // lane l reads (l + 8) mod 16 = l ^ 8
+constexpr int kDppRowBcast15 = 0x142, kDppRowBcast31 = 0x143;
+
+// Value of lane l ^ M (M in 1, 2, 4, 8: inside the 16-lane row).
+template <int M>
+__device__ __forceinline__ uint32_t xor_lane(uint32_t v) {
+  if constexpr (M == 1) {
+    return dpp<kDppQuadXor1>(v, v);
+  } else if constexpr (M == 2) {
+    return dpp<kDppQuadXor2>(v, v);
+  } else if constexpr (M == 4) {
+    const uint32_t t = dpp<kDppRowShl4, 0xF, 0x5>(v, v);  // banks 0, 2 read l + 4
+    return dpp<kDppRowShr4, 0xF, 0xA>(t, v);              // banks 1, 3 read l - 4
+  } else {
+    return dpp<kDppRowRor8>(v, v);
   }
-  return v;
+}
+
+template <int M>
+__device__ __forceinline__ float xor_lane_f(float v) {
+  return __uint_as_float(xor_lane<M>(__float_as_uint(v)));
+}
+
+// Inclusive prefix sum over the 64 lanes (row shifts, then row broadcasts).
+__device__ __forceinline__ uint32_t wave_scan_incl(uint32_t x) {
+  x += dpp<kDppRowShr1, 0xF, 0xF, true>(0u, x);
+  x += dpp<kDppRowShr2, 0xF, 0xF, true>(0u, x);
+  x += dpp<kDppRowShr4, 0xF, 0xF, true>(0u, x);
+  x += dpp<kDppRowShr8, 0xF, 0xF, true>(0u, x);
+  x += dpp<kDppRowBcast15, 0xA, 0xF>(0u, x);
+  x += dpp<kDppRowBcast31, 0xC, 0xF>(0u, x);
+  return x;
+}
+
+// Sum over the 64 lanes, as a wave-uniform value.
+__device__ __forceinline__ uint32_t wave_total(uint32_t x) {
+  return __builtin_amdgcn_readlane(wave_scan_incl(x), 63);
 }
 
 __device__ __forceinline__ uint32_t zigzag(int32_t v) {
@@ -375,41 +410,54 @@ __device__ __forceinline__ void fwht8_inlane_i(int32_t* v) {
 }
 
 // Butterfly with lane l ^ M: the lower lane keeps a + b, the upper a - b,
-// with a the lower lane's value.
+// with a the lower lane's value.  s = +1 (lower) or -1 (upper) makes it one
+// exact-multiplier fma: fma(v, s, p) = round(p + s v).
 template <int M>
-__device__ __forceinline__ void fwht_xlane(float* v, int lane) {
-  const bool upper = (lane & M) != 0;
+__device__ __forceinline__ void fwht_xlane(float* v, float s) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const float p = __shfl_xor(v[j], M, 64);
-    v[j] = upper ? (p - v[j]) : (v[j] + p);
+    const float p = xor_lane_f<M>(v[j]);
+    v[j] = __builtin_fmaf(v[j], s, p);
   }
 }
 
 template <int M>
-__device__ __forceinline__ void fwht_xlane_i(int32_t* v, int lane) {
-  const bool upper = (lane & M) != 0;
+__device__ __forceinline__ void fwht_xlane_i(int32_t* v, int32_t s) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    const int32_t p = __shfl_xor(v[j], M, 64);
-    v[j] = upper ? (p - v[j]) : (v[j] + p);
+    const int32_t p = (int32_t)xor_lane<M>((uint32_t)v[j]);
+    v[j] = p + __mul24(v[j], s);
   }
 }
 
-__device__ __forceinline__ void fwht128(float* v, int lane) {
+// Per-lane butterfly signs for the cross-lane stages (h = 8, 16, 32, 64).
+struct XSigns {
+  float f[4];
+  int32_t i[4];
+  __device__ __forceinline__ explicit XSigns(int lane) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const bool upper = (lane >> b) & 1;
+      f[b] = upper ? -1.0f : 1.0f;
+      i[b] = upper ? -1 : 1;
+    }
+  }
+};
+
+__device__ __forceinline__ void fwht128(float* v, const XSigns& sg) {
   fwht8_inlane(v);
-  fwht_xlane<1>(v, lane);
-  fwht_xlane<2>(v, lane);
-  fwht_xlane<4>(v, lane);
-  fwht_xlane<8>(v, lane);
+  fwht_xlane<1>(v, sg.f[0]);
+  fwht_xlane<2>(v, sg.f[1]);
+  fwht_xlane<4>(v, sg.f[2]);
+  fwht_xlane<8>(v, sg.f[3]);
 }
 
-__device__ __forceinline__ void fwht128_i(int32_t* v, int lane) {
+__device__ __forceinline__ void fwht128_i(int32_t* v, const XSigns& sg) {
   fwht8_inlane_i(v);
-  fwht_xlane_i<1>(v, lane);
-  fwht_xlane_i<2>(v, lane);
-  fwht_xlane_i<4>(v, lane);
-  fwht_xlane_i<8>(v, lane);
+  fwht_xlane_i<1>(v, sg.i[0]);
+  fwht_xlane_i<2>(v, sg.i[1]);
+  fwht_xlane_i<4>(v, sg.i[2]);
+  fwht_xlane_i<8>(v, sg.i[3]);
 }
 
 // The 8 sign bits of columns col0 .. col0 + 7 (col0 a multiple of 8).
@@ -422,15 +470,18 @@ __device__ __forceinline__ float flip(float v, uint32_t bits, int j) {
 }
 
 // ------------------------------------------------------------ look-back scan
-// Decoupled look-back (Merrill & Garland, 2016) over workgroups in ticket
-// order.  The scan scratch starts with one 64-bit counter holding
-// (epoch << 32 | next ticket); the workgroup that draws the last ticket of a
-// launch resets the ticket and advances the epoch, so every launch -- also a
-// replayed graph -- gets a fresh epoch without host help.  A status word packs
-// the value (32 bits: words since the start of this launch), a flag (2 bits:
-// 1 = aggregate, 2 = inclusive prefix) and the epoch (30 bits), so the array
-// never needs clearing.  Waits are bounded: a status that never arrives (only
-// possible after a corrupted scratch) ends the wait with an error status.
+// Decoupled look-back (Merrill & Garland, 2016) over workgroups in index
+// order.  Workgroups are dispatched in increasing index order, and a group
+// only ever waits for lower indices, so every wait ends; each wait is also
+// bounded, and a status that never arrives ends the wait with an error
+// status instead of a hang.  The scan scratch starts with a 64-bit epoch word
+// that the last workgroup of a launch advances after it has published its
+// inclusive prefix (by then every group has read the epoch, since that prefix
+// sums every group's published aggregate), so every launch -- also a
+// replayed graph -- gets a fresh epoch without host help.  A status word
+// packs the value (32 bits: words since the start of this launch), a flag
+// (2 bits: 1 = aggregate, 2 = inclusive prefix) and the epoch (30 bits), so
+// the array never needs clearing.
 
 constexpr uint32_t kEpochMask = 0x3FFFFFFFu;
 constexpr uint32_t kSpinLimit = 1u << 24;
@@ -441,108 +492,145 @@ __device__ __forceinline__ unsigned long long pack_status(uint32_t epoch, uint32
          (unsigned long long)value;
 }
 
+// Relaxed is enough: a status word carries its own value, and no other data
+// published by the workgroup is read through it.
 __device__ __forceinline__ void store_status(unsigned long long* p, unsigned long long v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ unsigned long long load_status(unsigned long long* p) {
-  return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ------------------------------------------------------------ bit assembly
 
-// OR `nbits` (<= 32) bits of v into the LDS bit array at bit position pos.
-__device__ __forceinline__ void or_bits(uint32_t* buf, uint32_t pos, uint32_t v) {
+// OR the 64 bits of v into the LDS bit array at bit position pos.
+__device__ __forceinline__ void or_bits64(uint32_t* buf, uint32_t pos, uint64_t v) {
   if (v == 0) return;
-  const uint32_t w = pos >> 5, sh = pos & 31;
-  atomicOr(&buf[w], v << sh);
-  if (sh) {
-    const uint32_t hi = v >> (32 - sh);
-    if (hi) atomicOr(&buf[w + 1], hi);
+  const uint32_t w = pos >> 5, sh = pos & 31u;
+  const uint32_t lo = (uint32_t)v, hi = (uint32_t)(v >> 32);
+  const uint32_t o0 = lo << sh;
+  const uint32_t o1 = sh ? ((hi << sh) | (lo >> (32u - sh))) : hi;
+  const uint32_t o2 = sh ? (hi >> (32u - sh)) : 0u;
+  if (o0) atomicOr(&buf[w], o0);
+  if (o1) atomicOr(&buf[w + 1], o1);
+  if (o2) atomicOr(&buf[w + 2], o2);
+}
+
+// 64 bits of the LDS bit array starting at bit pos (words past nw read 0).
+__device__ __forceinline__ uint64_t load_bits64(const uint32_t* buf, uint32_t pos, uint32_t nw) {
+  const uint32_t w = pos >> 5, sh = pos & 31u;
+  const uint32_t a = w < nw ? buf[w] : 0u;
+  const uint32_t b = w + 1 < nw ? buf[w + 1] : 0u;
+  const uint32_t c = w + 2 < nw ? buf[w + 2] : 0u;
+  const uint32_t lo = sh ? ((a >> sh) | (b << (32u - sh))) : a;
+  const uint32_t hi = sh ? ((b >> sh) | (c << (32u - sh))) : b;
+  return ((uint64_t)hi << 32) | lo;
+}
+
+// Bit offset of field j inside a lane's remainder region.
+template <int LAT>
+__device__ __forceinline__ uint32_t rem_offset(int j, uint32_t k0, uint32_t k1) {
+  if constexpr (LAT == kD4) {
+    return (uint32_t)(j >> 2) * (3u * k0 + k1) + (uint32_t)(j & 3) * k0;
+  } else if constexpr (LAT == kA2) {
+    return (uint32_t)(j >> 1) * (k0 + k1) + (uint32_t)(j & 1) * k0;
+  } else {
+    return (uint32_t)j * k0;
   }
 }
 
 // ------------------------------------------------------------ encode kernel
+// One workgroup encodes HQ_ENC_SUBS_PER_WG consecutive sub-streams (four
+// waves, HQ_ENC_SUBS_PER_WAVE each, one at a time), keeps their bits in LDS,
+// publishes the group's word count, and only then looks back for its
+// absolute word offset and writes payload and offsets.  KV = false is the
+// weight path (no rotation, no dither, fp32 norms) compiled without those
+// branches; KV = true reads the three options at run time.
 
-template <int LAT, int XT>
-__global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
-  extern __shared__ uint32_t smem[];
-  __shared__ uint32_t s_ticket, s_epoch;
-  __shared__ uint32_t s_words[HQ_WAVES_PER_WG];
-  __shared__ unsigned long long s_base;
-  __shared__ unsigned long long s_bits[2];
+// The 16 (bf16) or 32 (fp32) input bytes of one lane, loaded ahead of use.
+struct LaneInput {
+  uint4 a, b;
+};
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  if (tid == 0) {
-    const unsigned long long tk = atomicAdd(A.ticket, 1ull);
-    const uint32_t t = (uint32_t)tk, ep = (uint32_t)(tk >> 32);
-    // the last ticket of this launch: restart the tickets, advance the epoch
-    if (t == A.nwg - 1) atomicExch(A.ticket, (unsigned long long)(ep + 1u) << 32);
-    s_ticket = t;
-    s_epoch = ep & kEpochMask;
-    s_bits[0] = 0;
-    s_bits[1] = 0;
-  }
-  __syncthreads();
-  const uint32_t wg = s_ticket, epoch = s_epoch;
-  if (wg >= A.nwg) {  // only a corrupted scan scratch hands out such a ticket
-    if (tid == 0 && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_INVALID_ARG);
-    return;
-  }
-  const int64_t sub = (int64_t)wg * HQ_WAVES_PER_WG + wave;  // sub-stream within this call
-  const bool active = sub < A.nsub;
-
-  const int64_t lrow = active ? sub / A.spr : 0;              // row within x
-  const int64_t col0 = (active ? sub % A.spr : 0) * HQ_SUB;   // first column of the sub-stream
-  const int tile_in_sub = lane >> 4, q = lane & 15;
-  const int64_t col = col0 + tile_in_sub * HQ_TILE + q * 8;   // lane's first column
-  const int64_t grow = A.first_row + lrow;
-
-  // ---- load 8 scalars
-  float x[8];
-  if (active) {
+template <int XT>
+__device__ __forceinline__ LaneInput load_lane_input(const hq_encode_args& A, uint32_t sub, int lane) {
+  LaneInput in;
+  in.a = make_uint4(0u, 0u, 0u, 0u);
+  in.b = make_uint4(0u, 0u, 0u, 0u);
+  if (sub < (uint32_t)A.nsub) {
+    const uint32_t spr = (uint32_t)A.spr;
+    const uint32_t lrow = sub / spr;
+    const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
     if constexpr (XT == HQ_BF16) {
-      const uint4 raw = *(const uint4*)((const uint16_t*)A.x + lrow * A.ld + col);
-      const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
+      in.a = *(const uint4*)((const uint16_t*)A.x + (int64_t)lrow * A.ld + col);
+    } else {
+      const uint4* p = (const uint4*)((const float*)A.x + (int64_t)lrow * A.ld + col);
+      in.a = p[0];
+      in.b = p[1];
+    }
+  }
+  return in;
+}
+
+template <int LAT, int XT, bool KV>
+__device__ __forceinline__ void encode_substream(const hq_encode_args& A, uint32_t sub, int lane,
+                                                 const XSigns& sg, const LaneInput& in,
+                                                 uint32_t dbits, uint32_t* buf, uint32_t& W_out,
+                                                 uint32_t& kb_out, uint32_t& bits_out,
+                                                 bool& overflow_out) {
+  const bool active = sub < (uint32_t)A.nsub;  // wave-uniform
+  const uint32_t spr = (uint32_t)A.spr;
+  const uint32_t lrow = active ? sub / spr : 0u;
+  const uint32_t col0 = (active ? sub - lrow * spr : 0u) * HQ_SUB;
+  const uint32_t col = col0 + 8u * (uint32_t)lane;  // tile lane/16, coordinates 8 (lane % 16) + j
+  const int64_t grow = A.first_row + lrow;
+  const bool use_rot = KV && A.rotation;
+  const bool use_dither = KV && A.dither;
+  const bool fp16_norm = KV && A.norm_fp16;
+
+  // ---- the 8 scalars (loaded by the caller ahead of time)
+  float x[8];
+  {
+    const uint32_t w4[4] = {in.a.x, in.a.y, in.a.z, in.a.w};
+    if constexpr (XT == HQ_BF16) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         x[2 * i] = bf16_to_f32(w4[i] & 0xFFFFu);
         x[2 * i + 1] = bf16_to_f32(w4[i] >> 16);
       }
     } else {
-      const float4* p = (const float4*)((const float*)A.x + lrow * A.ld + col);
-      const float4 a = p[0], b = p[1];
-      x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-      x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-    }
-  } else {
+      const uint32_t w4b[4] = {in.b.x, in.b.y, in.b.z, in.b.w};
 #pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = 0.0f;
+      for (int i = 0; i < 4; ++i) {
+        x[i] = __uint_as_float(w4[i]);
+        x[4 + i] = __uint_as_float(w4b[i]);
+      }
+    }
   }
 
-  // ---- Normalize: tile norm as a pairwise tree in index order
+  // ---- Normalize: tile norm as a pairwise tree in index order (the lane
+  //      butterflies 1, 2, 4, 8 add the same pairs in the same order)
   float sq[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) sq[i] = x[i] * x[i];
   float ss = tree8(sq);
-  ss = ss + __shfl_xor(ss, 1, 64);
-  ss = ss + __shfl_xor(ss, 2, 64);
-  ss = ss + __shfl_xor(ss, 4, 64);
-  ss = ss + __shfl_xor(ss, 8, 64);
+  ss = ss + xor_lane_f<1>(ss);
+  ss = ss + xor_lane_f<2>(ss);
+  ss = ss + xor_lane_f<4>(ss);
+  ss = ss + xor_lane_f<8>(ss);
   const float r = __builtin_sqrtf(ss);
   float rs = r;
   bool bad_tile = !(r <= 3.0e38f);  // non-finite input
-  if (A.norm_fp16) {
-    const _Float16 h = (_Float16)r;
-    rs = (float)h;
+  if (fp16_norm) {
+    rs = (float)(_Float16)r;
     bad_tile = bad_tile || !(rs <= 65504.0f);
   }
   const float scale = (rs == 0.0f || bad_tile) ? 0.0f : A.alpha / rs;
-  if (active && q == 0) {
-    const int64_t t = grow * A.tpr + col / HQ_TILE;
-    if (A.norm_fp16) {
-      const _Float16 h = (_Float16)r;
-      ((_Float16*)A.norms)[t] = h;
+  if (active && (lane & 15) == 0) {
+    const int64_t t = grow * A.tpr + (col >> 7);
+    if (fp16_norm) {
+      ((_Float16*)A.norms)[t] = (_Float16)r;
     } else {
       ((float*)A.norms)[t] = r;
     }
@@ -553,16 +641,20 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   }
 
   // ---- RHT: v = H D x
-  const uint32_t dbits = sign_bits8(A.dmask, col);
 #pragma unroll
   for (int i = 0; i < 8; ++i) x[i] = flip(x[i], dbits, i);
-  fwht128(x, lane);
+  fwht128(x, sg);
 
   // ---- scale, rotate, dither
-  const uint32_t sbits = A.rotation ? sign_bits8(A.smask, q * 8) : 0u;
+  if (use_rot) {
+    const uint32_t sbits = sign_bits8(A.smask, (lane & 15) * 8);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) x[i] = flip(x[i] * scale, sbits, i);
-  if (A.dither) {
+    for (int i = 0; i < 8; ++i) x[i] = flip(x[i] * scale, sbits, i);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = x[i] * scale;
+  }
+  if (use_dither) {
     float u[8];
     dither8<LAT>(A.dither_seed, grow, col, u);
 #pragma unroll
@@ -582,51 +674,55 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   uint32_t sym[8];
   strip8<LAT>(c, sym);
 
-  // ---- Rice parameters (uniform per wave)
-  uint32_t sum0 = 0, sum1 = 0;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    if (sym_class<LAT>(j)) sum1 += sym[j]; else sum0 += sym[j];
-  }
+  // ---- Rice parameters (wave-uniform)
   uint32_t k0, k1;
   if (A.rice_k >= 0) {
     k0 = (uint32_t)A.rice_k;
     k1 = (LAT == kD4) ? (k0 > 0 ? k0 - 1 : 0) : k0;
   } else {
-    sum0 = readfirst(wave_sum_u32(sum0));
-    if (LAT == kA2) sum1 = readfirst(wave_sum_u32(sum1));
+    uint32_t s0 = 0, s1 = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (sym_class<LAT>(j)) s1 += sym[j]; else s0 += sym[j];
+    }
+    const uint32_t sum0 = wave_total(s0);
+    const uint32_t sum1 = (LAT == kA2) ? wave_total(s1) : 0u;
     uint32_t a0 = 0, a1 = 0;
 #pragma unroll
     for (int t = 1; t <= HQ_KMAX; ++t) {
       a0 += sum0 >= A.thr0[t];
-      a1 += sum1 >= A.thr1[t];
+      if (LAT == kA2) a1 += sum1 >= A.thr1[t];
     }
-    // the better of k* and k* + 1 on this sub-stream's symbols
+    // the better of k* and k* + 1: k* + 1 saves sum((m >> k) - (m >> (k+1)))
+    // unary bits and costs one remainder bit per symbol of the class
     const uint32_t b0 = a0 < HQ_KMAX ? a0 + 1 : a0;
     const uint32_t b1 = a1 < HQ_KMAX ? a1 + 1 : a1;
-    uint32_t la = 0, lb = 0, ma = 0, mb = 0;
+    uint32_t g0 = 0, g1 = 0;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       if (LAT == kD4) {
         const uint32_t ka = sym_class<LAT>(j) ? (a0 > 0 ? a0 - 1 : 0) : a0;
         const uint32_t kb = sym_class<LAT>(j) ? (b0 > 0 ? b0 - 1 : 0) : b0;
-        la += (sym[j] >> ka) + ka;
-        lb += (sym[j] >> kb) + kb;
+        g0 += (sym[j] >> ka) - (sym[j] >> kb);
       } else if (LAT == kA2 && sym_class<LAT>(j)) {
-        ma += (sym[j] >> a1) + a1;
-        mb += (sym[j] >> b1) + b1;
+        g1 += (sym[j] >> a1) - (sym[j] >> b1);
       } else {
-        la += (sym[j] >> a0) + a0;
-        lb += (sym[j] >> b0) + b0;
+        g0 += (sym[j] >> a0) - (sym[j] >> b0);
       }
     }
-    la = readfirst(wave_sum_u32(la));
-    lb = readfirst(wave_sum_u32(lb));
-    k0 = lb < la ? b0 : a0;
+    const uint32_t gain0 = wave_total(g0);
+    uint32_t cost0;
+    if (LAT == kD4) {
+      cost0 = (b0 - a0) * (3u * HQ_SUB / 4u) + ((b0 > 0 ? b0 - 1 : 0) - (a0 > 0 ? a0 - 1 : 0)) * (HQ_SUB / 4u);
+    } else if (LAT == kA2) {
+      cost0 = (b0 - a0) * (HQ_SUB / 2u);
+    } else {
+      cost0 = (b0 - a0) * HQ_SUB;
+    }
+    k0 = gain0 > cost0 ? b0 : a0;
     if (LAT == kA2) {
-      ma = readfirst(wave_sum_u32(ma));
-      mb = readfirst(wave_sum_u32(mb));
-      k1 = mb < ma ? b1 : a1;
+      const uint32_t gain1 = wave_total(g1);
+      k1 = gain1 > (b1 - a1) * (HQ_SUB / 2u) ? b1 : a1;
     } else {
       k1 = (LAT == kD4) ? (k0 > 0 ? k0 - 1 : 0) : k0;
     }
@@ -643,122 +739,245 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   }
   const uint32_t lrem = lane_rem_bits<LAT>(k0, k1);
   const uint32_t R = 64 * lrem;
-  const uint32_t uincl = wave_incl_scan_u32(ulen, lane);
-  const uint32_t U = readfirst(__shfl(uincl, 63, 64));
+  const uint32_t uincl = wave_scan_incl(ulen);
+  const uint32_t U = __builtin_amdgcn_readlane(uincl, 63);
   const uint32_t uoff = uincl - ulen;
   uint32_t W = (R + U + 31) >> 5;
-  const bool overflow = active && W > A.lds_words;
-  if (!active) W = 0;
-
   // A sub-stream that does not fit the plan's bound (only non-finite or
   // out-of-range input can do that) is written as all-zero symbols with
   // k = 0: 512 unary terminators, 16 words.
+  const bool overflow = active && W > A.lds_words;
+  if (!active) W = 0;
   if (overflow) W = HQ_SUB / 32;
-  if (lane == 0) s_words[wave] = W;
-  __syncthreads();
 
-  // ---- publish this workgroup's aggregate at once, so successors can pass it
-  uint32_t agg = 0;
-  for (int w = 0; w < HQ_WAVES_PER_WG; ++w) agg += s_words[w];
-  if (tid == 0 && wg > 0) store_status(&A.status[wg], pack_status(epoch, 1u, agg));
-
-  // ---- assemble the sub-stream in LDS (needs no global offset)
-  uint32_t* buf = smem + wave * A.lds_words;
-  for (uint32_t w = lane; w < W; w += 64) buf[w] = 0u;
-  __syncthreads();
+  // ---- assemble in this sub-stream's LDS buffer
+  for (uint32_t w = lane; w < W; w += 64) buf[w] = overflow ? 0xFFFFFFFFu : 0u;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
   if (active && !overflow) {
-    uint32_t pos = lane * lrem;
+    // remainder fields, packed per lane
+    const uint32_t rpos = (uint32_t)lane * lrem;
+    if (lrem <= 32) {
+      uint32_t acc = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-      or_bits(buf, pos, rv[j]);
-      pos += kk;
-    }
-    pos = R + uoff;
+      for (int j = 0; j < 8; ++j) acc |= rv[j] << rem_offset<LAT>(j, k0, k1);
+      or_bits64(buf, rpos, acc);
+    } else if (lrem <= 64) {
+      uint64_t acc = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      pos += qv[j];
-      or_bits(buf, pos, 1u);
-      pos += 1;
+      for (int j = 0; j < 8; ++j) acc |= (uint64_t)rv[j] << rem_offset<LAT>(j, k0, k1);
+      or_bits64(buf, rpos, acc);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) or_bits64(buf, rpos + rem_offset<LAT>(j, k0, k1), rv[j]);
     }
-  } else if (active && overflow) {
-    for (uint32_t w = lane; w < W; w += 64) buf[w] = 0xFFFFFFFFu;
+    // unary codes: q zeros and a one each
+    uint32_t upos = R + uoff;
+    if (ulen <= 64) {
+      uint64_t m = 0;
+      uint32_t t = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        t += qv[j];
+        m |= 1ull << t;
+        t += 1;
+      }
+      or_bits64(buf, upos, m);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        upos += qv[j];
+        or_bits64(buf, upos, 1ull);
+        upos += 1;
+      }
+    }
+  }
+  W_out = W;
+  kb_out = overflow ? 0u : (LAT == kA2 ? (k0 | (k1 << 4)) : k0);
+  bits_out = overflow ? (uint32_t)HQ_SUB : R + U;
+  overflow_out = overflow;
+}
+
+template <int LAT, int XT, bool KV>
+__global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
+  extern __shared__ uint32_t smem[];
+  __shared__ uint32_t s_epoch, s_stop;
+  __shared__ uint32_t s_words[HQ_ENC_SUBS_PER_WG];
+  __shared__ uint32_t s_part[HQ_WAVES_PER_WG], s_part2[HQ_WAVES_PER_WG];
+  __shared__ unsigned long long s_base;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = (int)readfirst((uint32_t)(tid >> 6));
+  const uint32_t wg = blockIdx.x;
+  if (tid == 0)
+    s_epoch = (uint32_t)__hip_atomic_load(A.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
+              kEpochMask;
+  const XSigns sg(lane);
+
+  // ---- issue every input load of this wave up front, so that only the first
+  //      one's latency is exposed
+  LaneInput in[HQ_ENC_SUBS_PER_WAVE];
+  uint32_t dbits[HQ_ENC_SUBS_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
+    const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)(i * HQ_WAVES_PER_WG + wave);
+    in[i] = load_lane_input<XT>(A, sub, lane);
+    const uint32_t spr = (uint32_t)A.spr;
+    const uint32_t lrow = sub < (uint32_t)A.nsub ? sub / spr : 0u;
+    const uint32_t col = (sub < (uint32_t)A.nsub ? sub - lrow * spr : 0u) * HQ_SUB + 8u * (uint32_t)lane;
+    dbits[i] = sign_bits8(A.dmask, col);
   }
 
-  // ---- look-back by wave 0: 64 predecessors per round trip
-  if (wave == 0) {
-    uint32_t prefix = 0;
-    bool timed_out = false;
-    int64_t hi = (int64_t)wg - 1;
-    while (hi >= 0) {
-      const int64_t idx = hi - lane;
-      unsigned long long st = 0;
-      bool ready = idx < 0;
-      uint32_t spins = 0;
-      // wait until every predecessor in this window has published something
-      for (;;) {
-        if (!ready) {
-          st = load_status(&A.status[idx]);
-          ready = (uint32_t)(st >> 34) == epoch && ((st >> 32) & 3u) != 0u;
-        }
-        if (__all(ready)) break;
-        if (++spins > kSpinLimit) {
-          timed_out = true;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
+  // ---- encode this group's sub-streams into LDS
+  uint32_t bitsum = 0, padsum = 0;
+#pragma unroll
+  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
+    const int li = i * HQ_WAVES_PER_WG + wave;  // neighbouring waves take neighbouring sub-streams
+    const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
+    uint32_t W, kb, bits;
+    bool ovf;
+    encode_substream<LAT, XT, KV>(A, sub, lane, sg, in[i], dbits[i], smem + li * A.lds_words, W, kb,
+                                  bits, ovf);
+    if (sub < (uint32_t)A.nsub) {
+      if (lane == 0) {
+        A.kparam[A.first_sub + sub] = (uint8_t)kb;
+        s_words[li] = W;
+        if (ovf && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_OVERFLOW);
       }
-      if (timed_out) break;
-      const bool incl = idx >= 0 && ((st >> 32) & 3u) == 2u;
-      const unsigned long long pmask = __ballot(incl);
-      const int stop = pmask ? __builtin_ctzll(pmask) : 64;  // nearest inclusive prefix
-      uint32_t v = (idx >= 0 && lane <= stop) ? (uint32_t)st : 0u;
-      v = wave_sum_u32(v);
-      prefix += v;
-      if (pmask) break;
-      hi -= 64;
+      bitsum += bits;
+      padsum += W * 32u - bits;
+    } else if (lane == 0) {
+      s_words[li] = 0;
     }
-    if (lane == 0) {
-      store_status(&A.status[wg], pack_status(epoch, 2u, prefix + agg));
-      if (timed_out && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
-      const unsigned long long base = A.append ? (unsigned long long)A.offsets[A.first_sub] : 0ull;
-      s_base = base + prefix;
+  }
+  if (lane == 0) {
+    s_part[wave] = bitsum;
+    s_part2[wave] = padsum;
+  }
+  __syncthreads();
+  const uint32_t epoch = readfirst(s_epoch);
+
+  // ---- publish this group's word count at once, so successors can pass it;
+  //      the group's bit counts go to its stats word first (at most 2^22
+  //      payload bits and 16 * 31 pad bits, packed as bits << 9 | pad)
+  uint32_t agg = 0;
+#pragma unroll
+  for (int li = 0; li < HQ_ENC_SUBS_PER_WG; ++li) agg += s_words[li];
+  if (tid == 0) {
+    if (A.stats) {
+      const uint32_t gb = s_part[0] + s_part[1] + s_part[2] + s_part[3];
+      const uint32_t gp = s_part2[0] + s_part2[1] + s_part2[2] + s_part2[3];
+      store_status(&A.wgstat[wg], pack_status(epoch, 1u, (gb << 9) | gp));
     }
+    if (wg > 0) store_status(&A.status[wg], pack_status(epoch, 1u, agg));
+  }
+
+  // ---- look-back: 256 predecessors per round trip, the whole group
+  uint32_t prefix = 0;
+  bool timed_out = false;
+  int64_t hi = (int64_t)wg - 1;
+  while (hi >= 0) {
+    const int64_t idx = hi - tid;
+    unsigned long long st = 0;
+    bool ready = idx < 0;
+    uint32_t spins = 0;
+    for (;;) {
+      if (!ready) {
+        st = load_status(&A.status[idx]);
+        ready = (uint32_t)(st >> 34) == epoch && ((st >> 32) & 3u) != 0u;
+      }
+      if (__syncthreads_and(ready)) break;
+      if (++spins > kSpinLimit) {
+        timed_out = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (timed_out) break;
+    const bool incl = idx >= 0 && ((st >> 32) & 3u) == 2u;
+    if (tid == 0) s_stop = 256u;
+    __syncthreads();
+    if (incl) atomicMin(&s_stop, (uint32_t)tid);
+    __syncthreads();
+    const uint32_t stop = s_stop;
+    const uint32_t v = wave_total((idx >= 0 && (uint32_t)tid <= stop) ? (uint32_t)st : 0u);
+    if (lane == 0) s_part[wave] = v;
+    __syncthreads();
+    prefix += s_part[0] + s_part[1] + s_part[2] + s_part[3];
+    __syncthreads();
+    if (stop < 256u) break;
+    hi -= 256;
+  }
+  if (tid == 0) {
+    store_status(&A.status[wg], pack_status(epoch, 2u, prefix + agg));
+    // the last group: every group has read this launch's epoch; advance it
+    if (wg == A.nwg - 1)
+      __hip_atomic_store(A.epoch, (unsigned long long)((epoch + 1u) & kEpochMask), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    if (timed_out && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
+    const unsigned long long base = A.append ? (unsigned long long)A.offsets[A.first_sub] : 0ull;
+    s_base = base + prefix;
   }
   __syncthreads();
 
+  // ---- write payload and offsets
+  const unsigned long long base = s_base;
   uint32_t before = 0;
-  for (int w = 0; w < wave; ++w) before += s_words[w];
-  const unsigned long long start = s_base + before;
-
-  // ---- write payload, offsets, k
-  if (active) {
+  int li_next = 0;
+  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
+    const int li = i * HQ_WAVES_PER_WG + wave;
+    const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
+    if (sub >= (uint32_t)A.nsub) break;
+    for (; li_next < li; ++li_next) before += s_words[li_next];
+    const uint32_t W = s_words[li];
+    const unsigned long long start = base + before;
+    const uint32_t* buf = smem + li * A.lds_words;
     const bool fits = start + W <= (unsigned long long)A.cap_words;
     if (fits) {
       for (uint32_t w = lane; w < W; w += 64) A.payload[start + w] = buf[w];
     }
     if (lane == 0) {
-      const int64_t gsub = A.first_sub + sub;
       if (sub == 0 && !A.append) A.offsets[A.first_sub] = 0u;
-      A.offsets[gsub + 1] = (uint32_t)(start + W);
-      const uint32_t kb = overflow ? 0u : (LAT == kA2 ? (k0 | (k1 << 4)) : k0);
-      A.kparam[gsub] = (uint8_t)kb;
-      if (A.stats) {
-        if (!fits) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CAPACITY);
-        if (overflow) {
-          atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_OVERFLOW);
-        }
-        const uint32_t bits = overflow ? (uint32_t)HQ_SUB : R + U;
-        atomicAdd(&s_bits[0], (unsigned long long)bits);
-        atomicAdd(&s_bits[1], (unsigned long long)(W * 32u - bits));
-      }
+      A.offsets[A.first_sub + sub + 1] = (uint32_t)(start + W);
+      if (!fits && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CAPACITY);
     }
   }
-  if (A.stats) {
+  // ---- bit counts: the last group of every 256 adds up their stats words
+  //      (all of them were stored before their owners' aggregates, which this
+  //      group's look-back has passed), so the stats block takes one atomic
+  //      per 256 groups instead of one per group
+  if (A.stats && ((wg & 255u) == 255u || wg == A.nwg - 1)) {
+    const uint32_t idx = (wg & ~255u) + (uint32_t)tid;
+    uint32_t v = 0;
+    bool late = false;
+    if (idx <= wg) {
+      uint32_t spins = 0;
+      for (;;) {
+        const unsigned long long st = load_status(&A.wgstat[idx]);
+        if ((uint32_t)(st >> 34) == epoch && ((st >> 32) & 3u) != 0u) {
+          v = (uint32_t)st;
+          break;
+        }
+        if (++spins > kSpinLimit) {
+          late = true;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    }
+    const uint32_t gb = wave_total(v >> 9), gp = wave_total(v & 511u);
     __syncthreads();
+    if (lane == 0) {
+      s_part[wave] = gb;
+      s_part2[wave] = gp;
+    }
+    __syncthreads();
+    if (late) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
     if (tid == 0) {
-      atomicAdd(&A.stats->payload_bits, s_bits[0]);
-      atomicAdd(&A.stats->pad_bits, s_bits[1]);
+      atomicAdd(&A.stats->payload_bits,
+                (unsigned long long)s_part[0] + s_part[1] + s_part[2] + s_part[3]);
+      atomicAdd(&A.stats->pad_bits,
+                (unsigned long long)s_part2[0] + s_part2[1] + s_part2[2] + s_part2[3]);
     }
   }
 }
@@ -767,18 +986,19 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
 // Rice decode of one sub-stream per wave: the remainder fields are at fixed
 // positions; the unary terminators are located by per-word popcounts, a
 // wave prefix sum and a select inside the word that holds terminator 8 l - 1,
-// after which lane l walks its own 8 codes.  MODE 0: fp32 out, 1: bf16 out,
-// 2: int8 lattice codes and per-tile g (no inverse RHT).
+// after which lane l walks its own 8 codes through a 64-bit register window.
+// MODE 0: fp32 out, 1: bf16 out, 2: int8 lattice codes and per-tile g (no
+// inverse RHT).
 
 template <int LAT>
-__device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, int64_t gsub, int lane,
-                                               uint32_t* buf, uint32_t* starts, bool active,
+__device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, uint32_t gsub, bool active,
+                                               int lane, uint32_t* buf, uint32_t* starts,
                                                uint32_t* sym) {
   uint32_t start = 0, end = 0, kb = 0;
   if (active) {
-    start = A.offsets[gsub];
-    end = A.offsets[gsub + 1];
-    kb = A.kparam[gsub];
+    start = readfirst(A.offsets[gsub]);
+    end = readfirst(A.offsets[gsub + 1]);
+    kb = readfirst(A.kparam[gsub]);
   }
   const uint32_t k0 = (LAT == kA2) ? (kb & 15u) : kb;
   const uint32_t k1 = (LAT == kA2) ? (kb >> 4) : (LAT == kD4 ? (k0 > 0 ? k0 - 1 : 0) : k0);
@@ -788,7 +1008,7 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, int64_t 
   bool ok = active && end >= start && (int64_t)end <= A.cap_words && W <= A.lds_words &&
             k0 <= HQ_KMAX && R <= 32u * W;
   const uint32_t Wl = ok ? W : 0u;
-  for (uint32_t w = lane; w < Wl; w += 64) buf[w] = A.payload[start + w];
+  for (uint32_t w = lane; w < Wl; w += 64) buf[w] = A.payload[(uint64_t)start + w];
   starts[lane] = (lane == 0) ? R : 0xFFFFFFFFu;
   __syncthreads();
 
@@ -800,58 +1020,58 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, int64_t 
     const uint32_t wi = base + lane;
     const uint32_t v = (wi < nuw) ? buf[uw0 + wi] : 0u;
     const uint32_t cnt = __popc(v);
-    const uint32_t incl = wave_incl_scan_u32(cnt, lane);
+    const uint32_t incl = wave_scan_incl(cnt);
     const uint32_t P = carry + incl - cnt;
     for (uint32_t t = (P & ~7u) + 7u; t < P + cnt; t += 8u) {
       const uint32_t j = (t + 1u) >> 3;
       if (j < 64u) starts[j] = (uw0 + wi) * 32u + select32(v, t - P) + 1u;
     }
-    carry += __shfl(incl, 63, 64);
+    carry += __builtin_amdgcn_readlane(incl, 63);
   }
   __syncthreads();
 
-  // lane's 8 quotients
+  // lane's 8 quotients through a 64-bit window
   uint32_t pos = starts[lane];
-  uint32_t qv[8];
   const uint32_t nbits = 32u * Wl;
+  ok = ok && pos < nbits;
+  uint32_t qv[8];
+  uint64_t win = ok ? load_bits64(buf, pos, Wl) : 0ull;
+  uint32_t valid = 64;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     uint32_t q = 0;
-    if (ok && pos < nbits) {
-      uint32_t wi = pos >> 5, b = pos & 31u;
-      uint32_t v = buf[wi] >> b;
-      while (v == 0u) {
-        q += 32u - b;
-        b = 0;
-        ++wi;
-        if (wi >= Wl) break;
-        v = buf[wi];
-      }
-      if (v == 0u) {
+    while (ok && win == 0ull) {  // the code runs past the window: slide it
+      q += valid;
+      pos += valid;
+      if (pos >= nbits) {
         ok = false;
-      } else {
-        const uint32_t tz = __builtin_ctz(v);
-        q += tz;
-        pos = wi * 32u + b + tz + 1u;
+        break;
       }
-    } else {
-      ok = false;
+      win = load_bits64(buf, pos, Wl);
+      valid = 64;
     }
+    const uint32_t lo = (uint32_t)win, hi = (uint32_t)(win >> 32);
+    const uint32_t tz = lo ? (uint32_t)__builtin_ctz(lo) : 32u + (uint32_t)__builtin_ctz(hi | (hi == 0u));
+    q += tz;
+    pos += tz + 1;
+    valid -= tz + 1;
+    win = (tz >= 63u) ? 0ull : (win >> (tz + 1));
     qv[j] = q;
   }
   // lane's 8 remainders
-  uint32_t rp = lane * lrem;
+  const uint32_t rpos = (uint32_t)lane * lrem;
+  const uint64_t rw = (ok && lrem) ? load_bits64(buf, rpos, Wl) : 0ull;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-    uint32_t r = 0;
-    if (ok && kk) {
-      const uint32_t wi = rp >> 5, sh = rp & 31u;
-      const unsigned long long lo = buf[wi];
-      const unsigned long long hi = (wi + 1 < Wl) ? buf[wi + 1] : 0ull;
-      r = (uint32_t)(((hi << 32) | lo) >> sh) & ((1u << kk) - 1u);
+    const uint32_t off = rem_offset<LAT>(j, k0, k1);
+    uint32_t r;
+    if (lrem <= 64) {
+      r = (uint32_t)(rw >> off);
+    } else {
+      r = ok ? (uint32_t)load_bits64(buf, rpos + off, Wl) : 0u;
     }
-    rp += kk;
+    r &= (1u << kk) - 1u;
     sym[j] = (qv[j] << kk) | r;
   }
   if (!ok) {
@@ -861,33 +1081,40 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, int64_t 
   return ok;
 }
 
-template <int LAT, int MODE>
+template <int LAT, int MODE, bool KV>
 __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
   extern __shared__ uint32_t smem[];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int64_t sub = (int64_t)blockIdx.x * HQ_WAVES_PER_WG + wave;
-  const bool active = sub < A.nsub;
-  const int64_t gsub = A.first_sub + sub;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint32_t wave = readfirst((uint32_t)(tid >> 6));
+  const uint32_t sub = blockIdx.x * HQ_WAVES_PER_WG + wave;
+  const bool active = sub < (uint32_t)A.nsub;
+  const uint32_t gsub = (uint32_t)A.first_sub + sub;
   uint32_t* buf = smem + wave * (A.lds_words + 64);
   uint32_t* starts = buf + A.lds_words;
+  const bool use_rot = KV && A.rotation;
+  const bool use_dither = KV && A.dither;
+  const bool fp16_norm = KV && A.norm_fp16;
 
   uint32_t sym[8];
-  const bool ok = decode_symbols<LAT>(A, gsub, lane, buf, starts, active, sym);
-  if (active && !ok && lane == 0 && A.stats) {
-    atomicAdd(&A.stats->corrupt_substreams, 1u);
-    atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+  const bool ok = decode_symbols<LAT>(A, gsub, active, lane, buf, starts, sym);
+  if (active && !ok && A.stats) {
+    // count the sub-stream once (its first failing lane reports)
+    const unsigned long long bad = __ballot(!ok);
+    if ((unsigned)lane == (unsigned)__builtin_ctzll(bad)) {
+      atomicAdd(&A.stats->corrupt_substreams, 1u);
+      atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+    }
   }
   int32_t c[8];
   unstrip8<LAT>(sym, c);
 
-  const int64_t lrow = active ? sub / A.spr : 0;
-  const int64_t col0 = (active ? sub % A.spr : 0) * HQ_SUB;
-  const int tile_in_sub = lane >> 4, q = lane & 15;
-  const int64_t col = col0 + tile_in_sub * HQ_TILE + q * 8;
+  const uint32_t spr = (uint32_t)A.spr;
+  const uint32_t lrow = active ? sub / spr : 0u;
+  const uint32_t col = (active ? sub - lrow * spr : 0u) * HQ_SUB + 8u * (uint32_t)lane;
   const int64_t grow = A.first_row + lrow;
-  const int64_t tix = grow * A.tpr + col / HQ_TILE;
+  const int64_t tix = grow * A.tpr + (col >> 7);
   float rs = 0.0f;
-  if (active) rs = A.norm_fp16 ? (float)((const _Float16*)A.norms)[tix] : ((const float*)A.norms)[tix];
+  if (active) rs = fp16_norm ? (float)((const _Float16*)A.norms)[tix] : ((const float*)A.norms)[tix];
   const float g = rs / A.alpha_n;
 
   if constexpr (MODE == 2) {
@@ -901,27 +1128,28 @@ __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
       if (v < -127) { v = -127; ++clamps; }
       packed[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
     }
-    int8_t* out = (int8_t*)A.y + lrow * A.ld + col;
+    int8_t* out = (int8_t*)A.y + (int64_t)lrow * A.ld + col;
     *(uint2*)out = make_uint2(packed[0], packed[1]);
-    if (q == 0) A.g[lrow * A.tpr + col / HQ_TILE] = g;
+    if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
     if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
     return;
   } else {
+    const XSigns sg(lane);
     float y[8];
-    const bool exact = !A.dither && LAT != kA2;
-    const uint32_t sbits = A.rotation ? sign_bits8(A.smask, q * 8) : 0u;
     const uint32_t dbits = sign_bits8(A.dmask, col);
-    if (exact) {
+    const uint32_t sbits = use_rot ? sign_bits8(A.smask, (lane & 15) * 8) : 0u;
+    if (!use_dither && LAT != kA2) {
+      // integer codes: the Walsh-Hadamard transform is exact in int32
       int32_t v[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) v[j] = ((sbits >> j) & 1u) ? -c[j] : c[j];
-      fwht128_i(v, lane);
+      fwht128_i(v, sg);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = (float)(((dbits >> j) & 1u) ? -v[j] : v[j]) * g;
+      for (int j = 0; j < 8; ++j) y[j] = flip((float)v[j], dbits, j) * g;
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j) y[j] = code_coord<LAT>(c[j], j);
-      if (A.dither) {
+      if (use_dither) {
         float u[8];
         dither8<LAT>(A.dither_seed, grow, col, u);
 #pragma unroll
@@ -929,20 +1157,20 @@ __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
       }
 #pragma unroll
       for (int j = 0; j < 8; ++j) y[j] = flip(y[j], sbits, j);
-      fwht128(y, lane);
+      fwht128(y, sg);
 #pragma unroll
       for (int j = 0; j < 8; ++j) y[j] = flip(y[j], dbits, j) * g;
     }
     if (!active) return;
     if constexpr (MODE == 0) {
-      float4* out = (float4*)((float*)A.y + lrow * A.ld + col);
+      float4* out = (float4*)((float*)A.y + (int64_t)lrow * A.ld + col);
       out[0] = make_float4(y[0], y[1], y[2], y[3]);
       out[1] = make_float4(y[4], y[5], y[6], y[7]);
     } else {
-      uint32_t w[4];
+      __bf16 b[8];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) w[i] = f32_to_bf16(y[2 * i]) | (f32_to_bf16(y[2 * i + 1]) << 16);
-      *(uint4*)((uint16_t*)A.y + lrow * A.ld + col) = make_uint4(w[0], w[1], w[2], w[3]);
+      for (int j = 0; j < 8; ++j) b[j] = (__bf16)y[j];
+      *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = *(const uint4*)b;
     }
   }
 }
@@ -957,6 +1185,7 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int64_t row = blockIdx.x;
   const uint16_t* arow = (const uint16_t*)A.a + row * A.lda;
+  const XSigns sg(lane);
   float amax = 0.0f;
   for (int64_t base = (int64_t)wave * HQ_SUB; base < A.K; base += 4 * HQ_SUB) {
     const int64_t col = base + (lane >> 4) * HQ_TILE + (lane & 15) * 8;
@@ -971,7 +1200,7 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
     const uint32_t dbits = sign_bits8(A.dmask, col);
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] = flip(v[i], dbits, i);
-    fwht128(v, lane);
+    fwht128(v, sg);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
@@ -1107,57 +1336,77 @@ __global__ void hq_zero_kernel(uint32_t* p, size_t n) {
 }
 
 template <int LAT>
-int launch_encode_lat(const hq_encode_args& a, int xt, hipStream_t st) {
-  const size_t lds = (size_t)a.lds_words * HQ_WAVES_PER_WG * sizeof(uint32_t);
-  if (xt == HQ_BF16)
-    hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_BF16>), dim3(a.nwg), dim3(256), lds, st, a);
-  else
-    hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_FP32>), dim3(a.nwg), dim3(256), lds, st, a);
+int launch_encode_lat(const hq_encode_args& a, int xt, bool kv, hipStream_t st) {
+  const size_t lds = (size_t)a.lds_words * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
+  if (xt == HQ_BF16) {
+    if (kv)
+      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_BF16, true>), dim3(a.nwg), dim3(256), lds, st, a);
+    else
+      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_BF16, false>), dim3(a.nwg), dim3(256), lds, st, a);
+  } else {
+    if (kv)
+      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_FP32, true>), dim3(a.nwg), dim3(256), lds, st, a);
+    else
+      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_FP32, false>), dim3(a.nwg), dim3(256), lds, st, a);
+  }
   return (int)hipGetLastError();
 }
 
+template <int LAT, int MODE>
+void launch_decode_mode(const hq_decode_args& a, bool kv, uint32_t nwg, size_t lds, hipStream_t st) {
+  if (kv)
+    hipLaunchKernelGGL((hq_decode_kernel<LAT, MODE, true>), dim3(nwg), dim3(256), lds, st, a);
+  else
+    hipLaunchKernelGGL((hq_decode_kernel<LAT, MODE, false>), dim3(nwg), dim3(256), lds, st, a);
+}
+
 template <int LAT>
-int launch_decode_lat(const hq_decode_args& a, int mode, hipStream_t st) {
+int launch_decode_lat(const hq_decode_args& a, int mode, bool kv, hipStream_t st) {
   const uint32_t nwg = (uint32_t)((a.nsub + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG);
   const size_t lds = (size_t)(a.lds_words + 64) * HQ_WAVES_PER_WG * sizeof(uint32_t);
   if (mode == 0)
-    hipLaunchKernelGGL((hq_decode_kernel<LAT, 0>), dim3(nwg), dim3(256), lds, st, a);
+    launch_decode_mode<LAT, 0>(a, kv, nwg, lds, st);
   else if (mode == 1)
-    hipLaunchKernelGGL((hq_decode_kernel<LAT, 1>), dim3(nwg), dim3(256), lds, st, a);
+    launch_decode_mode<LAT, 1>(a, kv, nwg, lds, st);
   else
-    hipLaunchKernelGGL((hq_decode_kernel<LAT, 2>), dim3(nwg), dim3(256), lds, st, a);
+    launch_decode_mode<LAT, 2>(a, kv, nwg, lds, st);
   return (int)hipGetLastError();
 }
 
 }  // namespace
 
+static bool kv_variant(const hq_plan_s* p) { return p->rotation || p->dither || p->norm_fp16; }
+
 int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, int xt, void* stream) {
   hipStream_t st = (hipStream_t)stream;
+  const bool kv = kv_variant(p);
   switch (p->lattice) {
-    case HQ_E8: return launch_encode_lat<kE8>(a, xt, st);
-    case HQ_D4: return launch_encode_lat<kD4>(a, xt, st);
-    case HQ_A2: return launch_encode_lat<kA2>(a, xt, st);
-    default: return launch_encode_lat<kZ>(a, xt, st);
+    case HQ_E8: return launch_encode_lat<kE8>(a, xt, kv, st);
+    case HQ_D4: return launch_encode_lat<kD4>(a, xt, kv, st);
+    case HQ_A2: return launch_encode_lat<kA2>(a, xt, kv, st);
+    default: return launch_encode_lat<kZ>(a, xt, kv, st);
   }
 }
 
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   const int mode = (yt == HQ_FP32) ? 0 : 1;
+  const bool kv = kv_variant(p);
   switch (p->lattice) {
-    case HQ_E8: return launch_decode_lat<kE8>(a, mode, st);
-    case HQ_D4: return launch_decode_lat<kD4>(a, mode, st);
-    case HQ_A2: return launch_decode_lat<kA2>(a, mode, st);
-    default: return launch_decode_lat<kZ>(a, mode, st);
+    case HQ_E8: return launch_decode_lat<kE8>(a, mode, kv, st);
+    case HQ_D4: return launch_decode_lat<kD4>(a, mode, kv, st);
+    case HQ_A2: return launch_decode_lat<kA2>(a, mode, kv, st);
+    default: return launch_decode_lat<kZ>(a, mode, kv, st);
   }
 }
 
 int hq_launch_decode_int8(const hq_plan_s* p, const hq_decode_args& a, void* stream) {
   hipStream_t st = (hipStream_t)stream;
+  const bool kv = kv_variant(p);
   switch (p->lattice) {
-    case HQ_E8: return launch_decode_lat<kE8>(a, 2, st);
-    case HQ_D4: return launch_decode_lat<kD4>(a, 2, st);
-    default: return launch_decode_lat<kZ>(a, 2, st);
+    case HQ_E8: return launch_decode_lat<kE8>(a, 2, kv, st);
+    case HQ_D4: return launch_decode_lat<kD4>(a, 2, kv, st);
+    default: return launch_decode_lat<kZ>(a, 2, kv, st);
   }
 }
 

@@ -64,8 +64,9 @@ def check_roundtrip(hq, P, snr, x, label, append_chunks=None):
     err = np.abs(g.astype(np.float64) - ref).reshape(rows, -1, 128).max(axis=2)
     assert np.all(err[~skip] <= 1e-5 * unit[~skip]), err.max()
     exact = np.mean(g.reshape(rows, -1, 128)[~skip] == ref.reshape(rows, -1, 128)[~skip])
-    ref16 = torch.from_numpy(ref).to(torch.bfloat16)
-    b16 = (y16.cpu().view(torch.int16) == ref16.view(torch.int16)).numpy().reshape(rows, -1, 128)
+    # bf16 output = RNE(fp32 reconstruction); compared by value (+0 == -0)
+    ref16 = torch.from_numpy(ref).to(torch.bfloat16).float()
+    b16 = (y16.cpu().float() == ref16).numpy().reshape(rows, -1, 128)
     assert b16[~skip].all()
     print(f"[parity] {label}: {res['substreams']} sub-streams, exempt blocks "
           f"{res['exempt_blocks']}, fp32 bit-exact fraction {exact:.6f}", flush=True)
