@@ -290,18 +290,27 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
     if (splitmix_negative(rht_seed, (uint64_t)j)) dm[(size_t)(j >> 5)] |= 1u << (j & 31);
   for (int j = 0; j < tile; ++j)
     if (splitmix_negative(o.rot_seed, (uint64_t)j)) sm[(size_t)(j >> 5)] |= 1u << (j & 31);
-  if (hipMalloc((void**)&p->d_dmask, sizeof(uint32_t) * (size_t)nw) != hipSuccess ||
-      hipMalloc((void**)&p->d_smask, sizeof(uint32_t) * 4) != hipSuccess) {
+  const int64_t npairs = (cols + 1) / 2;
+  std::vector<uint32_t> ds((size_t)npairs, 0u);
+  for (int64_t j = 0; j < cols; ++j)
+    if ((dm[(size_t)(j >> 5)] >> (j & 31)) & 1u) ds[(size_t)(j >> 1)] |= (j & 1) ? 0x80000000u : 0x8000u;
+  p->d_dmask = nullptr;
+  p->d_smask = nullptr;
+  p->d_dsign16 = nullptr;
+  bool ok = hipMalloc((void**)&p->d_dmask, sizeof(uint32_t) * (size_t)nw) == hipSuccess &&
+            hipMalloc((void**)&p->d_smask, sizeof(uint32_t) * 4) == hipSuccess &&
+            hipMalloc((void**)&p->d_dsign16, sizeof(uint32_t) * (size_t)npairs) == hipSuccess;
+  ok = ok &&
+       hipMemcpy(p->d_dmask, dm.data(), sizeof(uint32_t) * (size_t)nw, hipMemcpyHostToDevice) ==
+           hipSuccess &&
+       hipMemcpy(p->d_smask, sm.data(), sizeof(uint32_t) * 4, hipMemcpyHostToDevice) ==
+           hipSuccess &&
+       hipMemcpy(p->d_dsign16, ds.data(), sizeof(uint32_t) * (size_t)npairs,
+                 hipMemcpyHostToDevice) == hipSuccess;
+  if (!ok) {
     if (p->d_dmask) hipFree(p->d_dmask);
-    delete p;
-    return HQ_ERR_HIP;
-  }
-  if (hipMemcpy(p->d_dmask, dm.data(), sizeof(uint32_t) * (size_t)nw, hipMemcpyHostToDevice) !=
-          hipSuccess ||
-      hipMemcpy(p->d_smask, sm.data(), sizeof(uint32_t) * 4, hipMemcpyHostToDevice) !=
-          hipSuccess) {
-    hipFree(p->d_dmask);
-    hipFree(p->d_smask);
+    if (p->d_smask) hipFree(p->d_smask);
+    if (p->d_dsign16) hipFree(p->d_dsign16);
     delete p;
     return HQ_ERR_HIP;
   }
@@ -331,6 +340,7 @@ hq_status hq_plan_destroy(hq_plan_t p) {
   if (!p) return HQ_ERR_INVALID_ARG;
   hipFree(p->d_dmask);
   hipFree(p->d_smask);
+  hipFree(p->d_dsign16);
   delete p;
   return HQ_OK;
 }
@@ -385,6 +395,7 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
   a.kparam = s->kparam;
   a.norms = s->norms;
   a.dmask = p->d_dmask;
+  a.dsign16 = p->d_dsign16;
   a.smask = p->d_smask;
   a.stats = s->stats;
   a.epoch = (unsigned long long*)s->scan;
@@ -399,8 +410,12 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
   a.lds_words = (uint32_t)p->max_words_sub;
   a.dither_seed = p->dither_seed;
   a.alpha = p->alpha;
-  std::memcpy(a.thr0, p->thr[0], sizeof(a.thr0));
-  std::memcpy(a.thr1, p->thr[1], sizeof(a.thr1));
+  // class sums stay below 2^26 (512 symbols of at most 2^17), so thresholds
+  // past 2^30 are unreachable; the kernel compares in signed 32-bit
+  for (int t = 0; t <= HQ_KMAX; ++t) {
+    a.thr0[t] = std::min<uint32_t>(p->thr[0][t], 1u << 30);
+    a.thr1[t] = std::min<uint32_t>(p->thr[1][t], 1u << 30);
+  }
   const int e = hq_launch_encode(p, a, xt, stream);
   if (e) return HQ_ERR_HIP;
   s->rows = row0 + rows;

@@ -28,6 +28,8 @@ struct hq_plan_s {
   uint32_t thr[2][HQ_KMAX + 1];
   int64_t max_words_sub;   // capacity bound of one sub-stream, in 32-bit words
   uint32_t* d_dmask;       // device: RHT sign bit per global column (1 = -1)
+  uint32_t* d_dsign16;     // device: per column pair, the RHT signs as bf16 sign
+                           // bits (bit 15: even column, bit 31: odd column)
   uint32_t* d_smask;       // device: rotation sign bit per tile coordinate
   int device;
 };
@@ -47,6 +49,7 @@ struct hq_encode_args {
   uint8_t* kparam;
   void* norms;
   const uint32_t* dmask;
+  const uint32_t* dsign16;  // RHT signs as bf16 XOR words, one per column pair
   const uint32_t* smask;
   hq_stats* stats;
   unsigned long long* epoch;   // scan scratch: the launch epoch

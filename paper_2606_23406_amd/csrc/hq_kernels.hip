@@ -540,73 +540,241 @@ __device__ __forceinline__ uint32_t rem_offset(int j, uint32_t k0, uint32_t k1) 
   }
 }
 
+// ------------------------------------------------------------ twisted FWHT
+// A cross-lane butterfly written as one multiply-add per value,
+//   u <- u + s * u[l ^ M]      (s = +1 on the lower lane, -1 on the upper),
+// leaves the lower lane a + b and the upper lane b - a = -(a - b): the
+// butterfly output times s, rounded identically (round-to-nearest-even
+// commutes with negation).  The partner lane of a stage shares the signs of
+// every earlier stage, so earlier factors pull out of the butterfly and four
+// chained stages leave each lane its outputs times sigma, the product of its
+// four stage signs.  Callers fold sigma into the per-tile factor that
+// follows.  The h = 8, 16, 64 stages are one DPP-fused v_fmac each
+// (quad_perm and row_ror lane moves); the h = 32 stage (lane l ^ 4) reads
+// its partner through ds_swizzle.
+
+#define HQ_DPP_FULL "row_mask:0xf bank_mask:0xf bound_ctrl:1"
+// v[j] += s * v[partner lane][j] for the 8 values of a lane; the s_nop pairs
+// cover the two wait states between a VALU write and a DPP read of a VGPR.
+#define HQ_FMAC_DPP8(CTRL, v, s)                                                            \
+  asm("s_nop 1\n\t"                                                                         \
+      "v_fmac_f32_dpp %0, %0, %8 " CTRL " " HQ_DPP_FULL "\n\t"                              \
+      "v_fmac_f32_dpp %1, %1, %8 " CTRL " " HQ_DPP_FULL "\n\t"                              \
+      "v_fmac_f32_dpp %2, %2, %8 " CTRL " " HQ_DPP_FULL "\n\t"                              \
+      "v_fmac_f32_dpp %3, %3, %8 " CTRL " " HQ_DPP_FULL "\n\t"                              \
+      "v_fmac_f32_dpp %4, %4, %8 " CTRL " " HQ_DPP_FULL "\n\t"                              \
+      "v_fmac_f32_dpp %5, %5, %8 " CTRL " " HQ_DPP_FULL "\n\t"                              \
+      "v_fmac_f32_dpp %6, %6, %8 " CTRL " " HQ_DPP_FULL "\n\t"                              \
+      "v_fmac_f32_dpp %7, %7, %8 " CTRL " " HQ_DPP_FULL "\n\t"                              \
+      "s_nop 1"                                                                             \
+      : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), \
+        "+v"(v[7])                                                                          \
+      : "v"(s))
+
+// Value of lane l ^ 4 (ds_swizzle bit-mask mode: and 0x1F, or 0, xor 4).
+__device__ __forceinline__ float swz_xor4(float v) {
+  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x101F));
+}
+
+// Value of lane l ^ M for M = 1, 2, 8 (bound_ctrl DPP moves, which fold into
+// the consuming VOP2 instruction).
+template <int M>
+__device__ __forceinline__ float dpp_xor(float v) {
+  constexpr int ctrl = M == 1 ? kDppQuadXor1 : (M == 2 ? kDppQuadXor2 : kDppRowRor8);
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), ctrl, 0xF, 0xF, true));
+}
+
+// Stage signs of a lane (h = 8, 16, 32, 64 <-> lane bits 0..3) and sigma's
+// sign bit.
+struct TwSigns {
+  float f[4];
+  uint32_t sigma;  // 0 or 0x80000000
+  __device__ __forceinline__ explicit TwSigns(int lane) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b) f[b] = ((lane >> b) & 1) ? -1.0f : 1.0f;
+    sigma = (uint32_t)(__popc((uint32_t)lane & 15u) & 1) << 31;
+  }
+};
+
+// v = sigma * (H v) over the tile (in-lane stages h = 1, 2, 4 first).
+__device__ __forceinline__ void fwht128_tw(float* v, const TwSigns& sg) {
+  fwht8_inlane(v);
+  HQ_FMAC_DPP8("quad_perm:[1,0,3,2]", v, sg.f[0]);
+  HQ_FMAC_DPP8("quad_perm:[2,3,0,1]", v, sg.f[1]);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = __builtin_fmaf(swz_xor4(v[j]), sg.f[2], v[j]);
+  HQ_FMAC_DPP8("row_ror:8", v, sg.f[3]);
+}
+
+__device__ __forceinline__ float xor_sign(float v, uint32_t bit) {
+  return __uint_as_float(__float_as_uint(v) ^ bit);
+}
+
+// --------------------------------------------------- E8 decision in closed form
+// With ea_i = z_i - E_i (E_i the nearest even integer, exact in fp32) and the
+// odd candidate O_i = E_i + sgn(ea_i), |eb_i| = 1 - |ea_i|, so before the
+// parity fixes sum(ea^2) - sum(eb^2) = sum(2|ea_i| - 1); a fix moves one
+// coordinate to the next point of its class, adding 4 (1 - max|e|) to that
+// class's distance.  Hence
+//   da - db = 2 sum|ea_i| - 8 + [odd_a] 4 (1 - max|ea|) - [odd_b] 4 min|ea|.
+// Rounding moves the two fp32 tree sums by far less than kE8Tie, so a lane
+// outside the tie band takes the same coset as the two-sum comparison; a
+// wave with any lane inside the band runs quant_e8 step by step.
+
+constexpr float kE8Tie = 1.0e-3f;
+
+// Stripped 2E8 symbols of one lane: h_i = (c_i - cb) / 2 with c the nearest
+// point and cb its coset bit.
+__device__ __forceinline__ void e8_nearest(const float* z, int32_t* h, int32_t& cb) {
+  float E[8], ea[8], t[8];
+  float SA = 0.0f, ST = 0.0f, Sabs = 0.0f, mx = 0.0f, mn = 2.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float ka = __builtin_rintf(z[i] * 0.5f);
+    E[i] = ka * 2.0f;
+    ea[i] = z[i] - E[i];
+    t[i] = __builtin_copysignf(1.0f, ea[i]);
+    const float a = __builtin_fabsf(ea[i]);
+    SA += ka;
+    ST += t[i];
+    Sabs += a;
+    mx = __builtin_fmaxf(mx, a);
+    mn = __builtin_fminf(mn, a);
+  }
+  // parities of sum(ka) and of sum(fb) = sum(ka) - #{ea < 0} = SA + ST/2 - 4
+  const int32_t odd_a = (int32_t)SA & 1;
+  const int32_t odd_b = (int32_t)(SA + 0.5f * ST - 4.0f) & 1;
+  float D = 2.0f * Sabs - 8.0f;
+  if (odd_a) D += 4.0f - 4.0f * mx;
+  if (odd_b) D -= 4.0f * mn;
+  const bool tie = __builtin_fabsf(D) <= kE8Tie;
+  if (__ballot(tie) != 0ull) {
+    int32_t c[8];
+    quant_e8(z, c);
+    cb = c[0] & 1;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) h[i] = (c[i] - cb) >> 1;
+    return;
+  }
+  const bool even = D < 0.0f;
+  float c[8], e[8], m = 0.0f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    c[i] = even ? E[i] : E[i] + t[i];
+    e[i] = z[i] - c[i];  // ea exactly, or eb with the reference's single rounding
+    m = __builtin_fmaxf(m, __builtin_fabsf(e[i]));
+  }
+  // parity fix of the chosen class: its first coordinate of largest error
+  bool done = !(even ? odd_a : odd_b);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const bool hit = !done && __builtin_fabsf(e[i]) == m;
+    c[i] = hit ? c[i] + __builtin_copysignf(2.0f, e[i]) : c[i];
+    done = done || hit;
+  }
+  cb = even ? 0 : 1;
+  const float off = even ? 0.0f : -0.5f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) h[i] = (int32_t)__builtin_fmaf(c[i], 0.5f, off);
+}
+
+// E8 strip (Sec. 4.2) from h: s_i = zz(h_i) for i < 7, s_7 = 2 zz(t) + cb with
+// t = (h_7 - p) / 2 and p the parity of h_0 + .. + h_6.
+__device__ __forceinline__ void e8_strip(const int32_t* h, int32_t cb, uint32_t* s) {
+  int32_t p = 0;
+#pragma unroll
+  for (int i = 0; i < 7; ++i) {
+    p += h[i];
+    s[i] = zigzag(h[i]);
+  }
+  const int32_t t = (h[7] - (p & 1)) >> 1;
+  s[7] = 2u * zigzag(t) + (uint32_t)cb;
+}
+
 // ------------------------------------------------------------ encode kernel
 // One workgroup encodes HQ_ENC_SUBS_PER_WG consecutive sub-streams (four
-// waves, HQ_ENC_SUBS_PER_WAVE each, one at a time), keeps their bits in LDS,
-// publishes the group's word count, and only then looks back for its
-// absolute word offset and writes payload and offsets.  KV = false is the
+// waves, HQ_ENC_SUBS_PER_WAVE each, one at a time) and keeps their bits in
+// LDS; then its first wave alone publishes the group's word count, looks back
+// for the group's absolute word offset and writes payload and offsets.  KV = false is the
 // weight path (no rotation, no dither, fp32 norms) compiled without those
 // branches; KV = true reads the three options at run time.
 
-// The 16 (bf16) or 32 (fp32) input bytes of one lane, loaded ahead of use.
+// Number of k in 1..KMAX with sum >= thr[k] (thresholds clamped below 2^30
+// on the host, sums below 2^26), on scalar registers.
+__device__ __forceinline__ uint32_t kstar_count(uint32_t sum, const uint32_t* thr) {
+  uint32_t a = 0;
+#pragma unroll
+  for (int t = 1; t <= HQ_KMAX; ++t) a += (uint32_t)((int32_t)(thr[t] - 1u - sum)) >> 31;
+  return a;
+}
+
+// Position of one wave's sub-stream: wave-uniform row and first column.
+struct SubPos {
+  bool active;
+  uint32_t lrow, col0;
+};
+
+// The 16 (bf16) or 32 (fp32) input bytes of one lane and its RHT signs:
+// bf16 XOR words (bit 15 / bit 31 of each column pair) or fp32 sign bits.
 struct LaneInput {
-  uint4 a, b;
+  uint4 a, b, sw;
 };
 
 template <int XT>
-__device__ __forceinline__ LaneInput load_lane_input(const hq_encode_args& A, uint32_t sub, int lane) {
+__device__ __forceinline__ LaneInput load_lane_input(const hq_encode_args& A, const SubPos& P,
+                                                     int lane) {
   LaneInput in;
   in.a = make_uint4(0u, 0u, 0u, 0u);
   in.b = make_uint4(0u, 0u, 0u, 0u);
-  if (sub < (uint32_t)A.nsub) {
-    const uint32_t spr = (uint32_t)A.spr;
-    const uint32_t lrow = sub / spr;
-    const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
+  in.sw = make_uint4(0u, 0u, 0u, 0u);
+  if (P.active) {
+    const uint32_t col = P.col0 + 8u * (uint32_t)lane;
     if constexpr (XT == HQ_BF16) {
-      in.a = *(const uint4*)((const uint16_t*)A.x + (int64_t)lrow * A.ld + col);
+      in.a = *(const uint4*)((const uint16_t*)A.x + (int64_t)P.lrow * A.ld + col);
+      in.sw = *(const uint4*)(A.dsign16 + (col >> 1));
     } else {
-      const uint4* p = (const uint4*)((const float*)A.x + (int64_t)lrow * A.ld + col);
+      const uint4* p = (const uint4*)((const float*)A.x + (int64_t)P.lrow * A.ld + col);
       in.a = p[0];
       in.b = p[1];
+      in.sw.x = sign_bits8(A.dmask, col);
     }
   }
   return in;
 }
 
+// OR the low 32 + sh bits of v << sh into buf at bit pos (two words).
+__device__ __forceinline__ void or_word(uint32_t* buf, uint32_t pos, uint32_t v) {
+  const uint64_t t = (uint64_t)v << (pos & 31u);
+  atomicOr(&buf[pos >> 5], (uint32_t)t);
+  atomicOr(&buf[(pos >> 5) + 1], (uint32_t)(t >> 32));
+}
+
 template <int LAT, int XT, bool KV>
-__device__ __forceinline__ void encode_substream(const hq_encode_args& A, uint32_t sub, int lane,
-                                                 const XSigns& sg, const LaneInput& in,
-                                                 uint32_t dbits, uint32_t* buf, uint32_t& W_out,
-                                                 uint32_t& kb_out, uint32_t& bits_out,
-                                                 bool& overflow_out) {
-  const bool active = sub < (uint32_t)A.nsub;  // wave-uniform
-  const uint32_t spr = (uint32_t)A.spr;
-  const uint32_t lrow = active ? sub / spr : 0u;
-  const uint32_t col0 = (active ? sub - lrow * spr : 0u) * HQ_SUB;
-  const uint32_t col = col0 + 8u * (uint32_t)lane;  // tile lane/16, coordinates 8 (lane % 16) + j
-  const int64_t grow = A.first_row + lrow;
+__device__ __forceinline__ void encode_substream(const hq_encode_args& A, const SubPos& P,
+                                                 int lane, const TwSigns& sg, const LaneInput& in,
+                                                 uint32_t* buf, uint32_t& W_out, uint32_t& kb_out,
+                                                 uint32_t& bits_out, bool& overflow_out) {
+  const bool active = P.active;  // wave-uniform
+  const uint32_t col = P.col0 + 8u * (uint32_t)lane;  // tile lane/16, coordinates 8 (lane % 16) + j
+  const int64_t grow = A.first_row + P.lrow;
   const bool use_rot = KV && A.rotation;
   const bool use_dither = KV && A.dither;
   const bool fp16_norm = KV && A.norm_fp16;
 
-  // ---- the 8 scalars (loaded by the caller ahead of time)
+  // ---- the 8 scalars with the RHT signs D applied (|x| is unchanged)
   float x[8];
-  {
-    const uint32_t w4[4] = {in.a.x, in.a.y, in.a.z, in.a.w};
-    if constexpr (XT == HQ_BF16) {
+  if constexpr (XT == HQ_BF16) {
+    const uint32_t w4[4] = {in.a.x ^ in.sw.x, in.a.y ^ in.sw.y, in.a.z ^ in.sw.z,
+                            in.a.w ^ in.sw.w};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        x[2 * i] = bf16_to_f32(w4[i] & 0xFFFFu);
-        x[2 * i + 1] = bf16_to_f32(w4[i] >> 16);
-      }
-    } else {
-      const uint32_t w4b[4] = {in.b.x, in.b.y, in.b.z, in.b.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        x[i] = __uint_as_float(w4[i]);
-        x[4 + i] = __uint_as_float(w4b[i]);
-      }
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(w4[i] << 16);
+      x[2 * i + 1] = __uint_as_float(w4[i] & 0xFFFF0000u);
     }
+  } else {
+    const uint32_t w8[8] = {in.a.x, in.a.y, in.a.z, in.a.w, in.b.x, in.b.y, in.b.z, in.b.w};
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = flip(__uint_as_float(w8[i]), in.sw.x, i);
   }
 
   // ---- Normalize: tile norm as a pairwise tree in index order (the lane
@@ -615,10 +783,10 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, uint32
 #pragma unroll
   for (int i = 0; i < 8; ++i) sq[i] = x[i] * x[i];
   float ss = tree8(sq);
-  ss = ss + xor_lane_f<1>(ss);
-  ss = ss + xor_lane_f<2>(ss);
-  ss = ss + xor_lane_f<4>(ss);
-  ss = ss + xor_lane_f<8>(ss);
+  ss = ss + dpp_xor<1>(ss);
+  ss = ss + dpp_xor<2>(ss);
+  ss = ss + swz_xor4(ss);
+  ss = ss + dpp_xor<8>(ss);
   const float r = __builtin_sqrtf(ss);
   float rs = r;
   bool bad_tile = !(r <= 3.0e38f);  // non-finite input
@@ -640,19 +808,15 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, uint32
     }
   }
 
-  // ---- RHT: v = H D x
+  // ---- RHT: v = sigma H D x, then z = v * (sigma alpha / r)
+  fwht128_tw(x, sg);
+  const float scale_tw = xor_sign(scale, sg.sigma);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) x[i] = flip(x[i], dbits, i);
-  fwht128(x, sg);
-
-  // ---- scale, rotate, dither
+  for (int i = 0; i < 8; ++i) x[i] = x[i] * scale_tw;
   if (use_rot) {
     const uint32_t sbits = sign_bits8(A.smask, (lane & 15) * 8);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = flip(x[i] * scale, sbits, i);
-  } else {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = x[i] * scale;
+    for (int i = 0; i < 8; ++i) x[i] = flip(x[i], sbits, i);
   }
   if (use_dither) {
     float u[8];
@@ -662,81 +826,117 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, uint32
   }
 
   // ---- quantize + strip
-  int32_t c[8];
-  quantize8<LAT>(x, c);
-  bool huge = false;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) huge = huge || (c[i] > 65536 || c[i] < -65536);
-  if (huge || !active) {
-#pragma unroll
-    for (int i = 0; i < 8; ++i) c[i] = 0;
-  }
   uint32_t sym[8];
-  strip8<LAT>(c, sym);
-
-  // ---- Rice parameters (wave-uniform)
-  uint32_t k0, k1;
-  if (A.rice_k >= 0) {
-    k0 = (uint32_t)A.rice_k;
-    k1 = (LAT == kD4) ? (k0 > 0 ? k0 - 1 : 0) : k0;
+  bool huge = false;
+  if constexpr (LAT == kE8) {
+    int32_t h[8], cb;
+    e8_nearest(x, h, cb);
+    int32_t hmax = h[0], hmin = h[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) {
+      hmax = max(hmax, h[i]);
+      hmin = min(hmin, h[i]);
+    }
+    huge = hmax > 32768 - cb || hmin < -32768;  // some |c| = |2 h + cb| > 65536
+    if (huge || !active) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) h[i] = 0;
+      cb = 0;
+    }
+    e8_strip(h, cb, sym);
   } else {
-    uint32_t s0 = 0, s1 = 0;
+    int32_t c[8];
+    quantize8<LAT>(x, c);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) huge = huge || (c[i] > 65536 || c[i] < -65536);
+    if (huge || !active) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) c[i] = 0;
+    }
+    strip8<LAT>(c, sym);
+  }
+
+  // ---- Rice parameters (wave-uniform) and quotients
+  uint32_t k0, k1, qv[8], ulen;
+  if constexpr (LAT == kE8 || LAT == kZ) {
+    uint32_t s0 = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s0 += sym[j];
+    if (A.rice_k >= 0) {
+      k0 = (uint32_t)A.rice_k;
+    } else {
+      const uint32_t a0 = kstar_count(wave_total(s0), A.thr0);
+      // the better of k* and k* + 1: k* + 1 saves sum((m >> k) - (m >> (k+1)))
+      // unary bits and costs one remainder bit per symbol
+      uint32_t ga = 0, gb = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t qa = sym[j] >> a0;
+        ga += qa;
+        gb += qa >> 1;
+      }
+      const uint32_t gain = wave_total(ga - gb);
+      k0 = (a0 < HQ_KMAX && gain > (uint32_t)HQ_SUB) ? a0 + 1 : a0;
+    }
+    k1 = k0;
+    ulen = 8;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      if (sym_class<LAT>(j)) s1 += sym[j]; else s0 += sym[j];
+      qv[j] = sym[j] >> k0;
+      ulen += qv[j];
     }
-    const uint32_t sum0 = wave_total(s0);
-    const uint32_t sum1 = (LAT == kA2) ? wave_total(s1) : 0u;
-    uint32_t a0 = 0, a1 = 0;
+  } else {
+    if (A.rice_k >= 0) {
+      k0 = (uint32_t)A.rice_k;
+      k1 = (LAT == kD4) ? (k0 > 0 ? k0 - 1 : 0) : k0;
+    } else {
+      uint32_t s0 = 0, s1 = 0;
 #pragma unroll
-    for (int t = 1; t <= HQ_KMAX; ++t) {
-      a0 += sum0 >= A.thr0[t];
-      if (LAT == kA2) a1 += sum1 >= A.thr1[t];
-    }
-    // the better of k* and k* + 1: k* + 1 saves sum((m >> k) - (m >> (k+1)))
-    // unary bits and costs one remainder bit per symbol of the class
-    const uint32_t b0 = a0 < HQ_KMAX ? a0 + 1 : a0;
-    const uint32_t b1 = a1 < HQ_KMAX ? a1 + 1 : a1;
-    uint32_t g0 = 0, g1 = 0;
+      for (int j = 0; j < 8; ++j) {
+        if (sym_class<LAT>(j)) s1 += sym[j]; else s0 += sym[j];
+      }
+      const uint32_t a0 = kstar_count(wave_total(s0), A.thr0);
+      const uint32_t a1 = (LAT == kA2) ? kstar_count(wave_total(s1), A.thr1) : 0u;
+      const uint32_t b0 = a0 < HQ_KMAX ? a0 + 1 : a0;
+      const uint32_t b1 = a1 < HQ_KMAX ? a1 + 1 : a1;
+      uint32_t g0 = 0, g1 = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < 8; ++j) {
+        if (LAT == kD4) {
+          const uint32_t ka = sym_class<LAT>(j) ? (a0 > 0 ? a0 - 1 : 0) : a0;
+          const uint32_t kb = sym_class<LAT>(j) ? (b0 > 0 ? b0 - 1 : 0) : b0;
+          g0 += (sym[j] >> ka) - (sym[j] >> kb);
+        } else if (sym_class<LAT>(j)) {
+          g1 += (sym[j] >> a1) - (sym[j] >> b1);
+        } else {
+          g0 += (sym[j] >> a0) - (sym[j] >> b0);
+        }
+      }
+      const uint32_t gain0 = wave_total(g0);
+      uint32_t cost0;
       if (LAT == kD4) {
-        const uint32_t ka = sym_class<LAT>(j) ? (a0 > 0 ? a0 - 1 : 0) : a0;
-        const uint32_t kb = sym_class<LAT>(j) ? (b0 > 0 ? b0 - 1 : 0) : b0;
-        g0 += (sym[j] >> ka) - (sym[j] >> kb);
-      } else if (LAT == kA2 && sym_class<LAT>(j)) {
-        g1 += (sym[j] >> a1) - (sym[j] >> b1);
+        cost0 = (b0 - a0) * (3u * HQ_SUB / 4u) +
+                ((b0 > 0 ? b0 - 1 : 0) - (a0 > 0 ? a0 - 1 : 0)) * (HQ_SUB / 4u);
       } else {
-        g0 += (sym[j] >> a0) - (sym[j] >> b0);
+        cost0 = (b0 - a0) * (HQ_SUB / 2u);
+      }
+      k0 = gain0 > cost0 ? b0 : a0;
+      if (LAT == kA2) {
+        const uint32_t gain1 = wave_total(g1);
+        k1 = gain1 > (b1 - a1) * (HQ_SUB / 2u) ? b1 : a1;
+      } else {
+        k1 = k0 > 0 ? k0 - 1 : 0;
       }
     }
-    const uint32_t gain0 = wave_total(g0);
-    uint32_t cost0;
-    if (LAT == kD4) {
-      cost0 = (b0 - a0) * (3u * HQ_SUB / 4u) + ((b0 > 0 ? b0 - 1 : 0) - (a0 > 0 ? a0 - 1 : 0)) * (HQ_SUB / 4u);
-    } else if (LAT == kA2) {
-      cost0 = (b0 - a0) * (HQ_SUB / 2u);
-    } else {
-      cost0 = (b0 - a0) * HQ_SUB;
-    }
-    k0 = gain0 > cost0 ? b0 : a0;
-    if (LAT == kA2) {
-      const uint32_t gain1 = wave_total(g1);
-      k1 = gain1 > (b1 - a1) * (HQ_SUB / 2u) ? b1 : a1;
-    } else {
-      k1 = (LAT == kD4) ? (k0 > 0 ? k0 - 1 : 0) : k0;
+    ulen = 8;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      qv[j] = sym[j] >> (sym_class<LAT>(j) ? k1 : k0);
+      ulen += qv[j];
     }
   }
 
   // ---- code lengths: remainder region then unary region
-  uint32_t qv[8], rv[8], ulen = 0;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-    qv[j] = sym[j] >> kk;
-    rv[j] = sym[j] & ((1u << kk) - 1u);
-    ulen += qv[j] + 1;
-  }
   const uint32_t lrem = lane_rem_bits<LAT>(k0, k1);
   const uint32_t R = 64 * lrem;
   const uint32_t uincl = wave_scan_incl(ulen);
@@ -750,7 +950,8 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, uint32
   if (!active) W = 0;
   if (overflow) W = HQ_SUB / 32;
 
-  // ---- assemble in this sub-stream's LDS buffer
+  // ---- assemble in this sub-stream's LDS buffer (two spare words past W
+  //      take the zero high halves of the ORs)
   for (uint32_t w = lane; w < W; w += 64) buf[w] = overflow ? 0xFFFFFFFFu : 0u;
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
@@ -760,20 +961,38 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, uint32
     if (lrem <= 32) {
       uint32_t acc = 0;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc |= rv[j] << rem_offset<LAT>(j, k0, k1);
-      or_bits64(buf, rpos, acc);
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+        acc |= (sym[j] & ((1u << kk) - 1u)) << rem_offset<LAT>(j, k0, k1);
+      }
+      or_word(buf, rpos, acc);
     } else if (lrem <= 64) {
       uint64_t acc = 0;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc |= (uint64_t)rv[j] << rem_offset<LAT>(j, k0, k1);
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+        acc |= (uint64_t)(sym[j] & ((1u << kk) - 1u)) << rem_offset<LAT>(j, k0, k1);
+      }
       or_bits64(buf, rpos, acc);
     } else {
 #pragma unroll
-      for (int j = 0; j < 8; ++j) or_bits64(buf, rpos + rem_offset<LAT>(j, k0, k1), rv[j]);
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+        or_bits64(buf, rpos + rem_offset<LAT>(j, k0, k1), sym[j] & ((1u << kk) - 1u));
+      }
     }
     // unary codes: q zeros and a one each
     uint32_t upos = R + uoff;
-    if (ulen <= 64) {
+    if (ulen <= 32) {
+      uint32_t m = 0, t = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        t += qv[j];
+        m |= 1u << t;
+        t += 1;
+      }
+      or_word(buf, upos, m);
+    } else if (ulen <= 64) {
       uint64_t m = 0;
       uint32_t t = 0;
 #pragma unroll
@@ -801,44 +1020,52 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, uint32
 template <int LAT, int XT, bool KV>
 __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   extern __shared__ uint32_t smem[];
-  __shared__ uint32_t s_epoch, s_stop;
+  __shared__ uint32_t s_epoch;
   __shared__ uint32_t s_words[HQ_ENC_SUBS_PER_WG];
   __shared__ uint32_t s_part[HQ_WAVES_PER_WG], s_part2[HQ_WAVES_PER_WG];
-  __shared__ unsigned long long s_base;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = (int)readfirst((uint32_t)(tid >> 6));
   const uint32_t wg = blockIdx.x;
+  const uint32_t stride = A.lds_words + 2;  // words per sub-stream buffer
   if (tid == 0)
     s_epoch = (uint32_t)__hip_atomic_load(A.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
               kEpochMask;
-  const XSigns sg(lane);
+  const TwSigns sg(lane);
 
-  // ---- issue every input load of this wave up front, so that only the first
-  //      one's latency is exposed
-  LaneInput in[HQ_ENC_SUBS_PER_WAVE];
-  uint32_t dbits[HQ_ENC_SUBS_PER_WAVE];
-#pragma unroll
-  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
-    const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)(i * HQ_WAVES_PER_WG + wave);
-    in[i] = load_lane_input<XT>(A, sub, lane);
+  // ---- this wave's sub-streams: wg * 16 + i * 4 + wave, i = 0 .. 3 (row and
+  //      column advanced on scalar registers)
+  SubPos pos[HQ_ENC_SUBS_PER_WAVE];
+  {
     const uint32_t spr = (uint32_t)A.spr;
-    const uint32_t lrow = sub < (uint32_t)A.nsub ? sub / spr : 0u;
-    const uint32_t col = (sub < (uint32_t)A.nsub ? sub - lrow * spr : 0u) * HQ_SUB + 8u * (uint32_t)lane;
-    dbits[i] = sign_bits8(A.dmask, col);
+    const uint32_t sub0 = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)wave;
+    uint32_t row = sub0 / spr, c = sub0 - row * spr;
+#pragma unroll
+    for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
+      pos[i].active = sub0 + (uint32_t)(i * HQ_WAVES_PER_WG) < (uint32_t)A.nsub;
+      pos[i].lrow = pos[i].active ? row : 0u;
+      pos[i].col0 = pos[i].active ? c * HQ_SUB : 0u;
+      c += HQ_WAVES_PER_WG;
+      while (c >= spr) {
+        c -= spr;
+        ++row;
+      }
+    }
   }
-
-  // ---- encode this group's sub-streams into LDS
+  // ---- encode this group's sub-streams into LDS; the next sub-stream's
+  //      input is loaded while the current one is encoded
+  LaneInput in = load_lane_input<XT>(A, pos[0], lane);
   uint32_t bitsum = 0, padsum = 0;
 #pragma unroll
   for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
     const int li = i * HQ_WAVES_PER_WG + wave;  // neighbouring waves take neighbouring sub-streams
     const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
+    LaneInput next;
+    if (i + 1 < HQ_ENC_SUBS_PER_WAVE) next = load_lane_input<XT>(A, pos[i + 1], lane);
     uint32_t W, kb, bits;
     bool ovf;
-    encode_substream<LAT, XT, KV>(A, sub, lane, sg, in[i], dbits[i], smem + li * A.lds_words, W, kb,
-                                  bits, ovf);
-    if (sub < (uint32_t)A.nsub) {
+    encode_substream<LAT, XT, KV>(A, pos[i], lane, sg, in, smem + li * stride, W, kb, bits, ovf);
+    if (pos[i].active) {
       if (lane == 0) {
         A.kparam[A.first_sub + sub] = (uint8_t)kb;
         s_words[li] = W;
@@ -849,21 +1076,24 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
     } else if (lane == 0) {
       s_words[li] = 0;
     }
+    if (i + 1 < HQ_ENC_SUBS_PER_WAVE) in = next;
   }
   if (lane == 0) {
     s_part[wave] = bitsum;
     s_part2[wave] = padsum;
   }
   __syncthreads();
-  const uint32_t epoch = readfirst(s_epoch);
+  // Waves 1..3 are done: their slots go to the next workgroups while wave 0
+  // alone waits for the group's offset and writes every sub-stream out.
+  // (No workgroup barrier follows.)
+  if (wave != 0) return;
 
+  const uint32_t epoch = readfirst(s_epoch);
   // ---- publish this group's word count at once, so successors can pass it;
   //      the group's bit counts go to its stats word first (at most 2^22
   //      payload bits and 16 * 31 pad bits, packed as bits << 9 | pad)
-  uint32_t agg = 0;
-#pragma unroll
-  for (int li = 0; li < HQ_ENC_SUBS_PER_WG; ++li) agg += s_words[li];
-  if (tid == 0) {
+  const uint32_t agg = wave_total(lane < HQ_ENC_SUBS_PER_WG ? s_words[lane] : 0u);
+  if (lane == 0) {
     if (A.stats) {
       const uint32_t gb = s_part[0] + s_part[1] + s_part[2] + s_part[3];
       const uint32_t gp = s_part2[0] + s_part2[1] + s_part2[2] + s_part2[3];
@@ -872,21 +1102,30 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
     if (wg > 0) store_status(&A.status[wg], pack_status(epoch, 1u, agg));
   }
 
-  // ---- look-back: 256 predecessors per round trip, the whole group
+  // ---- look-back: 256 predecessors per round trip, four per lane (distance
+  //      r * 64 + lane + 1 below this group), until the nearest published
+  //      inclusive prefix
   uint32_t prefix = 0;
   bool timed_out = false;
   int64_t hi = (int64_t)wg - 1;
   while (hi >= 0) {
-    const int64_t idx = hi - tid;
-    unsigned long long st = 0;
-    bool ready = idx < 0;
+    unsigned long long st[4];
+    bool ready[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      st[r] = 0ull;
+      ready[r] = hi - (r * 64 + lane) < 0;
+    }
     uint32_t spins = 0;
     for (;;) {
-      if (!ready) {
-        st = load_status(&A.status[idx]);
-        ready = (uint32_t)(st >> 34) == epoch && ((st >> 32) & 3u) != 0u;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (!ready[r]) {
+          st[r] = load_status(&A.status[hi - (r * 64 + lane)]);
+          ready[r] = (uint32_t)(st[r] >> 34) == epoch && ((st[r] >> 32) & 3u) != 0u;
+        }
       }
-      if (__syncthreads_and(ready)) break;
+      if (__ballot(!(ready[0] && ready[1] && ready[2] && ready[3])) == 0ull) break;
       if (++spins > kSpinLimit) {
         timed_out = true;
         break;
@@ -894,44 +1133,40 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
       __builtin_amdgcn_s_sleep(1);
     }
     if (timed_out) break;
-    const bool incl = idx >= 0 && ((st >> 32) & 3u) == 2u;
-    if (tid == 0) s_stop = 256u;
-    __syncthreads();
-    if (incl) atomicMin(&s_stop, (uint32_t)tid);
-    __syncthreads();
-    const uint32_t stop = s_stop;
-    const uint32_t v = wave_total((idx >= 0 && (uint32_t)tid <= stop) ? (uint32_t)st : 0u);
-    if (lane == 0) s_part[wave] = v;
-    __syncthreads();
-    prefix += s_part[0] + s_part[1] + s_part[2] + s_part[3];
-    __syncthreads();
+    // nearest inclusive prefix: the first r with one, then its lowest lane
+    uint32_t stop = 256u;
+#pragma unroll
+    for (int r = 3; r >= 0; --r) {
+      const bool incl = hi - (r * 64 + lane) >= 0 && ((st[r] >> 32) & 3u) == 2u;
+      const unsigned long long m = __ballot(incl);
+      if (m) stop = (uint32_t)(r * 64) + (uint32_t)__builtin_ctzll(m);
+    }
+    uint32_t v = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (hi - (r * 64 + lane) >= 0 && (uint32_t)(r * 64 + lane) <= stop) v += (uint32_t)st[r];
+    prefix += wave_total(v);
     if (stop < 256u) break;
     hi -= 256;
   }
-  if (tid == 0) {
+  const unsigned long long base =
+      (A.append ? (unsigned long long)readfirst(A.offsets[A.first_sub]) : 0ull) + prefix;
+  if (lane == 0) {
     store_status(&A.status[wg], pack_status(epoch, 2u, prefix + agg));
     // the last group: every group has read this launch's epoch; advance it
     if (wg == A.nwg - 1)
       __hip_atomic_store(A.epoch, (unsigned long long)((epoch + 1u) & kEpochMask), __ATOMIC_RELAXED,
                          __HIP_MEMORY_SCOPE_AGENT);
     if (timed_out && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
-    const unsigned long long base = A.append ? (unsigned long long)A.offsets[A.first_sub] : 0ull;
-    s_base = base + prefix;
   }
-  __syncthreads();
 
-  // ---- write payload and offsets
-  const unsigned long long base = s_base;
-  uint32_t before = 0;
-  int li_next = 0;
-  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
-    const int li = i * HQ_WAVES_PER_WG + wave;
+  // ---- write payload and offsets of all of the group's sub-streams
+  unsigned long long start = base;
+  for (int li = 0; li < HQ_ENC_SUBS_PER_WG; ++li) {
     const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
     if (sub >= (uint32_t)A.nsub) break;
-    for (; li_next < li; ++li_next) before += s_words[li_next];
-    const uint32_t W = s_words[li];
-    const unsigned long long start = base + before;
-    const uint32_t* buf = smem + li * A.lds_words;
+    const uint32_t W = readfirst(s_words[li]);
+    const uint32_t* buf = smem + li * stride;
     const bool fits = start + W <= (unsigned long long)A.cap_words;
     if (fits) {
       for (uint32_t w = lane; w < W; w += 64) A.payload[start + w] = buf[w];
@@ -941,21 +1176,25 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
       A.offsets[A.first_sub + sub + 1] = (uint32_t)(start + W);
       if (!fits && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CAPACITY);
     }
+    start += W;
   }
   // ---- bit counts: the last group of every 256 adds up their stats words
   //      (all of them were stored before their owners' aggregates, which this
   //      group's look-back has passed), so the stats block takes one atomic
   //      per 256 groups instead of one per group
   if (A.stats && ((wg & 255u) == 255u || wg == A.nwg - 1)) {
-    const uint32_t idx = (wg & ~255u) + (uint32_t)tid;
-    uint32_t v = 0;
+    uint32_t gb = 0, gp = 0;
     bool late = false;
-    if (idx <= wg) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint32_t idx = (wg & ~255u) + (uint32_t)(r * 64 + lane);
+      if (idx > wg) continue;
       uint32_t spins = 0;
       for (;;) {
         const unsigned long long st = load_status(&A.wgstat[idx]);
         if ((uint32_t)(st >> 34) == epoch && ((st >> 32) & 3u) != 0u) {
-          v = (uint32_t)st;
+          gb += (uint32_t)st >> 9;
+          gp += (uint32_t)st & 511u;
           break;
         }
         if (++spins > kSpinLimit) {
@@ -965,19 +1204,11 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
         __builtin_amdgcn_s_sleep(1);
       }
     }
-    const uint32_t gb = wave_total(v >> 9), gp = wave_total(v & 511u);
-    __syncthreads();
-    if (lane == 0) {
-      s_part[wave] = gb;
-      s_part2[wave] = gp;
-    }
-    __syncthreads();
+    const uint32_t tb = wave_total(gb), tp = wave_total(gp);
     if (late) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
-    if (tid == 0) {
-      atomicAdd(&A.stats->payload_bits,
-                (unsigned long long)s_part[0] + s_part[1] + s_part[2] + s_part[3]);
-      atomicAdd(&A.stats->pad_bits,
-                (unsigned long long)s_part2[0] + s_part2[1] + s_part2[2] + s_part2[3]);
+    if (lane == 0) {
+      atomicAdd(&A.stats->payload_bits, (unsigned long long)tb);
+      atomicAdd(&A.stats->pad_bits, (unsigned long long)tp);
     }
   }
 }
@@ -1337,7 +1568,7 @@ __global__ void hq_zero_kernel(uint32_t* p, size_t n) {
 
 template <int LAT>
 int launch_encode_lat(const hq_encode_args& a, int xt, bool kv, hipStream_t st) {
-  const size_t lds = (size_t)a.lds_words * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
+  const size_t lds = (size_t)(a.lds_words + 2) * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
   if (xt == HQ_BF16) {
     if (kv)
       hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_BF16, true>), dim3(a.nwg), dim3(256), lds, st, a);
