@@ -436,6 +436,7 @@ static void fill_decode_args(const hq_plan_s* p, const hq_stream* s, int64_t row
   a->spr = p->spr;
   a->tpr = p->tpr;
   a->dmask = p->d_dmask;
+  a->dsign16 = p->d_dsign16;
   a->smask = p->d_smask;
   a->stats = s->stats;
   a->rotation = p->rotation;

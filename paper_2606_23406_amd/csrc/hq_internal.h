@@ -80,6 +80,7 @@ struct hq_decode_args {
   int64_t ld;
   float* g;                // decode_int8: per-tile factors (rows x tpr)
   const uint32_t* dmask;
+  const uint32_t* dsign16;  // RHT signs as bf16 XOR words, one per column pair
   const uint32_t* smask;
   hq_stats* stats;
   int32_t rotation, dither, norm_fp16;

@@ -1216,10 +1216,26 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
 // ------------------------------------------------------------ decode kernel
 // Rice decode of one sub-stream per wave: the remainder fields are at fixed
 // positions; the unary terminators are located by per-word popcounts, a
-// wave prefix sum and a select inside the word that holds terminator 8 l - 1,
-// after which lane l walks its own 8 codes through a 64-bit register window.
+// wave prefix sum and a select inside the word that holds terminator 8 l - 1.
+// Lane l then reads its 8 codes from a 32-bit window at that position (the
+// common case: its codes span at most 32 bits), clearing one terminator per
+// code; a lane whose codes run past the window walks a 64-bit window that
+// slides along the bit array.  Each wave only touches its own LDS region.
 // MODE 0: fp32 out, 1: bf16 out, 2: int8 lattice codes and per-tile g (no
 // inverse RHT).
+
+__device__ __forceinline__ void wave_sync_lds() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Bits [pos, pos + 32) of the LDS bit array (the word after the last one
+// read must exist).
+__device__ __forceinline__ uint32_t bits32_at(const uint32_t* buf, uint32_t pos) {
+  const uint32_t w = pos >> 5;
+  return __builtin_amdgcn_alignbit(buf[w + 1], buf[w], pos & 31u);
+}
 
 template <int LAT>
 __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, uint32_t gsub, bool active,
@@ -1240,8 +1256,9 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, uint32_t
             k0 <= HQ_KMAX && R <= 32u * W;
   const uint32_t Wl = ok ? W : 0u;
   for (uint32_t w = lane; w < Wl; w += 64) buf[w] = A.payload[(uint64_t)start + w];
+  if (lane < 2) buf[Wl + lane] = 0u;  // two zero words past the end
   starts[lane] = (lane == 0) ? R : 0xFFFFFFFFu;
-  __syncthreads();
+  wave_sync_lds();
 
   // unary terminators: popcount prefix, then the start of each lane's codes
   const uint32_t uw0 = R >> 5;
@@ -1259,51 +1276,77 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, uint32_t
     }
     carry += __builtin_amdgcn_readlane(incl, 63);
   }
-  __syncthreads();
+  wave_sync_lds();
 
-  // lane's 8 quotients through a 64-bit window
+  // lane's 8 quotients
   uint32_t pos = starts[lane];
   const uint32_t nbits = 32u * Wl;
   ok = ok && pos < nbits;
   uint32_t qv[8];
-  uint64_t win = ok ? load_bits64(buf, pos, Wl) : 0ull;
-  uint32_t valid = 64;
+  bool fast = false;
+  if (ok) {
+    uint32_t win = bits32_at(buf, pos);
+    fast = __popc(win) >= 8;
+    int32_t prev = -1;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    uint32_t q = 0;
-    while (ok && win == 0ull) {  // the code runs past the window: slide it
-      q += valid;
-      pos += valid;
-      if (pos >= nbits) {
-        ok = false;
-        break;
-      }
-      win = load_bits64(buf, pos, Wl);
-      valid = 64;
+    for (int j = 0; j < 8; ++j) {
+      const int32_t p = (int32_t)__builtin_ctz(win | 0x80000000u);
+      qv[j] = (uint32_t)(p - prev - 1);
+      prev = p;
+      win &= win - 1u;
     }
-    const uint32_t lo = (uint32_t)win, hi = (uint32_t)(win >> 32);
-    const uint32_t tz = lo ? (uint32_t)__builtin_ctz(lo) : 32u + (uint32_t)__builtin_ctz(hi | (hi == 0u));
-    q += tz;
-    pos += tz + 1;
-    valid -= tz + 1;
-    win = (tz >= 63u) ? 0ull : (win >> (tz + 1));
-    qv[j] = q;
   }
-  // lane's 8 remainders
-  const uint32_t rpos = (uint32_t)lane * lrem;
-  const uint64_t rw = (ok && lrem) ? load_bits64(buf, rpos, Wl) : 0ull;
+  if (ok && !fast) {
+    // the codes run past 32 bits: a 64-bit window sliding along the array
+    uint64_t win = load_bits64(buf, pos, Wl);
+    uint32_t valid = 64;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-    const uint32_t off = rem_offset<LAT>(j, k0, k1);
-    uint32_t r;
-    if (lrem <= 64) {
-      r = (uint32_t)(rw >> off);
-    } else {
-      r = ok ? (uint32_t)load_bits64(buf, rpos + off, Wl) : 0u;
+    for (int j = 0; j < 8; ++j) {
+      uint32_t q = 0;
+      while (ok && win == 0ull) {
+        q += valid;
+        pos += valid;
+        if (pos >= nbits) {
+          ok = false;
+          break;
+        }
+        win = load_bits64(buf, pos, Wl);
+        valid = 64;
+      }
+      const uint32_t lo = (uint32_t)win, hi = (uint32_t)(win >> 32);
+      const uint32_t tz =
+          lo ? (uint32_t)__builtin_ctz(lo) : 32u + (uint32_t)__builtin_ctz(hi | (hi == 0u));
+      q += tz;
+      pos += tz + 1;
+      valid -= tz + 1;
+      win = (tz >= 63u) ? 0ull : (win >> (tz + 1));
+      qv[j] = q;
     }
-    r &= (1u << kk) - 1u;
-    sym[j] = (qv[j] << kk) | r;
+  }
+  // lane's 8 remainders (fields at fixed positions)
+  const uint32_t rpos = (uint32_t)lane * lrem;
+  if (lrem <= 32) {
+    const uint32_t acc = (ok && lrem) ? bits32_at(buf, rpos) : 0u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+      sym[j] = (qv[j] << kk) | __builtin_amdgcn_ubfe(acc, rem_offset<LAT>(j, k0, k1), kk);
+    }
+  } else if (lrem <= 64) {
+    const uint64_t acc = ok ? ((uint64_t)bits32_at(buf, rpos + 32) << 32) | bits32_at(buf, rpos) : 0ull;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+      const uint32_t r = (uint32_t)(acc >> rem_offset<LAT>(j, k0, k1)) & ((1u << kk) - 1u);
+      sym[j] = (qv[j] << kk) | r;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+      const uint32_t r = ok ? (uint32_t)load_bits64(buf, rpos + rem_offset<LAT>(j, k0, k1), Wl) : 0u;
+      sym[j] = (qv[j] << kk) | (r & ((1u << kk) - 1u));
+    }
   }
   if (!ok) {
 #pragma unroll
@@ -1320,11 +1363,22 @@ __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
   const uint32_t sub = blockIdx.x * HQ_WAVES_PER_WG + wave;
   const bool active = sub < (uint32_t)A.nsub;
   const uint32_t gsub = (uint32_t)A.first_sub + sub;
-  uint32_t* buf = smem + wave * (A.lds_words + 64);
-  uint32_t* starts = buf + A.lds_words;
+  uint32_t* buf = smem + wave * (A.lds_words + 66);
+  uint32_t* starts = buf + A.lds_words + 2;
   const bool use_rot = KV && A.rotation;
   const bool use_dither = KV && A.dither;
   const bool fp16_norm = KV && A.norm_fp16;
+
+  const uint32_t spr = (uint32_t)A.spr;
+  const uint32_t lrow = active ? sub / spr : 0u;
+  const uint32_t col = (active ? sub - lrow * spr : 0u) * HQ_SUB + 8u * (uint32_t)lane;
+  const int64_t grow = A.first_row + lrow;
+  const int64_t tix = grow * A.tpr + (col >> 7);
+  // per-tile norm and output signs, loaded before the bit walk
+  float rs = 0.0f;
+  if (active) rs = fp16_norm ? (float)((const _Float16*)A.norms)[tix] : ((const float*)A.norms)[tix];
+  uint4 sw = make_uint4(0u, 0u, 0u, 0u);
+  if (MODE == 1 && active) sw = *(const uint4*)(A.dsign16 + (col >> 1));
 
   uint32_t sym[8];
   const bool ok = decode_symbols<LAT>(A, gsub, active, lane, buf, starts, sym);
@@ -1338,14 +1392,6 @@ __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
   }
   int32_t c[8];
   unstrip8<LAT>(sym, c);
-
-  const uint32_t spr = (uint32_t)A.spr;
-  const uint32_t lrow = active ? sub / spr : 0u;
-  const uint32_t col = (active ? sub - lrow * spr : 0u) * HQ_SUB + 8u * (uint32_t)lane;
-  const int64_t grow = A.first_row + lrow;
-  const int64_t tix = grow * A.tpr + (col >> 7);
-  float rs = 0.0f;
-  if (active) rs = fp16_norm ? (float)((const _Float16*)A.norms)[tix] : ((const float*)A.norms)[tix];
   const float g = rs / A.alpha_n;
 
   if constexpr (MODE == 2) {
@@ -1365,35 +1411,33 @@ __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
     if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
     return;
   } else {
-    const XSigns sg(lane);
-    float y[8];
-    const uint32_t dbits = sign_bits8(A.dmask, col);
+    // y = D H^T (S) (code - U) * r / (alpha n); the integer codes make the
+    // transform exact in fp32 (|sum| <= 128 * 65536 < 2^24) whenever there
+    // is no dither
+    const TwSigns sg(lane);
     const uint32_t sbits = use_rot ? sign_bits8(A.smask, (lane & 15) * 8) : 0u;
-    if (!use_dither && LAT != kA2) {
-      // integer codes: the Walsh-Hadamard transform is exact in int32
-      int32_t v[8];
+    float y[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) v[j] = ((sbits >> j) & 1u) ? -c[j] : c[j];
-      fwht128_i(v, sg);
+    for (int j = 0; j < 8; ++j) y[j] = code_coord<LAT>(c[j], j);
+    if (use_dither) {
+      float u[8];
+      dither8<LAT>(A.dither_seed, grow, col, u);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = flip((float)v[j], dbits, j) * g;
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = code_coord<LAT>(c[j], j);
-      if (use_dither) {
-        float u[8];
-        dither8<LAT>(A.dither_seed, grow, col, u);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) y[j] = y[j] - u[j];
-      }
+      for (int j = 0; j < 8; ++j) y[j] = y[j] - u[j];
+    }
+    if (use_rot) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) y[j] = flip(y[j], sbits, j);
-      fwht128(y, sg);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = flip(y[j], dbits, j) * g;
     }
+    fwht128_tw(y, sg);
+    const float g_tw = xor_sign(g, sg.sigma);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) y[j] = y[j] * g_tw;
     if (!active) return;
     if constexpr (MODE == 0) {
+      const uint32_t dbits = sign_bits8(A.dmask, col);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[j] = flip(y[j], dbits, j);
       float4* out = (float4*)((float*)A.y + (int64_t)lrow * A.ld + col);
       out[0] = make_float4(y[0], y[1], y[2], y[3]);
       out[1] = make_float4(y[4], y[5], y[6], y[7]);
@@ -1401,7 +1445,12 @@ __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
       __bf16 b[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) b[j] = (__bf16)y[j];
-      *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = *(const uint4*)b;
+      uint4 o = *(const uint4*)b;
+      o.x ^= sw.x;
+      o.y ^= sw.y;
+      o.z ^= sw.z;
+      o.w ^= sw.w;
+      *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = o;
     }
   }
 }
@@ -1594,7 +1643,7 @@ void launch_decode_mode(const hq_decode_args& a, bool kv, uint32_t nwg, size_t l
 template <int LAT>
 int launch_decode_lat(const hq_decode_args& a, int mode, bool kv, hipStream_t st) {
   const uint32_t nwg = (uint32_t)((a.nsub + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG);
-  const size_t lds = (size_t)(a.lds_words + 64) * HQ_WAVES_PER_WG * sizeof(uint32_t);
+  const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
   if (mode == 0)
     launch_decode_mode<LAT, 0>(a, kv, nwg, lds, st);
   else if (mode == 1)
