@@ -1260,26 +1260,49 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, uint32_t
   starts[lane] = (lane == 0) ? R : 0xFFFFFFFFu;
   wave_sync_lds();
 
-  // unary terminators: popcount prefix, then the start of each lane's codes
+  // unary terminators: popcount prefix over the unary words, then the start
+  // of each lane's codes (just past terminator 8 l - 1)
   const uint32_t uw0 = R >> 5;
   const uint32_t nuw = ok ? Wl - uw0 : 0u;
-  uint32_t carry = 0;
-  for (uint32_t base = 0; base < nuw; base += 64) {
-    const uint32_t wi = base + lane;
-    const uint32_t v = (wi < nuw) ? buf[uw0 + wi] : 0u;
-    const uint32_t cnt = __popc(v);
-    const uint32_t incl = wave_scan_incl(cnt);
-    const uint32_t P = carry + incl - cnt;
-    for (uint32_t t = (P & ~7u) + 7u; t < P + cnt; t += 8u) {
-      const uint32_t j = (t + 1u) >> 3;
-      if (j < 64u) starts[j] = (uw0 + wi) * 32u + select32(v, t - P) + 1u;
+  uint32_t pos;
+  if (nuw <= 64u) {
+    // one word per lane: lane l finds its word by binary search over the
+    // inclusive counts (kept in `starts`), then selects inside it
+    const uint32_t v = ((uint32_t)lane < nuw) ? buf[uw0 + lane] : 0u;
+    starts[lane] = wave_scan_incl(__popc(v));
+    wave_sync_lds();
+    const uint32_t target = 8u * (uint32_t)lane;  // terminators before this lane's codes
+    uint32_t w = 0;
+#pragma unroll
+    for (uint32_t step = 32; step >= 1; step >>= 1)
+      if (starts[w + step - 1] < target) w += step;
+    const uint32_t word = w < nuw ? buf[uw0 + w] : 0u;
+    const uint32_t incl = starts[w];
+    if (lane == 0) {
+      pos = R;
+    } else {
+      ok = ok && incl >= target && w < nuw;
+      pos = ok ? (uw0 + w) * 32u + select32(word, target - 1u - (incl - __popc(word))) + 1u : 0u;
     }
-    carry += __builtin_amdgcn_readlane(incl, 63);
+  } else {
+    uint32_t carry = 0;
+    for (uint32_t base = 0; base < nuw; base += 64) {
+      const uint32_t wi = base + lane;
+      const uint32_t v = (wi < nuw) ? buf[uw0 + wi] : 0u;
+      const uint32_t cnt = __popc(v);
+      const uint32_t incl = wave_scan_incl(cnt);
+      const uint32_t P = carry + incl - cnt;
+      for (uint32_t t = (P & ~7u) + 7u; t < P + cnt; t += 8u) {
+        const uint32_t j = (t + 1u) >> 3;
+        if (j < 64u) starts[j] = (uw0 + wi) * 32u + select32(v, t - P) + 1u;
+      }
+      carry += __builtin_amdgcn_readlane(incl, 63);
+    }
+    wave_sync_lds();
+    pos = starts[lane];
   }
-  wave_sync_lds();
 
   // lane's 8 quotients
-  uint32_t pos = starts[lane];
   const uint32_t nbits = 32u * Wl;
   ok = ok && pos < nbits;
   uint32_t qv[8];
