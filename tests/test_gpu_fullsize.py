@@ -1,0 +1,257 @@
+"""GPU parity at the full workload sizes, in the launch shapes the bench uses.
+
+The HIP path encodes and decodes each whole configuration; the oracle then
+recomputes a seeded sample of rows.  Sub-streams never cross a row and, apart
+from the KV dither (which takes the global row index), a row's words, k and
+norm depend only on that row, so a sampled row must match the oracle's
+encoding of that row alone, bit for bit.  Properties that hold at any size are
+checked over everything: the stream parses, the stats add up, and the
+reconstruction SNR sits at the operating point.  Same bar as the small-size
+parity tests.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from tests import parity as PT
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def hq():
+    from paper_2606_23406_amd import hq as H
+    H.lib()
+    assert torch.cuda.is_available()
+    return H
+
+
+def row_stream(gpu, r, spr):
+    """The sub-streams of row r of a GPU stream, as a one-row stream tuple."""
+    pay, off, kp, norms = gpu
+    o = off[r * spr:(r + 1) * spr + 1]
+    return pay[o[0]:o[-1]], o, kp[r * spr:(r + 1) * spr], norms[r:r + 1]
+
+
+def check_sampled_rows(hq, plan, s, P, x, rows_idx, label, dither=False):
+    """Bit-exact words, k and norms of the sampled rows, and their decode."""
+    spr = plan.info.subs_per_row
+    gpu = PT.gpu_stream_arrays(s, s.rows)
+    exempt = 0
+    for r in rows_idx:
+        xr = x[r:r + 1].float().numpy()
+        res = PT.compare_streams(P, xr, row_stream(gpu, int(r), spr), row0=int(r) if dither else 0)
+        exempt += res["exempt_blocks"]
+        y32 = hq.hq_decode(plan, s, row0=int(r), rows=1, out_dtype=torch.float32)
+        y16 = hq.hq_decode(plan, s, row0=int(r), rows=1, out_dtype=torch.bfloat16)
+        ref = O.backend(P, res["codes"], res["norms"], row0=int(r) if dither else 0)
+        skip = PT.tiles_with_code_diffs(res["codes"], res["gpu_codes"])
+        unit = PT.lattice_unit(P, res["norms"])
+        got = y32.cpu().numpy().astype(np.float64).reshape(-1, 128)
+        err = np.abs(got - ref.reshape(-1, 128)).max(axis=1)
+        assert np.all(err[~skip] <= 1e-5 * unit[~skip]), (label, r, err.max())
+        ref16 = torch.from_numpy(ref.astype(np.float32)).to(torch.bfloat16).float().numpy()
+        eq16 = (y16.cpu().float().numpy() == ref16).reshape(-1, 128)
+        assert eq16[~skip].all(), (label, r)
+    print(f"[fullsize] {label}: {len(rows_idx)} sampled rows bit-exact "
+          f"(exempt blocks {exempt})", flush=True)
+    assert exempt <= max(2, len(rows_idx) * spr // 100)
+
+
+def snr_db(x, y):
+    x = x.float()
+    e = (y.float() - x)
+    return 10.0 * torch.log10((x * x).sum() / (e * e).sum()).item()
+
+
+@pytest.mark.parametrize("bps", [4.0, 3.0])
+def test_c2_heavy_tailed_4096(hq, bps):
+    from paper_2606_23406_amd import workloads as W
+    print(f"[fullsize] C2 4096x4096 bf16 Student-t + outlier columns, E8@{bps}", flush=True)
+    x = W.heavy_tailed_weight()
+    snr = PT.op_snr("E8", bps)
+    P = PT.oracle_params(O.E8, snr, rht_seed=17)
+    plan = PT.gpu_plan(hq, P, snr, 4096)
+    s = hq.EncodedStream(plan, 4096)
+    xd = x.cuda()
+    hq.hq_encode(plan, xd, s)
+    y = hq.hq_decode(plan, s, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    st = s.read_stats()
+    assert st["status"] == 0 and st["corrupt_substreams"] == 0, st
+    rate = st["payload_bits"] / x.numel()
+    q = snr_db(xd, y)
+    print(f"[fullsize] C2 E8@{bps}: {rate:.4f} bits/scalar, SNR {q:.3f} dB "
+          f"(operating point {snr:.3f} dB)", flush=True)
+    assert abs(q - snr) < 0.5
+    assert abs(rate - bps) < 0.25
+    rng = np.random.default_rng(int(bps * 10))
+    rows = np.sort(rng.choice(4096, 24, replace=False))
+    check_sampled_rows(hq, plan, s, P, x, rows, f"C2 E8@{bps}")
+
+
+@pytest.mark.parametrize("idx,lat,bps", [(4, O.E8, 4.0), (6, O.E8, 4.0), (4, O.D4, 3.0),
+                                         (1, O.D4, 3.0)])
+def test_c3_llama_linears(hq, idx, lat, bps):
+    from paper_2606_23406_amd import workloads as W
+    name, out_f, in_f = W.LLAMA_LINEARS[idx]
+    layer = 31
+    lname = "E8" if lat == O.E8 else "D4"
+    print(f"[fullsize] C3 layer {layer} {name} {out_f}x{in_f} {lname}@{bps}", flush=True)
+    x = W.llama_linear(layer, idx)
+    snr = PT.op_snr(lname, bps)
+    P = PT.oracle_params(lat, snr, rht_seed=W.llama_linear_seed(layer, idx))
+    plan = PT.gpu_plan(hq, P, snr, in_f)
+    s = hq.EncodedStream(plan, out_f)
+    xd = x.cuda()
+    hq.hq_encode(plan, xd, s)
+    y = hq.hq_decode(plan, s, out_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    st = s.read_stats()
+    assert st["status"] == 0 and st["corrupt_substreams"] == 0, st
+    q = snr_db(xd, y)
+    rate = st["payload_bits"] / x.numel()
+    print(f"[fullsize] C3 {name} {lname}@{bps}: {rate:.4f} bits/scalar, SNR {q:.3f} dB", flush=True)
+    assert abs(q - snr) < 0.5 and abs(rate - bps) < 0.25
+    rng = np.random.default_rng(100 + idx + lat)
+    rows = np.sort(rng.choice(out_f, 16, replace=False))
+    check_sampled_rows(hq, plan, s, P, x, rows, f"C3 {name} {lname}@{bps}")
+
+
+@pytest.fixture(scope="module")
+def kv_keys():
+    from paper_2606_23406_amd import workloads as W
+    k = W.kv_cache(role="k")  # [16, 8192, 8, 128]
+    return k.reshape(16 * 8192, 8 * 128)
+
+
+@pytest.mark.parametrize("lat,bps", [(O.E8, 2.0), (O.A2, 1.7), (O.Z, 1.7)])
+def test_c4_kv_cache_keys(hq, kv_keys, lat, bps):
+    """Keys [16, 8192, 8, 128] quantized on append in 128-token blocks with the
+    bias correction (sign rotation + subtractive dither, fp16 norms); one
+    stream row = one token's 8 head vectors (8 tiles)."""
+    from paper_2606_23406_amd import workloads as W
+    lname = {O.E8: "E8", O.A2: "A2", O.Z: "Z"}[lat]
+    x = kv_keys
+    rows, cols = x.shape
+    print(f"[fullsize] C4 keys {rows}x{cols} {lname}@{bps}, 128-token appends", flush=True)
+    snr = PT.op_snr(lname, bps)
+    P = PT.oracle_params(lat, snr, rht_seed=71, rotation=1, rot_seed=72, dither=True,
+                         dither_seed=73 + lat, norm_fp16=True)
+    plan = PT.gpu_plan(hq, P, snr, cols)
+    s = hq.EncodedStream(plan, rows)
+    xd = x.cuda()
+    for r0 in range(0, rows, 128):
+        hq.hq_encode(plan, xd[r0:r0 + 128], s, append=r0 > 0)
+    y = hq.hq_decode(plan, s, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    st = s.read_stats()
+    assert s.rows == rows
+    assert st["status"] == 0 and st["corrupt_substreams"] == 0, st
+    q = snr_db(xd, y)
+    rate = st["payload_bits"] / x.numel()
+    print(f"[fullsize] C4 {lname}@{bps}: {rate:.4f} bits/scalar, SNR {q:.3f} dB", flush=True)
+    assert abs(rate - bps) < 0.3
+    rng = np.random.default_rng(200 + lat)
+    sample = np.sort(rng.choice(rows, 16, replace=False))
+    check_sampled_rows(hq, plan, s, P, x, sample, f"C4 keys {lname}@{bps}", dither=True)
+    # unbiased inner products: for each of 1024 fixed queries, the mean of
+    # q . (k_hat - k) over every key of head 0 is zero within its standard error
+    qs = W.queries(device="cpu").cuda()
+    k = xd[:, :128].float()
+    d = y[:, :128] - k
+    e = d @ qs.t()  # [keys, queries]
+    n = e.shape[0]
+    z = e.mean(0) / (e.std(0) / np.sqrt(n))
+    print(f"[fullsize] C4 {lname}: max |mean error| / standard error over 1024 queries "
+          f"{z.abs().max().item():.2f}", flush=True)
+    assert z.abs().max().item() < 5.0
+
+
+def test_c4_kv_cache_values_e8(hq):
+    from paper_2606_23406_amd import workloads as W
+    x = W.kv_cache(role="v").reshape(16 * 8192, 1024)
+    rows, cols = x.shape
+    print(f"[fullsize] C4 values {rows}x{cols} E8@2, 128-token appends", flush=True)
+    snr = PT.op_snr("E8", 2.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=81, rotation=1, rot_seed=82, dither=True,
+                         dither_seed=83, norm_fp16=True)
+    plan = PT.gpu_plan(hq, P, snr, cols)
+    s = hq.EncodedStream(plan, rows)
+    xd = x.cuda()
+    for r0 in range(0, rows, 128):
+        hq.hq_encode(plan, xd[r0:r0 + 128], s, append=r0 > 0)
+    torch.cuda.synchronize()
+    st = s.read_stats()
+    assert st["status"] == 0, st
+    rng = np.random.default_rng(300)
+    check_sampled_rows(hq, plan, s, P, x, np.sort(rng.choice(rows, 12, replace=False)),
+                       "C4 values E8@2", dither=True)
+
+
+def test_c5_gemm_fullsize(hq):
+    from paper_2606_23406_amd import workloads as W
+    print("[fullsize] C5 gemm W 14336x4096 E8@4, A 4096x4096", flush=True)
+    w = W.llama_linear(0, 4)
+    a = W.activations()
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=W.llama_linear_seed(0, 4))
+    plan = PT.gpu_plan(hq, P, snr, 4096)
+    s = hq.EncodedStream(plan, 14336)
+    hq.hq_encode(plan, w.cuda(), s)
+    out = hq.hq_dequant_gemm_int8(plan, s, a.cuda(), out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert s.read_stats()["status"] == 0
+    rng = np.random.default_rng(400)
+    mi = np.sort(rng.choice(4096, 48, replace=False))
+    ni = np.sort(rng.choice(14336, 48, replace=False))
+    codes, norms, _, _ = O.frontend(P, w[ni].float().numpy())
+    g = O.weight_factors(P, norms, len(ni), 4096)
+    xq, sx = O.act_prep(a[mi].float().numpy(), 128, P.rht_seed)
+    ref = O.gemm_blockscaled(codes, g, xq, sx, 128)
+    got = out.cpu().numpy()[mi][:, ni].astype(np.float64)
+    denom = np.maximum(np.abs(ref), np.sqrt((ref ** 2).mean()))
+    rel = np.max(np.abs(got - ref) / denom)
+    print(f"[fullsize] C5 sampled 48x48 outputs: max relative error {rel:.2e}", flush=True)
+    assert rel <= 1e-3
+
+
+def test_corrupt_streams_are_reported(hq):
+    """Damaged tables and payloads decode without faults: the damaged
+    sub-streams are counted and zero-filled, the others decode unchanged."""
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=91)
+    g = torch.Generator().manual_seed(92)
+    x = (torch.randn((16, 1024), generator=g) * 0.02).to(torch.bfloat16)
+    plan = PT.gpu_plan(hq, P, snr, 1024)
+    s = hq.EncodedStream(plan, 16)
+    hq.hq_encode(plan, x.cuda(), s)
+    good = hq.hq_decode(plan, s, out_dtype=torch.float32).cpu()
+    torch.cuda.synchronize()
+    spr = plan.info.subs_per_row
+    # row 3: k too large for its words; row 7: an empty sub-stream; row 11:
+    # random payload words; row 13: an end offset past the capacity
+    kp = s.kparam.clone()
+    kp[3 * spr] = 15
+    s.kparam.copy_(kp)
+    off = s.offsets.clone()
+    off[7 * spr + 1] = off[7 * spr]
+    s.offsets.copy_(off)
+    o11 = int(s.offsets[11 * spr].item()) & 0xFFFFFFFF
+    o12 = int(s.offsets[11 * spr + 1].item()) & 0xFFFFFFFF
+    rnd = torch.randint(-2**31, 2**31 - 1, (o12 - o11,), generator=g, dtype=torch.int64)
+    s.payload[o11:o12] = rnd.to(s.payload.dtype).cuda()
+    off = s.offsets.clone()
+    off[13 * spr + 1] = s.c.capacity_words + 5
+    s.offsets.copy_(off)
+    s.reset_stats()
+    bad = hq.hq_decode(plan, s, out_dtype=torch.float32).cpu()
+    torch.cuda.synchronize()
+    st = s.read_stats()
+    assert st["status"] == (-6 & 0xFFFFFFFF), st  # HQ_ERR_CORRUPT
+    assert st["corrupt_substreams"] >= 2
+    for r in range(16):
+        if r in (3, 7, 11, 13):
+            continue
+        assert torch.equal(bad[r], good[r]), r
