@@ -1534,81 +1534,141 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
 // ------------------------------------------------------------ block-scaled int8 GEMM
 // out[m, n] = s_x[m] * sum_t g[n, t] * P_t[m, n], P_t the exact int32 sum of
 // one 128-deep K tile on the int8 matrix cores (v_mfma_i32_32x32x32_i8).
-// Workgroup tile 128 (tokens) x 128 (weight rows), four waves in 2 x 2, each
-// 64 x 64 = 2 x 2 MFMA blocks.  A and B stage through LDS one K tile at a
-// time.  Both operands are K-contiguous rows and every lane loads the same
-// 16 contiguous k for A and B, so the contraction pairs identical k whatever
-// order the instruction assigns inside its 32-deep step.  Output lane l of a
-// 32 x 32 block holds column l % 32 and rows 8 (r / 4) + 4 (l / 32) + r % 4.
+// Workgroup tile 256 (tokens) x 128 (weight rows), eight waves in 4 x 2,
+// each 64 x 64 = 2 x 2 MFMA blocks.  K tiles are double-buffered in LDS and the
+// next tile's global loads sit in registers while the current one is
+// multiplied; each tile's int32 sums are then rescaled on the VALU (one
+// convert + one fma per output), two waves per SIMD.  Both operands are K-contiguous rows and every
+// lane reads the same 16 contiguous k for A and B, so the contraction pairs
+// identical k whatever order the instruction assigns inside its 32-deep
+// step.  Output lane l of a 32 x 32 block holds column l % 32 and rows
+// 8 (r / 4) + 4 (l / 32) + r % 4.
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 typedef int v16i_t __attribute__((ext_vector_type(16)));
 
-constexpr int kGemmTile = 128;
-constexpr int kGemmLd = 144;  // padded LDS row (bytes)
+constexpr int kGemmM = 256, kGemmN = 128;  // the prefetch below assumes 256 x 128
+constexpr int kGemmThreads = 512;           // 8 waves, 4 (m) x 2 (n)
+constexpr int kGemmNB = kGemmN / 64;  // 32 x 32 blocks per wave along n
+constexpr int kGemmLd = 144;  // padded LDS row (bytes): rows 16 bytes apart mod 128
+constexpr int kGemmStageA = kGemmM * kGemmLd, kGemmStageB = kGemmN * kGemmLd;
+constexpr int kGemmLds = 2 * (kGemmStageA + kGemmStageB);
 
-__global__ __launch_bounds__(256) void hq_gemm_i8_kernel(hq_gemm_args A) {
-  __shared__ __attribute__((aligned(16))) int8_t sa[kGemmTile * kGemmLd];
-  __shared__ __attribute__((aligned(16))) int8_t sb[kGemmTile * kGemmLd];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int64_t m0 = (int64_t)blockIdx.y * kGemmTile, n0 = (int64_t)blockIdx.x * kGemmTile;
-  const int64_t T = A.K / HQ_TILE;
+// One thread's share of a K tile, in 16-byte chunks (chunk c = row c / 8,
+// byte (c % 8) * 16; thread tid takes c = tid + 512 i): 4 of A's 2048, 2 of
+// B's 1024.
+struct GemmPrefetch {
+  uint4 a0, a1, a2, a3, b0, b1;
+};
 
-  float accf[2][2][16];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) accf[a][b][r] = 0.0f;
+// Rows past M or N read the last valid row instead: they only feed outputs
+// that are never stored, and the loads stay branch-free.
+__device__ __forceinline__ uint4 gemm_chunk(const int8_t* base, int64_t row0, int64_t rows,
+                                            int64_t K, int64_t t, int c) {
+  const int64_t r = min(row0 + (c >> 3), rows - 1);
+  return *(const uint4*)(base + r * K + t * HQ_TILE + (c & 7) * 16);
+}
 
-  for (int64_t t = 0; t < T; ++t) {
-    // stage the K tile: 128 rows x 128 bytes each for A and B
+__device__ __forceinline__ void gemm_load(const hq_gemm_args& A, int64_t m0, int64_t n0, int64_t t,
+                                          int tid, GemmPrefetch& p) {
+  p.a0 = gemm_chunk(A.xq, m0, A.M, A.K, t, tid);
+  p.a1 = gemm_chunk(A.xq, m0, A.M, A.K, t, tid + 512);
+  p.a2 = gemm_chunk(A.xq, m0, A.M, A.K, t, tid + 1024);
+  p.a3 = gemm_chunk(A.xq, m0, A.M, A.K, t, tid + 1536);
+  p.b0 = gemm_chunk(A.w, n0, A.N, A.K, t, tid);
+  p.b1 = gemm_chunk(A.w, n0, A.N, A.K, t, tid + 512);
+}
+
+__device__ __forceinline__ void gemm_put(int8_t* s, int c, uint4 v) {
+  *(uint4*)(s + (c >> 3) * kGemmLd + (c & 7) * 16) = v;
+}
+
+__device__ __forceinline__ void gemm_stash(int8_t* sa, int8_t* sb, int tid, const GemmPrefetch& p) {
+  gemm_put(sa, tid, p.a0);
+  gemm_put(sa, tid + 512, p.a1);
+  gemm_put(sa, tid + 1024, p.a2);
+  gemm_put(sa, tid + 1536, p.a3);
+  gemm_put(sb, tid, p.b0);
+  gemm_put(sb, tid + 512, p.b1);
+}
+
+__device__ __forceinline__ void gemm_load_g(const hq_gemm_args& A, int64_t n0, int wn, int lane,
+                                            int64_t T, int64_t t, float (&gv)[kGemmNB]) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + 256 * i;
-      const int row = c >> 3, kc = (c & 7) * 16;
-      const int64_t ma = m0 + row, nb = n0 + row;
-      uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
-      if (ma < A.M) va = *(const uint4*)(A.xq + ma * A.K + t * HQ_TILE + kc);
-      if (nb < A.N) vb = *(const uint4*)(A.w + nb * A.K + t * HQ_TILE + kc);
-      *(uint4*)(sa + row * kGemmLd + kc) = va;
-      *(uint4*)(sb + row * kGemmLd + kc) = vb;
-    }
-    __syncthreads();
-    v16i_t acc[2][2];
+  for (int b = 0; b < kGemmNB; ++b) {
+    const int64_t n = min(n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31), A.N - 1);
+    gv[b] = A.g[n * T + t];
+  }
+}
+
+// One K tile: the wave's 2 x kGemmNB MFMA blocks from LDS, then their exact
+// int32 sums rescaled by the tile's weight factors into the fp32
+// accumulators.
+__device__ __forceinline__ void gemm_step(const int8_t* sa, const int8_t* sb, int wm, int wn,
+                                          int lane, const float (&gv)[kGemmNB],
+                                          float (&accf)[2][kGemmNB][16]) {
+  v16i_t acc[2][kGemmNB];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int koff = ks * 32 + (lane >> 5) * 16;
+    v4i_t fa[2], fb[kGemmNB];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+      fa[a] = *(const v4i_t*)(sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff);
+#pragma unroll
+    for (int b = 0; b < kGemmNB; ++b)
+      fb[b] = *(const v4i_t*)(sb + (wn * (kGemmN / 2) + b * 32 + (lane & 31)) * kGemmLd + koff);
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) acc[a][b] = (v16i_t){};
+      for (int b = 0; b < kGemmNB; ++b)
+        acc[a][b] = ks == 0 ? __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], (v16i_t){}, 0, 0, 0)
+                            : __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], acc[a][b], 0, 0, 0);
+  }
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int koff = ks * 32 + (lane >> 5) * 16;
-      v4i_t fa[2], fb[2];
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
-        fa[a] = *(const v4i_t*)(sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff);
+    for (int b = 0; b < kGemmNB; ++b)
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
-        fb[b] = *(const v4i_t*)(sb + (wn * 64 + b * 32 + (lane & 31)) * kGemmLd + koff);
+      for (int r = 0; r < 16; ++r)
+        accf[a][b][r] = __builtin_fmaf((float)acc[a][b][r], gv[b], accf[a][b][r]);
+}
+
+__global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_i8_kernel(hq_gemm_args A) {
+  extern __shared__ __attribute__((aligned(16))) int8_t gsm[];
+  int8_t* const sa = gsm;                    // stage s at sa + s * kGemmStageA
+  int8_t* const sb = gsm + 2 * kGemmStageA;  // stage s at sb + s * kGemmStageB
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
+  const int64_t T = A.K / HQ_TILE;
+
+  float accf[2][kGemmNB][16];
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    for (int b = 0; b < kGemmNB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) accf[a][b][r] = 0.0f;
+
+  GemmPrefetch pf;
+  gemm_load(A, m0, n0, 0, tid, pf);
+  gemm_stash(sa, sb, tid, pf);
+  __syncthreads();
+  gemm_load(A, m0, n0, min<int64_t>(1, T - 1), tid, pf);
+
+  // tile t from stage t & 1; the prefetched tile t + 1 goes to the other
+  // stage (free since the last barrier) and tile t + 2's loads start
+  for (int64_t t = 0; t < T; ++t) {
+    float gv[kGemmNB];
+    gemm_load_g(A, n0, wn, lane, T, t, gv);
+    const int st = (int)(t & 1);
+    gemm_step(sa + st * kGemmStageA, sb + st * kGemmStageB, wm, wn, lane, gv, accf);
+    if (t + 1 < T) {
+      gemm_stash(sa + (st ^ 1) * kGemmStageA, sb + (st ^ 1) * kGemmStageB, tid, pf);
+      __syncthreads();
+      gemm_load(A, m0, n0, min(t + 2, T - 1), tid, pf);  // the last tile again at the end
     }
-    // rescale the exact tile sums by the weight factor of column n
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int64_t n = n0 + wn * 64 + b * 32 + (lane & 31);
-      const float gv = (n < A.N) ? A.g[n * T + t] : 0.0f;
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) accf[a][b][r] = accf[a][b][r] + (float)acc[a][b][r] * gv;
-    }
-    __syncthreads();
   }
 
 #pragma unroll
@@ -1619,8 +1679,8 @@ __global__ __launch_bounds__(256) void hq_gemm_i8_kernel(hq_gemm_args A) {
       if (m >= A.M) continue;
       const float sxm = A.sx[m];
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int64_t n = n0 + wn * 64 + b * 32 + (lane & 31);
+      for (int b = 0; b < kGemmNB; ++b) {
+        const int64_t n = n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31);
         if (n >= A.N) continue;
         const float v = sxm * accf[a][b][r];
         if (A.out_bf16)
@@ -1722,8 +1782,15 @@ int hq_launch_act_prep(const hq_actprep_args& a, void* stream) {
 
 int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
   if (a.K % HQ_TILE != 0) return -1;
-  const dim3 grid((uint32_t)((a.N + kGemmTile - 1) / kGemmTile), (uint32_t)((a.M + kGemmTile - 1) / kGemmTile));
-  hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(256), 0, (hipStream_t)stream, a);
+  static bool lds_set = false;  // more than 64 KB of dynamic LDS needs an opt-in
+  if (!lds_set) {
+    const hipError_t e = hipFuncSetAttribute((const void*)hq_gemm_i8_kernel,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+    if (e != hipSuccess) return (int)e;
+    lds_set = true;
+  }
+  const dim3 grid((uint32_t)((a.N + kGemmN - 1) / kGemmN), (uint32_t)((a.M + kGemmM - 1) / kGemmM));
+  hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
   return (int)hipGetLastError();
 }
 
