@@ -89,6 +89,31 @@ __device__ __forceinline__ int32_t unzigzag(uint32_t m) {
   return (int32_t)(m >> 1) ^ -(int32_t)(m & 1u);
 }
 
+// In-byte select table: entry v packs, 4 bits per rank k = 0..7, the position
+// of the k-th set bit of the byte value v (entries for ranks past popc(v)
+// are unused).
+__device__ __forceinline__ uint32_t byte_select_entry(uint32_t v) {
+  uint32_t e = 0, k = 0;
+#pragma unroll
+  for (uint32_t b = 0; b < 8; ++b) {
+    if ((v >> b) & 1u) {
+      e |= b << (4 * k);
+      ++k;
+    }
+  }
+  return e;
+}
+
+// Position (0..31) of the r-th set bit (r from 0, r < popc(w)) of w: the
+// byte from cumulative byte popcounts, the bit from the table.
+__device__ __forceinline__ uint32_t select32_lut(uint32_t w, uint32_t r, const uint32_t* tbl) {
+  const uint32_t c1 = __popc(w & 0xFFu), c2 = __popc(w & 0xFFFFu), c3 = __popc(w & 0xFFFFFFu);
+  const uint32_t b = (uint32_t)(r >= c1) + (uint32_t)(r >= c2) + (uint32_t)(r >= c3);
+  const uint32_t below = b == 0 ? 0u : (b == 1 ? c1 : (b == 2 ? c2 : c3));
+  const uint32_t byte = __builtin_amdgcn_ubfe(w, 8 * b, 8);
+  return 8 * b + __builtin_amdgcn_ubfe(tbl[byte], 4 * (r - below), 3);
+}
+
 // Position (0..31) of the r-th set bit (r from 0) of w.
 __device__ __forceinline__ uint32_t select32(uint32_t w, uint32_t r) {
   uint32_t pos = 0, c;
@@ -1237,25 +1262,46 @@ __device__ __forceinline__ uint32_t bits32_at(const uint32_t* buf, uint32_t pos)
   return __builtin_amdgcn_alignbit(buf[w + 1], buf[w], pos & 31u);
 }
 
+// One sub-stream's table entry, checked against the buffers, and its first
+// 128 payload words (two per lane): loaded one sub-stream ahead of its decode.
+struct DecHead {
+  uint32_t start, kb, W, R;  // wave-uniform
+  bool ok;                   // entry within bounds (wave-uniform)
+  uint32_t w0, w1;           // payload words lane and lane + 64
+};
+
 template <int LAT>
-__device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, uint32_t gsub, bool active,
-                                               int lane, uint32_t* buf, uint32_t* starts,
-                                               uint32_t* sym) {
-  uint32_t start = 0, end = 0, kb = 0;
-  if (active) {
-    start = readfirst(A.offsets[gsub]);
-    end = readfirst(A.offsets[gsub + 1]);
-    kb = readfirst(A.kparam[gsub]);
-  }
+__device__ __forceinline__ DecHead dec_head(const hq_decode_args& A, bool active, uint32_t start,
+                                            uint32_t end, uint32_t kb, int lane) {
+  DecHead h;
   const uint32_t k0 = (LAT == kA2) ? (kb & 15u) : kb;
   const uint32_t k1 = (LAT == kA2) ? (kb >> 4) : (LAT == kD4 ? (k0 > 0 ? k0 - 1 : 0) : k0);
-  const uint32_t W = end - start;
+  h.start = start;
+  h.kb = kb;
+  h.W = end - start;
+  h.R = 64 * lane_rem_bits<LAT>(k0, k1);
+  h.ok = active && end >= start && (int64_t)end <= A.cap_words && h.W <= A.lds_words &&
+         k0 <= HQ_KMAX && h.R <= 32u * h.W;
+  const uint32_t Wl = h.ok ? h.W : 0u;
+  h.w0 = (uint32_t)lane < Wl ? A.payload[(uint64_t)start + lane] : 0u;
+  h.w1 = (uint32_t)lane + 64u < Wl ? A.payload[(uint64_t)start + 64u + lane] : 0u;
+  return h;
+}
+
+template <int LAT>
+__device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const DecHead& h, int lane,
+                                               uint32_t* buf, uint32_t* starts,
+                                               const uint32_t* seltbl, uint32_t* sym) {
+  const uint32_t kb = h.kb;
+  const uint32_t k0 = (LAT == kA2) ? (kb & 15u) : kb;
+  const uint32_t k1 = (LAT == kA2) ? (kb >> 4) : (LAT == kD4 ? (k0 > 0 ? k0 - 1 : 0) : k0);
   const uint32_t lrem = lane_rem_bits<LAT>(k0, k1);
-  const uint32_t R = 64 * lrem;
-  bool ok = active && end >= start && (int64_t)end <= A.cap_words && W <= A.lds_words &&
-            k0 <= HQ_KMAX && R <= 32u * W;
-  const uint32_t Wl = ok ? W : 0u;
-  for (uint32_t w = lane; w < Wl; w += 64) buf[w] = A.payload[(uint64_t)start + w];
+  const uint32_t R = h.R;
+  bool ok = h.ok;
+  const uint32_t Wl = ok ? h.W : 0u;
+  if ((uint32_t)lane < Wl) buf[lane] = h.w0;
+  if ((uint32_t)lane + 64u < Wl) buf[lane + 64] = h.w1;
+  for (uint32_t w = 128u + lane; w < Wl; w += 64) buf[w] = A.payload[(uint64_t)h.start + w];
   if (lane < 2) buf[Wl + lane] = 0u;  // two zero words past the end
   starts[lane] = (lane == 0) ? R : 0xFFFFFFFFu;
   wave_sync_lds();
@@ -1282,7 +1328,8 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, uint32_t
       pos = R;
     } else {
       ok = ok && incl >= target && w < nuw;
-      pos = ok ? (uw0 + w) * 32u + select32(word, target - 1u - (incl - __popc(word))) + 1u : 0u;
+      pos = ok ? (uw0 + w) * 32u + select32_lut(word, target - 1u - (incl - __popc(word)), seltbl) + 1u
+               : 0u;
     }
   } else {
     uint32_t carry = 0;
@@ -1381,100 +1428,119 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, uint32_t
 template <int LAT, int MODE, bool KV>
 __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
   extern __shared__ uint32_t smem[];
+  __shared__ uint32_t s_sel[256];
   const int tid = threadIdx.x, lane = tid & 63;
   const uint32_t wave = readfirst((uint32_t)(tid >> 6));
-  const uint32_t sub = blockIdx.x * HQ_WAVES_PER_WG + wave;
-  const bool active = sub < (uint32_t)A.nsub;
-  const uint32_t gsub = (uint32_t)A.first_sub + sub;
   uint32_t* buf = smem + wave * (A.lds_words + 66);
   uint32_t* starts = buf + A.lds_words + 2;
   const bool use_rot = KV && A.rotation;
   const bool use_dither = KV && A.dither;
   const bool fp16_norm = KV && A.norm_fp16;
+  s_sel[tid] = byte_select_entry((uint32_t)tid);  // 256 threads, one entry each
+  __syncthreads();
 
-  const uint32_t spr = (uint32_t)A.spr;
-  const uint32_t lrow = active ? sub / spr : 0u;
-  const uint32_t col = (active ? sub - lrow * spr : 0u) * HQ_SUB + 8u * (uint32_t)lane;
-  const int64_t grow = A.first_row + lrow;
-  const int64_t tix = grow * A.tpr + (col >> 7);
-  // per-tile norm and output signs, loaded before the bit walk
-  float rs = 0.0f;
-  if (active) rs = fp16_norm ? (float)((const _Float16*)A.norms)[tix] : ((const float*)A.norms)[tix];
-  uint4 sw = make_uint4(0u, 0u, 0u, 0u);
-  if (MODE == 1 && active) sw = *(const uint4*)(A.dsign16 + (col >> 1));
-
-  uint32_t sym[8];
-  const bool ok = decode_symbols<LAT>(A, gsub, active, lane, buf, starts, sym);
-  if (active && !ok && A.stats) {
-    // count the sub-stream once (its first failing lane reports)
-    const unsigned long long bad = __ballot(!ok);
-    if ((unsigned)lane == (unsigned)__builtin_ctzll(bad)) {
-      atomicAdd(&A.stats->corrupt_substreams, 1u);
-      atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
-    }
+  // this wave's sub-streams: HQ_DEC_SUBS_PER_WAVE consecutive ones; their
+  // table entries are read at once, each one's payload one sub-stream ahead
+  const uint32_t sub0 = (blockIdx.x * HQ_WAVES_PER_WG + wave) * HQ_DEC_SUBS_PER_WAVE;
+  const uint32_t nsub = (uint32_t)A.nsub;
+  uint32_t off[HQ_DEC_SUBS_PER_WAVE + 1], kbs[HQ_DEC_SUBS_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i <= HQ_DEC_SUBS_PER_WAVE; ++i) {
+    const uint32_t sub = sub0 + (uint32_t)i;
+    off[i] = sub <= nsub ? readfirst(A.offsets[(uint32_t)A.first_sub + sub]) : 0u;
+    if (i < HQ_DEC_SUBS_PER_WAVE)
+      kbs[i] = sub < nsub ? readfirst(A.kparam[(uint32_t)A.first_sub + sub]) : 0u;
   }
-  int32_t c[8];
-  unstrip8<LAT>(sym, c);
-  const float g = rs / A.alpha_n;
+  DecHead head = dec_head<LAT>(A, sub0 < nsub, off[0], off[1], kbs[0], lane);
+  const uint32_t spr = (uint32_t)A.spr;
+  const TwSigns sg(lane);
+  const uint32_t sbits = use_rot ? sign_bits8(A.smask, (lane & 15) * 8) : 0u;
 
-  if constexpr (MODE == 2) {
-    if (!active) return;
-    uint32_t packed[2] = {0u, 0u};
-    uint32_t clamps = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      int32_t v = c[j];
-      if (v > 127) { v = 127; ++clamps; }
-      if (v < -127) { v = -127; ++clamps; }
-      packed[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
+  for (int i = 0; i < HQ_DEC_SUBS_PER_WAVE; ++i) {
+    const uint32_t sub = sub0 + (uint32_t)i;
+    if (sub >= nsub) break;
+    DecHead next;
+    if (i + 1 < HQ_DEC_SUBS_PER_WAVE)
+      next = dec_head<LAT>(A, sub + 1 < nsub, off[i + 1], off[i + 2], kbs[i + 1], lane);
+    const uint32_t lrow = sub / spr;
+    const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
+    const int64_t grow = A.first_row + lrow;
+    const int64_t tix = grow * A.tpr + (col >> 7);
+    // per-tile norm and output signs, loaded before the bit walk
+    const float rs = fp16_norm ? (float)((const _Float16*)A.norms)[tix] : ((const float*)A.norms)[tix];
+    uint4 sw = make_uint4(0u, 0u, 0u, 0u);
+    if (MODE == 1) sw = *(const uint4*)(A.dsign16 + (col >> 1));
+
+    uint32_t sym[8];
+    const bool ok = decode_symbols<LAT>(A, head, lane, buf, starts, s_sel, sym);
+    if (!ok && A.stats) {
+      // count the sub-stream once (its first failing lane reports)
+      const unsigned long long bad = __ballot(!ok);
+      if ((unsigned)lane == (unsigned)__builtin_ctzll(bad)) {
+        atomicAdd(&A.stats->corrupt_substreams, 1u);
+        atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+      }
     }
-    int8_t* out = (int8_t*)A.y + (int64_t)lrow * A.ld + col;
-    *(uint2*)out = make_uint2(packed[0], packed[1]);
-    if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
-    if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
-    return;
-  } else {
-    // y = D H^T (S) (code - U) * r / (alpha n); the integer codes make the
-    // transform exact in fp32 (|sum| <= 128 * 65536 < 2^24) whenever there
-    // is no dither
-    const TwSigns sg(lane);
-    const uint32_t sbits = use_rot ? sign_bits8(A.smask, (lane & 15) * 8) : 0u;
-    float y[8];
+    int32_t c[8];
+    unstrip8<LAT>(sym, c);
+    const float g = rs / A.alpha_n;
+
+    if constexpr (MODE == 2) {
+      uint32_t packed[2] = {0u, 0u};
+      uint32_t clamps = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) y[j] = code_coord<LAT>(c[j], j);
-    if (use_dither) {
-      float u[8];
-      dither8<LAT>(A.dither_seed, grow, col, u);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = y[j] - u[j];
-    }
-    if (use_rot) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = flip(y[j], sbits, j);
-    }
-    fwht128_tw(y, sg);
-    const float g_tw = xor_sign(g, sg.sigma);
-#pragma unroll
-    for (int j = 0; j < 8; ++j) y[j] = y[j] * g_tw;
-    if (!active) return;
-    if constexpr (MODE == 0) {
-      const uint32_t dbits = sign_bits8(A.dmask, col);
-#pragma unroll
-      for (int j = 0; j < 8; ++j) y[j] = flip(y[j], dbits, j);
-      float4* out = (float4*)((float*)A.y + (int64_t)lrow * A.ld + col);
-      out[0] = make_float4(y[0], y[1], y[2], y[3]);
-      out[1] = make_float4(y[4], y[5], y[6], y[7]);
+      for (int j = 0; j < 8; ++j) {
+        int32_t v = c[j];
+        if (v > 127) { v = 127; ++clamps; }
+        if (v < -127) { v = -127; ++clamps; }
+        packed[j >> 2] |= ((uint32_t)v & 0xFFu) << (8 * (j & 3));
+      }
+      int8_t* out = (int8_t*)A.y + (int64_t)lrow * A.ld + col;
+      *(uint2*)out = make_uint2(packed[0], packed[1]);
+      if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
+      if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
     } else {
-      __bf16 b[8];
+      // y = D H^T (S) (code - U) * r / (alpha n); the integer codes make the
+      // transform exact in fp32 (|sum| <= 128 * 65536 < 2^24) whenever there
+      // is no dither
+      float y[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) b[j] = (__bf16)y[j];
-      uint4 o = *(const uint4*)b;
-      o.x ^= sw.x;
-      o.y ^= sw.y;
-      o.z ^= sw.z;
-      o.w ^= sw.w;
-      *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = o;
+      for (int j = 0; j < 8; ++j) y[j] = code_coord<LAT>(c[j], j);
+      if (use_dither) {
+        float u[8];
+        dither8<LAT>(A.dither_seed, grow, col, u);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = y[j] - u[j];
+      }
+      if (use_rot) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = flip(y[j], sbits, j);
+      }
+      fwht128_tw(y, sg);
+      const float g_tw = xor_sign(g, sg.sigma);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[j] = y[j] * g_tw;
+      if constexpr (MODE == 0) {
+        const uint32_t dbits = sign_bits8(A.dmask, col);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = flip(y[j], dbits, j);
+        float4* out = (float4*)((float*)A.y + (int64_t)lrow * A.ld + col);
+        out[0] = make_float4(y[0], y[1], y[2], y[3]);
+        out[1] = make_float4(y[4], y[5], y[6], y[7]);
+      } else {
+        __bf16 b[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) b[j] = (__bf16)y[j];
+        uint4 o = *(const uint4*)b;
+        o.x ^= sw.x;
+        o.y ^= sw.y;
+        o.z ^= sw.z;
+        o.w ^= sw.w;
+        *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = o;
+      }
     }
+    if (i + 1 < HQ_DEC_SUBS_PER_WAVE) head = next;
   }
 }
 
@@ -1725,7 +1791,8 @@ void launch_decode_mode(const hq_decode_args& a, bool kv, uint32_t nwg, size_t l
 
 template <int LAT>
 int launch_decode_lat(const hq_decode_args& a, int mode, bool kv, hipStream_t st) {
-  const uint32_t nwg = (uint32_t)((a.nsub + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG);
+  constexpr int per_wg = HQ_WAVES_PER_WG * HQ_DEC_SUBS_PER_WAVE;
+  const uint32_t nwg = (uint32_t)((a.nsub + per_wg - 1) / per_wg);
   const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
   if (mode == 0)
     launch_decode_mode<LAT, 0>(a, kv, nwg, lds, st);
