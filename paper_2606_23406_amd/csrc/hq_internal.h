@@ -12,7 +12,8 @@
 #define HQ_SUB 512               // symbols per sub-stream the kernels are built for
 #define HQ_WAVES_PER_WG 4        // wave64s per workgroup
 #define HQ_ENC_SUBS_PER_WAVE 4   // encode: sub-streams per wave, one after another
-#define HQ_ENC_SUBS_PER_WG (HQ_WAVES_PER_WG * HQ_ENC_SUBS_PER_WAVE)
+#define HQ_ENC_WAVES 4           // encode: wave64s per workgroup
+#define HQ_ENC_SUBS_PER_WG (HQ_ENC_WAVES * HQ_ENC_SUBS_PER_WAVE)
 #define HQ_DEC_SUBS_PER_WAVE 4   // decode: consecutive sub-streams per wave
 #define HQ_SCAN_STATUS_OFFSET 128  // bytes before the look-back status array
 

@@ -1043,11 +1043,11 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
 }
 
 template <int LAT, int XT, bool KV>
-__global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
+__global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_kernel(hq_encode_args A) {
   extern __shared__ uint32_t smem[];
   __shared__ uint32_t s_epoch;
   __shared__ uint32_t s_words[HQ_ENC_SUBS_PER_WG];
-  __shared__ uint32_t s_part[HQ_WAVES_PER_WG], s_part2[HQ_WAVES_PER_WG];
+  __shared__ uint32_t s_pad[HQ_ENC_WAVES];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = (int)readfirst((uint32_t)(tid >> 6));
@@ -1067,10 +1067,10 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
     uint32_t row = sub0 / spr, c = sub0 - row * spr;
 #pragma unroll
     for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
-      pos[i].active = sub0 + (uint32_t)(i * HQ_WAVES_PER_WG) < (uint32_t)A.nsub;
+      pos[i].active = sub0 + (uint32_t)(i * HQ_ENC_WAVES) < (uint32_t)A.nsub;
       pos[i].lrow = pos[i].active ? row : 0u;
       pos[i].col0 = pos[i].active ? c * HQ_SUB : 0u;
-      c += HQ_WAVES_PER_WG;
+      c += HQ_ENC_WAVES;
       while (c >= spr) {
         c -= spr;
         ++row;
@@ -1080,10 +1080,10 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   // ---- encode this group's sub-streams into LDS; the next sub-stream's
   //      input is loaded while the current one is encoded
   LaneInput in = load_lane_input<XT>(A, pos[0], lane);
-  uint32_t bitsum = 0, padsum = 0;
+  uint32_t padsum = 0;
 #pragma unroll
   for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
-    const int li = i * HQ_WAVES_PER_WG + wave;  // neighbouring waves take neighbouring sub-streams
+    const int li = i * HQ_ENC_WAVES + wave;  // neighbouring waves take neighbouring sub-streams
     const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
     LaneInput next;
     if (i + 1 < HQ_ENC_SUBS_PER_WAVE) next = load_lane_input<XT>(A, pos[i + 1], lane);
@@ -1096,7 +1096,6 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
         s_words[li] = W;
         if (ovf && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_OVERFLOW);
       }
-      bitsum += bits;
       padsum += W * 32u - bits;
     } else if (lane == 0) {
       s_words[li] = 0;
@@ -1104,25 +1103,26 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
     if (i + 1 < HQ_ENC_SUBS_PER_WAVE) in = next;
   }
   if (lane == 0) {
-    s_part[wave] = bitsum;
-    s_part2[wave] = padsum;
+    s_pad[wave] = padsum;
   }
   __syncthreads();
-  // Waves 1..3 are done: their slots go to the next workgroups while wave 0
+  // The other waves are done: their slots go to the next workgroups while wave 0
   // alone waits for the group's offset and writes every sub-stream out.
   // (No workgroup barrier follows.)
   if (wave != 0) return;
 
   const uint32_t epoch = readfirst(s_epoch);
   // ---- publish this group's word count at once, so successors can pass it;
-  //      the group's bit counts go to its stats word first (at most 2^22
-  //      payload bits and 16 * 31 pad bits, packed as bits << 9 | pad)
+  //      the group's pad bits go to its stats word first (packed as
+  //      words << 11 | pad: at most 2^19 words and 64 * 31 pad bits)
+  static_assert(HQ_ENC_SUBS_PER_WG <= 64, "one sub-stream word count per lane");
   const uint32_t agg = wave_total(lane < HQ_ENC_SUBS_PER_WG ? s_words[lane] : 0u);
   if (lane == 0) {
     if (A.stats) {
-      const uint32_t gb = s_part[0] + s_part[1] + s_part[2] + s_part[3];
-      const uint32_t gp = s_part2[0] + s_part2[1] + s_part2[2] + s_part2[3];
-      store_status(&A.wgstat[wg], pack_status(epoch, 1u, (gb << 9) | gp));
+      uint32_t gp = 0;
+#pragma unroll
+      for (int w = 0; w < HQ_ENC_WAVES; ++w) gp += s_pad[w];
+      store_status(&A.wgstat[wg], pack_status(epoch, 1u, (agg << 11) | gp));
     }
     if (wg > 0) store_status(&A.status[wg], pack_status(epoch, 1u, agg));
   }
@@ -1208,7 +1208,7 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
   //      group's look-back has passed), so the stats block takes one atomic
   //      per 256 groups instead of one per group
   if (A.stats && ((wg & 255u) == 255u || wg == A.nwg - 1)) {
-    uint32_t gb = 0, gp = 0;
+    uint32_t gw = 0, gp = 0;  // words, pad bits
     bool late = false;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
@@ -1218,8 +1218,8 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
       for (;;) {
         const unsigned long long st = load_status(&A.wgstat[idx]);
         if ((uint32_t)(st >> 34) == epoch && ((st >> 32) & 3u) != 0u) {
-          gb += (uint32_t)st >> 9;
-          gp += (uint32_t)st & 511u;
+          gw += (uint32_t)st >> 11;
+          gp += (uint32_t)st & 2047u;
           break;
         }
         if (++spins > kSpinLimit) {
@@ -1229,10 +1229,10 @@ __global__ __launch_bounds__(256) void hq_encode_kernel(hq_encode_args A) {
         __builtin_amdgcn_s_sleep(1);
       }
     }
-    const uint32_t tb = wave_total(gb), tp = wave_total(gp);
+    const uint32_t tw = wave_total(gw), tp = wave_total(gp);  // < 2^27 words, < 2^19 pad bits
     if (late) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
     if (lane == 0) {
-      atomicAdd(&A.stats->payload_bits, (unsigned long long)tb);
+      atomicAdd(&A.stats->payload_bits, 32ull * tw - tp);
       atomicAdd(&A.stats->pad_bits, (unsigned long long)tp);
     }
   }
@@ -1769,14 +1769,14 @@ int launch_encode_lat(const hq_encode_args& a, int xt, bool kv, hipStream_t st) 
   const size_t lds = (size_t)(a.lds_words + 2) * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
   if (xt == HQ_BF16) {
     if (kv)
-      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_BF16, true>), dim3(a.nwg), dim3(256), lds, st, a);
+      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_BF16, true>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES), lds, st, a);
     else
-      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_BF16, false>), dim3(a.nwg), dim3(256), lds, st, a);
+      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_BF16, false>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES), lds, st, a);
   } else {
     if (kv)
-      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_FP32, true>), dim3(a.nwg), dim3(256), lds, st, a);
+      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_FP32, true>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES), lds, st, a);
     else
-      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_FP32, false>), dim3(a.nwg), dim3(256), lds, st, a);
+      hipLaunchKernelGGL((hq_encode_kernel<LAT, HQ_FP32, false>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES), lds, st, a);
   }
   return (int)hipGetLastError();
 }
