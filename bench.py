@@ -70,40 +70,100 @@ def decode_all(H, mats):
 
 
 def cpu_baseline(mats, seconds):
-    """The oracle as it stands, single-threaded, on row slices of layer 0's
-    seven matrices, repeated until `seconds` of CPU work.  Its alpha is the
+    """The oracle as it stands on row slices of layer 0's seven matrices: one
+    thread, then one thread per host core the process may run on (at most 16),
+    each encoding and decoding its own slices (the oracle's C calls release
+    the GIL), for about `seconds` of wall time each.  Its alpha is the
     oracle's own E8 at 4 bps operating point."""
+    from concurrent.futures import ThreadPoolExecutor
     from oracle import oracle as O
     from paper_2606_23406_amd import workloads as W
     pts = json.load(open(os.path.join(ROOT, "tests", "golden", "operating_points.json")))["points"]
     snr = [p["snr_db"] for p in pts if p["lattice"] == "E8" and p["bps"] == 4.0][0]
     names = [n for n, _, _ in W.LLAMA_LINEARS]
     rows_per = {"q": 256, "k": 128, "v": 128, "o": 256, "gate": 512, "up": 512, "down": 256}
+    threads = max(1, min(16, len(os.sched_getaffinity(0))))
     sample = []
     for m in mats[:7]:
-        x = m["x"][:rows_per[m["name"]]].float().cpu().numpy()
+        x = m["x"][:rows_per[m["name"]] * threads].float().cpu().numpy()
         seed = W.llama_linear_seed(m["layer"], names.index(m["name"]))
-        sample.append((O.Params(tile=128, lattice=O.E8, alpha=O.alpha(O.E8, snr), rht_seed=seed), x))
-    n_scalars = 0
-    t_enc = t_dec = 0.0
-    t_start = time.time()
-    while time.time() - t_start < seconds:
-        for P, x in sample:
-            t0 = time.perf_counter()
-            st = O.encode(P, x)
-            t1 = time.perf_counter()
-            O.decode(P, st)
-            t2 = time.perf_counter()
-            t_enc += t1 - t0
-            t_dec += t2 - t1
-            n_scalars += x.size
-    gbs = 2.0 * n_scalars / (t_enc + t_dec) / 1e9
-    desc = ("oracle encode+decode, 1 thread, on row slices of layer 0 "
-            "(q 256, k 128, v 128, o 256, gate 512, up 512, down 256 rows), "
-            f"{n_scalars / 1e6:.1f}M scalars in {t_enc + t_dec:.1f}s")
-    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle", "sample": desc,
-            "encode_GBs": round(2.0 * n_scalars / t_enc / 1e9, 4),
-            "decode_GBs": round(2.0 * n_scalars / t_dec / 1e9, 4)}
+        P = O.Params(tile=128, lattice=O.E8, alpha=O.alpha(O.E8, snr), rht_seed=seed)
+        sample.append((P, x, rows_per[m["name"]]))
+
+    def work(tid, nthreads, budget):
+        n = 0
+        t_enc = t_dec = 0.0
+        t_start = time.perf_counter()
+        while time.perf_counter() - t_start < budget:
+            for P, x, rows in sample:
+                xs = x[(tid % nthreads) * rows:(tid % nthreads + 1) * rows]
+                t0 = time.perf_counter()
+                st = O.encode(P, xs)
+                t1 = time.perf_counter()
+                O.decode(P, st)
+                t2 = time.perf_counter()
+                t_enc += t1 - t0
+                t_dec += t2 - t1
+                n += xs.size
+        return n, t_enc, t_dec
+
+    n1, e1, d1 = work(0, 1, seconds / 2)
+    gbs1 = 2.0 * n1 / (e1 + d1) / 1e9
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(threads) as ex:
+        res = list(ex.map(lambda t: work(t, threads, seconds / 2), range(threads)))
+    wall = time.perf_counter() - t0
+    nT = sum(r[0] for r in res)
+    gbsT = 2.0 * nT / wall / 1e9
+    desc = (f"oracle encode+decode on row slices of layer 0 (per thread: q 256, k 128, v 128, o 256, "
+            f"gate 512, up 512, down 256 rows), {threads} threads over their own slices: "
+            f"{nT / 1e6:.1f}M scalars in {wall:.1f}s wall; 1 thread: {n1 / 1e6:.1f}M scalars "
+            f"in {e1 + d1:.1f}s")
+    return {"value": round(gbsT, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
+            "sample": desc, "value_1thread": round(gbs1, 4),
+            "encode_GBs_1thread": round(2.0 * n1 / e1 / 1e9, 4),
+            "decode_GBs_1thread": round(2.0 * n1 / d1 / 1e9, 4)}
+
+
+def copy_bandwidth(dev, nbytes=1 << 30, reps=5):
+    """Device-to-device copy of `nbytes` (hipMemcpyAsync's copy kernel): the
+    practical HBM ceiling, and the known-size kernel that scales the HBM byte
+    counters."""
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) * 1e-3 / reps
+    del src, dst
+    return round(2.0 * nbytes / t / 1e9, 1)
+
+
+def measured_traffic(kernel_key):
+    """HBM bytes per launch of a codec kernel on this workload, from the
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary in profiles/, if it was taken on
+    the current kernel source (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "codec_e8_4bps_llama8b_stack_hbm_traffic.txt")
+    src = os.path.join(ROOT, "paper_2606_23406_amd", "csrc", "hq_kernels.hip")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    for line in open(path):
+        if "=" in line and not line.lstrip().startswith("#"):
+            k, v = line.split("=", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != hashlib.sha256(open(src, "rb").read()).hexdigest():
+        return None
+    try:
+        return float(kv[kernel_key + "_hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def gemm_extra(H, W, mats, dev):
@@ -194,6 +254,11 @@ def main():
     enc_gbs = enc_bytes / t_enc / 1e9
     dec_gbs = dec_bytes / t_dec / 1e9
 
+    copy_gbs = copy_bandwidth(dev)
+    alg_enc_launch = enc_bytes / len(mats)
+    alg_dec_launch = dec_bytes / len(mats)
+    tr_enc = measured_traffic("encode")
+    tr_dec = measured_traffic("decode")
     out = {
         "metric": "encode+decode GB/s of bf16 input (E8, 4 bps) and % of HBM peak, 1 GPU",
         "value": round(value, 2),
@@ -215,12 +280,18 @@ def main():
         "pct_hbm_peak": round(100.0 * (enc_bytes + dec_bytes) / t_step / 1e9 / HBM_PEAK_GBS, 2),
         "roofline": {"bound": "hbm", "kernel": "hq_encode_kernel (E8, bf16 in)",
                      "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(enc_gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                     "algorithmic_bytes_per_scalar": round(enc_bytes / n_scalars, 4)},
+                     "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": None if tr_enc is None else round(tr_enc),
+                     "algorithmic_bytes_per_launch": round(alg_enc_launch),
+                     "algorithmic_bytes_per_scalar": round(enc_bytes / n_scalars, 4),
+                     "launches_per_step": len(mats)},
         "decode_roofline": {"bound": "hbm", "kernel": "hq_decode_kernel (E8, bf16 out)",
                             "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                            "traffic": None if tr_dec is None else round(tr_dec),
+                            "algorithmic_bytes_per_launch": round(alg_dec_launch),
                             "algorithmic_bytes_per_scalar": round(dec_bytes / n_scalars, 4)},
+        "copy_GBs_device": copy_gbs,
         "encode_ms": round(t_enc * 1e3, 4),
         "decode_ms": round(t_dec * 1e3, 4),
         "encode_GBs_bf16_in": round(2.0 * n_scalars / t_enc / 1e9, 1),
