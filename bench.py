@@ -42,6 +42,7 @@ def parse_args():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemm", action="store_true")
+    ap.add_argument("--no-other", action="store_true", help="skip the C1, C2, C3-D4 and C4 measurements")
     return ap.parse_args()
 
 
@@ -55,7 +56,7 @@ def build_workload(H, W, layers, bps, dev, snr=None):
             x = W.llama_linear(layer, idx, device=dev)
             s = H.EncodedStream(plan, out_f, device=dev)
             y = torch.empty_like(x)
-            mats.append({"name": name, "layer": layer, "plan": plan, "x": x, "s": s, "y": y})
+            mats.append({"name": name, "layer": layer, "seed": seed, "plan": plan, "x": x, "s": s, "y": y})
     return mats
 
 
@@ -119,8 +120,17 @@ def cpu_baseline(mats, seconds):
             f"gate 512, up 512, down 256 rows), {threads} threads over their own slices: "
             f"{nT / 1e6:.1f}M scalars in {wall:.1f}s wall; 1 thread: {n1 / 1e6:.1f}M scalars "
             f"in {e1 + d1:.1f}s")
+    cpu_model = None
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": round(gbsT, 4), "unit": "GB/s", "cores": threads, "kind": "oracle",
-            "sample": desc, "value_1thread": round(gbs1, 4),
+            "sample": desc, "cpu_model": cpu_model,
+            "host_cpus_allowed": len(os.sched_getaffinity(0)), "value_1thread": round(gbs1, 4),
             "encode_GBs_1thread": round(2.0 * n1 / e1 / 1e9, 4),
             "decode_GBs_1thread": round(2.0 * n1 / d1 / 1e9, 4)}
 
@@ -164,6 +174,130 @@ def measured_traffic(kernel_key):
         return float(kv[kernel_key + "_hbm_bytes_per_launch"])
     except (KeyError, ValueError):
         return None
+
+
+def _median_ms(fn, reps, flush=None):
+    """Median over `reps` runs of fn() on the current stream, each preceded by
+    an untimed 1 GiB scratch write when `flush` is given (so inputs smaller
+    than the 256 MB last-level cache are read cold)."""
+    times = []
+    for _ in range(reps):
+        if flush is not None:
+            flush.fill_(0.0)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        b.synchronize()
+        times.append(a.elapsed_time(b))
+    times.sort()
+    return times[len(times) // 2]
+
+
+def other_workloads(H, W, dev, reps=20):
+    """The other synthetic configurations at 1 GPU: C1 (512x512 fp32), C2
+    (4096x4096 bf16 Student-t + outlier columns, E8 at 4 and 3 bps) and C4 (KV
+    keys [16, 8192, 8, 128] bf16 with signs rotation, dither and fp16 norms:
+    64 appends of [16, 128] tokens, then one full dequant), cold (1 GiB
+    scratch write between runs).  GB/s are of input bytes (bf16, or fp32 for
+    C1); pct_hbm is algorithmic bytes over time against 8 TB/s."""
+    import numpy as np
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    out = {}
+
+    def codec(name, x, lattice, bps, kv=False, rows_per_append=None):
+        print(f"[bench] {name}", file=sys.stderr, flush=True)
+        rows, cols = x.shape
+        opts = dict(rotation=1, dither=True, rot_seed=72, dither_seed=73, norm_fp16=True) if kv else {}
+        plan = H.hq_plan(128, lattice, bps, 17, -1, cols, **opts)
+        s = H.EncodedStream(plan, rows)
+        y = torch.empty((rows, cols), dtype=torch.bfloat16, device=dev)
+        esz = x.element_size()
+
+        def enc():
+            if rows_per_append:
+                for r0 in range(0, rows, rows_per_append):
+                    H.hq_encode(plan, x[r0:r0 + rows_per_append], s, append=r0 > 0)
+            else:
+                H.hq_encode(plan, x, s)
+
+        enc()
+        H.hq_decode(plan, s, out=y)
+        torch.cuda.synchronize()
+        s.reset_stats()
+        enc()
+        torch.cuda.synchronize()
+        bits = s.read_stats()["payload_bits"]
+        n = x.numel()
+        te = _median_ms(enc, reps, flush) * 1e-3
+        td = _median_ms(lambda: H.hq_decode(plan, s, out=y), reps, flush) * 1e-3
+        side = n / 128 * (2 if kv else 4) + n / 512 * 5
+        alg_e = n * esz + bits / 8 + side
+        alg_d = bits / 8 + side + n * 2
+        e = (y.float() - x.float())
+        snr_db = float(10 * torch.log10((x.float() ** 2).sum() / (e * e).sum()))
+        out[name] = {"scalars": n, "bits_per_scalar": round(bits / n, 4), "snr_db": round(snr_db, 3),
+                     "encode_us": round(te * 1e6, 1), "decode_us": round(td * 1e6, 1),
+                     "encode_GBs_in": round(n * esz / te / 1e9, 1),
+                     "decode_GBs_out": round(n * 2 / td / 1e9, 1),
+                     "encode_pct_hbm": round(100 * alg_e / te / 1e9 / HBM_PEAK_GBS, 2),
+                     "decode_pct_hbm": round(100 * alg_d / td / 1e9 / HBM_PEAK_GBS, 2)}
+        del s, y
+
+    x1 = torch.from_numpy(W.single_matrix_fp32()).to(dev)
+    codec("C1_512x512_fp32_E8@4", x1, H.HQ_E8, 4.0)
+    x2 = W.heavy_tailed_weight().to(dev)
+    codec("C2_4096x4096_bf16_E8@4", x2, H.HQ_E8, 4.0)
+    codec("C2_4096x4096_bf16_E8@3", x2, H.HQ_E8, 3.0)
+    del x2
+    k = W.kv_cache(device="cpu", role="k")  # [16, 8192, 8, 128], appended 128 tokens at a time
+    xk = k.permute(1, 0, 2, 3).reshape(64, 128, 16, 1024).permute(0, 2, 1, 3).reshape(-1, 1024)
+    xk = xk.contiguous().to(dev)  # rows (token block, batch, token), one row = 8 head vectors
+    del k
+    for name, lat, bps in (("E8@2", H.HQ_E8, 2.0), ("A2@1.7", H.HQ_A2, 1.7), ("Z@1.7", H.HQ_Z, 1.7)):
+        codec(f"C4_kv_keys_16x8192x8x128_{name}", xk, lat, bps, kv=True, rows_per_append=16 * 128)
+    del xk, flush
+    torch.cuda.empty_cache()
+    return out
+
+
+def stack_d4(H, mats, reps=3):
+    """The same linear stack with the D4 lattice at 3 bps (whole-model encode
+    then decode), on the inputs already resident; median of `reps` steps."""
+    print("[bench] C3_llama8b_stack_D4@3", file=sys.stderr, flush=True)
+    d4 = []
+    for m in mats:
+        plan = H.hq_plan(128, H.HQ_D4, 3.0, m["seed"], -1, m["x"].shape[1])
+        d4.append({"plan": plan, "x": m["x"], "s": H.EncodedStream(plan, m["x"].shape[0]), "y": m["y"]})
+    encode_all(H, d4)
+    decode_all(H, d4)
+    torch.cuda.synchronize()
+    te, td = [], []
+    for _ in range(reps):
+        a, b, c = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        for m in d4:
+            m["s"].reset_stats()
+        a.record()
+        encode_all(H, d4)
+        b.record()
+        decode_all(H, d4)
+        c.record()
+        c.synchronize()
+        te.append(a.elapsed_time(b) * 1e-3)
+        td.append(b.elapsed_time(c) * 1e-3)
+    te, td = sorted(te)[reps // 2], sorted(td)[reps // 2]
+    n = sum(m["x"].numel() for m in d4)
+    bits = sum(m["s"].read_stats()["payload_bits"] for m in d4)
+    ok = all(m["s"].read_stats()["status"] == 0 for m in d4)
+    stream_bytes = bits / 8 + 4 * n / 128 + 5 * n / 512
+    out = {"scalars": n, "bits_per_scalar": round(bits / n, 4), "encode_ms": round(te * 1e3, 3),
+           "decode_ms": round(td * 1e3, 3), "GBs_bf16_in": round(2 * n / (te + td) / 1e9, 1),
+           "encode_pct_hbm": round(100 * (2 * n + stream_bytes) / te / 1e9 / HBM_PEAK_GBS, 2),
+           "decode_pct_hbm": round(100 * (2 * n + stream_bytes) / td / 1e9 / HBM_PEAK_GBS, 2),
+           "device_status_ok": ok}
+    del d4
+    torch.cuda.empty_cache()
+    return out
 
 
 def gemm_extra(H, W, mats, dev):
@@ -303,6 +437,10 @@ def main():
         out["gemm_int8"] = gemm_extra(H, W, mats, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(mats, args.cpu_seconds)
+    if not args.no_other:
+        other = {"C3_llama8b_stack_D4@3": stack_d4(H, mats)}
+        other.update(other_workloads(H, W, dev))
+        out["other_workloads"] = other
     print(json.dumps(out), flush=True)
 
 

@@ -18,7 +18,7 @@ FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     # every fp32 rounding in the kernels is the one written; no fused contractions
     "-ffp-contract=off",
-    # packed fp32 vector ops stay disabled on the test machines
+    # no packed fp32 vector instructions (v_pk_*_f32) are generated
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]

@@ -91,32 +91,36 @@ def test_c2_heavy_tailed_4096(hq, bps):
     check_sampled_rows(hq, plan, s, P, x, rows, f"C2 E8@{bps}")
 
 
-@pytest.mark.parametrize("idx,lat,bps", [(4, O.E8, 4.0), (6, O.E8, 4.0), (4, O.D4, 3.0),
-                                         (1, O.D4, 3.0)])
-def test_c3_llama_linears(hq, idx, lat, bps):
+@pytest.mark.parametrize("layer", [0, 15, 31])
+@pytest.mark.parametrize("lat,bps", [(O.E8, 4.0), (O.D4, 3.0)])
+def test_c3_llama_linears(hq, layer, lat, bps):
+    """All seven linears of one layer (generated on the device, as the bench
+    does): the whole matrix through the HIP path, stats and SNR over all of
+    it, 8 sampled rows each bit for bit against the oracle."""
     from paper_2606_23406_amd import workloads as W
-    name, out_f, in_f = W.LLAMA_LINEARS[idx]
-    layer = 31
     lname = "E8" if lat == O.E8 else "D4"
-    print(f"[fullsize] C3 layer {layer} {name} {out_f}x{in_f} {lname}@{bps}", flush=True)
-    x = W.llama_linear(layer, idx)
     snr = PT.op_snr(lname, bps)
-    P = PT.oracle_params(lat, snr, rht_seed=W.llama_linear_seed(layer, idx))
-    plan = PT.gpu_plan(hq, P, snr, in_f)
-    s = hq.EncodedStream(plan, out_f)
-    xd = x.cuda()
-    hq.hq_encode(plan, xd, s)
-    y = hq.hq_decode(plan, s, out_dtype=torch.bfloat16)
-    torch.cuda.synchronize()
-    st = s.read_stats()
-    assert st["status"] == 0 and st["corrupt_substreams"] == 0, st
-    q = snr_db(xd, y)
-    rate = st["payload_bits"] / x.numel()
-    print(f"[fullsize] C3 {name} {lname}@{bps}: {rate:.4f} bits/scalar, SNR {q:.3f} dB", flush=True)
-    assert abs(q - snr) < 0.5 and abs(rate - bps) < 0.25
-    rng = np.random.default_rng(100 + idx + lat)
-    rows = np.sort(rng.choice(out_f, 16, replace=False))
-    check_sampled_rows(hq, plan, s, P, x, rows, f"C3 {name} {lname}@{bps}")
+    for idx, (name, out_f, in_f) in enumerate(W.LLAMA_LINEARS):
+        print(f"[fullsize] C3 layer {layer} {name} {out_f}x{in_f} {lname}@{bps}", flush=True)
+        xd = W.llama_linear(layer, idx, device="cuda")
+        P = PT.oracle_params(lat, snr, rht_seed=W.llama_linear_seed(layer, idx))
+        plan = PT.gpu_plan(hq, P, snr, in_f)
+        s = hq.EncodedStream(plan, out_f)
+        hq.hq_encode(plan, xd, s)
+        y = hq.hq_decode(plan, s, out_dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        st = s.read_stats()
+        assert st["status"] == 0 and st["corrupt_substreams"] == 0, st
+        q = snr_db(xd, y)
+        rate = st["payload_bits"] / xd.numel()
+        print(f"[fullsize] C3 {name} {lname}@{bps}: {rate:.4f} bits/scalar, SNR {q:.3f} dB", flush=True)
+        assert abs(q - snr) < 0.5 and abs(rate - bps) < 0.25
+        rng = np.random.default_rng(1000 * layer + 10 * idx + lat)
+        rows = np.sort(rng.choice(out_f, 8, replace=False))
+        x = torch.zeros((out_f, in_f), dtype=torch.bfloat16)
+        x[rows] = xd[torch.from_numpy(rows).cuda()].cpu()
+        check_sampled_rows(hq, plan, s, P, x, rows, f"C3 layer {layer} {name} {lname}@{bps}")
+        del xd, y, s
 
 
 @pytest.fixture(scope="module")
@@ -167,6 +171,68 @@ def test_c4_kv_cache_keys(hq, kv_keys, lat, bps):
     print(f"[fullsize] C4 {lname}: max |mean error| / standard error over 1024 queries "
           f"{z.abs().max().item():.2f}", flush=True)
     assert z.abs().max().item() < 5.0
+
+
+@pytest.mark.parametrize("lat,bps", [(O.E8, 2.0), (O.A2, 1.7), (O.Z, 1.7)])
+def test_c4_per_pair_unbiased(hq, kv_keys, lat, bps):
+    """Per (query, key) pair, over R = 64 dither seeds: the mean of
+    <q, k_hat> - <q, k> is zero (|t| > 4 no more often than a t distribution
+    with 63 degrees of freedom and some slack allow), and its variance is the
+    closed form of the subtractive-dither theorem (Sec. 3.4, Prop. on the
+    composed codec): sigma_Vor^2 |q|^2 (r_s / (alpha sqrt(n)))^2.  Control:
+    with the dither off the error is the same on every run (a fixed bias per
+    pair, not centred).  256 sampled keys (head 0 of each sampled row),
+    1024 queries."""
+    from paper_2606_23406_amd import workloads as W
+    lname = {O.E8: "E8", O.A2: "A2", O.Z: "Z"}[lat]
+    R, nk = 64, 256
+    rng = np.random.default_rng(300 + lat)
+    rows = np.sort(rng.choice(kv_keys.shape[0], nk, replace=False))
+    kfull = kv_keys[torch.from_numpy(rows)].contiguous().cuda()  # one row = 8 head vectors
+    k = kfull[:, :128]
+    qs = W.queries(device="cpu").cuda()  # [1024, 128]
+    snr = PT.op_snr(lname, bps)
+    print(f"[fullsize] C4 per-pair bias {lname}@{bps}: {nk} keys x {qs.shape[0]} queries, "
+          f"R = {R} dither seeds", flush=True)
+    exact = k.float() @ qs.t()
+
+    def run(seed, dither):
+        plan = hq.hq_plan(128, lat, 0.0, 71, -1, 1024, rotation=1, dither=dither, rot_seed=72,
+                          dither_seed=seed, norm_fp16=True, snr_db=snr)
+        s = hq.EncodedStream(plan, nk)
+        hq.hq_encode(plan, kfull, s)
+        y = hq.hq_decode(plan, s, out_dtype=torch.float32)[:, :128]
+        rs = s.norms[:nk * 8].float().reshape(nk, 8)[:, 0]
+        return y, rs, plan.info.alpha
+
+    acc = torch.zeros_like(exact, dtype=torch.float64)
+    acc2 = torch.zeros_like(acc)
+    for r in range(R):
+        y, rs, alpha = run(1000 + r, True)
+        e = (y @ qs.t() - exact).double()
+        acc += e
+        acc2 += e * e
+    torch.cuda.synchronize()
+    mean = acc / R
+    var = (acc2 - R * mean * mean) / (R - 1)
+    t = mean / torch.sqrt(var / R)
+    frac = (t.abs() > 4.0).double().mean().item()
+    qn2 = (qs.double() ** 2).sum(1)
+    pred = O.sigma2_vor(lat) * qn2[None, :] * (rs.double()[:, None] / (alpha * np.sqrt(128.0))) ** 2
+    ratio = (var / pred).mean().item()
+    print(f"[fullsize] C4 {lname}: fraction |t| > 4 = {frac:.2e}, mean var / closed form = {ratio:.4f}",
+          flush=True)
+    assert frac < 1e-3
+    assert abs(ratio - 1.0) < 0.05
+    # control: no dither -> the same error on every run, a fixed per-pair bias
+    y0, _, _ = run(5, False)
+    y1, _, _ = run(6, False)
+    assert torch.equal(y0, y1)
+    b = (y0 @ qs.t() - exact).double()
+    big = (b.abs() > 0.1 * torch.sqrt(pred)).double().mean().item()
+    print(f"[fullsize] C4 {lname} no dither: fraction of pairs with |bias| > 0.1 sd = {big:.3f}",
+          flush=True)
+    assert big > 0.8
 
 
 def test_c4_kv_cache_values_e8(hq):
