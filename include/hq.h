@@ -93,7 +93,8 @@ typedef struct {
  *             sub-stream, the better of the geometric optimum k* of Sec. 3.3
  *             and k* + 1 on the sub-stream's own symbols.
  *   cols      row length of every matrix encoded with this plan; a multiple of
- *             the tile and of the sub-stream length.
+ *             the tile and of the sub-stream length, at most 2^28
+ *             (HQ_ERR_UNSUPPORTED above).
  *   opt       nullable hq_options.
  * On success *out receives a plan (owned by the caller, free with
  * hq_plan_destroy) and *info (nullable) its derived values.  Plans are

@@ -242,7 +242,7 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   if (o.norm_dtype != 0 && o.norm_dtype != HQ_FP32 && o.norm_dtype != HQ_FP16)
     return HQ_ERR_INVALID_ARG;
   if (tile != HQ_TILE || S != HQ_SUB) return HQ_ERR_UNSUPPORTED;
-  if (cols > (int64_t)1 << 31) return HQ_ERR_UNSUPPORTED;
+  if (cols > (int64_t)1 << 28) return HQ_ERR_UNSUPPORTED;  // per-lane byte offsets stay 32-bit
 
   double snr;
   if (o.use_snr) {
@@ -410,6 +410,7 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
   a.lds_words = (uint32_t)p->max_words_sub;
   a.dither_seed = p->dither_seed;
   a.alpha = p->alpha;
+  a.alpha_half = 0.5f * p->alpha;
   // class sums stay below 2^26 (512 symbols of at most 2^17), so thresholds
   // past 2^30 are unreachable; the kernel compares in signed 32-bit
   for (int t = 0; t <= HQ_KMAX; ++t) {

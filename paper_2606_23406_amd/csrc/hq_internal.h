@@ -64,6 +64,7 @@ struct hq_encode_args {
   uint32_t lds_words;     // per-wave assembly buffer, in words
   uint64_t dither_seed;
   float alpha;
+  float alpha_half;       // alpha / 2, exact (the E8 decision works on z / 2)
   uint32_t thr0[HQ_KMAX + 1];
   uint32_t thr1[HQ_KMAX + 1];
 };

@@ -618,6 +618,11 @@ struct TwSigns {
 #pragma unroll
     for (int b = 0; b < 4; ++b) f[b] = ((lane >> b) & 1) ? -1.0f : 1.0f;
     sigma = (uint32_t)(__popc((uint32_t)lane & 15u) & 1) << 31;
+    // kept in registers for the whole kernel rather than recomputed from
+    // the lane index before every transform
+#pragma unroll
+    for (int b = 0; b < 4; ++b) asm volatile("" : "+v"(f[b]));
+    asm volatile("" : "+v"(sigma));
   }
 };
 
@@ -636,57 +641,64 @@ __device__ __forceinline__ float xor_sign(float v, uint32_t bit) {
 }
 
 // --------------------------------------------------- E8 decision in closed form
-// With ea_i = z_i - E_i (E_i the nearest even integer, exact in fp32) and the
-// odd candidate O_i = E_i + sgn(ea_i), |eb_i| = 1 - |ea_i|, so before the
-// parity fixes sum(ea^2) - sum(eb^2) = sum(2|ea_i| - 1); a fix moves one
-// coordinate to the next point of its class, adding 4 (1 - max|e|) to that
-// class's distance.  Hence
-//   da - db = 2 sum|ea_i| - 8 + [odd_a] 4 (1 - max|ea|) - [odd_b] 4 min|ea|.
-// Rounding moves the two fp32 tree sums by far less than kE8Tie, so a lane
-// outside the tie band takes the same coset as the two-sum comparison; a
-// wave with any lane inside the band runs quant_e8 step by step.
+// The decision works on w = z / 2 (the encoder's scale carries the factor
+// 1/2, which is exact), where the two classes of the 2E8 realization are the
+// integer points with even sum (D8 / 2) and that set shifted by 1/2.  With
+// k_i = rint(w_i), ea_i = w_i - k_i (exact, |ea_i| <= 1/2), the nearest
+// point of the shifted class takes floor(w_i) + 1/2 per coordinate, at
+// distance 1/2 - |ea_i|.  Before the parity fixes
+// sum(ea^2) - sum(eb^2) = sum(|ea_i| - 1/4); a fix moves one coordinate by 1,
+// adding 1 - 2 max|ea| (first class) or 2 min|ea| (second) to its distance.
+// In quarters of the full-scale difference:
+//   D = sum|ea_i| - 2 + [odd_a] (1 - 2 max|ea|) - [odd_b] 2 min|ea|,
+// odd_a the parity of sum k_i and odd_b that of sum floor(w_i), which differs
+// from odd_a by the number of negative ea_i (the parity of the XOR of their
+// sign bits).  Rounding moves the fp32 sums by far less than kE8Tie / 4, so
+// a lane outside the band takes the same class as the two-sum comparison; a
+// wave with any lane inside it runs quant_e8 step by step on z = 2 w.
 
-constexpr float kE8Tie = 1.0e-3f;
+constexpr float kE8Tie = 1.0e-3f;  // band on the full-scale distance difference
 
-// Stripped 2E8 symbols of one lane: h_i = (c_i - cb) / 2 with c the nearest
-// point and cb its coset bit.
-__device__ __forceinline__ void e8_nearest(const float* z, int32_t* h, int32_t& cb) {
-  float E[8], ea[8], t[8];
-  float SA = 0.0f, ST = 0.0f, Sabs = 0.0f, mx = 0.0f, mn = 2.0f;
+// Nearest 2E8 point of z = 2 w as x_i = c_i - cb = 2 h_i (c the point, cb its
+// coset bit; h the stripped coordinates of the strip table).
+__device__ __forceinline__ void e8_nearest(const float* w, int32_t* x, int32_t& cb) {
+  float ka[8], ea[8];
+  float SA = 0.0f, Sabs = 0.0f, mx = 0.0f, mn = 1.0f;
+  uint32_t sx = 0;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const float ka = __builtin_rintf(z[i] * 0.5f);
-    E[i] = ka * 2.0f;
-    ea[i] = z[i] - E[i];
-    t[i] = __builtin_copysignf(1.0f, ea[i]);
+    ka[i] = __builtin_rintf(w[i]);
+    ea[i] = w[i] - ka[i];
     const float a = __builtin_fabsf(ea[i]);
-    SA += ka;
-    ST += t[i];
+    SA += ka[i];
     Sabs += a;
     mx = __builtin_fmaxf(mx, a);
     mn = __builtin_fminf(mn, a);
+    sx ^= __float_as_uint(ea[i]);  // ea is never -0: w - rint(w) = +0 when equal
   }
-  // parities of sum(ka) and of sum(fb) = sum(ka) - #{ea < 0} = SA + ST/2 - 4
   const int32_t odd_a = (int32_t)SA & 1;
-  const int32_t odd_b = (int32_t)(SA + 0.5f * ST - 4.0f) & 1;
-  float D = 2.0f * Sabs - 8.0f;
-  if (odd_a) D += 4.0f - 4.0f * mx;
-  if (odd_b) D -= 4.0f * mn;
-  const bool tie = __builtin_fabsf(D) <= kE8Tie;
+  const int32_t odd_b = odd_a ^ (int32_t)(sx >> 31);
+  float D = Sabs - 2.0f;
+  if (odd_a) D += 1.0f - 2.0f * mx;
+  if (odd_b) D -= 2.0f * mn;
+  const bool tie = __builtin_fabsf(D) <= 0.25f * kE8Tie;
   if (__ballot(tie) != 0ull) {
+    float z[8];
     int32_t c[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[i] = w[i] + w[i];
     quant_e8(z, c);
     cb = c[0] & 1;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) h[i] = (c[i] - cb) >> 1;
+    for (int i = 0; i < 8; ++i) x[i] = c[i] - cb;
     return;
   }
   const bool even = D < 0.0f;
   float c[8], e[8], m = 0.0f;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    c[i] = even ? E[i] : E[i] + t[i];
-    e[i] = z[i] - c[i];  // ea exactly, or eb with the reference's single rounding
+    c[i] = even ? ka[i] : ka[i] + __builtin_copysignf(0.5f, ea[i]);
+    e[i] = w[i] - c[i];  // the full-scale error halved, with the same single rounding
     m = __builtin_fmaxf(m, __builtin_fabsf(e[i]));
   }
   // parity fix of the chosen class: its first coordinate of largest error
@@ -694,26 +706,27 @@ __device__ __forceinline__ void e8_nearest(const float* z, int32_t* h, int32_t& 
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const bool hit = !done && __builtin_fabsf(e[i]) == m;
-    c[i] = hit ? c[i] + __builtin_copysignf(2.0f, e[i]) : c[i];
+    c[i] = hit ? c[i] + __builtin_copysignf(1.0f, e[i]) : c[i];
     done = done || hit;
   }
   cb = even ? 0 : 1;
-  const float off = even ? 0.0f : -0.5f;
+  const float off = even ? 0.0f : -1.0f;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) h[i] = (int32_t)__builtin_fmaf(c[i], 0.5f, off);
+  for (int i = 0; i < 8; ++i) x[i] = (int32_t)__builtin_fmaf(c[i], 2.0f, off);
 }
 
-// E8 strip (Sec. 4.2) from h: s_i = zz(h_i) for i < 7, s_7 = 2 zz(t) + cb with
-// t = (h_7 - p) / 2 and p the parity of h_0 + .. + h_6.
-__device__ __forceinline__ void e8_strip(const int32_t* h, int32_t cb, uint32_t* s) {
+// E8 strip (Sec. 4.2) from x = 2 h: s_i = zz(h_i) for i < 7, s_7 = 2 zz(t) + cb
+// with t = (h_7 - p) / 2 and p the parity of h_0 + .. + h_6.  zz(h) =
+// x ^ (x >> 31) for x = 2 h.
+__device__ __forceinline__ void e8_strip(const int32_t* x, int32_t cb, uint32_t* s) {
   int32_t p = 0;
 #pragma unroll
   for (int i = 0; i < 7; ++i) {
-    p += h[i];
-    s[i] = zigzag(h[i]);
+    p += x[i];
+    s[i] = (uint32_t)(x[i] ^ (x[i] >> 31));
   }
-  const int32_t t = (h[7] - (p & 1)) >> 1;
-  s[7] = 2u * zigzag(t) + (uint32_t)cb;
+  const int32_t t2 = (x[7] - (p & 2)) >> 1;  // 2 t
+  s[7] = 2u * (uint32_t)(t2 ^ (t2 >> 31)) + (uint32_t)cb;
 }
 
 // ------------------------------------------------------------ encode kernel
@@ -745,24 +758,25 @@ struct LaneInput {
   uint4 a, b, sw;
 };
 
+// An inactive sub-stream (past the last row; its results are discarded) has
+// lrow = col0 = 0 and reads the first row, so no lane is zero-filled.
 template <int XT>
 __device__ __forceinline__ LaneInput load_lane_input(const hq_encode_args& A, const SubPos& P,
                                                      int lane) {
+  // uniform row base plus a 32-bit per-lane byte offset (columns < 2^28)
   LaneInput in;
-  in.a = make_uint4(0u, 0u, 0u, 0u);
-  in.b = make_uint4(0u, 0u, 0u, 0u);
-  in.sw = make_uint4(0u, 0u, 0u, 0u);
-  if (P.active) {
-    const uint32_t col = P.col0 + 8u * (uint32_t)lane;
-    if constexpr (XT == HQ_BF16) {
-      in.a = *(const uint4*)((const uint16_t*)A.x + (int64_t)P.lrow * A.ld + col);
-      in.sw = *(const uint4*)(A.dsign16 + (col >> 1));
-    } else {
-      const uint4* p = (const uint4*)((const float*)A.x + (int64_t)P.lrow * A.ld + col);
-      in.a = p[0];
-      in.b = p[1];
-      in.sw.x = sign_bits8(A.dmask, col);
-    }
+  const uint32_t col = P.col0 + 8u * (uint32_t)lane;
+  if constexpr (XT == HQ_BF16) {
+    const char* row = (const char*)((const uint16_t*)A.x + (int64_t)P.lrow * A.ld);
+    in.a = *(const uint4*)(row + (col << 1));
+    in.b = make_uint4(0u, 0u, 0u, 0u);
+    in.sw = *(const uint4*)((const char*)A.dsign16 + (col << 1));
+  } else {
+    const char* row = (const char*)((const float*)A.x + (int64_t)P.lrow * A.ld);
+    const uint4* p = (const uint4*)(row + (col << 2));
+    in.a = p[0];
+    in.b = p[1];
+    in.sw = make_uint4(sign_bits8(A.dmask, col), 0u, 0u, 0u);
   }
   return in;
 }
@@ -819,7 +833,8 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
     rs = (float)(_Float16)r;
     bad_tile = bad_tile || !(rs <= 65504.0f);
   }
-  const float scale = (rs == 0.0f || bad_tile) ? 0.0f : A.alpha / rs;
+  // E8 decides on z / 2: its scale is (alpha / 2) / r_s, exactly half of alpha / r_s
+  const float scale = (rs == 0.0f || bad_tile) ? 0.0f : (LAT == kE8 ? A.alpha_half : A.alpha) / rs;
   if (active && (lane & 15) == 0) {
     const int64_t t = grow * A.tpr + (col >> 7);
     if (fp16_norm) {
@@ -847,28 +862,28 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
     float u[8];
     dither8<LAT>(A.dither_seed, grow, col, u);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = x[i] + u[i];
+    for (int i = 0; i < 8; ++i) x[i] = x[i] + (LAT == kE8 ? 0.5f * u[i] : u[i]);
   }
 
   // ---- quantize + strip
   uint32_t sym[8];
   bool huge = false;
   if constexpr (LAT == kE8) {
-    int32_t h[8], cb;
-    e8_nearest(x, h, cb);
-    int32_t hmax = h[0], hmin = h[0];
+    int32_t h2[8], cb;  // 2 h = c - cb
+    e8_nearest(x, h2, cb);
+    int32_t hmax = h2[0], hmin = h2[0];
 #pragma unroll
     for (int i = 1; i < 8; ++i) {
-      hmax = max(hmax, h[i]);
-      hmin = min(hmin, h[i]);
+      hmax = max(hmax, h2[i]);
+      hmin = min(hmin, h2[i]);
     }
-    huge = hmax > 32768 - cb || hmin < -32768;  // some |c| = |2 h + cb| > 65536
+    huge = hmax > 65536 - 2 * cb || hmin < -65536;  // some |c| = |2 h + cb| > 65536
     if (huge || !active) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) h[i] = 0;
+      for (int i = 0; i < 8; ++i) h2[i] = 0;
       cb = 0;
     }
-    e8_strip(h, cb, sym);
+    e8_strip(h2, cb, sym);
   } else {
     int32_t c[8];
     quantize8<LAT>(x, c);
