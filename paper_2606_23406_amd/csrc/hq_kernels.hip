@@ -656,32 +656,72 @@ __device__ __forceinline__ float xor_sign(float v, uint32_t bit) {
 // sign bits).  Rounding moves the fp32 sums by far less than kE8Tie / 4, so
 // a lane outside the band takes the same class as the two-sum comparison; a
 // wave with any lane inside it runs quant_e8 step by step on z = 2 w.
+//
+// The chosen point, as h = (c - cb) / 2 (the stripped coordinates), is
+// k_i for the first class and floor(w_i) = k_i - [ea_i < 0] for the second,
+// plus the parity fix: +-1 on the first coordinate of largest error.  That
+// error is |ea_i| in the first class and fl(1/2 - |ea_i|) in the second
+// (fp32 w - (floor(w) + 1/2) has that magnitude with the reference's
+// rounding), and the fix moves towards w: +1 when ea_j >= 0 (first class),
+// +1 when ea_j < 0 (second; a coordinate with ea_j = +1/2 would move +1 too,
+// so min|ea| = 1/2 also takes the step-by-step path).  Every +-1 is a lane
+// mask folded into an add or subtract with carry.
 
 constexpr float kE8Tie = 1.0e-3f;  // band on the full-scale distance difference
 
-// Nearest 2E8 point of z = 2 w as x_i = c_i - cb = 2 h_i (c the point, cb its
-// coset bit; h the stripped coordinates of the strip table).
-__device__ __forceinline__ void e8_nearest(const float* w, int32_t* x, int32_t& cb) {
-  float ka[8], ea[8];
-  float SA = 0.0f, Sabs = 0.0f, mx = 0.0f, mn = 1.0f;
-  uint32_t sx = 0;
+// x + carry-in / x - borrow-in, the carry a lane mask (bit l for lane l).
+__device__ __forceinline__ int32_t add_lanemask(int32_t x, uint64_t m) {
+  int32_t r;
+  uint64_t co;
+  asm("v_addc_co_u32_e64 %0, %1, %2, 0, %3" : "=v"(r), "=s"(co) : "v"(x), "s"(m));
+  return r;
+}
+__device__ __forceinline__ int32_t sub_lanemask(int32_t x, uint64_t m) {
+  int32_t r;
+  uint64_t co;
+  asm("v_subb_co_u32_e64 %0, %1, %2, 0, %3" : "=v"(r), "=s"(co) : "v"(x), "s"(m));
+  return r;
+}
+
+// a ^ b ^ c in one instruction (gfx950 three-input bitwise op, truth table
+// 0x96 over S0 = 0xF0, S1 = 0xCC, S2 = 0xAA).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t r;
+  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+__device__ __forceinline__ void e8_nearest(const float* w, int32_t* h, int32_t& cb) {
+  float ea[8];
+  int32_t K[8];
+  uint32_t eb[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    ka[i] = __builtin_rintf(w[i]);
-    ea[i] = w[i] - ka[i];
-    const float a = __builtin_fabsf(ea[i]);
-    SA += ka[i];
-    Sabs += a;
-    mx = __builtin_fmaxf(mx, a);
-    mn = __builtin_fminf(mn, a);
-    sx ^= __float_as_uint(ea[i]);  // ea is never -0: w - rint(w) = +0 when equal
+    const float k = __builtin_rintf(w[i]);
+    ea[i] = w[i] - k;
+    K[i] = (int32_t)k;
+    eb[i] = __float_as_uint(ea[i]);  // ea is never -0: w - rint(w) = +0 when equal
   }
-  const int32_t odd_a = (int32_t)SA & 1;
-  const int32_t odd_b = odd_a ^ (int32_t)(sx >> 31);
-  float D = Sabs - 2.0f;
-  if (odd_a) D += 1.0f - 2.0f * mx;
-  if (odd_b) D -= 2.0f * mn;
-  const bool tie = __builtin_fabsf(D) <= 0.25f * kE8Tie;
+  float Sabs = __builtin_fabsf(ea[0]) + __builtin_fabsf(ea[1]);
+#pragma unroll
+  for (int i = 2; i < 8; ++i) Sabs += __builtin_fabsf(ea[i]);
+  float mx = __builtin_fabsf(ea[0]), mn = mx;
+#pragma unroll
+  for (int i = 1; i < 8; ++i) {
+    mx = __builtin_fmaxf(mx, __builtin_fabsf(ea[i]));
+    mn = __builtin_fminf(mn, __builtin_fabsf(ea[i]));
+  }
+  // parities: sum k_i (low bits of the XOR) and the count of negative ea_i
+  const uint32_t kp = xor3(xor3(xor3((uint32_t)K[0], (uint32_t)K[1], (uint32_t)K[2]), (uint32_t)K[3],
+                                (uint32_t)K[4]),
+                           (uint32_t)K[5], (uint32_t)K[6]) ^ (uint32_t)K[7];
+  const uint32_t sx = xor3(xor3(xor3(eb[0], eb[1], eb[2]), eb[3], eb[4]), eb[5], eb[6]) ^ eb[7];
+  const bool odd_a = kp & 1u;
+  const bool odd_b = ((kp << 31) ^ sx) >> 31;
+  const float D0 = Sabs - 2.0f;
+  const float D1 = odd_a ? __builtin_fmaf(-2.0f, mx, Sabs - 1.0f) : D0;
+  const float D = odd_b ? __builtin_fmaf(-2.0f, mn, D1) : D1;
+  const bool tie = __builtin_fabsf(D) <= 0.25f * kE8Tie || mn >= 0.5f;
   if (__ballot(tie) != 0ull) {
     float z[8];
     int32_t c[8];
@@ -690,43 +730,40 @@ __device__ __forceinline__ void e8_nearest(const float* w, int32_t* x, int32_t& 
     quant_e8(z, c);
     cb = c[0] & 1;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = c[i] - cb;
+    for (int i = 0; i < 8; ++i) h[i] = (c[i] - cb) >> 1;
     return;
   }
+  // lane masks: the class, whether its parity needs the fix, and per
+  // coordinate the largest-error hits and the sign of ea
   const bool even = D < 0.0f;
-  float c[8], e[8], m = 0.0f;
+  const uint64_t E = __ballot(even);
+  const uint64_t need = (E & __ballot(odd_a)) | (~E & __ballot(odd_b));
+  const float mb = 0.5f - mn;
+  uint64_t done = ~need;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    c[i] = even ? ka[i] : ka[i] + __builtin_copysignf(0.5f, ea[i]);
-    e[i] = w[i] - c[i];  // the full-scale error halved, with the same single rounding
-    m = __builtin_fmaxf(m, __builtin_fabsf(e[i]));
-  }
-  // parity fix of the chosen class: its first coordinate of largest error
-  bool done = !(even ? odd_a : odd_b);
-#pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const bool hit = !done && __builtin_fabsf(e[i]) == m;
-    c[i] = hit ? c[i] + __builtin_copysignf(1.0f, e[i]) : c[i];
-    done = done || hit;
+    const float a = __builtin_fabsf(ea[i]);
+    const uint64_t hit = (E & __ballot(a == mx)) | (~E & __ballot(0.5f - a == mb));
+    const uint64_t fix = hit & ~done;
+    done |= hit;
+    const uint64_t neg = __ballot(ea[i] < 0.0f);
+    const uint64_t up = E & fix & ~neg;
+    const uint64_t down = (E & fix & neg) | (~E & (neg ^ fix));
+    h[i] = sub_lanemask(add_lanemask(K[i], up), down);
   }
   cb = even ? 0 : 1;
-  const float off = even ? 0.0f : -1.0f;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) x[i] = (int32_t)__builtin_fmaf(c[i], 2.0f, off);
 }
 
-// E8 strip (Sec. 4.2) from x = 2 h: s_i = zz(h_i) for i < 7, s_7 = 2 zz(t) + cb
-// with t = (h_7 - p) / 2 and p the parity of h_0 + .. + h_6.  zz(h) =
-// x ^ (x >> 31) for x = 2 h.
-__device__ __forceinline__ void e8_strip(const int32_t* x, int32_t cb, uint32_t* s) {
-  int32_t p = 0;
+// E8 strip (Sec. 4.6) from h = (c - cb) / 2: s_i = zz(h_i) for i < 7,
+// s_7 = 2 zz(t) + cb with t = (h_7 - p) / 2 and p the parity of
+// h_0 + .. + h_6.
+__device__ __forceinline__ void e8_strip(const int32_t* h, int32_t cb, uint32_t* s) {
 #pragma unroll
-  for (int i = 0; i < 7; ++i) {
-    p += x[i];
-    s[i] = (uint32_t)(x[i] ^ (x[i] >> 31));
-  }
-  const int32_t t2 = (x[7] - (p & 2)) >> 1;  // 2 t
-  s[7] = 2u * (uint32_t)(t2 ^ (t2 >> 31)) + (uint32_t)cb;
+  for (int i = 0; i < 7; ++i) s[i] = zigzag(h[i]);
+  const uint32_t p = xor3(xor3((uint32_t)h[0], (uint32_t)h[1], (uint32_t)h[2]), (uint32_t)h[3],
+                          (uint32_t)h[4]) ^ (uint32_t)h[5] ^ (uint32_t)h[6];
+  const int32_t t = (h[7] - (int32_t)(p & 1u)) >> 1;
+  s[7] = 2u * zigzag(t) + (uint32_t)cb;
 }
 
 // ------------------------------------------------------------ encode kernel
@@ -788,20 +825,12 @@ __device__ __forceinline__ void or_word(uint32_t* buf, uint32_t pos, uint32_t v)
   atomicOr(&buf[(pos >> 5) + 1], (uint32_t)(t >> 32));
 }
 
-template <int LAT, int XT, bool KV>
-__device__ __forceinline__ void encode_substream(const hq_encode_args& A, const SubPos& P,
-                                                 int lane, const TwSigns& sg, const LaneInput& in,
-                                                 uint32_t* buf, uint32_t& W_out, uint32_t& kb_out,
-                                                 uint32_t& bits_out, bool& overflow_out) {
-  const bool active = P.active;  // wave-uniform
-  const uint32_t col = P.col0 + 8u * (uint32_t)lane;  // tile lane/16, coordinates 8 (lane % 16) + j
-  const int64_t grow = A.first_row + P.lrow;
-  const bool use_rot = KV && A.rotation;
-  const bool use_dither = KV && A.dither;
-  const bool fp16_norm = KV && A.norm_fp16;
-
-  // ---- the 8 scalars with the RHT signs D applied (|x| is unchanged)
-  float x[8];
+// Front end of one sub-stream: the lane's 8 scalars with the RHT signs D
+// applied, the tile's sum of squares (a pairwise tree in index order: the
+// lane butterflies 1, 2, 4, 8 add the same pairs in the same order), and
+// x <- sigma H D x.
+template <int XT>
+__device__ __forceinline__ float encode_front(const LaneInput& in, const TwSigns& sg, float* x) {
   if constexpr (XT == HQ_BF16) {
     const uint32_t w4[4] = {in.a.x ^ in.sw.x, in.a.y ^ in.sw.y, in.a.z ^ in.sw.z,
                             in.a.w ^ in.sw.w};
@@ -815,9 +844,6 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = flip(__uint_as_float(w8[i]), in.sw.x, i);
   }
-
-  // ---- Normalize: tile norm as a pairwise tree in index order (the lane
-  //      butterflies 1, 2, 4, 8 add the same pairs in the same order)
   float sq[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) sq[i] = x[i] * x[i];
@@ -826,31 +852,28 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   ss = ss + dpp_xor<2>(ss);
   ss = ss + swz_xor4(ss);
   ss = ss + dpp_xor<8>(ss);
-  const float r = __builtin_sqrtf(ss);
-  float rs = r;
-  bool bad_tile = !(r <= 3.0e38f);  // non-finite input
-  if (fp16_norm) {
-    rs = (float)(_Float16)r;
-    bad_tile = bad_tile || !(rs <= 65504.0f);
-  }
-  // E8 decides on z / 2: its scale is (alpha / 2) / r_s, exactly half of alpha / r_s
-  const float scale = (rs == 0.0f || bad_tile) ? 0.0f : (LAT == kE8 ? A.alpha_half : A.alpha) / rs;
-  if (active && (lane & 15) == 0) {
-    const int64_t t = grow * A.tpr + (col >> 7);
-    if (fp16_norm) {
-      ((_Float16*)A.norms)[t] = (_Float16)r;
-    } else {
-      ((float*)A.norms)[t] = r;
-    }
-    if (bad_tile && A.stats) {
-      atomicAdd(&A.stats->overflow_tiles, 1u);
-      atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_OVERFLOW);
-    }
-  }
-
-  // ---- RHT: v = sigma H D x, then z = v * (sigma alpha / r)
   fwht128_tw(x, sg);
-  const float scale_tw = xor_sign(scale, sg.sigma);
+  return ss;
+}
+
+// Value of lane (l & ~3) | I for every lane l (a quad broadcast).
+template <int I>
+__device__ __forceinline__ float quad_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), I * 0x55, 0xF, 0xF, true));
+}
+
+template <int LAT, int XT, bool KV>
+__device__ __forceinline__ void encode_substream(const hq_encode_args& A, const SubPos& P,
+                                                 int lane, float* x, float scale_tw,
+                                                 uint32_t* buf, uint32_t& W_out, uint32_t& kb_out,
+                                                 uint32_t& bits_out, bool& overflow_out) {
+  const bool active = P.active;  // wave-uniform
+  const uint32_t col = P.col0 + 8u * (uint32_t)lane;  // tile lane/16, coordinates 8 (lane % 16) + j
+  const int64_t grow = A.first_row + P.lrow;
+  const bool use_rot = KV && A.rotation;
+  const bool use_dither = KV && A.dither;
+
+  // ---- z = (sigma H D x) * (sigma alpha / r): the scale carries the sign sigma
 #pragma unroll
   for (int i = 0; i < 8; ++i) x[i] = x[i] * scale_tw;
   if (use_rot) {
@@ -869,21 +892,9 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   uint32_t sym[8];
   bool huge = false;
   if constexpr (LAT == kE8) {
-    int32_t h2[8], cb;  // 2 h = c - cb
-    e8_nearest(x, h2, cb);
-    int32_t hmax = h2[0], hmin = h2[0];
-#pragma unroll
-    for (int i = 1; i < 8; ++i) {
-      hmax = max(hmax, h2[i]);
-      hmin = min(hmin, h2[i]);
-    }
-    huge = hmax > 65536 - 2 * cb || hmin < -65536;  // some |c| = |2 h + cb| > 65536
-    if (huge || !active) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) h2[i] = 0;
-      cb = 0;
-    }
-    e8_strip(h2, cb, sym);
+    int32_t h[8], cb;  // c = 2 h + cb
+    e8_nearest(x, h, cb);  // an inactive sub-stream's symbols are never written
+    e8_strip(h, cb, sym);
   } else {
     int32_t c[8];
     quantize8<LAT>(x, c);
@@ -1092,19 +1103,63 @@ __global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_kernel(hq_encode_
       }
     }
   }
-  // ---- encode this group's sub-streams into LDS; the next sub-stream's
-  //      input is loaded while the current one is encoded
-  LaneInput in = load_lane_input<XT>(A, pos[0], lane);
+  // ---- front ends of the wave's four sub-streams: every input load is
+  //      issued first, then sign flips, tile sums of squares and transforms
+  static_assert(HQ_ENC_SUBS_PER_WAVE == 4, "one sub-stream per lane of a quad");
+  LaneInput in[HQ_ENC_SUBS_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) in[i] = load_lane_input<XT>(A, pos[i], lane);
+  float x[HQ_ENC_SUBS_PER_WAVE][8], ss[HQ_ENC_SUBS_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) ss[i] = encode_front<XT>(in[i], sg, x[i]);
+
+  // ---- tile norms and scales, once for the wave's 16 tiles: lane l takes
+  //      sub-stream i = l & 3, tile t = l >> 4 (each tile's 16 lanes hold its
+  //      sum of squares, so the merged value repeats in every quad)
+  {
+    const int qi = lane & 3;
+    const float ssm = qi == 0 ? ss[0] : (qi == 1 ? ss[1] : (qi == 2 ? ss[2] : ss[3]));
+    const bool fp16_norm = KV && A.norm_fp16;
+    const float r = __builtin_sqrtf(ssm);
+    float rs = r;
+    bool bad_tile = !(r <= 3.0e38f);  // non-finite input
+    if (fp16_norm) {
+      rs = (float)(_Float16)r;
+      bad_tile = bad_tile || !(rs <= 65504.0f);
+    }
+    // E8 decides on z / 2: its scale is (alpha / 2) / r_s, exactly half of alpha / r_s
+    const float scale =
+        (rs == 0.0f || bad_tile) ? 0.0f : (LAT == kE8 ? A.alpha_half : A.alpha) / rs;
+    const uint32_t sub_l = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)(qi * HQ_ENC_WAVES + wave);
+    if (((lane >> 2) & 3) == 0 && sub_l < (uint32_t)A.nsub) {
+      // tile (lane >> 4) of sub-stream sub_l: 4 tiles per sub-stream, rows contiguous
+      const int64_t t = A.first_row * A.tpr + 4 * (int64_t)sub_l + (lane >> 4);
+      if (fp16_norm) {
+        ((_Float16*)A.norms)[t] = (_Float16)r;
+      } else {
+        ((float*)A.norms)[t] = r;
+      }
+      if (bad_tile && A.stats) {
+        atomicAdd(&A.stats->overflow_tiles, 1u);
+        atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_OVERFLOW);
+      }
+    }
+    ss[0] = quad_bcast<0>(scale);
+    ss[1] = quad_bcast<1>(scale);
+    ss[2] = quad_bcast<2>(scale);
+    ss[3] = quad_bcast<3>(scale);
+  }
+
+  // ---- quantize and Rice-code each sub-stream into its LDS buffer
   uint32_t padsum = 0;
 #pragma unroll
   for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
     const int li = i * HQ_ENC_WAVES + wave;  // neighbouring waves take neighbouring sub-streams
     const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
-    LaneInput next;
-    if (i + 1 < HQ_ENC_SUBS_PER_WAVE) next = load_lane_input<XT>(A, pos[i + 1], lane);
     uint32_t W, kb, bits;
     bool ovf;
-    encode_substream<LAT, XT, KV>(A, pos[i], lane, sg, in, smem + li * stride, W, kb, bits, ovf);
+    encode_substream<LAT, XT, KV>(A, pos[i], lane, x[i], xor_sign(ss[i], sg.sigma),
+                                  smem + li * stride, W, kb, bits, ovf);
     if (pos[i].active) {
       if (lane == 0) {
         A.kparam[A.first_sub + sub] = (uint8_t)kb;
@@ -1115,7 +1170,6 @@ __global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_kernel(hq_encode_
     } else if (lane == 0) {
       s_words[li] = 0;
     }
-    if (i + 1 < HQ_ENC_SUBS_PER_WAVE) in = next;
   }
   if (lane == 0) {
     s_pad[wave] = padsum;
