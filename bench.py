@@ -43,6 +43,8 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemm", action="store_true")
     ap.add_argument("--no-other", action="store_true", help="skip the C1, C2, C3-D4 and C4 measurements")
+    ap.add_argument("--group", type=int, default=7,
+                    help="matrices per encode/decode launch (hq_encode_group); 1 = one launch each")
     return ap.parse_args()
 
 
@@ -60,14 +62,27 @@ def build_workload(H, W, layers, bps, dev, snr=None):
     return mats
 
 
-def encode_all(H, mats):
-    for m in mats:
-        H.hq_encode(m["plan"], m["x"], m["s"])
+def groups_of(mats, size):
+    """The stack in launch groups: one layer's seven matrices per group."""
+    return [mats[i:i + size] for i in range(0, len(mats), size)]
 
 
-def decode_all(H, mats):
-    for m in mats:
-        H.hq_decode(m["plan"], m["s"], out=m["y"])
+def encode_all(H, mats, group=7):
+    if group <= 1:
+        for m in mats:
+            H.hq_encode(m["plan"], m["x"], m["s"])
+        return
+    for g in groups_of(mats, group):
+        H.hq_encode_group([m["plan"] for m in g], [m["x"] for m in g], [m["s"] for m in g])
+
+
+def decode_all(H, mats, group=7):
+    if group <= 1:
+        for m in mats:
+            H.hq_decode(m["plan"], m["s"], out=m["y"])
+        return
+    for g in groups_of(mats, group):
+        H.hq_decode_group([m["plan"] for m in g], [m["s"] for m in g], [m["y"] for m in g])
 
 
 def cpu_baseline(mats, seconds):
@@ -353,8 +368,8 @@ def main():
     torch.cuda.synchronize()
 
     for _ in range(args.warmup):
-        encode_all(H, mats)
-        decode_all(H, mats)
+        encode_all(H, mats, args.group)
+        decode_all(H, mats, args.group)
     for m in mats:
         m["s"].reset_stats()
     torch.cuda.synchronize()
@@ -367,9 +382,9 @@ def main():
     for k in range(args.steps):
         a, b, c = ev[k]
         a.record(stream)
-        encode_all(H, mats)
+        encode_all(H, mats, args.group)
         b.record(stream)
-        decode_all(H, mats)
+        decode_all(H, mats, args.group)
         c.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -389,8 +404,9 @@ def main():
     dec_gbs = dec_bytes / t_dec / 1e9
 
     copy_gbs = copy_bandwidth(dev)
-    alg_enc_launch = enc_bytes / len(mats)
-    alg_dec_launch = dec_bytes / len(mats)
+    launches = len(groups_of(mats, args.group)) if args.group > 1 else len(mats)
+    alg_enc_launch = enc_bytes / launches
+    alg_dec_launch = dec_bytes / launches
     tr_enc = measured_traffic("encode")
     tr_dec = measured_traffic("decode")
     out = {
@@ -418,12 +434,13 @@ def main():
                      "traffic": None if tr_enc is None else round(tr_enc),
                      "algorithmic_bytes_per_launch": round(alg_enc_launch),
                      "algorithmic_bytes_per_scalar": round(enc_bytes / n_scalars, 4),
-                     "launches_per_step": len(mats)},
+                     "launches_per_step": launches},
         "decode_roofline": {"bound": "hbm", "kernel": "hq_decode_kernel (E8, bf16 out)",
                             "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
                             "traffic": None if tr_dec is None else round(tr_dec),
                             "algorithmic_bytes_per_launch": round(alg_dec_launch),
+                            "launches_per_step": launches,
                             "algorithmic_bytes_per_scalar": round(dec_bytes / n_scalars, 4)},
         "copy_GBs_device": copy_gbs,
         "encode_ms": round(t_enc * 1e3, 4),

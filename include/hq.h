@@ -167,6 +167,24 @@ size_t hq_scan_bytes(hq_plan_t plan, int64_t rows);
 hq_status hq_encode(hq_plan_t plan, const void* x, int32_t xt, int64_t rows, int64_t ld,
                     hq_stream* s, int32_t append, void* stream);
 
+/* hq_encode_group -- hq_encode (append = 0) of `count` matrices in as few
+ * launches as possible (up to 8 per launch): member i encodes rows[i] rows of
+ * x[i] (element type xt, row stride ld[i]) with plans[i] into s[i], exactly
+ * as hq_encode would, bit for bit.  Whole-model quantization (Sec. 6.1 codes
+ * every linear layer) calls it on a layer's matrices at once, so the small
+ * ones share the machine instead of each filling only part of it.
+ *   plans   host array of count plans; all of one lattice, tile, sub-stream
+ *           length and variant (rotation / dither / fp16 norms on or off
+ *           together); seeds, columns and rates may differ.
+ *   s       host array of count distinct streams, each with its own scan
+ *           scratch.
+ * Errors: as hq_encode, plus HQ_ERR_INVALID_ARG for mixed plans or a stream
+ * (or scan scratch) given twice.  Members before a failing one may already
+ * have been launched. */
+hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t xt,
+                          const int64_t* rows, const int64_t* ld, hq_stream* const* s,
+                          int32_t count, void* stream);
+
 /* hq_decode -- the decode path of Fig. 1, including the explicit inverse RHT,
  * for rows row0 .. row0+rows-1 of s into y (device, element type yt =
  * HQ_BF16 or HQ_FP32, row stride ld).  A sub-stream whose offsets or bits are
@@ -174,6 +192,15 @@ hq_status hq_encode(hq_plan_t plan, const void* x, int32_t xt, int64_t rows, int
  * bounds).  Errors: HQ_ERR_INVALID_ARG, HQ_ERR_HIP. */
 hq_status hq_decode(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows, void* y,
                     int32_t yt, int64_t ld, void* stream);
+
+/* hq_decode_group -- hq_decode of all rows of `count` streams in as few
+ * launches as possible (up to 8 per launch): member i decodes s[i] (all
+ * s[i]->rows rows) with plans[i] into y[i] (device, element type yt, row
+ * stride ld[i]), with the same results as hq_decode.  Plans as for
+ * hq_encode_group.  Errors: as hq_decode, plus HQ_ERR_INVALID_ARG for mixed
+ * plans. */
+hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, void* const* y,
+                          int32_t yt, const int64_t* ld, int32_t count, void* stream);
 
 /* hq_decode_int8 -- Rice decode and unstrip without the inverse RHT (Sec. 4.8
  * Cast): the int8 lattice codes c (device, rows x cols, row stride ldc) and

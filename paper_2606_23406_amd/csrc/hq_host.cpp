@@ -125,12 +125,18 @@ void class_counts(int lat, int S, int64_t* n0, int64_t* n1) {
 // 2 |coordinate| + 2, so a class sums to M <= T (2 sqrt(n) |c| + 2 n).  A
 // class with parameter k costs count (1 + k) + sum / 2^k bits, and the
 // encoder's k never costs more than the geometric k* of that sum.
+// Bound on the norm of one tile's lattice code (hence on every |c_i|).
+double code_norm_bound(const hq_plan_s& p) {
+  const int n = p.tile, m = p.dim;
+  const double fac = p.norm_fp16 ? 1.5 : 1.0;
+  return fac * (double)p.alpha * std::sqrt((double)n) * 1.001 +
+         lattice_rho(p.lattice) * std::sqrt((double)n / m) * (p.dither ? 2.0 : 1.0);
+}
+
 int64_t substream_word_bound(const hq_plan_s& p) {
   const int n = p.tile, m = p.dim, S = p.substream;
   const double T = (double)S / n;
-  const double fac = p.norm_fp16 ? 1.5 : 1.0;
-  const double cn = fac * (double)p.alpha * std::sqrt((double)n) * 1.001 +
-                    lattice_rho(p.lattice) * std::sqrt((double)n / m) * (p.dither ? 2.0 : 1.0);
+  const double cn = code_norm_bound(p);
   const double M = T * (2.0 * std::sqrt((double)n) * cn + 2.0 * n);
   const int64_t Mi = (int64_t)std::ceil(M) + 1;
   int64_t n0, n1;
@@ -277,6 +283,7 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   kstar_thresholds(n0, p->thr[0]);
   if (n1) kstar_thresholds(n1, p->thr[1]); else kstar_thresholds(1, p->thr[1]);
   p->max_words_sub = substream_word_bound(*p);
+  p->codes_int8 = (!p->dither && lattice != HQ_A2 && code_norm_bound(*p) <= 127.0) ? 1 : 0;
   if (p->max_words_sub > 8192) {
     delete p;
     return HQ_ERR_UNSUPPORTED;
@@ -353,8 +360,13 @@ size_t hq_scan_bytes(hq_plan_t p, int64_t rows) {
          2 * sizeof(unsigned long long) * (size_t)std::max<int64_t>(nwg, 1);
 }
 
-hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_t ld,
-                    hq_stream* s, int32_t append, void* stream) {
+// Validates one encode and fills its kernel arguments.  Returns HQ_OK with
+// *nwg = 0 when there is nothing to launch (rows == 0; the stream is then
+// already up to date).
+static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_t ld,
+                                hq_stream* s, int32_t append, hq_encode_args* out, int64_t* nwg_out,
+                                void* stream) {
+  *nwg_out = 0;
   if (!p || !s || rows < 0) return HQ_ERR_INVALID_ARG;
   if (xt != HQ_BF16 && xt != HQ_FP32) return HQ_ERR_INVALID_ARG;
   if (!s->payload || !s->offsets || !s->kparam || !s->norms || !s->scan) return HQ_ERR_INVALID_ARG;
@@ -380,7 +392,7 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
   if (nwg > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
   if ((size_t)s->scan_bytes < hq_scan_bytes(p, rows)) return HQ_ERR_CAPACITY;
 
-  hq_encode_args a;
+  hq_encode_args& a = *out;
   std::memset(&a, 0, sizeof(a));
   a.x = x;
   a.ld = ld;
@@ -417,9 +429,59 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
     a.thr0[t] = std::min<uint32_t>(p->thr[0][t], 1u << 30);
     a.thr1[t] = std::min<uint32_t>(p->thr[1][t], 1u << 30);
   }
-  const int e = hq_launch_encode(p, a, xt, stream);
-  if (e) return HQ_ERR_HIP;
-  s->rows = row0 + rows;
+  *nwg_out = nwg;
+  return HQ_OK;
+}
+
+hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_t ld,
+                    hq_stream* s, int32_t append, void* stream) {
+  hq_encode_args a;
+  int64_t nwg;
+  const hq_status st = encode_prepare(p, x, xt, rows, ld, s, append, &a, &nwg, stream);
+  if (st != HQ_OK || nwg == 0) return st;
+  if (hq_launch_encode(p, a, xt, stream)) return HQ_ERR_HIP;
+  s->rows = a.first_row + rows;
+  return HQ_OK;
+}
+
+static bool same_kernel_family(const hq_plan_s* a, const hq_plan_s* b) {
+  const bool kva = a->rotation || a->dither || a->norm_fp16;
+  const bool kvb = b->rotation || b->dither || b->norm_fp16;
+  return a->lattice == b->lattice && kva == kvb && a->tile == b->tile && a->substream == b->substream;
+}
+
+hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t xt,
+                          const int64_t* rows, const int64_t* ld, hq_stream* const* s,
+                          int32_t count, void* stream) {
+  if (count < 0 || (count > 0 && (!plans || !x || !rows || !ld || !s))) return HQ_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < count; ++i) {
+    if (!plans[i] || !s[i] || !same_kernel_family(plans[0], plans[i])) return HQ_ERR_INVALID_ARG;
+    for (int32_t j = 0; j < i; ++j)
+      if (s[j] == s[i] || s[j]->scan == s[i]->scan) return HQ_ERR_INVALID_ARG;
+  }
+  for (int32_t b = 0; b < count; b += HQ_GROUP_MAX) {
+    hq_encode_group_args g;
+    std::memset(&g, 0, sizeof(g));
+    int64_t total = 0;
+    uint32_t lds_words = 0;
+    int32_t members[HQ_GROUP_MAX];
+    for (int32_t i = b; i < std::min(count, b + HQ_GROUP_MAX); ++i) {
+      int64_t nwg;
+      const hq_status st =
+          encode_prepare(plans[i], x[i], xt, rows[i], ld[i], s[i], 0, &g.m[g.count], &nwg, stream);
+      if (st != HQ_OK) return st;
+      if (nwg == 0) continue;
+      g.wg_begin[g.count] = (uint32_t)total;
+      lds_words = std::max(lds_words, g.m[g.count].lds_words);
+      members[g.count++] = i;
+      total += nwg;
+    }
+    if (g.count == 0) continue;
+    if (total > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
+    if (hq_launch_encode_group(plans[members[0]], g, (uint32_t)total, lds_words, xt, stream))
+      return HQ_ERR_HIP;
+    for (int32_t k = 0; k < g.count; ++k) s[members[k]]->rows = rows[members[k]];
+  }
   return HQ_OK;
 }
 
@@ -464,6 +526,46 @@ hq_status hq_decode(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
   a.y = y;
   a.ld = ld;
   return hip_status(hq_launch_decode(p, a, yt, stream));
+}
+
+hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, void* const* y,
+                          int32_t yt, const int64_t* ld, int32_t count, void* stream) {
+  if (count < 0 || (count > 0 && (!plans || !s || !y || !ld))) return HQ_ERR_INVALID_ARG;
+  if (yt != HQ_BF16 && yt != HQ_FP32) return HQ_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < count; ++i)
+    if (!plans[i] || !s[i] || !same_kernel_family(plans[0], plans[i])) return HQ_ERR_INVALID_ARG;
+  const int64_t esz = (yt == HQ_BF16) ? 2 : 4;
+  for (int32_t b = 0; b < count; b += HQ_GROUP_MAX) {
+    hq_decode_group_args g;
+    std::memset(&g, 0, sizeof(g));
+    int64_t total = 0;
+    uint32_t lds_words = 0;
+    bool mx = true;
+    int32_t first = -1;
+    for (int32_t i = b; i < std::min(count, b + HQ_GROUP_MAX); ++i) {
+      const hq_plan_s* p = plans[i];
+      const int64_t rows = s[i]->rows;
+      if (rows == 0) continue;
+      if (!y[i] || ld[i] < p->cols || !s[i]->payload || !s[i]->offsets || !s[i]->kparam ||
+          !s[i]->norms || !aligned16(y[i]) || (ld[i] * esz) % 16 != 0)
+        return HQ_ERR_INVALID_ARG;
+      hq_decode_args& a = g.m[g.count];
+      fill_decode_args(p, s[i], 0, rows, &a);
+      a.y = y[i];
+      a.ld = ld[i];
+      g.wg_begin[g.count] = (uint32_t)total;
+      total += hq_decode_workgroups(a.nsub);
+      lds_words = std::max(lds_words, a.lds_words);
+      mx = mx && p->codes_int8;
+      if (first < 0) first = i;
+      ++g.count;
+    }
+    if (g.count == 0) continue;
+    if (total > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
+    if (hq_launch_decode_group(plans[first], g, (uint32_t)total, lds_words, yt, mx, stream))
+      return HQ_ERR_HIP;
+  }
+  return HQ_OK;
 }
 
 hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,

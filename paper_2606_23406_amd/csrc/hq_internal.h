@@ -29,6 +29,8 @@ struct hq_plan_s {
   // k0 = #{t in 1..KMAX : sum >= thr[c][t]} (thr[c][0] unused).
   uint32_t thr[2][HQ_KMAX + 1];
   int64_t max_words_sub;   // capacity bound of one sub-stream, in 32-bit words
+  int32_t codes_int8;      // every lattice code is bounded by 127 (and no dither):
+                           // the decoder's inverse transform is an int8 contraction
   uint32_t* d_dmask;       // device: RHT sign bit per global column (1 = -1)
   uint32_t* d_dsign16;     // device: per column pair, the RHT signs as bf16 sign
                            // bits (bit 15: even column, bit 31: odd column)
@@ -93,6 +95,20 @@ struct hq_decode_args {
   float alpha_n;           // alpha * tile, exact
 };
 
+// Several matrices in one launch (kernel arguments, by value): member i owns
+// workgroups wg_begin[i] .. wg_begin[i + 1] - 1 (the last one to the grid end).
+#define HQ_GROUP_MAX 8
+struct hq_encode_group_args {
+  hq_encode_args m[HQ_GROUP_MAX];
+  uint32_t wg_begin[HQ_GROUP_MAX];
+  int32_t count;
+};
+struct hq_decode_group_args {
+  hq_decode_args m[HQ_GROUP_MAX];
+  uint32_t wg_begin[HQ_GROUP_MAX];
+  int32_t count;
+};
+
 struct hq_actprep_args {
   const void* a;
   int64_t lda;
@@ -115,6 +131,11 @@ struct hq_gemm_args {
 // Kernel launchers (hq_kernels.hip); return a hipError_t as int.
 int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, int xt, void* stream);
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream);
+int hq_launch_encode_group(const hq_plan_s* p, const hq_encode_group_args& g, uint32_t nwg,
+                           uint32_t lds_words, int xt, void* stream);
+int hq_launch_decode_group(const hq_plan_s* p, const hq_decode_group_args& g, uint32_t nwg,
+                           uint32_t lds_words, int yt, bool mx, void* stream);
+uint32_t hq_decode_workgroups(int64_t nsub);
 int hq_launch_decode_int8(const hq_plan_s* p, const hq_decode_args& a, void* stream);
 int hq_launch_act_prep(const hq_actprep_args& a, void* stream);
 int hq_launch_gemm(const hq_gemm_args& a, void* stream);

@@ -83,6 +83,10 @@ def lib():
     L.hq_encode.argtypes = [p, p, i32, i64, i64, p, i32, p]
     L.hq_decode.restype = i32
     L.hq_decode.argtypes = [p, p, i64, i64, p, i32, i64, p]
+    L.hq_encode_group.restype = i32
+    L.hq_encode_group.argtypes = [p, p, i32, p, p, p, i32, p]
+    L.hq_decode_group.restype = i32
+    L.hq_decode_group.argtypes = [p, p, p, i32, p, i32, p]
     L.hq_decode_int8.restype = i32
     L.hq_decode_int8.argtypes = [p, p, i64, i64, p, i64, p, p]
     L.hq_act_prep.restype = i32
@@ -219,6 +223,41 @@ def hq_decode(plan: Plan, s: EncodedStream, row0=0, rows=None, out_dtype=torch.b
     return out
 
 
+def hq_encode_group(plans, xs, streams, stream=None):
+    """hq_encode_group: encode xs[i] with plans[i] into streams[i] (whole
+    matrices, as hq_encode with append = 0), several per launch."""
+    n = len(plans)
+    assert len(xs) == n and len(streams) == n and n > 0
+    dt = _dtype_code(xs[0].dtype)
+    for x in xs:
+        assert x.dim() == 2 and x.is_cuda and x.stride(1) == 1 and _dtype_code(x.dtype) == dt
+    ph = (C.c_void_p * n)(*[pl.handle for pl in plans])
+    xp = (C.c_void_p * n)(*[x.data_ptr() for x in xs])
+    rows = (C.c_int64 * n)(*[x.shape[0] for x in xs])
+    lds = (C.c_int64 * n)(*[x.stride(0) for x in xs])
+    sp = (C.c_void_p * n)(*[C.addressof(s.c) for s in streams])
+    st = lib().hq_encode_group(ph, xp, dt, rows, lds, sp, n, _stream_handle(stream))
+    _check("hq_encode_group", st)
+    return streams
+
+
+def hq_decode_group(plans, streams, outs, stream=None):
+    """hq_decode_group: decode every row of streams[i] with plans[i] into
+    outs[i] (bf16 or fp32, one dtype for the group), several per launch."""
+    n = len(plans)
+    assert len(streams) == n and len(outs) == n and n > 0
+    dt = _dtype_code(outs[0].dtype)
+    for y in outs:
+        assert y.is_cuda and y.stride(1) == 1 and _dtype_code(y.dtype) == dt
+    ph = (C.c_void_p * n)(*[pl.handle for pl in plans])
+    sp = (C.c_void_p * n)(*[C.addressof(s.c) for s in streams])
+    yp = (C.c_void_p * n)(*[y.data_ptr() for y in outs])
+    lds = (C.c_int64 * n)(*[y.stride(0) for y in outs])
+    st = lib().hq_decode_group(ph, sp, yp, dt, lds, n, _stream_handle(stream))
+    _check("hq_decode_group", st)
+    return outs
+
+
 def hq_decode_int8(plan: Plan, s: EncodedStream, row0=0, rows=None, stream=None):
     rows = s.rows - row0 if rows is None else rows
     codes = torch.empty((rows, plan.cols), dtype=torch.int8, device=s.device)
@@ -287,6 +326,6 @@ def hq_calibrated_snr(lattice, rice_k, bps):
 
 
 EXPORTED = ["hq_plan", "hq_plan_destroy", "hq_plan_get_info", "hq_scan_bytes", "hq_encode",
-            "hq_decode", "hq_decode_int8", "hq_act_prep", "hq_gemm_int8_blockscaled",
+            "hq_decode", "hq_encode_group", "hq_decode_group", "hq_decode_int8", "hq_act_prep", "hq_gemm_int8_blockscaled",
             "hq_gemm_workspace_bytes", "hq_dequant_gemm_int8", "hq_rice_kstar",
             "hq_calibrated_snr", "hq_status_string"]

@@ -94,3 +94,13 @@ def test_library_calibration_matches_oracle_operating_points(hq):
     assert hq.hq_calibrated_snr(hq.HQ_E8, 2, 4.0) > 0
     with pytest.raises(hq.HQError):
         hq.hq_calibrated_snr(hq.HQ_E8, 3, 2.0)
+
+
+def test_group_argument_errors_are_synchronous(hq):
+    L = hq.lib()
+    assert L.hq_encode_group(None, None, 0, None, None, None, 0, None) == 0  # nothing to do
+    assert L.hq_encode_group(None, None, 0, None, None, None, 2, None) == -1
+    assert L.hq_encode_group(None, None, 0, None, None, None, -1, None) == -1
+    assert L.hq_decode_group(None, None, None, 0, None, 0, None) == 0
+    assert L.hq_decode_group(None, None, None, 0, None, 3, None) == -1
+    assert L.hq_decode_group(None, None, None, 7, None, 0, None) == -1  # bad output type

@@ -220,3 +220,38 @@ def test_gemm_int8_blockscaled(hq, M, N):
     # one bf16 ulp of the reference, or fp32 accumulation noise near zero
     tol = np.maximum(np.abs(ref16) * 2.0 ** -7, 1e-5 * np.sqrt((ref ** 2).mean()))
     assert np.all(np.abs(got16 - ref16) <= tol)
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.Z])
+def test_group_calls_match_single_calls(hq, lat):
+    """hq_encode_group / hq_decode_group give the single-matrix calls' bits:
+    ten matrices of mixed shapes and seeds (more than one launch's worth of
+    members), ragged row counts, bf16 and fp32 outputs."""
+    shapes = [(64, 4096), (16, 1024), (40, 512), (1, 1536), (7, 2048), (33, 512), (128, 1024),
+              (5, 4096), (2, 512), (19, 1536)]
+    print(f"[parity] group {LAT_NAMES[lat]} x{len(shapes)}", flush=True)
+    snr = 20.0
+    plans, xs, grp, one = [], [], [], []
+    for i, (r, c) in enumerate(shapes):
+        plan = hq.hq_plan(128, lat, 0.0, 300 + i, -1, c, snr_db=snr)
+        plans.append(plan)
+        xs.append(gauss(r, c, 400 + i, 0.02, torch.bfloat16).cuda())
+        grp.append(hq.EncodedStream(plan, r))
+        one.append(hq.EncodedStream(plan, r))
+    hq.hq_encode_group(plans, xs, grp)
+    for plan, x, s in zip(plans, xs, one):
+        hq.hq_encode(plan, x, s)
+    torch.cuda.synchronize()
+    for a, b in zip(grp, one):
+        assert a.rows == b.rows
+        n = b.end_words()
+        assert a.end_words() == n
+        assert torch.equal(a.payload[:n], b.payload[:n])
+        assert torch.equal(a.offsets, b.offsets) and torch.equal(a.kparam, b.kparam)
+        assert torch.equal(a.norms, b.norms)
+        assert a.read_stats() == b.read_stats()
+    for dt in (torch.bfloat16, torch.float32):
+        ys = [torch.empty(x.shape, dtype=dt, device="cuda") for x in xs]
+        hq.hq_decode_group(plans, grp, ys)
+        for plan, s, y in zip(plans, one, ys):
+            assert torch.equal(y, hq.hq_decode(plan, s, out_dtype=dt))
