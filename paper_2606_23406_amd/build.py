@@ -20,8 +20,6 @@ FLAGS = [
     "-ffp-contract=off",
     # no packed fp32 vector instructions (v_pk_*_f32) are generated
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # matrix-core results land in ordinary VGPRs (no accumulator-register copies)
-    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall", "-Wno-unused-function",
 ]
 

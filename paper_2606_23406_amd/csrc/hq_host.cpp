@@ -283,7 +283,6 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   kstar_thresholds(n0, p->thr[0]);
   if (n1) kstar_thresholds(n1, p->thr[1]); else kstar_thresholds(1, p->thr[1]);
   p->max_words_sub = substream_word_bound(*p);
-  p->codes_int8 = (!p->dither && lattice != HQ_A2 && code_norm_bound(*p) <= 127.0) ? 1 : 0;
   if (p->max_words_sub > 8192) {
     delete p;
     return HQ_ERR_UNSUPPORTED;
@@ -540,7 +539,6 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
     std::memset(&g, 0, sizeof(g));
     int64_t total = 0;
     uint32_t lds_words = 0;
-    bool mx = true;
     int32_t first = -1;
     for (int32_t i = b; i < std::min(count, b + HQ_GROUP_MAX); ++i) {
       const hq_plan_s* p = plans[i];
@@ -556,13 +554,12 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
       g.wg_begin[g.count] = (uint32_t)total;
       total += hq_decode_workgroups(a.nsub);
       lds_words = std::max(lds_words, a.lds_words);
-      mx = mx && p->codes_int8;
       if (first < 0) first = i;
       ++g.count;
     }
     if (g.count == 0) continue;
     if (total > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
-    if (hq_launch_decode_group(plans[first], g, (uint32_t)total, lds_words, yt, mx, stream))
+    if (hq_launch_decode_group(plans[first], g, (uint32_t)total, lds_words, yt, stream))
       return HQ_ERR_HIP;
   }
   return HQ_OK;

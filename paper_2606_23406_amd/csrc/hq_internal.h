@@ -29,8 +29,6 @@ struct hq_plan_s {
   // k0 = #{t in 1..KMAX : sum >= thr[c][t]} (thr[c][0] unused).
   uint32_t thr[2][HQ_KMAX + 1];
   int64_t max_words_sub;   // capacity bound of one sub-stream, in 32-bit words
-  int32_t codes_int8;      // every lattice code is bounded by 127 (and no dither):
-                           // the decoder's inverse transform is an int8 contraction
   uint32_t* d_dmask;       // device: RHT sign bit per global column (1 = -1)
   uint32_t* d_dsign16;     // device: per column pair, the RHT signs as bf16 sign
                            // bits (bit 15: even column, bit 31: odd column)
@@ -134,7 +132,7 @@ int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* 
 int hq_launch_encode_group(const hq_plan_s* p, const hq_encode_group_args& g, uint32_t nwg,
                            uint32_t lds_words, int xt, void* stream);
 int hq_launch_decode_group(const hq_plan_s* p, const hq_decode_group_args& g, uint32_t nwg,
-                           uint32_t lds_words, int yt, bool mx, void* stream);
+                           uint32_t lds_words, int yt, void* stream);
 uint32_t hq_decode_workgroups(int64_t nsub);
 int hq_launch_decode_int8(const hq_plan_s* p, const hq_decode_args& a, void* stream);
 int hq_launch_act_prep(const hq_actprep_args& a, void* stream);

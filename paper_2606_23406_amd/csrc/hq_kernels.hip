@@ -1508,56 +1508,7 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const De
   return ok;
 }
 
-// ---------------------------------------------- inverse transform on the matrix cores
-// Without dither the decoded codes are integers, |c| <= 127 whenever the plan
-// bounds them so (E8 up to ~4.5 bits per scalar), and H c is an exact
-// integer contraction: W[i'][T] = sum_i H[i'][i] c[T][i] over a wave's 16
-// tiles T, as 8 row blocks (16 outputs each) x 4 k steps (32 inputs each) of
-// v_mfma_i32_16x16x32_i8 with A = H and B = the codes.  Both operands give
-// lane l row / column l % 16 and the same 8 k values 8 (l / 16) + j of a k
-// step, so the contraction pairs equal k whatever order the instruction
-// assigns inside its step; output lane l holds column l % 16 and rows
-// 4 (l / 16) + r, r = 0..3.
-// H[16 mb + rho][32 ks + 8 h + j] = (-1)^popc(i' & k) factors into a per-lane
-// pattern F0 (bits 0-3 of i' against bits 0-4 of k), a flip of the lanes with
-// h bit 1 for odd mb, and a wave-wide sign (-1)^popc((mb >> 1) & ks): four
-// fragments cover all 32 (mb, ks).
-
-constexpr int kCodeTileStride = 136;  // bytes per tile row of codes in LDS (conflict-free reads)
-constexpr int kOutTileStride = 272;   // bytes per tile row of bf16 / fp32 half-row outputs
-constexpr int kCodeWaveBytes = 16 * kOutTileStride;  // codes first, then outputs, per wave
-
-typedef int v4i_t __attribute__((ext_vector_type(4)));
-
-// Eight int32 codes -> eight int8 bytes, low byte first.
-__device__ __forceinline__ uint2 pack_codes8(const int32_t* c) {
-  const uint32_t p01 = __builtin_amdgcn_perm((uint32_t)c[1], (uint32_t)c[0], 0x0C0C0400u);
-  const uint32_t p23 = __builtin_amdgcn_perm((uint32_t)c[3], (uint32_t)c[2], 0x0C0C0400u);
-  const uint32_t p45 = __builtin_amdgcn_perm((uint32_t)c[5], (uint32_t)c[4], 0x0C0C0400u);
-  const uint32_t p67 = __builtin_amdgcn_perm((uint32_t)c[7], (uint32_t)c[6], 0x0C0C0400u);
-  return make_uint2(__builtin_amdgcn_perm(p23, p01, 0x05040100u),
-                    __builtin_amdgcn_perm(p67, p45, 0x05040100u));
-}
-
-struct HFrags {
-  long f[2][2];  // [mb odd][negated]
-  __device__ __forceinline__ explicit HFrags(int lane) {
-    // byte j of F0 is (-1)^(popc(rho & 7 & j) + rho_3 h_0) as int8: start from
-    // +1 everywhere and XOR 0xFE (+1 <-> -1) into the bytes each bit flips
-    constexpr uint32_t kAll = 0xFEFEFEFEu;
-    const uint32_t rho = (uint32_t)lane & 15u, h = (uint32_t)lane >> 4;
-    const uint32_t lo = 0x01010101u ^ ((rho & 1u) ? 0xFE00FE00u : 0u) ^ ((rho & 2u) ? 0xFEFE0000u : 0u) ^
-                        (((rho >> 3) & h & 1u) ? kAll : 0u);
-    const uint32_t hi = lo ^ ((rho & 4u) ? kAll : 0u);
-    const uint32_t odd = ((h >> 1) & 1u) ? kAll : 0u;  // lanes flipped for odd mb
-    f[0][0] = (long)(((uint64_t)hi << 32) | lo);
-    f[0][1] = (long)(((uint64_t)(hi ^ kAll) << 32) | (lo ^ kAll));
-    f[1][0] = (long)(((uint64_t)(hi ^ odd) << 32) | (lo ^ odd));
-    f[1][1] = (long)(((uint64_t)(hi ^ odd ^ kAll) << 32) | (lo ^ odd ^ kAll));
-  }
-};
-
-template <int LAT, int MODE, bool KV, bool MX>
+template <int LAT, int MODE, bool KV>
 __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_t wgi) {
   extern __shared__ uint32_t smem[];
   __shared__ uint32_t s_sel[256];
@@ -1565,8 +1516,6 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   const uint32_t wave = readfirst((uint32_t)(tid >> 6));
   uint32_t* buf = smem + wave * (A.lds_words + 66);
   uint32_t* starts = buf + A.lds_words + 2;
-  // MX: the wave's 16 tiles of int8 codes, after every wave's bit buffers
-  int8_t* cbuf = (int8_t*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66)) + wave * kCodeWaveBytes;
   const bool use_rot = KV && A.rotation;
   const bool use_dither = KV && A.dither;
   const bool fp16_norm = KV && A.norm_fp16;
@@ -1589,20 +1538,6 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   const uint32_t spr = (uint32_t)A.spr;
   const TwSigns sg(lane);
   const uint32_t sbits = use_rot ? sign_bits8(A.smask, (lane & 15) * 8) : 0u;
-  // MX: the output signs of each sub-stream (kept for the store), the count
-  // of sub-streams decoded, and lane l's tile factor r_s / (alpha n) for
-  // tile l % 16 of the wave, loaded ahead of the bit walks
-  uint4 mx_sw[HQ_DEC_SUBS_PER_WAVE];
-  int mx_live = 0;
-  float mx_g = 0.0f;
-  if constexpr (MX) {
-    const uint32_t subT = sub0 + (uint32_t)((lane & 15) >> 2);
-    if (subT < nsub) {
-      const uint32_t r = subT / spr;
-      const int64_t t = (A.first_row + r) * A.tpr + (subT - r * spr) * (HQ_SUB / HQ_TILE) + (lane & 3);
-      mx_g = ((const float*)A.norms)[t];
-    }
-  }
 
 #pragma unroll
   for (int i = 0; i < HQ_DEC_SUBS_PER_WAVE; ++i) {
@@ -1632,14 +1567,6 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
     }
     int32_t c[8];
     unstrip8<LAT>(sym, c);
-    if constexpr (MX) {
-      // tile 4 i + lane / 16 of the wave, coordinates 8 (lane % 16) ..
-      *(uint2*)(cbuf + (4 * i + (lane >> 4)) * kCodeTileStride + 8 * (lane & 15)) = pack_codes8(c);
-      mx_sw[i] = sw;
-      mx_live = i + 1;
-      if (i + 1 < HQ_DEC_SUBS_PER_WAVE) head = next;
-      continue;
-    }
     const float g = rs / A.alpha_n;
 
     if constexpr (MODE == 2) {
@@ -1698,60 +1625,18 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
     }
     if (i + 1 < HQ_DEC_SUBS_PER_WAVE) head = next;
   }
-  if constexpr (MX) {
-    wave_sync_lds();
-    // lane l: tile T = l % 16 (sub-stream sub0 + T / 4), k values 8 (l / 16) + j
-    const int T = lane & 15, hq = lane >> 4;
-    long bfr[4];
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) bfr[ks] = *(const long*)(cbuf + T * kCodeTileStride + 32 * ks + 8 * hq);
-    const HFrags hf(lane);
-    const float g = mx_g / A.alpha_n;
-    // W = H C^T, then y = w r_s / (alpha n) into LDS: tile T, outputs 16 mb + 4 hq + r
-    // (every code has been read into registers above; a wave's LDS
-    // operations complete in order)
-#pragma unroll
-    for (int mb = 0; mb < 8; ++mb) {
-      v4i_t acc = {0, 0, 0, 0};
-#pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        const int neg = __builtin_popcount((mb >> 1) & ks) & 1;
-        acc = __builtin_amdgcn_mfma_i32_16x16x32_i8(hf.f[mb & 1][neg], bfr[ks], acc, 0, 0, 0);
-      }
-      __bf16 b[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) b[r] = (__bf16)((float)acc[r] * g);
-      *(uint2*)(cbuf + T * kOutTileStride + 2 * (16 * mb + 4 * hq)) = *(const uint2*)b;
-    }
-    wave_sync_lds();
-    // store: sub-stream i, lane = 16 t + g holds coordinates 8 g .. 8 g + 7 of its tile t
-#pragma unroll
-    for (int i = 0; i < HQ_DEC_SUBS_PER_WAVE; ++i) {
-      if (i >= mx_live) break;
-      const uint32_t sub = sub0 + (uint32_t)i;
-      const uint32_t lrow = sub / spr;
-      const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
-      const int Ti = 4 * i + (lane >> 4);
-      uint4 o = *(const uint4*)(cbuf + Ti * kOutTileStride + 16 * (lane & 15));
-      o.x ^= mx_sw[i].x;
-      o.y ^= mx_sw[i].y;
-      o.z ^= mx_sw[i].z;
-      o.w ^= mx_sw[i].w;
-      *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = o;
-    }
-  }
 }
 
-template <int LAT, int MODE, bool KV, bool MX>
+template <int LAT, int MODE, bool KV>
 __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
-  decode_wg<LAT, MODE, KV, MX>(A, blockIdx.x);
+  decode_wg<LAT, MODE, KV>(A, blockIdx.x);
 }
 
-template <int LAT, int MODE, bool KV, bool MX>
+template <int LAT, int MODE, bool KV>
 __global__ __launch_bounds__(256) void hq_decode_group_kernel(hq_decode_group_args G) {
   int mi = 0;
   for (int i = 1; i < G.count; ++i) mi = blockIdx.x >= G.wg_begin[i] ? i : mi;
-  decode_wg<LAT, MODE, KV, MX>(G.m[mi], blockIdx.x - G.wg_begin[mi]);
+  decode_wg<LAT, MODE, KV>(G.m[mi], blockIdx.x - G.wg_begin[mi]);
 }
 
 // ------------------------------------------------------------ activation prep
@@ -1820,6 +1705,7 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
 // step.  Output lane l of a 32 x 32 block holds column l % 32 and rows
 // 8 (r / 4) + 4 (l / 32) + r % 4.
 
+typedef int v4i_t __attribute__((ext_vector_type(4)));
 typedef int v16i_t __attribute__((ext_vector_type(16)));
 
 constexpr int kGemmM = 256, kGemmN = 128;  // the prefetch below assumes 256 x 128
@@ -1999,43 +1885,28 @@ int launch_encode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int xt, b
 }
 
 // One decode launch: a single matrix (hq_decode_args) or a group.
-template <int LAT, int MODE, bool KV, bool MX, typename Args>
+template <int LAT, int MODE, bool KV, typename Args>
 void launch_decode_kernel(const Args& a, uint32_t nwg, size_t lds, hipStream_t st) {
   if constexpr (sizeof(Args) == sizeof(hq_decode_args))
-    hipLaunchKernelGGL((hq_decode_kernel<LAT, MODE, KV, MX>), dim3(nwg), dim3(256), lds, st, a);
+    hipLaunchKernelGGL((hq_decode_kernel<LAT, MODE, KV>), dim3(nwg), dim3(256), lds, st, a);
   else
-    hipLaunchKernelGGL((hq_decode_group_kernel<LAT, MODE, KV, MX>), dim3(nwg), dim3(256), lds, st, a);
+    hipLaunchKernelGGL((hq_decode_group_kernel<LAT, MODE, KV>), dim3(nwg), dim3(256), lds, st, a);
 }
 
-template <int LAT, int MODE, typename Args>
-void launch_decode_mode(const Args& a, bool kv, bool mx, uint32_t nwg, size_t lds, hipStream_t st) {
-  if (kv) {
-    launch_decode_kernel<LAT, MODE, true, false>(a, nwg, lds, st);
-  } else if (mx) {
-    if constexpr (LAT != kA2 && MODE == 1) {
-      const size_t lds_mx = lds + (size_t)HQ_WAVES_PER_WG * kCodeWaveBytes;
-      launch_decode_kernel<LAT, MODE, false, true>(a, nwg, lds_mx, st);
-    }
-  } else {
-    launch_decode_kernel<LAT, MODE, false, false>(a, nwg, lds, st);
-  }
-}
-
-// mx: the plan bounds every code by 127 and has no dither or rotation, so
-// the bf16 decode's inverse transform runs on the int8 matrix cores (not for
-// A2, whose first axis carries sqrt(3); the fp32 decode keeps the VALU
-// transform).
 template <int LAT, typename Args>
-int launch_decode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int mode, bool kv, bool mx,
+int launch_decode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int mode, bool kv,
                       hipStream_t st) {
   const size_t lds = (size_t)(lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
-  mx = mx && !kv && LAT != kA2 && mode == 1;
-  if (mode == 0)
-    launch_decode_mode<LAT, 0>(a, kv, mx, nwg, lds, st);
-  else if (mode == 1)
-    launch_decode_mode<LAT, 1>(a, kv, mx, nwg, lds, st);
-  else
-    launch_decode_mode<LAT, 2>(a, kv, false, nwg, lds, st);
+  if (mode == 0) {
+    if (kv) launch_decode_kernel<LAT, 0, true>(a, nwg, lds, st);
+    else launch_decode_kernel<LAT, 0, false>(a, nwg, lds, st);
+  } else if (mode == 1) {
+    if (kv) launch_decode_kernel<LAT, 1, true>(a, nwg, lds, st);
+    else launch_decode_kernel<LAT, 1, false>(a, nwg, lds, st);
+  } else {
+    if (kv) launch_decode_kernel<LAT, 2, true>(a, nwg, lds, st);
+    else launch_decode_kernel<LAT, 2, false>(a, nwg, lds, st);
+  }
   return (int)hipGetLastError();
 }
 
@@ -2078,23 +1949,23 @@ int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* 
   const bool kv = kv_variant(p);
   const uint32_t nwg = decode_wgs(a.nsub), lw = a.lds_words;
   switch (p->lattice) {
-    case HQ_E8: return launch_decode_lat<kE8>(a, nwg, lw, mode, kv, p->codes_int8, st);
-    case HQ_D4: return launch_decode_lat<kD4>(a, nwg, lw, mode, kv, p->codes_int8, st);
-    case HQ_A2: return launch_decode_lat<kA2>(a, nwg, lw, mode, kv, false, st);
-    default: return launch_decode_lat<kZ>(a, nwg, lw, mode, kv, p->codes_int8, st);
+    case HQ_E8: return launch_decode_lat<kE8>(a, nwg, lw, mode, kv, st);
+    case HQ_D4: return launch_decode_lat<kD4>(a, nwg, lw, mode, kv, st);
+    case HQ_A2: return launch_decode_lat<kA2>(a, nwg, lw, mode, kv, st);
+    default: return launch_decode_lat<kZ>(a, nwg, lw, mode, kv, st);
   }
 }
 
 int hq_launch_decode_group(const hq_plan_s* p, const hq_decode_group_args& g, uint32_t nwg,
-                           uint32_t lds_words, int yt, bool mx, void* stream) {
+                           uint32_t lds_words, int yt, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   const int mode = (yt == HQ_FP32) ? 0 : 1;
   const bool kv = kv_variant(p);
   switch (p->lattice) {
-    case HQ_E8: return launch_decode_lat<kE8>(g, nwg, lds_words, mode, kv, mx, st);
-    case HQ_D4: return launch_decode_lat<kD4>(g, nwg, lds_words, mode, kv, mx, st);
-    case HQ_A2: return launch_decode_lat<kA2>(g, nwg, lds_words, mode, kv, false, st);
-    default: return launch_decode_lat<kZ>(g, nwg, lds_words, mode, kv, mx, st);
+    case HQ_E8: return launch_decode_lat<kE8>(g, nwg, lds_words, mode, kv, st);
+    case HQ_D4: return launch_decode_lat<kD4>(g, nwg, lds_words, mode, kv, st);
+    case HQ_A2: return launch_decode_lat<kA2>(g, nwg, lds_words, mode, kv, st);
+    default: return launch_decode_lat<kZ>(g, nwg, lds_words, mode, kv, st);
   }
 }
 
@@ -2104,9 +1975,9 @@ int hq_launch_decode_int8(const hq_plan_s* p, const hq_decode_args& a, void* str
   hipStream_t st = (hipStream_t)stream;
   const bool kv = kv_variant(p);
   switch (p->lattice) {
-    case HQ_E8: return launch_decode_lat<kE8>(a, decode_wgs(a.nsub), a.lds_words, 2, kv, false, st);
-    case HQ_D4: return launch_decode_lat<kD4>(a, decode_wgs(a.nsub), a.lds_words, 2, kv, false, st);
-    default: return launch_decode_lat<kZ>(a, decode_wgs(a.nsub), a.lds_words, 2, kv, false, st);
+    case HQ_E8: return launch_decode_lat<kE8>(a, decode_wgs(a.nsub), a.lds_words, 2, kv, st);
+    case HQ_D4: return launch_decode_lat<kD4>(a, decode_wgs(a.nsub), a.lds_words, 2, kv, st);
+    default: return launch_decode_lat<kZ>(a, decode_wgs(a.nsub), a.lds_words, 2, kv, st);
   }
 }
 
