@@ -81,6 +81,14 @@ __device__ __forceinline__ uint32_t wave_total(uint32_t x) {
   return __builtin_amdgcn_readlane(wave_scan_incl(x), 63);
 }
 
+// a ^ b ^ c in one instruction (gfx950 three-input bitwise op, truth table
+// 0x96 over S0 = 0xF0, S1 = 0xCC, S2 = 0xAA).
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t r;
+  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 __device__ __forceinline__ uint32_t zigzag(int32_t v) {
   return (uint32_t)((v << 1) ^ (v >> 31));
 }
@@ -131,6 +139,13 @@ __device__ __forceinline__ uint32_t select32(uint32_t w, uint32_t r) {
 }
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+// Two fp32 -> bf16 (round to nearest even) in one word: lo in bits 0-15.
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float lo, float hi) {
+  uint32_t r;
+  asm("v_cvt_pk_bf16_f32 %0, %1, %2" : "=v"(r) : "v"(lo), "v"(hi));
+  return r;
+}
 
 // IEEE round-to-nearest-even fp32 -> bf16 bits.
 __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
@@ -358,20 +373,26 @@ __device__ __forceinline__ void strip8(const int32_t* c, uint32_t* s) {
   }
 }
 
+// E8 unstrip (Sec. 4.6) in closed form: 2 unzz(s) = s ^ -(s & 1), so
+// c_i = 2 h_i + cb = (s_i ^ -(s_i & 1)) + cb for i < 7; h_i = unzz(s_i) has the
+// parity of bit 1 ^ bit 0 of s_i, so p = bit 1 ^ bit 0 of the XOR of s_0..s_6;
+// s_7 = 2 zz(t) + cb gives 2 t = z ^ -(z & 1) with z = s_7 >> 1, and
+// c_7 = 2 (2 t + p) + cb.
+__device__ __forceinline__ void e8_unstrip(const uint32_t* s, int32_t* c) {
+  const uint32_t cb = s[7] & 1u;
+#pragma unroll
+  for (int i = 0; i < 7; ++i)
+    c[i] = (int32_t)((s[i] ^ (uint32_t)__builtin_amdgcn_sbfe((int32_t)s[i], 0, 1)) + cb);
+  const uint32_t X = xor3(xor3(s[0], s[1], s[2]), s[3], s[4]) ^ s[5] ^ s[6];
+  const uint32_t p = ((X >> 1) ^ X) & 1u;
+  const uint32_t t2 = (s[7] >> 1) ^ (uint32_t)__builtin_amdgcn_sbfe((int32_t)s[7], 1, 1);
+  c[7] = (int32_t)((t2 << 1) + ((p << 1) | cb));
+}
+
 template <int LAT>
 __device__ __forceinline__ void unstrip8(const uint32_t* s, int32_t* c) {
   if constexpr (LAT == kE8) {
-    const int32_t cb = (int32_t)(s[7] & 1u);
-    const int32_t t = unzigzag(s[7] >> 1);
-    int32_t h[8], p = 0;
-#pragma unroll
-    for (int i = 0; i < 7; ++i) {
-      h[i] = unzigzag(s[i]);
-      p += h[i];
-    }
-    h[7] = 2 * t + (p & 1);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) c[i] = 2 * h[i] + cb;
+    e8_unstrip(s, c);
   } else if constexpr (LAT == kD4) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) {
@@ -683,13 +704,6 @@ __device__ __forceinline__ int32_t sub_lanemask(int32_t x, uint64_t m) {
   return r;
 }
 
-// a ^ b ^ c in one instruction (gfx950 three-input bitwise op, truth table
-// 0x96 over S0 = 0xF0, S1 = 0xCC, S2 = 0xAA).
-__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
-  uint32_t r;
-  asm("v_bitop3_b32 %0, %1, %2, %3 bitop3:0x96" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
-}
 
 __device__ __forceinline__ void e8_nearest(const float* w, int32_t* h, int32_t& cb) {
   float ea[8];
@@ -1438,15 +1452,16 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const De
   uint32_t qv[8];
   bool fast = false;
   if (ok) {
-    uint32_t win = bits32_at(buf, pos);
+    // q_j = the zeros before the next terminator: shift the window past
+    // each code (all 8 terminators lie inside it on this path, so every
+    // shift is below 32; otherwise the values are discarded below)
+    const uint32_t win = bits32_at(buf, pos);
     fast = __popc(win) >= 8;
-    int32_t prev = -1;
+    uint32_t sh = 0;
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const int32_t p = (int32_t)__builtin_ctz(win | 0x80000000u);
-      qv[j] = (uint32_t)(p - prev - 1);
-      prev = p;
-      win &= win - 1u;
+      qv[j] = (uint32_t)__builtin_ctz(win >> sh);
+      sh += qv[j] + 1u;
     }
   }
   if (ok && !fast) {
@@ -1501,9 +1516,9 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const De
       sym[j] = (qv[j] << kk) | (r & ((1u << kk) - 1u));
     }
   }
-  if (!ok) {
+  if (__ballot(!ok) != 0ull) {  // a corrupt sub-stream decodes as zeros
 #pragma unroll
-    for (int j = 0; j < 8; ++j) sym[j] = 0;
+    for (int j = 0; j < 8; ++j) sym[j] = ok ? sym[j] : 0u;
   }
   return ok;
 }
@@ -1538,6 +1553,19 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   const uint32_t spr = (uint32_t)A.spr;
   const TwSigns sg(lane);
   const uint32_t sbits = use_rot ? sign_bits8(A.smask, (lane & 15) * 8) : 0u;
+  // tile factors g = r_s / (alpha n), once for the wave's 16 tiles: lane l
+  // takes sub-stream l & 3, tile l >> 4 (rows are contiguous, 4 tiles per
+  // sub-stream); sub-stream i reads them back by a quad broadcast
+  static_assert(HQ_DEC_SUBS_PER_WAVE == 4, "one sub-stream per lane of a quad");
+  float gm = 0.0f;
+  {
+    const uint32_t subq = sub0 + (uint32_t)(lane & 3);
+    if (subq < nsub) {
+      const int64_t t = A.first_row * A.tpr + 4 * (int64_t)subq + (lane >> 4);
+      const float rs = fp16_norm ? (float)((const _Float16*)A.norms)[t] : ((const float*)A.norms)[t];
+      gm = rs / A.alpha_n;
+    }
+  }
 
 #pragma unroll
   for (int i = 0; i < HQ_DEC_SUBS_PER_WAVE; ++i) {
@@ -1549,9 +1577,7 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
     const uint32_t lrow = sub / spr;
     const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
     const int64_t grow = A.first_row + lrow;
-    const int64_t tix = grow * A.tpr + (col >> 7);
-    // per-tile norm and output signs, loaded before the bit walk
-    const float rs = fp16_norm ? (float)((const _Float16*)A.norms)[tix] : ((const float*)A.norms)[tix];
+    // output signs, loaded before the bit walk
     uint4 sw = make_uint4(0u, 0u, 0u, 0u);
     if (MODE == 1) sw = *(const uint4*)(A.dsign16 + (col >> 1));
 
@@ -1567,7 +1593,7 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
     }
     int32_t c[8];
     unstrip8<LAT>(sym, c);
-    const float g = rs / A.alpha_n;
+    const float g = i == 0 ? quad_bcast<0>(gm) : (i == 1 ? quad_bcast<1>(gm) : (i == 2 ? quad_bcast<2>(gm) : quad_bcast<3>(gm)));
 
     if constexpr (MODE == 2) {
       uint32_t packed[2] = {0u, 0u};
@@ -1612,14 +1638,11 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
         out[0] = make_float4(y[0], y[1], y[2], y[3]);
         out[1] = make_float4(y[4], y[5], y[6], y[7]);
       } else {
-        __bf16 b[8];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) b[j] = (__bf16)y[j];
-        uint4 o = *(const uint4*)b;
-        o.x ^= sw.x;
-        o.y ^= sw.y;
-        o.z ^= sw.z;
-        o.w ^= sw.w;
+        uint4 o;
+        o.x = cvt_pk_bf16(y[0], y[1]) ^ sw.x;
+        o.y = cvt_pk_bf16(y[2], y[3]) ^ sw.y;
+        o.z = cvt_pk_bf16(y[4], y[5]) ^ sw.z;
+        o.w = cvt_pk_bf16(y[6], y[7]) ^ sw.w;
         *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = o;
       }
     }
