@@ -43,7 +43,7 @@ def parse_args():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemm", action="store_true")
     ap.add_argument("--no-other", action="store_true", help="skip the C1, C2, C3-D4 and C4 measurements")
-    ap.add_argument("--group", type=int, default=7,
+    ap.add_argument("--group", type=int, default=16,
                     help="matrices per encode/decode launch (hq_encode_group); 1 = one launch each")
     return ap.parse_args()
 
@@ -63,11 +63,11 @@ def build_workload(H, W, layers, bps, dev, snr=None):
 
 
 def groups_of(mats, size):
-    """The stack in launch groups: one layer's seven matrices per group."""
+    """The stack in launch groups of `size` consecutive matrices."""
     return [mats[i:i + size] for i in range(0, len(mats), size)]
 
 
-def encode_all(H, mats, group=7):
+def encode_all(H, mats, group=16):
     if group <= 1:
         for m in mats:
             H.hq_encode(m["plan"], m["x"], m["s"])
@@ -76,7 +76,7 @@ def encode_all(H, mats, group=7):
         H.hq_encode_group([m["plan"] for m in g], [m["x"] for m in g], [m["s"] for m in g])
 
 
-def decode_all(H, mats, group=7):
+def decode_all(H, mats, group=16):
     if group <= 1:
         for m in mats:
             H.hq_decode(m["plan"], m["s"], out=m["y"])

@@ -168,7 +168,7 @@ hq_status hq_encode(hq_plan_t plan, const void* x, int32_t xt, int64_t rows, int
                     hq_stream* s, int32_t append, void* stream);
 
 /* hq_encode_group -- hq_encode (append = 0) of `count` matrices in as few
- * launches as possible (up to 8 per launch): member i encodes rows[i] rows of
+ * launches as possible (up to 16 per launch): member i encodes rows[i] rows of
  * x[i] (element type xt, row stride ld[i]) with plans[i] into s[i], exactly
  * as hq_encode would, bit for bit.  Whole-model quantization (Sec. 6.1 codes
  * every linear layer) calls it on a layer's matrices at once, so the small
@@ -194,7 +194,7 @@ hq_status hq_decode(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t ro
                     int32_t yt, int64_t ld, void* stream);
 
 /* hq_decode_group -- hq_decode of all rows of `count` streams in as few
- * launches as possible (up to 8 per launch): member i decodes s[i] (all
+ * launches as possible (up to 16 per launch): member i decodes s[i] (all
  * s[i]->rows rows) with plans[i] into y[i] (device, element type yt, row
  * stride ld[i]), with the same results as hq_decode.  Plans as for
  * hq_encode_group.  Errors: as hq_decode, plus HQ_ERR_INVALID_ARG for mixed

@@ -422,14 +422,20 @@ static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t 
   a.dither_seed = p->dither_seed;
   a.alpha = p->alpha;
   a.alpha_half = 0.5f * p->alpha;
-  // class sums stay below 2^26 (512 symbols of at most 2^17), so thresholds
-  // past 2^30 are unreachable; the kernel compares in signed 32-bit
-  for (int t = 0; t <= HQ_KMAX; ++t) {
-    a.thr0[t] = std::min<uint32_t>(p->thr[0][t], 1u << 30);
-    a.thr1[t] = std::min<uint32_t>(p->thr[1][t], 1u << 30);
-  }
   *nwg_out = nwg;
   return HQ_OK;
+}
+
+// The plan's Rice-k thresholds as the kernel compares them.  Class sums stay
+// below 2^26 (512 symbols of at most 2^17), so thresholds past 2^30 are
+// unreachable; the kernel compares in signed 32-bit.
+static hq_rice_thr rice_thresholds(const hq_plan_s* p) {
+  hq_rice_thr t;
+  for (int k = 0; k <= HQ_KMAX; ++k) {
+    t.thr0[k] = std::min<uint32_t>(p->thr[0][k], 1u << 30);
+    t.thr1[k] = std::min<uint32_t>(p->thr[1][k], 1u << 30);
+  }
+  return t;
 }
 
 hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_t ld,
@@ -438,7 +444,7 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
   int64_t nwg;
   const hq_status st = encode_prepare(p, x, xt, rows, ld, s, append, &a, &nwg, stream);
   if (st != HQ_OK || nwg == 0) return st;
-  if (hq_launch_encode(p, a, xt, stream)) return HQ_ERR_HIP;
+  if (hq_launch_encode(p, a, rice_thresholds(p), xt, stream)) return HQ_ERR_HIP;
   s->rows = a.first_row + rows;
   return HQ_OK;
 }
@@ -477,6 +483,7 @@ hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t 
     }
     if (g.count == 0) continue;
     if (total > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
+    g.thr = rice_thresholds(plans[members[0]]);  // one lattice and sub-stream length
     if (hq_launch_encode_group(plans[members[0]], g, (uint32_t)total, lds_words, xt, stream))
       return HQ_ERR_HIP;
     for (int32_t k = 0; k < g.count; ++k) s[members[k]]->rows = rows[members[k]];

@@ -65,6 +65,11 @@ struct hq_encode_args {
   uint64_t dither_seed;
   float alpha;
   float alpha_half;       // alpha / 2, exact (the E8 decision works on z / 2)
+};
+
+// Automatic Rice-k thresholds of the two symbol classes (the same for every
+// plan of one lattice and sub-stream length).
+struct hq_rice_thr {
   uint32_t thr0[HQ_KMAX + 1];
   uint32_t thr1[HQ_KMAX + 1];
 };
@@ -95,8 +100,9 @@ struct hq_decode_args {
 
 // Several matrices in one launch (kernel arguments, by value): member i owns
 // workgroups wg_begin[i] .. wg_begin[i + 1] - 1 (the last one to the grid end).
-#define HQ_GROUP_MAX 8
+#define HQ_GROUP_MAX 16
 struct hq_encode_group_args {
+  hq_rice_thr thr;
   hq_encode_args m[HQ_GROUP_MAX];
   uint32_t wg_begin[HQ_GROUP_MAX];
   int32_t count;
@@ -127,7 +133,8 @@ struct hq_gemm_args {
 };
 
 // Kernel launchers (hq_kernels.hip); return a hipError_t as int.
-int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, int xt, void* stream);
+int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, const hq_rice_thr& t, int xt,
+                     void* stream);
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream);
 int hq_launch_encode_group(const hq_plan_s* p, const hq_encode_group_args& g, uint32_t nwg,
                            uint32_t lds_words, int xt, void* stream);

@@ -877,8 +877,8 @@ __device__ __forceinline__ float quad_bcast(float v) {
 }
 
 template <int LAT, int XT, bool KV>
-__device__ __forceinline__ void encode_substream(const hq_encode_args& A, const SubPos& P,
-                                                 int lane, float* x, float scale_tw,
+__device__ __forceinline__ void encode_substream(const hq_encode_args& A, const hq_rice_thr& T,
+                                                 const SubPos& P, int lane, float* x, float scale_tw,
                                                  uint32_t* buf, uint32_t& W_out, uint32_t& kb_out,
                                                  uint32_t& bits_out, bool& overflow_out) {
   const bool active = P.active;  // wave-uniform
@@ -930,7 +930,7 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
     if (A.rice_k >= 0) {
       k0 = (uint32_t)A.rice_k;
     } else {
-      const uint32_t a0 = kstar_count(wave_total(s0), A.thr0);
+      const uint32_t a0 = kstar_count(wave_total(s0), T.thr0);
       // the better of k* and k* + 1: k* + 1 saves sum((m >> k) - (m >> (k+1)))
       // unary bits and costs one remainder bit per symbol
       uint32_t ga = 0, gb = 0;
@@ -960,8 +960,8 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
       for (int j = 0; j < 8; ++j) {
         if (sym_class<LAT>(j)) s1 += sym[j]; else s0 += sym[j];
       }
-      const uint32_t a0 = kstar_count(wave_total(s0), A.thr0);
-      const uint32_t a1 = (LAT == kA2) ? kstar_count(wave_total(s1), A.thr1) : 0u;
+      const uint32_t a0 = kstar_count(wave_total(s0), T.thr0);
+      const uint32_t a1 = (LAT == kA2) ? kstar_count(wave_total(s1), T.thr1) : 0u;
       const uint32_t b0 = a0 < HQ_KMAX ? a0 + 1 : a0;
       const uint32_t b1 = a1 < HQ_KMAX ? a1 + 1 : a1;
       uint32_t g0 = 0, g1 = 0;
@@ -1083,7 +1083,8 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
 }
 
 template <int LAT, int XT, bool KV>
-__device__ __forceinline__ void encode_wg(const hq_encode_args& A, const uint32_t wg) {
+__device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice_thr& T,
+                                          const uint32_t wg) {
   extern __shared__ uint32_t smem[];
   __shared__ uint32_t s_epoch;
   __shared__ uint32_t s_words[HQ_ENC_SUBS_PER_WG];
@@ -1171,7 +1172,7 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const uint32_
     const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
     uint32_t W, kb, bits;
     bool ovf;
-    encode_substream<LAT, XT, KV>(A, pos[i], lane, x[i], xor_sign(ss[i], sg.sigma),
+    encode_substream<LAT, XT, KV>(A, T, pos[i], lane, x[i], xor_sign(ss[i], sg.sigma),
                                   smem + li * stride, W, kb, bits, ovf);
     if (pos[i].active) {
       if (lane == 0) {
@@ -1321,8 +1322,8 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const uint32_
 }
 
 template <int LAT, int XT, bool KV>
-__global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_kernel(hq_encode_args A) {
-  encode_wg<LAT, XT, KV>(A, blockIdx.x);
+__global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_kernel(hq_encode_args A, hq_rice_thr T) {
+  encode_wg<LAT, XT, KV>(A, T, blockIdx.x);
 }
 
 // Several matrices in one launch: workgroups wg_begin[i] .. wg_begin[i+1]-1
@@ -1332,7 +1333,7 @@ template <int LAT, int XT, bool KV>
 __global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_group_kernel(hq_encode_group_args G) {
   int mi = 0;
   for (int i = 1; i < G.count; ++i) mi = blockIdx.x >= G.wg_begin[i] ? i : mi;
-  encode_wg<LAT, XT, KV>(G.m[mi], blockIdx.x - G.wg_begin[mi]);
+  encode_wg<LAT, XT, KV>(G.m[mi], G.thr, blockIdx.x - G.wg_begin[mi]);
 }
 
 // ------------------------------------------------------------ decode kernel
@@ -1882,27 +1883,33 @@ __global__ void hq_zero_kernel(uint32_t* p, size_t n) {
   if (i < n) p[i] = 0u;
 }
 
-template <int LAT, int XT, bool KV, typename Args>
-void launch_encode_kernel(const Args& a, uint32_t nwg, size_t lds, hipStream_t st) {
-  if constexpr (sizeof(Args) == sizeof(hq_encode_args))
-    hipLaunchKernelGGL((hq_encode_kernel<LAT, XT, KV>), dim3(nwg), dim3(64 * HQ_ENC_WAVES), lds, st, a);
-  else
-    hipLaunchKernelGGL((hq_encode_group_kernel<LAT, XT, KV>), dim3(nwg), dim3(64 * HQ_ENC_WAVES), lds, st, a);
+// One encode launch: a single matrix (hq_encode_args + thresholds) or a group.
+template <int LAT, int XT, bool KV>
+void launch_encode_kernel(const hq_encode_args& a, const hq_rice_thr& t, uint32_t nwg, size_t lds,
+                          hipStream_t st) {
+  hipLaunchKernelGGL((hq_encode_kernel<LAT, XT, KV>), dim3(nwg), dim3(64 * HQ_ENC_WAVES), lds, st, a, t);
+}
+
+template <int LAT, int XT, bool KV>
+void launch_encode_kernel(const hq_encode_group_args& g, const hq_rice_thr&, uint32_t nwg, size_t lds,
+                          hipStream_t st) {
+  hipLaunchKernelGGL((hq_encode_group_kernel<LAT, XT, KV>), dim3(nwg), dim3(64 * HQ_ENC_WAVES), lds, st, g);
 }
 
 template <int LAT, typename Args>
-int launch_encode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int xt, bool kv, hipStream_t st) {
+int launch_encode_lat(const Args& a, const hq_rice_thr& t, uint32_t nwg, uint32_t lds_words, int xt,
+                      bool kv, hipStream_t st) {
   const size_t lds = (size_t)(lds_words + 2) * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
   if (xt == HQ_BF16) {
     if (kv)
-      launch_encode_kernel<LAT, HQ_BF16, true>(a, nwg, lds, st);
+      launch_encode_kernel<LAT, HQ_BF16, true>(a, t, nwg, lds, st);
     else
-      launch_encode_kernel<LAT, HQ_BF16, false>(a, nwg, lds, st);
+      launch_encode_kernel<LAT, HQ_BF16, false>(a, t, nwg, lds, st);
   } else {
     if (kv)
-      launch_encode_kernel<LAT, HQ_FP32, true>(a, nwg, lds, st);
+      launch_encode_kernel<LAT, HQ_FP32, true>(a, t, nwg, lds, st);
     else
-      launch_encode_kernel<LAT, HQ_FP32, false>(a, nwg, lds, st);
+      launch_encode_kernel<LAT, HQ_FP32, false>(a, t, nwg, lds, st);
   }
   return (int)hipGetLastError();
 }
@@ -1937,15 +1944,16 @@ int launch_decode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int mode,
 
 static bool kv_variant(const hq_plan_s* p) { return p->rotation || p->dither || p->norm_fp16; }
 
-int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, int xt, void* stream) {
+int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, const hq_rice_thr& t, int xt,
+                     void* stream) {
   hipStream_t st = (hipStream_t)stream;
   const bool kv = kv_variant(p);
   const uint32_t lw = a.lds_words;
   switch (p->lattice) {
-    case HQ_E8: return launch_encode_lat<kE8>(a, a.nwg, lw, xt, kv, st);
-    case HQ_D4: return launch_encode_lat<kD4>(a, a.nwg, lw, xt, kv, st);
-    case HQ_A2: return launch_encode_lat<kA2>(a, a.nwg, lw, xt, kv, st);
-    default: return launch_encode_lat<kZ>(a, a.nwg, lw, xt, kv, st);
+    case HQ_E8: return launch_encode_lat<kE8>(a, t, a.nwg, lw, xt, kv, st);
+    case HQ_D4: return launch_encode_lat<kD4>(a, t, a.nwg, lw, xt, kv, st);
+    case HQ_A2: return launch_encode_lat<kA2>(a, t, a.nwg, lw, xt, kv, st);
+    default: return launch_encode_lat<kZ>(a, t, a.nwg, lw, xt, kv, st);
   }
 }
 
@@ -1954,10 +1962,10 @@ int hq_launch_encode_group(const hq_plan_s* p, const hq_encode_group_args& g, ui
   hipStream_t st = (hipStream_t)stream;
   const bool kv = kv_variant(p);
   switch (p->lattice) {
-    case HQ_E8: return launch_encode_lat<kE8>(g, nwg, lds_words, xt, kv, st);
-    case HQ_D4: return launch_encode_lat<kD4>(g, nwg, lds_words, xt, kv, st);
-    case HQ_A2: return launch_encode_lat<kA2>(g, nwg, lds_words, xt, kv, st);
-    default: return launch_encode_lat<kZ>(g, nwg, lds_words, xt, kv, st);
+    case HQ_E8: return launch_encode_lat<kE8>(g, g.thr, nwg, lds_words, xt, kv, st);
+    case HQ_D4: return launch_encode_lat<kD4>(g, g.thr, nwg, lds_words, xt, kv, st);
+    case HQ_A2: return launch_encode_lat<kA2>(g, g.thr, nwg, lds_words, xt, kv, st);
+    default: return launch_encode_lat<kZ>(g, g.thr, nwg, lds_words, xt, kv, st);
   }
 }
 

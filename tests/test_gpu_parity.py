@@ -225,10 +225,11 @@ def test_gemm_int8_blockscaled(hq, M, N):
 @pytest.mark.parametrize("lat", [O.E8, O.D4, O.Z])
 def test_group_calls_match_single_calls(hq, lat):
     """hq_encode_group / hq_decode_group give the single-matrix calls' bits:
-    ten matrices of mixed shapes and seeds (more than one launch's worth of
-    members), ragged row counts, bf16 and fp32 outputs."""
+    eighteen matrices of mixed shapes and seeds (more than one launch's worth
+    of members), ragged row counts, bf16 and fp32 outputs."""
     shapes = [(64, 4096), (16, 1024), (40, 512), (1, 1536), (7, 2048), (33, 512), (128, 1024),
-              (5, 4096), (2, 512), (19, 1536)]
+              (5, 4096), (2, 512), (19, 1536), (3, 1024), (11, 512), (6, 2048), (1, 512), (9, 1024),
+              (4, 1536), (17, 512), (2, 4096)]
     print(f"[parity] group {LAT_NAMES[lat]} x{len(shapes)}", flush=True)
     snr = 20.0
     plans, xs, grp, one = [], [], [], []
