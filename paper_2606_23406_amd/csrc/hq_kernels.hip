@@ -1022,7 +1022,7 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   __builtin_amdgcn_wave_barrier();
   if (active && !overflow) {
     // remainder fields, packed per lane
-    const uint32_t rpos = (uint32_t)lane * lrem;
+    const uint32_t rpos = __umul24((uint32_t)lane, lrem);  // lrem < 2^24
     if (lrem <= 32) {
       uint32_t acc = 0;
 #pragma unroll
@@ -1493,7 +1493,7 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const De
     }
   }
   // lane's 8 remainders (fields at fixed positions)
-  const uint32_t rpos = (uint32_t)lane * lrem;
+  const uint32_t rpos = __umul24((uint32_t)lane, lrem);  // lrem < 2^24
   if (lrem <= 32) {
     const uint32_t acc = (ok && lrem) ? bits32_at(buf, rpos) : 0u;
 #pragma unroll
