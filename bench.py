@@ -428,14 +428,14 @@ def main():
                    "scalars": n_scalars, "matrices": len(mats), "bps_target": args.bps,
                    "bps_realized": round(bps, 4)},
         "pct_hbm_peak": round(100.0 * (enc_bytes + dec_bytes) / t_step / 1e9 / HBM_PEAK_GBS, 2),
-        "roofline": {"bound": "hbm", "kernel": "hq_encode_kernel (E8, bf16 in)",
+        "roofline": {"bound": "hbm", "kernel": "hq_encode_group_kernel (E8, bf16 in)",
                      "achieved": round(enc_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(enc_gbs / HBM_PEAK_GBS, 4),
                      "traffic": None if tr_enc is None else round(tr_enc),
                      "algorithmic_bytes_per_launch": round(alg_enc_launch),
                      "algorithmic_bytes_per_scalar": round(enc_bytes / n_scalars, 4),
                      "launches_per_step": launches},
-        "decode_roofline": {"bound": "hbm", "kernel": "hq_decode_kernel (E8, bf16 out)",
+        "decode_roofline": {"bound": "hbm", "kernel": "hq_decode_group_kernel (E8, bf16 out)",
                             "achieved": round(dec_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
                             "traffic": None if tr_dec is None else round(tr_dec),

@@ -29,8 +29,8 @@ from collections import defaultdict
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "paper_2606_23406_amd", "csrc", "hq_kernels.hip")
 KERNELS = {
-    "encode": "hq_encode_kernel<0, 0, false>",
-    "decode": "hq_decode_kernel<0, 1, false>",
+    "encode": "hq_encode_group_kernel<0, 0, false>",
+    "decode": "hq_decode_group_kernel<0, 1, false>",
     "gemm": "hq_gemm_i8_kernel",
     "copy": "__amd_rocclr_copyBuffer",
 }
@@ -131,10 +131,11 @@ def stats(stats_csv, log, out, cmd):
     rows = list(csv.DictReader(open(stats_csv)))
     lines = ["# Kernel time: E8 at 4 bps codec over the Llama-3.1-8B-shaped linear stack", "",
              "Command (repository root, one MI355X):", "", f"    {cmd}", "",
-             f"One step = encode then decode of the 224 matrices ({n} bf16 weights); "
-             f"{steps} steps ran ({b['warmup']} warmup + {b['steps']} timed), so each codec "
-             f"kernel has {steps} x 224 calls. The GEMM and act-prep lines come from the int8 "
-             "GEMM measurement at the end of the run.", "",
+             f"One step = encode then decode of the 224 matrices ({n} bf16 weights) in "
+             f"{b['roofline']['launches_per_step']} launches each way (hq_encode_group / "
+             f"hq_decode_group, up to 16 matrices per launch); {steps} steps ran "
+             f"({b['warmup']} warmup + {b['steps']} timed). The other rows come from the rest "
+             "of the run (the GEMM, the D4 stack, the C1/C2/C4 configurations).", "",
              "| kernel | calls | total ms | avg us | min us | max us |", "|---|---|---|---|---|---|"]
     per = {}
     for r in rows:
