@@ -1268,23 +1268,43 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     if (timed_out && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_HIP);
   }
 
-  // ---- write payload and offsets of all of the group's sub-streams
-  unsigned long long start = base;
-  for (int li = 0; li < HQ_ENC_SUBS_PER_WG; ++li) {
-    const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
-    if (sub >= (uint32_t)A.nsub) break;
-    const uint32_t W = readfirst(s_words[li]);
-    const uint32_t* buf = smem + li * stride;
-    const bool fits = start + W <= (unsigned long long)A.cap_words;
-    if (fits) {
-      for (uint32_t w = lane; w < W; w += 64) A.payload[start + w] = buf[w];
+  // ---- write payload and offsets of all of the group's sub-streams: lane
+  //      l < 16 takes sub-stream l's word count (0 when inactive) and its
+  //      prefix inside the group; then 16 lanes per sub-stream copy four
+  //      sub-streams at a time, every load of a lane issued before its stores
+  static_assert(HQ_ENC_SUBS_PER_WG == 16, "one row of lanes holds the group's word counts");
+  {
+    const uint32_t wl = lane < HQ_ENC_SUBS_PER_WG ? s_words[lane] : 0u;
+    uint32_t il = wl;  // inclusive prefix inside the first row of 16 lanes
+    il += dpp<kDppRowShr1, 0xF, 0xF, true>(0u, il);
+    il += dpp<kDppRowShr2, 0xF, 0xF, true>(0u, il);
+    il += dpp<kDppRowShr4, 0xF, 0xF, true>(0u, il);
+    il += dpp<kDppRowShr8, 0xF, 0xF, true>(0u, il);
+    const uint32_t xl = il - wl;
+    const uint32_t sub_l = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)lane;
+    if (lane < HQ_ENC_SUBS_PER_WG && sub_l < (uint32_t)A.nsub) {
+      const unsigned long long end = base + il;
+      if (sub_l == 0 && !A.append) A.offsets[A.first_sub] = 0u;
+      A.offsets[A.first_sub + sub_l + 1] = (uint32_t)end;
+      if (end > (unsigned long long)A.cap_words && A.stats)
+        atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CAPACITY);
     }
-    if (lane == 0) {
-      if (sub == 0 && !A.append) A.offsets[A.first_sub] = 0u;
-      A.offsets[A.first_sub + sub + 1] = (uint32_t)(start + W);
-      if (!fits && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CAPACITY);
+#pragma unroll
+    for (int r = 0; r < HQ_ENC_SUBS_PER_WG / 4; ++r) {
+      const int li = 4 * r + (lane >> 4);
+      const uint32_t W = (uint32_t)__shfl((int)wl, li);
+      const unsigned long long st = base + (uint32_t)__shfl((int)xl, li);
+      if (st + W > (unsigned long long)A.cap_words) continue;  // reported above
+      const uint32_t* buf = smem + li * stride;
+      for (uint32_t j = (uint32_t)(lane & 15); j < W; j += 64) {
+        uint32_t v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) v[u] = j + 16u * u < W ? buf[j + 16u * u] : 0u;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (j + 16u * u < W) A.payload[st + j + 16u * u] = v[u];
+      }
     }
-    start += W;
   }
   // ---- bit counts: the last group of every 256 adds up their stats words
   //      (all of them were stored before their owners' aggregates, which this
