@@ -89,6 +89,18 @@ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
   return r;
 }
 
+// (a << sh) | c and (1 << sh) | c in one instruction each.
+__device__ __forceinline__ uint32_t lshl_or(uint32_t a, uint32_t sh, uint32_t c) {
+  uint32_t r;
+  asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(sh), "v"(c));
+  return r;
+}
+__device__ __forceinline__ uint32_t bit_or(uint32_t sh, uint32_t c) {
+  uint32_t r;
+  asm("v_lshl_or_b32 %0, 1, %1, %2" : "=v"(r) : "v"(sh), "v"(c));
+  return r;
+}
+
 __device__ __forceinline__ uint32_t zigzag(int32_t v) {
   return (uint32_t)((v << 1) ^ (v >> 31));
 }
@@ -748,16 +760,19 @@ __device__ __forceinline__ void e8_nearest(const float* w, int32_t* h, int32_t& 
     return;
   }
   // lane masks: the class, whether its parity needs the fix, and per
-  // coordinate the largest-error hits and the sign of ea
+  // coordinate the largest-error hits and the sign of ea.  The error of
+  // coordinate i in the lane's class is key_i = fma(|ea_i|, +-1, 0 or 1/2):
+  // |ea_i| (exact) in the first class, fl(1/2 - |ea_i|) (one rounding, as
+  // the subtraction) in the second; its largest value is mx or fl(1/2 - mn).
   const bool even = D < 0.0f;
   const uint64_t E = __ballot(even);
   const uint64_t need = (E & __ballot(odd_a)) | (~E & __ballot(odd_b));
-  const float mb = 0.5f - mn;
+  const float ks = even ? 1.0f : -1.0f, kc = even ? 0.0f : 0.5f;
+  const float top = even ? mx : 0.5f - mn;
   uint64_t done = ~need;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
-    const float a = __builtin_fabsf(ea[i]);
-    const uint64_t hit = (E & __ballot(a == mx)) | (~E & __ballot(0.5f - a == mb));
+    const uint64_t hit = __ballot(__builtin_fmaf(__builtin_fabsf(ea[i]), ks, kc) == top);
     const uint64_t fix = hit & ~done;
     done |= hit;
     const uint64_t neg = __ballot(ea[i] < 0.0f);
@@ -929,6 +944,12 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
     for (int j = 0; j < 8; ++j) s0 += sym[j];
     if (A.rice_k >= 0) {
       k0 = (uint32_t)A.rice_k;
+      ulen = 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        qv[j] = sym[j] >> k0;
+        ulen += qv[j];
+      }
     } else {
       const uint32_t a0 = kstar_count(wave_total(s0), T.thr0);
       // the better of k* and k* + 1: k* + 1 saves sum((m >> k) - (m >> (k+1)))
@@ -936,20 +957,18 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
       uint32_t ga = 0, gb = 0;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const uint32_t qa = sym[j] >> a0;
-        ga += qa;
-        gb += qa >> 1;
+        qv[j] = sym[j] >> a0;
+        ga += qv[j];
+        gb += qv[j] >> 1;
       }
       const uint32_t gain = wave_total(ga - gb);
-      k0 = (a0 < HQ_KMAX && gain > (uint32_t)HQ_SUB) ? a0 + 1 : a0;
+      const uint32_t d = (a0 < HQ_KMAX && gain > (uint32_t)HQ_SUB) ? 1u : 0u;
+      k0 = a0 + d;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) qv[j] >>= d;
+      ulen = 8 + (d ? gb : ga);
     }
     k1 = k0;
-    ulen = 8;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      qv[j] = sym[j] >> k0;
-      ulen += qv[j];
-    }
   } else {
     if (A.rice_k >= 0) {
       k0 = (uint32_t)A.rice_k;
@@ -1028,7 +1047,7 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-        acc |= (sym[j] & ((1u << kk) - 1u)) << rem_offset<LAT>(j, k0, k1);
+        acc = lshl_or(sym[j] & ((1u << kk) - 1u), rem_offset<LAT>(j, k0, k1), acc);
       }
       or_word(buf, rpos, acc);
     } else if (lrem <= 64) {
@@ -1053,7 +1072,7 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         t += qv[j];
-        m |= 1u << t;
+        m = bit_or(t, m);
         t += 1;
       }
       or_word(buf, upos, m);
