@@ -351,6 +351,12 @@ hq_status hq_plan_destroy(hq_plan_t p) {
   return HQ_OK;
 }
 
+// Sub-streams per wave of an encode of nsub sub-streams: one for small
+// launches (unless the caller needs the four of a group launch).
+static int32_t encode_spw(int64_t nsub, bool allow_small) {
+  return (allow_small && nsub <= HQ_ENC_SMALL_SUBS) ? 1 : HQ_ENC_SUBS_PER_WAVE;
+}
+
 size_t hq_scan_bytes(hq_plan_t p, int64_t rows) {
   if (!p || rows < 0) return 0;
   const int64_t nwg = (rows * p->spr + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
@@ -363,8 +369,8 @@ size_t hq_scan_bytes(hq_plan_t p, int64_t rows) {
 // *nwg = 0 when there is nothing to launch (rows == 0; the stream is then
 // already up to date).
 static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_t ld,
-                                hq_stream* s, int32_t append, hq_encode_args* out, int64_t* nwg_out,
-                                void* stream) {
+                                hq_stream* s, int32_t append, bool allow_small, hq_encode_args* out,
+                                int64_t* nwg_out, void* stream) {
   *nwg_out = 0;
   if (!p || !s || rows < 0) return HQ_ERR_INVALID_ARG;
   if (xt != HQ_BF16 && xt != HQ_FP32) return HQ_ERR_INVALID_ARG;
@@ -387,6 +393,7 @@ static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t 
     }
     return HQ_OK;
   }
+  const int32_t spw = encode_spw(nsub, allow_small);
   const int64_t nwg = (nsub + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
   if (nwg > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
   if ((size_t)s->scan_bytes < hq_scan_bytes(p, rows)) return HQ_ERR_CAPACITY;
@@ -413,6 +420,7 @@ static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t 
   a.status = (unsigned long long*)((char*)s->scan + HQ_SCAN_STATUS_OFFSET);
   a.wgstat = a.status + nwg;
   a.nwg = (uint32_t)nwg;
+  a.spw = (uint32_t)spw;
   a.append = append ? 1 : 0;
   a.rice_k = p->rice_k;
   a.rotation = p->rotation;
@@ -442,7 +450,7 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
                     hq_stream* s, int32_t append, void* stream) {
   hq_encode_args a;
   int64_t nwg;
-  const hq_status st = encode_prepare(p, x, xt, rows, ld, s, append, &a, &nwg, stream);
+  const hq_status st = encode_prepare(p, x, xt, rows, ld, s, append, true, &a, &nwg, stream);
   if (st != HQ_OK || nwg == 0) return st;
   if (hq_launch_encode(p, a, rice_thresholds(p), xt, stream)) return HQ_ERR_HIP;
   s->rows = a.first_row + rows;
@@ -473,7 +481,7 @@ hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t 
     for (int32_t i = b; i < std::min(count, b + HQ_GROUP_MAX); ++i) {
       int64_t nwg;
       const hq_status st =
-          encode_prepare(plans[i], x[i], xt, rows[i], ld[i], s[i], 0, &g.m[g.count], &nwg, stream);
+          encode_prepare(plans[i], x[i], xt, rows[i], ld[i], s[i], 0, false, &g.m[g.count], &nwg, stream);
       if (st != HQ_OK) return st;
       if (nwg == 0) continue;
       g.wg_begin[g.count] = (uint32_t)total;

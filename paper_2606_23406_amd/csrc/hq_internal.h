@@ -14,6 +14,10 @@
 #define HQ_ENC_SUBS_PER_WAVE 4   // encode: sub-streams per wave, one after another
 #define HQ_ENC_WAVES 4           // encode: wave64s per workgroup
 #define HQ_ENC_SUBS_PER_WG (HQ_ENC_WAVES * HQ_ENC_SUBS_PER_WAVE)
+// Launches of at most this many sub-streams take one sub-stream per wave
+// (sixteen waves per workgroup): four times the waves for the same work, so
+// a small matrix or a KV append does not leave each SIMD a single long wave.
+#define HQ_ENC_SMALL_SUBS 16384
 #define HQ_DEC_SUBS_PER_WAVE 4   // decode: consecutive sub-streams per wave
 #define HQ_SCAN_STATUS_OFFSET 128  // bytes before the look-back status array
 
@@ -61,7 +65,8 @@ struct hq_encode_args {
   int32_t append;
   int32_t rice_k;
   int32_t rotation, dither, norm_fp16;
-  uint32_t lds_words;     // per-wave assembly buffer, in words
+  uint32_t lds_words;     // per-sub-stream assembly buffer, in words
+  uint32_t spw;           // sub-streams per wave: HQ_ENC_SUBS_PER_WAVE, or 1 for small launches
   uint64_t dither_seed;
   float alpha;
   float alpha_half;       // alpha / 2, exact (the E8 decision works on z / 2)

@@ -797,7 +797,8 @@ __device__ __forceinline__ void e8_strip(const int32_t* h, int32_t cb, uint32_t*
 
 // ------------------------------------------------------------ encode kernel
 // One workgroup encodes HQ_ENC_SUBS_PER_WG consecutive sub-streams (four
-// waves, HQ_ENC_SUBS_PER_WAVE each, one at a time) and keeps their bits in
+// waves with four each, one at a time, or sixteen waves with one each) and
+// keeps their bits in
 // LDS; then its first wave alone publishes the group's word count, looks back
 // for the group's absolute word offset and writes payload and offsets.  KV = false is the
 // weight path (no rotation, no dither, fp32 norms) compiled without those
@@ -810,6 +811,56 @@ __device__ __forceinline__ uint32_t kstar_count(uint32_t sum, const uint32_t* th
 #pragma unroll
   for (int t = 1; t <= HQ_KMAX; ++t) a += (uint32_t)((int32_t)(thr[t] - 1u - sum)) >> 31;
   return a;
+}
+
+// One look-back round over the NR * 64 workgroups hi, hi - 1, ... (lane l
+// takes distances r * 64 + l below hi + 1, r < NR): waits until each has
+// published, then adds their values down to the nearest inclusive prefix
+// into `prefix`.  Returns true when that prefix was among them (or the wait
+// timed out: then `timed_out` is set).
+template <int NR>
+__device__ __forceinline__ bool lookback_round(unsigned long long* status, int64_t hi,
+                                               uint32_t epoch, int lane, uint32_t& prefix,
+                                               bool& timed_out) {
+  unsigned long long st[NR];
+  bool ready[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    st[r] = 0ull;
+    ready[r] = hi - (r * 64 + lane) < 0;
+  }
+  uint32_t spins = 0;
+  for (;;) {
+    bool all = true;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      if (!ready[r]) {
+        st[r] = load_status(&status[hi - (r * 64 + lane)]);
+        ready[r] = (uint32_t)(st[r] >> 34) == epoch && ((st[r] >> 32) & 3u) != 0u;
+      }
+      all = all && ready[r];
+    }
+    if (__ballot(!all) == 0ull) break;
+    if (++spins > kSpinLimit) {
+      timed_out = true;
+      return true;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  // nearest inclusive prefix: the first r with one, then its lowest lane
+  uint32_t stop = 64u * NR;
+#pragma unroll
+  for (int r = NR - 1; r >= 0; --r) {
+    const bool incl = hi - (r * 64 + lane) >= 0 && ((st[r] >> 32) & 3u) == 2u;
+    const unsigned long long m = __ballot(incl);
+    if (m) stop = (uint32_t)(r * 64) + (uint32_t)__builtin_ctzll(m);
+  }
+  uint32_t v = 0;
+#pragma unroll
+  for (int r = 0; r < NR; ++r)
+    if (hi - (r * 64 + lane) >= 0 && (uint32_t)(r * 64 + lane) <= stop) v += (uint32_t)st[r];
+  prefix += wave_total(v);
+  return stop < 64u * NR;
 }
 
 // Position of one wave's sub-stream: wave-uniform row and first column.
@@ -1101,13 +1152,16 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   overflow_out = overflow;
 }
 
-template <int LAT, int XT, bool KV>
+template <int LAT, int XT, bool KV, int SPW>
 __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice_thr& T,
                                           const uint32_t wg) {
+  static_assert(SPW == 1 || SPW == 4, "one or four sub-streams per wave");
+  constexpr int NSUB = HQ_ENC_SUBS_PER_WG;  // sub-streams per workgroup
+  constexpr int WAVES = NSUB / SPW;         // wave64s per workgroup
   extern __shared__ uint32_t smem[];
   __shared__ uint32_t s_epoch;
-  __shared__ uint32_t s_words[HQ_ENC_SUBS_PER_WG];
-  __shared__ uint32_t s_pad[HQ_ENC_WAVES];
+  __shared__ uint32_t s_words[NSUB];
+  __shared__ uint32_t s_pad[WAVES];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = (int)readfirst((uint32_t)(tid >> 6));
@@ -1117,41 +1171,42 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
               kEpochMask;
   const TwSigns sg(lane);
 
-  // ---- this wave's sub-streams: wg * 16 + i * 4 + wave, i = 0 .. 3 (row and
+  // ---- this wave's sub-streams: wg * NSUB + i * 4 + wave, i < SPW (row and
   //      column advanced on scalar registers)
-  SubPos pos[HQ_ENC_SUBS_PER_WAVE];
+  SubPos pos[SPW];
   {
     const uint32_t spr = (uint32_t)A.spr;
-    const uint32_t sub0 = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)wave;
+    const uint32_t sub0 = wg * NSUB + (uint32_t)wave;
     uint32_t row = sub0 / spr, c = sub0 - row * spr;
 #pragma unroll
-    for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
-      pos[i].active = sub0 + (uint32_t)(i * HQ_ENC_WAVES) < (uint32_t)A.nsub;
+    for (int i = 0; i < SPW; ++i) {
+      pos[i].active = sub0 + (uint32_t)(i * WAVES) < (uint32_t)A.nsub;
       pos[i].lrow = pos[i].active ? row : 0u;
       pos[i].col0 = pos[i].active ? c * HQ_SUB : 0u;
-      c += HQ_ENC_WAVES;
+      c += WAVES;
       while (c >= spr) {
         c -= spr;
         ++row;
       }
     }
   }
-  // ---- front ends of the wave's four sub-streams: every input load is
-  //      issued first, then sign flips, tile sums of squares and transforms
-  static_assert(HQ_ENC_SUBS_PER_WAVE == 4, "one sub-stream per lane of a quad");
-  LaneInput in[HQ_ENC_SUBS_PER_WAVE];
+  // ---- front ends of the wave's sub-streams: every input load is issued
+  //      first, then sign flips, tile sums of squares and transforms
+  LaneInput in[SPW];
 #pragma unroll
-  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) in[i] = load_lane_input<XT>(A, pos[i], lane);
-  float x[HQ_ENC_SUBS_PER_WAVE][8], ss[HQ_ENC_SUBS_PER_WAVE];
+  for (int i = 0; i < SPW; ++i) in[i] = load_lane_input<XT>(A, pos[i], lane);
+  float x[SPW][8], ss[SPW];
 #pragma unroll
-  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) ss[i] = encode_front<XT>(in[i], sg, x[i]);
+  for (int i = 0; i < SPW; ++i) ss[i] = encode_front<XT>(in[i], sg, x[i]);
 
-  // ---- tile norms and scales, once for the wave's 16 tiles: lane l takes
-  //      sub-stream i = l & 3, tile t = l >> 4 (each tile's 16 lanes hold its
-  //      sum of squares, so the merged value repeats in every quad)
+  // ---- tile norms and scales, once for the wave's tiles: with four
+  //      sub-streams lane l takes sub-stream i = l & 3, tile t = l >> 4 (each
+  //      tile's 16 lanes hold its sum of squares, so the merged value repeats
+  //      in every quad); with one, every lane takes its own tile l >> 4
   {
-    const int qi = lane & 3;
-    const float ssm = qi == 0 ? ss[0] : (qi == 1 ? ss[1] : (qi == 2 ? ss[2] : ss[3]));
+    const int qi = SPW == 4 ? (lane & 3) : 0;
+    float ssm = ss[0];
+    if constexpr (SPW == 4) ssm = qi == 0 ? ss[0] : (qi == 1 ? ss[1] : (qi == 2 ? ss[2] : ss[3]));
     const bool fp16_norm = KV && A.norm_fp16;
     const float r = __builtin_sqrtf(ssm);
     float rs = r;
@@ -1163,8 +1218,9 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     // E8 decides on z / 2: its scale is (alpha / 2) / r_s, exactly half of alpha / r_s
     const float scale =
         (rs == 0.0f || bad_tile) ? 0.0f : (LAT == kE8 ? A.alpha_half : A.alpha) / rs;
-    const uint32_t sub_l = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)(qi * HQ_ENC_WAVES + wave);
-    if (((lane >> 2) & 3) == 0 && sub_l < (uint32_t)A.nsub) {
+    const uint32_t sub_l = wg * NSUB + (uint32_t)(qi * WAVES + wave);
+    const bool writer = SPW == 4 ? ((lane >> 2) & 3) == 0 : (lane & 15) == 0;
+    if (writer && sub_l < (uint32_t)A.nsub) {
       // tile (lane >> 4) of sub-stream sub_l: 4 tiles per sub-stream, rows contiguous
       const int64_t t = A.first_row * A.tpr + 4 * (int64_t)sub_l + (lane >> 4);
       if (fp16_norm) {
@@ -1177,18 +1233,22 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
         atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_OVERFLOW);
       }
     }
-    ss[0] = quad_bcast<0>(scale);
-    ss[1] = quad_bcast<1>(scale);
-    ss[2] = quad_bcast<2>(scale);
-    ss[3] = quad_bcast<3>(scale);
+    if constexpr (SPW == 4) {
+      ss[0] = quad_bcast<0>(scale);
+      ss[1] = quad_bcast<1>(scale);
+      ss[2] = quad_bcast<2>(scale);
+      ss[3] = quad_bcast<3>(scale);
+    } else {
+      ss[0] = scale;
+    }
   }
 
   // ---- quantize and Rice-code each sub-stream into its LDS buffer
   uint32_t padsum = 0;
 #pragma unroll
-  for (int i = 0; i < HQ_ENC_SUBS_PER_WAVE; ++i) {
-    const int li = i * HQ_ENC_WAVES + wave;  // neighbouring waves take neighbouring sub-streams
-    const uint32_t sub = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)li;
+  for (int i = 0; i < SPW; ++i) {
+    const int li = i * WAVES + wave;  // neighbouring waves take neighbouring sub-streams
+    const uint32_t sub = wg * NSUB + (uint32_t)li;
     uint32_t W, kb, bits;
     bool ovf;
     encode_substream<LAT, XT, KV>(A, T, pos[i], lane, x[i], xor_sign(ss[i], sg.sigma),
@@ -1217,65 +1277,24 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
   // ---- publish this group's word count at once, so successors can pass it;
   //      the group's pad bits go to its stats word first (packed as
   //      words << 11 | pad: at most 2^19 words and 64 * 31 pad bits)
-  static_assert(HQ_ENC_SUBS_PER_WG <= 64, "one sub-stream word count per lane");
-  const uint32_t agg = wave_total(lane < HQ_ENC_SUBS_PER_WG ? s_words[lane] : 0u);
+  static_assert(NSUB <= 64, "one sub-stream word count per lane");
+  const uint32_t agg = wave_total(lane < NSUB ? s_words[lane] : 0u);
   if (lane == 0) {
     if (A.stats) {
       uint32_t gp = 0;
 #pragma unroll
-      for (int w = 0; w < HQ_ENC_WAVES; ++w) gp += s_pad[w];
+      for (int w = 0; w < WAVES; ++w) gp += s_pad[w];
       store_status(&A.wgstat[wg], pack_status(epoch, 1u, (agg << 11) | gp));
     }
     if (wg > 0) store_status(&A.status[wg], pack_status(epoch, 1u, agg));
   }
 
-  // ---- look-back: 256 predecessors per round trip, four per lane (distance
-  //      r * 64 + lane + 1 below this group), until the nearest published
-  //      inclusive prefix
+  // ---- look-back: 256 predecessors per round trip, until the nearest
+  //      published inclusive prefix
   uint32_t prefix = 0;
   bool timed_out = false;
-  int64_t hi = (int64_t)wg - 1;
-  while (hi >= 0) {
-    unsigned long long st[4];
-    bool ready[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      st[r] = 0ull;
-      ready[r] = hi - (r * 64 + lane) < 0;
-    }
-    uint32_t spins = 0;
-    for (;;) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        if (!ready[r]) {
-          st[r] = load_status(&A.status[hi - (r * 64 + lane)]);
-          ready[r] = (uint32_t)(st[r] >> 34) == epoch && ((st[r] >> 32) & 3u) != 0u;
-        }
-      }
-      if (__ballot(!(ready[0] && ready[1] && ready[2] && ready[3])) == 0ull) break;
-      if (++spins > kSpinLimit) {
-        timed_out = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-    if (timed_out) break;
-    // nearest inclusive prefix: the first r with one, then its lowest lane
-    uint32_t stop = 256u;
-#pragma unroll
-    for (int r = 3; r >= 0; --r) {
-      const bool incl = hi - (r * 64 + lane) >= 0 && ((st[r] >> 32) & 3u) == 2u;
-      const unsigned long long m = __ballot(incl);
-      if (m) stop = (uint32_t)(r * 64) + (uint32_t)__builtin_ctzll(m);
-    }
-    uint32_t v = 0;
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-      if (hi - (r * 64 + lane) >= 0 && (uint32_t)(r * 64 + lane) <= stop) v += (uint32_t)st[r];
-    prefix += wave_total(v);
-    if (stop < 256u) break;
-    hi -= 256;
-  }
+  for (int64_t hi = (int64_t)wg - 1; hi >= 0; hi -= 256)
+    if (lookback_round<4>(A.status, hi, epoch, lane, prefix, timed_out)) break;
   const unsigned long long base =
       (A.append ? (unsigned long long)readfirst(A.offsets[A.first_sub]) : 0ull) + prefix;
   if (lane == 0) {
@@ -1288,20 +1307,20 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
   }
 
   // ---- write payload and offsets of all of the group's sub-streams: lane
-  //      l < 16 takes sub-stream l's word count (0 when inactive) and its
+  //      l < NSUB takes sub-stream l's word count (0 when inactive) and its
   //      prefix inside the group; then 16 lanes per sub-stream copy four
   //      sub-streams at a time, every load of a lane issued before its stores
-  static_assert(HQ_ENC_SUBS_PER_WG == 16, "one row of lanes holds the group's word counts");
+  static_assert(NSUB <= 16, "one row of lanes holds the group's word counts");
   {
-    const uint32_t wl = lane < HQ_ENC_SUBS_PER_WG ? s_words[lane] : 0u;
+    const uint32_t wl = lane < NSUB ? s_words[lane] : 0u;
     uint32_t il = wl;  // inclusive prefix inside the first row of 16 lanes
     il += dpp<kDppRowShr1, 0xF, 0xF, true>(0u, il);
     il += dpp<kDppRowShr2, 0xF, 0xF, true>(0u, il);
     il += dpp<kDppRowShr4, 0xF, 0xF, true>(0u, il);
     il += dpp<kDppRowShr8, 0xF, 0xF, true>(0u, il);
     const uint32_t xl = il - wl;
-    const uint32_t sub_l = wg * HQ_ENC_SUBS_PER_WG + (uint32_t)lane;
-    if (lane < HQ_ENC_SUBS_PER_WG && sub_l < (uint32_t)A.nsub) {
+    const uint32_t sub_l = wg * NSUB + (uint32_t)lane;
+    if (lane < NSUB && sub_l < (uint32_t)A.nsub) {
       const unsigned long long end = base + il;
       if (sub_l == 0 && !A.append) A.offsets[A.first_sub] = 0u;
       A.offsets[A.first_sub + sub_l + 1] = (uint32_t)end;
@@ -1309,7 +1328,7 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
         atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CAPACITY);
     }
 #pragma unroll
-    for (int r = 0; r < HQ_ENC_SUBS_PER_WG / 4; ++r) {
+    for (int r = 0; r < NSUB / 4; ++r) {
       const int li = 4 * r + (lane >> 4);
       const uint32_t W = (uint32_t)__shfl((int)wl, li);
       const unsigned long long st = base + (uint32_t)__shfl((int)xl, li);
@@ -1360,9 +1379,10 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
   }
 }
 
-template <int LAT, int XT, bool KV>
-__global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_kernel(hq_encode_args A, hq_rice_thr T) {
-  encode_wg<LAT, XT, KV>(A, T, blockIdx.x);
+template <int LAT, int XT, bool KV, int SPW>
+__global__ __launch_bounds__(64 * HQ_ENC_SUBS_PER_WG / SPW) void hq_encode_kernel(hq_encode_args A,
+                                                                                hq_rice_thr T) {
+  encode_wg<LAT, XT, KV, SPW>(A, T, blockIdx.x);
 }
 
 // Several matrices in one launch: workgroups wg_begin[i] .. wg_begin[i+1]-1
@@ -1372,7 +1392,7 @@ template <int LAT, int XT, bool KV>
 __global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_group_kernel(hq_encode_group_args G) {
   int mi = 0;
   for (int i = 1; i < G.count; ++i) mi = blockIdx.x >= G.wg_begin[i] ? i : mi;
-  encode_wg<LAT, XT, KV>(G.m[mi], G.thr, blockIdx.x - G.wg_begin[mi]);
+  encode_wg<LAT, XT, KV, HQ_ENC_SUBS_PER_WAVE>(G.m[mi], G.thr, blockIdx.x - G.wg_begin[mi]);
 }
 
 // ------------------------------------------------------------ decode kernel
@@ -1922,33 +1942,40 @@ __global__ void hq_zero_kernel(uint32_t* p, size_t n) {
   if (i < n) p[i] = 0u;
 }
 
-// One encode launch: a single matrix (hq_encode_args + thresholds) or a group.
+// One encode launch: a single matrix (hq_encode_args + thresholds; four or
+// one sub-streams per wave) or a group (four per wave).
 template <int LAT, int XT, bool KV>
-void launch_encode_kernel(const hq_encode_args& a, const hq_rice_thr& t, uint32_t nwg, size_t lds,
-                          hipStream_t st) {
-  hipLaunchKernelGGL((hq_encode_kernel<LAT, XT, KV>), dim3(nwg), dim3(64 * HQ_ENC_WAVES), lds, st, a, t);
+void launch_encode_kernel(const hq_encode_args& a, const hq_rice_thr& t, uint32_t nwg,
+                          uint32_t lds_words, hipStream_t st) {
+  const size_t per_sub = (size_t)(lds_words + 2) * sizeof(uint32_t);
+  if (a.spw == 1)
+    hipLaunchKernelGGL((hq_encode_kernel<LAT, XT, KV, 1>), dim3(nwg), dim3(64 * HQ_ENC_SUBS_PER_WG),
+                       per_sub * HQ_ENC_SUBS_PER_WG, st, a, t);
+  else
+    hipLaunchKernelGGL((hq_encode_kernel<LAT, XT, KV, HQ_ENC_SUBS_PER_WAVE>), dim3(nwg),
+                       dim3(64 * HQ_ENC_WAVES), per_sub * HQ_ENC_SUBS_PER_WG, st, a, t);
 }
 
 template <int LAT, int XT, bool KV>
-void launch_encode_kernel(const hq_encode_group_args& g, const hq_rice_thr&, uint32_t nwg, size_t lds,
-                          hipStream_t st) {
+void launch_encode_kernel(const hq_encode_group_args& g, const hq_rice_thr&, uint32_t nwg,
+                          uint32_t lds_words, hipStream_t st) {
+  const size_t lds = (size_t)(lds_words + 2) * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
   hipLaunchKernelGGL((hq_encode_group_kernel<LAT, XT, KV>), dim3(nwg), dim3(64 * HQ_ENC_WAVES), lds, st, g);
 }
 
 template <int LAT, typename Args>
 int launch_encode_lat(const Args& a, const hq_rice_thr& t, uint32_t nwg, uint32_t lds_words, int xt,
                       bool kv, hipStream_t st) {
-  const size_t lds = (size_t)(lds_words + 2) * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
   if (xt == HQ_BF16) {
     if (kv)
-      launch_encode_kernel<LAT, HQ_BF16, true>(a, t, nwg, lds, st);
+      launch_encode_kernel<LAT, HQ_BF16, true>(a, t, nwg, lds_words, st);
     else
-      launch_encode_kernel<LAT, HQ_BF16, false>(a, t, nwg, lds, st);
+      launch_encode_kernel<LAT, HQ_BF16, false>(a, t, nwg, lds_words, st);
   } else {
     if (kv)
-      launch_encode_kernel<LAT, HQ_FP32, true>(a, t, nwg, lds, st);
+      launch_encode_kernel<LAT, HQ_FP32, true>(a, t, nwg, lds_words, st);
     else
-      launch_encode_kernel<LAT, HQ_FP32, false>(a, t, nwg, lds, st);
+      launch_encode_kernel<LAT, HQ_FP32, false>(a, t, nwg, lds_words, st);
   }
   return (int)hipGetLastError();
 }
