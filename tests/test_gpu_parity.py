@@ -256,3 +256,24 @@ def test_group_calls_match_single_calls(hq, lat):
         hq.hq_decode_group(plans, grp, ys)
         for plan, s, y in zip(plans, one, ys):
             assert torch.equal(y, hq.hq_decode(plan, s, out_dtype=dt))
+
+
+@pytest.mark.parametrize("rows", [2048, 2049])
+def test_launch_shapes_agree_at_the_small_launch_bound(hq, rows):
+    """A single encode of at most 16384 sub-streams runs one sub-stream per
+    wave (sixteen waves per workgroup), a larger one and every group launch
+    four per wave: the same matrix through both shapes gives the same bits.
+    2048 x 4096 is exactly 16384 sub-streams; one more row crosses over."""
+    print(f"[parity] launch shapes rows={rows}", flush=True)
+    plan = hq.hq_plan(128, O.E8, 0.0, 77, -1, 4096, snr_db=20.0)
+    x = gauss(rows, 4096, 78, 0.02, torch.bfloat16).cuda()
+    a, b = hq.EncodedStream(plan, rows), hq.EncodedStream(plan, rows)
+    hq.hq_encode(plan, x, a)
+    hq.hq_encode_group([plan], [x], [b])
+    torch.cuda.synchronize()
+    n = a.end_words()
+    assert b.end_words() == n
+    assert torch.equal(a.payload[:n], b.payload[:n])
+    assert torch.equal(a.offsets, b.offsets) and torch.equal(a.kparam, b.kparam)
+    assert torch.equal(a.norms, b.norms)
+    assert a.read_stats() == b.read_stats()
