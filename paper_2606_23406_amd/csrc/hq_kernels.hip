@@ -459,18 +459,6 @@ __device__ __forceinline__ void fwht8_inlane(float* v) {
       }
 }
 
-__device__ __forceinline__ void fwht8_inlane_i(int32_t* v) {
-#pragma unroll
-  for (int h = 1; h < 8; h <<= 1)
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-      if ((i & h) == 0) {
-        const int32_t a = v[i], b = v[i + h];
-        v[i] = a + b;
-        v[i + h] = a - b;
-      }
-}
-
 // Butterfly with lane l ^ M: the lower lane keeps a + b, the upper a - b,
 // with a the lower lane's value.  s = +1 (lower) or -1 (upper) makes it one
 // exact-multiplier fma: fma(v, s, p) = round(p + s v).
@@ -483,26 +471,12 @@ __device__ __forceinline__ void fwht_xlane(float* v, float s) {
   }
 }
 
-template <int M>
-__device__ __forceinline__ void fwht_xlane_i(int32_t* v, int32_t s) {
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int32_t p = (int32_t)xor_lane<M>((uint32_t)v[j]);
-    v[j] = p + __mul24(v[j], s);
-  }
-}
-
 // Per-lane butterfly signs for the cross-lane stages (h = 8, 16, 32, 64).
 struct XSigns {
   float f[4];
-  int32_t i[4];
   __device__ __forceinline__ explicit XSigns(int lane) {
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const bool upper = (lane >> b) & 1;
-      f[b] = upper ? -1.0f : 1.0f;
-      i[b] = upper ? -1 : 1;
-    }
+    for (int b = 0; b < 4; ++b) f[b] = ((lane >> b) & 1) ? -1.0f : 1.0f;
   }
 };
 
@@ -514,13 +488,6 @@ __device__ __forceinline__ void fwht128(float* v, const XSigns& sg) {
   fwht_xlane<8>(v, sg.f[3]);
 }
 
-__device__ __forceinline__ void fwht128_i(int32_t* v, const XSigns& sg) {
-  fwht8_inlane_i(v);
-  fwht_xlane_i<1>(v, sg.i[0]);
-  fwht_xlane_i<2>(v, sg.i[1]);
-  fwht_xlane_i<4>(v, sg.i[2]);
-  fwht_xlane_i<8>(v, sg.i[3]);
-}
 
 // The 8 sign bits of columns col0 .. col0 + 7 (col0 a multiple of 8).
 __device__ __forceinline__ uint32_t sign_bits8(const uint32_t* mask, int64_t col0) {
