@@ -1455,10 +1455,16 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const De
     starts[lane] = wave_scan_incl(__popc(v));
     wave_sync_lds();
     const uint32_t target = 8u * (uint32_t)lane;  // terminators before this lane's codes
-    uint32_t w = 0;
+    // the search moves a byte pointer: a step is taken when starts[...] -
+    // target is negative, its sign bit the mask, so every step is a few
+    // fast-rate adds and ands (counts and targets are below 2^12)
+    const char* sp = (const char*)starts;
 #pragma unroll
-    for (uint32_t step = 32; step >= 1; step >>= 1)
-      if (starts[w + step - 1] < target) w += step;
+    for (uint32_t step = 32; step >= 1; step >>= 1) {
+      const int32_t d = (int32_t)(*(const uint32_t*)(sp + 4u * (step - 1u)) - target);
+      sp += (4u * step) & (uint32_t)(d >> 31);
+    }
+    const uint32_t w = (uint32_t)(sp - (const char*)starts) >> 2;
     const uint32_t word = w < nuw ? buf[uw0 + w] : 0u;
     const uint32_t incl = starts[w];
     if (lane == 0) {
