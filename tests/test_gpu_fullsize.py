@@ -123,6 +123,52 @@ def test_c3_llama_linears(hq, layer, lat, bps):
         del xd, y, s
 
 
+def test_c3_first_launch_group_as_benched(hq):
+    """The bench's first launch of the E8@4 stack: sixteen matrices (layers 0
+    and 1, then layer 2's q and k) through one hq_encode_group and one
+    hq_decode_group launch.  Every stream and output equals the
+    single-matrix calls word for word, and sampled rows of one member of each
+    shape match the oracle bit for bit."""
+    from paper_2606_23406_amd import workloads as W
+    snr = PT.op_snr("E8", 4.0)
+    members = [(layer, idx) for layer in range(3) for idx in range(len(W.LLAMA_LINEARS))][:16]
+    plans, Ps, xs, grp = [], [], [], []
+    for layer, idx in members:
+        _, out_f, in_f = W.LLAMA_LINEARS[idx]
+        P = PT.oracle_params(O.E8, snr, rht_seed=W.llama_linear_seed(layer, idx))
+        plan = PT.gpu_plan(hq, P, snr, in_f)
+        plans.append(plan)
+        Ps.append(P)
+        xs.append(W.llama_linear(layer, idx, device="cuda"))
+        grp.append(hq.EncodedStream(plan, out_f))
+    print("[fullsize] C3 first launch group: 16 matrices, E8@4", flush=True)
+    hq.hq_encode_group(plans, xs, grp)
+    ys = [torch.empty_like(x) for x in xs]
+    hq.hq_decode_group(plans, grp, ys)
+    torch.cuda.synchronize()
+    shapes = set()
+    for (layer, idx), plan, P, x, s, y in zip(members, plans, Ps, xs, grp, ys):
+        name, out_f, in_f = W.LLAMA_LINEARS[idx]
+        assert s.read_stats()["status"] == 0
+        one = hq.EncodedStream(plan, out_f)
+        hq.hq_encode(plan, x, one)
+        y1 = hq.hq_decode(plan, one, out_dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        n = one.end_words()
+        assert s.end_words() == n and torch.equal(s.payload[:n], one.payload[:n]), (layer, name)
+        assert torch.equal(s.offsets, one.offsets) and torch.equal(s.kparam, one.kparam)
+        assert torch.equal(s.norms, one.norms) and torch.equal(y, y1), (layer, name)
+        if (out_f, in_f) not in shapes:
+            shapes.add((out_f, in_f))
+            rng = np.random.default_rng(7000 + 10 * layer + idx)
+            rows = np.sort(rng.choice(out_f, 4, replace=False))
+            xc = torch.zeros((out_f, in_f), dtype=torch.bfloat16)
+            xc[rows] = x[torch.from_numpy(rows).cuda()].cpu()
+            check_sampled_rows(hq, plan, s, P, xc, rows, f"C3 group launch, layer {layer} {name}")
+        del one, y1
+    assert len(shapes) == 4
+
+
 @pytest.fixture(scope="module")
 def kv_keys():
     from paper_2606_23406_amd import workloads as W
