@@ -9,8 +9,12 @@
 // in that order, so every fp32 value equals the reference stage order.
 //
 // Floating-point contraction is off for this file: each a * b + c that the
-// method writes as two roundings stays two roundings; the few fused
-// multiply-adds used below are exact (a multiplier of +-2 or an integer sum).
+// method writes as two roundings stays two roundings.  The fused
+// multiply-adds used below either have a multiplier of +-1 or +-2 (one
+// rounding of a sum or difference, the same as the add or subtract they
+// replace) or work on integer values (exact); the one exception is the int8
+// GEMM's per-tile rescale, a floating-point accumulation whose results are
+// held to a tolerance rather than bit for bit.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -778,11 +782,11 @@ __device__ __forceinline__ void e8_strip(const int32_t* h, int32_t cb, uint32_t*
 // ------------------------------------------------------------ encode kernel
 // One workgroup encodes HQ_ENC_SUBS_PER_WG consecutive sub-streams (four
 // waves with four each, one at a time, or sixteen waves with one each) and
-// keeps their bits in
-// LDS; then its first wave alone publishes the group's word count, looks back
-// for the group's absolute word offset and writes payload and offsets.  KV = false is the
-// weight path (no rotation, no dither, fp32 norms) compiled without those
-// branches; KV = true reads the three options at run time.
+// keeps their bits in LDS; then its first wave alone publishes the group's
+// word count, looks back for the group's absolute word offset and writes
+// payload and offsets.  KV = false is the weight path (no rotation, no
+// dither, fp32 norms) compiled without those branches; KV = true reads the
+// three options at run time.
 
 // Number of k in 1..KMAX with sum >= thr[k] (thresholds clamped below 2^30
 // on the host, sums below 2^26), on scalar registers.
