@@ -349,6 +349,44 @@ def gemm_extra(H, W, mats, dev):
             "end_to_end_TOPS": round(ops / t_e2e / 1e12, 2)}
 
 
+def gemv_extra(H, W, mats, dev, reps=10):
+    """Fused decode-GEMV (hq_decode_gemv) for one bf16 token through layer 0's
+    seven E8@4 matrices, against a bf16 GEMV (torch.mv) on the same weights
+    decoded to bf16; both cold (1 GiB scratch write before each run)."""
+    layer = [m for m in mats if m["layer"] == 0]
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    xs = [W.activations(device=dev, tokens=1, features=m["plan"].cols)[0].contiguous() for m in layer]
+    ws = [torch.empty(H.hq_gemv_workspace_bytes(m["plan"]), dtype=torch.uint8, device=dev)
+          for m in layer]
+    ys = [torch.empty((m["s"].rows,), dtype=torch.float32, device=dev) for m in layer]
+    wb = [H.hq_decode(m["plan"], m["s"], out_dtype=torch.bfloat16) for m in layer]
+    yb = [torch.empty((m["s"].rows,), dtype=torch.bfloat16, device=dev) for m in layer]
+
+    def fused():
+        for m, x, w, y in zip(layer, xs, ws, ys):
+            H.hq_decode_gemv(m["plan"], m["s"], x, workspace=w, out=y)
+
+    def dense():
+        for w, x, y in zip(wb, xs, yb):
+            torch.mv(w, x, out=y)
+
+    fused()
+    dense()
+    torch.cuda.synchronize()
+    tf = _median_ms(fused, reps, flush) * 1e-3
+    td = _median_ms(dense, reps, flush) * 1e-3
+    n = sum(m["x"].numel() for m in layer)
+    stream_bytes = sum(int(m["s"].end_words()) * 4 for m in layer) + n / 128 * 4 + n / 512 * 5
+    del flush, wb
+    torch.cuda.empty_cache()
+    return {"workload": "layer 0 of the stack (7 matrices, 218M E8@4 weights), one bf16 token",
+            "fused_ms": round(tf * 1e3, 4), "bf16_gemv_ms": round(td * 1e3, 4),
+            "fused_weights_per_s_e9": round(n / tf / 1e9, 1),
+            "fused_stream_GBs": round(stream_bytes / tf / 1e9, 1),
+            "bf16_gemv_GBs": round(2 * n / td / 1e9, 1),
+            "speedup_vs_bf16": round(td / tf, 3)}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -452,6 +490,7 @@ def main():
     }
     if not args.no_gemm:
         out["gemm_int8"] = gemm_extra(H, W, mats, dev)
+        out["decode_gemv"] = gemv_extra(H, W, mats, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(mats, args.cpu_seconds)
     if not args.no_other:

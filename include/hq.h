@@ -239,6 +239,26 @@ hq_status hq_dequant_gemm_int8(hq_plan_t plan, const hq_stream* w, int64_t N, co
                                int64_t M, void* out, int32_t ot, void* workspace,
                                size_t ws_bytes, void* stream);
 
+/* Workspace bytes for hq_decode_gemv: one fp32 per column (the transformed x). */
+size_t hq_gemv_workspace_bytes(hq_plan_t plan);
+
+/* hq_decode_gemv -- y[r] = sum_k W^[row0 + r, k] x[k] for r < rows: the
+ * decode of a weight stream fused with a matrix-vector product (the fused
+ * decode-GEMV of Sec. 6.6, for one token).  The RHT moves onto x (Sec. 4.1:
+ * H is symmetric, so each tile's product is g coord(c) . (H D x)), and the
+ * decoded rows never reach memory.
+ *   x          device, plan.cols values, HQ_BF16 or HQ_FP32, 16-byte aligned.
+ *   y          device, rows values, HQ_FP32 or HQ_BF16 (round to nearest even).
+ *   workspace  device, 16-byte aligned, >= hq_gemv_workspace_bytes(plan).
+ * The sums run in fp32 in a fixed order (per lane along the row, a butterfly
+ * over each wave, then the four waves of the row's workgroup), so they differ
+ * from a decode-then-multiply by rounding only and repeat bit for bit.
+ * Plans with a rotation or a dither (KV streams): HQ_ERR_UNSUPPORTED.  A
+ * corrupt sub-stream contributes zero and is reported in s->stats. */
+hq_status hq_decode_gemv(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows,
+                         const void* x, int32_t xt, void* y, int32_t yt, void* workspace,
+                         size_t ws_bytes, void* stream);
+
 /* The library's automatic Rice-k rule for `count` symbols summing to `sum`
  * (the geometric optimum k* of Sec. 3.3), as the kernels evaluate it. */
 int32_t hq_rice_kstar(int64_t count, int64_t sum);

@@ -386,6 +386,14 @@ def decode(params: Params, st: Stream):
     return backend(params, codes, st.norms)
 
 
+def decode_gemv(params: Params, codes, norms, x, row0=0):
+    """The decode fused with a matrix-vector product (the fused decode-GEMV of
+    Sec. 6.6): y = W^ x for one token, W^ the decoded rows exactly as the
+    decode defines them (backend), the products summed in fp64."""
+    w = backend(params, codes, norms, row0=row0).astype(np.float64)
+    return w @ np.asarray(x, dtype=np.float64)
+
+
 def weight_factors(params: Params, norms, rows, cols):
     g = np.zeros((rows, cols // params.tile), dtype=np.float32)
     P = params.c()

@@ -542,6 +542,25 @@ hq_status hq_decode(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
   return hip_status(hq_launch_decode(p, a, yt, stream));
 }
 
+size_t hq_gemv_workspace_bytes(hq_plan_t p) { return p ? (size_t)p->cols * sizeof(float) : 0; }
+
+hq_status hq_decode_gemv(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
+                         const void* x, int32_t xt, void* y, int32_t yt, void* workspace,
+                         size_t ws_bytes, void* stream) {
+  if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
+  if ((xt != HQ_BF16 && xt != HQ_FP32) || (yt != HQ_BF16 && yt != HQ_FP32)) return HQ_ERR_INVALID_ARG;
+  if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
+  if (p->rotation || p->dither) return HQ_ERR_UNSUPPORTED;
+  if (rows == 0) return HQ_OK;
+  if (!x || !y || !workspace || !s->payload || !s->offsets || !s->kparam || !s->norms)
+    return HQ_ERR_INVALID_ARG;
+  if (!aligned16(x) || !aligned16(workspace) || ws_bytes < hq_gemv_workspace_bytes(p))
+    return HQ_ERR_INVALID_ARG;
+  hq_decode_args a;
+  fill_decode_args(p, s, row0, rows, &a);
+  return hip_status(hq_launch_decode_gemv(p, a, x, xt, (float*)workspace, y, yt, stream));
+}
+
 hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, void* const* y,
                           int32_t yt, const int64_t* ld, int32_t count, void* stream) {
   if (count < 0 || (count > 0 && (!plans || !s || !y || !ld))) return HQ_ERR_INVALID_ARG;

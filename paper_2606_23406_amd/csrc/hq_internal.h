@@ -141,6 +141,10 @@ struct hq_gemm_args {
 int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, const hq_rice_thr& t, int xt,
                      void* stream);
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream);
+// Fused decode + GEMV: xtr (cols fp32) receives H D x per tile, then y (rows)
+// the decoded rows' products with x.
+int hq_launch_decode_gemv(const hq_plan_s* p, const hq_decode_args& a, const void* x, int xt,
+                          float* xtr, void* y, int yt, void* stream);
 int hq_launch_encode_group(const hq_plan_s* p, const hq_encode_group_args& g, uint32_t nwg,
                            uint32_t lds_words, int xt, void* stream);
 int hq_launch_decode_group(const hq_plan_s* p, const hq_decode_group_args& g, uint32_t nwg,

@@ -132,6 +132,23 @@ __device__ __forceinline__ uint32_t byte_select_entry(uint32_t v) {
   return e;
 }
 
+// The whole table, built at compile time; kernels copy it into LDS.
+struct ByteSelectTable {
+  uint32_t e[256];
+  constexpr ByteSelectTable() : e() {
+    for (uint32_t v = 0; v < 256; ++v) {
+      uint32_t x = 0, k = 0;
+      for (uint32_t b = 0; b < 8; ++b)
+        if ((v >> b) & 1u) {
+          x |= b << (4 * k);
+          ++k;
+        }
+      e[v] = x;
+    }
+  }
+};
+__constant__ ByteSelectTable kByteSelect = ByteSelectTable();
+
 // Position (0..31) of the r-th set bit (r from 0, r < popc(w)) of w: the
 // byte from cumulative byte popcounts, the bit from the table.
 __device__ __forceinline__ uint32_t select32_lut(uint32_t w, uint32_t r, const uint32_t* tbl) {
@@ -1155,7 +1172,7 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
               kEpochMask;
   const TwSigns sg(lane);
 
-  // ---- this wave's sub-streams: wg * NSUB + i * 4 + wave, i < SPW (row and
+  // ---- this wave's sub-streams: wg * NSUB + i * WAVES + wave, i < SPW (row and
   //      column advanced on scalar registers)
   SubPos pos[SPW];
   {
@@ -1712,6 +1729,114 @@ __global__ __launch_bounds__(256) void hq_decode_group_kernel(hq_decode_group_ar
   decode_wg<LAT, MODE, KV>(G.m[mi], blockIdx.x - G.wg_begin[mi]);
 }
 
+// ------------------------------------------------------------ fused decode + GEMV
+// y[r] = sum_k W^[r, k] x[k] for one token: the decode fused with a
+// matrix-vector product (the fused decode-GEMV kernel of Sec. 6.6).  On a
+// weight plan, tile t of decoded row r is
+// g_t D_t H coord(c_t) with H the symmetric unnormalized Walsh-Hadamard
+// matrix (the RHT absorbed into the product, Sec. 4.1), so its product with
+// x_t is g_t coord(c_t) . (H D_t x_t): the transform moves from every row
+// onto x, once per call (hq_gemv_prep_kernel), and a row costs its Rice
+// decode, the unstrip and one dot product per lattice block.  One workgroup
+// per row: each wave walks a fixed share of the row's sub-streams with a
+// per-lane partial sum, a fixed butterfly over the wave and a fixed order
+// over the four waves follow, so the result does not depend on scheduling.
+
+// xt = H D x per 128-column tile, fp32; one wave per 512 columns.
+__global__ __launch_bounds__(256) void hq_gemv_prep_kernel(const void* x, int x_bf16, int64_t K,
+                                                           const uint32_t* dmask, float* xt) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int64_t base = ((int64_t)blockIdx.x * 4 + (tid >> 6)) * HQ_SUB;
+  if (base >= K) return;  // K is a multiple of 512
+  const int64_t col = base + (lane >> 4) * HQ_TILE + (lane & 15) * 8;
+  float v[8];
+  if (x_bf16) {
+    const uint4 raw = *(const uint4*)((const uint16_t*)x + col);
+    const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = bf16_to_f32(w4[i] & 0xFFFFu);
+      v[2 * i + 1] = bf16_to_f32(w4[i] >> 16);
+    }
+  } else {
+    const float4 a = *(const float4*)((const float*)x + col);
+    const float4 b = *(const float4*)((const float*)x + col + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+  const uint32_t dbits = sign_bits8(dmask, col);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = flip(v[i], dbits, i);
+  const XSigns sg(lane);
+  fwht128(v, sg);
+  *(float4*)(xt + col) = make_float4(v[0], v[1], v[2], v[3]);
+  *(float4*)(xt + col + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+template <int LAT>
+__global__ __launch_bounds__(256) void hq_decode_gemv_kernel(hq_decode_args A, const float* xt,
+                                                             void* y, int y_bf16) {
+  extern __shared__ uint32_t smem[];
+  __shared__ uint32_t s_sel[256];
+  __shared__ float s_part[HQ_WAVES_PER_WG];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint32_t wave = readfirst((uint32_t)(tid >> 6));
+  uint32_t* buf = smem + wave * (A.lds_words + 66);
+  uint32_t* starts = buf + A.lds_words + 2;
+  s_sel[tid] = kByteSelect.e[tid];  // 256 threads, one entry each
+  __syncthreads();
+  // one row per workgroup: wave w takes the row's sub-streams w, w + 4, ...,
+  // each one's table entry and first payload words loaded a step ahead
+  const uint32_t spr = (uint32_t)A.spr;
+  const int64_t row = blockIdx.x;  // within the call's rows
+  const uint32_t sub0 = (uint32_t)A.first_sub + (uint32_t)row * spr;
+  const bool fp16_norm = A.norm_fp16;
+  auto head_of = [&](uint32_t j) {
+    const uint32_t start = readfirst(A.offsets[sub0 + j]), end = readfirst(A.offsets[sub0 + j + 1]);
+    return dec_head<LAT>(A, true, start, end, readfirst(A.kparam[sub0 + j]), lane);
+  };
+  float acc = 0.0f;
+  DecHead head;
+  if (wave < spr) head = head_of(wave);
+  for (uint32_t j = wave; j < spr; j += HQ_WAVES_PER_WG) {
+    DecHead next;
+    if (j + HQ_WAVES_PER_WG < spr) next = head_of(j + HQ_WAVES_PER_WG);
+    uint32_t sym[8];
+    const bool ok = decode_symbols<LAT>(A, head, lane, buf, starts, s_sel, sym);
+    if (!ok && A.stats) {
+      const unsigned long long bad = __ballot(!ok);
+      if ((unsigned)lane == (unsigned)__builtin_ctzll(bad)) {
+        atomicAdd(&A.stats->corrupt_substreams, 1u);
+        atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+      }
+    }
+    int32_t c[8];
+    unstrip8<LAT>(sym, c);
+    const int64_t col = (int64_t)j * HQ_SUB + 8 * lane;
+    const float4 xa = *(const float4*)(xt + col);
+    const float4 xb = *(const float4*)(xt + col + 4);
+    const float xv[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+    float d = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) d = __builtin_fmaf(code_coord<LAT>(c[i], i), xv[i], d);
+    const int64_t t = (A.first_row + row) * A.tpr + 4 * (int64_t)j + (lane >> 4);
+    const float rs = fp16_norm ? (float)((const _Float16*)A.norms)[t] : ((const float*)A.norms)[t];
+    acc = __builtin_fmaf(rs, d, acc);  // the common 1 / (alpha n) once per row
+    head = next;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
+  if (lane == 0) s_part[wave] = acc;
+  __syncthreads();
+  if (tid == 0) {
+    const float v = (((s_part[0] + s_part[1]) + s_part[2]) + s_part[3]) / A.alpha_n;
+    if (y_bf16)
+      ((uint16_t*)y)[row] = (uint16_t)f32_to_bf16(v);
+    else
+      ((float*)y)[row] = v;
+  }
+}
+
 // ------------------------------------------------------------ activation prep
 // One workgroup per token row: per 128-column tile y = H D a (canonical stage
 // order, the weights' signs), amax over the row, then int8.
@@ -2094,5 +2219,30 @@ int hq_launch_zero(void* ptr, size_t bytes, void* stream) {
   if (n == 0) return 0;
   hipLaunchKernelGGL(hq_zero_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0,
                      (hipStream_t)stream, (uint32_t*)ptr, n);
+  return (int)hipGetLastError();
+}
+
+int hq_launch_decode_gemv(const hq_plan_s* p, const hq_decode_args& a, const void* x, int xt,
+                          float* xtr, void* y, int yt, void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  const int64_t K = p->cols;
+  hipLaunchKernelGGL(hq_gemv_prep_kernel, dim3((uint32_t)((K + 4 * HQ_SUB - 1) / (4 * HQ_SUB))),
+                     dim3(256), 0, st, x, xt == HQ_BF16 ? 1 : 0, K, a.dmask, xtr);
+  const uint32_t nwg = (uint32_t)(a.nsub / a.spr);  // one workgroup per row
+  const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
+  const int yb = yt == HQ_BF16 ? 1 : 0;
+  switch (p->lattice) {
+    case HQ_E8:
+      hipLaunchKernelGGL(hq_decode_gemv_kernel<kE8>, dim3(nwg), dim3(256), lds, st, a, xtr, y, yb);
+      break;
+    case HQ_D4:
+      hipLaunchKernelGGL(hq_decode_gemv_kernel<kD4>, dim3(nwg), dim3(256), lds, st, a, xtr, y, yb);
+      break;
+    case HQ_A2:
+      hipLaunchKernelGGL(hq_decode_gemv_kernel<kA2>, dim3(nwg), dim3(256), lds, st, a, xtr, y, yb);
+      break;
+    default:
+      hipLaunchKernelGGL(hq_decode_gemv_kernel<kZ>, dim3(nwg), dim3(256), lds, st, a, xtr, y, yb);
+  }
   return (int)hipGetLastError();
 }

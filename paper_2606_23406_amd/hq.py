@@ -97,6 +97,10 @@ def lib():
     L.hq_gemm_workspace_bytes.argtypes = [p, i64, i64]
     L.hq_dequant_gemm_int8.restype = i32
     L.hq_dequant_gemm_int8.argtypes = [p, p, i64, p, i64, p, i32, p, C.c_size_t, p]
+    L.hq_gemv_workspace_bytes.restype = C.c_size_t
+    L.hq_gemv_workspace_bytes.argtypes = [p]
+    L.hq_decode_gemv.restype = i32
+    L.hq_decode_gemv.argtypes = [p, p, i64, i64, p, i32, p, i32, p, C.c_size_t, p]
     L.hq_rice_kstar.restype = i32
     L.hq_rice_kstar.argtypes = [i64, i64]
     L.hq_calibrated_snr.restype = i32
@@ -314,6 +318,28 @@ def hq_dequant_gemm_int8(plan: Plan, w: EncodedStream, a: torch.Tensor, out_dtyp
     return out
 
 
+def hq_gemv_workspace_bytes(plan: Plan):
+    return lib().hq_gemv_workspace_bytes(plan.handle)
+
+
+def hq_decode_gemv(plan: Plan, s: EncodedStream, x: torch.Tensor, row0=0, rows=None,
+                   out_dtype=torch.float32, workspace=None, out=None, stream=None):
+    """hq_decode_gemv: y[r] = sum_k W^[row0 + r, k] x[k], the decoded rows
+    never materialized.  x: plan.cols values (bf16 or fp32) on the device."""
+    rows = s.rows - row0 if rows is None else rows
+    assert x.is_cuda and x.dim() == 1 and x.stride(0) == 1 and x.numel() == plan.cols
+    if workspace is None:
+        workspace = torch.empty(hq_gemv_workspace_bytes(plan), dtype=torch.uint8, device=x.device)
+    if out is None:
+        out = torch.empty((rows,), dtype=out_dtype, device=x.device)
+    st = lib().hq_decode_gemv(plan.handle, C.byref(s.c), row0, rows, C.c_void_p(x.data_ptr()),
+                              _dtype_code(x.dtype), C.c_void_p(out.data_ptr()),
+                              _dtype_code(out.dtype), C.c_void_p(workspace.data_ptr()),
+                              workspace.numel(), _stream_handle(stream))
+    _check("hq_decode_gemv", st)
+    return out
+
+
 def hq_rice_kstar(count, total):
     return lib().hq_rice_kstar(int(count), int(total))
 
@@ -327,5 +353,6 @@ def hq_calibrated_snr(lattice, rice_k, bps):
 
 EXPORTED = ["hq_plan", "hq_plan_destroy", "hq_plan_get_info", "hq_scan_bytes", "hq_encode",
             "hq_decode", "hq_encode_group", "hq_decode_group", "hq_decode_int8", "hq_act_prep", "hq_gemm_int8_blockscaled",
-            "hq_gemm_workspace_bytes", "hq_dequant_gemm_int8", "hq_rice_kstar",
+            "hq_gemm_workspace_bytes", "hq_dequant_gemm_int8", "hq_gemv_workspace_bytes",
+            "hq_decode_gemv", "hq_rice_kstar",
             "hq_calibrated_snr", "hq_status_string"]

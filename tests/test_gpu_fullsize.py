@@ -169,6 +169,42 @@ def test_c3_first_launch_group_as_benched(hq):
     assert len(shapes) == 4
 
 
+def test_c3_decode_gemv_gate(hq):
+    """The fused decode-GEMV on layer 0's gate matrix (14336 x 4096, E8@4) with
+    one bf16 token: sampled rows against the oracle's decoded row times x in
+    fp64, to 1e-6 of sum_k |W^[r, k] x[k]|."""
+    from paper_2606_23406_amd import workloads as W
+    snr = PT.op_snr("E8", 4.0)
+    idx = [n for n, _, _ in W.LLAMA_LINEARS].index("gate")
+    _, out_f, in_f = W.LLAMA_LINEARS[idx]
+    P = PT.oracle_params(O.E8, snr, rht_seed=W.llama_linear_seed(0, idx))
+    plan = PT.gpu_plan(hq, P, snr, in_f)
+    xd = W.llama_linear(0, idx, device="cuda")
+    s = hq.EncodedStream(plan, out_f)
+    hq.hq_encode(plan, xd, s)
+    x = W.activations(tokens=1, features=in_f)[0].cuda()
+    print(f"[fullsize] decode_gemv gate {out_f}x{in_f}", flush=True)
+    y = hq.hq_decode_gemv(plan, s, x).cpu().numpy().astype(np.float64)
+    torch.cuda.synchronize()
+    assert s.read_stats()["status"] == 0
+    xs = x.float().cpu().numpy().astype(np.float64)
+    spr = plan.info.subs_per_row
+    gpu = PT.gpu_stream_arrays(s, s.rows)
+    rng = np.random.default_rng(77)
+    worst = 0.0
+    for r in np.sort(rng.choice(out_f, 8, replace=False)):
+        xr = xd[int(r):int(r) + 1].float().cpu().numpy()
+        res = PT.compare_streams(P, xr, row_stream(gpu, int(r), spr))
+        gc = res["codes"] if res["gpu_codes"] is None else res["gpu_codes"]  # the stream's codes
+        ref = O.decode_gemv(P, gc, res["norms"], xs)[0]
+        scale = np.abs(O.backend(P, gc, res["norms"]).astype(np.float64)[0]) @ np.abs(xs)
+        err = abs(y[r] - ref) / scale
+        worst = max(worst, err)
+        assert err <= 1e-6, (r, err)
+    print(f"[fullsize] decode_gemv gate: 8 sampled rows, worst error {worst:.2e} of sum |w x|",
+          flush=True)
+
+
 @pytest.fixture(scope="module")
 def kv_keys():
     from paper_2606_23406_amd import workloads as W

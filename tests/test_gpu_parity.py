@@ -277,3 +277,55 @@ def test_launch_shapes_agree_at_the_small_launch_bound(hq, rows):
     assert torch.equal(a.offsets, b.offsets) and torch.equal(a.kparam, b.kparam)
     assert torch.equal(a.norms, b.norms)
     assert a.read_stats() == b.read_stats()
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2, O.Z])
+def test_decode_gemv_matches_oracle(hq, lat):
+    """hq_decode_gemv (the decode fused with a matrix-vector product) against
+    the oracle's decoded rows times x in fp64: row windows with ragged
+    counts, bf16 and fp32 x, fp32 and bf16 y.  Tolerance 1e-6 of
+    sum_k |W^[r, k] x[k]| (fp32 sums, some 60x the largest error seen; one
+    wrong element moves y by about 1/1536 of it); the bf16 result is the
+    fp32 one rounded to nearest even."""
+    snr = 20.0
+    rows, cols = 37, 1536
+    P = PT.oracle_params(lat, snr, rht_seed=71)
+    w = gauss(rows, cols, 72, 0.02, torch.bfloat16)
+    plan, s = encode_gpu(hq, P, snr, w)
+    res = PT.compare_streams(P, w.float().numpy(), PT.gpu_stream_arrays(s, rows))
+    gc = res["codes"] if res["gpu_codes"] is None else res["gpu_codes"]  # the stream's codes
+    wd = O.backend(P, gc, res["norms"]).astype(np.float64)
+    worst = 0.0
+    for xdt in (torch.float32, torch.bfloat16):
+        x = gauss(1, cols, 73, 1.0, xdt)[0]
+        xs = x.float().numpy().astype(np.float64)
+        for row0, n in ((0, rows), (5, 17), (36, 1)):
+            print(f"[parity] decode_gemv {LAT_NAMES[lat]} x={xdt} rows {row0}+{n}", flush=True)
+            ref = O.decode_gemv(P, gc[row0:row0 + n], res["norms"][row0:row0 + n], xs, row0=row0)
+            scale = np.abs(wd[row0:row0 + n]) @ np.abs(xs)
+            y = hq.hq_decode_gemv(plan, s, x.cuda(), row0=row0, rows=n).cpu().numpy()
+            err = np.abs(y.astype(np.float64) - ref) / scale
+            worst = max(worst, float(err.max()))
+            assert np.all(err <= 1e-6), (row0, n, err.max())
+            yb = hq.hq_decode_gemv(plan, s, x.cuda(), row0=row0, rows=n, out_dtype=torch.bfloat16)
+            assert torch.equal(yb.cpu(), torch.from_numpy(y).to(torch.bfloat16))
+    print(f"[parity] decode_gemv {LAT_NAMES[lat]}: worst error {worst:.2e} of sum |w x|", flush=True)
+    assert s.read_stats()["corrupt_substreams"] == 0
+
+
+def test_decode_gemv_argument_errors(hq):
+    P = PT.oracle_params(O.E8, 20.0)
+    plan = PT.gpu_plan(hq, P, 20.0, 512)
+    s = hq.EncodedStream(plan, 4)
+    hq.hq_encode(plan, torch.zeros((4, 512), device="cuda"), s)
+    x = torch.zeros(512, device="cuda")
+    with pytest.raises(hq.HQError):  # workspace too small
+        hq.hq_decode_gemv(plan, s, x, workspace=torch.empty(16, dtype=torch.uint8, device="cuda"))
+    with pytest.raises(hq.HQError):  # rows past the stream
+        hq.hq_decode_gemv(plan, s, x, row0=3, rows=2)
+    kv = hq.hq_plan(128, hq.HQ_E8, 0.0, 5, -1, 512, snr_db=20.0, rotation=1, dither=True)
+    skv = hq.EncodedStream(kv, 4)
+    hq.hq_encode(kv, torch.zeros((4, 512), device="cuda"), skv)
+    with pytest.raises(hq.HQError):  # dithered / rotated streams are not supported
+        hq.hq_decode_gemv(kv, skv, x)
+    torch.cuda.synchronize()

@@ -297,3 +297,34 @@ def test_gemm_blockscaled_equals_dense_fp64():
     # the decoded weights equal the oracle's decoder output
     st = O.encode(P, w)
     assert np.allclose(O.decode(P, st), w_hat, rtol=0, atol=1e-6 * np.abs(w_hat).max())
+
+
+@pytest.mark.parametrize("lat", LATS)
+def test_decode_gemv_equals_transform_on_x(lat):
+    # Sec. 6.6 with Sec. 4.1: tile t of a decoded row is g D H coord(c) with H
+    # symmetric, so W^ x = sum_t g coord(c) . (H D x) -- the identity the fused
+    # decode-GEMV kernel evaluates -- against the decode's definition times x.
+    rng = np.random.default_rng(11 + lat)
+    N, K, n = 24, 1024, 128
+    w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    x = rng.standard_normal(K).astype(np.float32)
+    P = O.Params(lattice=lat, alpha=O.alpha(lat, 20.0), rht_seed=29)
+    codes, norms, _, _ = O.frontend(P, w)
+    y = O.decode_gemv(P, codes, norms, x)
+    g = O.weight_factors(P, norms, N, K).astype(np.float64)
+    pts = O.lattice_points(lat, codes)
+    xt = (x.astype(np.float64) * O.signs(29, K)).reshape(K // n, n)
+    xt = O.fwht(xt)
+    ref = np.zeros(N)
+    for t in range(K // n):
+        ref += g[:, t] * (pts[:, t * n:(t + 1) * n] @ xt[t])
+    scale = np.abs(O.backend(P, codes, norms).astype(np.float64)) @ np.abs(x.astype(np.float64))
+    assert np.all(np.abs(y - ref) <= 1e-6 * scale)
+    # and it approximates the unquantized product
+    exact = w.astype(np.float64) @ x.astype(np.float64)
+    assert np.linalg.norm(y - exact) / np.linalg.norm(exact) < 0.2
+    # x = e_k picks column k of the decoded rows
+    e = np.zeros(K, np.float32)
+    e[300] = 1.0
+    assert np.array_equal(O.decode_gemv(P, codes, norms, e),
+                          O.backend(P, codes, norms)[:, 300].astype(np.float64))
