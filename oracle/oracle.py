@@ -394,6 +394,41 @@ def decode_gemv(params: Params, codes, norms, x, row0=0):
     return w @ np.asarray(x, dtype=np.float64)
 
 
+def decode_attention(pk: Params, k_codes, k_norms, pv: Params, v_codes, v_norms, q,
+                     block_table, seq_lens, block_tokens, scale):
+    """One-token attention over a coded KV cache (the KV path of Sec. 5.2 and
+    the decode of Sec. 5.3 feeding attention, as the end-to-end runs of Sec.
+    6.6 use it): the cached keys and values are the decoded rows exactly as
+    the decode defines them (backend), gathered per sequence through a block
+    table, and each query head attends with a softmax in fp64.
+      k_codes, v_codes  all stored rows' lattice codes, [rows, H_kv * tile].
+      q                 [batch, H_q, tile]; query head h reads KV head
+                        h // (H_q / H_kv).
+      block_table       [batch, max_blocks]: token t of sequence b is stored
+                        row block_table[b, t // block_tokens] * block_tokens
+                        + t % block_tokens.
+      seq_lens          [batch] token counts; an empty sequence gives zeros.
+    Returns [batch, H_q, tile] fp64."""
+    kd = backend(pk, k_codes, k_norms).astype(np.float64)
+    vd = backend(pv, v_codes, v_norms).astype(np.float64)
+    q = np.asarray(q, dtype=np.float64)
+    B, Hq, n = q.shape
+    G = Hq // (kd.shape[1] // n)
+    out = np.zeros((B, Hq, n))
+    for b in range(B):
+        T = int(seq_lens[b])
+        if T == 0:
+            continue
+        t = np.arange(T)
+        rows = np.asarray(block_table[b])[t // block_tokens].astype(np.int64) * block_tokens + t % block_tokens
+        for h in range(Hq):
+            cs = slice((h // G) * n, (h // G + 1) * n)
+            s = (kd[rows, cs] @ q[b, h]) * scale
+            p = np.exp(s - s.max())
+            out[b, h] = (p / p.sum()) @ vd[rows, cs]
+    return out
+
+
 def weight_factors(params: Params, norms, rows, cols):
     g = np.zeros((rows, cols // params.tile), dtype=np.float32)
     P = params.c()
