@@ -259,6 +259,55 @@ hq_status hq_decode_gemv(hq_plan_t plan, const hq_stream* s, int64_t row0, int64
                          const void* x, int32_t xt, void* y, int32_t yt, void* workspace,
                          size_t ws_bytes, void* stream);
 
+/* Workspace bytes for hq_decode_attention with `batch` sequences of at most
+ * max_tokens = max_blocks * block_tokens tokens and heads_q query heads:
+ * the query in coded coordinates plus one partial sum (128 values, a maximum
+ * and a weight) per query head and token split; 0 for invalid arguments. */
+size_t hq_attention_workspace_bytes(hq_plan_t k_plan, int64_t batch, int32_t heads_q,
+                                    int64_t max_tokens);
+
+/* hq_decode_attention -- one query token per sequence attending over a coded
+ * KV cache: out[b, h] = sum_t softmax_t(scale q[b, h] . k^_t) v^_t, k^ and
+ * v^ the rows hq_decode would return for the key and value streams (the KV
+ * path of Sec. 5.2 read as in Sec. 5.3, for the one-token decoding of Sec.
+ * 6.6).  The decoded keys and values never reach memory: a key tile is
+ * g D H S (code - U) (Sec. 4.1, 4.2, 4.4, H symmetric), so the query is
+ * moved once into those coordinates, each score is g (S H D q) . (code - U),
+ * the value sum stays in the same coordinates and one inverse transform per
+ * head ends it.
+ *   k_plan, k / v_plan, v   key and value plans and streams: one lattice,
+ *               tile 128, sub-stream 512 and column count (H_kv * 128: row r
+ *               of a stream holds token r's H_kv head vectors); seeds,
+ *               rates, rotation, dither and norm precision may differ.  Rows
+ *               are used up to min(k->rows, v->rows).
+ *   q           device [batch, heads_q, 128], HQ_BF16 or HQ_FP32, 16-byte
+ *               aligned; head h reads KV head h / (heads_q / H_kv), a group
+ *               of 1, 2, 4 or 8 (HQ_ERR_UNSUPPORTED otherwise).
+ *   scale       softmax scale (1 / sqrt(128) for standard attention).
+ *   block_table device int32 [batch, max_blocks]: token t of sequence b is
+ *               row block_table[b, t / block_tokens] * block_tokens
+ *               + t % block_tokens of both streams (a paged cache; one block
+ *               per sequence with block_tokens = its length is a plain one).
+ *   seq_lens    device int32 [batch] token counts; an empty sequence gives
+ *               zeros.
+ *   out         device [batch, heads_q, 128], HQ_FP32 or HQ_BF16 (round to
+ *               nearest even), 16-byte aligned.
+ *   workspace   device, 16-byte aligned, >= hq_attention_workspace_bytes(
+ *               k_plan, batch, heads_q, max_blocks * block_tokens).
+ * Sums run in fp32 in an order fixed by the call's shape (batch, heads,
+ * max_blocks * block_tokens), so results repeat bit for bit and differ from
+ * decode-then-attend by rounding only.  Device-side errors go to k->stats:
+ * a length outside 0 .. max_blocks * block_tokens is clamped and a block id
+ * whose rows lie outside the streams is skipped (both HQ_ERR_INVALID_ARG);
+ * a corrupt sub-stream counts as HQ_ERR_CORRUPT.  Host errors:
+ * HQ_ERR_INVALID_ARG, HQ_ERR_UNSUPPORTED, HQ_ERR_HIP. */
+hq_status hq_decode_attention(hq_plan_t k_plan, const hq_stream* k, hq_plan_t v_plan,
+                              const hq_stream* v, const void* q, int32_t qt, int64_t batch,
+                              int32_t heads_q, float scale, const int32_t* block_table,
+                              int32_t max_blocks, int32_t block_tokens, const int32_t* seq_lens,
+                              void* out, int32_t ot, void* workspace, size_t ws_bytes,
+                              void* stream);
+
 /* The library's automatic Rice-k rule for `count` symbols summing to `sum`
  * (the geometric optimum k* of Sec. 3.3), as the kernels evaluate it. */
 int32_t hq_rice_kstar(int64_t count, int64_t sum);

@@ -561,6 +561,83 @@ hq_status hq_decode_gemv(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t 
   return hip_status(hq_launch_decode_gemv(p, a, x, xt, (float*)workspace, y, yt, stream));
 }
 
+// Tokens per wave of the fused attention: about 4096 waves over the call
+// (every SIMD four deep), from 16 to 1024 tokens each.
+static int64_t attn_chunk(const hq_plan_s* k, int64_t batch, int64_t max_tokens) {
+  const int64_t work = batch * k->spr * max_tokens;
+  return std::min<int64_t>(1024, std::max<int64_t>(16, (work + 4095) / 4096));
+}
+
+static int64_t attn_splits(int64_t max_tokens, int64_t chunk) {
+  const int64_t per = HQ_WAVES_PER_WG * chunk;
+  return (max_tokens + per - 1) / per;
+}
+
+size_t hq_attention_workspace_bytes(hq_plan_t k, int64_t batch, int32_t heads_q,
+                                    int64_t max_tokens) {
+  if (!k || batch < 0 || heads_q <= 0 || max_tokens <= 0) return 0;
+  const int64_t nx = attn_splits(max_tokens, attn_chunk(k, batch, max_tokens));
+  const int64_t heads = batch * heads_q;
+  return (size_t)(heads * HQ_TILE + heads * nx * (HQ_TILE + 2)) * sizeof(float);
+}
+
+hq_status hq_decode_attention(hq_plan_t pk, const hq_stream* k, hq_plan_t pv, const hq_stream* v,
+                              const void* q, int32_t qt, int64_t batch, int32_t heads_q,
+                              float scale, const int32_t* block_table, int32_t max_blocks,
+                              int32_t block_tokens, const int32_t* seq_lens, void* out,
+                              int32_t ot, void* workspace, size_t ws_bytes, void* stream) {
+  if (!pk || !k || !pv || !v || batch < 0) return HQ_ERR_INVALID_ARG;
+  if ((qt != HQ_BF16 && qt != HQ_FP32) || (ot != HQ_BF16 && ot != HQ_FP32)) return HQ_ERR_INVALID_ARG;
+  if (pk->lattice != pv->lattice || pk->cols != pv->cols || pk->tile != HQ_TILE ||
+      pv->tile != HQ_TILE || pk->substream != HQ_SUB || pv->substream != HQ_SUB)
+    return HQ_ERR_INVALID_ARG;
+  const int64_t hkv = pk->cols / HQ_TILE;
+  if (heads_q <= 0 || heads_q % hkv != 0) return HQ_ERR_INVALID_ARG;
+  const int64_t group = heads_q / hkv;
+  if (group != 1 && group != 2 && group != 4 && group != 8) return HQ_ERR_UNSUPPORTED;
+  if (max_blocks <= 0 || block_tokens <= 0 || !std::isfinite(scale)) return HQ_ERR_INVALID_ARG;
+  const int64_t max_tokens = (int64_t)max_blocks * block_tokens;
+  if (max_tokens > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
+  if (batch == 0) return HQ_OK;
+  if (!q || !out || !block_table || !seq_lens || !workspace || !aligned16(q) || !aligned16(out) ||
+      !aligned16(workspace))
+    return HQ_ERR_INVALID_ARG;
+  if (ws_bytes < hq_attention_workspace_bytes(pk, batch, heads_q, max_tokens))
+    return HQ_ERR_INVALID_ARG;
+  if (!k->payload || !k->offsets || !k->kparam || !k->norms || !v->payload || !v->offsets ||
+      !v->kparam || !v->norms)
+    return HQ_ERR_INVALID_ARG;
+  const int64_t chunk = attn_chunk(pk, batch, max_tokens);
+  const int64_t nx = attn_splits(max_tokens, chunk);
+  if (batch * pk->spr * nx > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
+  hq_attn_args a;
+  std::memset(&a, 0, sizeof(a));
+  fill_decode_args(pk, k, 0, k->rows, &a.K);
+  fill_decode_args(pv, v, 0, v->rows, &a.V);
+  a.q = q;
+  a.out = out;
+  a.table = block_table;
+  a.seq_lens = seq_lens;
+  const int64_t heads = batch * heads_q;
+  a.qt = (float*)workspace;
+  a.part_acc = a.qt + heads * HQ_TILE;
+  a.part_m = a.part_acc + heads * nx * HQ_TILE;
+  a.part_l = a.part_m + heads * nx;
+  a.batch = batch;
+  a.rows = std::min(k->rows, v->rows);
+  a.heads_q = heads_q;
+  a.group = (int32_t)group;
+  a.max_blocks = max_blocks;
+  a.block_tokens = block_tokens;
+  a.chunk = (int32_t)chunk;
+  a.nx = (int32_t)nx;
+  a.q_bf16 = qt == HQ_BF16;
+  a.out_bf16 = ot == HQ_BF16;
+  a.lds_words = std::max(a.K.lds_words, a.V.lds_words);
+  a.qscale = scale * 1.4426950408889634f;  // log2(e): the softmax runs in base 2
+  return hip_status(hq_launch_decode_attention(a, pk->lattice, stream));
+}
+
 hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, void* const* y,
                           int32_t yt, const int64_t* ld, int32_t count, void* stream) {
   if (count < 0 || (count > 0 && (!plans || !s || !y || !ld))) return HQ_ERR_INVALID_ARG;

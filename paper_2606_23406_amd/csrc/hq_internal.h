@@ -103,6 +103,31 @@ struct hq_decode_args {
   float alpha_n;           // alpha * tile, exact
 };
 
+// One-token attention over coded K and V streams (fused decode + attention).
+// Workspace: qt [batch * heads_q * 128] query in coded coordinates, then per
+// (sequence, query head, token split) the running sum of 128 values, its
+// running maximum and its weight.
+struct hq_attn_args {
+  hq_decode_args K, V;
+  const void* q;
+  void* out;
+  const int32_t* table;     // batch x max_blocks block ids
+  const int32_t* seq_lens;  // batch token counts
+  float* qt;
+  float* part_acc;
+  float* part_m;
+  float* part_l;
+  int64_t batch;
+  int64_t rows;             // rows present in both streams
+  int32_t heads_q, group;   // query heads, query heads per KV head
+  int32_t max_blocks, block_tokens;
+  int32_t chunk;            // tokens per wave
+  int32_t nx;               // token splits per sequence (4 waves each)
+  int32_t q_bf16, out_bf16;
+  uint32_t lds_words;       // decode buffer words (the larger of K's and V's)
+  float qscale;             // softmax scale times log2(e)
+};
+
 // Several matrices in one launch (kernel arguments, by value): member i owns
 // workgroups wg_begin[i] .. wg_begin[i + 1] - 1 (the last one to the grid end).
 #define HQ_GROUP_MAX 16
@@ -143,6 +168,7 @@ int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, const hq_rice_
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream);
 // Fused decode + GEMV: xtr (cols fp32) receives H D x per tile, then y (rows)
 // the decoded rows' products with x.
+int hq_launch_decode_attention(const hq_attn_args& a, int lattice, void* stream);
 int hq_launch_decode_gemv(const hq_plan_s* p, const hq_decode_args& a, const void* x, int xt,
                           float* xtr, void* y, int yt, void* stream);
 int hq_launch_encode_group(const hq_plan_s* p, const hq_encode_group_args& g, uint32_t nwg,

@@ -1837,6 +1837,329 @@ __global__ __launch_bounds__(256) void hq_decode_gemv_kernel(hq_decode_args A, c
   }
 }
 
+// ------------------------------------------------------------ fused decode + attention
+// One query token per sequence attending over its coded KV cache (the KV
+// path of Sec. 5.2, read back as in Sec. 5.3, for the one-token decoding of
+// Sec. 6.6).  A decoded key tile is k^ = g D H S (code - U), H the symmetric
+// unnormalized Walsh-Hadamard matrix (Sec. 4.1, 4.2, 4.4), so
+// q . k^ = g (S H D q) . (code - U): the query moves into the coded
+// coordinates once per call (hq_attn_prep_kernel) and a key then costs its
+// Rice decode, the unstrip, its dither and one dot product.  The values are
+// summed in the same coordinates, sum_t p_t v^_t = D H S sum_t p_t g_t
+// (code_t - U_t), and transformed back once per head (hq_attn_combine_kernel).
+// The softmax runs online in base 2 (the query carries scale * log2 e).
+// Work: one workgroup per (sequence, sub-stream column j, split of 4 * chunk
+// tokens); wave w walks its chunk of tokens, its lane group of 16 holding one
+// KV head's tile and the G query heads that read it.  Every sum has a fixed
+// order, so results depend on the call's shape only, not on scheduling.
+
+// Sum over the 16 lanes of a row; every lane gets the same bits.
+__device__ __forceinline__ float row16_sum(float v) {
+  v += xor_lane_f<8>(v);
+  v += xor_lane_f<4>(v);
+  v += xor_lane_f<2>(v);
+  v += xor_lane_f<1>(v);
+  return v;
+}
+
+// Token count of sequence b, clamped to what its table row can hold; a bad
+// value is reported in the key stream's counters.
+__device__ __forceinline__ int64_t attn_seq_len(const hq_attn_args& A, int64_t b, bool report) {
+  const int64_t cap = (int64_t)A.max_blocks * A.block_tokens;
+  int64_t len = A.seq_lens[b];
+  if (len < 0 || len > cap) {
+    if (report && A.K.stats) atomicCAS(&A.K.stats->status, 0u, (uint32_t)HQ_ERR_INVALID_ARG);
+    len = len < 0 ? 0 : cap;
+  }
+  return len;
+}
+
+// qt = (S H D q) * scale * log2(e) per query head, with the key plan's signs
+// (D of the head's own columns); one lane group of 16 per head.
+__global__ __launch_bounds__(256) void hq_attn_prep_kernel(hq_attn_args A) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int64_t pair = ((int64_t)blockIdx.x * HQ_WAVES_PER_WG + (tid >> 6)) * 4 + (lane >> 4);
+  if (pair >= A.batch * A.heads_q) return;  // whole lane groups
+  const int32_t kvh = (int32_t)(pair % A.heads_q) / A.group;
+  const int c0 = (lane & 15) * 8;
+  float v[8];
+  if (A.q_bf16) {
+    const uint4 raw = *(const uint4*)((const uint16_t*)A.q + pair * HQ_TILE + c0);
+    const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = bf16_to_f32(w4[i] & 0xFFFFu);
+      v[2 * i + 1] = bf16_to_f32(w4[i] >> 16);
+    }
+  } else {
+    const float4 a = *(const float4*)((const float*)A.q + pair * HQ_TILE + c0);
+    const float4 b = *(const float4*)((const float*)A.q + pair * HQ_TILE + c0 + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+  const uint32_t dbits = sign_bits8(A.K.dmask, (int64_t)kvh * HQ_TILE + c0);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = flip(v[i], dbits, i);
+  const XSigns sg(lane);
+  fwht128(v, sg);
+  const uint32_t sbits = A.K.rotation ? sign_bits8(A.K.smask, c0) : 0u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = flip(v[i], sbits, i) * A.qscale;
+  float* o = A.qt + pair * HQ_TILE + c0;
+  *(float4*)o = make_float4(v[0], v[1], v[2], v[3]);
+  *(float4*)(o + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+// The lane's 8 coordinates of one coded tile, code - U (U the stream's
+// dither at that row), and the tile factor g = r / (alpha n).
+template <int LAT>
+__device__ __forceinline__ bool attn_tile(const hq_decode_args& S, const DecHead& head, int lane,
+                                          uint32_t* buf, uint32_t* starts, const uint32_t* sel,
+                                          int64_t row, uint32_t j, float* y, float& g) {
+  uint32_t sym[8];
+  const bool ok = decode_symbols<LAT>(S, head, lane, buf, starts, sel, sym);
+  int32_t c[8];
+  unstrip8<LAT>(sym, c);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) y[i] = code_coord<LAT>(c[i], i);
+  if (S.dither) {
+    float u[8];
+    dither8<LAT>(S.dither_seed, row, (int64_t)j * HQ_SUB + 8 * lane, u);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) y[i] = y[i] - u[i];
+  }
+  const int64_t t = row * S.tpr + 4 * (int64_t)j + (lane >> 4);
+  const float rs = S.norm_fp16 ? (float)((const _Float16*)S.norms)[t] : ((const float*)S.norms)[t];
+  g = rs / S.alpha_n;
+  return ok;
+}
+
+template <int LAT>
+__device__ __forceinline__ DecHead attn_head(const hq_decode_args& S, int64_t row, uint32_t j,
+                                             int lane) {
+  const int64_t sub = row * S.spr + j;
+  const uint32_t start = readfirst(S.offsets[sub]), end = readfirst(S.offsets[sub + 1]);
+  return dec_head<LAT>(S, true, start, end, readfirst(S.kparam[sub]), lane);
+}
+
+template <int LAT, int G>
+__global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
+  extern __shared__ uint32_t smem[];
+  __shared__ uint32_t s_sel[256];
+  __shared__ float s_m[HQ_WAVES_PER_WG][4 * G];
+  __shared__ float s_l[HQ_WAVES_PER_WG][4 * G];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint32_t wave = readfirst((uint32_t)(tid >> 6));
+  const uint32_t spr = (uint32_t)A.K.spr;
+  const uint32_t x = blockIdx.x % (uint32_t)A.nx;
+  const uint32_t bj = blockIdx.x / (uint32_t)A.nx;
+  const uint32_t b = bj / spr, j = bj - b * spr;
+  const int64_t len = attn_seq_len(A, b, tid == 0 && x == 0 && j == 0);
+  const int64_t wg_t0 = (int64_t)x * HQ_WAVES_PER_WG * A.chunk;
+  if (wg_t0 >= len) return;  // the whole workgroup, before any barrier
+  s_sel[tid] = kByteSelect.e[tid];
+  __syncthreads();
+  uint32_t* buf = smem + wave * (A.lds_words + 66);
+  uint32_t* starts = buf + A.lds_words + 2;
+  float* comb = (float*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66));
+
+  const int q4 = lane >> 4, c0 = (lane & 15) * 8;
+  const int64_t h0 = (int64_t)b * A.heads_q + (int64_t)(j * 4 + q4) * G;
+  float qv[G][8], acc[G][8], m[G], l[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const float4 a = *(const float4*)(A.qt + (h0 + g) * HQ_TILE + c0);
+    const float4 c = *(const float4*)(A.qt + (h0 + g) * HQ_TILE + c0 + 4);
+    qv[g][0] = a.x; qv[g][1] = a.y; qv[g][2] = a.z; qv[g][3] = a.w;
+    qv[g][4] = c.x; qv[g][5] = c.y; qv[g][6] = c.z; qv[g][7] = c.w;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[g][i] = 0.0f;
+    m[g] = -__builtin_inff();
+    l[g] = 0.0f;
+  }
+
+  const int64_t t0 = wg_t0 + (int64_t)wave * A.chunk;
+  const int64_t t1 = t0 + A.chunk < len ? t0 + A.chunk : len;
+  const uint32_t bt = (uint32_t)A.block_tokens;
+  const int32_t* trow = A.table + (int64_t)b * A.max_blocks;
+  // token position as (block, index in block), stepped without division
+  uint32_t bi = 0, wi = 0;
+  if (t0 < t1) {
+    bi = (uint32_t)(t0 / bt);
+    wi = (uint32_t)(t0 - (int64_t)bi * bt);
+  }
+  auto row_at = [&](uint32_t blk_i, uint32_t in_blk) -> int64_t {
+    const int32_t blk = trow[blk_i];
+    const int64_t r = (int64_t)blk * bt + in_blk;
+    return (blk >= 0 && r < A.rows) ? r : -1;
+  };
+  int64_t row = t0 < t1 ? row_at(bi, wi) : -1;
+  DecHead hk, hv;
+  if (row >= 0) {
+    hk = attn_head<LAT>(A.K, row, j, lane);
+    hv = attn_head<LAT>(A.V, row, j, lane);
+  }
+  bool bad = false;
+  for (int64_t t = t0; t < t1; ++t) {
+    // the next token's row and heads, loaded a step ahead
+    if (++wi == bt) {
+      wi = 0;
+      ++bi;
+    }
+    const int64_t nrow = t + 1 < t1 ? row_at(bi, wi) : -1;
+    DecHead nk, nv;
+    if (nrow >= 0) {
+      nk = attn_head<LAT>(A.K, nrow, j, lane);
+      nv = attn_head<LAT>(A.V, nrow, j, lane);
+    }
+    if (row >= 0) {
+      float y[8], gk;
+      bad |= !attn_tile<LAT>(A.K, hk, lane, buf, starts, s_sel, row, j, y, gk);
+      float s[G];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float d = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) d = __builtin_fmaf(qv[g][i], y[i], d);
+        s[g] = gk * row16_sum(d);
+      }
+      float gv;
+      bad |= !attn_tile<LAT>(A.V, hv, lane, buf, starts, s_sel, row, j, y, gv);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float mn = __builtin_fmaxf(m[g], s[g]);
+        const float a = exp2f(m[g] - mn);  // 0 for the first token (m = -inf)
+        const float p = exp2f(s[g] - mn);
+        l[g] = __builtin_fmaf(l[g], a, p);
+        const float pg = p * gv;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[g][i] = __builtin_fmaf(acc[g][i], a, pg * y[i]);
+        m[g] = mn;
+      }
+    } else if (lane == 0 && A.K.stats) {
+      atomicCAS(&A.K.stats->status, 0u, (uint32_t)HQ_ERR_INVALID_ARG);  // block id out of range
+    }
+    row = nrow;
+    hk = nk;
+    hv = nv;
+  }
+  if (bad && A.K.stats) {
+    const unsigned long long anyb = __ballot(bad);
+    if ((unsigned)lane == (unsigned)__builtin_ctzll(anyb)) {
+      atomicAdd(&A.K.stats->corrupt_substreams, 1u);
+      atomicCAS(&A.K.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+    }
+  }
+
+  // the four waves' sums, rescaled to their common maximum, in wave order
+  if ((lane & 15) == 0) {
+#pragma unroll
+    for (int g = 0; g < G; ++g) s_m[wave][q4 * G + g] = m[g];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    float M = s_m[0][q4 * G + g];
+#pragma unroll
+    for (int w = 1; w < HQ_WAVES_PER_WG; ++w) M = __builtin_fmaxf(M, s_m[w][q4 * G + g]);
+    const float f = m[g] == -__builtin_inff() ? 0.0f : exp2f(m[g] - M);
+    l[g] *= f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[g][i] *= f;
+    m[g] = M;
+  }
+  if (wave > 0) {
+    float* cw = comb + ((wave - 1) * 64 + lane) * 8 * G;
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      *(float4*)(cw + 8 * g) = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
+      *(float4*)(cw + 8 * g + 4) = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
+      if ((lane & 15) == 0) s_l[wave][q4 * G + g] = l[g];
+    }
+  }
+  __syncthreads();
+  if (wave == 0) {
+#pragma unroll
+    for (int w = 1; w < HQ_WAVES_PER_WG; ++w) {
+      const float* cw = comb + ((w - 1) * 64 + lane) * 8 * G;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float4 a = *(const float4*)(cw + 8 * g);
+        const float4 c = *(const float4*)(cw + 8 * g + 4);
+        acc[g][0] += a.x; acc[g][1] += a.y; acc[g][2] += a.z; acc[g][3] += a.w;
+        acc[g][4] += c.x; acc[g][5] += c.y; acc[g][6] += c.z; acc[g][7] += c.w;
+        l[g] += s_l[w][q4 * G + g];
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      const int64_t pi = (h0 + g) * A.nx + x;
+      float* o = A.part_acc + pi * HQ_TILE + c0;
+      *(float4*)o = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
+      *(float4*)(o + 4) = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
+      if ((lane & 15) == 0) {
+        A.part_m[pi] = m[g];
+        A.part_l[pi] = l[g];
+      }
+    }
+  }
+}
+
+// out = D H S (sum_x f_x acc_x) / (sum_x f_x l_x), f_x = 2^(m_x - max m), over
+// the splits that hold tokens, in split order, with the value plan's signs;
+// an empty sequence gives zeros.  One lane group of 16 per query head.
+__global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int64_t pair = ((int64_t)blockIdx.x * HQ_WAVES_PER_WG + (tid >> 6)) * 4 + (lane >> 4);
+  if (pair >= A.batch * A.heads_q) return;  // whole lane groups
+  const int64_t b = pair / A.heads_q;
+  const int32_t kvh = (int32_t)(pair - b * A.heads_q) / A.group;
+  const int c0 = (lane & 15) * 8;
+  const int64_t len = attn_seq_len(A, b, false);
+  const int64_t per = (int64_t)HQ_WAVES_PER_WG * A.chunk;
+  const int32_t n = (int32_t)((len + per - 1) / per);
+  const float* pm = A.part_m + pair * A.nx;
+  const float* pl = A.part_l + pair * A.nx;
+  float M = -__builtin_inff();
+  for (int32_t x = 0; x < n; ++x) M = __builtin_fmaxf(M, pm[x]);
+  float L = 0.0f, v[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  if (M != -__builtin_inff()) {
+    for (int32_t x = 0; x < n; ++x) {
+      const float mx = pm[x];
+      const float f = mx == -__builtin_inff() ? 0.0f : exp2f(mx - M);
+      L = __builtin_fmaf(f, pl[x], L);
+      const float* a = A.part_acc + (pair * A.nx + x) * HQ_TILE + c0;
+      const float4 a0 = *(const float4*)a;
+      const float4 a1 = *(const float4*)(a + 4);
+      v[0] = __builtin_fmaf(f, a0.x, v[0]); v[1] = __builtin_fmaf(f, a0.y, v[1]);
+      v[2] = __builtin_fmaf(f, a0.z, v[2]); v[3] = __builtin_fmaf(f, a0.w, v[3]);
+      v[4] = __builtin_fmaf(f, a1.x, v[4]); v[5] = __builtin_fmaf(f, a1.y, v[5]);
+      v[6] = __builtin_fmaf(f, a1.z, v[6]); v[7] = __builtin_fmaf(f, a1.w, v[7]);
+    }
+  }
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  const uint32_t sbits = A.V.rotation ? sign_bits8(A.V.smask, c0) : 0u;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = flip(v[i] * inv, sbits, i);
+  const XSigns sg(lane);
+  fwht128(v, sg);
+  const uint32_t dbits = sign_bits8(A.V.dmask, (int64_t)kvh * HQ_TILE + c0);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = flip(v[i], dbits, i);
+  if (A.out_bf16) {
+    uint4 o;
+    o.x = cvt_pk_bf16(v[0], v[1]);
+    o.y = cvt_pk_bf16(v[2], v[3]);
+    o.z = cvt_pk_bf16(v[4], v[5]);
+    o.w = cvt_pk_bf16(v[6], v[7]);
+    *(uint4*)((uint16_t*)A.out + pair * HQ_TILE + c0) = o;
+  } else {
+    float* o = (float*)A.out + pair * HQ_TILE + c0;
+    *(float4*)o = make_float4(v[0], v[1], v[2], v[3]);
+    *(float4*)(o + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  }
+}
+
 // ------------------------------------------------------------ activation prep
 // One workgroup per token row: per 128-column tile y = H D a (canonical stage
 // order, the weights' signs), amax over the row, then int8.
@@ -2244,5 +2567,33 @@ int hq_launch_decode_gemv(const hq_plan_s* p, const hq_decode_args& a, const voi
     default:
       hipLaunchKernelGGL(hq_decode_gemv_kernel<kZ>, dim3(nwg), dim3(256), lds, st, a, xtr, y, yb);
   }
+  return (int)hipGetLastError();
+}
+
+int hq_launch_decode_attention(const hq_attn_args& a, int lattice, void* stream) {
+  const hipStream_t st = (hipStream_t)stream;
+  const uint32_t heads = (uint32_t)((a.batch * a.heads_q + 15) / 16);
+  hipLaunchKernelGGL(hq_attn_prep_kernel, dim3(heads), dim3(256), 0, st, a);
+  const uint32_t nwg = (uint32_t)(a.batch * a.K.spr * a.nx);
+  const size_t lds = ((size_t)HQ_WAVES_PER_WG * (a.lds_words + 66) +
+                      (size_t)(HQ_WAVES_PER_WG - 1) * 64 * 8 * a.group) * 4;
+#define HQ_ATTN_CASE(L, GG) \
+  hipLaunchKernelGGL((hq_attn_kernel<L, GG>), dim3(nwg), dim3(256), lds, st, a)
+#define HQ_ATTN_GROUPS(L)           \
+  switch (a.group) {                \
+    case 1: HQ_ATTN_CASE(L, 1); break; \
+    case 2: HQ_ATTN_CASE(L, 2); break; \
+    case 4: HQ_ATTN_CASE(L, 4); break; \
+    default: HQ_ATTN_CASE(L, 8);    \
+  }
+  switch (lattice) {
+    case HQ_E8: HQ_ATTN_GROUPS(kE8); break;
+    case HQ_D4: HQ_ATTN_GROUPS(kD4); break;
+    case HQ_A2: HQ_ATTN_GROUPS(kA2); break;
+    default: HQ_ATTN_GROUPS(kZ);
+  }
+#undef HQ_ATTN_GROUPS
+#undef HQ_ATTN_CASE
+  hipLaunchKernelGGL(hq_attn_combine_kernel, dim3(heads), dim3(256), 0, st, a);
   return (int)hipGetLastError();
 }

@@ -101,6 +101,11 @@ def lib():
     L.hq_gemv_workspace_bytes.argtypes = [p]
     L.hq_decode_gemv.restype = i32
     L.hq_decode_gemv.argtypes = [p, p, i64, i64, p, i32, p, i32, p, C.c_size_t, p]
+    L.hq_attention_workspace_bytes.restype = C.c_size_t
+    L.hq_attention_workspace_bytes.argtypes = [p, i64, i32, i64]
+    L.hq_decode_attention.restype = i32
+    L.hq_decode_attention.argtypes = [p, p, p, p, p, i32, i64, i32, C.c_float, p, i32, i32, p, p,
+                                      i32, p, C.c_size_t, p]
     L.hq_rice_kstar.restype = i32
     L.hq_rice_kstar.argtypes = [i64, i64]
     L.hq_calibrated_snr.restype = i32
@@ -340,6 +345,39 @@ def hq_decode_gemv(plan: Plan, s: EncodedStream, x: torch.Tensor, row0=0, rows=N
     return out
 
 
+def hq_attention_workspace_bytes(k_plan: Plan, batch, heads_q, max_tokens):
+    return lib().hq_attention_workspace_bytes(k_plan.handle, batch, heads_q, max_tokens)
+
+
+def hq_decode_attention(k_plan: Plan, k: EncodedStream, v_plan: Plan, v: EncodedStream,
+                        q: torch.Tensor, block_table: torch.Tensor, seq_lens: torch.Tensor,
+                        block_tokens, scale=None, out_dtype=torch.float32, workspace=None,
+                        out=None, stream=None):
+    """hq_decode_attention: q [batch, heads_q, 128] (bf16 or fp32) attends
+    over the coded cache; block_table int32 [batch, max_blocks] and seq_lens
+    int32 [batch] on the device.  Returns [batch, heads_q, 128]."""
+    assert q.is_cuda and q.dim() == 3 and q.shape[2] == 128 and q.is_contiguous()
+    assert block_table.dtype == torch.int32 and block_table.is_contiguous() and block_table.dim() == 2
+    assert seq_lens.dtype == torch.int32 and seq_lens.is_contiguous()
+    batch, heads_q = q.shape[0], q.shape[1]
+    max_blocks = block_table.shape[1]
+    scale = 128 ** -0.5 if scale is None else scale
+    if workspace is None:
+        nb = hq_attention_workspace_bytes(k_plan, batch, heads_q, max_blocks * block_tokens)
+        workspace = torch.empty(max(nb, 16), dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = torch.empty((batch, heads_q, 128), dtype=out_dtype, device=q.device)
+    st = lib().hq_decode_attention(k_plan.handle, C.byref(k.c), v_plan.handle, C.byref(v.c),
+                                   C.c_void_p(q.data_ptr()), _dtype_code(q.dtype), batch, heads_q,
+                                   C.c_float(scale), C.c_void_p(block_table.data_ptr()),
+                                   max_blocks, block_tokens, C.c_void_p(seq_lens.data_ptr()),
+                                   C.c_void_p(out.data_ptr()), _dtype_code(out.dtype),
+                                   C.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                   _stream_handle(stream))
+    _check("hq_decode_attention", st)
+    return out
+
+
 def hq_rice_kstar(count, total):
     return lib().hq_rice_kstar(int(count), int(total))
 
@@ -354,5 +392,6 @@ def hq_calibrated_snr(lattice, rice_k, bps):
 EXPORTED = ["hq_plan", "hq_plan_destroy", "hq_plan_get_info", "hq_scan_bytes", "hq_encode",
             "hq_decode", "hq_encode_group", "hq_decode_group", "hq_decode_int8", "hq_act_prep", "hq_gemm_int8_blockscaled",
             "hq_gemm_workspace_bytes", "hq_dequant_gemm_int8", "hq_gemv_workspace_bytes",
-            "hq_decode_gemv", "hq_rice_kstar",
+            "hq_decode_gemv", "hq_attention_workspace_bytes", "hq_decode_attention",
+            "hq_rice_kstar",
             "hq_calibrated_snr", "hq_status_string"]
