@@ -395,7 +395,7 @@ def decode_gemv(params: Params, codes, norms, x, row0=0):
 
 
 def decode_attention(pk: Params, k_codes, k_norms, pv: Params, v_codes, v_norms, q,
-                     block_table, seq_lens, block_tokens, scale):
+                     block_table, seq_lens, block_tokens, scale, rows=None):
     """One-token attention over a coded KV cache (the KV path of Sec. 5.2 and
     the decode of Sec. 5.3 feeding attention, as the end-to-end runs of Sec.
     6.6 use it): the cached keys and values are the decoded rows exactly as
@@ -408,9 +408,25 @@ def decode_attention(pk: Params, k_codes, k_norms, pv: Params, v_codes, v_norms,
                         row block_table[b, t // block_tokens] * block_tokens
                         + t % block_tokens.
       seq_lens          [batch] token counts; an empty sequence gives zeros.
+      rows              optional stored-row index of each given code row
+                        (default 0, 1, ...): lets a caller pass only the rows
+                        the table reaches; each is decoded at its own index
+                        (the dither depends on it).
     Returns [batch, H_q, tile] fp64."""
-    kd = backend(pk, k_codes, k_norms).astype(np.float64)
-    vd = backend(pv, v_codes, v_norms).astype(np.float64)
+    if rows is None:
+        kd = backend(pk, k_codes, k_norms).astype(np.float64)
+        vd = backend(pv, v_codes, v_norms).astype(np.float64)
+        local = None
+    else:
+        rows = np.asarray(rows, dtype=np.int64)
+        kd = np.zeros(k_codes.shape)
+        vd = np.zeros(v_codes.shape)
+        cut = np.flatnonzero(np.diff(rows) != 1) + 1  # runs of consecutive stored rows
+        for a, b in zip(np.r_[0, cut], np.r_[cut, rows.size]):
+            kd[a:b] = backend(pk, k_codes[a:b], k_norms[a:b], row0=int(rows[a]))
+            vd[a:b] = backend(pv, v_codes[a:b], v_norms[a:b], row0=int(rows[a]))
+        order = np.argsort(rows)
+        local = (rows[order], order)
     q = np.asarray(q, dtype=np.float64)
     B, Hq, n = q.shape
     G = Hq // (kd.shape[1] // n)
@@ -420,12 +436,16 @@ def decode_attention(pk: Params, k_codes, k_norms, pv: Params, v_codes, v_norms,
         if T == 0:
             continue
         t = np.arange(T)
-        rows = np.asarray(block_table[b])[t // block_tokens].astype(np.int64) * block_tokens + t % block_tokens
+        r = np.asarray(block_table[b])[t // block_tokens].astype(np.int64) * block_tokens + t % block_tokens
+        if local is not None:
+            i = np.searchsorted(local[0], r)
+            assert np.array_equal(local[0][i], r), "a row the table reaches was not given"
+            r = local[1][i]
         for h in range(Hq):
             cs = slice((h // G) * n, (h // G + 1) * n)
-            s = (kd[rows, cs] @ q[b, h]) * scale
+            s = (kd[r, cs] @ q[b, h]) * scale
             p = np.exp(s - s.max())
-            out[b, h] = (p / p.sum()) @ vd[rows, cs]
+            out[b, h] = (p / p.sum()) @ vd[r, cs]
     return out
 
 

@@ -338,6 +338,72 @@ def test_c4_kv_cache_values_e8(hq):
                        "C4 values E8@2", dither=True)
 
 
+def test_c4_decode_attention_as_benched(hq):
+    """hq_decode_attention at the KV workload's full size, in the layout and
+    launch shape the bench times: keys and values [16, 8192, 8, 128] E8 at 2
+    bps (signs rotation, dither, fp16 norms) appended in 128-token blocks, a
+    stream row being (block, sequence, token); 32 query heads (4 per KV
+    head), one sequence cut to 5000 tokens.  Three sampled sequences against
+    the oracle over those sequences' rows, within 2e-5 of max |v^|."""
+    from paper_2606_23406_amd import workloads as W
+    B, T, Hkv, Hq, bt = 16, 8192, 8, 32, 128
+    snr = PT.op_snr("E8", 2.0)
+    streams = []
+    for role, seed in (("k", 91), ("v", 95)):
+        x = W.kv_cache(role=role).permute(1, 0, 2, 3).reshape(T // bt, bt, B, Hkv * 128)
+        x = x.permute(0, 2, 1, 3).reshape(-1, Hkv * 128).contiguous()
+        P = PT.oracle_params(O.E8, snr, rht_seed=seed, rotation=1, rot_seed=seed + 1, dither=True,
+                             dither_seed=seed + 2, norm_fp16=True)
+        plan = PT.gpu_plan(hq, P, snr, Hkv * 128)
+        s = hq.EncodedStream(plan, x.shape[0])
+        xd = x.cuda()
+        for r0 in range(0, x.shape[0], B * bt):
+            hq.hq_encode(plan, xd[r0:r0 + B * bt], s, append=r0 > 0)
+        del xd
+        streams.append((P, plan, s))
+    (pk, plk, sk), (pv, plv, sv) = streams
+    table = (np.arange(T // bt)[None, :] * B + np.arange(B)[:, None]).astype(np.int32)
+    lens = np.full(B, T, dtype=np.int32)
+    lens[5] = 5000
+    q = W.queries(n=B * Hq).reshape(B, Hq, 128).to(torch.bfloat16)
+    print(f"[fullsize] C4 decode attention: batch {B}, {T} tokens, {Hkv} KV heads, {Hq} query "
+          f"heads, E8@2 keys and values", flush=True)
+    out = hq.hq_decode_attention(plk, sk, plv, sv, q.cuda(), torch.from_numpy(table).cuda(),
+                                 torch.from_numpy(lens).cuda(), bt)
+    torch.cuda.synchronize()
+    for st in (sk.read_stats(), sv.read_stats()):
+        assert st["status"] == 0 and st["corrupt_substreams"] == 0, st
+    got = out.cpu().numpy().astype(np.float64)
+    arrays = [PT.gpu_stream_arrays(s, s.rows) for s in (sk, sv)]
+    worst = 0.0
+    for b in (0, 5, 15):
+        rows = np.concatenate([table[b, k] * bt + np.arange(bt) for k in range(-(-lens[b] // bt))])
+        codes, norms = [], []
+        for P, (pay, off, kp, nrm) in zip((pk, pv), arrays):
+            parts = []
+            for k in range(0, rows.size, bt):  # one 128-row block at a time
+                r0 = int(rows[k])
+                o = off[r0 * 2:(r0 + bt) * 2 + 1]
+                c, rc = O.unpack(P, pay[o[0] - off[0]:o[-1] - off[0]], o - o[0],
+                                 kp[r0 * 2:(r0 + bt) * 2], bt, Hkv * 128, 0)
+                assert rc == O.OK
+                parts.append(c)
+            codes.append(np.concatenate(parts))
+            norms.append(nrm[rows])
+        ref = O.decode_attention(pk, codes[0], norms[0], pv, codes[1], norms[1],
+                                 q[b:b + 1].float().numpy(), table[b:b + 1], lens[b:b + 1], bt,
+                                 128 ** -0.5, rows=rows)[0]
+        vd = np.concatenate([O.backend(pv, codes[1][k:k + bt], norms[1][k:k + bt], row0=int(rows[k]))
+                             for k in range(0, rows.size, bt)])
+        for h in range(Hq):
+            cs = slice((h // 4) * 128, (h // 4 + 1) * 128)
+            err = np.abs(got[b, h] - ref[h]).max() / np.abs(vd[:lens[b], cs]).max()
+            worst = max(worst, err)
+            assert err <= 2e-5, (b, h, err)
+    print(f"[fullsize] C4 decode attention: 3 sequences x {Hq} heads, worst error {worst:.2e} "
+          f"of max |v|", flush=True)
+
+
 def test_c5_gemm_fullsize(hq):
     from paper_2606_23406_amd import workloads as W
     print("[fullsize] C5 gemm W 14336x4096 E8@4, A 4096x4096", flush=True)

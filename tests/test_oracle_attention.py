@@ -144,3 +144,16 @@ def test_rotated_domain_identity(lat):
         acc += p[r] * gv[r, 1] * (ptsv[r, N:2 * N] - u)
     back = Dv * O.fwht(Sv * acc)
     np.testing.assert_allclose(back, p @ vd[:, N:2 * N], rtol=0, atol=1e-5 * np.abs(vd).max())
+
+
+def test_subset_of_rows_at_their_indices(cache):
+    # passing only the rows a sequence reaches, at their stored indices, gives
+    # the same answer as passing every row
+    rng = np.random.default_rng(8)
+    q = rng.standard_normal((3, 8, N))
+    full = attend(cache, q, [37, 1, 0])
+    keep = np.array(sorted(ROWS0 + ROWS1))
+    c = cache
+    sub = O.decode_attention(c["pk"], c["kc"][keep], c["kn"][keep], c["pv"], c["vc"][keep],
+                             c["vn"][keep], q, TABLE, np.array([37, 1, 0]), BT, 1.0, rows=keep)
+    assert np.array_equal(sub, full)
