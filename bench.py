@@ -42,6 +42,7 @@ def parse_args():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-gemm", action="store_true")
+    ap.add_argument("--no-attention", action="store_true")
     ap.add_argument("--no-other", action="store_true", help="skip the C1, C2, C3-D4 and C4 measurements")
     ap.add_argument("--group", type=int, default=16,
                     help="matrices per encode/decode launch (hq_encode_group); 1 = one launch each")
@@ -387,6 +388,79 @@ def gemv_extra(H, W, mats, dev, reps=10):
             "speedup_vs_bf16": round(td / tf, 3)}
 
 
+def attention_extra(H, W, dev, reps=10):
+    """Fused decode-attention (hq_decode_attention): one bf16 query token per
+    sequence over the KV workload's cache (batch 16, 8192 tokens, 8 KV heads
+    of 128; keys and values E8 at 2 bps with signs rotation, dither and fp16
+    norms, appended in 128-token blocks, a stream row being (block,
+    sequence, token)), 32 query heads (4 per KV head).  Beside it: decoding
+    both streams to bf16 (hq_decode) and attention over a bf16 cache of the
+    same shape held contiguous per head (two batched matmuls with contiguous
+    right operands and an fp32 softmax); all cold."""
+    B, T, Hkv, Hq, D, bt = 16, 8192, 8, 32, 128, 128
+    G = Hq // Hkv
+    flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+    streams, dense = [], []
+    for role, seed in (("k", 91), ("v", 95)):
+        x = W.kv_cache(role=role)  # [B, T, Hkv, D]
+        dense.append(x.permute(0, 2, 1, 3).contiguous().to(dev))  # [B, Hkv, T, D]
+        xr = x.permute(1, 0, 2, 3).reshape(T // bt, bt, B, Hkv * D).permute(0, 2, 1, 3)
+        xr = xr.reshape(-1, Hkv * D).contiguous().to(dev)
+        del x
+        plan = H.hq_plan(128, H.HQ_E8, 2.0, seed, -1, Hkv * D, rotation=1, dither=True,
+                         rot_seed=seed + 1, dither_seed=seed + 2, norm_fp16=True)
+        s = H.EncodedStream(plan, xr.shape[0])
+        for r0 in range(0, xr.shape[0], B * bt):
+            H.hq_encode(plan, xr[r0:r0 + B * bt], s, append=r0 > 0)
+        del xr
+        streams.append((plan, s))
+    (pk, sk), (pv, sv) = streams
+    table = (torch.arange(T // bt)[None, :] * B + torch.arange(B)[:, None]).to(torch.int32).to(dev)
+    lens = torch.full((B,), T, dtype=torch.int32, device=dev)
+    q = W.queries(n=B * Hq).reshape(B, Hq, D).to(torch.bfloat16).to(dev)
+    ws = torch.empty(H.hq_attention_workspace_bytes(pk, B, Hq, T), dtype=torch.uint8, device=dev)
+    out = torch.empty((B, Hq, D), dtype=torch.bfloat16, device=dev)
+    ybuf = [torch.empty((B * T, Hkv * D), dtype=torch.bfloat16, device=dev) for _ in range(2)]
+    qT = q.reshape(B, Hkv, G, D).transpose(-1, -2).contiguous()  # [B, Hkv, D, G]
+
+    def fused():
+        H.hq_decode_attention(pk, sk, pv, sv, q, table, lens, bt, workspace=ws, out=out)
+
+    def decode_both():
+        H.hq_decode(pk, sk, out=ybuf[0])
+        H.hq_decode(pv, sv, out=ybuf[1])
+
+    def attend_bf16():
+        sc = torch.matmul(dense[0], qT).float() * D ** -0.5  # [B, Hkv, T, G]
+        p = torch.softmax(sc, dim=2).to(torch.bfloat16).transpose(-1, -2).contiguous()
+        return torch.matmul(p, dense[1])  # [B, Hkv, G, D]
+
+    fused()
+    decode_both()
+    ref = attend_bf16()
+    torch.cuda.synchronize()
+    st = [s.read_stats()["status"] for s in (sk, sv)]
+    err = (out.float() - ref.reshape(B, Hq, D).float()).abs().max().item()
+    tf = _median_ms(fused, reps, flush) * 1e-3
+    td = _median_ms(decode_both, reps, flush) * 1e-3
+    ta = _median_ms(attend_bf16, reps, flush) * 1e-3
+    n = 2 * B * T * Hkv * D
+    stream_bytes = sum(int(s.end_words()) * 4 for s in (sk, sv)) + n / 128 * 2 + n / 512 * 5
+    del flush, ybuf, dense, streams, sk, sv, ws
+    torch.cuda.empty_cache()
+    return {"workload": "KV cache 16 x 8192 tokens x 8 KV heads x 128, keys and values E8@2, "
+                        "32 query heads, one bf16 query token per sequence",
+            "fused_ms": round(tf * 1e3, 4), "decode_then_attend_ms": round((td + ta) * 1e3, 4),
+            "decode_both_ms": round(td * 1e3, 4), "bf16_resident_attend_ms": round(ta * 1e3, 4),
+            "fused_scalars_per_s_e9": round(n / tf / 1e9, 1),
+            "fused_stream_GBs": round(stream_bytes / tf / 1e9, 1),
+            "bf16_attend_GBs": round(2 * n / ta / 1e9, 1),
+            "speedup_vs_decode_then_attend": round((td + ta) / tf, 3),
+            "speedup_vs_bf16_resident": round(ta / tf, 3),
+            "cache_bytes_coded": int(stream_bytes), "cache_bytes_bf16": 2 * n,
+            "max_abs_diff_vs_unquantized_bf16_attend": round(err, 4), "status": st}
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -491,6 +565,8 @@ def main():
     if not args.no_gemm:
         out["gemm_int8"] = gemm_extra(H, W, mats, dev)
         out["decode_gemv"] = gemv_extra(H, W, mats, dev)
+    if not args.no_attention:
+        out["decode_attention"] = attention_extra(H, W, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(mats, args.cpu_seconds)
     if not args.no_other:

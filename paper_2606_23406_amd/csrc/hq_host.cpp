@@ -561,11 +561,12 @@ hq_status hq_decode_gemv(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t 
   return hip_status(hq_launch_decode_gemv(p, a, x, xt, (float*)workspace, y, yt, stream));
 }
 
-// Tokens per wave of the fused attention: about 4096 waves over the call
-// (every SIMD four deep), from 16 to 1024 tokens each.
+// Tokens per wave of the fused attention: about 16384 waves over the call
+// (several rounds of the waves that fit at once, so the last round is a
+// small share), from 16 to 1024 tokens each.
 static int64_t attn_chunk(const hq_plan_s* k, int64_t batch, int64_t max_tokens) {
   const int64_t work = batch * k->spr * max_tokens;
-  return std::min<int64_t>(1024, std::max<int64_t>(16, (work + 4095) / 4096));
+  return std::min<int64_t>(1024, std::max<int64_t>(16, (work + 16383) / 16384));
 }
 
 static int64_t attn_splits(int64_t max_tokens, int64_t chunk) {
@@ -609,7 +610,7 @@ hq_status hq_decode_attention(hq_plan_t pk, const hq_stream* k, hq_plan_t pv, co
     return HQ_ERR_INVALID_ARG;
   const int64_t chunk = attn_chunk(pk, batch, max_tokens);
   const int64_t nx = attn_splits(max_tokens, chunk);
-  if (batch * pk->spr * nx > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
+  if (batch * pk->spr * nx > 0x7FFFFFFF || batch * heads_q > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
   hq_attn_args a;
   std::memset(&a, 0, sizeof(a));
   fill_decode_args(pk, k, 0, k->rows, &a.K);
@@ -625,6 +626,7 @@ hq_status hq_decode_attention(hq_plan_t pk, const hq_stream* k, hq_plan_t pv, co
   a.part_l = a.part_m + heads * nx;
   a.batch = batch;
   a.rows = std::min(k->rows, v->rows);
+  if (a.rows > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;  // rows travel as 32-bit lane values
   a.heads_q = heads_q;
   a.group = (int32_t)group;
   a.max_blocks = max_blocks;

@@ -1911,11 +1911,11 @@ __global__ __launch_bounds__(256) void hq_attn_prep_kernel(hq_attn_args A) {
 }
 
 // The lane's 8 coordinates of one coded tile, code - U (U the stream's
-// dither at that row), and the tile factor g = r / (alpha n).
+// dither at that row).
 template <int LAT>
 __device__ __forceinline__ bool attn_tile(const hq_decode_args& S, const DecHead& head, int lane,
                                           uint32_t* buf, uint32_t* starts, const uint32_t* sel,
-                                          int64_t row, uint32_t j, float* y, float& g) {
+                                          uint32_t row, uint32_t j, float* y) {
   uint32_t sym[8];
   const bool ok = decode_symbols<LAT>(S, head, lane, buf, starts, sel, sym);
   int32_t c[8];
@@ -1928,18 +1928,24 @@ __device__ __forceinline__ bool attn_tile(const hq_decode_args& S, const DecHead
 #pragma unroll
     for (int i = 0; i < 8; ++i) y[i] = y[i] - u[i];
   }
-  const int64_t t = row * S.tpr + 4 * (int64_t)j + (lane >> 4);
-  const float rs = S.norm_fp16 ? (float)((const _Float16*)S.norms)[t] : ((const float*)S.norms)[t];
-  g = rs / S.alpha_n;
   return ok;
 }
 
-template <int LAT>
-__device__ __forceinline__ DecHead attn_head(const hq_decode_args& S, int64_t row, uint32_t j,
-                                             int lane) {
-  const int64_t sub = row * S.spr + j;
-  const uint32_t start = readfirst(S.offsets[sub]), end = readfirst(S.offsets[sub + 1]);
-  return dec_head<LAT>(S, true, start, end, readfirst(S.kparam[sub]), lane);
+// Stored tile norm r of the lane's tile in `row` (fp32 or fp16).
+__device__ __forceinline__ float attn_norm(const hq_decode_args& S, uint32_t row, uint32_t j,
+                                           int lane) {
+  const int64_t t = (int64_t)row * S.tpr + 4 * (int64_t)j + (lane >> 4);
+  return S.norm_fp16 ? (float)((const _Float16*)S.norms)[t] : ((const float*)S.norms)[t];
+}
+
+// Table entry (start, end, k) of one token's sub-stream, fetched earlier by
+// lane i of the wave for the i-th token of a run of 64.
+struct AttnMeta {
+  uint32_t s, e, k;
+};
+
+__device__ __forceinline__ uint32_t lane_val(uint32_t v, uint32_t i) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)i);
 }
 
 template <int LAT, int G>
@@ -1948,6 +1954,7 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
   __shared__ uint32_t s_sel[256];
   __shared__ float s_m[HQ_WAVES_PER_WG][4 * G];
   __shared__ float s_l[HQ_WAVES_PER_WG][4 * G];
+  __shared__ float4 s_q[4 * G * 32];  // the workgroup's query tiles, coded coordinates
   const int tid = threadIdx.x, lane = tid & 63;
   const uint32_t wave = readfirst((uint32_t)(tid >> 6));
   const uint32_t spr = (uint32_t)A.K.spr;
@@ -1958,20 +1965,19 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
   const int64_t wg_t0 = (int64_t)x * HQ_WAVES_PER_WG * A.chunk;
   if (wg_t0 >= len) return;  // the whole workgroup, before any barrier
   s_sel[tid] = kByteSelect.e[tid];
+  // KV heads 4j .. 4j+3 read query heads (4j) G .. (4j + 4) G - 1: one block
+  const int64_t hq0 = (int64_t)b * A.heads_q + (int64_t)j * 4 * G;
+  for (int i = tid; i < 4 * G * 32; i += 256) s_q[i] = ((const float4*)(A.qt + hq0 * HQ_TILE))[i];
   __syncthreads();
   uint32_t* buf = smem + wave * (A.lds_words + 66);
   uint32_t* starts = buf + A.lds_words + 2;
   float* comb = (float*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66));
 
   const int q4 = lane >> 4, c0 = (lane & 15) * 8;
-  const int64_t h0 = (int64_t)b * A.heads_q + (int64_t)(j * 4 + q4) * G;
-  float qv[G][8], acc[G][8], m[G], l[G];
+  const float4* qrow = s_q + (q4 * G) * 32 + (lane & 15) * 2;  // head g: + 32 g
+  float acc[G][8], m[G], l[G];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    const float4 a = *(const float4*)(A.qt + (h0 + g) * HQ_TILE + c0);
-    const float4 c = *(const float4*)(A.qt + (h0 + g) * HQ_TILE + c0 + 4);
-    qv[g][0] = a.x; qv[g][1] = a.y; qv[g][2] = a.z; qv[g][3] = a.w;
-    qv[g][4] = c.x; qv[g][5] = c.y; qv[g][6] = c.z; qv[g][7] = c.w;
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[g][i] = 0.0f;
     m[g] = -__builtin_inff();
@@ -1982,66 +1988,84 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
   const int64_t t1 = t0 + A.chunk < len ? t0 + A.chunk : len;
   const uint32_t bt = (uint32_t)A.block_tokens;
   const int32_t* trow = A.table + (int64_t)b * A.max_blocks;
-  // token position as (block, index in block), stepped without division
-  uint32_t bi = 0, wi = 0;
-  if (t0 < t1) {
-    bi = (uint32_t)(t0 / bt);
-    wi = (uint32_t)(t0 - (int64_t)bi * bt);
-  }
-  auto row_at = [&](uint32_t blk_i, uint32_t in_blk) -> int64_t {
-    const int32_t blk = trow[blk_i];
-    const int64_t r = (int64_t)blk * bt + in_blk;
-    return (blk >= 0 && r < A.rows) ? r : -1;
-  };
-  int64_t row = t0 < t1 ? row_at(bi, wi) : -1;
-  DecHead hk, hv;
-  if (row >= 0) {
-    hk = attn_head<LAT>(A.K, row, j, lane);
-    hv = attn_head<LAT>(A.V, row, j, lane);
-  }
   bool bad = false;
-  for (int64_t t = t0; t < t1; ++t) {
-    // the next token's row and heads, loaded a step ahead
-    if (++wi == bt) {
-      wi = 0;
-      ++bi;
-    }
-    const int64_t nrow = t + 1 < t1 ? row_at(bi, wi) : -1;
-    DecHead nk, nv;
-    if (nrow >= 0) {
-      nk = attn_head<LAT>(A.K, nrow, j, lane);
-      nv = attn_head<LAT>(A.V, nrow, j, lane);
-    }
-    if (row >= 0) {
-      float y[8], gk;
-      bad |= !attn_tile<LAT>(A.K, hk, lane, buf, starts, s_sel, row, j, y, gk);
-      float s[G];
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        float d = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) d = __builtin_fmaf(qv[g][i], y[i], d);
-        s[g] = gk * row16_sum(d);
+  for (int64_t tb = t0; tb < t1; tb += 64) {
+    // lane i fetches token tb + i's row and both table entries (rows past the
+    // streams or a negative block id: row ~0u, the token is skipped)
+    const uint32_t n = (uint32_t)(t1 - tb < 64 ? t1 - tb : 64);
+    uint32_t rv = ~0u;
+    AttnMeta mk = {0u, 0u, 0u}, mv = {0u, 0u, 0u};
+    if ((uint32_t)lane < n) {
+      const uint32_t t = (uint32_t)(tb + lane);
+      const uint32_t bi = t / bt;
+      const int32_t blk = trow[bi];
+      const int64_t r = (int64_t)blk * bt + (t - bi * bt);
+      if (blk >= 0 && r < A.rows) {
+        rv = (uint32_t)r;
+        const int64_t sub = r * spr + j;
+        mk = {A.K.offsets[sub], A.K.offsets[sub + 1], A.K.kparam[sub]};
+        mv = {A.V.offsets[sub], A.V.offsets[sub + 1], A.V.kparam[sub]};
       }
-      float gv;
-      bad |= !attn_tile<LAT>(A.V, hv, lane, buf, starts, s_sel, row, j, y, gv);
-#pragma unroll
-      for (int g = 0; g < G; ++g) {
-        const float mn = __builtin_fmaxf(m[g], s[g]);
-        const float a = exp2f(m[g] - mn);  // 0 for the first token (m = -inf)
-        const float p = exp2f(s[g] - mn);
-        l[g] = __builtin_fmaf(l[g], a, p);
-        const float pg = p * gv;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) acc[g][i] = __builtin_fmaf(acc[g][i], a, pg * y[i]);
-        m[g] = mn;
-      }
-    } else if (lane == 0 && A.K.stats) {
+    }
+    if (__ballot(rv == ~0u && (uint32_t)lane < n) && lane == 0 && A.K.stats)
       atomicCAS(&A.K.stats->status, 0u, (uint32_t)HQ_ERR_INVALID_ARG);  // block id out of range
+    // token i's heads and norms, each loaded one token ahead
+    auto fetch = [&](uint32_t i, uint32_t& row, DecHead& hk, DecHead& hv, float& nk, float& nv) {
+      row = lane_val(rv, i);
+      if (row != ~0u) {
+        hk = dec_head<LAT>(A.K, true, lane_val(mk.s, i), lane_val(mk.e, i), lane_val(mk.k, i), lane);
+        hv = dec_head<LAT>(A.V, true, lane_val(mv.s, i), lane_val(mv.e, i), lane_val(mv.k, i), lane);
+        nk = attn_norm(A.K, row, j, lane);
+        nv = attn_norm(A.V, row, j, lane);
+      }
+    };
+    uint32_t row;
+    DecHead hk, hv;
+    float nk = 0.0f, nv = 0.0f;
+    fetch(0, row, hk, hv, nk, nv);
+    for (uint32_t i = 0; i < n; ++i) {
+      uint32_t nrow = ~0u;
+      DecHead nhk, nhv;
+      float nnk = 0.0f, nnv = 0.0f;
+      if (i + 1 < n) fetch(i + 1, nrow, nhk, nhv, nnk, nnv);
+      if (row != ~0u) {
+        float y[8];
+        bad |= !attn_tile<LAT>(A.K, hk, lane, buf, starts, s_sel, row, j, y);
+        const float gk = nk / A.K.alpha_n;
+        float s[G];
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const float4 qa = qrow[32 * g], qb = qrow[32 * g + 1];
+          float d = qa.x * y[0];
+          d = __builtin_fmaf(qa.y, y[1], d);
+          d = __builtin_fmaf(qa.z, y[2], d);
+          d = __builtin_fmaf(qa.w, y[3], d);
+          d = __builtin_fmaf(qb.x, y[4], d);
+          d = __builtin_fmaf(qb.y, y[5], d);
+          d = __builtin_fmaf(qb.z, y[6], d);
+          d = __builtin_fmaf(qb.w, y[7], d);
+          s[g] = gk * row16_sum(d);
+        }
+        bad |= !attn_tile<LAT>(A.V, hv, lane, buf, starts, s_sel, row, j, y);
+        const float gv = nv / A.V.alpha_n;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const float mn = __builtin_fmaxf(m[g], s[g]);
+          const float a = exp2f(m[g] - mn);  // 0 for the first token (m = -inf)
+          const float p = exp2f(s[g] - mn);
+          l[g] = __builtin_fmaf(l[g], a, p);
+          const float pg = p * gv;
+#pragma unroll
+          for (int i2 = 0; i2 < 8; ++i2) acc[g][i2] = __builtin_fmaf(acc[g][i2], a, pg * y[i2]);
+          m[g] = mn;
+        }
+      }
+      row = nrow;
+      hk = nhk;
+      hv = nhv;
+      nk = nnk;
+      nv = nnv;
     }
-    row = nrow;
-    hk = nk;
-    hv = nv;
   }
   if (bad && A.K.stats) {
     const unsigned long long anyb = __ballot(bad);
@@ -2091,6 +2115,7 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
         l[g] += s_l[w][q4 * G + g];
       }
     }
+    const int64_t h0 = hq0 + (int64_t)q4 * G;
 #pragma unroll
     for (int g = 0; g < G; ++g) {
       const int64_t pi = (h0 + g) * A.nx + x;
@@ -2106,12 +2131,14 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
 }
 
 // out = D H S (sum_x f_x acc_x) / (sum_x f_x l_x), f_x = 2^(m_x - max m), over
-// the splits that hold tokens, in split order, with the value plan's signs;
-// an empty sequence gives zeros.  One lane group of 16 per query head.
+// the splits that hold tokens, with the value plan's signs; an empty sequence
+// gives zeros.  One workgroup per query head: lane group k of 16 takes splits
+// k, k + 16, ..., and the 16 groups' sums meet in LDS in group order.
 __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int64_t pair = ((int64_t)blockIdx.x * HQ_WAVES_PER_WG + (tid >> 6)) * 4 + (lane >> 4);
-  if (pair >= A.batch * A.heads_q) return;  // whole lane groups
+  __shared__ float s_red[16];
+  __shared__ float4 s_acc[16][32];
+  const int tid = threadIdx.x, lane = tid & 63, grp = tid >> 4;
+  const int64_t pair = blockIdx.x;
   const int64_t b = pair / A.heads_q;
   const int32_t kvh = (int32_t)(pair - b * A.heads_q) / A.group;
   const int c0 = (lane & 15) * 8;
@@ -2121,10 +2148,15 @@ __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
   const float* pm = A.part_m + pair * A.nx;
   const float* pl = A.part_l + pair * A.nx;
   float M = -__builtin_inff();
-  for (int32_t x = 0; x < n; ++x) M = __builtin_fmaxf(M, pm[x]);
+  for (int32_t x = grp; x < n; x += 16) M = __builtin_fmaxf(M, pm[x]);
+  if ((tid & 15) == 0) s_red[grp] = M;
+  __syncthreads();
+  M = s_red[0];
+#pragma unroll
+  for (int k = 1; k < 16; ++k) M = __builtin_fmaxf(M, s_red[k]);
   float L = 0.0f, v[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
   if (M != -__builtin_inff()) {
-    for (int32_t x = 0; x < n; ++x) {
+    for (int32_t x = grp; x < n; x += 16) {
       const float mx = pm[x];
       const float f = mx == -__builtin_inff() ? 0.0f : exp2f(mx - M);
       L = __builtin_fmaf(f, pl[x], L);
@@ -2136,6 +2168,25 @@ __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
       v[4] = __builtin_fmaf(f, a1.x, v[4]); v[5] = __builtin_fmaf(f, a1.y, v[5]);
       v[6] = __builtin_fmaf(f, a1.z, v[6]); v[7] = __builtin_fmaf(f, a1.w, v[7]);
     }
+  }
+  __syncthreads();  // every group has read s_red
+  s_acc[grp][(lane & 15) * 2] = make_float4(v[0], v[1], v[2], v[3]);
+  s_acc[grp][(lane & 15) * 2 + 1] = make_float4(v[4], v[5], v[6], v[7]);
+  if ((tid & 15) == 0) s_red[grp] = L;
+  __syncthreads();
+  if (tid >= 16) return;  // group 0 finishes: no barrier follows
+  L = 0.0f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const float4 a0 = s_acc[k][tid * 2], a1 = s_acc[k][tid * 2 + 1];
+    if (k == 0) {
+      v[0] = a0.x; v[1] = a0.y; v[2] = a0.z; v[3] = a0.w;
+      v[4] = a1.x; v[5] = a1.y; v[6] = a1.z; v[7] = a1.w;
+    } else {
+      v[0] += a0.x; v[1] += a0.y; v[2] += a0.z; v[3] += a0.w;
+      v[4] += a1.x; v[5] += a1.y; v[6] += a1.z; v[7] += a1.w;
+    }
+    L += s_red[k];
   }
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
   const uint32_t sbits = A.V.rotation ? sign_bits8(A.V.smask, c0) : 0u;
@@ -2594,6 +2645,7 @@ int hq_launch_decode_attention(const hq_attn_args& a, int lattice, void* stream)
   }
 #undef HQ_ATTN_GROUPS
 #undef HQ_ATTN_CASE
-  hipLaunchKernelGGL(hq_attn_combine_kernel, dim3(heads), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(hq_attn_combine_kernel, dim3((uint32_t)(a.batch * a.heads_q)), dim3(256), 0,
+                     st, a);
   return (int)hipGetLastError();
 }
