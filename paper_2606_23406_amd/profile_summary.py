@@ -135,7 +135,8 @@ def stats(stats_csv, log, out, cmd):
              f"{b['roofline']['launches_per_step']} launches each way (hq_encode_group / "
              f"hq_decode_group, up to 16 matrices per launch); {steps} steps ran "
              f"({b['warmup']} warmup + {b['steps']} timed). The other rows come from the rest "
-             "of the run (the GEMM, the D4 stack, the C1/C2/C4 configurations).", "",
+             "of the run (the GEMM, the fused decode-GEMV and decode-attention legs, the D4 "
+             "stack, the C1/C2/C4 configurations).", "",
              "| kernel | calls | total ms | avg us | min us | max us |", "|---|---|---|---|---|---|"]
     per = {}
     for r in rows:
