@@ -395,7 +395,8 @@ def decode_gemv(params: Params, codes, norms, x, row0=0):
 
 
 def decode_attention(pk: Params, k_codes, k_norms, pv: Params, v_codes, v_norms, q,
-                     block_table, seq_lens, block_tokens, scale, rows=None):
+                     block_table, seq_lens, block_tokens, scale, rows=None, window=0,
+                     window_k=None, window_v=None):
     """One-token attention over a coded KV cache (the KV path of Sec. 5.2 and
     the decode of Sec. 5.3 feeding attention, as the end-to-end runs of Sec.
     6.6 use it): the cached keys and values are the decoded rows exactly as
@@ -412,6 +413,12 @@ def decode_attention(pk: Params, k_codes, k_norms, pv: Params, v_codes, v_norms,
                         (default 0, 1, ...): lets a caller pass only the rows
                         the table reaches; each is decoded at its own index
                         (the dither depends on it).
+      window            residual window W (the most recent tokens kept exact,
+                        as in the KV comparison of Sec. 6.7.2, where W = 32
+                        costs about 0.1 bps): the last min(W, seq_len)
+                        tokens of a sequence are read from window_k /
+                        window_v [batch, W, H_kv * tile] at slot t % W, the
+                        rest from the coded rows.
     Returns [batch, H_q, tile] fp64."""
     if rows is None:
         kd = backend(pk, k_codes, k_norms).astype(np.float64)
@@ -435,6 +442,9 @@ def decode_attention(pk: Params, k_codes, k_norms, pv: Params, v_codes, v_norms,
         T = int(seq_lens[b])
         if T == 0:
             continue
+        w = min(window, T)
+        tw = np.arange(T - w, T)  # exact tokens, ring slots tw % window
+        T -= w
         t = np.arange(T)
         r = np.asarray(block_table[b])[t // block_tokens].astype(np.int64) * block_tokens + t % block_tokens
         if local is not None:
@@ -443,9 +453,13 @@ def decode_attention(pk: Params, k_codes, k_norms, pv: Params, v_codes, v_norms,
             r = local[1][i]
         for h in range(Hq):
             cs = slice((h // G) * n, (h // G + 1) * n)
-            s = (kd[r, cs] @ q[b, h]) * scale
+            keys, vals = kd[r, cs], vd[r, cs]
+            if w:
+                keys = np.concatenate([keys, np.asarray(window_k, np.float64)[b, tw % window, cs]])
+                vals = np.concatenate([vals, np.asarray(window_v, np.float64)[b, tw % window, cs]])
+            s = (keys @ q[b, h]) * scale
             p = np.exp(s - s.max())
-            out[b, h] = (p / p.sum()) @ vd[r, cs]
+            out[b, h] = (p / p.sum()) @ vals
     return out
 
 

@@ -157,3 +157,44 @@ def test_subset_of_rows_at_their_indices(cache):
     sub = O.decode_attention(c["pk"], c["kc"][keep], c["kn"][keep], c["pv"], c["vc"][keep],
                              c["vn"][keep], q, TABLE, np.array([37, 1, 0]), BT, 1.0, rows=keep)
     assert np.array_equal(sub, full)
+
+
+def test_residual_window(cache):
+    # the last min(W, len) tokens come exact from the ring slots t % W
+    rng = np.random.default_rng(9)
+    W = 8
+    wk = rng.standard_normal((3, W, 4 * N))
+    wv = rng.standard_normal((3, W, 4 * N))
+    c = cache
+
+    def att(q, lens, scale=1.0):
+        return O.decode_attention(c["pk"], c["kc"], c["kn"], c["pv"], c["vc"], c["vn"], q, TABLE,
+                                  np.asarray(lens), BT, scale, window=W, window_k=wk, window_v=wv)
+
+    q = np.zeros((3, 8, N))
+    out = att(q, [37, 1, 0])
+    vd = c["vd"]
+    for h in range(8):
+        cs = slice((h // 2) * N, (h // 2 + 1) * N)
+        # tokens 0..28 coded (rows listed by hand), 29..36 exact in slots 5, 6, 7, 0, 1, 2, 3, 4
+        rows = ROWS0[:29]
+        allv = np.concatenate([vd[rows, cs], wv[0, [5, 6, 7, 0, 1, 2, 3, 4], cs]])
+        np.testing.assert_allclose(out[0, h], allv.mean(axis=0), rtol=0, atol=1e-12)
+        # one token, exact: slot 0 of sequence 1
+        assert np.array_equal(out[1, h], wv[1, 0, cs])
+    assert np.array_equal(out[2], np.zeros((8, N)))
+    # a huge scale picks the best key, coded or exact
+    q = rng.standard_normal((3, 8, N))
+    out = att(q, [37, 1, 0], scale=1e6)
+    kd = c["kd"]
+    for h in range(8):
+        cs = slice((h // 2) * N, (h // 2 + 1) * N)
+        keys = np.concatenate([kd[ROWS0[:29], cs], wk[0, [5, 6, 7, 0, 1, 2, 3, 4], cs]])
+        vals = np.concatenate([vd[ROWS0[:29], cs], wv[0, [5, 6, 7, 0, 1, 2, 3, 4], cs]])
+        np.testing.assert_allclose(out[0, h], vals[int(np.argmax(keys @ q[0, h]))], rtol=0, atol=1e-9)
+    # W = 0 is the plain coded cache
+    q = rng.standard_normal((3, 8, N))
+    plain = attend(c, q, [37, 1, 0])
+    zero = O.decode_attention(c["pk"], c["kc"], c["kn"], c["pv"], c["vc"], c["vn"], q, TABLE,
+                              np.array([37, 1, 0]), BT, 1.0, window=0)
+    assert np.array_equal(plain, zero)
