@@ -290,6 +290,13 @@ size_t hq_attention_workspace_bytes(hq_plan_t k_plan, int64_t batch, int32_t hea
  *               per sequence with block_tokens = its length is a plain one).
  *   seq_lens    device int32 [batch] token counts; an empty sequence gives
  *               zeros.
+ *   window      residual window W, 0 .. 256 (0: none): the last
+ *               min(W, seq_len) tokens of each sequence are read exact from
+ *               window_k / window_v instead of the streams (the most recent
+ *               tokens kept exact, as in the KV comparison of Sec. 6.7.2).
+ *   window_k, window_v  device rings [batch, W, H_kv * 128] of element type
+ *               wt (HQ_BF16 or HQ_FP32), 16-byte aligned: token t sits in
+ *               slot t % W.  Ignored (may be null) when window = 0.
  *   out         device [batch, heads_q, 128], HQ_FP32 or HQ_BF16 (round to
  *               nearest even), 16-byte aligned.
  *   workspace   device, 16-byte aligned, >= hq_attention_workspace_bytes(
@@ -305,8 +312,9 @@ hq_status hq_decode_attention(hq_plan_t k_plan, const hq_stream* k, hq_plan_t v_
                               const hq_stream* v, const void* q, int32_t qt, int64_t batch,
                               int32_t heads_q, float scale, const int32_t* block_table,
                               int32_t max_blocks, int32_t block_tokens, const int32_t* seq_lens,
-                              void* out, int32_t ot, void* workspace, size_t ws_bytes,
-                              void* stream);
+                              const void* window_k, const void* window_v, int32_t wt,
+                              int32_t window, void* out, int32_t ot, void* workspace,
+                              size_t ws_bytes, void* stream);
 
 /* The library's automatic Rice-k rule for `count` symbols summing to `sum`
  * (the geometric optimum k* of Sec. 3.3), as the kernels evaluate it. */

@@ -585,8 +585,10 @@ size_t hq_attention_workspace_bytes(hq_plan_t k, int64_t batch, int32_t heads_q,
 hq_status hq_decode_attention(hq_plan_t pk, const hq_stream* k, hq_plan_t pv, const hq_stream* v,
                               const void* q, int32_t qt, int64_t batch, int32_t heads_q,
                               float scale, const int32_t* block_table, int32_t max_blocks,
-                              int32_t block_tokens, const int32_t* seq_lens, void* out,
-                              int32_t ot, void* workspace, size_t ws_bytes, void* stream) {
+                              int32_t block_tokens, const int32_t* seq_lens,
+                              const void* window_k, const void* window_v, int32_t wt,
+                              int32_t window, void* out, int32_t ot, void* workspace,
+                              size_t ws_bytes, void* stream) {
   if (!pk || !k || !pv || !v || batch < 0) return HQ_ERR_INVALID_ARG;
   if ((qt != HQ_BF16 && qt != HQ_FP32) || (ot != HQ_BF16 && ot != HQ_FP32)) return HQ_ERR_INVALID_ARG;
   if (pk->lattice != pv->lattice || pk->cols != pv->cols || pk->tile != HQ_TILE ||
@@ -597,6 +599,10 @@ hq_status hq_decode_attention(hq_plan_t pk, const hq_stream* k, hq_plan_t pv, co
   const int64_t group = heads_q / hkv;
   if (group != 1 && group != 2 && group != 4 && group != 8) return HQ_ERR_UNSUPPORTED;
   if (max_blocks <= 0 || block_tokens <= 0 || !std::isfinite(scale)) return HQ_ERR_INVALID_ARG;
+  if (window < 0 || window > HQ_ATTN_WINDOW_MAX) return HQ_ERR_INVALID_ARG;
+  if (window > 0 && (!window_k || !window_v || !aligned16(window_k) || !aligned16(window_v) ||
+                     (wt != HQ_BF16 && wt != HQ_FP32)))
+    return HQ_ERR_INVALID_ARG;
   const int64_t max_tokens = (int64_t)max_blocks * block_tokens;
   if (max_tokens > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
   if (batch == 0) return HQ_OK;
@@ -637,6 +643,10 @@ hq_status hq_decode_attention(hq_plan_t pk, const hq_stream* k, hq_plan_t pv, co
   a.out_bf16 = ot == HQ_BF16;
   a.lds_words = std::max(a.K.lds_words, a.V.lds_words);
   a.qscale = scale * 1.4426950408889634f;  // log2(e): the softmax runs in base 2
+  a.win_k = window_k;
+  a.win_v = window_v;
+  a.window = window;
+  a.win_bf16 = wt == HQ_BF16;
   return hip_status(hq_launch_decode_attention(a, pk->lattice, stream));
 }
 

@@ -126,7 +126,13 @@ struct hq_attn_args {
   int32_t q_bf16, out_bf16;
   uint32_t lds_words;       // decode buffer words (the larger of K's and V's)
   float qscale;             // softmax scale times log2(e)
+  const void* win_k;        // residual window rings [batch, window, H_kv * 128]
+  const void* win_v;
+  int32_t window;           // 0: none
+  int32_t win_bf16;
 };
+
+#define HQ_ATTN_WINDOW_MAX 256  // residual window tokens a call may keep exact
 
 // Several matrices in one launch (kernel arguments, by value): member i owns
 // workgroups wg_begin[i] .. wg_begin[i + 1] - 1 (the last one to the grid end).

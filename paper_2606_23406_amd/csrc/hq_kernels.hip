@@ -1874,6 +1874,30 @@ __device__ __forceinline__ int64_t attn_seq_len(const hq_attn_args& A, int64_t b
   return len;
 }
 
+// Tokens of a sequence read from the coded streams: all but the residual
+// window's last min(window, len).
+__device__ __forceinline__ int64_t attn_coded_len(const hq_attn_args& A, int64_t len) {
+  return len - (len < A.window ? len : (int64_t)A.window);
+}
+
+// 8 consecutive values (16-byte aligned) of a bf16 or fp32 array as fp32.
+__device__ __forceinline__ void load8(const void* p, int64_t i, bool bf16, float* v) {
+  if (bf16) {
+    const uint4 raw = *(const uint4*)((const uint16_t*)p + i);
+    const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      v[2 * k] = bf16_to_f32(w4[k] & 0xFFFFu);
+      v[2 * k + 1] = bf16_to_f32(w4[k] >> 16);
+    }
+  } else {
+    const float4 a = *(const float4*)((const float*)p + i);
+    const float4 b = *(const float4*)((const float*)p + i + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+}
+
 // qt = (S H D q) * scale * log2(e) per query head, with the key plan's signs
 // (D of the head's own columns); one lane group of 16 per head.
 __global__ __launch_bounds__(256) void hq_attn_prep_kernel(hq_attn_args A) {
@@ -1883,20 +1907,7 @@ __global__ __launch_bounds__(256) void hq_attn_prep_kernel(hq_attn_args A) {
   const int32_t kvh = (int32_t)(pair % A.heads_q) / A.group;
   const int c0 = (lane & 15) * 8;
   float v[8];
-  if (A.q_bf16) {
-    const uint4 raw = *(const uint4*)((const uint16_t*)A.q + pair * HQ_TILE + c0);
-    const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[2 * i] = bf16_to_f32(w4[i] & 0xFFFFu);
-      v[2 * i + 1] = bf16_to_f32(w4[i] >> 16);
-    }
-  } else {
-    const float4 a = *(const float4*)((const float*)A.q + pair * HQ_TILE + c0);
-    const float4 b = *(const float4*)((const float*)A.q + pair * HQ_TILE + c0 + 4);
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-  }
+  load8(A.q, pair * HQ_TILE + c0, A.q_bf16, v);
   const uint32_t dbits = sign_bits8(A.K.dmask, (int64_t)kvh * HQ_TILE + c0);
 #pragma unroll
   for (int i = 0; i < 8; ++i) v[i] = flip(v[i], dbits, i);
@@ -1961,7 +1972,7 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
   const uint32_t x = blockIdx.x % (uint32_t)A.nx;
   const uint32_t bj = blockIdx.x / (uint32_t)A.nx;
   const uint32_t b = bj / spr, j = bj - b * spr;
-  const int64_t len = attn_seq_len(A, b, tid == 0 && x == 0 && j == 0);
+  const int64_t len = attn_coded_len(A, attn_seq_len(A, b, tid == 0 && x == 0 && j == 0));
   const int64_t wg_t0 = (int64_t)x * HQ_WAVES_PER_WG * A.chunk;
   if (wg_t0 >= len) return;  // the whole workgroup, before any barrier
   s_sel[tid] = kByteSelect.e[tid];
@@ -2130,24 +2141,47 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
   }
 }
 
-// out = D H S (sum_x f_x acc_x) / (sum_x f_x l_x), f_x = 2^(m_x - max m), over
-// the splits that hold tokens, with the value plan's signs; an empty sequence
-// gives zeros.  One workgroup per query head: lane group k of 16 takes splits
-// k, k + 16, ..., and the 16 groups' sums meet in LDS in group order.
+// out = (D H S sum_x f_x acc_x + sum_i p_i v_i) / (sum_x f_x l_x + sum_i p_i):
+// the coded splits that hold tokens (f_x = 2^(m_x - M)) with the value
+// plan's signs, plus the residual window's exact tokens i (p_i = 2^(s_i - M),
+// s_i = q . k_i scaled in natural coordinates), M the maximum over both; an
+// empty sequence gives zeros.  One workgroup per query head: lane group k of
+// 16 takes splits k, k + 16, ... and window tokens k, k + 16, ..., and the 16
+// groups' sums meet in LDS in group order.
 __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
   __shared__ float s_red[16];
+  __shared__ float s_win[HQ_ATTN_WINDOW_MAX];
   __shared__ float4 s_acc[16][32];
+  __shared__ float4 s_nat[16][32];
   const int tid = threadIdx.x, lane = tid & 63, grp = tid >> 4;
   const int64_t pair = blockIdx.x;
   const int64_t b = pair / A.heads_q;
   const int32_t kvh = (int32_t)(pair - b * A.heads_q) / A.group;
   const int c0 = (lane & 15) * 8;
   const int64_t len = attn_seq_len(A, b, false);
+  const int64_t clen = attn_coded_len(A, len);
+  const int32_t w = (int32_t)(len - clen);
   const int64_t per = (int64_t)HQ_WAVES_PER_WG * A.chunk;
-  const int32_t n = (int32_t)((len + per - 1) / per);
+  const int32_t n = (int32_t)((clen + per - 1) / per);
   const float* pm = A.part_m + pair * A.nx;
   const float* pl = A.part_l + pair * A.nx;
+  const int64_t hkv = (int64_t)A.heads_q / A.group;
   float M = -__builtin_inff();
+  if (w > 0) {
+    float q[8];
+    load8(A.q, pair * HQ_TILE + c0, A.q_bf16, q);
+    for (int32_t i = grp; i < w; i += 16) {
+      const int64_t slot = (clen + i) % A.window;
+      float k[8];
+      load8(A.win_k, ((b * A.window + slot) * hkv + kvh) * HQ_TILE + c0, A.win_bf16, k);
+      float d = q[0] * k[0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) d = __builtin_fmaf(q[e], k[e], d);
+      const float si = row16_sum(d) * A.qscale;
+      if ((tid & 15) == 0) s_win[i] = si;
+      M = __builtin_fmaxf(M, si);
+    }
+  }
   for (int32_t x = grp; x < n; x += 16) M = __builtin_fmaxf(M, pm[x]);
   if ((tid & 15) == 0) s_red[grp] = M;
   __syncthreads();
@@ -2155,6 +2189,7 @@ __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
 #pragma unroll
   for (int k = 1; k < 16; ++k) M = __builtin_fmaxf(M, s_red[k]);
   float L = 0.0f, v[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
+  float vn[8] = {0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f, 0.0f};
   if (M != -__builtin_inff()) {
     for (int32_t x = grp; x < n; x += 16) {
       const float mx = pm[x];
@@ -2168,10 +2203,21 @@ __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
       v[4] = __builtin_fmaf(f, a1.x, v[4]); v[5] = __builtin_fmaf(f, a1.y, v[5]);
       v[6] = __builtin_fmaf(f, a1.z, v[6]); v[7] = __builtin_fmaf(f, a1.w, v[7]);
     }
+    for (int32_t i = grp; i < w; i += 16) {
+      const int64_t slot = (clen + i) % A.window;
+      const float p = exp2f(s_win[i] - M);
+      L += p;
+      float val[8];
+      load8(A.win_v, ((b * A.window + slot) * hkv + kvh) * HQ_TILE + c0, A.win_bf16, val);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) vn[e] = __builtin_fmaf(p, val[e], vn[e]);
+    }
   }
   __syncthreads();  // every group has read s_red
   s_acc[grp][(lane & 15) * 2] = make_float4(v[0], v[1], v[2], v[3]);
   s_acc[grp][(lane & 15) * 2 + 1] = make_float4(v[4], v[5], v[6], v[7]);
+  s_nat[grp][(lane & 15) * 2] = make_float4(vn[0], vn[1], vn[2], vn[3]);
+  s_nat[grp][(lane & 15) * 2 + 1] = make_float4(vn[4], vn[5], vn[6], vn[7]);
   if ((tid & 15) == 0) s_red[grp] = L;
   __syncthreads();
   if (tid >= 16) return;  // group 0 finishes: no barrier follows
@@ -2179,12 +2225,17 @@ __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
 #pragma unroll
   for (int k = 0; k < 16; ++k) {
     const float4 a0 = s_acc[k][tid * 2], a1 = s_acc[k][tid * 2 + 1];
+    const float4 n0 = s_nat[k][tid * 2], n1 = s_nat[k][tid * 2 + 1];
     if (k == 0) {
       v[0] = a0.x; v[1] = a0.y; v[2] = a0.z; v[3] = a0.w;
       v[4] = a1.x; v[5] = a1.y; v[6] = a1.z; v[7] = a1.w;
+      vn[0] = n0.x; vn[1] = n0.y; vn[2] = n0.z; vn[3] = n0.w;
+      vn[4] = n1.x; vn[5] = n1.y; vn[6] = n1.z; vn[7] = n1.w;
     } else {
       v[0] += a0.x; v[1] += a0.y; v[2] += a0.z; v[3] += a0.w;
       v[4] += a1.x; v[5] += a1.y; v[6] += a1.z; v[7] += a1.w;
+      vn[0] += n0.x; vn[1] += n0.y; vn[2] += n0.z; vn[3] += n0.w;
+      vn[4] += n1.x; vn[5] += n1.y; vn[6] += n1.z; vn[7] += n1.w;
     }
     L += s_red[k];
   }
@@ -2196,7 +2247,7 @@ __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
   fwht128(v, sg);
   const uint32_t dbits = sign_bits8(A.V.dmask, (int64_t)kvh * HQ_TILE + c0);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) v[i] = flip(v[i], dbits, i);
+  for (int i = 0; i < 8; ++i) v[i] = __builtin_fmaf(vn[i], inv, flip(v[i], dbits, i));
   if (A.out_bf16) {
     uint4 o;
     o.x = cvt_pk_bf16(v[0], v[1]);

@@ -105,7 +105,7 @@ def lib():
     L.hq_attention_workspace_bytes.argtypes = [p, i64, i32, i64]
     L.hq_decode_attention.restype = i32
     L.hq_decode_attention.argtypes = [p, p, p, p, p, i32, i64, i32, C.c_float, p, i32, i32, p, p,
-                                      i32, p, C.c_size_t, p]
+                                      p, i32, i32, p, i32, p, C.c_size_t, p]
     L.hq_rice_kstar.restype = i32
     L.hq_rice_kstar.argtypes = [i64, i64]
     L.hq_calibrated_snr.restype = i32
@@ -352,10 +352,12 @@ def hq_attention_workspace_bytes(k_plan: Plan, batch, heads_q, max_tokens):
 def hq_decode_attention(k_plan: Plan, k: EncodedStream, v_plan: Plan, v: EncodedStream,
                         q: torch.Tensor, block_table: torch.Tensor, seq_lens: torch.Tensor,
                         block_tokens, scale=None, out_dtype=torch.float32, workspace=None,
-                        out=None, stream=None):
+                        out=None, stream=None, window_k=None, window_v=None):
     """hq_decode_attention: q [batch, heads_q, 128] (bf16 or fp32) attends
     over the coded cache; block_table int32 [batch, max_blocks] and seq_lens
-    int32 [batch] on the device.  Returns [batch, heads_q, 128]."""
+    int32 [batch] on the device.  window_k / window_v: optional residual
+    window rings [batch, W, H_kv * 128] (bf16 or fp32, token t in slot t % W).
+    Returns [batch, heads_q, 128]."""
     assert q.is_cuda and q.dim() == 3 and q.shape[2] == 128 and q.is_contiguous()
     assert block_table.dtype == torch.int32 and block_table.is_contiguous() and block_table.dim() == 2
     assert seq_lens.dtype == torch.int32 and seq_lens.is_contiguous()
@@ -367,10 +369,17 @@ def hq_decode_attention(k_plan: Plan, k: EncodedStream, v_plan: Plan, v: Encoded
         workspace = torch.empty(max(nb, 16), dtype=torch.uint8, device=q.device)
     if out is None:
         out = torch.empty((batch, heads_q, 128), dtype=out_dtype, device=q.device)
+    window, wk, wv, wt = 0, None, None, 0
+    if window_k is not None:
+        assert window_v is not None and window_k.shape == window_v.shape and window_k.dim() == 3
+        assert window_k.is_contiguous() and window_v.is_contiguous() and window_k.dtype == window_v.dtype
+        window, wt = window_k.shape[1], _dtype_code(window_k.dtype)
+        wk, wv = C.c_void_p(window_k.data_ptr()), C.c_void_p(window_v.data_ptr())
     st = lib().hq_decode_attention(k_plan.handle, C.byref(k.c), v_plan.handle, C.byref(v.c),
                                    C.c_void_p(q.data_ptr()), _dtype_code(q.dtype), batch, heads_q,
                                    C.c_float(scale), C.c_void_p(block_table.data_ptr()),
                                    max_blocks, block_tokens, C.c_void_p(seq_lens.data_ptr()),
+                                   wk, wv, wt, window,
                                    C.c_void_p(out.data_ptr()), _dtype_code(out.dtype),
                                    C.c_void_p(workspace.data_ptr()), workspace.numel(),
                                    _stream_handle(stream))

@@ -57,27 +57,36 @@ def kv_pair(hq, lat, rows, hkv, seed, kv=True):
     return (pk,) + coded(hq, pk, k), (pv,) + coded(hq, pv, v)
 
 
-def check(hq, K, V, q, table, lens, bt, label, scale=N ** -0.5):
+def check(hq, K, V, q, table, lens, bt, label, scale=N ** -0.5, wk=None, wv=None):
     pk, plk, sk, kc, kn = K
     pv, plv, sv, vc, vn = V
-    ref = O.decode_attention(pk, kc, kn, pv, vc, vn, q.float().numpy(), table, lens, bt, scale)
+    W = 0 if wk is None else wk.shape[1]
+    ref = O.decode_attention(pk, kc, kn, pv, vc, vn, q.float().numpy(), table, lens, bt, scale,
+                             window=W, window_k=None if wk is None else wk.float().numpy(),
+                             window_v=None if wv is None else wv.float().numpy())
     vd = O.backend(pv, vc, vn)
     B, Hq = q.shape[0], q.shape[1]
     G = Hq // (vd.shape[1] // N)
     tab, ln = torch.from_numpy(table).cuda(), torch.from_numpy(np.asarray(lens, np.int32)).cuda()
     print(f"[attn] {label} q={q.dtype} batch={B} heads={Hq} lens={list(lens)}", flush=True)
-    out = hq.hq_decode_attention(plk, sk, plv, sv, q.cuda(), tab, ln, bt, scale=scale)
+    win = {} if wk is None else dict(window_k=wk.cuda(), window_v=wv.cuda())
+    out = hq.hq_decode_attention(plk, sk, plv, sv, q.cuda(), tab, ln, bt, scale=scale, **win)
     out16 = hq.hq_decode_attention(plk, sk, plv, sv, q.cuda(), tab, ln, bt, scale=scale,
-                                   out_dtype=torch.bfloat16)
+                                   out_dtype=torch.bfloat16, **win)
     torch.cuda.synchronize()
     got = out.cpu().numpy().astype(np.float64)
     worst = 0.0
     for b in range(B):
         t = np.arange(lens[b])
         rows = table[b][t // bt].astype(np.int64) * bt + t % bt
+        w = min(W, lens[b])
+        rows = rows[:lens[b] - w]
         for h in range(Hq):
             cs = slice((h // G) * N, (h // G + 1) * N)
-            unit = np.abs(vd[rows, cs]).max() if lens[b] else 1.0
+            vals = np.abs(vd[rows, cs])
+            if w:
+                vals = np.concatenate([vals, np.abs(wv.float().numpy()[b, :, cs])])
+            unit = vals.max() if lens[b] else 1.0
             err = np.abs(got[b, h] - ref[b, h]).max() / unit
             worst = max(worst, err)
             assert err <= 2e-5, (label, b, h, err)
@@ -127,6 +136,22 @@ def test_attention_head_groups_and_splits(hq, group):
     check(hq, K, V, q, table, lens, 16, f"E8 group {group}")
 
 
+@pytest.mark.parametrize("W", [8, 32])
+def test_attention_residual_window(hq, W):
+    # the last min(W, len) tokens read exact from a ring (token t in slot
+    # t % W), bf16 and fp32 rings; lengths below, at and above W, and empty
+    rng = np.random.default_rng(95 + W)
+    K, V = kv_pair(hq, O.E8, 40 * 16, 4, 96)
+    lens = [37, 5, 0, W, 300]
+    table = paged(rng, lens, 16, 40)
+    q = torch.from_numpy(rng.standard_normal((5, 8, N)).astype(np.float32))
+    for dt in (torch.bfloat16, torch.float32):
+        wk = torch.from_numpy(rng.standard_normal((5, W, 4 * N)).astype(np.float32)).to(dt)
+        wk[:, :, 3::N] *= 10
+        wv = torch.from_numpy(rng.standard_normal((5, W, 4 * N)).astype(np.float32)).to(dt)
+        check(hq, K, V, q, table, lens, 16, f"E8 window {W} {dt}", wk=wk, wv=wv)
+
+
 def test_attention_plain_streams_and_contiguous_table(hq):
     # weight-style plans (no rotation, dither or fp16 norms) and one block per
     # sequence (a contiguous cache)
@@ -165,6 +190,9 @@ def test_attention_errors(hq):
     other = hq.hq_plan(128, hq.HQ_E8, 0.0, 5, -1, 1024, snr_db=20.0)
     with pytest.raises(hq.HQError):  # key and value plans of different widths
         hq.hq_decode_attention(plk, sk, other, sv, q, table, ln, 16)
+    big = torch.zeros((1, 257, 4 * N), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(hq.HQError):  # residual window above 256 tokens
+        hq.hq_decode_attention(plk, sk, plv, sv, q, table, ln, 16, window_k=big, window_v=big)
     # a block id past the streams' rows is skipped and reported; the rest is
     # the attention over the remaining tokens
     sk.reset_stats()
