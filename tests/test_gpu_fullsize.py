@@ -343,14 +343,23 @@ def test_c4_decode_attention_as_benched(hq):
     launch shape the bench times: keys and values [16, 8192, 8, 128] E8 at 2
     bps (signs rotation, dither, fp16 norms) appended in 128-token blocks, a
     stream row being (block, sequence, token); 32 query heads (4 per KV
-    head), one sequence cut to 5000 tokens.  Three sampled sequences against
-    the oracle over those sequences' rows, within 2e-5 of max |v^|."""
+    head), one sequence cut to 5000 tokens; without and with a 32-token exact
+    window (the ring holding the last 32 tokens of the unquantized cache).
+    Three sampled sequences against the oracle over those sequences' rows,
+    within 2e-5 of max |v^|."""
     from paper_2606_23406_amd import workloads as W
     B, T, Hkv, Hq, bt = 16, 8192, 8, 32, 128
     snr = PT.op_snr("E8", 2.0)
-    streams = []
+    streams, rings = [], []
     for role, seed in (("k", 91), ("v", 95)):
-        x = W.kv_cache(role=role).permute(1, 0, 2, 3).reshape(T // bt, bt, B, Hkv * 128)
+        x = W.kv_cache(role=role)
+        lens_ring = np.full(B, T)
+        lens_ring[5] = 5000
+        # ring slot t % 32 holds token t of the last 32 of each sequence
+        ring = torch.stack([x[b, n - 32:n].reshape(32, Hkv * 128).roll(n % 32, 0)
+                            for b, n in enumerate(lens_ring)]).contiguous()
+        rings.append(ring)
+        x = x.permute(1, 0, 2, 3).reshape(T // bt, bt, B, Hkv * 128)
         x = x.permute(0, 2, 1, 3).reshape(-1, Hkv * 128).contiguous()
         P = PT.oracle_params(O.E8, snr, rht_seed=seed, rotation=1, rot_seed=seed + 1, dither=True,
                              dither_seed=seed + 2, norm_fp16=True)
@@ -370,6 +379,9 @@ def test_c4_decode_attention_as_benched(hq):
           f"heads, E8@2 keys and values", flush=True)
     out = hq.hq_decode_attention(plk, sk, plv, sv, q.cuda(), torch.from_numpy(table).cuda(),
                                  torch.from_numpy(lens).cuda(), bt)
+    outw = hq.hq_decode_attention(plk, sk, plv, sv, q.cuda(), torch.from_numpy(table).cuda(),
+                                  torch.from_numpy(lens).cuda(), bt, window_k=rings[0].cuda(),
+                                  window_v=rings[1].cuda())
     torch.cuda.synchronize()
     for st in (sk.read_stats(), sv.read_stats()):
         assert st["status"] == 0 and st["corrupt_substreams"] == 0, st
@@ -393,15 +405,24 @@ def test_c4_decode_attention_as_benched(hq):
         ref = O.decode_attention(pk, codes[0], norms[0], pv, codes[1], norms[1],
                                  q[b:b + 1].float().numpy(), table[b:b + 1], lens[b:b + 1], bt,
                                  128 ** -0.5, rows=rows)[0]
+        refw = O.decode_attention(pk, codes[0], norms[0], pv, codes[1], norms[1],
+                                  q[b:b + 1].float().numpy(), table[b:b + 1], lens[b:b + 1], bt,
+                                  128 ** -0.5, rows=rows, window=32,
+                                  window_k=rings[0][b:b + 1].float().numpy(),
+                                  window_v=rings[1][b:b + 1].float().numpy())[0]
+        gotw = outw.cpu().numpy().astype(np.float64)
         vd = np.concatenate([O.backend(pv, codes[1][k:k + bt], norms[1][k:k + bt], row0=int(rows[k]))
                              for k in range(0, rows.size, bt)])
         for h in range(Hq):
             cs = slice((h // 4) * 128, (h // 4 + 1) * 128)
             err = np.abs(got[b, h] - ref[h]).max() / np.abs(vd[:lens[b], cs]).max()
-            worst = max(worst, err)
-            assert err <= 2e-5, (b, h, err)
-    print(f"[fullsize] C4 decode attention: 3 sequences x {Hq} heads, worst error {worst:.2e} "
-          f"of max |v|", flush=True)
+            unit_w = max(np.abs(vd[:lens[b] - 32, cs]).max(),
+                         float(rings[1][b, :, cs].float().abs().max()))
+            errw = np.abs(gotw[b, h] - refw[h]).max() / unit_w
+            worst = max(worst, err, errw)
+            assert err <= 2e-5 and errw <= 2e-5, (b, h, err, errw)
+    print(f"[fullsize] C4 decode attention (plain and 32-token window): 3 sequences x {Hq} heads, "
+          f"worst error {worst:.2e} of max |v|", flush=True)
 
 
 def test_c5_gemm_fullsize(hq):
