@@ -104,3 +104,13 @@ def test_group_argument_errors_are_synchronous(hq):
     assert L.hq_decode_group(None, None, None, 0, None, 0, None) == 0
     assert L.hq_decode_group(None, None, None, 0, None, 3, None) == -1
     assert L.hq_decode_group(None, None, None, 7, None, 0, None) == -1  # bad output type
+
+
+def test_fused_entry_points_reject_null_plans(hq):
+    # argument errors come back before any device work (no GPU needed)
+    L = hq.lib()
+    assert L.hq_gemv_workspace_bytes(None) == 0
+    assert L.hq_attention_workspace_bytes(None, 1, 8, 64) == 0
+    assert L.hq_decode_gemv(None, None, 0, 1, None, 0, None, 0, None, 0, None) == -1
+    assert L.hq_decode_attention(None, None, None, None, None, 0, 1, 8, C.c_float(0.1), None, 1, 16,
+                                 None, None, None, 0, 0, None, 0, None, 0, None) == -1
