@@ -250,9 +250,11 @@ size_t hq_gemv_workspace_bytes(hq_plan_t plan);
  *   x          device, plan.cols values, HQ_BF16 or HQ_FP32, 16-byte aligned.
  *   y          device, rows values, HQ_FP32 or HQ_BF16 (round to nearest even).
  *   workspace  device, 16-byte aligned, >= hq_gemv_workspace_bytes(plan).
- * The sums run in fp32 in a fixed order (per lane along the row, a butterfly
- * over each wave, then the four waves of the row's workgroup), so they differ
- * from a decode-then-multiply by rounding only and repeat bit for bit.
+ * The sums run in fp32 in a fixed order (per lane along the row, then a
+ * butterfly over the wave; below 8192 rows a row's four waves split its
+ * sub-streams and meet in wave order), so they differ from a
+ * decode-then-multiply by rounding only and repeat bit for bit for a given
+ * row count.
  * Plans with a rotation or a dither (KV streams): HQ_ERR_UNSUPPORTED.  A
  * corrupt sub-stream contributes zero and is reported in s->stats. */
 hq_status hq_decode_gemv(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows,

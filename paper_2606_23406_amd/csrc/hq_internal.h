@@ -133,6 +133,7 @@ struct hq_attn_args {
 };
 
 #define HQ_ATTN_WINDOW_MAX 256  // residual window tokens a call may keep exact
+#define HQ_GEMV_WAVE_ROWS 8192  // fused GEMV: one wave per row from this many rows
 
 // Several matrices in one launch (kernel arguments, by value): member i owns
 // workgroups wg_begin[i] .. wg_begin[i + 1] - 1 (the last one to the grid end).

@@ -720,14 +720,19 @@ __device__ __forceinline__ void e8_nearest(const float* w, int32_t* h, int32_t& 
   // spacing is 1, so it rounds w to the nearest integer, ties to even (the
   // shift is even); the integer is the sum's bit pattern less the shift's.
   // Four fast-rate adds instead of a rounding and a conversion.
+  // ea = w + (shift - t) = w - rint(w), exact; written as a sum so that it is
+  // never -0 (w = -0, which the signed scale makes of an exact zero, gives
+  // -0 + +0 = +0, where w - rint(w) would give -0): the parity below reads
+  // the sign bits of ea, the rounding the sign of its value, and the two
+  // must agree.
   constexpr float kShift = 12582912.0f;  // 1.5 * 2^23, bits 0x4B400000
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     const float t = w[i] + kShift;
-    const float k = t - kShift;
-    ea[i] = w[i] - k;
+    const float nk = kShift - t;
+    ea[i] = w[i] + nk;
     K[i] = (int32_t)(__float_as_uint(t) - 0x4B400000u);
-    eb[i] = __float_as_uint(ea[i]);  // ea is never -0: w - rint(w) = +0 when equal
+    eb[i] = __float_as_uint(ea[i]);
   }
   float Sabs = __builtin_fabsf(ea[0]) + __builtin_fabsf(ea[1]);
 #pragma unroll
@@ -1837,6 +1842,76 @@ __global__ __launch_bounds__(256) void hq_decode_gemv_kernel(hq_decode_args A, c
   }
 }
 
+// The same product with one wave per row (rows >= HQ_GEMV_WAVE_ROWS): the
+// wave walks all of its row's sub-streams, each one's table entry and first
+// payload words a step ahead, and a butterfly over the wave ends the sum; no
+// barrier after the table copy.
+template <int LAT>
+__global__ __launch_bounds__(256) void hq_decode_gemv_rows_kernel(hq_decode_args A, const float* xt,
+                                                                  void* y, int y_bf16, int64_t rows) {
+  extern __shared__ uint32_t smem[];
+  __shared__ uint32_t s_sel[256];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint32_t wave = readfirst((uint32_t)(tid >> 6));
+  s_sel[tid] = kByteSelect.e[tid];  // 256 threads, one entry each
+  __syncthreads();
+  const int64_t row = (int64_t)blockIdx.x * HQ_WAVES_PER_WG + wave;  // within the call's rows
+  if (row >= rows) return;  // whole waves; no barrier follows
+  uint32_t* buf = smem + wave * (A.lds_words + 66);
+  uint32_t* starts = buf + A.lds_words + 2;
+  const uint32_t spr = (uint32_t)A.spr;
+  const uint32_t sub0 = (uint32_t)A.first_sub + (uint32_t)row * spr;
+  const bool fp16_norm = A.norm_fp16;
+  auto head_of = [&](uint32_t j) {
+    const uint32_t start = readfirst(A.offsets[sub0 + j]), end = readfirst(A.offsets[sub0 + j + 1]);
+    return dec_head<LAT>(A, true, start, end, readfirst(A.kparam[sub0 + j]), lane);
+  };
+  const int64_t t0 = (A.first_row + row) * A.tpr + (lane >> 4);
+  float acc = 0.0f;
+  DecHead head = head_of(0);
+  float rs = fp16_norm ? (float)((const _Float16*)A.norms)[t0] : ((const float*)A.norms)[t0];
+  bool bad = false;
+  for (uint32_t j = 0; j < spr; ++j) {
+    DecHead next;
+    float rs_next = 0.0f;
+    if (j + 1 < spr) {
+      next = head_of(j + 1);
+      const int64_t t = t0 + 4 * (int64_t)(j + 1);
+      rs_next = fp16_norm ? (float)((const _Float16*)A.norms)[t] : ((const float*)A.norms)[t];
+    }
+    uint32_t sym[8];
+    bad |= !decode_symbols<LAT>(A, head, lane, buf, starts, s_sel, sym);
+    int32_t c[8];
+    unstrip8<LAT>(sym, c);
+    const int64_t col = (int64_t)j * HQ_SUB + 8 * lane;
+    const float4 xa = *(const float4*)(xt + col);
+    const float4 xb = *(const float4*)(xt + col + 4);
+    const float xv[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+    float d = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) d = __builtin_fmaf(code_coord<LAT>(c[i], i), xv[i], d);
+    acc = __builtin_fmaf(rs, d, acc);  // the common 1 / (alpha n) once per row
+    head = next;
+    rs = rs_next;
+  }
+  if (bad && A.stats) {
+    const unsigned long long anyb = __ballot(bad);
+    if ((unsigned)lane == (unsigned)__builtin_ctzll(anyb)) {
+      atomicAdd(&A.stats->corrupt_substreams, 1u);
+      atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+    }
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m, 64);
+  if (lane == 0) {
+    const float v = acc / A.alpha_n;
+    if (y_bf16)
+      ((uint16_t*)y)[row] = (uint16_t)f32_to_bf16(v);
+    else
+      ((float*)y)[row] = v;
+  }
+}
+
 // ------------------------------------------------------------ fused decode + attention
 // One query token per sequence attending over its coded KV cache (the KV
 // path of Sec. 5.2, read back as in Sec. 5.3, for the one-token decoding of
@@ -2653,9 +2728,27 @@ int hq_launch_decode_gemv(const hq_plan_s* p, const hq_decode_args& a, const voi
   const int64_t K = p->cols;
   hipLaunchKernelGGL(hq_gemv_prep_kernel, dim3((uint32_t)((K + 4 * HQ_SUB - 1) / (4 * HQ_SUB))),
                      dim3(256), 0, st, x, xt == HQ_BF16 ? 1 : 0, K, a.dmask, xtr);
-  const uint32_t nwg = (uint32_t)(a.nsub / a.spr);  // one workgroup per row
+  const int64_t rows = a.nsub / a.spr;
   const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
   const int yb = yt == HQ_BF16 ? 1 : 0;
+  if (rows >= HQ_GEMV_WAVE_ROWS) {  // enough rows to fill the chip one wave each
+    const uint32_t nwr = (uint32_t)((rows + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG);
+    switch (p->lattice) {
+      case HQ_E8:
+        hipLaunchKernelGGL(hq_decode_gemv_rows_kernel<kE8>, dim3(nwr), dim3(256), lds, st, a, xtr, y, yb, rows);
+        break;
+      case HQ_D4:
+        hipLaunchKernelGGL(hq_decode_gemv_rows_kernel<kD4>, dim3(nwr), dim3(256), lds, st, a, xtr, y, yb, rows);
+        break;
+      case HQ_A2:
+        hipLaunchKernelGGL(hq_decode_gemv_rows_kernel<kA2>, dim3(nwr), dim3(256), lds, st, a, xtr, y, yb, rows);
+        break;
+      default:
+        hipLaunchKernelGGL(hq_decode_gemv_rows_kernel<kZ>, dim3(nwr), dim3(256), lds, st, a, xtr, y, yb, rows);
+    }
+    return (int)hipGetLastError();
+  }
+  const uint32_t nwg = (uint32_t)rows;  // one workgroup per row
   switch (p->lattice) {
     case HQ_E8:
       hipLaunchKernelGGL(hq_decode_gemv_kernel<kE8>, dim3(nwg), dim3(256), lds, st, a, xtr, y, yb);

@@ -118,6 +118,29 @@ def test_kv_rotation_dither_fp16_append(hq, lat):
     check_roundtrip(hq, P, snr, x, f"kv {LAT_NAMES[lat]}", append_chunks=16)
 
 
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2, O.Z])
+def test_exact_zeros_after_the_rht(hq, lat):
+    """Tiles whose RHT output is exactly a sparse integer vector v (x = D H v /
+    128, exact in bf16): most coordinates of z are exact zeros, which the
+    GPU's sign-twisted transform and signed scale turn into -0 on half of the
+    lanes.  Codes and streams must still be the oracle's (regression test for
+    an E8 parity read from the sign bit of a -0 rounding error)."""
+    rng = np.random.default_rng(500 + lat)
+    rows, cols, n = 48, 1024, 128
+    v = np.zeros((rows, cols))
+    for r in range(rows):
+        for t in range(cols // n):
+            k = rng.integers(1, 4)
+            idx = rng.choice(n, k, replace=False)
+            v[r, t * n + idx] = rng.integers(-3, 4, k)
+    x = O.fwht(v.reshape(-1, n)).reshape(rows, cols) / n * O.signs(19, cols)
+    xt = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16)
+    assert np.array_equal(xt.float().numpy(), x.astype(np.float32))  # exact in bf16
+    snr = 20.0
+    P = PT.oracle_params(lat, snr, rht_seed=19)
+    check_roundtrip(hq, P, snr, xt, f"exact zeros after the RHT {LAT_NAMES[lat]}")
+
+
 def test_zero_tiles_and_tiny_norms(hq):
     snr = PT.op_snr("E8", 4.0)
     P = PT.oracle_params(O.E8, snr, rht_seed=2)
@@ -310,6 +333,34 @@ def test_decode_gemv_matches_oracle(hq, lat):
             yb = hq.hq_decode_gemv(plan, s, x.cuda(), row0=row0, rows=n, out_dtype=torch.bfloat16)
             assert torch.equal(yb.cpu(), torch.from_numpy(y).to(torch.bfloat16))
     print(f"[parity] decode_gemv {LAT_NAMES[lat]}: worst error {worst:.2e} of sum |w x|", flush=True)
+    assert s.read_stats()["corrupt_substreams"] == 0
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2, O.Z])
+def test_decode_gemv_wave_per_row(hq, lat):
+    """From 8192 rows a call runs one wave per row: 8195 rows (a ragged last
+    workgroup) and windows at and just below the switch, each against the
+    oracle at the same bar as the workgroup-per-row shape."""
+    snr = 20.0
+    rows, cols = 8195, 512
+    P = PT.oracle_params(lat, snr, rht_seed=77)
+    w = gauss(rows, cols, 78, 0.02, torch.bfloat16)
+    plan, s = encode_gpu(hq, P, snr, w)
+    res = PT.compare_streams(P, w.float().numpy(), PT.gpu_stream_arrays(s, rows))
+    gc = res["codes"] if res["gpu_codes"] is None else res["gpu_codes"]
+    wd = O.backend(P, gc, res["norms"]).astype(np.float64)
+    x = gauss(1, cols, 79, 1.0, torch.bfloat16)[0]
+    xs = x.float().numpy().astype(np.float64)
+    worst = 0.0
+    for row0, n in ((0, rows), (3, 8192), (2, 8191)):
+        print(f"[parity] decode_gemv one wave per row {LAT_NAMES[lat]} rows {row0}+{n}", flush=True)
+        ref = O.decode_gemv(P, gc[row0:row0 + n], res["norms"][row0:row0 + n], xs, row0=row0)
+        scale = np.abs(wd[row0:row0 + n]) @ np.abs(xs)
+        y = hq.hq_decode_gemv(plan, s, x.cuda(), row0=row0, rows=n).cpu().numpy()
+        err = np.abs(y.astype(np.float64) - ref) / scale
+        worst = max(worst, float(err.max()))
+        assert np.all(err <= 1e-6), (row0, n, err.max())
+    print(f"[parity] decode_gemv one wave per row {LAT_NAMES[lat]}: worst error {worst:.2e}", flush=True)
     assert s.read_stats()["corrupt_substreams"] == 0
 
 
