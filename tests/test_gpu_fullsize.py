@@ -91,6 +91,55 @@ def test_c2_heavy_tailed_4096(hq, bps):
     check_sampled_rows(hq, plan, s, P, x, rows, f"C2 E8@{bps}")
 
 
+WHOLE = {
+    "C2_E8@4": ("c2", O.E8, 4.0), "C2_E8@3": ("c2", O.E8, 3.0),
+    "C3_l0_gate_E8@4": ("gate", O.E8, 4.0), "C3_l0_down_D4@3": ("down", O.D4, 3.0),
+    "C4_keys_E8@2": ("keys", O.E8, 2.0), "C4_keys_A2@1.7": ("keys", O.A2, 1.7),
+    "C4_keys_Z@1.7": ("keys", O.Z, 1.7),
+}
+
+
+@pytest.mark.parametrize("case", list(WHOLE))
+def test_whole_stream_bit_exact(hq, kv_keys, case):
+    """Every sub-stream of a full-size encode (C2 whole, C3 layer 0's gate and
+    down, C4 keys appended in 128-token blocks with signs + dither + fp16
+    norms) against the oracle's encode of the same input: words, k and norms
+    bit for bit, codes different only in blocks within 1e-6 of a Voronoi
+    boundary (counted; at most 1 in 10^5)."""
+    from paper_2606_23406_amd import workloads as W
+    what, lat, bps = WHOLE[case]
+    lname = {O.E8: "E8", O.D4: "D4", O.A2: "A2", O.Z: "Z"}[lat]
+    snr = PT.op_snr(lname, bps)
+    kv = what == "keys"
+    if what == "c2":
+        x, seed = W.heavy_tailed_weight(), 17
+    elif what == "keys":
+        x, seed = kv_keys, 71
+    else:
+        idx = 4 if what == "gate" else 6
+        x, seed = W.llama_linear(0, idx, device="cuda").cpu(), W.llama_linear_seed(0, idx)
+    rows, cols = x.shape
+    print(f"[fullsize] whole stream {case}: {rows}x{cols}", flush=True)
+    opts = dict(rotation=1, rot_seed=72, dither=True, dither_seed=73 + lat, norm_fp16=True) if kv else {}
+    P = PT.oracle_params(lat, snr, rht_seed=seed, **opts)
+    plan = PT.gpu_plan(hq, P, snr, cols)
+    s = hq.EncodedStream(plan, rows)
+    xd = x.cuda()
+    step = 128 if kv else rows
+    for r0 in range(0, rows, step):
+        hq.hq_encode(plan, xd[r0:r0 + step], s, append=r0 > 0)
+    torch.cuda.synchronize()
+    del xd
+    st = s.read_stats()
+    assert st["status"] == 0, st
+    res = PT.compare_streams(P, x.float().numpy(), PT.gpu_stream_arrays(s, rows))
+    blocks = x.numel() // O.DIM[lat]
+    print(f"[fullsize] whole stream {case}: {res['substreams']} sub-streams, {blocks} blocks, "
+          f"exempt blocks {res['exempt_blocks']} (sub-streams {res['exempt_substreams']})", flush=True)
+    assert res["exempt_blocks"] <= max(2, blocks // 100000)
+    assert st["payload_bits"] == res["payload_bits"] or res["exempt_substreams"] > 0
+
+
 @pytest.mark.parametrize("layer", [0, 15, 31])
 @pytest.mark.parametrize("lat,bps", [(O.E8, 4.0), (O.D4, 3.0)])
 def test_c3_llama_linears(hq, layer, lat, bps):
