@@ -105,7 +105,8 @@ def test_whole_stream_bit_exact(hq, kv_keys, case):
     down, C4 keys appended in 128-token blocks with signs + dither + fp16
     norms) against the oracle's encode of the same input: words, k and norms
     bit for bit, codes different only in blocks within 1e-6 of a Voronoi
-    boundary (counted; at most 1 in 10^5)."""
+    boundary (counted; at most 1 in 10^5); then every decoded tile against
+    the oracle's reconstruction."""
     from paper_2606_23406_amd import workloads as W
     what, lat, bps = WHOLE[case]
     lname = {O.E8: "E8", O.D4: "D4", O.A2: "A2", O.Z: "Z"}[lat]
@@ -138,6 +139,17 @@ def test_whole_stream_bit_exact(hq, kv_keys, case):
           f"exempt blocks {res['exempt_blocks']} (sub-streams {res['exempt_substreams']})", flush=True)
     assert res["exempt_blocks"] <= max(2, blocks // 100000)
     assert st["payload_bits"] == res["payload_bits"] or res["exempt_substreams"] > 0
+    # and the whole decode: every tile within 1e-5 of its lattice unit of the
+    # oracle's fp32 reconstruction from the stream's own codes
+    codes = res["codes"] if res["gpu_codes"] is None else res["gpu_codes"]
+    y = hq.hq_decode(plan, s, out_dtype=torch.float32).cpu().numpy()
+    ref = O.backend(P, codes, res["norms"])
+    unit = PT.lattice_unit(P, res["norms"]).reshape(-1)
+    err = np.abs(y.astype(np.float64) - ref).reshape(-1, 128).max(axis=1)
+    exact = float(np.mean(y == ref))
+    print(f"[fullsize] whole stream {case}: decode max error {float((err / unit).max()):.2e} of the "
+          f"lattice unit, bit-exact fraction {exact:.6f}", flush=True)
+    assert np.all(err <= 1e-5 * unit)
 
 
 @pytest.mark.parametrize("layer", [0, 15, 31])
