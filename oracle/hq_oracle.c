@@ -59,10 +59,12 @@ typedef struct {
   float alpha;         /* scale realizing the SNR (App. B eq. alpha-calib) */
   int32_t norm_fp16;   /* store per-tile norms as fp16 (Sec. 6.6 KV) */
   uint64_t rht_seed;   /* sign diagonal D of eq. rht */
-  int32_t rotation;    /* 0 = none, 1 = signs (Sec. 4.2) */
+  int32_t rotation;    /* 0 = none, 1 = signs, 2 = qjl (Sec. 4.2) */
   int32_t dither;      /* subtractive dither on/off (Sec. 4.4) */
   uint64_t rot_seed;
   uint64_t dither_seed;
+  const float* qjl;    /* rotation 2: the n x n orthogonal S, row-major (the
+                          Haar draw of Sec. 4.2, supplied by the caller) */
 } hqo_params;
 
 /* ------------------------------------------------------------------------ */
@@ -748,10 +750,26 @@ void hqo_dither_block(int lat, uint64_t seed, int64_t row, int64_t col0, float* 
 static int check_params(const hqo_params* P, int64_t cols) {
   int n = P->tile, m = hqo_lattice_dim(P->lattice);
   if (m == 0 || n < m || (n & (n - 1)) != 0) return HQO_ERR_ARG;
+  if (P->rotation < 0 || P->rotation > 2 || (P->rotation == 2 && !P->qjl)) return HQO_ERR_ARG;
   if (cols % n != 0) return HQO_ERR_ARG;
   if (P->substream <= 0 || P->substream % n != 0 || cols % P->substream != 0) return HQO_ERR_ARG;
   if (P->rice_k > HQO_KMAX) return HQO_ERR_ARG;
   return HQO_OK;
+}
+
+/* The qjl rotation (Sec. 4.2): y = S v (transpose 0, encode) or S^T v
+   (transpose 1, decode) for the n x n row-major S; each output is the
+   left-to-right fp32 sum of the rounded products, starting from the first. */
+static void qjl_apply(const float* S, int transpose, const float* v, float* y, int n) {
+  for (int i = 0; i < n; ++i) {
+    float acc = (transpose ? S[i] : S[(int64_t)i * n]) * v[0];
+    for (int k = 1; k < n; ++k) {
+      const float sk = transpose ? S[(int64_t)k * n + i] : S[(int64_t)i * n + k];
+      const float p = sk * v[k];
+      acc = acc + p;
+    }
+    y[i] = acc;
+  }
 }
 
 /* Front end, one tile at a time: norm, RHT, rotate, normalize, dither,
@@ -797,6 +815,10 @@ int hqo_frontend(const hqo_params* P, const float* x, int64_t rows, int64_t cols
         float zi = v[i] * scale;
         if (P->rotation == 1 && hqo_sign(P->rot_seed, i) < 0) zi = -zi;
         v[i] = zi;
+      }
+      if (P->rotation == 2) {
+        qjl_apply(P->qjl, 0, v, sq, n);
+        for (int i = 0; i < n; ++i) v[i] = sq[i];
       }
       /* Add dither (Sec. 4.4) then quantize (Sec. 4.5), block by block. */
       for (int b = 0; b < n / m; ++b) {
@@ -907,8 +929,9 @@ int hqo_backend(const hqo_params* P, const int32_t* codes, const void* norms, in
   int n = P->tile, lat = P->lattice, m = hqo_lattice_dim(lat);
   int64_t tpr = cols / n;
   float* v = (float*)malloc(sizeof(float) * n);
+  float* vq = (float*)malloc(sizeof(float) * n);
   int64_t* vi = (int64_t*)malloc(sizeof(int64_t) * n);
-  int exact = !P->dither && lat != HQO_A2;
+  int exact = !P->dither && lat != HQO_A2 && P->rotation != 2;
   float an = P->alpha * (float)n; /* exact: n is a power of two */
   for (int64_t r = 0; r < rows; ++r) {
     for (int64_t t = 0; t < tpr; ++t) {
@@ -940,6 +963,10 @@ int hqo_backend(const hqo_params* P, const int32_t* codes, const void* norms, in
         if (P->rotation == 1)
           for (int i = 0; i < n; ++i)
             if (hqo_sign(P->rot_seed, i) < 0) v[i] = -v[i];
+        if (P->rotation == 2) {
+          qjl_apply(P->qjl, 1, v, vq, n);
+          for (int i = 0; i < n; ++i) v[i] = vq[i];
+        }
         hqo_fwht_f32(v, n);
         for (int i = 0; i < n; ++i) {
           float w = (hqo_sign(P->rht_seed, t * n + i) < 0) ? -v[i] : v[i];
@@ -949,6 +976,7 @@ int hqo_backend(const hqo_params* P, const int32_t* codes, const void* norms, in
     }
   }
   free(v);
+  free(vq);
   free(vi);
   return HQO_OK;
 }

@@ -35,6 +35,7 @@ class _Params(C.Structure):
         ("dither", C.c_int32),
         ("rot_seed", C.c_uint64),
         ("dither_seed", C.c_uint64),
+        ("qjl", C.c_void_p),
     ]
 
 
@@ -123,11 +124,16 @@ class Params:
     dither: bool = False
     rot_seed: int = 0
     dither_seed: int = 0
+    qjl: object = None  # rotation 2: the tile x tile orthogonal S (Sec. 4.2), float32
 
     def c(self):
+        if self.qjl is not None:
+            self._qjl32 = np.ascontiguousarray(self.qjl, dtype=np.float32)  # kept alive with self
+            assert self._qjl32.shape == (self.tile, self.tile)
+        q = self._qjl32.ctypes.data_as(C.c_void_p) if self.qjl is not None else None
         return _Params(self.tile, self.lattice, self.substream, self.rice_k, np.float32(self.alpha),
                        int(self.norm_fp16), self.rht_seed & (2**64 - 1), self.rotation,
-                       int(self.dither), self.rot_seed & (2**64 - 1), self.dither_seed & (2**64 - 1))
+                       int(self.dither), self.rot_seed & (2**64 - 1), self.dither_seed & (2**64 - 1), q)
 
 
 # ---------------------------------------------------------------- constants
