@@ -50,7 +50,7 @@ typedef enum {
 
 typedef enum { HQ_E8 = 0, HQ_D4 = 1, HQ_A2 = 2, HQ_Z = 3 } hq_lattice;
 typedef enum { HQ_BF16 = 0, HQ_FP32 = 1, HQ_FP16 = 2, HQ_INT8 = 3 } hq_dtype;
-typedef enum { HQ_ROT_NONE = 0, HQ_ROT_SIGNS = 1 } hq_rotation;
+typedef enum { HQ_ROT_NONE = 0, HQ_ROT_SIGNS = 1, HQ_ROT_QJL = 2 } hq_rotation;
 
 /* Options beyond the five knobs of hq_plan; all-zero means the weight-path
    defaults (no rotation, no dither, fp32 norms, 512-symbol sub-streams, SNR
@@ -65,6 +65,12 @@ typedef struct {
   int32_t use_snr;      /* 1 = take snr_db below instead of the table lookup */
   int32_t reserved0;
   double snr_db;        /* quantization SNR in dB (App. B) when use_snr = 1 */
+  const float* qjl;     /* HQ_ROT_QJL: host, tile x tile row-major orthogonal S
+                           (the caller's Haar draw, Sec. 4.2); the plan keeps
+                           its own device copy.  Encode applies S after the
+                           normalization, decode S^T after the undither; each
+                           coordinate is the left-to-right fp32 sum of the
+                           rounded products. */
 } hq_options;
 
 typedef struct hq_plan_s* hq_plan_t;
@@ -179,8 +185,9 @@ hq_status hq_encode(hq_plan_t plan, const void* x, int32_t xt, int64_t rows, int
  *   s       host array of count distinct streams, each with its own scan
  *           scratch.
  * Errors: as hq_encode, plus HQ_ERR_INVALID_ARG for mixed plans or a stream
- * (or scan scratch) given twice.  Members before a failing one may already
- * have been launched. */
+ * (or scan scratch) given twice, and HQ_ERR_UNSUPPORTED for a qjl plan (a KV
+ * rotation: those streams are appended with hq_encode).  Members before a
+ * failing one may already have been launched. */
 hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t xt,
                           const int64_t* rows, const int64_t* ld, hq_stream* const* s,
                           int32_t count, void* stream);
@@ -198,7 +205,8 @@ hq_status hq_decode(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t ro
  * s[i]->rows rows) with plans[i] into y[i] (device, element type yt, row
  * stride ld[i]), with the same results as hq_decode.  Plans as for
  * hq_encode_group.  Errors: as hq_decode, plus HQ_ERR_INVALID_ARG for mixed
- * plans. */
+ * plans and HQ_ERR_UNSUPPORTED for a qjl plan (single calls only, as for
+ * hq_encode_group). */
 hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, void* const* y,
                           int32_t yt, const int64_t* ld, int32_t count, void* stream);
 
@@ -207,7 +215,8 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
  * the per-tile factors g = r / (alpha n) (device fp32, rows x tiles_per_row),
  * so that a decoded weight row is D H c g.  Codes beyond +-127 are clamped
  * and counted.  E8, D4 and Z only (A2 has a sqrt3 axis): HQ_ERR_UNSUPPORTED
- * otherwise; dithered streams are HQ_ERR_UNSUPPORTED too. */
+ * otherwise; dithered or rotated streams are HQ_ERR_UNSUPPORTED too (their
+ * codes are not D H-coordinates of the weights alone). */
 hq_status hq_decode_int8(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows,
                          int8_t* codes, int64_t ldc, float* g, void* stream);
 

@@ -244,7 +244,9 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   if (S <= 0 || S % tile != 0 || cols <= 0 || cols % tile != 0 || cols % S != 0)
     return HQ_ERR_INVALID_ARG;
   if (rice_k < -1 || rice_k > HQ_KMAX) return HQ_ERR_INVALID_ARG;
-  if (o.rotation != HQ_ROT_NONE && o.rotation != HQ_ROT_SIGNS) return HQ_ERR_INVALID_ARG;
+  if (o.rotation != HQ_ROT_NONE && o.rotation != HQ_ROT_SIGNS && o.rotation != HQ_ROT_QJL)
+    return HQ_ERR_INVALID_ARG;
+  if (o.rotation == HQ_ROT_QJL && !o.qjl) return HQ_ERR_INVALID_ARG;
   if (o.norm_dtype != 0 && o.norm_dtype != HQ_FP32 && o.norm_dtype != HQ_FP16)
     return HQ_ERR_INVALID_ARG;
   if (tile != HQ_TILE || S != HQ_SUB) return HQ_ERR_UNSUPPORTED;
@@ -303,9 +305,21 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   p->d_dmask = nullptr;
   p->d_smask = nullptr;
   p->d_dsign16 = nullptr;
+  p->d_qjl = nullptr;
+  p->d_qjlt = nullptr;
   bool ok = hipMalloc((void**)&p->d_dmask, sizeof(uint32_t) * (size_t)nw) == hipSuccess &&
             hipMalloc((void**)&p->d_smask, sizeof(uint32_t) * 4) == hipSuccess &&
             hipMalloc((void**)&p->d_dsign16, sizeof(uint32_t) * (size_t)npairs) == hipSuccess;
+  if (ok && o.rotation == HQ_ROT_QJL) {
+    const size_t nn = (size_t)tile * tile;
+    std::vector<float> st(nn);
+    for (int i = 0; i < tile; ++i)
+      for (int k = 0; k < tile; ++k) st[(size_t)k * tile + i] = o.qjl[(size_t)i * tile + k];
+    ok = hipMalloc((void**)&p->d_qjl, sizeof(float) * nn) == hipSuccess &&
+         hipMalloc((void**)&p->d_qjlt, sizeof(float) * nn) == hipSuccess &&
+         hipMemcpy(p->d_qjl, o.qjl, sizeof(float) * nn, hipMemcpyHostToDevice) == hipSuccess &&
+         hipMemcpy(p->d_qjlt, st.data(), sizeof(float) * nn, hipMemcpyHostToDevice) == hipSuccess;
+  }
   ok = ok &&
        hipMemcpy(p->d_dmask, dm.data(), sizeof(uint32_t) * (size_t)nw, hipMemcpyHostToDevice) ==
            hipSuccess &&
@@ -317,6 +331,8 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
     if (p->d_dmask) hipFree(p->d_dmask);
     if (p->d_smask) hipFree(p->d_smask);
     if (p->d_dsign16) hipFree(p->d_dsign16);
+    if (p->d_qjl) hipFree(p->d_qjl);
+    if (p->d_qjlt) hipFree(p->d_qjlt);
     delete p;
     return HQ_ERR_HIP;
   }
@@ -347,6 +363,8 @@ hq_status hq_plan_destroy(hq_plan_t p) {
   hipFree(p->d_dmask);
   hipFree(p->d_smask);
   hipFree(p->d_dsign16);
+  if (p->d_qjl) hipFree(p->d_qjl);
+  if (p->d_qjlt) hipFree(p->d_qjlt);
   delete p;
   return HQ_OK;
 }
@@ -415,6 +433,7 @@ static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t 
   a.dmask = p->d_dmask;
   a.dsign16 = p->d_dsign16;
   a.smask = p->d_smask;
+  a.qjlt = p->d_qjlt;
   a.stats = s->stats;
   a.epoch = (unsigned long long*)s->scan;
   a.status = (unsigned long long*)((char*)s->scan + HQ_SCAN_STATUS_OFFSET);
@@ -469,6 +488,7 @@ hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t 
   if (count < 0 || (count > 0 && (!plans || !x || !rows || !ld || !s))) return HQ_ERR_INVALID_ARG;
   for (int32_t i = 0; i < count; ++i) {
     if (!plans[i] || !s[i] || !same_kernel_family(plans[0], plans[i])) return HQ_ERR_INVALID_ARG;
+    if (plans[i]->rotation == HQ_ROT_QJL) return HQ_ERR_UNSUPPORTED;  // single calls only
     for (int32_t j = 0; j < i; ++j)
       if (s[j] == s[i] || s[j]->scan == s[i]->scan) return HQ_ERR_INVALID_ARG;
   }
@@ -515,6 +535,8 @@ static void fill_decode_args(const hq_plan_s* p, const hq_stream* s, int64_t row
   a->dmask = p->d_dmask;
   a->dsign16 = p->d_dsign16;
   a->smask = p->d_smask;
+  a->qjl = p->d_qjl;
+  a->qjlt = p->d_qjlt;
   a->stats = s->stats;
   a->rotation = p->rotation;
   a->dither = p->dither;
@@ -656,6 +678,8 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
   if (yt != HQ_BF16 && yt != HQ_FP32) return HQ_ERR_INVALID_ARG;
   for (int32_t i = 0; i < count; ++i)
     if (!plans[i] || !s[i] || !same_kernel_family(plans[0], plans[i])) return HQ_ERR_INVALID_ARG;
+  for (int32_t i = 0; i < count; ++i)
+    if (plans[i]->rotation == HQ_ROT_QJL) return HQ_ERR_UNSUPPORTED;  // single calls only
   const int64_t esz = (yt == HQ_BF16) ? 2 : 4;
   for (int32_t b = 0; b < count; b += HQ_GROUP_MAX) {
     hq_decode_group_args g;
@@ -691,7 +715,7 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
 hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                          int8_t* codes, int64_t ldc, float* g, void* stream) {
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
-  if (p->lattice == HQ_A2 || p->dither) return HQ_ERR_UNSUPPORTED;
+  if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
   if (rows == 0) return HQ_OK;
   if (!codes || !g || ldc < p->cols || ldc % 8 != 0 || ((uintptr_t)codes & 7u) != 0)

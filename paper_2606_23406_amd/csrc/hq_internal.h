@@ -37,6 +37,8 @@ struct hq_plan_s {
   uint32_t* d_dsign16;     // device: per column pair, the RHT signs as bf16 sign
                            // bits (bit 15: even column, bit 31: odd column)
   uint32_t* d_smask;       // device: rotation sign bit per tile coordinate
+  float* d_qjl;            // device: qjl rotation S (128 x 128, row-major), or null
+  float* d_qjlt;           // device: its transpose
   int device;
 };
 
@@ -70,6 +72,7 @@ struct hq_encode_args {
   uint64_t dither_seed;
   float alpha;
   float alpha_half;       // alpha / 2, exact (the E8 decision works on z / 2)
+  const float* qjlt;      // qjl rotation: S^T (row k = column k of S), or null
 };
 
 // Automatic Rice-k thresholds of the two symbol classes (the same for every
@@ -101,6 +104,8 @@ struct hq_decode_args {
   uint64_t dither_seed;
   float alpha;
   float alpha_n;           // alpha * tile, exact
+  const float* qjl;        // qjl rotation: S (row-major) and S^T, or null
+  const float* qjlt;
 };
 
 // One-token attention over coded K and V streams (fused decode + attention).
@@ -134,6 +139,7 @@ struct hq_attn_args {
 
 #define HQ_ATTN_WINDOW_MAX 256  // residual window tokens a call may keep exact
 #define HQ_GEMV_WAVE_ROWS 8192  // fused GEMV: one wave per row from this many rows
+#define HQ_QJL_STAGE 512        // qjl rotation: LDS floats per wave (four tiles)
 
 // Several matrices in one launch (kernel arguments, by value): member i owns
 // workgroups wg_begin[i] .. wg_begin[i + 1] - 1 (the last one to the grid end).

@@ -521,6 +521,49 @@ __device__ __forceinline__ float flip(float v, uint32_t bits, int j) {
   return __uint_as_float(__float_as_uint(v) ^ (((bits >> j) & 1u) << 31));
 }
 
+// Lanes of one wave exchange values through LDS: every lane's earlier LDS
+// writes are visible to the others' later reads.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// v <- M v for the tile of the lane's group of 16 (its coordinates
+// 8 (lane % 16) + j): the qjl rotation of Sec. 4.2 with M = S (encode) or S^T
+// (decode).  Mt is M^T row-major, so row k holds column k of M and a lane's 8
+// outputs read 32 contiguous bytes of it per k.  Each output is the
+// left-to-right fp32 sum of the rounded products from k = 0, the order the
+// oracle defines; v passes through the group's 128 floats of `stage` (LDS).
+__device__ __forceinline__ void qjl_tile(const float* __restrict__ Mt, float* stage, int lane,
+                                         float* v) {
+  float* t = stage + (lane >> 4) * HQ_TILE;
+  const int c0 = (lane & 15) * 8;
+  *(float4*)(t + c0) = make_float4(v[0], v[1], v[2], v[3]);
+  *(float4*)(t + c0 + 4) = make_float4(v[4], v[5], v[6], v[7]);
+  wave_lds_sync();
+  float acc[8];
+  {
+    const float z = t[0];
+    const float4 a = *(const float4*)(Mt + c0), b = *(const float4*)(Mt + c0 + 4);
+    acc[0] = a.x * z; acc[1] = a.y * z; acc[2] = a.z * z; acc[3] = a.w * z;
+    acc[4] = b.x * z; acc[5] = b.y * z; acc[6] = b.z * z; acc[7] = b.w * z;
+  }
+#pragma unroll 4
+  for (int k = 1; k < HQ_TILE; ++k) {
+    const float z = t[k];
+    const float4 a = *(const float4*)(Mt + k * HQ_TILE + c0);
+    const float4 b = *(const float4*)(Mt + k * HQ_TILE + c0 + 4);
+    acc[0] = acc[0] + a.x * z; acc[1] = acc[1] + a.y * z;
+    acc[2] = acc[2] + a.z * z; acc[3] = acc[3] + a.w * z;
+    acc[4] = acc[4] + b.x * z; acc[5] = acc[5] + b.y * z;
+    acc[6] = acc[6] + b.z * z; acc[7] = acc[7] + b.w * z;
+  }
+  wave_lds_sync();  // every lane has read the stage before it is written again
+#pragma unroll
+  for (int i = 0; i < 8; ++i) v[i] = acc[i];
+}
+
 // ------------------------------------------------------------ look-back scan
 // Decoupled look-back (Merrill & Garland, 2016) over workgroups in index
 // order.  Workgroups are dispatched in increasing index order, and a group
@@ -951,12 +994,13 @@ __device__ __forceinline__ float quad_bcast(float v) {
 template <int LAT, int XT, bool KV>
 __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const hq_rice_thr& T,
                                                  const SubPos& P, int lane, float* x, float scale_tw,
-                                                 uint32_t* buf, uint32_t& W_out, uint32_t& kb_out,
-                                                 uint32_t& bits_out, bool& overflow_out) {
+                                                 uint32_t* buf, float* stage, uint32_t& W_out,
+                                                 uint32_t& kb_out, uint32_t& bits_out,
+                                                 bool& overflow_out) {
   const bool active = P.active;  // wave-uniform
   const uint32_t col = P.col0 + 8u * (uint32_t)lane;  // tile lane/16, coordinates 8 (lane % 16) + j
   const int64_t grow = A.first_row + P.lrow;
-  const bool use_rot = KV && A.rotation;
+  const bool use_rot = KV && A.rotation == HQ_ROT_SIGNS;
   const bool use_dither = KV && A.dither;
 
   // ---- z = (sigma H D x) * (sigma alpha / r): the scale carries the sign sigma
@@ -967,6 +1011,7 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = flip(x[i], sbits, i);
   }
+  if (KV && A.rotation == HQ_ROT_QJL) qjl_tile(A.qjlt, stage, lane, x);  // z <- S z
   if (use_dither) {
     float u[8];
     dither8<LAT>(A.dither_seed, grow, col, u);
@@ -1258,7 +1303,9 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     uint32_t W, kb, bits;
     bool ovf;
     encode_substream<LAT, XT, KV>(A, T, pos[i], lane, x[i], xor_sign(ss[i], sg.sigma),
-                                  smem + li * stride, W, kb, bits, ovf);
+                                  smem + li * stride,
+                                  (float*)(smem + NSUB * stride) + wave * HQ_QJL_STAGE, W, kb,
+                                  bits, ovf);
     if (pos[i].active) {
       if (lane == 0) {
         A.kparam[A.first_sub + sub] = (uint8_t)kb;
@@ -1603,7 +1650,8 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   const uint32_t wave = readfirst((uint32_t)(tid >> 6));
   uint32_t* buf = smem + wave * (A.lds_words + 66);
   uint32_t* starts = buf + A.lds_words + 2;
-  const bool use_rot = KV && A.rotation;
+  const bool use_rot = KV && A.rotation == HQ_ROT_SIGNS;
+  const bool use_qjl = KV && A.rotation == HQ_ROT_QJL;
   const bool use_dither = KV && A.dither;
   const bool fp16_norm = KV && A.norm_fp16;
   s_sel[tid] = byte_select_entry((uint32_t)tid);  // 256 threads, one entry each
@@ -1698,6 +1746,9 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
 #pragma unroll
         for (int j = 0; j < 8; ++j) y[j] = flip(y[j], sbits, j);
       }
+      if (use_qjl)  // y <- S^T y, through this wave's stage after the four buffers
+        qjl_tile(A.qjl, (float*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66)) + wave * HQ_QJL_STAGE,
+                 lane, y);
       fwht128_tw(y, sg);
       const float g_tw = xor_sign(g, sg.sigma);
 #pragma unroll
@@ -1976,6 +2027,7 @@ __device__ __forceinline__ void load8(const void* p, int64_t i, bool bf16, float
 // qt = (S H D q) * scale * log2(e) per query head, with the key plan's signs
 // (D of the head's own columns); one lane group of 16 per head.
 __global__ __launch_bounds__(256) void hq_attn_prep_kernel(hq_attn_args A) {
+  __shared__ float s_stage[HQ_WAVES_PER_WG * HQ_QJL_STAGE];  // qjl keys only
   const int tid = threadIdx.x, lane = tid & 63;
   const int64_t pair = ((int64_t)blockIdx.x * HQ_WAVES_PER_WG + (tid >> 6)) * 4 + (lane >> 4);
   if (pair >= A.batch * A.heads_q) return;  // whole lane groups
@@ -1988,7 +2040,8 @@ __global__ __launch_bounds__(256) void hq_attn_prep_kernel(hq_attn_args A) {
   for (int i = 0; i < 8; ++i) v[i] = flip(v[i], dbits, i);
   const XSigns sg(lane);
   fwht128(v, sg);
-  const uint32_t sbits = A.K.rotation ? sign_bits8(A.K.smask, c0) : 0u;
+  if (A.K.rotation == HQ_ROT_QJL) qjl_tile(A.K.qjlt, s_stage + (tid >> 6) * HQ_QJL_STAGE, lane, v);
+  const uint32_t sbits = A.K.rotation == HQ_ROT_SIGNS ? sign_bits8(A.K.smask, c0) : 0u;
 #pragma unroll
   for (int i = 0; i < 8; ++i) v[i] = flip(v[i], sbits, i) * A.qscale;
   float* o = A.qt + pair * HQ_TILE + c0;
@@ -2315,9 +2368,10 @@ __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
     L += s_red[k];
   }
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-  const uint32_t sbits = A.V.rotation ? sign_bits8(A.V.smask, c0) : 0u;
+  const uint32_t sbits = A.V.rotation == HQ_ROT_SIGNS ? sign_bits8(A.V.smask, c0) : 0u;
 #pragma unroll
   for (int i = 0; i < 8; ++i) v[i] = flip(v[i] * inv, sbits, i);
+  if (A.V.rotation == HQ_ROT_QJL) qjl_tile(A.V.qjl, (float*)s_acc, lane, v);  // v <- S^T v
   const XSigns sg(lane);
   fwht128(v, sg);
   const uint32_t dbits = sign_bits8(A.V.dmask, (int64_t)kvh * HQ_TILE + c0);
@@ -2563,12 +2617,15 @@ template <int LAT, int XT, bool KV>
 void launch_encode_kernel(const hq_encode_args& a, const hq_rice_thr& t, uint32_t nwg,
                           uint32_t lds_words, hipStream_t st) {
   const size_t per_sub = (size_t)(lds_words + 2) * sizeof(uint32_t);
+  const size_t lds = per_sub * HQ_ENC_SUBS_PER_WG;
+  // the qjl rotation stages four tiles per wave after the sub-stream buffers
+  const size_t stage = a.qjlt ? (size_t)HQ_QJL_STAGE * sizeof(float) : 0;
   if (a.spw == 1)
     hipLaunchKernelGGL((hq_encode_kernel<LAT, XT, KV, 1>), dim3(nwg), dim3(64 * HQ_ENC_SUBS_PER_WG),
-                       per_sub * HQ_ENC_SUBS_PER_WG, st, a, t);
+                       lds + stage * HQ_ENC_SUBS_PER_WG, st, a, t);
   else
     hipLaunchKernelGGL((hq_encode_kernel<LAT, XT, KV, HQ_ENC_SUBS_PER_WAVE>), dim3(nwg),
-                       dim3(64 * HQ_ENC_WAVES), per_sub * HQ_ENC_SUBS_PER_WG, st, a, t);
+                       dim3(64 * HQ_ENC_WAVES), lds + stage * HQ_ENC_WAVES, st, a, t);
 }
 
 template <int LAT, int XT, bool KV>
@@ -2607,7 +2664,9 @@ void launch_decode_kernel(const Args& a, uint32_t nwg, size_t lds, hipStream_t s
 template <int LAT, typename Args>
 int launch_decode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int mode, bool kv,
                       hipStream_t st) {
-  const size_t lds = (size_t)(lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
+  size_t lds = (size_t)(lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
+  if constexpr (sizeof(Args) == sizeof(hq_decode_args))
+    if (a.qjl) lds += (size_t)HQ_QJL_STAGE * HQ_WAVES_PER_WG * sizeof(float);  // qjl stage
   if (mode == 0) {
     if (kv) launch_decode_kernel<LAT, 0, true>(a, nwg, lds, st);
     else launch_decode_kernel<LAT, 0, false>(a, nwg, lds, st);

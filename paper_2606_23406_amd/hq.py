@@ -8,6 +8,7 @@ missing or fails to load, every call raises.
 import ctypes as C
 import os
 
+import numpy as np
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -16,7 +17,7 @@ LIB_PATH = os.path.join(HERE, "libhq.so")
 HQ_OK = 0
 HQ_E8, HQ_D4, HQ_A2, HQ_Z = 0, 1, 2, 3
 HQ_BF16, HQ_FP32, HQ_FP16, HQ_INT8 = 0, 1, 2, 3
-HQ_ROT_NONE, HQ_ROT_SIGNS = 0, 1
+HQ_ROT_NONE, HQ_ROT_SIGNS, HQ_ROT_QJL = 0, 1, 2
 LATTICES = {"E8": HQ_E8, "D4": HQ_D4, "A2": HQ_A2, "Z": HQ_Z}
 STATUS = {0: "HQ_OK", -1: "HQ_ERR_INVALID_ARG", -2: "HQ_ERR_UNSUPPORTED", -3: "HQ_ERR_CAPACITY",
           -4: "HQ_ERR_OVERFLOW", -5: "HQ_ERR_HIP", -6: "HQ_ERR_CORRUPT",
@@ -32,7 +33,8 @@ class HQError(RuntimeError):
 class Options(C.Structure):
     _fields_ = [("rotation", C.c_int32), ("dither", C.c_int32), ("rot_seed", C.c_uint64),
                 ("dither_seed", C.c_uint64), ("norm_dtype", C.c_int32), ("substream", C.c_int32),
-                ("use_snr", C.c_int32), ("reserved0", C.c_int32), ("snr_db", C.c_double)]
+                ("use_snr", C.c_int32), ("reserved0", C.c_int32), ("snr_db", C.c_double),
+                ("qjl", C.c_void_p)]
 
 
 class PlanInfo(C.Structure):
@@ -153,12 +155,19 @@ class Plan:
 
 
 def hq_plan(tile=128, lattice=HQ_E8, bps=4.0, rht_seed=0, rice_k=-1, cols=4096, *, rotation=0,
-            dither=False, rot_seed=0, dither_seed=0, norm_fp16=False, snr_db=None, substream=0):
-    """hq_plan of include/hq.h; snr_db bypasses the calibration table."""
+            dither=False, rot_seed=0, dither_seed=0, norm_fp16=False, snr_db=None, substream=0,
+            qjl=None):
+    """hq_plan of include/hq.h; snr_db bypasses the calibration table; qjl: the
+    tile x tile orthogonal S of rotation HQ_ROT_QJL (host array, copied)."""
     L = lib()
+    S = None
+    if qjl is not None:
+        S = np.ascontiguousarray(np.asarray(qjl, dtype=np.float32))
+        assert S.shape == (tile, tile)
     o = Options(rotation, int(bool(dither)), rot_seed & (2**64 - 1), dither_seed & (2**64 - 1),
                 HQ_FP16 if norm_fp16 else HQ_FP32, substream, 0 if snr_db is None else 1, 0,
-                0.0 if snr_db is None else float(snr_db))
+                0.0 if snr_db is None else float(snr_db),
+                None if S is None else S.ctypes.data_as(C.c_void_p))
     h = C.c_void_p()
     info = PlanInfo()
     st = L.hq_plan(tile, lattice, C.c_float(bps), rht_seed & (2**64 - 1), rice_k, cols, C.byref(o),
