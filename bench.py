@@ -213,18 +213,21 @@ def _median_ms(fn, reps, flush=None):
 def other_workloads(H, W, dev, reps=20):
     """The other synthetic configurations at 1 GPU: C1 (512x512 fp32), C2
     (4096x4096 bf16 Student-t + outlier columns, E8 at 4 and 3 bps) and C4 (KV
-    keys [16, 8192, 8, 128] bf16 with signs rotation, dither and fp16 norms:
-    64 appends of [16, 128] tokens, then one full dequant), cold (1 GiB
+    keys [16, 8192, 8, 128] bf16 with signs rotation, dither and fp16 norms,
+    and once at E8@2 with the qjl rotation instead of the signs: 64 appends of
+    [16, 128] tokens, then one full dequant), cold (1 GiB
     scratch write between runs).  GB/s are of input bytes (bf16, or fp32 for
     C1); pct_hbm is algorithmic bytes over time against 8 TB/s."""
     import numpy as np
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     out = {}
 
-    def codec(name, x, lattice, bps, kv=False, rows_per_append=None):
+    def codec(name, x, lattice, bps, kv=False, rows_per_append=None, qjl=None):
         print(f"[bench] {name}", file=sys.stderr, flush=True)
         rows, cols = x.shape
         opts = dict(rotation=1, dither=True, rot_seed=72, dither_seed=73, norm_fp16=True) if kv else {}
+        if qjl is not None:
+            opts.update(rotation=H.HQ_ROT_QJL, qjl=qjl)
         plan = H.hq_plan(128, lattice, bps, 17, -1, cols, **opts)
         s = H.EncodedStream(plan, rows)
         y = torch.empty((rows, cols), dtype=torch.bfloat16, device=dev)
@@ -272,6 +275,11 @@ def other_workloads(H, W, dev, reps=20):
     del k
     for name, lat, bps in (("E8@2", H.HQ_E8, 2.0), ("A2@1.7", H.HQ_A2, 1.7), ("Z@1.7", H.HQ_Z, 1.7)):
         codec(f"C4_kv_keys_16x8192x8x128_{name}", xk, lat, bps, kv=True, rows_per_append=16 * 128)
+    # the qjl rotation (a Haar S drawn here: QR of a seeded Gaussian, sign-fixed)
+    g = np.random.default_rng(74).standard_normal((128, 128))
+    q, r = np.linalg.qr(g)
+    codec("C4_kv_keys_16x8192x8x128_E8@2_qjl", xk, H.HQ_E8, 2.0, kv=True, rows_per_append=16 * 128,
+          qjl=(q * np.sign(np.diag(r))).astype(np.float32))
     del xk, flush
     torch.cuda.empty_cache()
     return out

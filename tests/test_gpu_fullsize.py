@@ -96,14 +96,22 @@ WHOLE = {
     "C3_l0_gate_E8@4": ("gate", O.E8, 4.0), "C3_l0_down_D4@3": ("down", O.D4, 3.0),
     "C4_keys_E8@2": ("keys", O.E8, 2.0), "C4_keys_A2@1.7": ("keys", O.A2, 1.7),
     "C4_keys_Z@1.7": ("keys", O.Z, 1.7),
+    "C4_keys_E8@2_qjl": ("keys_qjl", O.E8, 2.0),
 }
+
+
+def haar128(seed):
+    g = np.random.default_rng(seed).standard_normal((128, 128))
+    q, r = np.linalg.qr(g)
+    return (q * np.sign(np.diag(r))).astype(np.float32)
 
 
 @pytest.mark.parametrize("case", list(WHOLE))
 def test_whole_stream_bit_exact(hq, kv_keys, case):
     """Every sub-stream of a full-size encode (C2 whole, C3 layer 0's gate and
     down, C4 keys appended in 128-token blocks with signs + dither + fp16
-    norms) against the oracle's encode of the same input: words, k and norms
+    norms; one case with the qjl rotation instead of the signs) against the
+    oracle's encode of the same input: words, k and norms
     bit for bit, codes different only in blocks within 1e-6 of a Voronoi
     boundary (counted; at most 1 in 10^5); then every decoded tile against
     the oracle's reconstruction."""
@@ -111,10 +119,10 @@ def test_whole_stream_bit_exact(hq, kv_keys, case):
     what, lat, bps = WHOLE[case]
     lname = {O.E8: "E8", O.D4: "D4", O.A2: "A2", O.Z: "Z"}[lat]
     snr = PT.op_snr(lname, bps)
-    kv = what == "keys"
+    kv = what.startswith("keys")
     if what == "c2":
         x, seed = W.heavy_tailed_weight(), 17
-    elif what == "keys":
+    elif kv:
         x, seed = kv_keys, 71
     else:
         idx = 4 if what == "gate" else 6
@@ -122,6 +130,8 @@ def test_whole_stream_bit_exact(hq, kv_keys, case):
     rows, cols = x.shape
     print(f"[fullsize] whole stream {case}: {rows}x{cols}", flush=True)
     opts = dict(rotation=1, rot_seed=72, dither=True, dither_seed=73 + lat, norm_fp16=True) if kv else {}
+    if what == "keys_qjl":
+        opts.update(rotation=2, qjl=haar128(74))
     P = PT.oracle_params(lat, snr, rht_seed=seed, **opts)
     plan = PT.gpu_plan(hq, P, snr, cols)
     s = hq.EncodedStream(plan, rows)
