@@ -495,3 +495,71 @@ def gemm_blockscaled(codes, g, xq, sx, tile):
                                _ptr(np.ascontiguousarray(sx, dtype=np.float32)), M, N, K, tile,
                                _ptr(out))
     return out
+
+
+# ---------------------------------------------------------------- fp8 cast (Sec. 4.8)
+# OCP FP8 E4M3: sign, 4 exponent bits (bias 7), 3 fraction bits; exponent 0
+# is subnormal (m / 8) 2^-6; code 0x7F / 0xFF is NaN and there is no infinity,
+# so the largest finite magnitude is (1 + 6/8) 2^8 = 448.
+
+def _e4m3_magnitudes():
+    """The 127 finite non-negative E4M3 values, in code order 0x00 .. 0x7E."""
+    v = []
+    for code in range(0x7F):
+        e, m = code >> 3, code & 7
+        v.append((m / 8.0) * 2.0 ** -6 if e == 0 else (1.0 + m / 8.0) * 2.0 ** (e - 7))
+    return np.array(v)
+
+
+def e4m3_bits(x):
+    """Round each value to the nearest E4M3 value, ties to the even code (even
+    fraction), magnitudes above 448 saturating to 448, the sign kept (a
+    negative value that rounds to zero gives -0, 0x80); returns the bytes."""
+    x = np.asarray(x, dtype=np.float64)
+    mag = _e4m3_magnitudes()
+    a = np.minimum(np.abs(x), mag[-1])
+    hi = np.clip(np.searchsorted(mag, a), 0, mag.size - 1)  # first value >= a
+    lo = np.maximum(hi - 1, 0)
+    dlo, dhi = a - mag[lo], mag[hi] - a
+    pick_hi = (dhi < dlo) | ((dhi == dlo) & (hi % 2 == 0))
+    code = np.where(pick_hi, hi, lo).astype(np.uint8)
+    return (code | np.where(np.signbit(x), 0x80, 0).astype(np.uint8)).astype(np.uint8)
+
+
+def e4m3_value(bits):
+    bits = np.asarray(bits, dtype=np.uint8)
+    v = _e4m3_magnitudes()[np.minimum(bits & 0x7F, 0x7E)]
+    return np.where(bits & 0x80, -v, v)
+
+
+def weight_codes_fp8(codes):
+    """The fp8 cast of the weight side: E4M3 of each lattice code."""
+    return e4m3_bits(np.asarray(codes, dtype=np.float64))
+
+
+def act_prep_fp8(a, tile, rht_seed):
+    """Activation side in fp8: per K-tile y = H D a (fp32, the weights' signs),
+    then per token x = E4M3(y * (448 / amax)) and s_x = amax / 448, all in
+    fp32 as written."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    M, K = a.shape
+    y = (a * signs(rht_seed, K).astype(np.float32)).reshape(M, K // tile, tile)
+    y = fwht(y.astype(np.float32)).reshape(M, K)
+    amax = np.abs(y).max(axis=1).astype(np.float32)
+    inv = np.where(amax == 0, np.float32(0), np.float32(448.0) / np.where(amax == 0, 1, amax))
+    xq = e4m3_bits((y * inv[:, None].astype(np.float32)).astype(np.float32))
+    return xq, (amax / np.float32(448.0)).astype(np.float32)
+
+
+def gemm_fp8_blockscaled(w8, g, x8, sx, tile):
+    """out[m, n] = s_x[m] sum_t g[n, t] sum_{k in t} x[m, k] w[n, k] over the
+    E4M3 values, in fp64."""
+    w = e4m3_value(w8)
+    x = e4m3_value(x8)
+    N, K = w.shape
+    T = K // tile
+    out = np.zeros((x.shape[0], N))
+    for t in range(T):
+        ks = slice(t * tile, (t + 1) * tile)
+        out += (x[:, ks] @ w[:, ks].T) * np.asarray(g, np.float64)[:, t][None, :]
+    return out * np.asarray(sx, np.float64)[:, None]
