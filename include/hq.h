@@ -236,6 +236,26 @@ hq_status hq_gemm_int8_blockscaled(hq_plan_t plan, const int8_t* xq, const float
                                    const int8_t* codes, const float* g, int64_t N, void* out,
                                    int32_t ot, void* stream);
 
+/* The fp8 cast path (Sec. 4.8 Cast, Sec. 6.3: E4M3 at the matrix-core
+ * boundary; int8 is the path the paper finds better on post-RHT data).  E4M3
+ * is the OCP FP8 format (bias 7, 3 fraction bits, largest magnitude 448);
+ * every cast rounds to nearest even.
+ * hq_decode_fp8 -- as hq_decode_int8, with the codes as E4M3 bytes (exact up
+ *   to |c| = 16, then the nearest E4M3 value; beyond 448 saturated and
+ *   counted in clamps).  Same plans and errors as hq_decode_int8.
+ * hq_act_prep_fp8 -- as hq_act_prep, with x = E4M3(y * 448 / amax) and
+ *   s_x = amax / 448.
+ * hq_gemm_fp8_blockscaled -- as hq_gemm_int8_blockscaled over the E4M3
+ *   values: fp32 tile sums on the fp8 matrix cores (v_mfma_f32_32x32x16_fp8),
+ *   each rescaled by g into fp32 accumulators. */
+hq_status hq_decode_fp8(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows,
+                        uint8_t* codes, int64_t ldc, float* g, void* stream);
+hq_status hq_act_prep_fp8(hq_plan_t plan, const void* a, int64_t M, int64_t lda, uint8_t* xq,
+                          float* sx, void* stream);
+hq_status hq_gemm_fp8_blockscaled(hq_plan_t plan, const uint8_t* xq, const float* sx, int64_t M,
+                                  const uint8_t* codes, const float* g, int64_t N, void* out,
+                                  int32_t ot, void* stream);
+
 /* Workspace bytes for hq_dequant_gemm_int8 with M tokens and N weight rows. */
 size_t hq_gemm_workspace_bytes(hq_plan_t plan, int64_t M, int64_t N);
 

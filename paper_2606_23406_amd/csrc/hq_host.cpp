@@ -728,8 +728,24 @@ hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t 
   return hip_status(hq_launch_decode_int8(p, a, stream));
 }
 
-hq_status hq_act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t* xq, float* sx,
-                      void* stream) {
+hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
+                        uint8_t* codes, int64_t ldc, float* g, void* stream) {
+  if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
+  if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
+  if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
+  if (rows == 0) return HQ_OK;
+  if (!codes || !g || ldc < p->cols || ldc % 8 != 0 || ((uintptr_t)codes & 7u) != 0)
+    return HQ_ERR_INVALID_ARG;
+  hq_decode_args a;
+  fill_decode_args(p, s, row0, rows, &a);
+  a.y = codes;
+  a.ld = ldc;
+  a.g = g;
+  return hip_status(hq_launch_decode_fp8(p, a, stream));
+}
+
+static hq_status act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t* xq,
+                          float* sx, int fp8, void* stream) {
   if (!p || M < 0) return HQ_ERR_INVALID_ARG;
   if (M == 0) return HQ_OK;
   if (!a || !xq || !sx || lda < p->cols || !aligned16(a) || (lda * 2) % 16 != 0 ||
@@ -744,12 +760,23 @@ hq_status hq_act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t
   args.xq = xq;
   args.sx = sx;
   args.dmask = p->d_dmask;
+  args.fp8 = fp8;
   return hip_status(hq_launch_act_prep(args, stream));
 }
 
-hq_status hq_gemm_int8_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx, int64_t M,
-                                   const int8_t* codes, const float* g, int64_t N, void* out,
-                                   int32_t ot, void* stream) {
+hq_status hq_act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t* xq, float* sx,
+                      void* stream) {
+  return act_prep(p, a, M, lda, xq, sx, 0, stream);
+}
+
+hq_status hq_act_prep_fp8(hq_plan_t p, const void* a, int64_t M, int64_t lda, uint8_t* xq,
+                          float* sx, void* stream) {
+  return act_prep(p, a, M, lda, (int8_t*)xq, sx, 1, stream);
+}
+
+static hq_status gemm_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx, int64_t M,
+                                  const int8_t* codes, const float* g, int64_t N, void* out,
+                                  int32_t ot, int fp8, void* stream) {
   if (!p || M < 0 || N < 0) return HQ_ERR_INVALID_ARG;
   if (ot != HQ_BF16 && ot != HQ_FP32) return HQ_ERR_INVALID_ARG;
   if (M == 0 || N == 0) return HQ_OK;
@@ -765,9 +792,23 @@ hq_status hq_gemm_int8_blockscaled(hq_plan_t p, const int8_t* xq, const float* s
   a.N = N;
   a.K = p->cols;
   a.out_bf16 = (ot == HQ_BF16) ? 1 : 0;
+  a.fp8 = fp8;
   const int e = hq_launch_gemm(a, stream);
   if (e == -1) return HQ_ERR_UNSUPPORTED;
   return hip_status(e);
+}
+
+hq_status hq_gemm_int8_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx, int64_t M,
+                                   const int8_t* codes, const float* g, int64_t N, void* out,
+                                   int32_t ot, void* stream) {
+  return gemm_blockscaled(p, xq, sx, M, codes, g, N, out, ot, 0, stream);
+}
+
+hq_status hq_gemm_fp8_blockscaled(hq_plan_t p, const uint8_t* xq, const float* sx, int64_t M,
+                                  const uint8_t* codes, const float* g, int64_t N, void* out,
+                                  int32_t ot, void* stream) {
+  return gemm_blockscaled(p, (const int8_t*)xq, sx, M, (const int8_t*)codes, g, N, out, ot, 1,
+                          stream);
 }
 
 size_t hq_gemm_workspace_bytes(hq_plan_t p, int64_t M, int64_t N) {

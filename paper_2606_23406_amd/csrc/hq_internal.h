@@ -160,9 +160,10 @@ struct hq_actprep_args {
   const void* a;
   int64_t lda;
   int64_t M, K;
-  int8_t* xq;
+  int8_t* xq;             // int8, or E4M3 bytes when fp8
   float* sx;
   const uint32_t* dmask;
+  int32_t fp8;            // 1: E4M3 at 448 / amax instead of int8 at 127 / amax
 };
 
 struct hq_gemm_args {
@@ -173,12 +174,14 @@ struct hq_gemm_args {
   void* out;          // M x N
   int64_t M, N, K;
   int32_t out_bf16;
+  int32_t fp8;        // 1: xq and w are E4M3 bytes (fp32 tile sums on the fp8 matrix cores)
 };
 
 // Kernel launchers (hq_kernels.hip); return a hipError_t as int.
 int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, const hq_rice_thr& t, int xt,
                      void* stream);
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream);
+int hq_launch_decode_fp8(const hq_plan_s* p, const hq_decode_args& a, void* stream);
 // Fused decode + GEMV: xtr (cols fp32) receives H D x per tile, then y (rows)
 // the decoded rows' products with x.
 int hq_launch_decode_attention(const hq_attn_args& a, int lattice, void* stream);

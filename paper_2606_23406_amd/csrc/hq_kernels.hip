@@ -521,6 +521,13 @@ __device__ __forceinline__ float flip(float v, uint32_t bits, int j) {
   return __uint_as_float(__float_as_uint(v) ^ (((bits >> j) & 1u) << 31));
 }
 
+// Four fp32 values as OCP E4M3 bytes (v_cvt_pk_fp8_f32: round to nearest
+// even), the first in the low byte; the caller keeps them within +-448.
+__device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(a, b, 0, false);
+  return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true);
+}
+
 // Lanes of one wave exchange values through LDS: every lane's earlier LDS
 // writes are visible to the others' later reads.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -1729,6 +1736,22 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
       *(uint2*)out = make_uint2(packed[0], packed[1]);
       if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
       if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
+    } else if constexpr (MODE == 3) {
+      // the fp8 cast (Sec. 4.8): E4M3 of each code, round to nearest even,
+      // magnitudes beyond 448 saturated and counted
+      float v[8];
+      uint32_t clamps = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        v[j] = (float)c[j];
+        if (v[j] > 448.0f) { v[j] = 448.0f; ++clamps; }
+        if (v[j] < -448.0f) { v[j] = -448.0f; ++clamps; }
+      }
+      const uint32_t w0 = e4m3x4(v[0], v[1], v[2], v[3]), w1 = e4m3x4(v[4], v[5], v[6], v[7]);
+      uint8_t* out = (uint8_t*)A.y + (int64_t)lrow * A.ld + col;
+      *(uint2*)out = make_uint2(w0, w1);
+      if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
+      if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
     } else {
       // y = D H^T (S) (code - U) * r / (alpha n); the integer codes make the
       // transform exact in fp32 (|sum| <= 128 * 65536 < 2^24) whenever there
@@ -2428,19 +2451,27 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
   if (lane == 0) s_max[wave] = amax;
   __syncthreads();
   amax = __builtin_fmaxf(__builtin_fmaxf(s_max[0], s_max[1]), __builtin_fmaxf(s_max[2], s_max[3]));
-  const float inv = (amax == 0.0f) ? 0.0f : 127.0f / amax;
+  const float top = A.fp8 ? 448.0f : 127.0f;  // E4M3's largest magnitude, or int8's
+  const float inv = (amax == 0.0f) ? 0.0f : top / amax;
   int8_t* xrow = A.xq + row * A.K;
   for (int64_t col = (int64_t)tid * 4; col < A.K; col += 1024) {
     uint32_t packed = 0;
+    if (A.fp8) {
+      float q[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float qv = __builtin_rintf(ybuf[col + i] * inv);
-      qv = __builtin_fminf(__builtin_fmaxf(qv, -127.0f), 127.0f);
-      packed |= ((uint32_t)(int32_t)qv & 0xFFu) << (8 * i);
+      for (int i = 0; i < 4; ++i) q[i] = __builtin_fminf(__builtin_fmaxf(ybuf[col + i] * inv, -448.0f), 448.0f);
+      packed = e4m3x4(q[0], q[1], q[2], q[3]);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float qv = __builtin_rintf(ybuf[col + i] * inv);
+        qv = __builtin_fminf(__builtin_fmaxf(qv, -127.0f), 127.0f);
+        packed |= ((uint32_t)(int32_t)qv & 0xFFu) << (8 * i);
+      }
     }
     *(uint32_t*)(xrow + col) = packed;
   }
-  if (tid == 0) A.sx[row] = amax / 127.0f;
+  if (tid == 0) A.sx[row] = amax / top;
 }
 
 
@@ -2459,6 +2490,7 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
 typedef int v16i_t __attribute__((ext_vector_type(16)));
+typedef float v16f_t __attribute__((ext_vector_type(16)));
 
 constexpr int kGemmM = 256, kGemmN = 128;  // the prefetch below assumes 256 x 128
 constexpr int kGemmThreads = 512;           // 8 waves, 4 (m) x 2 (n)
@@ -2517,9 +2549,47 @@ __device__ __forceinline__ void gemm_load_g(const hq_gemm_args& A, int64_t n0, i
 // One K tile: the wave's 2 x kGemmNB MFMA blocks from LDS, then their exact
 // int32 sums rescaled by the tile's weight factors into the fp32
 // accumulators.
+// FP8: the same bytes as E4M3 on the fp8 matrix cores
+// (v_mfma_f32_32x32x16_fp8_fp8), two per 32-deep step on the low and high
+// eight bytes of each lane's fragment (A and B split alike, so the two
+// products cover the step's 32 k), fp32 tile sums.
+template <bool FP8>
 __device__ __forceinline__ void gemm_step(const int8_t* sa, const int8_t* sb, int wm, int wn,
                                           int lane, const float (&gv)[kGemmNB],
                                           float (&accf)[2][kGemmNB][16]) {
+  if constexpr (FP8) {
+    v16f_t acc[2][kGemmNB];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int koff = ks * 32 + (lane >> 5) * 16;
+      v4i_t fa[2], fb[kGemmNB];
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+        fa[a] = *(const v4i_t*)(sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff);
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b)
+        fb[b] = *(const v4i_t*)(sb + (wn * (kGemmN / 2) + b * 32 + (lane & 31)) * kGemmLd + koff);
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < kGemmNB; ++b) {
+          const long alo = (long)(((unsigned long)(uint32_t)fa[a][1] << 32) | (uint32_t)fa[a][0]);
+          const long ahi = (long)(((unsigned long)(uint32_t)fa[a][3] << 32) | (uint32_t)fa[a][2]);
+          const long blo = (long)(((unsigned long)(uint32_t)fb[b][1] << 32) | (uint32_t)fb[b][0]);
+          const long bhi = (long)(((unsigned long)(uint32_t)fb[b][3] << 32) | (uint32_t)fb[b][2]);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(
+              alo, blo, ks == 0 ? (v16f_t){} : acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(ahi, bhi, acc[a][b], 0, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) accf[a][b][r] = __builtin_fmaf(acc[a][b][r], gv[b], accf[a][b][r]);
+    return;
+  }
   v16i_t acc[2][kGemmNB];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -2547,7 +2617,8 @@ __device__ __forceinline__ void gemm_step(const int8_t* sa, const int8_t* sb, in
         accf[a][b][r] = __builtin_fmaf((float)acc[a][b][r], gv[b], accf[a][b][r]);
 }
 
-__global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_i8_kernel(hq_gemm_args A) {
+template <bool FP8>
+__device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
   extern __shared__ __attribute__((aligned(16))) int8_t gsm[];
   int8_t* const sa = gsm;                    // stage s at sa + s * kGemmStageA
   int8_t* const sb = gsm + 2 * kGemmStageA;  // stage s at sb + s * kGemmStageB
@@ -2576,7 +2647,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_i8_kernel(hq_gemm_arg
     float gv[kGemmNB];
     gemm_load_g(A, n0, wn, lane, T, t, gv);
     const int st = (int)(t & 1);
-    gemm_step(sa + st * kGemmStageA, sb + st * kGemmStageB, wm, wn, lane, gv, accf);
+    gemm_step<FP8>(sa + st * kGemmStageA, sb + st * kGemmStageB, wm, wn, lane, gv, accf);
     if (t + 1 < T) {
       gemm_stash(sa + (st ^ 1) * kGemmStageA, sb + (st ^ 1) * kGemmStageB, tid, pf);
       __syncthreads();
@@ -2602,6 +2673,14 @@ __global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_i8_kernel(hq_gemm_arg
           ((float*)A.out)[m * A.N + n] = v;
       }
     }
+}
+
+__global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_i8_kernel(hq_gemm_args A) {
+  gemm_body<false>(A);
+}
+
+__global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_f8_kernel(hq_gemm_args A) {
+  gemm_body<true>(A);
 }
 
 // ------------------------------------------------------------ utilities
@@ -2763,13 +2842,31 @@ int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
   if (a.K % HQ_TILE != 0) return -1;
   static bool lds_set = false;  // more than 64 KB of dynamic LDS needs an opt-in
   if (!lds_set) {
-    const hipError_t e = hipFuncSetAttribute((const void*)hq_gemm_i8_kernel,
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+    hipError_t e = hipFuncSetAttribute((const void*)hq_gemm_i8_kernel,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void*)hq_gemm_f8_kernel,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
     if (e != hipSuccess) return (int)e;
     lds_set = true;
   }
   const dim3 grid((uint32_t)((a.N + kGemmN - 1) / kGemmN), (uint32_t)((a.M + kGemmM - 1) / kGemmM));
-  hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
+  if (a.fp8)
+    hipLaunchKernelGGL(hq_gemm_f8_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
+  else
+    hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
+
+int hq_launch_decode_fp8(const hq_plan_s* p, const hq_decode_args& a, void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
+  const uint32_t nwg = decode_wgs(a.nsub);
+  switch (p->lattice) {
+    case HQ_E8: launch_decode_kernel<kE8, 3, false>(a, nwg, lds, st); break;
+    case HQ_D4: launch_decode_kernel<kD4, 3, false>(a, nwg, lds, st); break;
+    default: launch_decode_kernel<kZ, 3, false>(a, nwg, lds, st);
+  }
   return (int)hipGetLastError();
 }
 
