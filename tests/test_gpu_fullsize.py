@@ -521,6 +521,19 @@ def test_c5_gemm_fullsize(hq):
     rel = np.max(np.abs(got - ref) / denom)
     print(f"[fullsize] C5 sampled 48x48 outputs: max relative error {rel:.2e}", flush=True)
     assert rel <= 1e-3
+    # the fp8 E4M3 cast path on the same operands, same samples
+    x8, sx8 = hq.hq_act_prep_fp8(plan, a.cuda())
+    c8, g8 = hq.hq_decode_fp8(plan, s)
+    out8 = hq.hq_gemm_fp8_blockscaled(plan, x8, sx8, c8, g8, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ox8, osx8 = O.act_prep_fp8(a[mi].float().numpy(), 128, P.rht_seed)
+    assert np.array_equal(x8.cpu().numpy()[mi], ox8) and np.array_equal(sx8.cpu().numpy()[mi], osx8)
+    assert np.array_equal(c8.cpu().numpy()[ni], O.weight_codes_fp8(codes))
+    ref8 = O.gemm_fp8_blockscaled(O.weight_codes_fp8(codes), g, ox8, osx8, 128)
+    got8 = out8.cpu().numpy()[mi][:, ni].astype(np.float64)
+    rel8 = np.max(np.abs(got8 - ref8) / np.maximum(np.abs(ref8), np.sqrt((ref8 ** 2).mean())))
+    print(f"[fullsize] C5 fp8 sampled 48x48 outputs: max relative error {rel8:.2e}", flush=True)
+    assert rel8 <= 1e-4
 
 
 def test_corrupt_streams_are_reported(hq):
