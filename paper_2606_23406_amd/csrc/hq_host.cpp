@@ -285,7 +285,9 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   kstar_thresholds(n0, p->thr[0]);
   if (n1) kstar_thresholds(n1, p->thr[1]); else kstar_thresholds(1, p->thr[1]);
   p->max_words_sub = substream_word_bound(*p);
-  if (p->max_words_sub > 8192) {
+  // qjl decodes also hold S (64 KB) and 2 KB of stage per wave in LDS, next to
+  // the four sub-stream buffers; keep the workgroup within 160 KB
+  if (p->max_words_sub > 8192 || (o.rotation == HQ_ROT_QJL && p->max_words_sub > 4096)) {
     delete p;
     return HQ_ERR_UNSUPPORTED;
   }

@@ -1018,7 +1018,9 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = flip(x[i], sbits, i);
   }
-  if (KV && A.rotation == HQ_ROT_QJL) qjl_tile(A.qjlt, stage, lane, x);  // z <- S z
+  // z <- S z, S^T read from global memory (a workgroup copy in LDS measured
+  // 3x slower on the one-sub-stream-per-wave appends)
+  if (KV && A.rotation == HQ_ROT_QJL) qjl_tile(A.qjlt, stage, lane, x);
   if (use_dither) {
     float u[8];
     dither8<LAT>(A.dither_seed, grow, col, u);
@@ -1661,6 +1663,13 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   const bool use_qjl = KV && A.rotation == HQ_ROT_QJL;
   const bool use_dither = KV && A.dither;
   const bool fp16_norm = KV && A.norm_fp16;
+  // qjl: this wave's stage after the four buffers, then the workgroup's copy of S
+  float* const qstage = (float*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66)) + wave * HQ_QJL_STAGE;
+  float* const qmat = (float*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66)) +
+                      HQ_WAVES_PER_WG * HQ_QJL_STAGE;
+  if (use_qjl)
+    for (int i = tid; i < HQ_TILE * HQ_TILE / 4; i += 256)
+      ((float4*)qmat)[i] = ((const float4*)A.qjl)[i];
   s_sel[tid] = byte_select_entry((uint32_t)tid);  // 256 threads, one entry each
   __syncthreads();
 
@@ -1769,9 +1778,7 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
 #pragma unroll
         for (int j = 0; j < 8; ++j) y[j] = flip(y[j], sbits, j);
       }
-      if (use_qjl)  // y <- S^T y, through this wave's stage after the four buffers
-        qjl_tile(A.qjl, (float*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66)) + wave * HQ_QJL_STAGE,
-                 lane, y);
+      if (use_qjl) qjl_tile(qmat, qstage, lane, y);  // y <- S^T y
       fwht128_tw(y, sg);
       const float g_tw = xor_sign(g, sg.sigma);
 #pragma unroll
@@ -2690,6 +2697,15 @@ __global__ void hq_zero_kernel(uint32_t* p, size_t n) {
   if (i < n) p[i] = 0u;
 }
 
+// Dynamic LDS above 64 KB needs a per-kernel opt-in, a costly runtime call:
+// made when a launch needs more than the kernel's largest opt-in so far.
+inline void allow_lds(const void* kernel, size_t bytes, size_t& granted) {
+  if (bytes > 65536 && bytes > granted &&
+      hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) ==
+          hipSuccess)
+    granted = bytes;
+}
+
 // One encode launch: a single matrix (hq_encode_args + thresholds; four or
 // one sub-streams per wave) or a group (four per wave).
 template <int LAT, int XT, bool KV>
@@ -2734,6 +2750,10 @@ int launch_encode_lat(const Args& a, const hq_rice_thr& t, uint32_t nwg, uint32_
 // One decode launch: a single matrix (hq_decode_args) or a group.
 template <int LAT, int MODE, bool KV, typename Args>
 void launch_decode_kernel(const Args& a, uint32_t nwg, size_t lds, hipStream_t st) {
+  static size_t granted = 0;
+  allow_lds(sizeof(Args) == sizeof(hq_decode_args) ? (const void*)hq_decode_kernel<LAT, MODE, KV>
+                                                   : (const void*)hq_decode_group_kernel<LAT, MODE, KV>,
+            lds, granted);
   if constexpr (sizeof(Args) == sizeof(hq_decode_args))
     hipLaunchKernelGGL((hq_decode_kernel<LAT, MODE, KV>), dim3(nwg), dim3(256), lds, st, a);
   else
@@ -2745,7 +2765,8 @@ int launch_decode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int mode,
                       hipStream_t st) {
   size_t lds = (size_t)(lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
   if constexpr (sizeof(Args) == sizeof(hq_decode_args))
-    if (a.qjl) lds += (size_t)HQ_QJL_STAGE * HQ_WAVES_PER_WG * sizeof(float);  // qjl stage
+    if (a.qjl)  // qjl: the waves' stages, then a copy of S (over 64 KB in all: opt in)
+      lds += ((size_t)HQ_QJL_STAGE * HQ_WAVES_PER_WG + (size_t)HQ_TILE * HQ_TILE) * sizeof(float);
   if (mode == 0) {
     if (kv) launch_decode_kernel<LAT, 0, true>(a, nwg, lds, st);
     else launch_decode_kernel<LAT, 0, false>(a, nwg, lds, st);
