@@ -179,7 +179,10 @@ def hq_plan(tile=128, lattice=HQ_E8, bps=4.0, rht_seed=0, rice_k=-1, cols=4096, 
     st = L.hq_plan(tile, lattice, C.c_float(bps), rht_seed & (2**64 - 1), rice_k, cols, C.byref(o),
                    C.byref(h), C.byref(info))
     _check("hq_plan", st)
-    return Plan(h, info, o)
+    o.qjl = None  # the plan holds its own device copy of S
+    plan = Plan(h, info, o)
+    plan.qjl = S
+    return plan
 
 
 class EncodedStream:
