@@ -59,7 +59,12 @@ typedef struct {
   int32_t rotation;     /* hq_rotation: the KV pre-rotation of Sec. 4.2 */
   int32_t dither;       /* 1 = subtractive dither (Sec. 4.4), KV only */
   uint64_t rot_seed;    /* seed of the +-1 rotation diagonal S */
-  uint64_t dither_seed; /* key of the dither generator; change per forward call */
+  uint64_t dither_seed; /* key of the dither generator, fixed for the life of a
+                           stream: decode regenerates U from this seed and the
+                           global row index, so a stream's rows must all be
+                           written and read with one seed.  The fresh draw per
+                           forward call (Sec. 4.4, App. A) comes from the row
+                           index, which keeps counting across appends. */
   int32_t norm_dtype;   /* HQ_FP32 (default) or HQ_FP16 (KV, Sec. 6.6) */
   int32_t substream;    /* symbols per sub-stream S (Sec. 5.3); 0 = 512 */
   int32_t use_snr;      /* 1 = take snr_db below instead of the table lookup */
@@ -167,7 +172,9 @@ size_t hq_scan_bytes(hq_plan_t plan, int64_t rows);
  *           1: the rows continue the stream after s->rows (KV
  *           quantize-on-append, Sec. 5.2); their dither keys use the global
  *           row index, and the payload continues at offsets[first sub-stream]
- *           as written by the previous encode on the same stream.
+ *           as written by the previous encode on the same stream.  An append
+ *           to an empty stream (s->rows = 0) starts at word 0 and writes
+ *           offsets[0] = 0 itself, like append = 0.
  * Errors (synchronous): HQ_ERR_INVALID_ARG, HQ_ERR_CAPACITY (rows_capacity),
  * HQ_ERR_HIP.  Device-side: payload capacity and fp16 overflow in s->stats. */
 hq_status hq_encode(hq_plan_t plan, const void* x, int32_t xt, int64_t rows, int64_t ld,
@@ -199,6 +206,8 @@ hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t 
  * bounds).  Errors: HQ_ERR_INVALID_ARG, HQ_ERR_HIP. */
 hq_status hq_decode(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows, void* y,
                     int32_t yt, int64_t ld, void* stream);
+/* (A corrupt sub-stream's 512 outputs are all +-0, dithered streams too: the
+   whole sub-stream is dropped, not just the symbols that failed to parse.) */
 
 /* hq_decode_group -- hq_decode of all rows of `count` streams in as few
  * launches as possible (up to 16 per launch): member i decodes s[i] (all
@@ -231,7 +240,9 @@ hq_status hq_act_prep(hq_plan_t plan, const void* a, int64_t M, int64_t lda, int
 /* hq_gemm_int8_blockscaled -- out[i, r] = s_x[i] * sum_t g[r, t] *
  * sum_{j in tile t} c[r, j] * x_q[i, j] with exact int32 tile sums on the
  * int8 matrix cores and fp32 accumulation (N = weight rows, K = plan.cols).
- * out: device M x N, HQ_BF16 or HQ_FP32. */
+ * Every operand is contiguous: xq is M x K and codes N x K with row stride
+ * K = plan.cols (decode the codes with ldc = plan.cols), g is N x K/tile and
+ * out is M x N, HQ_BF16 or HQ_FP32.  The same holds for the fp8 variant. */
 hq_status hq_gemm_int8_blockscaled(hq_plan_t plan, const int8_t* xq, const float* sx, int64_t M,
                                    const int8_t* codes, const float* g, int64_t N, void* out,
                                    int32_t ot, void* stream);

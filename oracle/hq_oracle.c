@@ -793,6 +793,12 @@ int hqo_frontend(const hqo_params* P, const float* x, int64_t rows, int64_t cols
          unnormalized FWHT scales by sqrt(n). */
       for (int i = 0; i < n; ++i) sq[i] = xt[i] * xt[i];
       float nrm = sqrtf(tree_sum_f32(sq, n));
+      /* A tile whose norm is not finite (an infinite or NaN input) has no
+         scale: it is coded as if its transform were zero and reported, the
+         way an fp16 norm overflow is (an error path the paper does not
+         define). */
+      const int nonfinite = !isfinite(nrm);
+      if (nonfinite) status = HQO_ERR_OVERFLOW;
       float rs;
       if (P->norm_fp16) {
         uint16_t h = hqo_f32_to_f16(nrm);
@@ -803,13 +809,15 @@ int hqo_frontend(const hqo_params* P, const float* x, int64_t rows, int64_t cols
         ((float*)norms)[r * tpr + t] = nrm;
         rs = nrm;
       }
-      float scale = (rs == 0.0f) ? 0.0f : P->alpha / rs;
+      float scale = (rs == 0.0f || nonfinite) ? 0.0f : P->alpha / rs;
       /* RHT (eq. rht): v = H D x. */
       for (int i = 0; i < n; ++i) {
         int64_t col = t * n + i;
         v[i] = (hqo_sign(P->rht_seed, col) < 0) ? -xt[i] : xt[i];
       }
       hqo_fwht_f32(v, n);
+      if (nonfinite)
+        for (int i = 0; i < n; ++i) v[i] = 0.0f;
       /* z = alpha sqrt(n) S y / ||y|| = (alpha / r) S y. */
       for (int i = 0; i < n; ++i) {
         float zi = v[i] * scale;

@@ -15,8 +15,8 @@ import numpy as np
 
 from . import oracle as O
 
-POINTS = [("E8", 2.0), ("E8", 3.0), ("E8", 4.0), ("E8", 5.0), ("D4", 3.0), ("D4", 4.0),
-          ("A2", 1.7), ("A2", 4.0), ("Z", 1.7), ("Z", 4.0)]
+POINTS = [("E8", 2.0), ("E8", 3.0), ("E8", 4.0), ("E8", 5.0), ("D4", 3.0), ("D4", 4.0), ("D4", 5.0),
+          ("A2", 1.7), ("A2", 4.0), ("A2", 5.0), ("Z", 1.7), ("Z", 4.0), ("Z", 5.0)]
 N_TILES = 4096
 TILE = 128
 SEED = 42

@@ -1263,6 +1263,7 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
   //      sub-streams lane l takes sub-stream i = l & 3, tile t = l >> 4 (each
   //      tile's 16 lanes hold its sum of squares, so the merged value repeats
   //      in every quad); with one, every lane takes its own tile l >> 4
+  bool nonfinite;
   {
     const int qi = SPW == 4 ? (lane & 3) : 0;
     float ssm = ss[0];
@@ -1270,7 +1271,8 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     const bool fp16_norm = KV && A.norm_fp16;
     const float r = __builtin_sqrtf(ssm);
     float rs = r;
-    bool bad_tile = !(r <= 3.0e38f);  // non-finite input
+    nonfinite = !(r <= 3.0e38f);  // an infinite or NaN input (r is at most 2^64 otherwise)
+    bool bad_tile = nonfinite;
     if (fp16_norm) {
       rs = (float)(_Float16)r;
       bad_tile = bad_tile || !(rs <= 65504.0f);
@@ -1301,6 +1303,15 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     } else {
       ss[0] = scale;
     }
+  }
+  // A non-finite tile has scale 0 and is coded as if its transform were
+  // zero (its values would turn the product into NaN); zero tiles, the other
+  // tiles with scale 0, hold zeros already.
+  if (__ballot(nonfinite) != 0ull) {
+#pragma unroll
+    for (int i = 0; i < SPW; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[i][j] = ss[i] == 0.0f ? 0.0f : x[i][j];
   }
 
   // ---- quantize and Rice-code each sub-stream into its LDS buffer
@@ -1357,8 +1368,9 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
   bool timed_out = false;
   for (int64_t hi = (int64_t)wg - 1; hi >= 0; hi -= 256)
     if (lookback_round<4>(A.status, hi, epoch, lane, prefix, timed_out)) break;
+  // an append to an empty stream starts at word 0, like a fresh encode
   const unsigned long long base =
-      (A.append ? (unsigned long long)readfirst(A.offsets[A.first_sub]) : 0ull) + prefix;
+      (A.first_sub > 0 ? (unsigned long long)readfirst(A.offsets[A.first_sub]) : 0ull) + prefix;
   if (lane == 0) {
     store_status(&A.status[wg], pack_status(epoch, 2u, prefix + agg));
     // the last group: every group has read this launch's epoch; advance it
@@ -1384,7 +1396,7 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     const uint32_t sub_l = wg * NSUB + (uint32_t)lane;
     if (lane < NSUB && sub_l < (uint32_t)A.nsub) {
       const unsigned long long end = base + il;
-      if (sub_l == 0 && !A.append) A.offsets[A.first_sub] = 0u;
+      if (sub_l == 0 && A.first_sub == 0) A.offsets[0] = 0u;
       A.offsets[A.first_sub + sub_l + 1] = (uint32_t)end;
       if (end > (unsigned long long)A.cap_words && A.stats)
         atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CAPACITY);
@@ -1644,9 +1656,11 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const De
       sym[j] = (qv[j] << kk) | (r & ((1u << kk) - 1u));
     }
   }
-  if (__ballot(!ok) != 0ull) {  // a corrupt sub-stream decodes as zeros
+  // a corrupt sub-stream (any lane's parse failed) decodes as all-zero
+  // symbols in every lane; callers drop its factor too
+  if (__ballot(!ok) != 0ull) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) sym[j] = ok ? sym[j] : 0u;
+    for (int j = 0; j < 8; ++j) sym[j] = 0u;
   }
   return ok;
 }
@@ -1719,9 +1733,9 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
 
     uint32_t sym[8];
     const bool ok = decode_symbols<LAT>(A, head, lane, buf, starts, s_sel, sym);
-    if (!ok && A.stats) {
+    const unsigned long long bad = __ballot(!ok);  // wave-uniform
+    if (bad && A.stats) {
       // count the sub-stream once (its first failing lane reports)
-      const unsigned long long bad = __ballot(!ok);
       if ((unsigned)lane == (unsigned)__builtin_ctzll(bad)) {
         atomicAdd(&A.stats->corrupt_substreams, 1u);
         atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
@@ -1729,7 +1743,8 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
     }
     int32_t c[8];
     unstrip8<LAT>(sym, c);
-    const float g = i == 0 ? quad_bcast<0>(gm) : (i == 1 ? quad_bcast<1>(gm) : (i == 2 ? quad_bcast<2>(gm) : quad_bcast<3>(gm)));
+    float g = i == 0 ? quad_bcast<0>(gm) : (i == 1 ? quad_bcast<1>(gm) : (i == 2 ? quad_bcast<2>(gm) : quad_bcast<3>(gm)));
+    if (bad) g = 0.0f;  // a corrupt sub-stream decodes as zeros, dither included
 
     if constexpr (MODE == 2) {
       uint32_t packed[2] = {0u, 0u};
@@ -2096,6 +2111,10 @@ __device__ __forceinline__ bool attn_tile(const hq_decode_args& S, const DecHead
     dither8<LAT>(S.dither_seed, row, (int64_t)j * HQ_SUB + 8 * lane, u);
 #pragma unroll
     for (int i = 0; i < 8; ++i) y[i] = y[i] - u[i];
+  }
+  if (__ballot(!ok) != 0ull) {  // a corrupt sub-stream contributes zeros
+#pragma unroll
+    for (int i = 0; i < 8; ++i) y[i] = 0.0f;
   }
   return ok;
 }

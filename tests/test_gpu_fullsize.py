@@ -537,8 +537,11 @@ def test_c5_gemm_fullsize(hq):
 
 
 def test_corrupt_streams_are_reported(hq):
-    """Damaged tables and payloads decode without faults: the damaged
-    sub-streams are counted and zero-filled, the others decode unchanged."""
+    """Damaged tables and payloads decode without faults: each damaged
+    sub-stream is counted once and decodes as zeros over its whole 512-column
+    span (every lane, not just the lanes whose codes failed to parse), the
+    fused GEMV takes zero from it, and every other sub-stream decodes
+    unchanged."""
     snr = PT.op_snr("E8", 4.0)
     P = PT.oracle_params(O.E8, snr, rht_seed=91)
     g = torch.Generator().manual_seed(92)
@@ -549,28 +552,46 @@ def test_corrupt_streams_are_reported(hq):
     good = hq.hq_decode(plan, s, out_dtype=torch.float32).cpu()
     torch.cuda.synchronize()
     spr = plan.info.subs_per_row
-    # row 3: k too large for its words; row 7: an empty sub-stream; row 11:
-    # random payload words; row 13: an end offset past the capacity
+    assert spr == 2
+    # Each damage is one the decoder must detect:
+    #   row 3:  k = 15 needs more remainder bits than the sub-stream has;
+    #   row 7:  sub-stream 0 ends before it starts, so sub-stream 1 spans
+    #           more words than any sub-stream may hold;
+    #   row 11: sub-stream 0's words zeroed, so its codes have no terminators;
+    #   row 13: an end offset past the capacity (sub-streams 0 and 1).
     kp = s.kparam.clone()
     kp[3 * spr] = 15
     s.kparam.copy_(kp)
     off = s.offsets.clone()
-    off[7 * spr + 1] = off[7 * spr]
+    off[7 * spr + 1] = off[7 * spr] - 1
     s.offsets.copy_(off)
     o11 = int(s.offsets[11 * spr].item()) & 0xFFFFFFFF
     o12 = int(s.offsets[11 * spr + 1].item()) & 0xFFFFFFFF
-    rnd = torch.randint(-2**31, 2**31 - 1, (o12 - o11,), generator=g, dtype=torch.int64)
-    s.payload[o11:o12] = rnd.to(s.payload.dtype).cuda()
+    s.payload[o11:o12] = 0
     off = s.offsets.clone()
     off[13 * spr + 1] = s.c.capacity_words + 5
     s.offsets.copy_(off)
+    assert (int(s.offsets[7 * spr + 2]) - int(s.offsets[7 * spr + 1])) > plan.info.max_words_per_substream
     s.reset_stats()
     bad = hq.hq_decode(plan, s, out_dtype=torch.float32).cpu()
     torch.cuda.synchronize()
     st = s.read_stats()
     assert st["status"] == (-6 & 0xFFFFFFFF), st  # HQ_ERR_CORRUPT
-    assert st["corrupt_substreams"] >= 2
+    damaged = {(3, 0), (7, 0), (7, 1), (11, 0), (13, 0), (13, 1)}
+    assert st["corrupt_substreams"] == len(damaged), st
     for r in range(16):
-        if r in (3, 7, 11, 13):
-            continue
-        assert torch.equal(bad[r], good[r]), r
+        for j in range(spr):
+            span = slice(512 * j, 512 * (j + 1))
+            if (r, j) in damaged:
+                assert torch.all(bad[r, span] == 0), (r, j)
+            else:
+                assert torch.equal(bad[r, span], good[r, span]), (r, j)
+    # the fused GEMV: damaged sub-streams contribute zero, the rest as decoded
+    xv = torch.randn(1024, generator=g).cuda()
+    s.reset_stats()
+    yv = hq.hq_decode_gemv(plan, s, xv, out_dtype=torch.float32).cpu().double()
+    torch.cuda.synchronize()
+    assert s.read_stats()["corrupt_substreams"] == len(damaged)
+    ref = bad.double() @ xv.cpu().double()
+    scale = bad.double().abs() @ xv.cpu().double().abs()
+    assert torch.all((yv - ref).abs() <= 1e-5 * scale + 1e-30)

@@ -380,3 +380,115 @@ def test_decode_gemv_argument_errors(hq):
     with pytest.raises(hq.HQError):  # dithered / rotated streams are not supported
         hq.hq_decode_gemv(kv, skv, x)
     torch.cuda.synchronize()
+
+
+def spike_matrix(rows, cols, rht_seed, seed, frac=0.5):
+    """bf16-exact rows where a fraction of the tiles are D times a row of the
+    Hadamard matrix (times +-1/16): the RHT maps such a tile to one spike of
+    height n, so its normalized coordinate is alpha sqrt(n), the largest code
+    the scale allows.  The other tiles are Gaussian."""
+    from scipy.linalg import hadamard
+    n = 128
+    rng = np.random.default_rng(seed)
+    x = (rng.standard_normal((rows, cols)) * 0.02).astype(np.float32)
+    d = O.signs(rht_seed, cols).astype(np.float32)
+    H = hadamard(n).astype(np.float32)
+    for r in range(rows):
+        for t in range(cols // n):
+            if rng.random() < frac:
+                k = int(rng.integers(n))
+                x[r, t * n:(t + 1) * n] = H[k] * d[t * n:(t + 1) * n] * np.float32(rng.choice([-1, 1]) / 16)
+    return torch.from_numpy(x).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("snr,limit", [(PT.op_snr("E8", 5.0), 127), (38.0, 448)])
+def test_decode_clamps_and_saturation(hq, snr, limit):
+    """int8 codes clamp at +-127 (E8 at 5 bps: a spike tile's code is about
+    alpha sqrt(128) = 166) and E4M3 codes saturate at 448 (38 dB: about 481),
+    each counted; the codes are the oracle's, clipped or cast."""
+    P = PT.oracle_params(O.E8, snr, rht_seed=23)
+    x = spike_matrix(24, 1024, 23, 7 + limit)
+    plan, s, res = check_roundtrip(hq, P, snr, x, f"spikes at {snr:.2f} dB")
+    oc = res["codes"]
+    assert np.abs(oc).max() > limit
+    s.reset_stats()
+    codes, g = hq.hq_decode_int8(plan, s)
+    torch.cuda.synchronize()
+    assert np.array_equal(codes.cpu().numpy().astype(np.int32), np.clip(oc, -127, 127))
+    assert s.read_stats()["clamps"] == int((np.abs(oc) > 127).sum())
+    assert np.array_equal(g.cpu().numpy(), O.weight_factors(P, res["norms"], 24, 1024))
+    s.reset_stats()
+    c8, g8 = hq.hq_decode_fp8(plan, s)
+    torch.cuda.synchronize()
+    assert np.array_equal(c8.cpu().numpy(), O.weight_codes_fp8(oc))
+    assert s.read_stats()["clamps"] == int((np.abs(oc) > 448).sum())
+
+
+def test_payload_capacity_overflow_is_reported(hq):
+    """A payload buffer declared smaller than the stream: HQ_ERR_CAPACITY in
+    the stats, no word written at or past the declared capacity, the offset
+    table complete, and every sub-stream that fits written in full."""
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=27)
+    x = gauss(32, 1024, 28, 0.02, torch.bfloat16)
+    codes, norms, _, _ = O.frontend(P, x.float().numpy())
+    o_pay, o_off, o_kp, _ = O.pack(P, codes)
+    need = int(o_off[-1])
+    for label, group in (("one launch", False), ("group launch", True)):
+        print(f"[parity] capacity {label}", flush=True)
+        plan = PT.gpu_plan(hq, P, snr, 1024)
+        s = hq.EncodedStream(plan, 32)
+        cap = need // 2
+        s.payload.fill_(0x5A5A5A5A)
+        s.c.capacity_words = cap
+        if group:
+            hq.hq_encode_group([plan], [x.cuda()], [s])
+        else:
+            hq.hq_encode(plan, x.cuda(), s)
+        torch.cuda.synchronize()
+        st = s.read_stats()
+        assert st["status"] == (-3 & 0xFFFFFFFF), st
+        pay = s.payload.cpu().numpy().view(np.uint32)
+        assert np.all(pay[cap:] == 0x5A5A5A5A)
+        off = s.offsets[:o_off.size].cpu().numpy().view(np.uint32)
+        assert np.array_equal(off, o_off)
+        fits = np.nonzero(o_off[1:] <= cap)[0]
+        assert fits.size > 0
+        for sub in fits:
+            assert np.array_equal(pay[o_off[sub]:o_off[sub + 1]], o_pay[o_off[sub]:o_off[sub + 1]])
+
+
+def test_nonfinite_tiles_are_zero_coded_and_reported(hq):
+    """Tiles with an infinite or NaN value: HQ_ERR_OVERFLOW, one count per bad
+    tile, the bad tiles coded as zeros and every other tile bit-exact with
+    the oracle (which codes a non-finite tile as zeros), in both launch
+    shapes."""
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=29)
+    x = gauss(16, 1024, 30, 0.02, torch.bfloat16)
+    x[2, 130] = float("inf")
+    x[9, 700] = float("nan")
+    x[9, 701] = float("-inf")
+    x[11, 1000] = float("-inf")
+    xn = x.float().numpy()
+    codes, norms, _, rc = O.frontend(P, xn)
+    assert rc == O.ERR_OVERFLOW
+    o_pay, o_off, o_kp, _ = O.pack(P, codes)
+    bad = ~np.isfinite(norms)
+    assert bad.sum() == 3
+    for label, group in (("one launch", False), ("group launch", True)):
+        print(f"[parity] non-finite tiles, {label}", flush=True)
+        plan = PT.gpu_plan(hq, P, snr, 1024)
+        s = hq.EncodedStream(plan, 16)
+        if group:
+            hq.hq_encode_group([plan], [x.cuda()], [s])
+        else:
+            hq.hq_encode(plan, x.cuda(), s)
+        torch.cuda.synchronize()
+        st = s.read_stats()
+        assert st["status"] == (-4 & 0xFFFFFFFF) and st["overflow_tiles"] == 3, st
+        g_pay, g_off, g_kp, g_norm = PT.gpu_stream_arrays(s, 16)
+        assert np.array_equal(g_off, o_off) and np.array_equal(g_kp, o_kp)
+        assert np.array_equal(g_pay, o_pay[:o_off[-1]])
+        assert np.array_equal(g_norm[~bad].view(np.uint32), norms[~bad].view(np.uint32))
+        assert not np.any(np.isfinite(g_norm[bad]))
