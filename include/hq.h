@@ -180,6 +180,28 @@ size_t hq_scan_bytes(hq_plan_t plan, int64_t rows);
 hq_status hq_encode(hq_plan_t plan, const void* x, int32_t xt, int64_t rows, int64_t ld,
                     hq_stream* s, int32_t append, void* stream);
 
+/* hq_encode_noalloc -- hq_encode for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops (the KV
+ * quantize-on-append of every forward step), harnesses that forbid it.  The
+ * same kernels and bit-identical results, with the look-back scratch taken
+ * from a fixed array inside the library (HQ_NOALLOC_SCAN_BYTES = 1 MiB on
+ * each device the library runs on, held until the process ends) instead of
+ * s->scan, which is ignored and may be null.  The caller still provides
+ * every input and output buffer of s.
+ *   Limit: hq_scan_bytes(plan, rows) <= 1 MiB, i.e. at most 65528
+ *   workgroups of 16 sub-streams = 1048448 sub-streams (536,805,376 scalars
+ *   at 512 per sub-stream) per call; larger calls return HQ_ERR_CAPACITY
+ *   before any work is enqueued.
+ *   The first call on a device looks the array up and clears it on `stream`.
+ *   Every call on one device shares that array and leaves its contents for
+ *   the next, so calls that overlap on one GPU (two streams, two host
+ *   threads) race; the caller serializes them.
+ * Allocates nothing (no hipMalloc, hipFree or allocating library call).
+ * Errors: as hq_encode, plus HQ_ERR_CAPACITY for the limit above. */
+#define HQ_NOALLOC_SCAN_BYTES (1u << 20)
+hq_status hq_encode_noalloc(hq_plan_t plan, const void* x, int32_t xt, int64_t rows, int64_t ld,
+                            hq_stream* s, int32_t append, void* stream);
+
 /* hq_encode_group -- hq_encode (append = 0) of `count` matrices in as few
  * launches as possible (up to 16 per launch): member i encodes rows[i] rows of
  * x[i] (element type xt, row stride ld[i]) with plans[i] into s[i], exactly

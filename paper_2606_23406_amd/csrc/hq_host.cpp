@@ -478,6 +478,20 @@ hq_status hq_encode(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_
   return HQ_OK;
 }
 
+hq_status hq_encode_noalloc(hq_plan_t p, const void* x, int32_t xt, int64_t rows, int64_t ld,
+                            hq_stream* s, int32_t append, void* stream) {
+  if (!p || !s || rows < 0) return HQ_ERR_INVALID_ARG;
+  if (hq_scan_bytes(p, rows) > (size_t)HQ_NOALLOC_SCAN_BYTES) return HQ_ERR_CAPACITY;
+  void* scan = nullptr;
+  if (hq_noalloc_scan(&scan, stream) != 0) return HQ_ERR_HIP;
+  hq_stream t = *s;  // the caller's stream with the fixed scratch in place of s->scan
+  t.scan = scan;
+  t.scan_bytes = (int64_t)HQ_NOALLOC_SCAN_BYTES;
+  const hq_status st = hq_encode(p, x, xt, rows, ld, &t, append, stream);
+  s->rows = t.rows;
+  return st;
+}
+
 static bool same_kernel_family(const hq_plan_s* a, const hq_plan_s* b) {
   const bool kva = a->rotation || a->dither || a->norm_fp16;
   const bool kvb = b->rotation || b->dither || b->norm_fp16;

@@ -196,3 +196,7 @@ int hq_launch_decode_int8(const hq_plan_s* p, const hq_decode_args& a, void* str
 int hq_launch_act_prep(const hq_actprep_args& a, void* stream);
 int hq_launch_gemm(const hq_gemm_args& a, void* stream);
 int hq_launch_zero(void* ptr, size_t bytes, void* stream);
+// Device address of the current device's fixed encode scratch
+// (HQ_NOALLOC_SCAN_BYTES); the first call on a device looks it up and clears
+// it on `stream`.  0 on success.
+int hq_noalloc_scan(void** ptr, void* stream);

@@ -18,6 +18,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "hq_internal.h"
 
 #pragma clang fp contract(off)
@@ -2916,6 +2918,36 @@ int hq_launch_zero(void* ptr, size_t bytes, void* stream) {
   hipLaunchKernelGGL(hq_zero_kernel, dim3((uint32_t)((n + 255) / 256)), dim3(256), 0,
                      (hipStream_t)stream, (uint32_t*)ptr, n);
   return (int)hipGetLastError();
+}
+
+// ------------------------------------------------------------ fixed scratch
+// The look-back scratch of hq_encode_noalloc, for callers that cannot
+// allocate: one array per device, alive until the process ends.  Host code
+// never passes the array's name to a kernel (on the host it is a stand-in,
+// not a device address); it uses the address hipGetSymbolAddress returns for
+// the current device, looked up once per device.
+static __device__ __align__(256) unsigned char scratch[HQ_NOALLOC_SCAN_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+int hq_noalloc_scan(void** ptr, void* stream) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return -1;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return -1;
+    // the epoch word and every status word start at zero (a fill kernel, so
+    // a first call under graph capture records no memset node)
+    if (hq_launch_zero(p, HQ_NOALLOC_SCAN_BYTES, stream) != 0) return -1;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return 0;
 }
 
 int hq_launch_decode_gemv(const hq_plan_s* p, const hq_decode_args& a, const void* x, int xt,

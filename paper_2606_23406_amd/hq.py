@@ -83,6 +83,8 @@ def lib():
     L.hq_scan_bytes.argtypes = [p, i64]
     L.hq_encode.restype = i32
     L.hq_encode.argtypes = [p, p, i32, i64, i64, p, i32, p]
+    L.hq_encode_noalloc.restype = i32
+    L.hq_encode_noalloc.argtypes = [p, p, i32, i64, i64, p, i32, p]
     L.hq_decode.restype = i32
     L.hq_decode.argtypes = [p, p, i64, i64, p, i32, i64, p]
     L.hq_encode_group.restype = i32
@@ -236,6 +238,19 @@ def hq_encode(plan: Plan, x: torch.Tensor, s: EncodedStream, append=False, strea
     st = lib().hq_encode(plan.handle, C.c_void_p(x.data_ptr()), _dtype_code(x.dtype), rows, ld,
                          C.byref(s.c), int(bool(append)), _stream_handle(stream))
     _check("hq_encode", st)
+    return s
+
+
+def hq_encode_noalloc(plan: Plan, x: torch.Tensor, s: EncodedStream, append=False, stream=None):
+    """hq_encode_noalloc: hq_encode with the library's fixed look-back scratch
+    (s.scan is not used)."""
+    assert x.dim() == 2 and x.is_cuda
+    rows = x.shape[0]
+    ld = x.stride(0)
+    assert x.stride(1) == 1
+    st = lib().hq_encode_noalloc(plan.handle, C.c_void_p(x.data_ptr()), _dtype_code(x.dtype), rows,
+                                 ld, C.byref(s.c), int(bool(append)), _stream_handle(stream))
+    _check("hq_encode_noalloc", st)
     return s
 
 
@@ -454,6 +469,7 @@ def hq_calibrated_snr(lattice, rice_k, bps):
 
 
 EXPORTED = ["hq_plan", "hq_plan_destroy", "hq_plan_get_info", "hq_scan_bytes", "hq_encode",
+            "hq_encode_noalloc",
             "hq_decode", "hq_encode_group", "hq_decode_group", "hq_decode_int8", "hq_act_prep", "hq_gemm_int8_blockscaled",
             "hq_gemm_workspace_bytes", "hq_dequant_gemm_int8", "hq_gemv_workspace_bytes",
             "hq_decode_gemv", "hq_attention_workspace_bytes", "hq_decode_attention",
