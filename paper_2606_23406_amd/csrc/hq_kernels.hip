@@ -763,6 +763,40 @@ __device__ __forceinline__ int32_t sub_lanemask(int32_t x, uint64_t m) {
 }
 
 
+// The class decision of a block inside the tie band, exactly as the
+// step-by-step procedure takes it: the two classes' squared distances in
+// fp32 (z units, z = 2 w), each error rebuilt exactly from ea = w - rint(w).
+// The first class's error on coordinate i is 2 ea_i, and its parity fix
+// (the first coordinate of largest |ea|) leaves 2 (1 - |ea_j|) in magnitude;
+// the second class's is 2 (1/2 - |ea_i|), and its fix (the first coordinate
+// of largest 1/2 - |ea|) leaves 2 (|ea_j| + 1/2).  Every doubling is exact,
+// so each value is the procedure's own rounding; the squares are summed in
+// its tree order, and the first class wins ties.
+__device__ __forceinline__ bool e8_even_exact(const float* ea, float mx, float mn, bool odd_a,
+                                              bool odd_b) {
+  const float topb = 0.5f - mn;
+  bool fixa = odd_a, fixb = odd_b;
+  float sa[8], sb[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float a = __builtin_fabsf(ea[i]);
+    float ua = a, ub = 0.5f - a;
+    if (fixa && a == mx) {
+      ua = 1.0f - a;
+      fixa = false;
+    }
+    if (fixb && ub == topb) {
+      ub = a + 0.5f;
+      fixb = false;
+    }
+    ua = ua + ua;
+    ub = ub + ub;
+    sa[i] = ua * ua;
+    sb[i] = ub * ub;
+  }
+  return tree8(sa) <= tree8(sb);
+}
+
 __device__ __forceinline__ void e8_nearest(const float* w, int32_t* h, int32_t& cb) {
   float ea[8];
   int32_t K[8];
@@ -805,24 +839,18 @@ __device__ __forceinline__ void e8_nearest(const float* w, int32_t* h, int32_t& 
   const float D0 = Sabs - 2.0f;
   const float D1 = odd_a ? __builtin_fmaf(-2.0f, mx, Sabs - 1.0f) : D0;
   const float D = odd_b ? __builtin_fmaf(-2.0f, mn, D1) : D1;
+  bool even = D < 0.0f;
+  // Inside the tie band (or with every |ea_i| = 1/2, where the second
+  // class's fix moves up from ea_j = +1/2 too) the lane takes the exact
+  // decision; a wave with no such lane skips it.
   const bool tie = __builtin_fabsf(D) <= 0.25f * kE8Tie || mn >= 0.5f;
-  if (__ballot(tie) != 0ull) {
-    float z[8];
-    int32_t c[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) z[i] = w[i] + w[i];
-    quant_e8(z, c);
-    cb = c[0] & 1;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) h[i] = (c[i] - cb) >> 1;
-    return;
-  }
+  const bool any_tie = __ballot(tie) != 0ull;
+  if (any_tie && tie) even = e8_even_exact(ea, mx, mn, odd_a, odd_b);
   // lane masks: the class, whether its parity needs the fix, and per
   // coordinate the largest-error hits and the sign of ea.  The error of
   // coordinate i in the lane's class is key_i = fma(|ea_i|, +-1, 0 or 1/2):
   // |ea_i| (exact) in the first class, fl(1/2 - |ea_i|) (one rounding, as
   // the subtraction) in the second; its largest value is mx or fl(1/2 - mn).
-  const bool even = D < 0.0f;
   const uint64_t E = __ballot(even);
   const uint64_t need = (E & __ballot(odd_a)) | (~E & __ballot(odd_b));
   const float ks = even ? 1.0f : -1.0f, kc = even ? 0.0f : 0.5f;
@@ -838,6 +866,9 @@ __device__ __forceinline__ void e8_nearest(const float* w, int32_t* h, int32_t& 
     const uint64_t down = (E & fix & neg) | (~E & (neg ^ fix));
     h[i] = sub_lanemask(add_lanemask(K[i], up), down);
   }
+  // every |ea_i| = 1/2: the second class wins and its fix (coordinate 0)
+  // moves up also from ea_0 = +1/2, where the masks above moved it down
+  if (any_tie && mn >= 0.5f && !even && odd_b && ea[0] > 0.0f) h[0] += 2;
   cb = even ? 0 : 1;
 }
 
@@ -963,26 +994,52 @@ __device__ __forceinline__ void or_word(uint32_t* buf, uint32_t pos, uint32_t v)
   atomicOr(&buf[(pos >> 5) + 1], (uint32_t)(t >> 32));
 }
 
-// Front end of one sub-stream: the lane's 8 scalars with the RHT signs D
-// applied, the tile's sum of squares (a pairwise tree in index order: the
-// lane butterflies 1, 2, 4, 8 add the same pairs in the same order), and
-// x <- sigma H D x.
+// The lane's 8 input values with the RHT signs D applied, kept in their
+// loaded form until the transform needs them: four bf16 pairs or eight fp32
+// words.  A wave holding several sub-streams keeps the pending ones at half
+// the registers of their fp32 values (bf16), which is what lets the encoder
+// run eight waves per SIMD.
 template <int XT>
-__device__ __forceinline__ float encode_front(const LaneInput& in, const TwSigns& sg, float* x) {
+struct Packed {
+  uint32_t w[XT == HQ_BF16 ? 4 : 8];
+};
+
+template <int XT>
+__device__ __forceinline__ Packed<XT> pack_signed(const LaneInput& in) {
+  Packed<XT> p;
   if constexpr (XT == HQ_BF16) {
-    const uint32_t w4[4] = {in.a.x ^ in.sw.x, in.a.y ^ in.sw.y, in.a.z ^ in.sw.z,
-                            in.a.w ^ in.sw.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      x[2 * i] = __uint_as_float(w4[i] << 16);
-      x[2 * i + 1] = __uint_as_float(w4[i] & 0xFFFF0000u);
-    }
+    p.w[0] = in.a.x ^ in.sw.x;
+    p.w[1] = in.a.y ^ in.sw.y;
+    p.w[2] = in.a.z ^ in.sw.z;
+    p.w[3] = in.a.w ^ in.sw.w;
   } else {
     const uint32_t w8[8] = {in.a.x, in.a.y, in.a.z, in.a.w, in.b.x, in.b.y, in.b.z, in.b.w};
 #pragma unroll
-    for (int i = 0; i < 8; ++i) x[i] = flip(__uint_as_float(w8[i]), in.sw.x, i);
+    for (int i = 0; i < 8; ++i) p.w[i] = w8[i] ^ (((in.sw.x >> i) & 1u) << 31);
   }
-  float sq[8];
+  return p;
+}
+
+template <int XT>
+__device__ __forceinline__ void unpack(const Packed<XT>& p, float* x) {
+  if constexpr (XT == HQ_BF16) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      x[2 * i] = __uint_as_float(p.w[i] << 16);
+      x[2 * i + 1] = __uint_as_float(p.w[i] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) x[i] = __uint_as_float(p.w[i]);
+  }
+}
+
+// The tile's sum of squares: a pairwise tree in index order (the lane
+// butterflies 1, 2, 4, 8 add the same pairs in the same order).
+template <int XT>
+__device__ __forceinline__ float tile_sumsq(const Packed<XT>& p) {
+  float x[8], sq[8];
+  unpack<XT>(p, x);
 #pragma unroll
   for (int i = 0; i < 8; ++i) sq[i] = x[i] * x[i];
   float ss = tree8(sq);
@@ -990,7 +1047,6 @@ __device__ __forceinline__ float encode_front(const LaneInput& in, const TwSigns
   ss = ss + dpp_xor<2>(ss);
   ss = ss + swz_xor4(ss);
   ss = ss + dpp_xor<8>(ss);
-  fwht128_tw(x, sg);
   return ss;
 }
 
@@ -1252,14 +1308,15 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
       }
     }
   }
-  // ---- front ends of the wave's sub-streams: every input load is issued
-  //      first, then sign flips, tile sums of squares and transforms
-  LaneInput in[SPW];
+  // ---- every input load of the wave's sub-streams is issued first; each is
+  //      kept packed with its signs applied, and its tile sums of squares
+  //      taken (the transforms wait until each sub-stream is coded)
+  Packed<XT> pk[SPW];
 #pragma unroll
-  for (int i = 0; i < SPW; ++i) in[i] = load_lane_input<XT>(A, pos[i], lane);
-  float x[SPW][8], ss[SPW];
+  for (int i = 0; i < SPW; ++i) pk[i] = pack_signed<XT>(load_lane_input<XT>(A, pos[i], lane));
+  float ss[SPW];
 #pragma unroll
-  for (int i = 0; i < SPW; ++i) ss[i] = encode_front<XT>(in[i], sg, x[i]);
+  for (int i = 0; i < SPW; ++i) ss[i] = tile_sumsq<XT>(pk[i]);
 
   // ---- tile norms and scales, once for the wave's tiles: with four
   //      sub-streams lane l takes sub-stream i = l & 3, tile t = l >> 4 (each
@@ -1313,7 +1370,7 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
 #pragma unroll
     for (int i = 0; i < SPW; ++i)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) x[i][j] = ss[i] == 0.0f ? 0.0f : x[i][j];
+      for (int j = 0; j < (XT == HQ_BF16 ? 4 : 8); ++j) pk[i].w[j] = ss[i] == 0.0f ? 0u : pk[i].w[j];
   }
 
   // ---- quantize and Rice-code each sub-stream into its LDS buffer
@@ -1324,7 +1381,10 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     const uint32_t sub = wg * NSUB + (uint32_t)li;
     uint32_t W, kb, bits;
     bool ovf;
-    encode_substream<LAT, XT, KV>(A, T, pos[i], lane, x[i], xor_sign(ss[i], sg.sigma),
+    float x[8];  // x <- sigma H D x
+    unpack<XT>(pk[i], x);
+    fwht128_tw(x, sg);
+    encode_substream<LAT, XT, KV>(A, T, pos[i], lane, x, xor_sign(ss[i], sg.sigma),
                                   smem + li * stride,
                                   (float*)(smem + NSUB * stride) + wave * HQ_QJL_STAGE, W, kb,
                                   bits, ovf);
