@@ -82,6 +82,23 @@ __device__ __forceinline__ uint32_t wave_scan_incl(uint32_t x) {
   return x;
 }
 
+// Two inclusive prefix sums over the 64 lanes at once (interleaved, so the
+// two chains' latencies overlap).
+__device__ __forceinline__ void wave_scan_incl2(uint32_t& a, uint32_t& b) {
+  a += dpp<kDppRowShr1, 0xF, 0xF, true>(0u, a);
+  b += dpp<kDppRowShr1, 0xF, 0xF, true>(0u, b);
+  a += dpp<kDppRowShr2, 0xF, 0xF, true>(0u, a);
+  b += dpp<kDppRowShr2, 0xF, 0xF, true>(0u, b);
+  a += dpp<kDppRowShr4, 0xF, 0xF, true>(0u, a);
+  b += dpp<kDppRowShr4, 0xF, 0xF, true>(0u, b);
+  a += dpp<kDppRowShr8, 0xF, 0xF, true>(0u, a);
+  b += dpp<kDppRowShr8, 0xF, 0xF, true>(0u, b);
+  a += dpp<kDppRowBcast15, 0xA, 0xF>(0u, a);
+  b += dpp<kDppRowBcast15, 0xA, 0xF>(0u, b);
+  a += dpp<kDppRowBcast31, 0xC, 0xF>(0u, a);
+  b += dpp<kDppRowBcast31, 0xC, 0xF>(0u, b);
+}
+
 // Sum over the 64 lanes, as a wave-uniform value.
 __device__ __forceinline__ uint32_t wave_total(uint32_t x) {
   return __builtin_amdgcn_readlane(wave_scan_incl(x), 63);
@@ -99,6 +116,12 @@ __device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c) {
 __device__ __forceinline__ uint32_t lshl_or(uint32_t a, uint32_t sh, uint32_t c) {
   uint32_t r;
   asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(sh), "v"(c));
+  return r;
+}
+// (a << sh) | c with a wave-uniform shift held in a scalar register
+__device__ __forceinline__ uint32_t lshl_or_s(uint32_t a, uint32_t sh, uint32_t c) {
+  uint32_t r;
+  asm("v_lshl_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "s"(sh), "v"(c));
   return r;
 }
 __device__ __forceinline__ uint32_t bit_or(uint32_t sh, uint32_t c) {
@@ -862,8 +885,11 @@ __device__ __forceinline__ void e8_nearest(const float* w, int32_t* h, int32_t& 
     const uint64_t fix = hit & ~done;
     done |= hit;
     const uint64_t neg = __ballot(ea[i] < 0.0f);
-    const uint64_t up = E & fix & ~neg;
-    const uint64_t down = (E & fix & neg) | (~E & (neg ^ fix));
+    // up by the fix where the class and the sign agree to move up; down by
+    // the fix otherwise, or by the odd class's floor (never both)
+    const uint64_t t = E ^ neg;
+    const uint64_t up = fix & t;
+    const uint64_t down = (fix & ~t) | (neg & ~E);
     h[i] = sub_lanemask(add_lanemask(K[i], up), down);
   }
   // every |ea_i| = 1/2: the second class wins and its fix (coordinate 0)
@@ -896,9 +922,16 @@ __device__ __forceinline__ void e8_strip(const int32_t* h, int32_t cb, uint32_t*
 // Number of k in 1..KMAX with sum >= thr[k] (thresholds clamped below 2^30
 // on the host, sums below 2^26), on scalar registers.
 __device__ __forceinline__ uint32_t kstar_count(uint32_t sum, const uint32_t* thr) {
-  uint32_t a = 0;
-#pragma unroll
-  for (int t = 1; t <= HQ_KMAX; ++t) a += (uint32_t)((int32_t)(thr[t] - 1u - sum)) >> 31;
+  // thr[1..15] is nondecreasing, so the count is the largest t with
+  // sum >= thr[t]: a binary search, each level's threshold picked by selects
+  uint32_t a = sum >= thr[8] ? 8u : 0u;
+  const uint32_t t4 = a ? thr[12] : thr[4];
+  a += sum >= t4 ? 4u : 0u;
+  const uint32_t t2 = a < 8u ? (a ? thr[6] : thr[2]) : (a == 8u ? thr[10] : thr[14]);
+  a += sum >= t2 ? 2u : 0u;
+  const uint32_t t1 = a < 8u ? (a < 4u ? (a ? thr[3] : thr[1]) : (a == 4u ? thr[5] : thr[7]))
+                             : (a < 12u ? (a == 8u ? thr[9] : thr[11]) : (a == 12u ? thr[13] : thr[15]));
+  a += sum >= t1 ? 1u : 0u;
   return a;
 }
 
@@ -1105,8 +1138,9 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
     strip8<LAT>(c, sym);
   }
 
-  // ---- Rice parameters (wave-uniform) and quotients
-  uint32_t k0, k1, qv[8], ulen;
+  // ---- Rice parameters (wave-uniform), quotients and the unary-length scan
+  uint32_t k0, k1, qv[8], ulen, uincl;
+  bool scanned = false;
   if constexpr (LAT == kE8 || LAT == kZ) {
     uint32_t s0 = 0;
 #pragma unroll
@@ -1122,7 +1156,9 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
     } else {
       const uint32_t a0 = kstar_count(wave_total(s0), T.thr0);
       // the better of k* and k* + 1: k* + 1 saves sum((m >> k) - (m >> (k+1)))
-      // unary bits and costs one remainder bit per symbol
+      // unary bits and costs one remainder bit per symbol.  Both candidates'
+      // unary-length scans run in one pass; their totals give that saving,
+      // and the chosen one's scan places the codes.
       uint32_t ga = 0, gb = 0;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -1130,12 +1166,16 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
         ga += qv[j];
         gb += qv[j] >> 1;
       }
-      const uint32_t gain = wave_total(ga - gb);
-      const uint32_t d = (a0 < HQ_KMAX && gain > (uint32_t)HQ_SUB) ? 1u : 0u;
+      uint32_t ia = 8 + ga, ib = 8 + gb;
+      wave_scan_incl2(ia, ib);
+      const uint32_t Ua = __builtin_amdgcn_readlane(ia, 63), Ub = __builtin_amdgcn_readlane(ib, 63);
+      const uint32_t d = (a0 < HQ_KMAX && Ua - Ub > (uint32_t)HQ_SUB) ? 1u : 0u;
       k0 = a0 + d;
 #pragma unroll
       for (int j = 0; j < 8; ++j) qv[j] >>= d;
       ulen = 8 + (d ? gb : ga);
+      uincl = d ? ib : ia;
+      scanned = true;
     }
     k1 = k0;
   } else {
@@ -1192,7 +1232,7 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   // ---- code lengths: remainder region then unary region
   const uint32_t lrem = lane_rem_bits<LAT>(k0, k1);
   const uint32_t R = 64 * lrem;
-  const uint32_t uincl = wave_scan_incl(ulen);
+  if (!scanned) uincl = wave_scan_incl(ulen);
   const uint32_t U = __builtin_amdgcn_readlane(uincl, 63);
   const uint32_t uoff = uincl - ulen;
   uint32_t W = (R + U + 31) >> 5;
@@ -1216,7 +1256,7 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-        acc = lshl_or(sym[j] & ((1u << kk) - 1u), rem_offset<LAT>(j, k0, k1), acc);
+        acc = lshl_or_s(sym[j] & ((1u << kk) - 1u), readfirst(rem_offset<LAT>(j, k0, k1)), acc);
       }
       or_word(buf, rpos, acc);
     } else if (lrem <= 64) {
@@ -1605,30 +1645,33 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const De
   const uint32_t nuw = ok ? Wl - uw0 : 0u;
   uint32_t pos;
   if (nuw <= 64u) {
-    // one word per lane: lane l finds its word by binary search over the
-    // inclusive counts (kept in `starts`), then selects inside it
+    // one word per lane: word w holds terminators excl_w .. incl_w - 1, and
+    // lane l >= 1 starts just past terminator 8 l - 1, so word w is the
+    // start word of lanes l in [(excl_w + 8) / 8, incl_w / 8] (at most four,
+    // a word holding at most 32 terminators).  Each word's lane writes its
+    // index and excl_w into those lanes' slots; each lane then reads its own
+    // and selects inside that word.  A lane past the last terminator (8 l >
+    // the total) gets no slot and reports a corrupt sub-stream.
     const uint32_t v = ((uint32_t)lane < nuw) ? buf[uw0 + lane] : 0u;
-    starts[lane] = wave_scan_incl(__popc(v));
+    const uint32_t cnt = __popc(v);
+    const uint32_t incl = wave_scan_incl(cnt);
+    const uint32_t total = __builtin_amdgcn_readlane(incl, 63);
+    const uint32_t excl = incl - cnt;
+    const uint32_t llo = (excl + 8u) >> 3, lhi = incl >> 3;
+    const uint32_t entry = (uint32_t)lane | (excl << 8);
+#pragma unroll
+    for (uint32_t i = 0; i < 4; ++i)
+      if (llo + i <= lhi && llo + i < 64u) starts[llo + i] = entry;
     wave_sync_lds();
     const uint32_t target = 8u * (uint32_t)lane;  // terminators before this lane's codes
-    // the search moves a byte pointer: a step is taken when starts[...] -
-    // target is negative, its sign bit the mask, so every step is a few
-    // fast-rate adds and ands (counts and targets are below 2^12)
-    const char* sp = (const char*)starts;
-#pragma unroll
-    for (uint32_t step = 32; step >= 1; step >>= 1) {
-      const int32_t d = (int32_t)(*(const uint32_t*)(sp + 4u * (step - 1u)) - target);
-      sp += (4u * step) & (uint32_t)(d >> 31);
-    }
-    const uint32_t w = (uint32_t)(sp - (const char*)starts) >> 2;
-    const uint32_t word = w < nuw ? buf[uw0 + w] : 0u;
-    const uint32_t incl = starts[w];
     if (lane == 0) {
       pos = R;
     } else {
-      ok = ok && incl >= target && w < nuw;
-      pos = ok ? (uw0 + w) * 32u + select32_lut(word, target - 1u - (incl - __popc(word)), seltbl) + 1u
-               : 0u;
+      ok = ok && target <= total;
+      const uint32_t e = ok ? starts[lane] : 0u;
+      const uint32_t w = e & 0xFFu;
+      const uint32_t word = ok ? buf[uw0 + w] : 0u;
+      pos = ok ? (uw0 + w) * 32u + select32_lut(word, target - 1u - (e >> 8), seltbl) + 1u : 0u;
     }
   } else {
     uint32_t carry = 0;
