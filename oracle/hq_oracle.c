@@ -752,7 +752,10 @@ static int check_params(const hqo_params* P, int64_t cols) {
   if (m == 0 || n < m || (n & (n - 1)) != 0) return HQO_ERR_ARG;
   if (P->rotation < 0 || P->rotation > 2 || (P->rotation == 2 && !P->qjl)) return HQO_ERR_ARG;
   if (cols % n != 0) return HQO_ERR_ARG;
-  if (P->substream <= 0 || P->substream % n != 0 || cols % P->substream != 0) return HQO_ERR_ARG;
+  /* a sub-stream holds whole tiles, or a tile spans whole sub-streams */
+  if (P->substream <= 0 || (P->substream % n != 0 && n % P->substream != 0) ||
+      cols % P->substream != 0)
+    return HQO_ERR_ARG;
   if (P->rice_k > HQO_KMAX) return HQO_ERR_ARG;
   return HQO_OK;
 }

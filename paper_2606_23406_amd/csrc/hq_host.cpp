@@ -137,7 +137,10 @@ int64_t substream_word_bound(const hq_plan_s& p) {
   const int n = p.tile, m = p.dim, S = p.substream;
   const double T = (double)S / n;
   const double cn = code_norm_bound(p);
-  const double M = T * (2.0 * std::sqrt((double)n) * cn + 2.0 * n);
+  // a sub-stream of whole tiles sums T tiles' bounds; a sub-stream inside a
+  // longer tile may hold all of that tile's code norm on its S coordinates
+  const double M = S >= n ? T * (2.0 * std::sqrt((double)n) * cn + 2.0 * n)
+                          : 2.0 * std::sqrt((double)S) * cn + 2.0 * S;
   const int64_t Mi = (int64_t)std::ceil(M) + 1;
   int64_t n0, n1;
   class_counts(p.lattice, S, &n0, &n1);
@@ -241,7 +244,8 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   const int m = lattice_dim(lattice);
   if (tile < m || tile <= 0 || (tile & (tile - 1)) != 0) return HQ_ERR_INVALID_ARG;
   const int S = o.substream ? o.substream : HQ_SUB;
-  if (S <= 0 || S % tile != 0 || cols <= 0 || cols % tile != 0 || cols % S != 0)
+  // a sub-stream holds whole tiles, or a tile spans whole sub-streams
+  if (S <= 0 || (S % tile != 0 && tile % S != 0) || cols <= 0 || cols % tile != 0 || cols % S != 0)
     return HQ_ERR_INVALID_ARG;
   if (rice_k < -1 || rice_k > HQ_KMAX) return HQ_ERR_INVALID_ARG;
   if (o.rotation != HQ_ROT_NONE && o.rotation != HQ_ROT_SIGNS && o.rotation != HQ_ROT_QJL)
@@ -249,7 +253,13 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   if (o.rotation == HQ_ROT_QJL && !o.qjl) return HQ_ERR_INVALID_ARG;
   if (o.norm_dtype != 0 && o.norm_dtype != HQ_FP32 && o.norm_dtype != HQ_FP16)
     return HQ_ERR_INVALID_ARG;
-  if (tile != HQ_TILE || S != HQ_SUB) return HQ_ERR_UNSUPPORTED;
+  if (S != HQ_SUB) return HQ_ERR_UNSUPPORTED;
+  // tiles of 256 .. 2048 (the sweep of Sec. 7.2) are built for weight plans:
+  // no rotation, no dither, fp32 norms
+  if (tile != HQ_TILE &&
+      (tile < 256 || tile > HQ_TILE_MAX || o.rotation != HQ_ROT_NONE || o.dither ||
+       o.norm_dtype == HQ_FP16))
+    return HQ_ERR_UNSUPPORTED;
   if (cols > (int64_t)1 << 28) return HQ_ERR_UNSUPPORTED;  // per-lane byte offsets stay 32-bit
 
   double snr;
@@ -295,7 +305,8 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
 
   // sign bitmasks: bit j set means the sign is -1
   const int64_t nw = (cols + 31) / 32;
-  std::vector<uint32_t> dm((size_t)nw, 0u), sm(4, 0u);
+  const int64_t snw = ((int64_t)tile + 31) / 32;  // words of the rotation mask (one bit per coordinate)
+  std::vector<uint32_t> dm((size_t)nw, 0u), sm((size_t)snw, 0u);
   for (int64_t j = 0; j < cols; ++j)
     if (splitmix_negative(rht_seed, (uint64_t)j)) dm[(size_t)(j >> 5)] |= 1u << (j & 31);
   for (int j = 0; j < tile; ++j)
@@ -310,7 +321,7 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   p->d_qjl = nullptr;
   p->d_qjlt = nullptr;
   bool ok = hipMalloc((void**)&p->d_dmask, sizeof(uint32_t) * (size_t)nw) == hipSuccess &&
-            hipMalloc((void**)&p->d_smask, sizeof(uint32_t) * 4) == hipSuccess &&
+            hipMalloc((void**)&p->d_smask, sizeof(uint32_t) * (size_t)snw) == hipSuccess &&
             hipMalloc((void**)&p->d_dsign16, sizeof(uint32_t) * (size_t)npairs) == hipSuccess;
   if (ok && o.rotation == HQ_ROT_QJL) {
     const size_t nn = (size_t)tile * tile;
@@ -325,7 +336,7 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   ok = ok &&
        hipMemcpy(p->d_dmask, dm.data(), sizeof(uint32_t) * (size_t)nw, hipMemcpyHostToDevice) ==
            hipSuccess &&
-       hipMemcpy(p->d_smask, sm.data(), sizeof(uint32_t) * 4, hipMemcpyHostToDevice) ==
+       hipMemcpy(p->d_smask, sm.data(), sizeof(uint32_t) * (size_t)snw, hipMemcpyHostToDevice) ==
            hipSuccess &&
        hipMemcpy(p->d_dsign16, ds.data(), sizeof(uint32_t) * (size_t)npairs,
                  hipMemcpyHostToDevice) == hipSuccess;
@@ -413,7 +424,7 @@ static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t 
     }
     return HQ_OK;
   }
-  const int32_t spw = encode_spw(nsub, allow_small);
+  const int32_t spw = p->tile != HQ_TILE ? HQ_ENC_SUBS_PER_WAVE : encode_spw(nsub, allow_small);
   const int64_t nwg = (nsub + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
   if (nwg > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
   if ((size_t)s->scan_bytes < hq_scan_bytes(p, rows)) return HQ_ERR_CAPACITY;
@@ -451,6 +462,7 @@ static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t 
   a.dither_seed = p->dither_seed;
   a.alpha = p->alpha;
   a.alpha_half = 0.5f * p->alpha;
+  a.tile = p->tile;
   *nwg_out = nwg;
   return HQ_OK;
 }
@@ -504,7 +516,8 @@ hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t 
   if (count < 0 || (count > 0 && (!plans || !x || !rows || !ld || !s))) return HQ_ERR_INVALID_ARG;
   for (int32_t i = 0; i < count; ++i) {
     if (!plans[i] || !s[i] || !same_kernel_family(plans[0], plans[i])) return HQ_ERR_INVALID_ARG;
-    if (plans[i]->rotation == HQ_ROT_QJL) return HQ_ERR_UNSUPPORTED;  // single calls only
+    if (plans[i]->rotation == HQ_ROT_QJL || plans[i]->tile != HQ_TILE)
+      return HQ_ERR_UNSUPPORTED;  // single calls only
     for (int32_t j = 0; j < i; ++j)
       if (s[j] == s[i] || s[j]->scan == s[i]->scan) return HQ_ERR_INVALID_ARG;
   }
@@ -561,6 +574,7 @@ static void fill_decode_args(const hq_plan_s* p, const hq_stream* s, int64_t row
   a->dither_seed = p->dither_seed;
   a->alpha = p->alpha;
   a->alpha_n = p->alpha * (float)p->tile;
+  a->tile = p->tile;
 }
 
 hq_status hq_decode(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows, void* y,
@@ -588,7 +602,7 @@ hq_status hq_decode_gemv(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t 
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if ((xt != HQ_BF16 && xt != HQ_FP32) || (yt != HQ_BF16 && yt != HQ_FP32)) return HQ_ERR_INVALID_ARG;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
-  if (p->rotation || p->dither) return HQ_ERR_UNSUPPORTED;
+  if (p->rotation || p->dither || p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;
   if (rows == 0) return HQ_OK;
   if (!x || !y || !workspace || !s->payload || !s->offsets || !s->kparam || !s->norms)
     return HQ_ERR_INVALID_ARG;
@@ -695,7 +709,8 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
   for (int32_t i = 0; i < count; ++i)
     if (!plans[i] || !s[i] || !same_kernel_family(plans[0], plans[i])) return HQ_ERR_INVALID_ARG;
   for (int32_t i = 0; i < count; ++i)
-    if (plans[i]->rotation == HQ_ROT_QJL) return HQ_ERR_UNSUPPORTED;  // single calls only
+    if (plans[i]->rotation == HQ_ROT_QJL || plans[i]->tile != HQ_TILE)
+      return HQ_ERR_UNSUPPORTED;  // single calls only
   const int64_t esz = (yt == HQ_BF16) ? 2 : 4;
   for (int32_t b = 0; b < count; b += HQ_GROUP_MAX) {
     hq_decode_group_args g;
@@ -730,6 +745,7 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
 
 hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                          int8_t* codes, int64_t ldc, float* g, void* stream) {
+  if (p && p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;  // the GEMM's K tiles are 128
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
@@ -746,6 +762,7 @@ hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t 
 
 hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                         uint8_t* codes, int64_t ldc, float* g, void* stream) {
+  if (p && p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;  // the GEMM's K tiles are 128
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
@@ -763,6 +780,7 @@ hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t r
 static hq_status act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t* xq,
                           float* sx, int fp8, void* stream) {
   if (!p || M < 0) return HQ_ERR_INVALID_ARG;
+  if (p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;
   if (M == 0) return HQ_OK;
   if (!a || !xq || !sx || lda < p->cols || !aligned16(a) || (lda * 2) % 16 != 0 ||
       ((uintptr_t)xq & 3u) != 0)
@@ -794,6 +812,7 @@ static hq_status gemm_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx
                                   const int8_t* codes, const float* g, int64_t N, void* out,
                                   int32_t ot, int fp8, void* stream) {
   if (!p || M < 0 || N < 0) return HQ_ERR_INVALID_ARG;
+  if (p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;
   if (ot != HQ_BF16 && ot != HQ_FP32) return HQ_ERR_INVALID_ARG;
   if (M == 0 || N == 0) return HQ_OK;
   if (!xq || !sx || !codes || !g || !out) return HQ_ERR_INVALID_ARG;

@@ -8,7 +8,8 @@
 #include "../../include/hq.h"
 
 #define HQ_KMAX 15
-#define HQ_TILE 128              // tile length the kernels are built for
+#define HQ_TILE 128              // tile length of the fused and GEMM kernels
+#define HQ_TILE_MAX 2048         // longest tile of the codec kernels (four sub-streams)
 #define HQ_SUB 512               // symbols per sub-stream the kernels are built for
 #define HQ_WAVES_PER_WG 4        // wave64s per workgroup
 #define HQ_ENC_SUBS_PER_WAVE 4   // encode: sub-streams per wave, one after another
@@ -69,6 +70,7 @@ struct hq_encode_args {
   int32_t rotation, dither, norm_fp16;
   uint32_t lds_words;     // per-sub-stream assembly buffer, in words
   uint32_t spw;           // sub-streams per wave: HQ_ENC_SUBS_PER_WAVE, or 1 for small launches
+  int32_t tile;           // RHT tile (128, or 256 .. 2048 for weight plans)
   uint64_t dither_seed;
   float alpha;
   float alpha_half;       // alpha / 2, exact (the E8 decision works on z / 2)
@@ -104,6 +106,7 @@ struct hq_decode_args {
   uint64_t dither_seed;
   float alpha;
   float alpha_n;           // alpha * tile, exact
+  int32_t tile;            // RHT tile (128, or 256 .. 2048 for weight plans)
   const float* qjl;        // qjl rotation: S (row-major) and S^T, or null
   const float* qjlt;
 };

@@ -703,6 +703,16 @@ __device__ __forceinline__ float swz_xor4(float v) {
   return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x101F));
 }
 
+// Value of lane l ^ 16 (the same mode with xor 16) and of lane l ^ 32.
+__device__ __forceinline__ float swz_xor16(float v) {
+  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));
+}
+__device__ __forceinline__ float lane_xor32(float v) {
+  return __int_as_float(__shfl_xor(__float_as_int(v), 32, 64));
+}
+
+
+
 // Value of lane l ^ M for M = 1, 2, 8 (bound_ctrl DPP moves, which fold into
 // the consuming VOP2 instruction).
 template <int M>
@@ -736,6 +746,59 @@ __device__ __forceinline__ void fwht128_tw(float* v, const TwSigns& sg) {
 #pragma unroll
   for (int j = 0; j < 8; ++j) v[j] = __builtin_fmaf(swz_xor4(v[j]), sg.f[2], v[j]);
   HQ_FMAC_DPP8("row_ror:8", v, sg.f[3]);
+}
+
+// Tiles longer than 128 (Sec. 7.2 sweeps 128 .. 2048).  A wave holds four
+// consecutive sub-streams of 512 scalars, lane l coordinates 8 l .. 8 l + 7
+// of each, so a tile of n <= 512 spans n / 8 lanes of one sub-stream and a
+// longer one spans n / 512 whole sub-streams of the wave.  The transform's
+// stages h = 128 and 256 pair lanes l ^ 16 and l ^ 32 (twisted as the
+// h = 8 .. 64 stages, which multiplies sigma by the two lane signs); the
+// stages h = 512 and 1024 pair sub-streams i ^ 1 and i ^ 2 of the same lane,
+// plain butterflies (both operands carry the lane's sigma).  Returns the
+// sign bit of the lane's sigma.
+__device__ __forceinline__ uint32_t fwht_tiled(float (*x)[8], int lane, uint32_t tile,
+                                               const TwSigns& sg) {
+  uint32_t sigma = sg.sigma;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) fwht128_tw(x[i], sg);
+  if (tile >= 256u) {
+    const float s4 = (lane & 16) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[i][j] = __builtin_fmaf(swz_xor16(x[i][j]), s4, x[i][j]);
+    sigma ^= (uint32_t)(lane & 16) << 27;
+  }
+  if (tile >= 512u) {
+    const float s5 = (lane & 32) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[i][j] = __builtin_fmaf(lane_xor32(x[i][j]), s5, x[i][j]);
+    sigma ^= (uint32_t)(lane & 32) << 26;
+  }
+  if (tile >= 1024u) {
+#pragma unroll
+    for (int i = 0; i < 4; i += 2)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float a = x[i][j], b = x[i + 1][j];
+        x[i][j] = a + b;
+        x[i + 1][j] = a - b;
+      }
+  }
+  if (tile >= 2048u) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float a = x[i][j], b = x[i + 2][j];
+        x[i][j] = a + b;
+        x[i + 2][j] = a - b;
+      }
+  }
+  return sigma;
 }
 
 __device__ __forceinline__ float xor_sign(float v, uint32_t bit) {
@@ -1310,10 +1373,14 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   overflow_out = overflow;
 }
 
-template <int LAT, int XT, bool KV, int SPW>
+// TILED: a plan whose tile is not 128 (weights only: no rotation or
+// dither); the wave takes four consecutive sub-streams, so that every tile
+// of up to 2048 scalars lies inside one wave.
+template <int LAT, int XT, bool KV, int SPW, bool TILED = false>
 __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice_thr& T,
                                           const uint32_t wg) {
   static_assert(SPW == 1 || SPW == 4, "one or four sub-streams per wave");
+  static_assert(!TILED || (SPW == 4 && !KV), "long tiles: four sub-streams per wave, weights");
   constexpr int NSUB = HQ_ENC_SUBS_PER_WG;  // sub-streams per workgroup
   constexpr int WAVES = NSUB / SPW;         // wave64s per workgroup
   extern __shared__ uint32_t smem[];
@@ -1334,27 +1401,87 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
   SubPos pos[SPW];
   {
     const uint32_t spr = (uint32_t)A.spr;
-    const uint32_t sub0 = wg * NSUB + (uint32_t)wave;
+    const uint32_t step = TILED ? 1u : (uint32_t)WAVES;
+    const uint32_t sub0 = wg * NSUB + (uint32_t)wave * (TILED ? (uint32_t)SPW : 1u);
     uint32_t row = sub0 / spr, c = sub0 - row * spr;
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
-      pos[i].active = sub0 + (uint32_t)(i * WAVES) < (uint32_t)A.nsub;
+      pos[i].active = sub0 + (uint32_t)i * step < (uint32_t)A.nsub;
       pos[i].lrow = pos[i].active ? row : 0u;
       pos[i].col0 = pos[i].active ? c * HQ_SUB : 0u;
-      c += WAVES;
+      c += step;
       while (c >= spr) {
         c -= spr;
         ++row;
       }
     }
   }
+  Packed<XT> pk[SPW];
+  float ss[SPW];
+  bool nonfinite = false;
+  float xt[TILED ? SPW : 1][8];  // long tiles: the transformed values of the wave
+  uint32_t tsig = 0;             // long tiles: the sign bit of the lane's sigma
+  if constexpr (TILED) {
+    // ---- long tiles: every load first, then each 128-block's sum of squares
+    //      (tree8 and the lane butterflies 1, 2, 4, 8), widened to the tile
+    //      by lanes l ^ 16, l ^ 32 and then across sub-streams, in the
+    //      pairwise tree's order
+    const uint32_t n = (uint32_t)A.tile;
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) unpack<XT>(pack_signed<XT>(load_lane_input<XT>(A, pos[i], lane)), xt[i]);
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      float sq[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) sq[j] = xt[i][j] * xt[i][j];
+      float v = tree8(sq);
+      v = v + dpp_xor<1>(v);
+      v = v + dpp_xor<2>(v);
+      v = v + swz_xor4(v);
+      v = v + dpp_xor<8>(v);
+      if (n >= 256u) v = v + swz_xor16(v);
+      if (n >= 512u) v = v + lane_xor32(v);
+      ss[i] = v;
+    }
+    if (n >= 1024u) {
+      const float a = ss[0] + ss[1], b = ss[2] + ss[3];
+      ss[0] = a; ss[1] = a; ss[2] = b; ss[3] = b;
+    }
+    if (n >= 2048u) {
+      const float a = ss[0] + ss[2];
+      ss[0] = a; ss[1] = a; ss[2] = a; ss[3] = a;
+    }
+    // ---- norms and scales: every lane its own tile's; the lane holding a
+    //      tile's first coordinate stores the norm
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const float r = __builtin_sqrtf(ss[i]);
+      const bool bad = !(r <= 3.0e38f);  // an infinite or NaN input
+      nonfinite = nonfinite || bad;
+      ss[i] = (r == 0.0f || bad) ? 0.0f : (LAT == kE8 ? A.alpha_half : A.alpha) / r;
+      const uint32_t sub = wg * NSUB + (uint32_t)(wave * SPW + i);
+      const uint64_t flat = (uint64_t)sub * HQ_SUB + 8u * (uint32_t)lane;
+      if (pos[i].active && (flat & (n - 1u)) == 0u) {
+        ((float*)A.norms)[A.first_row * A.tpr + (int64_t)(flat / n)] = r;
+        if (bad && A.stats) {
+          atomicAdd(&A.stats->overflow_tiles, 1u);
+          atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_OVERFLOW);
+        }
+      }
+    }
+    if (__ballot(nonfinite) != 0ull) {
+#pragma unroll
+      for (int i = 0; i < SPW; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) xt[i][j] = ss[i] == 0.0f ? 0.0f : xt[i][j];
+    }
+    tsig = fwht_tiled(xt, lane, n, sg);
+  } else {
   // ---- every input load of the wave's sub-streams is issued first; each is
   //      kept packed with its signs applied, and its tile sums of squares
   //      taken (the transforms wait until each sub-stream is coded)
-  Packed<XT> pk[SPW];
 #pragma unroll
   for (int i = 0; i < SPW; ++i) pk[i] = pack_signed<XT>(load_lane_input<XT>(A, pos[i], lane));
-  float ss[SPW];
 #pragma unroll
   for (int i = 0; i < SPW; ++i) ss[i] = tile_sumsq<XT>(pk[i]);
 
@@ -1362,7 +1489,6 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
   //      sub-streams lane l takes sub-stream i = l & 3, tile t = l >> 4 (each
   //      tile's 16 lanes hold its sum of squares, so the merged value repeats
   //      in every quad); with one, every lane takes its own tile l >> 4
-  bool nonfinite;
   {
     const int qi = SPW == 4 ? (lane & 3) : 0;
     float ssm = ss[0];
@@ -1412,19 +1538,26 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
 #pragma unroll
       for (int j = 0; j < (XT == HQ_BF16 ? 4 : 8); ++j) pk[i].w[j] = ss[i] == 0.0f ? 0u : pk[i].w[j];
   }
+  }  // 128-tiles
 
   // ---- quantize and Rice-code each sub-stream into its LDS buffer
   uint32_t padsum = 0;
 #pragma unroll
   for (int i = 0; i < SPW; ++i) {
-    const int li = i * WAVES + wave;  // neighbouring waves take neighbouring sub-streams
+    // 128-tiles: neighbouring waves take neighbouring sub-streams
+    const int li = TILED ? wave * SPW + i : i * WAVES + wave;
     const uint32_t sub = wg * NSUB + (uint32_t)li;
     uint32_t W, kb, bits;
     bool ovf;
     float x[8];  // x <- sigma H D x
-    unpack<XT>(pk[i], x);
-    fwht128_tw(x, sg);
-    encode_substream<LAT, XT, KV>(A, T, pos[i], lane, x, xor_sign(ss[i], sg.sigma),
+    if constexpr (TILED) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = xt[i][j];
+    } else {
+      unpack<XT>(pk[i], x);
+      fwht128_tw(x, sg);
+    }
+    encode_substream<LAT, XT, KV>(A, T, pos[i], lane, x, xor_sign(ss[i], TILED ? tsig : sg.sigma),
                                   smem + li * stride,
                                   (float*)(smem + NSUB * stride) + wave * HQ_QJL_STAGE, W, kb,
                                   bits, ovf);
@@ -1559,6 +1692,12 @@ template <int LAT, int XT, bool KV, int SPW>
 __global__ __launch_bounds__(64 * HQ_ENC_SUBS_PER_WG / SPW) void hq_encode_kernel(hq_encode_args A,
                                                                                 hq_rice_thr T) {
   encode_wg<LAT, XT, KV, SPW>(A, T, blockIdx.x);
+}
+
+template <int LAT, int XT>
+__global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_tiled_kernel(hq_encode_args A,
+                                                                           hq_rice_thr T) {
+  encode_wg<LAT, XT, false, HQ_ENC_SUBS_PER_WAVE, true>(A, T, blockIdx.x);
 }
 
 // Several matrices in one launch: workgroups wg_begin[i] .. wg_begin[i+1]-1
@@ -1921,6 +2060,99 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
     }
     if (i + 1 < HQ_DEC_SUBS_PER_WAVE) head = next;
   }
+}
+
+// Long tiles (weights, bf16 or fp32 out): the wave's four consecutive
+// sub-streams are decoded first and kept as lattice coordinates, then the
+// tiles they form are transformed together (fwht_tiled) and denormalized.
+// A corrupt sub-stream's codes count as zeros in its tile.
+template <int LAT, int MODE>
+__device__ __forceinline__ void decode_wg_tiled(const hq_decode_args& A, const uint32_t wgi) {
+  extern __shared__ uint32_t smem[];
+  __shared__ uint32_t s_sel[256];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint32_t wave = readfirst((uint32_t)(tid >> 6));
+  uint32_t* buf = smem + wave * (A.lds_words + 66);
+  uint32_t* starts = buf + A.lds_words + 2;
+  s_sel[tid] = byte_select_entry((uint32_t)tid);  // 256 threads, one entry each
+  __syncthreads();
+
+  const uint32_t sub0 = (wgi * HQ_WAVES_PER_WG + wave) * HQ_DEC_SUBS_PER_WAVE;
+  const uint32_t nsub = (uint32_t)A.nsub;
+  const uint32_t n = (uint32_t)A.tile;
+  uint32_t off[HQ_DEC_SUBS_PER_WAVE + 1], kbs[HQ_DEC_SUBS_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i <= HQ_DEC_SUBS_PER_WAVE; ++i) {
+    const uint32_t sub = sub0 + (uint32_t)i;
+    off[i] = sub <= nsub ? readfirst(A.offsets[(uint32_t)A.first_sub + sub]) : 0u;
+    if (i < HQ_DEC_SUBS_PER_WAVE)
+      kbs[i] = sub < nsub ? readfirst(A.kparam[(uint32_t)A.first_sub + sub]) : 0u;
+  }
+  DecHead head = dec_head<LAT>(A, sub0 < nsub, off[0], off[1], kbs[0], lane);
+  const uint32_t spr = (uint32_t)A.spr;
+  const TwSigns sg(lane);
+  float y[HQ_DEC_SUBS_PER_WAVE][8];
+#pragma unroll
+  for (int i = 0; i < HQ_DEC_SUBS_PER_WAVE; ++i) {
+    const uint32_t sub = sub0 + (uint32_t)i;
+    DecHead next;
+    if (i + 1 < HQ_DEC_SUBS_PER_WAVE)
+      next = dec_head<LAT>(A, sub + 1 < nsub, off[i + 1], off[i + 2], kbs[i + 1], lane);
+    if (sub < nsub) {
+      uint32_t sym[8];
+      const bool ok = decode_symbols<LAT>(A, head, lane, buf, starts, s_sel, sym);
+      const unsigned long long bad = __ballot(!ok);
+      if (bad && A.stats && (unsigned)lane == (unsigned)__builtin_ctzll(bad)) {
+        atomicAdd(&A.stats->corrupt_substreams, 1u);
+        atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+      }
+      int32_t c[8];
+      unstrip8<LAT>(sym, c);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[i][j] = code_coord<LAT>(c[j], j);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[i][j] = 0.0f;
+    }
+    if (i + 1 < HQ_DEC_SUBS_PER_WAVE) head = next;
+  }
+  // y = D H^T code * r / (alpha n): the tiles' transforms, then each lane
+  // its own tile's factor
+  const uint32_t sigma = fwht_tiled(y, lane, n, sg);
+#pragma unroll
+  for (int i = 0; i < HQ_DEC_SUBS_PER_WAVE; ++i) {
+    const uint32_t sub = sub0 + (uint32_t)i;
+    if (sub >= nsub) break;
+    const uint32_t lrow = sub / spr;
+    const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
+    const uint64_t flat = (uint64_t)sub * HQ_SUB + 8u * (uint32_t)lane;
+    const float rs = ((const float*)A.norms)[A.first_row * A.tpr + (int64_t)(flat / n)];
+    const float g_tw = xor_sign(rs / A.alpha_n, sigma);
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = y[i][j] * g_tw;
+    if constexpr (MODE == 0) {
+      const uint32_t dbits = sign_bits8(A.dmask, col);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = flip(v[j], dbits, j);
+      float4* out = (float4*)((float*)A.y + (int64_t)lrow * A.ld + col);
+      out[0] = make_float4(v[0], v[1], v[2], v[3]);
+      out[1] = make_float4(v[4], v[5], v[6], v[7]);
+    } else {
+      const uint4 sw = *(const uint4*)(A.dsign16 + (col >> 1));
+      uint4 o;
+      o.x = cvt_pk_bf16(v[0], v[1]) ^ sw.x;
+      o.y = cvt_pk_bf16(v[2], v[3]) ^ sw.y;
+      o.z = cvt_pk_bf16(v[4], v[5]) ^ sw.z;
+      o.w = cvt_pk_bf16(v[6], v[7]) ^ sw.w;
+      *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = o;
+    }
+  }
+}
+
+template <int LAT, int MODE>
+__global__ __launch_bounds__(256) void hq_decode_tiled_kernel(hq_decode_args A) {
+  decode_wg_tiled<LAT, MODE>(A, blockIdx.x);
 }
 
 template <int LAT, int MODE, bool KV>
@@ -2904,6 +3136,37 @@ int launch_decode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int mode,
   return (int)hipGetLastError();
 }
 
+// Long tiles (weight plans): four consecutive sub-streams per wave.
+template <int LAT>
+int launch_encode_tiled(const hq_encode_args& a, const hq_rice_thr& t, int xt, hipStream_t st) {
+  const size_t lds = (size_t)(a.lds_words + 2) * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
+  static size_t granted_b = 0, granted_f = 0;
+  if (xt == HQ_BF16) {
+    allow_lds((const void*)hq_encode_tiled_kernel<LAT, HQ_BF16>, lds, granted_b);
+    hipLaunchKernelGGL((hq_encode_tiled_kernel<LAT, HQ_BF16>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES),
+                       lds, st, a, t);
+  } else {
+    allow_lds((const void*)hq_encode_tiled_kernel<LAT, HQ_FP32>, lds, granted_f);
+    hipLaunchKernelGGL((hq_encode_tiled_kernel<LAT, HQ_FP32>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES),
+                       lds, st, a, t);
+  }
+  return (int)hipGetLastError();
+}
+
+template <int LAT>
+int launch_decode_tiled(const hq_decode_args& a, uint32_t nwg, int mode, hipStream_t st) {
+  const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
+  static size_t granted_0 = 0, granted_1 = 0;
+  if (mode == 0) {
+    allow_lds((const void*)hq_decode_tiled_kernel<LAT, 0>, lds, granted_0);
+    hipLaunchKernelGGL((hq_decode_tiled_kernel<LAT, 0>), dim3(nwg), dim3(256), lds, st, a);
+  } else {
+    allow_lds((const void*)hq_decode_tiled_kernel<LAT, 1>, lds, granted_1);
+    hipLaunchKernelGGL((hq_decode_tiled_kernel<LAT, 1>), dim3(nwg), dim3(256), lds, st, a);
+  }
+  return (int)hipGetLastError();
+}
+
 }  // namespace
 
 static bool kv_variant(const hq_plan_s* p) { return p->rotation || p->dither || p->norm_fp16; }
@@ -2911,6 +3174,14 @@ static bool kv_variant(const hq_plan_s* p) { return p->rotation || p->dither || 
 int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, const hq_rice_thr& t, int xt,
                      void* stream) {
   hipStream_t st = (hipStream_t)stream;
+  if (p->tile != HQ_TILE) {
+    switch (p->lattice) {
+      case HQ_E8: return launch_encode_tiled<kE8>(a, t, xt, st);
+      case HQ_D4: return launch_encode_tiled<kD4>(a, t, xt, st);
+      case HQ_A2: return launch_encode_tiled<kA2>(a, t, xt, st);
+      default: return launch_encode_tiled<kZ>(a, t, xt, st);
+    }
+  }
   const bool kv = kv_variant(p);
   const uint32_t lw = a.lds_words;
   switch (p->lattice) {
@@ -2943,6 +3214,14 @@ int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* 
   const int mode = (yt == HQ_FP32) ? 0 : 1;
   const bool kv = kv_variant(p);
   const uint32_t nwg = decode_wgs(a.nsub), lw = a.lds_words;
+  if (p->tile != HQ_TILE) {
+    switch (p->lattice) {
+      case HQ_E8: return launch_decode_tiled<kE8>(a, nwg, mode, st);
+      case HQ_D4: return launch_decode_tiled<kD4>(a, nwg, mode, st);
+      case HQ_A2: return launch_decode_tiled<kA2>(a, nwg, mode, st);
+      default: return launch_decode_tiled<kZ>(a, nwg, mode, st);
+    }
+  }
   switch (p->lattice) {
     case HQ_E8: return launch_decode_lat<kE8>(a, nwg, lw, mode, kv, st);
     case HQ_D4: return launch_decode_lat<kD4>(a, nwg, lw, mode, kv, st);

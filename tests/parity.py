@@ -21,14 +21,14 @@ def op_snr(name, bps):
 
 
 def oracle_params(lat, snr, rht_seed=0, rice_k=-1, rotation=0, rot_seed=0, dither=False,
-                  dither_seed=0, norm_fp16=False, qjl=None):
-    return O.Params(tile=128, lattice=lat, alpha=O.alpha(lat, snr), substream=512, rice_k=rice_k,
+                  dither_seed=0, norm_fp16=False, qjl=None, tile=128):
+    return O.Params(tile=tile, lattice=lat, alpha=O.alpha(lat, snr), substream=512, rice_k=rice_k,
                     norm_fp16=norm_fp16, rht_seed=rht_seed, rotation=rotation, dither=dither,
                     rot_seed=rot_seed, dither_seed=dither_seed, qjl=qjl)
 
 
 def gpu_plan(hq, P: O.Params, snr, cols):
-    plan = hq.hq_plan(128, P.lattice, 0.0, P.rht_seed, P.rice_k, cols, rotation=P.rotation,
+    plan = hq.hq_plan(P.tile, P.lattice, 0.0, P.rht_seed, P.rice_k, cols, rotation=P.rotation,
                       dither=P.dither, rot_seed=P.rot_seed, dither_seed=P.dither_seed,
                       norm_fp16=P.norm_fp16, snr_db=snr, qjl=P.qjl)
     assert np.float32(plan.info.alpha) == np.float32(P.alpha), "alpha differs from the oracle's"

@@ -54,10 +54,17 @@ def test_plan_argument_errors_are_synchronous(hq):
     assert L.hq_plan(128, 0, 4.0, 0, -1, 4000, C.byref(o), C.byref(h), C.byref(info)) == -1
     assert L.hq_plan(128, 7, 4.0, 0, -1, 4096, C.byref(o), C.byref(h), C.byref(info)) == -1
     assert L.hq_plan(128, 0, 4.0, 0, 16, 4096, C.byref(o), C.byref(h), C.byref(info)) == -1
-    # valid for the method, not built here: other tile sizes / sub-stream lengths
-    assert L.hq_plan(256, 0, 4.0, 0, -1, 4096, C.byref(o), C.byref(h), C.byref(info)) == -2
+    # valid for the method, not built here: tiles past 2048, long tiles with a
+    # KV option (rotation, dither, fp16 norms), other sub-stream lengths
+    assert L.hq_plan(4096, 0, 4.0, 0, -1, 8192, C.byref(o), C.byref(h), C.byref(info)) == -2
+    for rot, dith, nd in ((1, 0, 0), (0, 1, 0), (0, 0, 2)):
+        ok = hq.Options(rot, dith, 0, 0, nd, 0, 1, 0, 20.0)
+        assert L.hq_plan(256, 0, 4.0, 0, -1, 4096, C.byref(ok), C.byref(h), C.byref(info)) == -2
     o2 = hq.Options(0, 0, 0, 0, 0, 1024, 1, 0, 20.0)
     assert L.hq_plan(128, 0, 4.0, 0, -1, 4096, C.byref(o2), C.byref(h), C.byref(info)) == -2
+    # a sub-stream length that neither holds whole tiles nor divides one
+    o3 = hq.Options(0, 0, 0, 0, 0, 768, 1, 0, 20.0)
+    assert L.hq_plan(1024, 0, 4.0, 0, -1, 6144, C.byref(o3), C.byref(h), C.byref(info)) == -1
     # null output handle
     assert L.hq_plan(128, 0, 4.0, 0, -1, 4096, C.byref(o), None, None) == -1
 
@@ -114,3 +121,30 @@ def test_fused_entry_points_reject_null_plans(hq):
     assert L.hq_decode_gemv(None, None, 0, 1, None, 0, None, 0, None, 0, None) == -1
     assert L.hq_decode_attention(None, None, None, None, None, 0, 1, 8, C.c_float(0.1), None, 1, 16,
                                  None, None, None, 0, 0, None, 0, None, 0, None) == -1
+
+
+def test_long_tile_plans_keep_the_heap_intact(hq):
+    # Regression: the rotation sign mask was built over the whole tile into a
+    # four-word buffer, so a 256..2048-tile plan wrote past it.  glibc's heap
+    # checks (MALLOC_CHECK_=3) abort a process whose heap was overrun; plans
+    # of every long tile are made in a child process with them on (without a
+    # GPU hq_plan returns HQ_ERR_HIP after its host work, which is the part
+    # under test).
+    import subprocess
+    import sys
+    code = (
+        "import ctypes as C, sys\n"
+        f"sys.path.insert(0, {ROOT!r})\n"
+        "from paper_2606_23406_amd import hq\n"
+        "L = hq.lib()\n"
+        "for t in (256, 512, 1024, 2048, 2048, 1024):\n"
+        "    o = hq.Options(0, 0, 0, 0, 0, 0, 1, 0, 20.0)\n"
+        "    h = C.c_void_p(); info = hq.PlanInfo()\n"
+        "    rc = L.hq_plan(t, 0, 4.0, 0, -1, 8192, C.byref(o), C.byref(h), C.byref(info))\n"
+        "    assert rc in (0, -5), rc\n"
+        "    if rc == 0: L.hq_plan_destroy(h)\n"
+        "    junk = [bytearray(64) for _ in range(2000)]\n"
+        "print('heap ok')\n")
+    env = dict(os.environ, MALLOC_CHECK_="3", HIP_VISIBLE_DEVICES=os.environ.get("HIP_VISIBLE_DEVICES", ""))
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, timeout=120)
+    assert r.returncode == 0 and "heap ok" in r.stdout, r.stdout + r.stderr

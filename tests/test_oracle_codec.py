@@ -416,3 +416,39 @@ def test_decode_gemv_equals_transform_on_x(lat):
     e[300] = 1.0
     assert np.array_equal(O.decode_gemv(P, codes, norms, e),
                           O.backend(P, codes, norms)[:, 300].astype(np.float64))
+
+
+@pytest.mark.parametrize("bps", [3.0, 4.0])
+def test_rate_across_rht_tiles(bps):
+    # Sec. 7.2 (RHT tile size): with the SNR calibrated once and held fixed,
+    # the realized rate stays within about 0.01 bps of target for tiles of
+    # 128 .. 2048, larger tiles coding marginally fewer bits.  Tiles above
+    # the 512-symbol sub-stream span several sub-streams.
+    x = gauss(8192).reshape(-1, 2048)
+    snr = op_point("E8", bps)
+    rates = {}
+    for tile in (128, 256, 512, 1024, 2048):
+        P = O.Params(tile=tile, lattice=O.E8, alpha=O.alpha(O.E8, snr))
+        st = O.encode(P, x)
+        rates[tile] = st.payload_bits / x.size
+        y = O.decode(P, st)
+        assert abs(snr_db(x, y) - snr) < 0.1
+    for tile, r in rates.items():
+        assert abs(r - bps) < 0.02, rates
+    assert rates[2048] <= rates[128] + 0.002, rates
+
+
+def test_tile_of_several_substreams_round_trips():
+    # A 1024-tile over 512-symbol sub-streams: each sub-stream is half a tile;
+    # the stream decodes losslessly to the codes and the sub-stream table is
+    # the same as a 512-symbol chunking of the row-major symbols.
+    x = gauss(2048).reshape(-1, 2048)
+    P = O.Params(tile=1024, lattice=O.E8, alpha=O.alpha(O.E8, 22.0), rht_seed=6)
+    codes, norms, _, _ = O.frontend(P, x)
+    st = O.encode(P, x)
+    back, rc = O.unpack(P, st.payload, st.offsets, st.kparam, x.shape[0], x.shape[1])
+    assert rc == O.OK and np.array_equal(back, codes)
+    assert norms.shape == (x.shape[0], 2)
+    # a sub-stream length that neither holds whole tiles nor divides one
+    with pytest.raises(ValueError):
+        O.frontend(O.Params(tile=512, lattice=O.E8, alpha=1.0, substream=768), x[:, :1536])
