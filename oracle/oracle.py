@@ -563,3 +563,93 @@ def gemm_fp8_blockscaled(w8, g, x8, sx, tile):
         ks = slice(t * tile, (t + 1) * tile)
         out += (x[:, ks] @ w[:, ks].T) * np.asarray(g, np.float64)[:, t][None, :]
     return out * np.asarray(sx, np.float64)[:, None]
+
+
+# ---------------------------------------------------------------- MXFP4 cast (Sec. 4.8, 6.4)
+# OCP Microscaling MXFP4: blocks of 32 consecutive values (along K) share one
+# E8M0 scale 2^X, stored as the byte X + 127; each element is FP4 E2M1 --
+# sign, 2 exponent bits (bias 1), 1 fraction bit -- with magnitudes 0, 0.5,
+# 1, 1.5, 2, 3, 4, 6 (codes 0 .. 7; exponent 0 is the subnormal 0.5).  The
+# MX conversion takes X = floor(log2(amax)) - 2 (2: E2M1's largest exponent)
+# and each element E2M1(v / 2^X), nearest value with ties to the even code,
+# magnitudes above 6 saturating to 6.  An all-zero block takes X = -127.
+
+MX_BLOCK = 32
+_E2M1 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def e2m1_bits(x):
+    """Nearest E2M1 value of each x (ties to the even code, saturation at 6,
+    sign kept: a negative value that rounds to zero gives -0, code 8)."""
+    x = np.asarray(x, dtype=np.float64)
+    a = np.minimum(np.abs(x), 6.0)
+    hi = np.clip(np.searchsorted(_E2M1, a), 0, 7)
+    lo = np.maximum(hi - 1, 0)
+    dlo, dhi = a - _E2M1[lo], _E2M1[hi] - a
+    pick_hi = (dhi < dlo) | ((dhi == dlo) & (hi % 2 == 0))
+    code = np.where(pick_hi, hi, lo).astype(np.uint8)
+    return (code | np.where(np.signbit(x), 8, 0).astype(np.uint8)).astype(np.uint8)
+
+
+def e2m1_value(bits):
+    bits = np.asarray(bits, dtype=np.uint8)
+    v = _E2M1[bits & 7]
+    return np.where(bits & 8, -v, v)
+
+
+def mx_scale_exponent(amax):
+    """X = floor(log2(amax)) - 2 per block (exact, from the binary exponent),
+    clamped to E8M0's range [-127, 127]; -127 for an all-zero block."""
+    amax = np.asarray(amax, dtype=np.float64)
+    _, e = np.frexp(amax)  # amax = m 2^e, m in [0.5, 1)
+    x = np.where(amax > 0, e - 1 - 2, -127)
+    return np.clip(x, -127, 127).astype(np.int32)
+
+
+def mxfp4_cast(v):
+    """MXFP4 of a [rows, K] array along K: E2M1 codes (one per byte, low
+    nibble) and the blocks' E8M0 scale bytes [rows, K / 32]."""
+    v = np.asarray(v, dtype=np.float64)
+    rows, K = v.shape
+    b = v.reshape(rows, K // MX_BLOCK, MX_BLOCK)
+    X = mx_scale_exponent(np.abs(b).max(axis=2))
+    codes = e2m1_bits(b / np.ldexp(1.0, X)[:, :, None]).reshape(rows, K)
+    return codes, (X + 127).astype(np.uint8)
+
+
+def mxfp4_value(codes, scales):
+    """The values an MXFP4 array stands for: E2M1 value times 2^X per block."""
+    c = e2m1_value(codes)
+    rows, K = c.shape
+    X = np.asarray(scales, dtype=np.int32) - 127
+    return (c.reshape(rows, K // MX_BLOCK, MX_BLOCK) * np.ldexp(1.0, X)[:, :, None]).reshape(rows, K)
+
+
+def weight_codes_mxfp4(codes):
+    """The MXFP4 cast of the weight side: the lattice codes, 32 along K per
+    block (the per-tile factors g stay as in the int8 path)."""
+    return mxfp4_cast(np.asarray(codes, dtype=np.float64))
+
+
+def act_prep_mxfp4(a, tile, rht_seed):
+    """Activation side in MXFP4: per K-tile y = H D a (fp32, the weights'
+    signs), then the MX cast of y per 32 values; the block scales carry the
+    magnitude, so there is no per-token factor."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    M, K = a.shape
+    y = (a * signs(rht_seed, K).astype(np.float32)).reshape(M, K // tile, tile)
+    y = fwht(y.astype(np.float32)).reshape(M, K)
+    return mxfp4_cast(y)
+
+
+def gemm_mxfp4_blockscaled(w4, ws, g, x4, xs, tile):
+    """out[m, n] = sum_t g[n, t] sum_{k in t} X[m, k] W[n, k] over the MXFP4
+    values (element times block scale), in fp64."""
+    W = mxfp4_value(w4, ws)
+    X = mxfp4_value(x4, xs)
+    N, K = W.shape
+    out = np.zeros((X.shape[0], N))
+    for t in range(K // tile):
+        ks = slice(t * tile, (t + 1) * tile)
+        out += (X[:, ks] @ W[:, ks].T) * np.asarray(g, np.float64)[:, t][None, :]
+    return out
