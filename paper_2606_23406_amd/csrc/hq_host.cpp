@@ -777,13 +777,30 @@ hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t r
   return hip_status(hq_launch_decode_fp8(p, a, stream));
 }
 
+hq_status hq_decode_mxfp4(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
+                          uint8_t* codes, uint8_t* scales, float* g, void* stream) {
+  if (p && p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;  // the GEMM's K tiles are 128
+  if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
+  if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
+  if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
+  if (rows == 0) return HQ_OK;
+  if (!codes || !scales || !g || ((uintptr_t)codes & 3u) != 0) return HQ_ERR_INVALID_ARG;
+  hq_decode_args a;
+  fill_decode_args(p, s, row0, rows, &a);
+  a.y = codes;
+  a.ld = p->cols / 2;  // contiguous rows of cols / 2 bytes
+  a.g = g;
+  a.mxs = scales;
+  return hip_status(hq_launch_decode_mxfp4(p, a, stream));
+}
+
 static hq_status act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t* xq,
-                          float* sx, int fp8, void* stream) {
+                          float* sx, int fp8, void* stream, uint8_t* mxs = nullptr) {
   if (!p || M < 0) return HQ_ERR_INVALID_ARG;
   if (p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;
   if (M == 0) return HQ_OK;
-  if (!a || !xq || !sx || lda < p->cols || !aligned16(a) || (lda * 2) % 16 != 0 ||
-      ((uintptr_t)xq & 3u) != 0)
+  if (!a || !xq || (fp8 == 2 ? !mxs : !sx) || lda < p->cols || !aligned16(a) ||
+      (lda * 2) % 16 != 0 || ((uintptr_t)xq & 3u) != 0)
     return HQ_ERR_INVALID_ARG;
   if (p->cols > 16384 || M > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
   hq_actprep_args args;
@@ -795,7 +812,13 @@ static hq_status act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, in
   args.sx = sx;
   args.dmask = p->d_dmask;
   args.fp8 = fp8;
+  args.mxs = mxs;
   return hip_status(hq_launch_act_prep(args, stream));
+}
+
+hq_status hq_act_prep_mxfp4(hq_plan_t p, const void* a, int64_t M, int64_t lda, uint8_t* xq,
+                            uint8_t* scales, void* stream) {
+  return act_prep(p, a, M, lda, (int8_t*)xq, nullptr, 2, stream, scales);
 }
 
 hq_status hq_act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t* xq, float* sx,
@@ -810,12 +833,14 @@ hq_status hq_act_prep_fp8(hq_plan_t p, const void* a, int64_t M, int64_t lda, ui
 
 static hq_status gemm_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx, int64_t M,
                                   const int8_t* codes, const float* g, int64_t N, void* out,
-                                  int32_t ot, int fp8, void* stream) {
+                                  int32_t ot, int fp8, void* stream, const uint8_t* xs = nullptr,
+                                  const uint8_t* ws = nullptr) {
   if (!p || M < 0 || N < 0) return HQ_ERR_INVALID_ARG;
   if (p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;
   if (ot != HQ_BF16 && ot != HQ_FP32) return HQ_ERR_INVALID_ARG;
   if (M == 0 || N == 0) return HQ_OK;
-  if (!xq || !sx || !codes || !g || !out) return HQ_ERR_INVALID_ARG;
+  if (!xq || (fp8 == 2 ? (!xs || !ws) : !sx) || !codes || !g || !out) return HQ_ERR_INVALID_ARG;
+  if (fp8 == 2 && (((uintptr_t)xs & 7u) != 0 || ((uintptr_t)ws & 7u) != 0)) return HQ_ERR_INVALID_ARG;
   if (!aligned16(xq) || !aligned16(codes) || !aligned16(out)) return HQ_ERR_INVALID_ARG;
   hq_gemm_args a;
   a.xq = xq;
@@ -828,6 +853,8 @@ static hq_status gemm_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx
   a.K = p->cols;
   a.out_bf16 = (ot == HQ_BF16) ? 1 : 0;
   a.fp8 = fp8;
+  a.xs = xs;
+  a.ws = ws;
   const int e = hq_launch_gemm(a, stream);
   if (e == -1) return HQ_ERR_UNSUPPORTED;
   return hip_status(e);
@@ -844,6 +871,13 @@ hq_status hq_gemm_fp8_blockscaled(hq_plan_t p, const uint8_t* xq, const float* s
                                   int32_t ot, void* stream) {
   return gemm_blockscaled(p, (const int8_t*)xq, sx, M, (const int8_t*)codes, g, N, out, ot, 1,
                           stream);
+}
+
+hq_status hq_gemm_mxfp4_blockscaled(hq_plan_t plan, const uint8_t* xq, const uint8_t* xs, int64_t M,
+                                    const uint8_t* codes, const uint8_t* ws, const float* g,
+                                    int64_t N, void* out, int32_t ot, void* stream) {
+  return gemm_blockscaled(plan, (const int8_t*)xq, nullptr, M, (const int8_t*)codes, g, N, out, ot,
+                          2, stream, xs, ws);
 }
 
 size_t hq_gemm_workspace_bytes(hq_plan_t p, int64_t M, int64_t N) {

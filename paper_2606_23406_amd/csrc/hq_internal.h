@@ -97,6 +97,7 @@ struct hq_decode_args {
   void* y;                 // decode: output rows; decode_int8: int8 codes
   int64_t ld;
   float* g;                // decode_int8: per-tile factors (rows x tpr)
+  uint8_t* mxs;            // decode_mxfp4: E8M0 scale bytes (rows x cols / 32)
   const uint32_t* dmask;
   const uint32_t* dsign16;  // RHT signs as bf16 XOR words, one per column pair
   const uint32_t* smask;
@@ -166,7 +167,9 @@ struct hq_actprep_args {
   int8_t* xq;             // int8, or E4M3 bytes when fp8
   float* sx;
   const uint32_t* dmask;
-  int32_t fp8;            // 1: E4M3 at 448 / amax instead of int8 at 127 / amax
+  int32_t fp8;            // 1: E4M3 at 448 / amax instead of int8 at 127 / amax;
+                          // 2: MXFP4 (E2M1 pairs per byte, E8M0 scale per 32 in mxs)
+  uint8_t* mxs;           // MXFP4: scale bytes (M x K / 32)
 };
 
 struct hq_gemm_args {
@@ -177,7 +180,10 @@ struct hq_gemm_args {
   void* out;          // M x N
   int64_t M, N, K;
   int32_t out_bf16;
-  int32_t fp8;        // 1: xq and w are E4M3 bytes (fp32 tile sums on the fp8 matrix cores)
+  int32_t fp8;        // 1: xq and w are E4M3 bytes (fp32 tile sums on the fp8 matrix cores);
+                      // 2: MXFP4 (E2M1 pairs per byte, rows of K / 2 bytes)
+  const uint8_t* xs;  // MXFP4: activation scale bytes (M x K / 32)
+  const uint8_t* ws;  // MXFP4: weight scale bytes (N x K / 32)
 };
 
 // Kernel launchers (hq_kernels.hip); return a hipError_t as int.
@@ -185,6 +191,7 @@ int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, const hq_rice_
                      void* stream);
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream);
 int hq_launch_decode_fp8(const hq_plan_s* p, const hq_decode_args& a, void* stream);
+int hq_launch_decode_mxfp4(const hq_plan_s* p, const hq_decode_args& a, void* stream);
 // Fused decode + GEMV: xtr (cols fp32) receives H D x per tile, then y (rows)
 // the decoded rows' products with x.
 int hq_launch_decode_attention(const hq_attn_args& a, int lattice, void* stream);

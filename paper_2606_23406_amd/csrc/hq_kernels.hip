@@ -553,6 +553,26 @@ __device__ __forceinline__ uint32_t e4m3x4(float a, float b, float c, float d) {
   return (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(c, d, lo, true);
 }
 
+// OCP FP4 E2M1 code of v (magnitudes 0, .5, 1, 1.5, 2, 3, 4, 6 as codes 0 .. 7):
+// the nearest value, ties to the even code, saturating at 6, the sign bit
+// (bit 3) kept also when v rounds to zero.  The comparisons place each tie
+// on its even side.
+__device__ __forceinline__ uint32_t e2m1_code(float v) {
+  const float a = __builtin_fabsf(v);
+  const uint32_t c = (uint32_t)(a > 0.25f) + (uint32_t)(a >= 0.75f) + (uint32_t)(a > 1.25f) +
+                     (uint32_t)(a >= 1.75f) + (uint32_t)(a > 2.5f) + (uint32_t)(a >= 3.5f) +
+                     (uint32_t)(a > 5.0f);
+  return c | ((__float_as_uint(v) >> 28) & 8u);
+}
+
+// The MX block exponent X = floor(log2 amax) - 2 of a block whose largest
+// magnitude is amax (E8M0's range; -127 for an all-zero block).
+__device__ __forceinline__ int32_t mx_exponent(float amax) {
+  if (!(amax > 0.0f)) return -127;
+  const int32_t e = __builtin_amdgcn_frexp_expf(amax);  // amax = m 2^e, m in [0.5, 1)
+  return max(-127, min(127, e - 3));
+}
+
 // Lanes of one wave exchange values through LDS: every lane's earlier LDS
 // writes are visible to the others' later reads.
 __device__ __forceinline__ void wave_lds_sync() {
@@ -2004,6 +2024,24 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
       *(uint2*)out = make_uint2(packed[0], packed[1]);
       if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
       if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
+    } else if constexpr (MODE == 4) {
+      // the MXFP4 cast (Sec. 4.8, Sec. 6.4): blocks of 32 codes (four lanes)
+      // share X = floor(log2 amax) - 2; each code becomes E2M1(c / 2^X),
+      // two per byte (the even k in the low nibble), the scale byte X + 127
+      float am = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) am = __builtin_fmaxf(am, __builtin_fabsf((float)c[j]));
+      am = __builtin_fmaxf(am, dpp_xor<1>(am));
+      am = __builtin_fmaxf(am, dpp_xor<2>(am));
+      const int32_t X = mx_exponent(am);
+      const float inv = __builtin_ldexpf(1.0f, -X);  // exact; c / 2^X is exact
+      uint32_t packed = 0;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) packed |= e2m1_code((float)c[j] * inv) << (4 * j);
+      uint8_t* out = (uint8_t*)A.y + (int64_t)lrow * A.ld + (col >> 1);
+      *(uint32_t*)out = packed;
+      if ((lane & 3) == 0) A.mxs[(int64_t)lrow * (A.tpr * 4) + (col >> 5)] = (uint8_t)(X + 127);
+      if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
     } else if constexpr (MODE == 3) {
       // the fp8 cast (Sec. 4.8): E4M3 of each code, round to nearest even,
       // magnitudes beyond 448 saturated and counted
@@ -2813,6 +2851,32 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
   for (int m = 1; m < 64; m <<= 1) amax = __builtin_fmaxf(amax, __shfl_xor(amax, m, 64));
   if (lane == 0) s_max[wave] = amax;
   __syncthreads();
+  if (A.fp8 == 2) {
+    // MXFP4: blocks of 32 (eight threads of four values each) share
+    // X = floor(log2 amax) - 2 and hold E2M1(y / 2^X); no per-token factor
+    for (int64_t base = 0; base < A.K; base += 1024) {
+      const int64_t col = base + (int64_t)tid * 4;
+      const bool in = col < A.K;  // whole 32-blocks are in or out (K is a multiple of 512)
+      float q[4], am = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        q[i] = in ? ybuf[col + i] : 0.0f;
+        am = __builtin_fmaxf(am, __builtin_fabsf(q[i]));
+      }
+      am = __builtin_fmaxf(am, __shfl_xor(am, 1, 64));
+      am = __builtin_fmaxf(am, __shfl_xor(am, 2, 64));
+      am = __builtin_fmaxf(am, __shfl_xor(am, 4, 64));
+      const int32_t X = mx_exponent(am);
+      uint32_t packed = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) packed |= e2m1_code(__builtin_ldexpf(q[i], -X)) << (4 * i);
+      if (in) {
+        *(uint16_t*)((uint8_t*)A.xq + row * (A.K / 2) + col / 2) = (uint16_t)packed;
+        if ((tid & 7) == 0) A.mxs[row * (A.K / 32) + col / 32] = (uint8_t)(X + 127);
+      }
+    }
+    return;
+  }
   amax = __builtin_fmaxf(__builtin_fmaxf(s_max[0], s_max[1]), __builtin_fmaxf(s_max[2], s_max[3]));
   const float top = A.fp8 ? 448.0f : 127.0f;  // E4M3's largest magnitude, or int8's
   const float inv = (amax == 0.0f) ? 0.0f : top / amax;
@@ -2870,21 +2934,45 @@ struct GemmPrefetch {
 };
 
 // Rows past M or N read the last valid row instead: they only feed outputs
-// that are never stored, and the loads stay branch-free.
+// that are never stored, and the loads stay branch-free.  A stage is 128
+// bytes of every row (128 int8 / E4M3 values, or 256 MXFP4 values); rows
+// are `rb` bytes apart.
 __device__ __forceinline__ uint4 gemm_chunk(const int8_t* base, int64_t row0, int64_t rows,
-                                            int64_t K, int64_t t, int c) {
+                                            int64_t rb, int64_t t, int c) {
   const int64_t r = min(row0 + (c >> 3), rows - 1);
-  return *(const uint4*)(base + r * K + t * HQ_TILE + (c & 7) * 16);
+  return *(const uint4*)(base + r * rb + t * 128 + (c & 7) * 16);
 }
 
 __device__ __forceinline__ void gemm_load(const hq_gemm_args& A, int64_t m0, int64_t n0, int64_t t,
                                           int tid, GemmPrefetch& p) {
-  p.a0 = gemm_chunk(A.xq, m0, A.M, A.K, t, tid);
-  p.a1 = gemm_chunk(A.xq, m0, A.M, A.K, t, tid + 512);
-  p.a2 = gemm_chunk(A.xq, m0, A.M, A.K, t, tid + 1024);
-  p.a3 = gemm_chunk(A.xq, m0, A.M, A.K, t, tid + 1536);
-  p.b0 = gemm_chunk(A.w, n0, A.N, A.K, t, tid);
-  p.b1 = gemm_chunk(A.w, n0, A.N, A.K, t, tid + 512);
+  const int64_t rb = A.fp8 == 2 ? A.K / 2 : A.K;
+  p.a0 = gemm_chunk(A.xq, m0, A.M, rb, t, tid);
+  p.a1 = gemm_chunk(A.xq, m0, A.M, rb, t, tid + 512);
+  p.a2 = gemm_chunk(A.xq, m0, A.M, rb, t, tid + 1024);
+  p.a3 = gemm_chunk(A.xq, m0, A.M, rb, t, tid + 1536);
+  p.b0 = gemm_chunk(A.w, n0, A.N, rb, t, tid);
+  p.b1 = gemm_chunk(A.w, n0, A.N, rb, t, tid + 512);
+}
+
+// MXFP4: the scale bytes of a lane's rows for stage t (eight 32-blocks of
+// each row), shifted so that byte 0 / byte 2 of the low word are the lane's
+// blocks of the stage's first / second 64-deep step and those of the high
+// word its third / fourth (the lane's half of each step is block 2 s + l / 32).
+__device__ __forceinline__ uint2 mx_scales(const uint8_t* sc, int64_t row, int64_t rows, int64_t K,
+                                           int64_t t, int lane) {
+  const uint2 w = *(const uint2*)(sc + min(row, rows - 1) * (K / 32) + t * 8);
+  const uint32_t sh = 8u * (uint32_t)(lane >> 5);
+  return make_uint2(w.x >> sh, w.y >> sh);
+}
+
+template <int OPSEL>
+__device__ __forceinline__ v16f_t mfma_mxfp4(v4i_t a, v4i_t b, v16f_t c, uint32_t sa, uint32_t sb) {
+  typedef int v8i_t __attribute__((ext_vector_type(8)));
+  const v8i_t a8 = {a[0], a[1], a[2], a[3], 0, 0, 0, 0};
+  const v8i_t b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
+  // cbsz = blgp = 4: both operands E2M1; the scales are E8M0 bytes
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, OPSEL, (int)sa, OPSEL,
+                                                         (int)sb);
 }
 
 __device__ __forceinline__ void gemm_put(int8_t* s, int c, uint4 v) {
@@ -2916,6 +3004,46 @@ __device__ __forceinline__ void gemm_load_g(const hq_gemm_args& A, int64_t n0, i
 // (v_mfma_f32_32x32x16_fp8_fp8), two per 32-deep step on the low and high
 // eight bytes of each lane's fragment (A and B split alike, so the two
 // products cover the step's 32 k), fp32 tile sums.
+// MXFP4: a stage is two 128-deep K tiles, four 64-deep scaled MFMA steps
+// (v_mfma_scale_f32_32x32x64_f8f6f4): a lane's 16 fragment bytes are 32
+// E2M1 values, one MX block, scaled by its row's block scale; the fp32 sums
+// of steps 0-1 and 2-3 are each rescaled by their tile's weight factor.
+__device__ __forceinline__ void gemm_step_mx(const int8_t* sa, const int8_t* sb, int wm, int wn,
+                                             int lane, const float (&gv)[2][kGemmNB],
+                                             const uint2 (&xs)[2], const uint2 (&ws)[kGemmNB],
+                                             float (&accf)[2][kGemmNB][16]) {
+  v16f_t acc[2][kGemmNB];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int koff = ks * 32 + (lane >> 5) * 16;
+    v4i_t fa[2], fb[kGemmNB];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+      fa[a] = *(const v4i_t*)(sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff);
+#pragma unroll
+    for (int b = 0; b < kGemmNB; ++b)
+      fb[b] = *(const v4i_t*)(sb + (wn * (kGemmN / 2) + b * 32 + (lane & 31)) * kGemmLd + koff);
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b) {
+        const uint32_t xa = ks < 2 ? xs[a].x : xs[a].y, wb = ks < 2 ? ws[b].x : ws[b].y;
+        const v16f_t c0 = (ks & 1) ? acc[a][b] : (v16f_t){};
+        acc[a][b] = (ks & 1) ? mfma_mxfp4<2>(fa[a], fb[b], c0, xa, wb)
+                             : mfma_mxfp4<0>(fa[a], fb[b], c0, xa, wb);
+      }
+    if (ks & 1) {
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < kGemmNB; ++b)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            accf[a][b][r] = __builtin_fmaf(acc[a][b][r], gv[ks >> 1][b], accf[a][b][r]);
+    }
+  }
+}
+
 template <bool FP8>
 __device__ __forceinline__ void gemm_step(const int8_t* sa, const int8_t* sb, int wm, int wn,
                                           int lane, const float (&gv)[kGemmNB],
@@ -2980,7 +3108,8 @@ __device__ __forceinline__ void gemm_step(const int8_t* sa, const int8_t* sb, in
         accf[a][b][r] = __builtin_fmaf((float)acc[a][b][r], gv[b], accf[a][b][r]);
 }
 
-template <bool FP8>
+// MODE 0: int8, 1: fp8 (E4M3), 2: MXFP4.
+template <int MODE>
 __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
   extern __shared__ __attribute__((aligned(16))) int8_t gsm[];
   int8_t* const sa = gsm;                    // stage s at sa + s * kGemmStageA
@@ -2988,7 +3117,8 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
-  const int64_t T = A.K / HQ_TILE;
+  const int64_t T = A.K / HQ_TILE;                    // 128-deep K tiles (weight factors)
+  const int64_t TS = MODE == 2 ? T / 2 : T;          // LDS stages of 128 bytes per row
 
   float accf[2][kGemmNB][16];
 #pragma unroll
@@ -3002,19 +3132,33 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
   gemm_load(A, m0, n0, 0, tid, pf);
   gemm_stash(sa, sb, tid, pf);
   __syncthreads();
-  gemm_load(A, m0, n0, min<int64_t>(1, T - 1), tid, pf);
+  gemm_load(A, m0, n0, min<int64_t>(1, TS - 1), tid, pf);
 
-  // tile t from stage t & 1; the prefetched tile t + 1 goes to the other
-  // stage (free since the last barrier) and tile t + 2's loads start
-  for (int64_t t = 0; t < T; ++t) {
-    float gv[kGemmNB];
-    gemm_load_g(A, n0, wn, lane, T, t, gv);
+  // stage t from buffer t & 1; the prefetched stage t + 1 goes to the other
+  // buffer (free since the last barrier) and stage t + 2's loads start
+  for (int64_t t = 0; t < TS; ++t) {
     const int st = (int)(t & 1);
-    gemm_step<FP8>(sa + st * kGemmStageA, sb + st * kGemmStageB, wm, wn, lane, gv, accf);
-    if (t + 1 < T) {
+    if constexpr (MODE == 2) {
+      float gv[2][kGemmNB];
+      gemm_load_g(A, n0, wn, lane, T, 2 * t, gv[0]);
+      gemm_load_g(A, n0, wn, lane, T, 2 * t + 1, gv[1]);
+      uint2 xs[2], ws[kGemmNB];
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+        xs[a] = mx_scales(A.xs, m0 + wm * 64 + a * 32 + (lane & 31), A.M, A.K, t, lane);
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b)
+        ws[b] = mx_scales(A.ws, n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31), A.N, A.K, t, lane);
+      gemm_step_mx(sa + st * kGemmStageA, sb + st * kGemmStageB, wm, wn, lane, gv, xs, ws, accf);
+    } else {
+      float gv[kGemmNB];
+      gemm_load_g(A, n0, wn, lane, T, t, gv);
+      gemm_step<MODE == 1>(sa + st * kGemmStageA, sb + st * kGemmStageB, wm, wn, lane, gv, accf);
+    }
+    if (t + 1 < TS) {
       gemm_stash(sa + (st ^ 1) * kGemmStageA, sb + (st ^ 1) * kGemmStageB, tid, pf);
       __syncthreads();
-      gemm_load(A, m0, n0, min(t + 2, T - 1), tid, pf);  // the last tile again at the end
+      gemm_load(A, m0, n0, min(t + 2, TS - 1), tid, pf);  // the last stage again at the end
     }
   }
 
@@ -3024,7 +3168,7 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
     for (int r = 0; r < 16; ++r) {
       const int64_t m = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (m >= A.M) continue;
-      const float sxm = A.sx[m];
+      const float sxm = MODE == 2 ? 1.0f : A.sx[m];  // MXFP4 blocks carry their own scale
 #pragma unroll
       for (int b = 0; b < kGemmNB; ++b) {
         const int64_t n = n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31);
@@ -3039,11 +3183,15 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
 }
 
 __global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_i8_kernel(hq_gemm_args A) {
-  gemm_body<false>(A);
+  gemm_body<0>(A);
 }
 
 __global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_f8_kernel(hq_gemm_args A) {
-  gemm_body<true>(A);
+  gemm_body<1>(A);
+}
+
+__global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_mx4_kernel(hq_gemm_args A) {
+  gemm_body<2>(A);
 }
 
 // ------------------------------------------------------------ utilities
@@ -3263,7 +3411,7 @@ int hq_launch_act_prep(const hq_actprep_args& a, void* stream) {
 }
 
 int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
-  if (a.K % HQ_TILE != 0) return -1;
+  if (a.K % HQ_TILE != 0 || (a.fp8 == 2 && a.K % 256 != 0)) return -1;
   static bool lds_set = false;  // more than 64 KB of dynamic LDS needs an opt-in
   if (!lds_set) {
     hipError_t e = hipFuncSetAttribute((const void*)hq_gemm_i8_kernel,
@@ -3271,14 +3419,31 @@ int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void*)hq_gemm_f8_kernel,
                               hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void*)hq_gemm_mx4_kernel,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
     if (e != hipSuccess) return (int)e;
     lds_set = true;
   }
   const dim3 grid((uint32_t)((a.N + kGemmN - 1) / kGemmN), (uint32_t)((a.M + kGemmM - 1) / kGemmM));
-  if (a.fp8)
+  if (a.fp8 == 2)
+    hipLaunchKernelGGL(hq_gemm_mx4_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
+  else if (a.fp8)
     hipLaunchKernelGGL(hq_gemm_f8_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
   else
     hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
+  return (int)hipGetLastError();
+}
+
+int hq_launch_decode_mxfp4(const hq_plan_s* p, const hq_decode_args& a, void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
+  const uint32_t nwg = decode_wgs(a.nsub);
+  switch (p->lattice) {
+    case HQ_E8: launch_decode_kernel<kE8, 4, false>(a, nwg, lds, st); break;
+    case HQ_D4: launch_decode_kernel<kD4, 4, false>(a, nwg, lds, st); break;
+    default: launch_decode_kernel<kZ, 4, false>(a, nwg, lds, st);
+  }
   return (int)hipGetLastError();
 }
 

@@ -103,6 +103,12 @@ def lib():
     L.hq_act_prep_fp8.argtypes = [p, p, i64, i64, p, p, p]
     L.hq_gemm_fp8_blockscaled.restype = i32
     L.hq_gemm_fp8_blockscaled.argtypes = [p, p, p, i64, p, p, i64, p, i32, p]
+    L.hq_decode_mxfp4.restype = i32
+    L.hq_decode_mxfp4.argtypes = [p, p, i64, i64, p, p, p, p]
+    L.hq_act_prep_mxfp4.restype = i32
+    L.hq_act_prep_mxfp4.argtypes = [p, p, i64, i64, p, p, p]
+    L.hq_gemm_mxfp4_blockscaled.restype = i32
+    L.hq_gemm_mxfp4_blockscaled.argtypes = [p, p, p, i64, p, p, p, i64, p, i32, p]
     L.hq_gemm_workspace_bytes.restype = C.c_size_t
     L.hq_gemm_workspace_bytes.argtypes = [p, i64, i64]
     L.hq_dequant_gemm_int8.restype = i32
@@ -310,6 +316,46 @@ def hq_decode_int8(plan: Plan, s: EncodedStream, row0=0, rows=None, stream=None)
     return codes, g
 
 
+def hq_decode_mxfp4(plan: Plan, s: EncodedStream, row0=0, rows=None, stream=None):
+    """hq_decode_mxfp4: E2M1 code pairs (uint8, cols / 2 per row), E8M0 scale
+    bytes (cols / 32 per row) and the per-tile factors."""
+    rows = s.rows - row0 if rows is None else rows
+    codes = torch.empty((rows, plan.cols // 2), dtype=torch.uint8, device=s.device)
+    scales = torch.empty((rows, plan.cols // 32), dtype=torch.uint8, device=s.device)
+    g = torch.empty((rows, plan.info.tiles_per_row), dtype=torch.float32, device=s.device)
+    st = lib().hq_decode_mxfp4(plan.handle, C.byref(s.c), row0, rows, C.c_void_p(codes.data_ptr()),
+                               C.c_void_p(scales.data_ptr()), C.c_void_p(g.data_ptr()),
+                               _stream_handle(stream))
+    _check("hq_decode_mxfp4", st)
+    return codes, scales, g
+
+
+def hq_act_prep_mxfp4(plan: Plan, a: torch.Tensor, stream=None):
+    """hq_act_prep_mxfp4: MXFP4 of the rotated activations (codes, scales)."""
+    assert a.dim() == 2 and a.dtype == torch.bfloat16 and a.stride(1) == 1
+    M = a.shape[0]
+    xq = torch.empty((M, plan.cols // 2), dtype=torch.uint8, device=a.device)
+    xs = torch.empty((M, plan.cols // 32), dtype=torch.uint8, device=a.device)
+    st = lib().hq_act_prep_mxfp4(plan.handle, C.c_void_p(a.data_ptr()), M, a.stride(0),
+                                 C.c_void_p(xq.data_ptr()), C.c_void_p(xs.data_ptr()),
+                                 _stream_handle(stream))
+    _check("hq_act_prep_mxfp4", st)
+    return xq, xs
+
+
+def hq_gemm_mxfp4_blockscaled(plan: Plan, xq, xs, codes, ws, g, out_dtype=torch.float32,
+                              stream=None):
+    M, N = xq.shape[0], codes.shape[0]
+    out = torch.empty((M, N), dtype=out_dtype, device=xq.device)
+    st = lib().hq_gemm_mxfp4_blockscaled(plan.handle, C.c_void_p(xq.data_ptr()),
+                                         C.c_void_p(xs.data_ptr()), M, C.c_void_p(codes.data_ptr()),
+                                         C.c_void_p(ws.data_ptr()), C.c_void_p(g.data_ptr()), N,
+                                         C.c_void_p(out.data_ptr()), _dtype_code(out_dtype),
+                                         _stream_handle(stream))
+    _check("hq_gemm_mxfp4_blockscaled", st)
+    return out
+
+
 def hq_decode_fp8(plan: Plan, s: EncodedStream, row0=0, rows=None, stream=None):
     """hq_decode_fp8: E4M3 code bytes (uint8) and the per-tile factors."""
     rows = s.rows - row0 if rows is None else rows
@@ -474,5 +520,6 @@ EXPORTED = ["hq_plan", "hq_plan_destroy", "hq_plan_get_info", "hq_scan_bytes", "
             "hq_gemm_workspace_bytes", "hq_dequant_gemm_int8", "hq_gemv_workspace_bytes",
             "hq_decode_gemv", "hq_attention_workspace_bytes", "hq_decode_attention",
             "hq_decode_fp8", "hq_act_prep_fp8", "hq_gemm_fp8_blockscaled",
+            "hq_decode_mxfp4", "hq_act_prep_mxfp4", "hq_gemm_mxfp4_blockscaled",
             "hq_rice_kstar",
             "hq_calibrated_snr", "hq_status_string"]

@@ -116,7 +116,7 @@ def test_zero_and_nonfinite_tiles(hq, tile):
 
 
 def test_long_tiles_reject_the_128_paths(hq):
-    # the int8 / fp8 casts, the GEMM, the fused GEMV and group launches are
+    # the int8 / fp8 / MXFP4 casts, the GEMM, the fused GEMV and group launches are
     # built for 128-tiles: a long-tile plan gets HQ_ERR_UNSUPPORTED
     snr = PT.op_snr("E8", 4.0)
     plan = hq.hq_plan(512, hq.HQ_E8, 0.0, 1, -1, 2048, snr_db=snr)
@@ -126,7 +126,8 @@ def test_long_tiles_reject_the_128_paths(hq):
     for fn in (lambda: hq.hq_decode_int8(plan, s), lambda: hq.hq_decode_fp8(plan, s),
                lambda: hq.hq_decode_gemv(plan, s, x[0].contiguous()),
                lambda: hq.hq_encode_group([plan], [x], [hq.EncodedStream(plan, 4)]),
-               lambda: hq.hq_act_prep(plan, x)):
+               lambda: hq.hq_act_prep(plan, x), lambda: hq.hq_decode_mxfp4(plan, s),
+               lambda: hq.hq_act_prep_mxfp4(plan, x)):
         with pytest.raises(hq.HQError) as e:
             fn()
         assert e.value.status == -2
