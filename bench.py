@@ -29,6 +29,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, vendor figure
 INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA, vendor figure
 FP8_PEAK_TFLOPS = 5000.0   # MI355X dense fp8 MFMA, vendor figure
+FP4_PEAK_TFLOPS = 10100.0  # MI355X dense fp4 MFMA, vendor figure
 
 
 def parse_args():
@@ -379,6 +380,29 @@ def gemm_extra(H, W, mats, dev):
     torch.cuda.synchronize()
     t_gemm8 = f0.elapsed_time(f1) / reps * 1e-3
     t_e2e8 = f1.elapsed_time(f2) / reps * 1e-3
+    # the MXFP4 cast path: GEMM alone, and act prep + decode to MXFP4 + GEMM
+    x4, xs4 = H.hq_act_prep_mxfp4(plan, a)
+    c4, ws4, g4 = H.hq_decode_mxfp4(plan, s)
+
+    def mx_e2e():
+        xa, xsa = H.hq_act_prep_mxfp4(plan, a)
+        cw, wsw, gw = H.hq_decode_mxfp4(plan, s)
+        H.hq_gemm_mxfp4_blockscaled(plan, xa, xsa, cw, wsw, gw, out=out)
+
+    for _ in range(3):
+        H.hq_gemm_mxfp4_blockscaled(plan, x4, xs4, c4, ws4, g4, out=out)
+        mx_e2e()
+    torch.cuda.synchronize()
+    f0.record()
+    for _ in range(reps):
+        H.hq_gemm_mxfp4_blockscaled(plan, x4, xs4, c4, ws4, g4, out=out)
+    f1.record()
+    for _ in range(reps):
+        mx_e2e()
+    f2.record()
+    torch.cuda.synchronize()
+    t_gemm4 = f0.elapsed_time(f1) / reps * 1e-3
+    t_e2e4 = f1.elapsed_time(f2) / reps * 1e-3
     ops = 2.0 * M * N * K
     return {"workload": f"W {N}x{K} E8@4 Rice stream, A {M}x{K} bf16 (1% outlier channels x30)",
             "gemm_ms": round(t_gemm * 1e3, 4), "gemm_TOPS": round(ops / t_gemm / 1e12, 2),
@@ -387,7 +411,10 @@ def gemm_extra(H, W, mats, dev):
             "end_to_end_TOPS": round(ops / t_e2e / 1e12, 2),
             "fp8_gemm_ms": round(t_gemm8 * 1e3, 4), "fp8_gemm_TOPS": round(ops / t_gemm8 / 1e12, 2),
             "fp8_gemm_frac_fp8_peak": round(ops / t_gemm8 / 1e12 / FP8_PEAK_TFLOPS, 4),
-            "fp8_end_to_end_ms": round(t_e2e8 * 1e3, 4)}
+            "fp8_end_to_end_ms": round(t_e2e8 * 1e3, 4),
+            "mxfp4_gemm_ms": round(t_gemm4 * 1e3, 4), "mxfp4_gemm_TOPS": round(ops / t_gemm4 / 1e12, 2),
+            "mxfp4_gemm_frac_fp4_peak": round(ops / t_gemm4 / 1e12 / FP4_PEAK_TFLOPS, 4),
+            "mxfp4_end_to_end_ms": round(t_e2e4 * 1e3, 4)}
 
 
 def gemv_extra(H, W, mats, dev, reps=10):
@@ -411,17 +438,27 @@ def gemv_extra(H, W, mats, dev, reps=10):
         for w, x, y in zip(wb, xs, yb):
             torch.mv(w, x, out=y)
 
+    def decode_then_gemv():
+        # the unfused baseline: decode each matrix to bf16 in HBM, then GEMV
+        for m, w, x, y in zip(layer, wb, xs, yb):
+            H.hq_decode(m["plan"], m["s"], out=w)
+            torch.mv(w, x, out=y)
+
     fused()
     dense()
+    decode_then_gemv()
     torch.cuda.synchronize()
     tf = _median_ms(fused, reps, flush) * 1e-3
     td = _median_ms(dense, reps, flush) * 1e-3
+    tdd = _median_ms(decode_then_gemv, reps, flush) * 1e-3
     n = sum(m["x"].numel() for m in layer)
     stream_bytes = sum(int(m["s"].end_words()) * 4 for m in layer) + n / 128 * 4 + n / 512 * 5
     del flush, wb
     torch.cuda.empty_cache()
     return {"workload": "layer 0 of the stack (7 matrices, 218M E8@4 weights), one bf16 token",
             "fused_ms": round(tf * 1e3, 4), "bf16_gemv_ms": round(td * 1e3, 4),
+            "decode_then_gemv_ms": round(tdd * 1e3, 4),
+            "speedup_vs_decode_then_gemv": round(tdd / tf, 3),
             "fused_weights_per_s_e9": round(n / tf / 1e9, 1),
             "fused_stream_GBs": round(stream_bytes / tf / 1e9, 1),
             "bf16_gemv_GBs": round(2 * n / td / 1e9, 1),

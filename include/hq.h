@@ -279,7 +279,7 @@ hq_status hq_gemm_int8_blockscaled(hq_plan_t plan, const int8_t* xq, const float
  * hq_act_prep_fp8 -- as hq_act_prep, with x = E4M3(y * 448 / amax) and
  *   s_x = amax / 448.
  * hq_gemm_fp8_blockscaled -- as hq_gemm_int8_blockscaled over the E4M3
- *   values: fp32 tile sums on the fp8 matrix cores (v_mfma_f32_32x32x16_fp8),
+ *   values: fp32 tile sums on the f8f6f4 matrix cores (v_mfma_scale_f32_32x32x64_f8f6f4),
  *   each rescaled by g into fp32 accumulators. */
 hq_status hq_decode_fp8(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows,
                         uint8_t* codes, int64_t ldc, float* g, void* stream);

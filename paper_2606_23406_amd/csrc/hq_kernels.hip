@@ -3000,10 +3000,10 @@ __device__ __forceinline__ void gemm_load_g(const hq_gemm_args& A, int64_t n0, i
 // One K tile: the wave's 2 x kGemmNB MFMA blocks from LDS, then their exact
 // int32 sums rescaled by the tile's weight factors into the fp32
 // accumulators.
-// FP8: the same bytes as E4M3 on the fp8 matrix cores
-// (v_mfma_f32_32x32x16_fp8_fp8), two per 32-deep step on the low and high
-// eight bytes of each lane's fragment (A and B split alike, so the two
-// products cover the step's 32 k), fp32 tile sums.
+// FP8: the same bytes as E4M3 on gfx950's f8f6f4 matrix cores
+// (v_mfma_scale_f32_32x32x64_f8f6f4 with both block scales 2^0), two
+// 64-deep steps per tile, 32 fragment bytes per lane (A and B read alike, so
+// the products pair identical k), fp32 tile sums.
 // MXFP4: a stage is two 128-deep K tiles, four 64-deep scaled MFMA steps
 // (v_mfma_scale_f32_32x32x64_f8f6f4): a lane's 16 fragment bytes are 32
 // E2M1 values, one MX block, scaled by its row's block scale; the fp32 sums
@@ -3049,29 +3049,31 @@ __device__ __forceinline__ void gemm_step(const int8_t* sa, const int8_t* sb, in
                                           int lane, const float (&gv)[kGemmNB],
                                           float (&accf)[2][kGemmNB][16]) {
   if constexpr (FP8) {
+    typedef int v8i_t __attribute__((ext_vector_type(8)));
     v16f_t acc[2][kGemmNB];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int koff = ks * 32 + (lane >> 5) * 16;
-      v4i_t fa[2], fb[kGemmNB];
+    for (int ks = 0; ks < 2; ++ks) {
+      const int koff = ks * 64 + (lane >> 5) * 32;
+      v8i_t fa[2], fb[kGemmNB];
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        const int8_t* q = sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff;
+        const v4i_t lo = *(const v4i_t*)q, hi = *(const v4i_t*)(q + 16);
+        fa[a] = (v8i_t){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b) {
+        const int8_t* q = sb + (wn * (kGemmN / 2) + b * 32 + (lane & 31)) * kGemmLd + koff;
+        const v4i_t lo = *(const v4i_t*)q, hi = *(const v4i_t*)(q + 16);
+        fb[b] = (v8i_t){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
 #pragma unroll
       for (int a = 0; a < 2; ++a)
-        fa[a] = *(const v4i_t*)(sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff);
 #pragma unroll
-      for (int b = 0; b < kGemmNB; ++b)
-        fb[b] = *(const v4i_t*)(sb + (wn * (kGemmN / 2) + b * 32 + (lane & 31)) * kGemmLd + koff);
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < kGemmNB; ++b) {
-          const long alo = (long)(((unsigned long)(uint32_t)fa[a][1] << 32) | (uint32_t)fa[a][0]);
-          const long ahi = (long)(((unsigned long)(uint32_t)fa[a][3] << 32) | (uint32_t)fa[a][2]);
-          const long blo = (long)(((unsigned long)(uint32_t)fb[b][1] << 32) | (uint32_t)fb[b][0]);
-          const long bhi = (long)(((unsigned long)(uint32_t)fb[b][3] << 32) | (uint32_t)fb[b][2]);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(
-              alo, blo, ks == 0 ? (v16f_t){} : acc[a][b], 0, 0, 0);
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_fp8_fp8(ahi, bhi, acc[a][b], 0, 0, 0);
-        }
+        for (int b = 0; b < kGemmNB; ++b)
+          // cbsz = blgp = 0: both operands E4M3; scale bytes 127 (2^0)
+          acc[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+              fa[a], fb[b], ks == 0 ? (v16f_t){} : acc[a][b], 0, 0, 0, 127, 0, 127);
     }
 #pragma unroll
     for (int a = 0; a < 2; ++a)

@@ -343,14 +343,15 @@ def hq_act_prep_mxfp4(plan: Plan, a: torch.Tensor, stream=None):
     return xq, xs
 
 
-def hq_gemm_mxfp4_blockscaled(plan: Plan, xq, xs, codes, ws, g, out_dtype=torch.float32,
-                              stream=None):
+def hq_gemm_mxfp4_blockscaled(plan: Plan, xq, xs, codes, ws, g, out_dtype=torch.bfloat16,
+                              out=None, stream=None):
     M, N = xq.shape[0], codes.shape[0]
-    out = torch.empty((M, N), dtype=out_dtype, device=xq.device)
+    if out is None:
+        out = torch.empty((M, N), dtype=out_dtype, device=xq.device)
     st = lib().hq_gemm_mxfp4_blockscaled(plan.handle, C.c_void_p(xq.data_ptr()),
                                          C.c_void_p(xs.data_ptr()), M, C.c_void_p(codes.data_ptr()),
                                          C.c_void_p(ws.data_ptr()), C.c_void_p(g.data_ptr()), N,
-                                         C.c_void_p(out.data_ptr()), _dtype_code(out_dtype),
+                                         C.c_void_p(out.data_ptr()), _dtype_code(out.dtype),
                                          _stream_handle(stream))
     _check("hq_gemm_mxfp4_blockscaled", st)
     return out
