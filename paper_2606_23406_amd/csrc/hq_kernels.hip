@@ -2902,72 +2902,161 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
 }
 
 
-// ------------------------------------------------------------ block-scaled int8 GEMM
-// out[m, n] = s_x[m] * sum_t g[n, t] * P_t[m, n], P_t the exact int32 sum of
-// one 128-deep K tile on the int8 matrix cores (v_mfma_i32_32x32x32_i8).
-// Workgroup tile 256 (tokens) x 128 (weight rows), eight waves in 4 x 2,
-// each 64 x 64 = 2 x 2 MFMA blocks.  K tiles are double-buffered in LDS and the
-// next tile's global loads sit in registers while the current one is
-// multiplied; each tile's int32 sums are then rescaled on the VALU (one
-// convert + one fma per output), two waves per SIMD.  Both operands are K-contiguous rows and every
-// lane reads the same 16 contiguous k for A and B, so the contraction pairs
-// identical k whatever order the instruction assigns inside its 32-deep
-// step.  Output lane l of a 32 x 32 block holds column l % 32 and rows
-// 8 (r / 4) + 4 (l / 32) + r % 4.
+// ------------------------------------------------------------ block-scaled GEMM
+// out[m, n] = s_x[m] * sum_t g[n, t] * P_t[m, n], P_t the sum over one
+// 128-deep K tile: exact int32 on the int8 matrix cores
+// (v_mfma_i32_32x32x32_i8), fp32 on the f8f6f4 ones for E4M3 and MXFP4
+// (v_mfma_scale_f32_32x32x64_f8f6f4; MXFP4 scales every 32-block itself and
+// has s_x = 1).
+// Workgroup tile 256 (tokens) x 128 (weight rows), eight waves in 4 x 2, each
+// 64 x 64 = 2 x 2 MFMA blocks, one workgroup per CU.  An LDS stage is 128
+// bytes of every A and B row (one K tile of int8 / E4M3, two of MXFP4) plus
+// its side data (tile factors, MX block scales).  Stages are double-buffered
+// and filled straight from global memory by direct-to-LDS loads, with no
+// register staging: stage t + 1 streams in while stage t is multiplied.
+// The partial sums are double-buffered too: each K tile's MFMAs write one
+// set while the previous tile's set is rescaled by its factors on the VALU,
+// a few elements after each MFMA, so that the two pipes overlap.
+// LDS rows are 128 bytes with the 16-byte chunk c of row r at position
+// c ^ ((r / 2) % 8): a wave's 1 KB direct load fills rows 8q .. 8q + 7 (lane
+// l at row 8q + l / 8, position l % 8), and the 16 lanes of one LDS cycle
+// reading one chunk of 16 consecutive rows cover the 64 banks exactly once.
+// Both operands are K-contiguous rows and every lane reads the same k range
+// of A and B, so the contraction pairs identical k whatever order the
+// instruction assigns inside a step.  Output lane l of a 32 x 32 block holds
+// column l % 32 and rows 8 (r / 4) + 4 (l / 32) + r % 4.
 
 typedef int v4i_t __attribute__((ext_vector_type(4)));
+typedef int v8i_t __attribute__((ext_vector_type(8)));
 typedef int v16i_t __attribute__((ext_vector_type(16)));
 typedef float v16f_t __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef const __attribute__((address_space(1))) void gbl_void_t;
 
-constexpr int kGemmM = 256, kGemmN = 128;  // the prefetch below assumes 256 x 128
+constexpr int kGemmM = 256, kGemmN = 128;  // the loads below assume 256 x 128 and 8 waves
 constexpr int kGemmThreads = 512;           // 8 waves, 4 (m) x 2 (n)
-constexpr int kGemmNB = kGemmN / 64;  // 32 x 32 blocks per wave along n
-constexpr int kGemmLd = 144;  // padded LDS row (bytes): rows 16 bytes apart mod 128
-constexpr int kGemmStageA = kGemmM * kGemmLd, kGemmStageB = kGemmN * kGemmLd;
-constexpr int kGemmLds = 2 * (kGemmStageA + kGemmStageB);
+constexpr int kGemmNB = kGemmN / 64;        // 32 x 32 blocks per wave along n
+constexpr int kGemmStageA = kGemmM * 128, kGemmStageB = kGemmN * 128;
+// side data of a stage: the weight rows' factors (K tile h of the stage at
+// float h * 128 + column), then for MXFP4 the 8 scale bytes of each A row
+// and of each B row
+constexpr int kGemmSideG = 0, kGemmSideXs = 1024, kGemmSideWs = 3072;
+constexpr int kGemmStages = 3;  // LDS ring: stage t + 2 loads while stage t is multiplied
+template <int MODE> constexpr int gemm_stage_bytes() {
+  return kGemmStageA + kGemmStageB + (MODE == 2 ? 4096 : 512);
+}
+template <int MODE> constexpr int gemm_lds_bytes() { return kGemmStages * gemm_stage_bytes<MODE>(); }
+static_assert(gemm_lds_bytes<2>() <= 160 * 1024, "the LDS ring fits one CU");
 
-// One thread's share of a K tile, in 16-byte chunks (chunk c = row c / 8,
-// byte (c % 8) * 16; thread tid takes c = tid + 512 i): 4 of A's 2048, 2 of
-// B's 1024.
-struct GemmPrefetch {
-  uint4 a0, a1, a2, a3, b0, b1;
+template <bool C, class T, class F> struct gemm_pick { using type = T; };
+template <class T, class F> struct gemm_pick<false, T, F> { using type = F; };
+template <int MODE> struct GemmMode {
+  static constexpr int U = MODE == 2 ? 2 : 1;      // 128-deep K tiles per stage
+  static constexpr int STEPS = MODE == 0 ? 4 : 2;  // MFMA steps per K tile
+  using acc_t = typename gemm_pick<MODE == 0, v16i_t, v16f_t>::type;
 };
 
-// Rows past M or N read the last valid row instead: they only feed outputs
-// that are never stored, and the loads stay branch-free.  A stage is 128
-// bytes of every row (128 int8 / E4M3 values, or 256 MXFP4 values); rows
-// are `rb` bytes apart.
-__device__ __forceinline__ uint4 gemm_chunk(const int8_t* base, int64_t row0, int64_t rows,
-                                            int64_t rb, int64_t t, int c) {
-  const int64_t r = min(row0 + (c >> 3), rows - 1);
-  return *(const uint4*)(base + r * rb + t * 128 + (c & 7) * 16);
+// The direct-to-LDS loads go through buffer resources based at the
+// workgroup's first A row, B row, factor row and scale rows: a lane's 32-bit
+// offset within them is fixed for the whole K loop and the stage's offset is
+// a scalar.  4 A and 2 B row groups per wave (16 bytes a lane, lane l at row
+// 8q + l / 8 and K chunk (l % 8) ^ ((4q + l / 16) % 8)), then the side data
+// (4 bytes a lane): factor dword j * 64 + l = g[n0 + (j % 2) 64 + l, U t +
+// j / 2] with j = w % 2U, and for MXFP4 scale dword d = w * 64 + l of the A
+// rows and d = (w % 4) * 64 + l of the B rows (row d / 2, half d % 2).  Waves
+// with equal j (or w % 4) load the same values to the same place, so every
+// wave issues the same loads and the loop has no branch.  Rows past M or N
+// read the last valid row: they only feed outputs that are never stored,
+// and every access stays inside its resource.
+struct GemmLoads {
+  __amdgpu_buffer_rsrc_t ra, rb, rg, rxs, rws;
+  uint32_t a[4], b[2], g, xs, ws;
+};
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void* base, int64_t bytes) {
+  // raw buffer (stride 0); the third descriptor word of gfx9 data buffers.
+  // The operands are workgroup-uniform: read them into scalar registers.
+  const uint64_t p = (uint64_t)base;
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)p);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(p >> 32));
+  const int n = __builtin_amdgcn_readfirstlane((int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)(((uint64_t)hi << 32) | lo), (short)0, n, 0x00020000);
 }
 
-__device__ __forceinline__ void gemm_load(const hq_gemm_args& A, int64_t m0, int64_t n0, int64_t t,
-                                          int tid, GemmPrefetch& p) {
-  const int64_t rb = A.fp8 == 2 ? A.K / 2 : A.K;
-  p.a0 = gemm_chunk(A.xq, m0, A.M, rb, t, tid);
-  p.a1 = gemm_chunk(A.xq, m0, A.M, rb, t, tid + 512);
-  p.a2 = gemm_chunk(A.xq, m0, A.M, rb, t, tid + 1024);
-  p.a3 = gemm_chunk(A.xq, m0, A.M, rb, t, tid + 1536);
-  p.b0 = gemm_chunk(A.w, n0, A.N, rb, t, tid);
-  p.b1 = gemm_chunk(A.w, n0, A.N, rb, t, tid + 512);
+template <int MODE>
+__device__ __forceinline__ GemmLoads gemm_loads(const hq_gemm_args& A, int64_t m0, int64_t n0,
+                                                int wave, int lane) {
+  const int64_t rb = MODE == 2 ? A.K / 2 : A.K;  // row bytes
+  const int64_t T = A.K / HQ_TILE, ks = A.K / 32;  // factors and MX scale bytes per row
+  const int64_t ma = min<int64_t>(A.M - m0, kGemmM), nb = min<int64_t>(A.N - n0, kGemmN);
+  GemmLoads L;
+  L.ra = gemm_rsrc(A.xq + m0 * rb, ma * rb);
+  L.rb = gemm_rsrc(A.w + n0 * rb, nb * rb);
+  L.rg = gemm_rsrc(A.g + n0 * T, nb * T * 4);
+  L.rxs = gemm_rsrc(MODE == 2 ? A.xs + m0 * ks : nullptr, MODE == 2 ? ma * ks : 0);
+  L.rws = gemm_rsrc(MODE == 2 ? A.ws + n0 * ks : nullptr, MODE == 2 ? nb * ks : 0);
+  const int rr = lane >> 3;
+  // row 8q + rr holds chunk (lane % 8) ^ ((4q + lane / 16) % 8) at position lane % 8
+  auto kc = [&](int q) { return (uint32_t)(((lane & 7) ^ ((4 * q + (lane >> 4)) & 7)) << 4); };
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int q = wave * 4 + i;
+    L.a[i] = (uint32_t)(min<int64_t>(8 * q + rr, ma - 1) * rb) + kc(q);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int q = wave * 2 + i;
+    L.b[i] = (uint32_t)(min<int64_t>(8 * q + rr, nb - 1) * rb) + kc(q);
+  }
+  const int j = wave % (2 * GemmMode<MODE>::U);
+  L.g = (uint32_t)((min<int64_t>((j & 1) * 64 + lane, nb - 1) * T + (j >> 1)) * 4);
+  const int d = wave * 64 + lane, e = (wave & 3) * 64 + lane;
+  L.xs = (uint32_t)(min<int64_t>(d >> 1, ma - 1) * ks + (d & 1) * 4);
+  L.ws = (uint32_t)(min<int64_t>(e >> 1, nb - 1) * ks + (e & 1) * 4);
+  return L;
 }
 
-// MXFP4: the scale bytes of a lane's rows for stage t (eight 32-blocks of
-// each row), shifted so that byte 0 / byte 2 of the low word are the lane's
-// blocks of the stage's first / second 64-deep step and those of the high
-// word its third / fourth (the lane's half of each step is block 2 s + l / 32).
-__device__ __forceinline__ uint2 mx_scales(const uint8_t* sc, int64_t row, int64_t rows, int64_t K,
-                                           int64_t t, int lane) {
-  const uint2 w = *(const uint2*)(sc + min(row, rows - 1) * (K / 32) + t * 8);
+// Direct-to-LDS loads of stage t into `stage` (wave is wave-uniform).
+template <int MODE>
+__device__ __forceinline__ void gemm_fetch(const GemmLoads& L, int64_t t, int wave, int8_t* stage) {
+  constexpr int U = GemmMode<MODE>::U;
+  const uint32_t so = (uint32_t)(t * 128);
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.ra, (lds_void_t*)(stage + (wave * 4 + i) * 1024), 16,
+                                             L.a[i], so, 0, 0);
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, (lds_void_t*)(stage + kGemmStageA + (wave * 2 + i) * 1024),
+                                             16, L.b[i], so, 0, 0);
+  int8_t* const side = stage + kGemmStageA + kGemmStageB;
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rg, (lds_void_t*)(side + kGemmSideG + (wave % (2 * U)) * 256),
+                                           4, L.g, (uint32_t)(U * t * 4), 0, 0);
+  if constexpr (MODE == 2) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rxs, (lds_void_t*)(side + kGemmSideXs + wave * 256), 4,
+                                             L.xs, (uint32_t)(t * 8), 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rws, (lds_void_t*)(side + kGemmSideWs + (wave & 3) * 256),
+                                             4, L.ws, (uint32_t)(t * 8), 0, 0);
+  }
+}
+
+// 16 bytes of row `row`, K chunk c (0..7) of a stage operand
+__device__ __forceinline__ v4i_t gemm_frag(const int8_t* base, int row, int c) {
+  return *(const v4i_t*)(base + row * 128 + ((c ^ ((row >> 1) & 7)) << 4));
+}
+
+// MXFP4: a lane's scale words from the side data: the 8 scale bytes of its
+// row, shifted so that byte 0 / byte 2 of the low word are the lane's blocks
+// of the stage's first / second 64-deep step and those of the high word its
+// third / fourth (the lane's half of step s is block 2 s + l / 32).
+__device__ __forceinline__ uint2 mx_scales(const int8_t* side, int row, int lane) {
+  const uint2 w = *(const uint2*)(side + row * 8);
   const uint32_t sh = 8u * (uint32_t)(lane >> 5);
   return make_uint2(w.x >> sh, w.y >> sh);
 }
 
 template <int OPSEL>
 __device__ __forceinline__ v16f_t mfma_mxfp4(v4i_t a, v4i_t b, v16f_t c, uint32_t sa, uint32_t sb) {
-  typedef int v8i_t __attribute__((ext_vector_type(8)));
   const v8i_t a8 = {a[0], a[1], a[2], a[3], 0, 0, 0, 0};
   const v8i_t b8 = {b[0], b[1], b[2], b[3], 0, 0, 0, 0};
   // cbsz = blgp = 4: both operands E2M1; the scales are E8M0 bytes
@@ -2975,194 +3064,189 @@ __device__ __forceinline__ v16f_t mfma_mxfp4(v4i_t a, v4i_t b, v16f_t c, uint32_
                                                          (int)sb);
 }
 
-__device__ __forceinline__ void gemm_put(int8_t* s, int c, uint4 v) {
-  *(uint4*)(s + (c >> 3) * kGemmLd + (c & 7) * 16) = v;
-}
-
-__device__ __forceinline__ void gemm_stash(int8_t* sa, int8_t* sb, int tid, const GemmPrefetch& p) {
-  gemm_put(sa, tid, p.a0);
-  gemm_put(sa, tid + 512, p.a1);
-  gemm_put(sa, tid + 1024, p.a2);
-  gemm_put(sa, tid + 1536, p.a3);
-  gemm_put(sb, tid, p.b0);
-  gemm_put(sb, tid + 512, p.b1);
-}
-
-__device__ __forceinline__ void gemm_load_g(const hq_gemm_args& A, int64_t n0, int wn, int lane,
-                                            int64_t T, int64_t t, float (&gv)[kGemmNB]) {
+// A lane's factors for its kGemmNB weight columns, K tile h of the stage.
+__device__ __forceinline__ void gemm_side_g(const int8_t* side, int h, int wn, int lane,
+                                            float (&gv)[kGemmNB]) {
 #pragma unroll
-  for (int b = 0; b < kGemmNB; ++b) {
-    const int64_t n = min(n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31), A.N - 1);
-    gv[b] = A.g[n * T + t];
+  for (int b = 0; b < kGemmNB; ++b)
+    gv[b] = ((const float*)(side + kGemmSideG))[h * 128 + wn * (kGemmN / 2) + b * 32 + (lane & 31)];
+}
+
+// Rescale elements [e0, e0 + E) of a finished tile's partials (block
+// j = e / 16 = 2 a + b, register r = e % 16) into the fp32 accumulators.
+template <int MODE, int E>
+__device__ __forceinline__ void gemm_rescale(int e0, const typename GemmMode<MODE>::acc_t (&p)[2][kGemmNB],
+                                             const float (&gv)[kGemmNB], float (&accf)[2][kGemmNB][16]) {
+#pragma unroll
+  for (int e = e0; e < e0 + E; ++e) {
+    const int j = e >> 4, r = e & 15, a = j / kGemmNB, b = j % kGemmNB;
+    accf[a][b][r] = __builtin_fmaf((float)p[a][b][r], gv[b], accf[a][b][r]);
   }
 }
 
-// One K tile: the wave's 2 x kGemmNB MFMA blocks from LDS, then their exact
-// int32 sums rescaled by the tile's weight factors into the fp32
-// accumulators.
-// FP8: the same bytes as E4M3 on gfx950's f8f6f4 matrix cores
-// (v_mfma_scale_f32_32x32x64_f8f6f4 with both block scales 2^0), two
-// 64-deep steps per tile, 32 fragment bytes per lane (A and B read alike, so
-// the products pair identical k), fp32 tile sums.
-// MXFP4: a stage is two 128-deep K tiles, four 64-deep scaled MFMA steps
-// (v_mfma_scale_f32_32x32x64_f8f6f4): a lane's 16 fragment bytes are 32
-// E2M1 values, one MX block, scaled by its row's block scale; the fp32 sums
-// of steps 0-1 and 2-3 are each rescaled by their tile's weight factor.
-__device__ __forceinline__ void gemm_step_mx(const int8_t* sa, const int8_t* sb, int wm, int wn,
-                                             int lane, const float (&gv)[2][kGemmNB],
-                                             const uint2 (&xs)[2], const uint2 (&ws)[kGemmNB],
-                                             float (&accf)[2][kGemmNB][16]) {
-  v16f_t acc[2][kGemmNB];
+// One 128-deep K tile (tile UNIT of the stage): its MFMAs into `cur`, with
+// the previous tile's partials `prev` rescaled by `gprev` a few elements
+// after each MFMA.
+template <int MODE, int UNIT>
+__device__ __forceinline__ void gemm_tile(const int8_t* stage, int wm, int wn, int lane,
+                                          typename GemmMode<MODE>::acc_t (&cur)[2][kGemmNB],
+                                          const typename GemmMode<MODE>::acc_t (&prev)[2][kGemmNB],
+                                          const float (&gprev)[kGemmNB],
+                                          float (&accf)[2][kGemmNB][16], const uint2 (&xs)[2],
+                                          const uint2 (&ws)[kGemmNB]) {
+  using acc_t = typename GemmMode<MODE>::acc_t;
+  constexpr int STEPS = GemmMode<MODE>::STEPS;
+  constexpr int E = 64 / (STEPS * 2 * kGemmNB);  // rescaled elements per MFMA
+  const int8_t* sa = stage;
+  const int8_t* sb = stage + kGemmStageA;
+  const int h = lane >> 5;
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const int koff = ks * 32 + (lane >> 5) * 16;
-    v4i_t fa[2], fb[kGemmNB];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-      fa[a] = *(const v4i_t*)(sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff);
-#pragma unroll
-    for (int b = 0; b < kGemmNB; ++b)
-      fb[b] = *(const v4i_t*)(sb + (wn * (kGemmN / 2) + b * 32 + (lane & 31)) * kGemmLd + koff);
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b) {
-        const uint32_t xa = ks < 2 ? xs[a].x : xs[a].y, wb = ks < 2 ? ws[b].x : ws[b].y;
-        const v16f_t c0 = (ks & 1) ? acc[a][b] : (v16f_t){};
-        acc[a][b] = (ks & 1) ? mfma_mxfp4<2>(fa[a], fb[b], c0, xa, wb)
-                             : mfma_mxfp4<0>(fa[a], fb[b], c0, xa, wb);
-      }
-    if (ks & 1) {
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < kGemmNB; ++b)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            accf[a][b][r] = __builtin_fmaf(acc[a][b][r], gv[ks >> 1][b], accf[a][b][r]);
-    }
-  }
-}
-
-template <bool FP8>
-__device__ __forceinline__ void gemm_step(const int8_t* sa, const int8_t* sb, int wm, int wn,
-                                          int lane, const float (&gv)[kGemmNB],
-                                          float (&accf)[2][kGemmNB][16]) {
-  if constexpr (FP8) {
-    typedef int v8i_t __attribute__((ext_vector_type(8)));
-    v16f_t acc[2][kGemmNB];
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const int koff = ks * 64 + (lane >> 5) * 32;
+  for (int s = 0; s < STEPS; ++s) {
+    if constexpr (MODE == 1) {
+      // 64-deep E4M3 step: 32 bytes a lane, chunks 4 s + 2 h and the next
       v8i_t fa[2], fb[kGemmNB];
 #pragma unroll
       for (int a = 0; a < 2; ++a) {
-        const int8_t* q = sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff;
-        const v4i_t lo = *(const v4i_t*)q, hi = *(const v4i_t*)(q + 16);
+        const int row = wm * 64 + a * 32 + (lane & 31);
+        const v4i_t lo = gemm_frag(sa, row, 4 * s + 2 * h), hi = gemm_frag(sa, row, 4 * s + 2 * h + 1);
         fa[a] = (v8i_t){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       }
 #pragma unroll
       for (int b = 0; b < kGemmNB; ++b) {
-        const int8_t* q = sb + (wn * (kGemmN / 2) + b * 32 + (lane & 31)) * kGemmLd + koff;
-        const v4i_t lo = *(const v4i_t*)q, hi = *(const v4i_t*)(q + 16);
+        const int row = wn * (kGemmN / 2) + b * 32 + (lane & 31);
+        const v4i_t lo = gemm_frag(sb, row, 4 * s + 2 * h), hi = gemm_frag(sb, row, 4 * s + 2 * h + 1);
         fb[b] = (v8i_t){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       }
 #pragma unroll
       for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int b = 0; b < kGemmNB; ++b)
+        for (int b = 0; b < kGemmNB; ++b) {
           // cbsz = blgp = 0: both operands E4M3; scale bytes 127 (2^0)
-          acc[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-              fa[a], fb[b], ks == 0 ? (v16f_t){} : acc[a][b], 0, 0, 0, 127, 0, 127);
+          cur[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+              fa[a], fb[b], s == 0 ? (acc_t){} : cur[a][b], 0, 0, 0, 127, 0, 127);
+          gemm_rescale<MODE, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
+        }
+    } else {
+      // int8: 32-deep step, chunk 2 s + h; MXFP4: 64-deep step ks = 2 UNIT + s,
+      // chunk 2 ks + h (32 E2M1 values, one MX block)
+      const int c = MODE == 2 ? 2 * (2 * UNIT + s) + h : 2 * s + h;
+      v4i_t fa[2], fb[kGemmNB];
+#pragma unroll
+      for (int a = 0; a < 2; ++a) fa[a] = gemm_frag(sa, wm * 64 + a * 32 + (lane & 31), c);
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b) fb[b] = gemm_frag(sb, wn * (kGemmN / 2) + b * 32 + (lane & 31), c);
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < kGemmNB; ++b) {
+          if constexpr (MODE == 0) {
+            cur[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], s == 0 ? (acc_t){} : cur[a][b],
+                                                              0, 0, 0);
+          } else {
+            constexpr int ks = 2 * UNIT;  // + s: the scale byte of step ks is byte 2 (ks % 2) of word ks / 2
+            const uint32_t xa = UNIT == 0 ? xs[a].x : xs[a].y, wb = UNIT == 0 ? ws[b].x : ws[b].y;
+            cur[a][b] = s == 0 ? mfma_mxfp4<0>(fa[a], fb[b], (acc_t){}, xa, wb)
+                               : mfma_mxfp4<2>(fa[a], fb[b], cur[a][b], xa, wb);
+            (void)ks;
+          }
+          gemm_rescale<MODE, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
+        }
     }
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) accf[a][b][r] = __builtin_fmaf(acc[a][b][r], gv[b], accf[a][b][r]);
-    return;
   }
-  v16i_t acc[2][kGemmNB];
+  // Pin the interleave for the scheduler: a step's fragment reads, then each
+  // MFMA followed by its share of the rescale (int8: a convert and an fma per
+  // element).
+  constexpr int DSR = MODE == 1 ? 8 : 4;  // 16-byte LDS reads per step
+  constexpr int VPM = MODE == 0 ? 2 * E : E;
 #pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    const int koff = ks * 32 + (lane >> 5) * 16;
-    v4i_t fa[2], fb[kGemmNB];
+  for (int s = 0; s < STEPS; ++s) {
+    __builtin_amdgcn_sched_group_barrier(0x100, DSR, 0);
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
-      fa[a] = *(const v4i_t*)(sa + (wm * 64 + a * 32 + (lane & 31)) * kGemmLd + koff);
-#pragma unroll
-    for (int b = 0; b < kGemmNB; ++b)
-      fb[b] = *(const v4i_t*)(sb + (wn * (kGemmN / 2) + b * 32 + (lane & 31)) * kGemmLd + koff);
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b)
-        acc[a][b] = ks == 0 ? __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], (v16i_t){}, 0, 0, 0)
-                            : __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    for (int i = 0; i < 2 * kGemmNB; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);
+    }
   }
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < kGemmNB; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        accf[a][b][r] = __builtin_fmaf((float)acc[a][b][r], gv[b], accf[a][b][r]);
 }
 
 // MODE 0: int8, 1: fp8 (E4M3), 2: MXFP4.
 template <int MODE>
 __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
-  extern __shared__ __attribute__((aligned(16))) int8_t gsm[];
-  int8_t* const sa = gsm;                    // stage s at sa + s * kGemmStageA
-  int8_t* const sb = gsm + 2 * kGemmStageA;  // stage s at sb + s * kGemmStageB
+  using acc_t = typename GemmMode<MODE>::acc_t;
+  constexpr int SB = gemm_stage_bytes<MODE>();
+  extern __shared__ __attribute__((aligned(16))) int8_t gsm[];  // ring slot s at gsm + s * SB
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
-  const int64_t T = A.K / HQ_TILE;                    // 128-deep K tiles (weight factors)
-  const int64_t TS = MODE == 2 ? T / 2 : T;          // LDS stages of 128 bytes per row
+  const int64_t T = A.K / HQ_TILE;                            // 128-deep K tiles
+  const int64_t TS = T / GemmMode<MODE>::U;                   // LDS stages
 
   float accf[2][kGemmNB][16];
+  acc_t acc0[2][kGemmNB], acc1[2][kGemmNB];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < kGemmNB; ++b)
+    for (int b = 0; b < kGemmNB; ++b) {
+      acc1[a][b] = (acc_t){};  // the "previous tile" of the first: zero, factor 0
 #pragma unroll
       for (int r = 0; r < 16; ++r) accf[a][b][r] = 0.0f;
-
-  GemmPrefetch pf;
-  gemm_load(A, m0, n0, 0, tid, pf);
-  gemm_stash(sa, sb, tid, pf);
-  __syncthreads();
-  gemm_load(A, m0, n0, min<int64_t>(1, TS - 1), tid, pf);
-
-  // stage t from buffer t & 1; the prefetched stage t + 1 goes to the other
-  // buffer (free since the last barrier) and stage t + 2's loads start
-  for (int64_t t = 0; t < TS; ++t) {
-    const int st = (int)(t & 1);
-    if constexpr (MODE == 2) {
-      float gv[2][kGemmNB];
-      gemm_load_g(A, n0, wn, lane, T, 2 * t, gv[0]);
-      gemm_load_g(A, n0, wn, lane, T, 2 * t + 1, gv[1]);
-      uint2 xs[2], ws[kGemmNB];
+    }
+  float gprev[kGemmNB];
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
-        xs[a] = mx_scales(A.xs, m0 + wm * 64 + a * 32 + (lane & 31), A.M, A.K, t, lane);
+  for (int b = 0; b < kGemmNB; ++b) gprev[b] = 0.0f;
+
+  const int wsc = __builtin_amdgcn_readfirstlane(wave);  // wave-uniform, in a scalar register
+  const GemmLoads gl = gemm_loads<MODE>(A, m0, n0, wsc, lane);
+  // Stage t sits in ring slot t % 3.  Before it is read: this wave's loads
+  // of stage t are done (only stage t + 1's, issued later, may be in
+  // flight), its LDS reads of stage t - 1 have returned, and every wave has
+  // got that far; then slot (t + 2) % 3, last read as stage t - 1, takes
+  // stage t + 2 (the last stage is fetched again near the end, into a slot
+  // no wave reads).  A bare barrier: the loads still in flight are not
+  // waited for.
+  constexpr int NL = MODE == 2 ? 9 : 7;  // buffer loads per wave and stage
+  auto begin_stage = [&](int64_t t) -> const int8_t* {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NL) : "memory");
+    gemm_fetch<MODE>(gl, min(t + 2, TS - 1), wsc, gsm + ((t + 2) % 3) * SB);
+    return gsm + (t % 3) * SB;
+  };
+  uint2 xs[2], ws[kGemmNB];
+  gemm_fetch<MODE>(gl, 0, wsc, gsm);
+  gemm_fetch<MODE>(gl, min<int64_t>(1, TS - 1), wsc, gsm + SB);
+  if constexpr (MODE == 2) {
+    // two K tiles per stage: tile 0 into acc0 (rescaling acc1), tile 1 into acc1
+    for (int64_t t = 0; t < TS; ++t) {
+      const int8_t* const stage = begin_stage(t);
+      const int8_t* const side = stage + kGemmStageA + kGemmStageB;
+#pragma unroll
+      for (int a = 0; a < 2; ++a) xs[a] = mx_scales(side + kGemmSideXs, wm * 64 + a * 32 + (lane & 31), lane);
 #pragma unroll
       for (int b = 0; b < kGemmNB; ++b)
-        ws[b] = mx_scales(A.ws, n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31), A.N, A.K, t, lane);
-      gemm_step_mx(sa + st * kGemmStageA, sb + st * kGemmStageB, wm, wn, lane, gv, xs, ws, accf);
-    } else {
-      float gv[kGemmNB];
-      gemm_load_g(A, n0, wn, lane, T, t, gv);
-      gemm_step<MODE == 1>(sa + st * kGemmStageA, sb + st * kGemmStageB, wm, wn, lane, gv, accf);
+        ws[b] = mx_scales(side + kGemmSideWs, wn * (kGemmN / 2) + b * 32 + (lane & 31), lane);
+      float g0[kGemmNB], g1[kGemmNB];
+      gemm_side_g(side, 0, wn, lane, g0);
+      gemm_side_g(side, 1, wn, lane, g1);
+      gemm_tile<MODE, 0>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+      gemm_tile<MODE, 1>(stage, wm, wn, lane, acc1, acc0, g0, accf, xs, ws);
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b) gprev[b] = g1[b];
     }
-    if (t + 1 < TS) {
-      gemm_stash(sa + (st ^ 1) * kGemmStageA, sb + (st ^ 1) * kGemmStageB, tid, pf);
-      __syncthreads();
-      gemm_load(A, m0, n0, min(t + 2, TS - 1), tid, pf);  // the last stage again at the end
+  } else {
+    // one K tile per stage and an even number of stages (K is a multiple of
+    // 256): stage t into acc0, stage t + 1 into acc1
+    for (int64_t t = 0; t < TS; t += 2) {
+      float g0[kGemmNB], g1[kGemmNB];
+      const int8_t* stage = begin_stage(t);
+      gemm_side_g(stage + kGemmStageA + kGemmStageB, 0, wn, lane, g0);
+      gemm_tile<MODE, 0>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+      stage = begin_stage(t + 1);
+      gemm_side_g(stage + kGemmStageA + kGemmStageB, 0, wn, lane, g1);
+      gemm_tile<MODE, 0>(stage, wm, wn, lane, acc1, acc0, g0, accf, xs, ws);
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b) gprev[b] = g1[b];
     }
   }
+  gemm_rescale<MODE, 64>(0, acc1, gprev, accf);  // the last tile's partials
 
 #pragma unroll
   for (int a = 0; a < 2; ++a)
@@ -3184,15 +3268,15 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
     }
 }
 
-__global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_i8_kernel(hq_gemm_args A) {
+__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_i8_kernel(hq_gemm_args A) {
   gemm_body<0>(A);
 }
 
-__global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_f8_kernel(hq_gemm_args A) {
+__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_f8_kernel(hq_gemm_args A) {
   gemm_body<1>(A);
 }
 
-__global__ __launch_bounds__(kGemmThreads, 2) void hq_gemm_mx4_kernel(hq_gemm_args A) {
+__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_mx4_kernel(hq_gemm_args A) {
   gemm_body<2>(A);
 }
 
@@ -3413,27 +3497,28 @@ int hq_launch_act_prep(const hq_actprep_args& a, void* stream) {
 }
 
 int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
-  if (a.K % HQ_TILE != 0 || (a.fp8 == 2 && a.K % 256 != 0)) return -1;
+  if (a.K % 256 != 0) return -1;  // an even number of 128-deep K tiles
   static bool lds_set = false;  // more than 64 KB of dynamic LDS needs an opt-in
   if (!lds_set) {
     hipError_t e = hipFuncSetAttribute((const void*)hq_gemm_i8_kernel,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<0>());
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void*)hq_gemm_f8_kernel,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+                              hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<1>());
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void*)hq_gemm_mx4_kernel,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, kGemmLds);
+                              hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<2>());
     if (e != hipSuccess) return (int)e;
     lds_set = true;
   }
   const dim3 grid((uint32_t)((a.N + kGemmN - 1) / kGemmN), (uint32_t)((a.M + kGemmM - 1) / kGemmM));
+  hipStream_t st = (hipStream_t)stream;
   if (a.fp8 == 2)
-    hipLaunchKernelGGL(hq_gemm_mx4_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
+    hipLaunchKernelGGL(hq_gemm_mx4_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<2>(), st, a);
   else if (a.fp8)
-    hipLaunchKernelGGL(hq_gemm_f8_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
+    hipLaunchKernelGGL(hq_gemm_f8_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<1>(), st, a);
   else
-    hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(kGemmThreads), kGemmLds, (hipStream_t)stream, a);
+    hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<0>(), st, a);
   return (int)hipGetLastError();
 }
 
