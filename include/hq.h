@@ -66,7 +66,13 @@ typedef struct {
                            forward call (Sec. 4.4, App. A) comes from the row
                            index, which keeps counting across appends. */
   int32_t norm_dtype;   /* HQ_FP32 (default) or HQ_FP16 (KV, Sec. 6.6) */
-  int32_t substream;    /* symbols per sub-stream S (Sec. 5.3); 0 = 512 */
+  int32_t substream;    /* symbols per sub-stream S (Sec. 5.3): 0 = 512; 1024 and
+                           2048 for weight plans (no rotation, no dither, fp32
+                           norms; any tile), whose encode / decode keep one
+                           Rice k and one word offset per S symbols.  The casts
+                           (int8 / fp8 / MXFP4), the fused GEMV and attention,
+                           and the group calls take S = 512 only
+                           (HQ_ERR_UNSUPPORTED otherwise). */
   int32_t use_snr;      /* 1 = take snr_db below instead of the table lookup */
   int32_t reserved0;
   double snr_db;        /* quantization SNR in dB (App. B) when use_snr = 1 */

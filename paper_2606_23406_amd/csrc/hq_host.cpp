@@ -253,7 +253,11 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
   if (o.rotation == HQ_ROT_QJL && !o.qjl) return HQ_ERR_INVALID_ARG;
   if (o.norm_dtype != 0 && o.norm_dtype != HQ_FP32 && o.norm_dtype != HQ_FP16)
     return HQ_ERR_INVALID_ARG;
-  if (S != HQ_SUB) return HQ_ERR_UNSUPPORTED;
+  // sub-streams of 1024 or 2048 symbols (two or four 512-symbol blocks) are
+  // built for weight plans: no rotation, no dither, fp32 norms
+  if (S != HQ_SUB && ((S != 2 * HQ_SUB && S != 4 * HQ_SUB) || o.rotation != HQ_ROT_NONE ||
+                      o.dither || o.norm_dtype == HQ_FP16))
+    return HQ_ERR_UNSUPPORTED;
   // tiles of 256 .. 2048 (the sweep of Sec. 7.2) are built for weight plans:
   // no rotation, no dither, fp32 norms
   if (tile != HQ_TILE &&
@@ -390,7 +394,8 @@ static int32_t encode_spw(int64_t nsub, bool allow_small) {
 
 size_t hq_scan_bytes(hq_plan_t p, int64_t rows) {
   if (!p || rows < 0) return 0;
-  const int64_t nwg = (rows * p->spr + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
+  // one workgroup per 16 blocks of 512 symbols
+  const int64_t nwg = (rows * p->spr * (p->substream / HQ_SUB) + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
   // the epoch word, then a look-back status word and a stats word per workgroup
   return (size_t)HQ_SCAN_STATUS_OFFSET +
          2 * sizeof(unsigned long long) * (size_t)std::max<int64_t>(nwg, 1);
@@ -424,8 +429,9 @@ static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t 
     }
     return HQ_OK;
   }
-  const int32_t spw = p->tile != HQ_TILE ? HQ_ENC_SUBS_PER_WAVE : encode_spw(nsub, allow_small);
-  const int64_t nwg = (nsub + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
+  const int32_t mb = p->substream / HQ_SUB;  // 512-symbol blocks per sub-stream
+  const int32_t spw = (p->tile != HQ_TILE || mb > 1) ? HQ_ENC_SUBS_PER_WAVE : encode_spw(nsub, allow_small);
+  const int64_t nwg = (nsub * mb + HQ_ENC_SUBS_PER_WG - 1) / HQ_ENC_SUBS_PER_WG;
   if (nwg > 0x7FFFFFFF) return HQ_ERR_UNSUPPORTED;
   if ((size_t)s->scan_bytes < hq_scan_bytes(p, rows)) return HQ_ERR_CAPACITY;
 
@@ -463,6 +469,7 @@ static hq_status encode_prepare(hq_plan_t p, const void* x, int32_t xt, int64_t 
   a.alpha = p->alpha;
   a.alpha_half = 0.5f * p->alpha;
   a.tile = p->tile;
+  a.mb = mb;
   *nwg_out = nwg;
   return HQ_OK;
 }
@@ -516,7 +523,7 @@ hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t 
   if (count < 0 || (count > 0 && (!plans || !x || !rows || !ld || !s))) return HQ_ERR_INVALID_ARG;
   for (int32_t i = 0; i < count; ++i) {
     if (!plans[i] || !s[i] || !same_kernel_family(plans[0], plans[i])) return HQ_ERR_INVALID_ARG;
-    if (plans[i]->rotation == HQ_ROT_QJL || plans[i]->tile != HQ_TILE)
+    if (plans[i]->rotation == HQ_ROT_QJL || plans[i]->tile != HQ_TILE || plans[i]->substream != HQ_SUB)
       return HQ_ERR_UNSUPPORTED;  // single calls only
     for (int32_t j = 0; j < i; ++j)
       if (s[j] == s[i] || s[j]->scan == s[i]->scan) return HQ_ERR_INVALID_ARG;
@@ -575,6 +582,7 @@ static void fill_decode_args(const hq_plan_s* p, const hq_stream* s, int64_t row
   a->alpha = p->alpha;
   a->alpha_n = p->alpha * (float)p->tile;
   a->tile = p->tile;
+  a->mb = p->substream / HQ_SUB;
 }
 
 hq_status hq_decode(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows, void* y,
@@ -602,7 +610,8 @@ hq_status hq_decode_gemv(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t 
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if ((xt != HQ_BF16 && xt != HQ_FP32) || (yt != HQ_BF16 && yt != HQ_FP32)) return HQ_ERR_INVALID_ARG;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
-  if (p->rotation || p->dither || p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;
+  if (p->rotation || p->dither || p->tile != HQ_TILE || p->substream != HQ_SUB)
+    return HQ_ERR_UNSUPPORTED;
   if (rows == 0) return HQ_OK;
   if (!x || !y || !workspace || !s->payload || !s->offsets || !s->kparam || !s->norms)
     return HQ_ERR_INVALID_ARG;
@@ -709,7 +718,7 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
   for (int32_t i = 0; i < count; ++i)
     if (!plans[i] || !s[i] || !same_kernel_family(plans[0], plans[i])) return HQ_ERR_INVALID_ARG;
   for (int32_t i = 0; i < count; ++i)
-    if (plans[i]->rotation == HQ_ROT_QJL || plans[i]->tile != HQ_TILE)
+    if (plans[i]->rotation == HQ_ROT_QJL || plans[i]->tile != HQ_TILE || plans[i]->substream != HQ_SUB)
       return HQ_ERR_UNSUPPORTED;  // single calls only
   const int64_t esz = (yt == HQ_BF16) ? 2 : 4;
   for (int32_t b = 0; b < count; b += HQ_GROUP_MAX) {
@@ -745,7 +754,8 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
 
 hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                          int8_t* codes, int64_t ldc, float* g, void* stream) {
-  if (p && p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;  // the GEMM's K tiles are 128
+  // the GEMM's K tiles are 128; sub-streams of 512
+  if (p && (p->tile != HQ_TILE || p->substream != HQ_SUB)) return HQ_ERR_UNSUPPORTED;
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
@@ -762,7 +772,8 @@ hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t 
 
 hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                         uint8_t* codes, int64_t ldc, float* g, void* stream) {
-  if (p && p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;  // the GEMM's K tiles are 128
+  // the GEMM's K tiles are 128; sub-streams of 512
+  if (p && (p->tile != HQ_TILE || p->substream != HQ_SUB)) return HQ_ERR_UNSUPPORTED;
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
@@ -779,7 +790,8 @@ hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t r
 
 hq_status hq_decode_mxfp4(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                           uint8_t* codes, uint8_t* scales, float* g, void* stream) {
-  if (p && p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;  // the GEMM's K tiles are 128
+  // the GEMM's K tiles are 128; sub-streams of 512
+  if (p && (p->tile != HQ_TILE || p->substream != HQ_SUB)) return HQ_ERR_UNSUPPORTED;
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;

@@ -71,6 +71,7 @@ struct hq_encode_args {
   uint32_t lds_words;     // per-sub-stream assembly buffer, in words
   uint32_t spw;           // sub-streams per wave: HQ_ENC_SUBS_PER_WAVE, or 1 for small launches
   int32_t tile;           // RHT tile (128, or 256 .. 2048 for weight plans)
+  int32_t mb;             // 512-symbol blocks per sub-stream (S / 512: 1, 2 or 4)
   uint64_t dither_seed;
   float alpha;
   float alpha_half;       // alpha / 2, exact (the E8 decision works on z / 2)
@@ -108,6 +109,7 @@ struct hq_decode_args {
   float alpha;
   float alpha_n;           // alpha * tile, exact
   int32_t tile;            // RHT tile (128, or 256 .. 2048 for weight plans)
+  int32_t mb;              // 512-symbol blocks per sub-stream (S / 512: 1, 2 or 4)
   const float* qjl;        // qjl rotation: S (row-major) and S^T, or null
   const float* qjlt;
 };

@@ -1172,6 +1172,69 @@ __device__ __forceinline__ float quad_bcast(float v) {
   return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), I * 0x55, 0xF, 0xF, true));
 }
 
+// The lane's 8 remainder fields (k0 / k1 bits by class, packed in symbol
+// order), ORed into the buffer at bit rpos.
+template <int LAT>
+__device__ __forceinline__ void put_remainders(uint32_t* buf, uint32_t rpos, const uint32_t (&sym)[8],
+                                               uint32_t k0, uint32_t k1, uint32_t lrem) {
+  if (lrem <= 32) {
+    uint32_t acc = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+      acc = lshl_or_s(sym[j] & ((1u << kk) - 1u), readfirst(rem_offset<LAT>(j, k0, k1)), acc);
+    }
+    or_word(buf, rpos, acc);
+  } else if (lrem <= 64) {
+    uint64_t acc = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+      acc |= (uint64_t)(sym[j] & ((1u << kk) - 1u)) << rem_offset<LAT>(j, k0, k1);
+    }
+    or_bits64(buf, rpos, acc);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+      or_bits64(buf, rpos + rem_offset<LAT>(j, k0, k1), sym[j] & ((1u << kk) - 1u));
+    }
+  }
+}
+
+// The lane's 8 unary codes (q zeros and a one each, ulen bits in all),
+// ORed into the buffer from bit upos.
+__device__ __forceinline__ void put_unary(uint32_t* buf, uint32_t upos, const uint32_t (&qv)[8],
+                                          uint32_t ulen) {
+  if (ulen <= 32) {
+    uint32_t m = 0, t = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      t += qv[j];
+      m = bit_or(t, m);
+      t += 1;
+    }
+    or_word(buf, upos, m);
+  } else if (ulen <= 64) {
+    uint64_t m = 0;
+    uint32_t t = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      t += qv[j];
+      m |= 1ull << t;
+      t += 1;
+    }
+    or_bits64(buf, upos, m);
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      upos += qv[j];
+      or_bits64(buf, upos, 1ull);
+      upos += 1;
+    }
+  }
+}
+
 template <int LAT, int XT, bool KV>
 __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const hq_rice_thr& T,
                                                  const SubPos& P, int lane, float* x, float scale_tw,
@@ -1333,59 +1396,9 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   __builtin_amdgcn_wave_barrier();
   if (active && !overflow) {
     // remainder fields, packed per lane
-    const uint32_t rpos = __umul24((uint32_t)lane, lrem);  // lrem < 2^24
-    if (lrem <= 32) {
-      uint32_t acc = 0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-        acc = lshl_or_s(sym[j] & ((1u << kk) - 1u), readfirst(rem_offset<LAT>(j, k0, k1)), acc);
-      }
-      or_word(buf, rpos, acc);
-    } else if (lrem <= 64) {
-      uint64_t acc = 0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-        acc |= (uint64_t)(sym[j] & ((1u << kk) - 1u)) << rem_offset<LAT>(j, k0, k1);
-      }
-      or_bits64(buf, rpos, acc);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
-        or_bits64(buf, rpos + rem_offset<LAT>(j, k0, k1), sym[j] & ((1u << kk) - 1u));
-      }
-    }
-    // unary codes: q zeros and a one each
-    uint32_t upos = R + uoff;
-    if (ulen <= 32) {
-      uint32_t m = 0, t = 0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        t += qv[j];
-        m = bit_or(t, m);
-        t += 1;
-      }
-      or_word(buf, upos, m);
-    } else if (ulen <= 64) {
-      uint64_t m = 0;
-      uint32_t t = 0;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        t += qv[j];
-        m |= 1ull << t;
-        t += 1;
-      }
-      or_bits64(buf, upos, m);
-    } else {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        upos += qv[j];
-        or_bits64(buf, upos, 1ull);
-        upos += 1;
-      }
-    }
+    put_remainders<LAT>(buf, __umul24((uint32_t)lane, lrem), sym, k0, k1, lrem);  // lrem < 2^24
+    // unary codes
+    put_unary(buf, R + uoff, qv, ulen);
   }
   W_out = W;
   kb_out = overflow ? 0u : (LAT == kA2 ? (k0 | (k1 << 4)) : k0);
@@ -1393,14 +1406,157 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   overflow_out = overflow;
 }
 
+// One sub-stream of B consecutive 512-symbol blocks (S = 512 B, weight
+// plans): x[b] holds block b's transformed values and scl[b] its tile scale.
+// Every block is quantized and stripped first; the Rice parameters then
+// follow from the whole sub-stream's symbols (the sums and the k* / k* + 1
+// decision taken over all S symbols), and the split layout places the S
+// remainder fields (block b's at bit b 64 lrem) before the S unary codes
+// (block b's after the unary bits of blocks 0 .. b - 1).
+template <int LAT, int B>
+__device__ __forceinline__ void encode_multiblock(const hq_encode_args& A, const hq_rice_thr& T,
+                                                  bool active, int lane, float (*x)[8],
+                                                  const float* scl, uint32_t tsig, uint32_t* buf,
+                                                  uint32_t& W_out, uint32_t& kb_out,
+                                                  uint32_t& bits_out, bool& overflow_out) {
+  constexpr uint32_t S = (uint32_t)HQ_SUB * B;
+  uint32_t sym[B][8];
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    float z[8];
+    const float sc = xor_sign(scl[b], tsig);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) z[i] = x[b][i] * sc;
+    if constexpr (LAT == kE8) {
+      int32_t h[8], cb;
+      e8_nearest(z, h, cb);
+      e8_strip(h, cb, sym[b]);
+    } else {
+      int32_t c[8];
+      quantize8<LAT>(z, c);
+      bool huge = false;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) huge = huge || (c[i] > 65536 || c[i] < -65536);
+      if (huge || !active) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) c[i] = 0;
+      }
+      strip8<LAT>(c, sym[b]);
+    }
+  }
+  // ---- Rice parameters over the whole sub-stream (wave-uniform)
+  uint32_t k0, k1;
+  if (A.rice_k >= 0) {
+    k0 = (uint32_t)A.rice_k;
+    k1 = (LAT == kD4) ? (k0 > 0 ? k0 - 1 : 0) : k0;
+  } else if constexpr (LAT == kE8 || LAT == kZ) {
+    uint32_t s0 = 0;
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) s0 += sym[b][j];
+    const uint32_t a0 = kstar_count(wave_total(s0), T.thr0);
+    // k* + 1 saves sum((m >> k*) - (m >> (k* + 1))) unary bits for S remainder bits
+    uint32_t g = 0;
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t q = sym[b][j] >> a0;
+        g += q - (q >> 1);
+      }
+    k0 = (a0 < HQ_KMAX && wave_total(g) > S) ? a0 + 1 : a0;
+    k1 = k0;
+  } else {
+    uint32_t s0 = 0, s1 = 0;
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (sym_class<LAT>(j)) s1 += sym[b][j]; else s0 += sym[b][j];
+      }
+    const uint32_t a0 = kstar_count(wave_total(s0), T.thr0);
+    const uint32_t a1 = (LAT == kA2) ? kstar_count(wave_total(s1), T.thr1) : 0u;
+    const uint32_t b0 = a0 < HQ_KMAX ? a0 + 1 : a0;
+    const uint32_t b1 = a1 < HQ_KMAX ? a1 + 1 : a1;
+    uint32_t g0 = 0, g1 = 0;
+#pragma unroll
+    for (int b = 0; b < B; ++b)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t m = sym[b][j];
+        if (LAT == kD4) {
+          const uint32_t ka = sym_class<LAT>(j) ? (a0 > 0 ? a0 - 1 : 0) : a0;
+          const uint32_t kb = sym_class<LAT>(j) ? (b0 > 0 ? b0 - 1 : 0) : b0;
+          g0 += (m >> ka) - (m >> kb);
+        } else if (sym_class<LAT>(j)) {
+          g1 += (m >> a1) - (m >> b1);
+        } else {
+          g0 += (m >> a0) - (m >> b0);
+        }
+      }
+    const uint32_t gain0 = wave_total(g0);
+    // one more remainder bit on each symbol of the class (D4: 3 S / 4 of
+    // class 0, S / 4 of class 1; A2: S / 2 each)
+    const uint32_t cost0 = (LAT == kD4)
+                               ? (b0 - a0) * (3u * S / 4u) +
+                                     ((b0 > 0 ? b0 - 1 : 0) - (a0 > 0 ? a0 - 1 : 0)) * (S / 4u)
+                               : (b0 - a0) * (S / 2u);
+    k0 = gain0 > cost0 ? b0 : a0;
+    if (LAT == kA2) {
+      const uint32_t gain1 = wave_total(g1);
+      k1 = gain1 > (b1 - a1) * (S / 2u) ? b1 : a1;
+    } else {
+      k1 = k0 > 0 ? k0 - 1 : 0;
+    }
+  }
+  // ---- code lengths: the B remainder regions, then the B unary regions
+  const uint32_t lrem = lane_rem_bits<LAT>(k0, k1);
+  const uint32_t Rb = 64 * lrem, Rt = (uint32_t)B * Rb;
+  uint32_t ulen[B], uincl[B], U = 0;
+#pragma unroll
+  for (int b = 0; b < B; ++b) {
+    ulen[b] = 8;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ulen[b] += sym[b][j] >> (sym_class<LAT>(j) ? k1 : k0);
+    uincl[b] = wave_scan_incl(ulen[b]);
+    U += __builtin_amdgcn_readlane(uincl[b], 63);
+  }
+  uint32_t W = (Rt + U + 31) >> 5;
+  // a sub-stream past the plan's bound is written as S zero symbols with k = 0
+  const bool overflow = active && W > A.lds_words;
+  if (!active) W = 0;
+  if (overflow) W = S / 32;
+  for (uint32_t w = lane; w < W; w += 64) buf[w] = overflow ? 0xFFFFFFFFu : 0u;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  if (active && !overflow) {
+    uint32_t ubase = Rt;  // where block b's unary codes begin
+#pragma unroll
+    for (int b = 0; b < B; ++b) {
+      uint32_t qv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) qv[j] = sym[b][j] >> (sym_class<LAT>(j) ? k1 : k0);
+      put_remainders<LAT>(buf, (uint32_t)b * Rb + __umul24((uint32_t)lane, lrem), sym[b], k0, k1, lrem);
+      put_unary(buf, ubase + uincl[b] - ulen[b], qv, ulen[b]);
+      ubase += __builtin_amdgcn_readlane(uincl[b], 63);
+    }
+  }
+  W_out = W;
+  kb_out = overflow ? 0u : (LAT == kA2 ? (k0 | (k1 << 4)) : k0);
+  bits_out = overflow ? S : Rt + U;
+  overflow_out = overflow;
+}
+
 // TILED: a plan whose tile is not 128 (weights only: no rotation or
 // dither); the wave takes four consecutive sub-streams, so that every tile
 // of up to 2048 scalars lies inside one wave.
-template <int LAT, int XT, bool KV, int SPW, bool TILED = false>
+template <int LAT, int XT, bool KV, int SPW, bool TILED = false, int MB = 1>
 __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice_thr& T,
                                           const uint32_t wg) {
   static_assert(SPW == 1 || SPW == 4, "one or four sub-streams per wave");
   static_assert(!TILED || (SPW == 4 && !KV), "long tiles: four sub-streams per wave, weights");
+  static_assert(MB == 1 || (TILED && (MB == 2 || MB == 4)), "multi-block sub-streams: long-tile front end");
   constexpr int NSUB = HQ_ENC_SUBS_PER_WG;  // sub-streams per workgroup
   constexpr int WAVES = NSUB / SPW;         // wave64s per workgroup
   extern __shared__ uint32_t smem[];
@@ -1415,18 +1571,22 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     s_epoch = (uint32_t)__hip_atomic_load(A.epoch, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) &
               kEpochMask;
   const TwSigns sg(lane);
+  // sub-streams of MB > 1 consecutive 512-symbol blocks (the long-tile
+  // front end, any tile): positions below count blocks
+  constexpr uint32_t mb = (uint32_t)MB;
+  const uint32_t nblk = (uint32_t)A.nsub * mb;
 
   // ---- this wave's sub-streams: wg * NSUB + i * WAVES + wave, i < SPW (row and
   //      column advanced on scalar registers)
   SubPos pos[SPW];
   {
-    const uint32_t spr = (uint32_t)A.spr;
+    const uint32_t spr = (uint32_t)A.spr * mb;
     const uint32_t step = TILED ? 1u : (uint32_t)WAVES;
     const uint32_t sub0 = wg * NSUB + (uint32_t)wave * (TILED ? (uint32_t)SPW : 1u);
     uint32_t row = sub0 / spr, c = sub0 - row * spr;
 #pragma unroll
     for (int i = 0; i < SPW; ++i) {
-      pos[i].active = sub0 + (uint32_t)i * step < (uint32_t)A.nsub;
+      pos[i].active = sub0 + (uint32_t)i * step < nblk;
       pos[i].lrow = pos[i].active ? row : 0u;
       pos[i].col0 = pos[i].active ? c * HQ_SUB : 0u;
       c += step;
@@ -1562,6 +1722,34 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
 
   // ---- quantize and Rice-code each sub-stream into its LDS buffer
   uint32_t padsum = 0;
+  if constexpr (MB > 1) {
+    // sub-streams of MB blocks: the wave's four blocks are 4 / MB of them,
+    // sub-stream ls of the group in buffer ls (s_words past the group's
+    // 16 / MB sub-streams stay 0)
+    constexpr uint32_t ns = (uint32_t)NSUB / MB;
+    if (lane == 0 && wave == 0)
+      for (uint32_t q = ns; q < (uint32_t)NSUB; ++q) s_words[q] = 0;
+#pragma unroll
+    for (int j = 0; j < SPW / MB; ++j) {
+      const uint32_t ls = (uint32_t)wave * (uint32_t)(SPW / MB) + (uint32_t)j;
+      const uint32_t gs = wg * ns + ls;
+      const bool act = pos[j * MB].active;
+      uint32_t W, kb, bits;
+      bool ovf;
+      encode_multiblock<LAT, MB>(A, T, act, lane, xt + j * MB, ss + j * MB, tsig, smem + ls * stride,
+                                 W, kb, bits, ovf);
+      if (act) {
+        if (lane == 0) {
+          A.kparam[A.first_sub + gs] = (uint8_t)kb;
+          s_words[ls] = W;
+          if (ovf && A.stats) atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_OVERFLOW);
+        }
+        padsum += W * 32u - bits;
+      } else if (lane == 0) {
+        s_words[ls] = 0;
+      }
+    }
+  } else
 #pragma unroll
   for (int i = 0; i < SPW; ++i) {
     // 128-tiles: neighbouring waves take neighbouring sub-streams
@@ -1648,8 +1836,9 @@ __device__ __forceinline__ void encode_wg(const hq_encode_args& A, const hq_rice
     il += dpp<kDppRowShr4, 0xF, 0xF, true>(0u, il);
     il += dpp<kDppRowShr8, 0xF, 0xF, true>(0u, il);
     const uint32_t xl = il - wl;
-    const uint32_t sub_l = wg * NSUB + (uint32_t)lane;
-    if (lane < NSUB && sub_l < (uint32_t)A.nsub) {
+    const uint32_t ns = (uint32_t)NSUB / mb;  // sub-streams per group
+    const uint32_t sub_l = wg * ns + (uint32_t)lane;
+    if ((uint32_t)lane < ns && sub_l < (uint32_t)A.nsub) {
       const unsigned long long end = base + il;
       if (sub_l == 0 && A.first_sub == 0) A.offsets[0] = 0u;
       A.offsets[A.first_sub + sub_l + 1] = (uint32_t)end;
@@ -1714,10 +1903,11 @@ __global__ __launch_bounds__(64 * HQ_ENC_SUBS_PER_WG / SPW) void hq_encode_kerne
   encode_wg<LAT, XT, KV, SPW>(A, T, blockIdx.x);
 }
 
-template <int LAT, int XT>
+// MB: 512-symbol blocks per sub-stream (1, or 2 / 4 for S = 1024 / 2048)
+template <int LAT, int XT, int MB>
 __global__ __launch_bounds__(64 * HQ_ENC_WAVES) void hq_encode_tiled_kernel(hq_encode_args A,
                                                                            hq_rice_thr T) {
-  encode_wg<LAT, XT, false, HQ_ENC_SUBS_PER_WAVE, true>(A, T, blockIdx.x);
+  encode_wg<LAT, XT, false, HQ_ENC_SUBS_PER_WAVE, true, MB>(A, T, blockIdx.x);
 }
 
 // Several matrices in one launch: workgroups wg_begin[i] .. wg_begin[i+1]-1
@@ -2100,6 +2290,85 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   }
 }
 
+// Block b of a sub-stream of B 512-symbol blocks (already in `buf`, Wl
+// words): its remainder fields sit at bit b 64 lrem, its unary codes begin
+// at bit ustart (anywhere in a word: the bits below it belong to block
+// b - 1).  Lane l's codes start just past this block's terminator 8 l - 1,
+// found by a popcount scan from ustart that stops once all 64 starts are
+// known.  Returns false (in every lane) for a parse that runs out of words;
+// `uend` becomes the bit past the block's last code.
+template <int LAT>
+__device__ __forceinline__ bool decode_block_mb(const uint32_t* buf, uint32_t Wl, uint32_t* starts,
+                                                uint32_t ustart, uint32_t rem_base, uint32_t k0,
+                                                uint32_t k1, int lane, bool ok, uint32_t* sym,
+                                                uint32_t& uend) {
+  const uint32_t lrem = lane_rem_bits<LAT>(k0, k1);
+  const uint32_t nbits = 32u * Wl;
+  starts[lane] = (lane == 0) ? ustart : 0xFFFFFFFFu;
+  wave_sync_lds();
+  const uint32_t uw0 = ustart >> 5;
+  const uint32_t nuw = (ok && Wl > uw0) ? Wl - uw0 : 0u;
+  const uint32_t lowmask = ~((1u << (ustart & 31u)) - 1u);
+  uint32_t carry = 0;
+  for (uint32_t base = 0; base < nuw && carry < 504u; base += 64) {
+    const uint32_t wi = base + lane;
+    uint32_t v = (wi < nuw) ? buf[uw0 + wi] : 0u;
+    if (wi == 0u) v &= lowmask;
+    const uint32_t cnt = __popc(v);
+    const uint32_t incl = wave_scan_incl(cnt);
+    const uint32_t P = carry + incl - cnt;
+    for (uint32_t t = (P & ~7u) + 7u; t < P + cnt; t += 8u) {
+      const uint32_t j = (t + 1u) >> 3;
+      if (j < 64u) starts[j] = (uw0 + wi) * 32u + select32(v, t - P) + 1u;
+    }
+    carry += __builtin_amdgcn_readlane(incl, 63);
+  }
+  wave_sync_lds();
+  uint32_t pos = starts[lane];
+  ok = ok && pos < nbits;
+  uint32_t qv[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) qv[j] = 0;
+  if (ok) {
+    // the q_j: zeros before each of the lane's 8 terminators, a 64-bit
+    // window sliding along the buffer
+    uint64_t win = load_bits64(buf, pos, Wl);
+    uint32_t valid = 64;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      uint32_t q = 0;
+      while (ok && win == 0ull) {
+        q += valid;
+        pos += valid;
+        if (pos >= nbits) {
+          ok = false;
+          break;
+        }
+        win = load_bits64(buf, pos, Wl);
+        valid = 64;
+      }
+      const uint32_t lo = (uint32_t)win, hi = (uint32_t)(win >> 32);
+      const uint32_t tz =
+          lo ? (uint32_t)__builtin_ctz(lo) : 32u + (uint32_t)__builtin_ctz(hi | (hi == 0u));
+      q += tz;
+      pos += tz + 1;
+      valid -= tz + 1;
+      win = (tz >= 63u) ? 0ull : (win >> (tz + 1));
+      qv[j] = q;
+    }
+  }
+  uend = __builtin_amdgcn_readlane(pos, 63);
+  // the lane's 8 remainders
+  const uint32_t rpos = rem_base + __umul24((uint32_t)lane, lrem);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t kk = sym_class<LAT>(j) ? k1 : k0;
+    const uint32_t r = (ok && kk) ? (uint32_t)load_bits64(buf, rpos + rem_offset<LAT>(j, k0, k1), Wl) : 0u;
+    sym[j] = (qv[j] << kk) | (r & ((1u << kk) - 1u));
+  }
+  return __ballot(!ok) == 0ull;
+}
+
 // Long tiles (weights, bf16 or fp32 out): the wave's four consecutive
 // sub-streams are decoded first and kept as lattice coordinates, then the
 // tiles they form are transformed together (fwht_tiled) and denormalized.
@@ -2115,9 +2384,65 @@ __device__ __forceinline__ void decode_wg_tiled(const hq_decode_args& A, const u
   s_sel[tid] = byte_select_entry((uint32_t)tid);  // 256 threads, one entry each
   __syncthreads();
 
-  const uint32_t sub0 = (wgi * HQ_WAVES_PER_WG + wave) * HQ_DEC_SUBS_PER_WAVE;
-  const uint32_t nsub = (uint32_t)A.nsub;
   const uint32_t n = (uint32_t)A.tile;
+  const uint32_t mb = (uint32_t)A.mb;
+  float y[HQ_DEC_SUBS_PER_WAVE][8];
+  // the wave's four consecutive 512-symbol blocks (sub-streams when mb = 1)
+  const uint32_t sub0 = (wgi * HQ_WAVES_PER_WG + wave) * HQ_DEC_SUBS_PER_WAVE;
+  const uint32_t nsub = (uint32_t)A.nsub * mb;  // blocks
+  const uint32_t spr = (uint32_t)A.spr * mb;
+  const TwSigns sg(lane);
+  if (mb > 1u) {
+    // sub-streams of mb blocks: the whole sub-stream goes to the wave's
+    // buffer, then its blocks are parsed in order (each block's unary codes
+    // start where the previous block's end); a corrupt sub-stream decodes
+    // as zeros in all of its blocks
+    for (uint32_t j = 0; j < HQ_DEC_SUBS_PER_WAVE / mb; ++j) {
+      const uint32_t s = sub0 / mb + j;  // sub-stream
+      const bool act = s < (uint32_t)A.nsub;
+      uint32_t start = 0, end = 0, kb = 0;
+      if (act) {
+        start = readfirst(A.offsets[(uint32_t)A.first_sub + s]);
+        end = readfirst(A.offsets[(uint32_t)A.first_sub + s + 1]);
+        kb = readfirst(A.kparam[(uint32_t)A.first_sub + s]);
+      }
+      const uint32_t k0 = (LAT == kA2) ? (kb & 15u) : kb;
+      const uint32_t k1 = (LAT == kA2) ? (kb >> 4) : (LAT == kD4 ? (k0 > 0 ? k0 - 1 : 0) : k0);
+      const uint32_t Rb = 64u * lane_rem_bits<LAT>(k0, k1);
+      const uint32_t W = end - start;
+      bool ok = act && end >= start && (int64_t)end <= A.cap_words && W <= A.lds_words &&
+                k0 <= HQ_KMAX && mb * Rb <= 32u * W;
+      const uint32_t Wl = ok ? W : 0u;
+      for (uint32_t w = lane; w < Wl; w += 64) buf[w] = A.payload[(uint64_t)start + w];
+      if (lane < 2) buf[Wl + lane] = 0u;  // two zero words past the end
+      wave_sync_lds();
+      uint32_t ustart = mb * Rb;
+      for (uint32_t b = 0; b < mb; ++b) {
+        uint32_t sym[8], uend;
+        ok = decode_block_mb<LAT>(buf, Wl, starts, ustart, b * Rb, k0, k1, lane, ok, sym, uend);
+        ustart = uend;
+        int32_t c[8];
+        unstrip8<LAT>(sym, c);
+        const uint32_t i = j * mb + b;
+#pragma unroll
+        for (int q = 0; q < HQ_DEC_SUBS_PER_WAVE; ++q)
+          if ((uint32_t)q == i)
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) y[q][jj] = act ? code_coord<LAT>(c[jj], jj) : 0.0f;
+      }
+      if (act && !ok) {
+#pragma unroll
+        for (int q = 0; q < HQ_DEC_SUBS_PER_WAVE; ++q)
+          if ((uint32_t)q / mb == j)
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) y[q][jj] = 0.0f;
+        if (A.stats && lane == 0) {
+          atomicAdd(&A.stats->corrupt_substreams, 1u);
+          atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+        }
+      }
+    }
+  } else {
   uint32_t off[HQ_DEC_SUBS_PER_WAVE + 1], kbs[HQ_DEC_SUBS_PER_WAVE];
 #pragma unroll
   for (int i = 0; i <= HQ_DEC_SUBS_PER_WAVE; ++i) {
@@ -2127,9 +2452,6 @@ __device__ __forceinline__ void decode_wg_tiled(const hq_decode_args& A, const u
       kbs[i] = sub < nsub ? readfirst(A.kparam[(uint32_t)A.first_sub + sub]) : 0u;
   }
   DecHead head = dec_head<LAT>(A, sub0 < nsub, off[0], off[1], kbs[0], lane);
-  const uint32_t spr = (uint32_t)A.spr;
-  const TwSigns sg(lane);
-  float y[HQ_DEC_SUBS_PER_WAVE][8];
 #pragma unroll
   for (int i = 0; i < HQ_DEC_SUBS_PER_WAVE; ++i) {
     const uint32_t sub = sub0 + (uint32_t)i;
@@ -2154,6 +2476,7 @@ __device__ __forceinline__ void decode_wg_tiled(const hq_decode_args& A, const u
     }
     if (i + 1 < HQ_DEC_SUBS_PER_WAVE) head = next;
   }
+  }  // one block per sub-stream
   // y = D H^T code * r / (alpha n): the tiles' transforms, then each lane
   // its own tile's factor
   const uint32_t sigma = fwht_tiled(y, lane, n, sg);
@@ -3370,21 +3693,28 @@ int launch_decode_lat(const Args& a, uint32_t nwg, uint32_t lds_words, int mode,
   return (int)hipGetLastError();
 }
 
-// Long tiles (weight plans): four consecutive sub-streams per wave.
+// Long tiles, or sub-streams of several blocks (weight plans): four
+// consecutive 512-symbol blocks per wave.
+template <int LAT, int XT, int MB>
+int launch_encode_tiled_mb(const hq_encode_args& a, const hq_rice_thr& t, hipStream_t st) {
+  const size_t lds = (size_t)(a.lds_words + 2) * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
+  static size_t granted = 0;
+  allow_lds((const void*)hq_encode_tiled_kernel<LAT, XT, MB>, lds, granted);
+  hipLaunchKernelGGL((hq_encode_tiled_kernel<LAT, XT, MB>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES), lds, st,
+                     a, t);
+  return (int)hipGetLastError();
+}
+
 template <int LAT>
 int launch_encode_tiled(const hq_encode_args& a, const hq_rice_thr& t, int xt, hipStream_t st) {
-  const size_t lds = (size_t)(a.lds_words + 2) * HQ_ENC_SUBS_PER_WG * sizeof(uint32_t);
-  static size_t granted_b = 0, granted_f = 0;
   if (xt == HQ_BF16) {
-    allow_lds((const void*)hq_encode_tiled_kernel<LAT, HQ_BF16>, lds, granted_b);
-    hipLaunchKernelGGL((hq_encode_tiled_kernel<LAT, HQ_BF16>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES),
-                       lds, st, a, t);
-  } else {
-    allow_lds((const void*)hq_encode_tiled_kernel<LAT, HQ_FP32>, lds, granted_f);
-    hipLaunchKernelGGL((hq_encode_tiled_kernel<LAT, HQ_FP32>), dim3(a.nwg), dim3(64 * HQ_ENC_WAVES),
-                       lds, st, a, t);
+    if (a.mb == 4) return launch_encode_tiled_mb<LAT, HQ_BF16, 4>(a, t, st);
+    if (a.mb == 2) return launch_encode_tiled_mb<LAT, HQ_BF16, 2>(a, t, st);
+    return launch_encode_tiled_mb<LAT, HQ_BF16, 1>(a, t, st);
   }
-  return (int)hipGetLastError();
+  if (a.mb == 4) return launch_encode_tiled_mb<LAT, HQ_FP32, 4>(a, t, st);
+  if (a.mb == 2) return launch_encode_tiled_mb<LAT, HQ_FP32, 2>(a, t, st);
+  return launch_encode_tiled_mb<LAT, HQ_FP32, 1>(a, t, st);
 }
 
 template <int LAT>
@@ -3408,7 +3738,7 @@ static bool kv_variant(const hq_plan_s* p) { return p->rotation || p->dither || 
 int hq_launch_encode(const hq_plan_s* p, const hq_encode_args& a, const hq_rice_thr& t, int xt,
                      void* stream) {
   hipStream_t st = (hipStream_t)stream;
-  if (p->tile != HQ_TILE) {
+  if (p->tile != HQ_TILE || p->substream != HQ_SUB) {  // long tiles, or sub-streams of 2 or 4 blocks
     switch (p->lattice) {
       case HQ_E8: return launch_encode_tiled<kE8>(a, t, xt, st);
       case HQ_D4: return launch_encode_tiled<kD4>(a, t, xt, st);
@@ -3447,8 +3777,8 @@ int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* 
   hipStream_t st = (hipStream_t)stream;
   const int mode = (yt == HQ_FP32) ? 0 : 1;
   const bool kv = kv_variant(p);
-  const uint32_t nwg = decode_wgs(a.nsub), lw = a.lds_words;
-  if (p->tile != HQ_TILE) {
+  const uint32_t nwg = decode_wgs(a.nsub * a.mb), lw = a.lds_words;
+  if (p->tile != HQ_TILE || p->substream != HQ_SUB) {
     switch (p->lattice) {
       case HQ_E8: return launch_decode_tiled<kE8>(a, nwg, mode, st);
       case HQ_D4: return launch_decode_tiled<kD4>(a, nwg, mode, st);

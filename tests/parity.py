@@ -21,8 +21,8 @@ def op_snr(name, bps):
 
 
 def oracle_params(lat, snr, rht_seed=0, rice_k=-1, rotation=0, rot_seed=0, dither=False,
-                  dither_seed=0, norm_fp16=False, qjl=None, tile=128):
-    return O.Params(tile=tile, lattice=lat, alpha=O.alpha(lat, snr), substream=512, rice_k=rice_k,
+                  dither_seed=0, norm_fp16=False, qjl=None, tile=128, substream=512):
+    return O.Params(tile=tile, lattice=lat, alpha=O.alpha(lat, snr), substream=substream, rice_k=rice_k,
                     norm_fp16=norm_fp16, rht_seed=rht_seed, rotation=rotation, dither=dither,
                     rot_seed=rot_seed, dither_seed=dither_seed, qjl=qjl)
 
@@ -30,7 +30,8 @@ def oracle_params(lat, snr, rht_seed=0, rice_k=-1, rotation=0, rot_seed=0, dithe
 def gpu_plan(hq, P: O.Params, snr, cols):
     plan = hq.hq_plan(P.tile, P.lattice, 0.0, P.rht_seed, P.rice_k, cols, rotation=P.rotation,
                       dither=P.dither, rot_seed=P.rot_seed, dither_seed=P.dither_seed,
-                      norm_fp16=P.norm_fp16, snr_db=snr, qjl=P.qjl)
+                      norm_fp16=P.norm_fp16, snr_db=snr, qjl=P.qjl,
+                      substream=0 if P.substream == 512 else P.substream)
     assert np.float32(plan.info.alpha) == np.float32(P.alpha), "alpha differs from the oracle's"
     return plan
 
@@ -56,8 +57,9 @@ def compare_streams(P: O.Params, x_np, gpu, row0=0, check_decode=None):
     rows, cols = x_np.shape
     codes, norms, zin, _ = O.frontend(P, x_np, row0=row0, want_z=True)
     o_pay, o_off, o_kp, bits = O.pack(P, codes, row0=0)
-    o_off = o_off[: rows * (cols // 512) + 1]
-    o_kp = o_kp[: rows * (cols // 512)]
+    S = P.substream
+    o_off = o_off[: rows * (cols // S) + 1]
+    o_kp = o_kp[: rows * (cols // S)]
     assert np.array_equal(g_norm.view(np.uint8), norms.view(np.uint8)), "stored norms differ"
     m = O.DIM[P.lattice]
     gsz = np.diff(g_off.astype(np.int64))
@@ -82,7 +84,7 @@ def compare_streams(P: O.Params, x_np, gpu, row0=0, check_decode=None):
         flat_c = codes.reshape(-1, m)
         flat_g = g_codes.reshape(-1, m)
         for s in mismatched:
-            b0, b1 = s * 512 // m, (s + 1) * 512 // m
+            b0, b1 = s * S // m, (s + 1) * S // m
             diff = np.any(flat_c[b0:b1] != flat_g[b0:b1], axis=1)
             if not diff.any():
                 raise AssertionError(f"sub-stream {s}: same codes, different bits")
@@ -94,8 +96,8 @@ def compare_streams(P: O.Params, x_np, gpu, row0=0, check_decode=None):
             exempt_blocks += int(diff.sum())
             exempt_subs += 1
             # the GPU's bits must be exactly the oracle's Rice code of the GPU's symbols
-            rp, roff, rkp, _ = O.pack(P, g_codes[(s * 512) // cols:(s * 512) // cols + 1], row0=0)
-            srow = s % (cols // 512)
+            rp, roff, rkp, _ = O.pack(P, g_codes[(s * S) // cols:(s * S) // cols + 1], row0=0)
+            srow = s % (cols // S)
             gw = g_pay[g_off[s] - g_off[0]: g_off[s + 1] - g_off[0]]
             assert rkp[srow] == g_kp[s]
             assert np.array_equal(rp[roff[srow]:roff[srow + 1]], gw)

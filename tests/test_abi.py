@@ -54,14 +54,19 @@ def test_plan_argument_errors_are_synchronous(hq):
     assert L.hq_plan(128, 0, 4.0, 0, -1, 4000, C.byref(o), C.byref(h), C.byref(info)) == -1
     assert L.hq_plan(128, 7, 4.0, 0, -1, 4096, C.byref(o), C.byref(h), C.byref(info)) == -1
     assert L.hq_plan(128, 0, 4.0, 0, 16, 4096, C.byref(o), C.byref(h), C.byref(info)) == -1
-    # valid for the method, not built here: tiles past 2048, long tiles with a
-    # KV option (rotation, dither, fp16 norms), other sub-stream lengths
+    # valid for the method, not built here: tiles past 2048; long tiles, or
+    # sub-streams of 1024 / 2048 symbols, with a KV option (rotation, dither,
+    # fp16 norms); sub-stream lengths other than 512, 1024 and 2048
     assert L.hq_plan(4096, 0, 4.0, 0, -1, 8192, C.byref(o), C.byref(h), C.byref(info)) == -2
     for rot, dith, nd in ((1, 0, 0), (0, 1, 0), (0, 0, 2)):
         ok = hq.Options(rot, dith, 0, 0, nd, 0, 1, 0, 20.0)
         assert L.hq_plan(256, 0, 4.0, 0, -1, 4096, C.byref(ok), C.byref(h), C.byref(info)) == -2
-    o2 = hq.Options(0, 0, 0, 0, 0, 1024, 1, 0, 20.0)
-    assert L.hq_plan(128, 0, 4.0, 0, -1, 4096, C.byref(o2), C.byref(h), C.byref(info)) == -2
+        for S in (1024, 2048):
+            ok = hq.Options(rot, dith, 0, 0, nd, S, 1, 0, 20.0)
+            assert L.hq_plan(128, 0, 4.0, 0, -1, 4096, C.byref(ok), C.byref(h), C.byref(info)) == -2
+    for S in (256, 4096):
+        o2 = hq.Options(0, 0, 0, 0, 0, S, 1, 0, 20.0)
+        assert L.hq_plan(128, 0, 4.0, 0, -1, 8192, C.byref(o2), C.byref(h), C.byref(info)) == -2
     # a sub-stream length that neither holds whole tiles nor divides one
     o3 = hq.Options(0, 0, 0, 0, 0, 768, 1, 0, 20.0)
     assert L.hq_plan(1024, 0, 4.0, 0, -1, 6144, C.byref(o3), C.byref(h), C.byref(info)) == -1

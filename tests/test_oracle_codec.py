@@ -452,3 +452,60 @@ def test_tile_of_several_substreams_round_trips():
     # a sub-stream length that neither holds whole tiles nor divides one
     with pytest.raises(ValueError):
         O.frontend(O.Params(tile=512, lattice=O.E8, alpha=1.0, substream=768), x[:, :1536])
+
+
+def _rice_bits(lat, sym, k0, k1):
+    """Bits of a Rice-coded run of symbols (class-1 positions at k1), counted
+    symbol by symbol from the code length (m >> k) + 1 + k."""
+    m = O.DIM[lat]
+    cls = np.zeros(m, dtype=bool)
+    if lat == O.D4:
+        cls[3] = True
+    elif lat == O.A2:
+        cls[1] = True
+    kk = np.where(np.tile(cls, sym.size // m), k1, k0).astype(np.int64)
+    return int(((sym.astype(np.int64) >> kk) + 1 + kk).sum())
+
+
+@pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2, O.Z])
+def test_substream_length_fixed_k_bits_add_up(lat):
+    # Sec. 5.3: sub-streams of S symbols, each with its word offset and k.
+    # With a fixed k every symbol costs (m >> k) + 1 + k bits wherever the
+    # sub-stream boundaries fall, so each sub-stream's word count is the
+    # rounded-up sum of its own symbols' lengths, the unpadded totals agree
+    # at S = 512, 1024 and 2048, and every S round-trips to the codes.
+    x = gauss(1024, seed=91).reshape(-1, 2048)
+    snr = 20.0
+    totals = {}
+    for S in (512, 1024, 2048):
+        P = O.Params(tile=128, lattice=lat, alpha=O.alpha(lat, snr), substream=S, rice_k=3)
+        codes, norms, _, _ = O.frontend(P, x)
+        st = O.encode(P, x)
+        sym = O.strip(lat, codes).reshape(-1, S)
+        k1 = 2 if lat == O.D4 else 3
+        bits = [_rice_bits(lat, sym[j], 3, k1) for j in range(sym.shape[0])]
+        assert np.array_equal(np.diff(st.offsets.astype(np.int64)), (np.array(bits) + 31) // 32)
+        assert st.payload_bits == sum(bits)
+        assert len(st.kparam) == x.size // S
+        back, rc = O.unpack(P, st.payload, st.offsets, st.kparam, x.shape[0], x.shape[1])
+        assert rc == O.OK and np.array_equal(back, codes)
+        totals[S] = st.payload_bits
+    assert totals[512] == totals[1024] == totals[2048]
+
+
+@pytest.mark.parametrize("S", [1024, 2048])
+def test_substream_length_auto_k_near_optimal(S):
+    # The automatic k (the better of k* and k* + 1 on the sub-stream's own
+    # S symbols) codes each sub-stream within 0.5% of the best fixed k found
+    # by trying all 16; a k taken from a wrong symbol count or mean would
+    # miss by a whole step (several percent).
+    x = gauss(2048, seed=93).reshape(-1, 4096)
+    for lat in (O.E8, O.Z):
+        P = O.Params(tile=128, lattice=lat, alpha=O.alpha(lat, 22.0), substream=S)
+        codes, _, _, _ = O.frontend(P, x)
+        st = O.encode(P, x)
+        sym = O.strip(lat, codes).reshape(-1, S)
+        for j in range(sym.shape[0]):
+            best = min(_rice_bits(lat, sym[j], k, k) for k in range(16))
+            got = _rice_bits(lat, sym[j], int(st.kparam[j]), int(st.kparam[j]))
+            assert got <= best * 1.005, (lat, j, int(st.kparam[j]))
