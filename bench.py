@@ -224,13 +224,13 @@ def other_workloads(H, W, dev, reps=20):
     flush = torch.empty(1 << 28, dtype=torch.float32, device=dev)
     out = {}
 
-    def codec(name, x, lattice, bps, kv=False, rows_per_append=None, qjl=None, tile=128):
+    def codec(name, x, lattice, bps, kv=False, rows_per_append=None, qjl=None, tile=128, substream=0):
         print(f"[bench] {name}", file=sys.stderr, flush=True)
         rows, cols = x.shape
         opts = dict(rotation=1, dither=True, rot_seed=72, dither_seed=73, norm_fp16=True) if kv else {}
         if qjl is not None:
             opts.update(rotation=H.HQ_ROT_QJL, qjl=qjl)
-        plan = H.hq_plan(tile, lattice, bps, 17, -1, cols, **opts)
+        plan = H.hq_plan(tile, lattice, bps, 17, -1, cols, substream=substream, **opts)
         s = H.EncodedStream(plan, rows)
         y = torch.empty((rows, cols), dtype=torch.bfloat16, device=dev)
         esz = x.element_size()
@@ -252,7 +252,7 @@ def other_workloads(H, W, dev, reps=20):
         n = x.numel()
         te = _median_ms(enc, reps, flush) * 1e-3
         td = _median_ms(lambda: H.hq_decode(plan, s, out=y), reps, flush) * 1e-3
-        side = n / tile * (2 if kv else 4) + n / 512 * 5
+        side = n / tile * (2 if kv else 4) + n / (substream or 512) * 5
         alg_e = n * esz + bits / 8 + side
         alg_d = bits / 8 + side + n * 2
         e = (y.float() - x.float())
@@ -273,6 +273,9 @@ def other_workloads(H, W, dev, reps=20):
     # the RHT tile sweep of Sec. 7.2 on the same matrix (weights, E8 at 4 bps)
     for t in (256, 512, 1024, 2048):
         codec(f"C2_4096x4096_bf16_E8@4_tile{t}", x2, H.HQ_E8, 4.0, tile=t)
+    # the sub-stream length S of Sec. 5.3 (metadata against parallel occupancy)
+    for sl in (1024, 2048):
+        codec(f"C2_4096x4096_bf16_E8@4_S{sl}", x2, H.HQ_E8, 4.0, substream=sl)
     del x2
     k = W.kv_cache(device="cpu", role="k")  # [16, 8192, 8, 128], appended 128 tokens at a time
     xk = k.permute(1, 0, 2, 3).reshape(64, 128, 16, 1024).permute(0, 2, 1, 3).reshape(-1, 1024)
