@@ -15,9 +15,17 @@ on, so bench.py reports the figure only while the kernels are unchanged.
 `stats`: rocprofv3 --stats kernel times of a default bench.py run next to the
 bench line's own HIP-event figures.
 
-`counters`: instruction and cycle counters of the codec kernels (and the
-GEMM), summed over every dispatch of each kernel; the codec columns also per
-scalar, SCALARS being the scalars each codec direction processed in the run.
+`counters`: instruction and cycle counters of the codec kernels, the three
+GEMMs and the fused one-token kernels, summed over every dispatch of each
+kernel; the codec columns also per scalar, SCALARS being the scalars each
+codec direction processed in the run.  Derived lines, for the kernels whose
+counters include SQ_BUSY_CYCLES: SQ_BUSY_CYCLES counts each of the 32 shader
+engines (it reads four times GRBM_GUI_ACTIVE, which counts each of the 8
+XCDs), so a dispatch's SIMD-cycles are SQ_BUSY_CYCLES / 32 x 1024 SIMDs, and
+  VALU (SALU) instructions per SIMD-cycle = SQ_INSTS_VALU (SALU) / (32 SQ_BUSY_CYCLES),
+  MFMA busy                                = SQ_VALU_MFMA_BUSY_CYCLES / (32 SQ_BUSY_CYCLES).
+A SIMD issues at most one wave64 VALU instruction per ~2.5 cycles of the fast
+forms and ~4.3 of the slow ones (0.4 and 0.23 per cycle).
 """
 import csv
 import hashlib
@@ -32,8 +40,15 @@ KERNELS = {
     "encode": "hq_encode_group_kernel<0, 0, false>",
     "decode": "hq_decode_group_kernel<0, 1, false>",
     "gemm": "hq_gemm_i8_kernel",
+    "gemm_fp8": "hq_gemm_f8_kernel",
+    "gemm_mxfp4": "hq_gemm_mx4_kernel",
+    "decode_gemv": "hq_decode_gemv_kernel",
+    "decode_gemv_rows": "hq_decode_gemv_rows_kernel",
+    "attention": "hq_attn_kernel",
     "copy": "__amd_rocclr_copyBuffer",
 }
+CODEC = ("encode", "decode")
+SIMDS, SHADER_ENGINES = 1024, 32
 
 
 def read_counter(path, counter):
@@ -112,14 +127,23 @@ def counters(out, scalars, csvs, cmd):
     lines = ["# Instruction and cycle counters, summed over every dispatch of each kernel.",
              "# Commands (repository root):"] + [f"#   {c}" for c in cmd]
     lines.append(f"# per scalar = total / {scalars:.0f} scalars (codec kernels)")
-    for key in ("encode", "decode", "gemm"):
-        if key not in vals:
+    for key in KERNELS:
+        if key not in vals or key == "copy":
             continue
         lines.append(f"[{key}: {KERNELS[key]}]")
         for c in sorted(vals[key]):
             n = len(disp[(key, c)])
-            per = f"  per scalar {vals[key][c] / scalars:.4f}" if key != "gemm" else ""
+            per = f"  per scalar {vals[key][c] / scalars:.4f}" if key in CODEC else ""
             lines.append(f"{c:28s} total {vals[key][c]:.4g}  dispatches {n}{per}")
+        v = vals[key]
+        busy = v.get("SQ_BUSY_CYCLES", 0.0)
+        if busy > 0:
+            simd_cycles = busy / SHADER_ENGINES * SIMDS
+            for c, label in (("SQ_INSTS_VALU", "VALU instructions per SIMD-cycle"),
+                             ("SQ_INSTS_SALU", "SALU instructions per SIMD-cycle"),
+                             ("SQ_VALU_MFMA_BUSY_CYCLES", "MFMA busy")):
+                if c in v:
+                    lines.append(f"= {label:36s} {v[c] / simd_cycles:.4f}")
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
 
