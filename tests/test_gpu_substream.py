@@ -121,3 +121,16 @@ def test_substreams_reject_the_512_paths(hq):
         with pytest.raises(hq.HQError) as e:
             hq.hq_plan(128, hq.HQ_E8, 0.0, 1, -1, 8192, snr_db=snr, substream=S)
         assert e.value.status == -2
+
+
+@pytest.mark.parametrize("S", [1024, 2048])
+def test_c2_whole_stream_per_substream_length(hq, S):
+    """C2 (4096 x 4096 bf16, Student-t with outlier columns) at E8 @ 4 bps with
+    sub-streams of S symbols, in the launch configuration the bench times:
+    every sub-stream bit-exact, every row's fp32 decode equal to the oracle's
+    reconstruction."""
+    from paper_2606_23406_amd import workloads
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=2, substream=S)
+    x = workloads.heavy_tailed_weight()
+    assert roundtrip(hq, P, snr, x, "C2 E8@4") == 1.0
