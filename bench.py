@@ -407,6 +407,38 @@ def gemm_extra(H, W, mats, dev):
     t_gemm4 = f0.elapsed_time(f1) / reps * 1e-3
     t_e2e4 = f1.elapsed_time(f2) / reps * 1e-3
     ops = 2.0 * M * N * K
+    # the same product at long RHT tiles (Sec. 7.2): the weight factors span
+    # the tile, so the per-tile rescale runs tile / 128 times less often
+    sweep = {}
+    for tile in (512, 2048):
+        tp = H.hq_plan(tile, H.HQ_E8, 4.0, gate["seed"], -1, K)
+        ts = H.EncodedStream(tp, N)
+        H.hq_encode(tp, gate["x"], ts)
+        ci, gi = H.hq_decode_int8(tp, ts)
+        xi, sxi = H.hq_act_prep(tp, a)
+        cf, gf = H.hq_decode_fp8(tp, ts)
+        xf, sxf = H.hq_act_prep_fp8(tp, a)
+        cm, wm, gm = H.hq_decode_mxfp4(tp, ts)
+        xm, xsm = H.hq_act_prep_mxfp4(tp, a)
+        row = {}
+        for name, fn, peak in (
+                ("int8", lambda: H.hq_gemm_int8_blockscaled(tp, xi, sxi, ci, gi, out=out), INT8_PEAK_TOPS),
+                ("fp8", lambda: H.hq_gemm_fp8_blockscaled(tp, xf, sxf, cf, gf, out=out), FP8_PEAK_TFLOPS),
+                ("mxfp4", lambda: H.hq_gemm_mxfp4_blockscaled(tp, xm, xsm, cm, wm, gm, out=out),
+                 FP4_PEAK_TFLOPS)):
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            f0.record()
+            for _ in range(reps):
+                fn()
+            f1.record()
+            torch.cuda.synchronize()
+            tt = f0.elapsed_time(f1) / reps * 1e-3
+            row[f"{name}_ms"] = round(tt * 1e3, 4)
+            row[f"{name}_frac_peak"] = round(ops / tt / 1e12 / peak, 4)
+        sweep[f"tile{tile}"] = row
+        del ts, ci, gi, xi, cf, gf, xf, cm, wm, gm, xm
     return {"workload": f"W {N}x{K} E8@4 Rice stream, A {M}x{K} bf16 (1% outlier channels x30)",
             "gemm_ms": round(t_gemm * 1e3, 4), "gemm_TOPS": round(ops / t_gemm / 1e12, 2),
             "gemm_frac_int8_peak": round(ops / t_gemm / 1e12 / INT8_PEAK_TOPS, 4),
@@ -417,7 +449,8 @@ def gemm_extra(H, W, mats, dev):
             "fp8_end_to_end_ms": round(t_e2e8 * 1e3, 4),
             "mxfp4_gemm_ms": round(t_gemm4 * 1e3, 4), "mxfp4_gemm_TOPS": round(ops / t_gemm4 / 1e12, 2),
             "mxfp4_gemm_frac_fp4_peak": round(ops / t_gemm4 / 1e12 / FP4_PEAK_TFLOPS, 4),
-            "mxfp4_end_to_end_ms": round(t_e2e4 * 1e3, 4)}
+            "mxfp4_end_to_end_ms": round(t_e2e4 * 1e3, 4),
+            "long_tiles": sweep}
 
 
 def gemv_extra(H, W, mats, dev, reps=10):

@@ -98,7 +98,9 @@ typedef struct {
 
 /* hq_plan -- validate the knobs of the paper's problem statement (Sec. 4.9,
  * Tab. params) and derive the codec constants.
- *   tile      n_tile, a power of two; this build runs 128 (Sec. 4.1 default).
+ *   tile      n_tile, a power of two: 128 (Sec. 4.1 default), or 256 .. 2048
+ *             for weight plans (the sweep of Sec. 7.2; no rotation, dither or
+ *             fp16 norms); HQ_ERR_UNSUPPORTED otherwise.
  *   lattice   hq_lattice (Sec. 4.5).
  *   bps       target payload bits per scalar (App. B); mapped to an SNR by the
  *             library's calibration table unless opt->use_snr is set.
@@ -253,7 +255,8 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
  * so that a decoded weight row is D H c g.  Codes beyond +-127 are clamped
  * and counted.  E8, D4 and Z only (A2 has a sqrt3 axis): HQ_ERR_UNSUPPORTED
  * otherwise; dithered or rotated streams are HQ_ERR_UNSUPPORTED too (their
- * codes are not D H-coordinates of the weights alone). */
+ * codes are not D H-coordinates of the weights alone).  Any tile; sub-streams
+ * of 512 only (HQ_ERR_UNSUPPORTED otherwise). */
 hq_status hq_decode_int8(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows,
                          int8_t* codes, int64_t ldc, float* g, void* stream);
 
@@ -267,7 +270,8 @@ hq_status hq_act_prep(hq_plan_t plan, const void* a, int64_t M, int64_t lda, int
 
 /* hq_gemm_int8_blockscaled -- out[i, r] = s_x[i] * sum_t g[r, t] *
  * sum_{j in tile t} c[r, j] * x_q[i, j] with exact int32 tile sums on the
- * int8 matrix cores and fp32 accumulation (N = weight rows, K = plan.cols).
+ * int8 matrix cores and fp32 accumulation (N = weight rows, K = plan.cols;
+ * the tile is the plan's, 128 .. 2048: a longer tile rescales less often).
  * Every operand is contiguous: xq is M x K and codes N x K with row stride
  * K = plan.cols (decode the codes with ldc = plan.cols), g is N x K/tile and
  * out is M x N, HQ_BF16 or HQ_FP32.  The same holds for the fp8 variant. */

@@ -754,8 +754,8 @@ hq_status hq_decode_group(const hq_plan_t* plans, const hq_stream* const* s, voi
 
 hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                          int8_t* codes, int64_t ldc, float* g, void* stream) {
-  // the GEMM's K tiles are 128; sub-streams of 512
-  if (p && (p->tile != HQ_TILE || p->substream != HQ_SUB)) return HQ_ERR_UNSUPPORTED;
+  // sub-streams of 512 (any tile: the codes carry no transform)
+  if (p && p->substream != HQ_SUB) return HQ_ERR_UNSUPPORTED;
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
@@ -772,8 +772,8 @@ hq_status hq_decode_int8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t 
 
 hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                         uint8_t* codes, int64_t ldc, float* g, void* stream) {
-  // the GEMM's K tiles are 128; sub-streams of 512
-  if (p && (p->tile != HQ_TILE || p->substream != HQ_SUB)) return HQ_ERR_UNSUPPORTED;
+  // sub-streams of 512 (any tile: the codes carry no transform)
+  if (p && p->substream != HQ_SUB) return HQ_ERR_UNSUPPORTED;
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
@@ -790,8 +790,8 @@ hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t r
 
 hq_status hq_decode_mxfp4(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
                           uint8_t* codes, uint8_t* scales, float* g, void* stream) {
-  // the GEMM's K tiles are 128; sub-streams of 512
-  if (p && (p->tile != HQ_TILE || p->substream != HQ_SUB)) return HQ_ERR_UNSUPPORTED;
+  // sub-streams of 512 (any tile: the codes carry no transform)
+  if (p && p->substream != HQ_SUB) return HQ_ERR_UNSUPPORTED;
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
@@ -809,7 +809,6 @@ hq_status hq_decode_mxfp4(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t
 static hq_status act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, int8_t* xq,
                           float* sx, int fp8, void* stream, uint8_t* mxs = nullptr) {
   if (!p || M < 0) return HQ_ERR_INVALID_ARG;
-  if (p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;
   if (M == 0) return HQ_OK;
   if (!a || !xq || (fp8 == 2 ? !mxs : !sx) || lda < p->cols || !aligned16(a) ||
       (lda * 2) % 16 != 0 || ((uintptr_t)xq & 3u) != 0)
@@ -825,6 +824,7 @@ static hq_status act_prep(hq_plan_t p, const void* a, int64_t M, int64_t lda, in
   args.dmask = p->d_dmask;
   args.fp8 = fp8;
   args.mxs = mxs;
+  args.tile = p->tile;
   return hip_status(hq_launch_act_prep(args, stream));
 }
 
@@ -848,7 +848,6 @@ static hq_status gemm_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx
                                   int32_t ot, int fp8, void* stream, const uint8_t* xs = nullptr,
                                   const uint8_t* ws = nullptr) {
   if (!p || M < 0 || N < 0) return HQ_ERR_INVALID_ARG;
-  if (p->tile != HQ_TILE) return HQ_ERR_UNSUPPORTED;
   if (ot != HQ_BF16 && ot != HQ_FP32) return HQ_ERR_INVALID_ARG;
   if (M == 0 || N == 0) return HQ_OK;
   if (!xq || (fp8 == 2 ? (!xs || !ws) : !sx) || !codes || !g || !out) return HQ_ERR_INVALID_ARG;
@@ -867,6 +866,7 @@ static hq_status gemm_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx
   a.fp8 = fp8;
   a.xs = xs;
   a.ws = ws;
+  a.tile = p->tile;
   const int e = hq_launch_gemm(a, stream);
   if (e == -1) return HQ_ERR_UNSUPPORTED;
   return hip_status(e);

@@ -172,13 +172,14 @@ struct hq_actprep_args {
   int32_t fp8;            // 1: E4M3 at 448 / amax instead of int8 at 127 / amax;
                           // 2: MXFP4 (E2M1 pairs per byte, E8M0 scale per 32 in mxs)
   uint8_t* mxs;           // MXFP4: scale bytes (M x K / 32)
+  int32_t tile;           // RHT tile (128 .. 2048)
 };
 
 struct hq_gemm_args {
   const int8_t* xq;   // M x K
   const float* sx;    // M
   const int8_t* w;    // N x K
-  const float* g;     // N x (K / 128)
+  const float* g;     // N x (K / tile)
   void* out;          // M x N
   int64_t M, N, K;
   int32_t out_bf16;
@@ -186,6 +187,7 @@ struct hq_gemm_args {
                       // 2: MXFP4 (E2M1 pairs per byte, rows of K / 2 bytes)
   const uint8_t* xs;  // MXFP4: activation scale bytes (M x K / 32)
   const uint8_t* ws;  // MXFP4: weight scale bytes (N x K / 32)
+  int32_t tile;       // RHT tile: the weight factors' K span (128 .. 2048)
 };
 
 // Kernel launchers (hq_kernels.hip); return a hipError_t as int.

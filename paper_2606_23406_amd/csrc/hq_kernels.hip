@@ -2165,7 +2165,12 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   {
     const uint32_t subq = sub0 + (uint32_t)(lane & 3);
     if (subq < nsub) {
-      const int64_t t = A.first_row * A.tpr + 4 * (int64_t)subq + (lane >> 4);
+      // the casts (MODE >= 2) also serve long-tile weight plans: tile of the
+      // 128 columns at flat position subq * 512 + 128 (lane >> 4)
+      const int64_t t =
+          MODE >= 2 ? A.first_row * A.tpr + (int64_t)((((uint64_t)subq << 9) + (uint64_t)((lane >> 4) << 7)) >>
+                                                       __builtin_ctz((uint32_t)A.tile))
+                    : A.first_row * A.tpr + 4 * (int64_t)subq + (lane >> 4);
       const float rs = fp16_norm ? (float)((const _Float16*)A.norms)[t] : ((const float*)A.norms)[t];
       gm = rs / A.alpha_n;
     }
@@ -2212,7 +2217,8 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
       }
       int8_t* out = (int8_t*)A.y + (int64_t)lrow * A.ld + col;
       *(uint2*)out = make_uint2(packed[0], packed[1]);
-      if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
+      if ((col & (uint32_t)(A.tile - 1)) == 0)
+        A.g[(int64_t)lrow * A.tpr + (col >> __builtin_ctz((uint32_t)A.tile))] = g;
       if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
     } else if constexpr (MODE == 4) {
       // the MXFP4 cast (Sec. 4.8, Sec. 6.4): blocks of 32 codes (four lanes)
@@ -2230,8 +2236,9 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
       for (int j = 0; j < 8; ++j) packed |= e2m1_code((float)c[j] * inv) << (4 * j);
       uint8_t* out = (uint8_t*)A.y + (int64_t)lrow * A.ld + (col >> 1);
       *(uint32_t*)out = packed;
-      if ((lane & 3) == 0) A.mxs[(int64_t)lrow * (A.tpr * 4) + (col >> 5)] = (uint8_t)(X + 127);
-      if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
+      if ((lane & 3) == 0) A.mxs[(int64_t)lrow * (A.spr * (HQ_SUB / 32)) + (col >> 5)] = (uint8_t)(X + 127);
+      if ((col & (uint32_t)(A.tile - 1)) == 0)
+        A.g[(int64_t)lrow * A.tpr + (col >> __builtin_ctz((uint32_t)A.tile))] = g;
     } else if constexpr (MODE == 3) {
       // the fp8 cast (Sec. 4.8): E4M3 of each code, round to nearest even,
       // magnitudes beyond 448 saturated and counted
@@ -2246,7 +2253,8 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
       const uint32_t w0 = e4m3x4(v[0], v[1], v[2], v[3]), w1 = e4m3x4(v[4], v[5], v[6], v[7]);
       uint8_t* out = (uint8_t*)A.y + (int64_t)lrow * A.ld + col;
       *(uint2*)out = make_uint2(w0, w1);
-      if ((lane & 15) == 0) A.g[(int64_t)lrow * A.tpr + (col >> 7)] = g;
+      if ((col & (uint32_t)(A.tile - 1)) == 0)
+        A.g[(int64_t)lrow * A.tpr + (col >> __builtin_ctz((uint32_t)A.tile))] = g;
       if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
     } else {
       // y = D H^T (S) (code - U) * r / (alpha n); the integer codes make the
@@ -3139,8 +3147,9 @@ __global__ __launch_bounds__(256) void hq_attn_combine_kernel(hq_attn_args A) {
 }
 
 // ------------------------------------------------------------ activation prep
-// One workgroup per token row: per 128-column tile y = H D a (canonical stage
-// order, the weights' signs), amax over the row, then int8.
+// One workgroup per token row: per tile y = H D a (canonical stage order, the
+// weights' signs: stages h = 1 .. 64 in registers per 128 columns, then for a
+// longer tile h = 128 .. tile / 2 in LDS), amax over the row, then the cast.
 
 __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
   extern __shared__ float ybuf[];
@@ -3169,6 +3178,22 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
       amax = __builtin_fmaxf(amax, __builtin_fabsf(v[i]));
       ybuf[col + i] = v[i];
     }
+  }
+  if (A.tile > HQ_TILE) {
+    // the remaining butterflies of a long tile, one stage at a time over the
+    // row: pair p of stage h is (j, j + h) with j = (p / h) 2h + p % h
+    for (int64_t h = HQ_TILE; h < A.tile; h <<= 1) {
+      __syncthreads();
+      for (int64_t p2 = tid; p2 < A.K / 2; p2 += 256) {
+        const int64_t j = (p2 / h) * 2 * h + p2 % h;
+        const float a = ybuf[j], b = ybuf[j + h];
+        ybuf[j] = a + b;
+        ybuf[j + h] = a - b;
+      }
+    }
+    __syncthreads();
+    amax = 0.0f;
+    for (int64_t c = tid; c < A.K; c += 256) amax = __builtin_fmaxf(amax, __builtin_fabsf(ybuf[c]));
   }
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) amax = __builtin_fmaxf(amax, __shfl_xor(amax, m, 64));
@@ -3294,6 +3319,7 @@ template <int MODE> struct GemmMode {
 struct GemmLoads {
   __amdgpu_buffer_rsrc_t ra, rb, rg, rxs, rws;
   uint32_t a[4], b[2], g, xs, ws;
+  int lm;  // log2 of the 128-deep K units per factor tile
 };
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t gemm_rsrc(const void* base, int64_t bytes) {
@@ -3310,7 +3336,7 @@ template <int MODE>
 __device__ __forceinline__ GemmLoads gemm_loads(const hq_gemm_args& A, int64_t m0, int64_t n0,
                                                 int wave, int lane) {
   const int64_t rb = MODE == 2 ? A.K / 2 : A.K;  // row bytes
-  const int64_t T = A.K / HQ_TILE, ks = A.K / 32;  // factors and MX scale bytes per row
+  const int64_t T = A.K / A.tile, ks = A.K / 32;  // factors and MX scale bytes per row
   const int64_t ma = min<int64_t>(A.M - m0, kGemmM), nb = min<int64_t>(A.N - n0, kGemmN);
   GemmLoads L;
   L.ra = gemm_rsrc(A.xq + m0 * rb, ma * rb);
@@ -3332,7 +3358,10 @@ __device__ __forceinline__ GemmLoads gemm_loads(const hq_gemm_args& A, int64_t m
     L.b[i] = (uint32_t)(min<int64_t>(8 * q + rr, nb - 1) * rb) + kc(q);
   }
   const int j = wave % (2 * GemmMode<MODE>::U);
-  L.g = (uint32_t)((min<int64_t>((j & 1) * 64 + lane, nb - 1) * T + (j >> 1)) * 4);
+  L.lm = __builtin_ctz((uint32_t)(A.tile / HQ_TILE));
+  // a stage holds U units of one factor tile, or (128-tiles) U tiles: unit
+  // j / 2 of the stage reads its own factor only when tiles are 128 deep
+  L.g = (uint32_t)((min<int64_t>((j & 1) * 64 + lane, nb - 1) * T + (L.lm == 0 ? (j >> 1) : 0)) * 4);
   const int d = wave * 64 + lane, e = (wave & 3) * 64 + lane;
   L.xs = (uint32_t)(min<int64_t>(d >> 1, ma - 1) * ks + (d & 1) * 4);
   L.ws = (uint32_t)(min<int64_t>(e >> 1, nb - 1) * ks + (e & 1) * 4);
@@ -3354,7 +3383,7 @@ __device__ __forceinline__ void gemm_fetch(const GemmLoads& L, int64_t t, int wa
                                              16, L.b[i], so, 0, 0);
   int8_t* const side = stage + kGemmStageA + kGemmStageB;
   __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rg, (lds_void_t*)(side + kGemmSideG + (wave % (2 * U)) * 256),
-                                           4, L.g, (uint32_t)(U * t * 4), 0, 0);
+                                           4, L.g, (uint32_t)(((U * t) >> L.lm) * 4), 0, 0);
   if constexpr (MODE == 2) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rxs, (lds_void_t*)(side + kGemmSideXs + wave * 256), 4,
                                              L.xs, (uint32_t)(t * 8), 0, 0);
@@ -3407,10 +3436,11 @@ __device__ __forceinline__ void gemm_rescale(int e0, const typename GemmMode<MOD
   }
 }
 
-// One 128-deep K tile (tile UNIT of the stage): its MFMAs into `cur`, with
-// the previous tile's partials `prev` rescaled by `gprev` a few elements
-// after each MFMA.
-template <int MODE, int UNIT>
+// One 128-deep K unit (unit UNIT of the stage): its MFMAs into `cur` (from
+// zero when FRESH, the first unit of a factor tile; accumulated otherwise),
+// with the previous tile's partials `prev` rescaled by `gprev` a few
+// elements after each MFMA when RS.
+template <int MODE, int UNIT, bool FRESH = true, bool RS = true>
 __device__ __forceinline__ void gemm_tile(const int8_t* stage, int wm, int wn, int lane,
                                           typename GemmMode<MODE>::acc_t (&cur)[2][kGemmNB],
                                           const typename GemmMode<MODE>::acc_t (&prev)[2][kGemmNB],
@@ -3446,8 +3476,8 @@ __device__ __forceinline__ void gemm_tile(const int8_t* stage, int wm, int wn, i
         for (int b = 0; b < kGemmNB; ++b) {
           // cbsz = blgp = 0: both operands E4M3; scale bytes 127 (2^0)
           cur[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-              fa[a], fb[b], s == 0 ? (acc_t){} : cur[a][b], 0, 0, 0, 127, 0, 127);
-          gemm_rescale<MODE, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
+              fa[a], fb[b], (FRESH && s == 0) ? (acc_t){} : cur[a][b], 0, 0, 0, 127, 0, 127);
+          if constexpr (RS) gemm_rescale<MODE, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
         }
     } else {
       // int8: 32-deep step, chunk 2 s + h; MXFP4: 64-deep step ks = 2 UNIT + s,
@@ -3463,16 +3493,17 @@ __device__ __forceinline__ void gemm_tile(const int8_t* stage, int wm, int wn, i
 #pragma unroll
         for (int b = 0; b < kGemmNB; ++b) {
           if constexpr (MODE == 0) {
-            cur[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[a], fb[b], s == 0 ? (acc_t){} : cur[a][b],
-                                                              0, 0, 0);
+            cur[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+                fa[a], fb[b], (FRESH && s == 0) ? (acc_t){} : cur[a][b], 0, 0, 0);
           } else {
             constexpr int ks = 2 * UNIT;  // + s: the scale byte of step ks is byte 2 (ks % 2) of word ks / 2
             const uint32_t xa = UNIT == 0 ? xs[a].x : xs[a].y, wb = UNIT == 0 ? ws[b].x : ws[b].y;
-            cur[a][b] = s == 0 ? mfma_mxfp4<0>(fa[a], fb[b], (acc_t){}, xa, wb)
-                               : mfma_mxfp4<2>(fa[a], fb[b], cur[a][b], xa, wb);
+            const acc_t c0 = (FRESH && s == 0) ? (acc_t){} : cur[a][b];
+            cur[a][b] = s == 0 ? mfma_mxfp4<0>(fa[a], fb[b], c0, xa, wb)
+                               : mfma_mxfp4<2>(fa[a], fb[b], c0, xa, wb);
             (void)ks;
           }
-          gemm_rescale<MODE, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
+          if constexpr (RS) gemm_rescale<MODE, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
         }
     }
   }
@@ -3481,6 +3512,7 @@ __device__ __forceinline__ void gemm_tile(const int8_t* stage, int wm, int wn, i
   // element).
   constexpr int DSR = MODE == 1 ? 8 : 4;  // 16-byte LDS reads per step
   constexpr int VPM = MODE == 0 ? 2 * E : E;
+  if constexpr (RS)
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
     __builtin_amdgcn_sched_group_barrier(0x100, DSR, 0);
@@ -3501,7 +3533,7 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
-  const int64_t T = A.K / HQ_TILE;                            // 128-deep K tiles
+  const int64_t T = A.K / HQ_TILE;                            // 128-deep K units
   const int64_t TS = T / GemmMode<MODE>::U;                   // LDS stages
 
   float accf[2][kGemmNB][16];
@@ -3536,7 +3568,39 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
   uint2 xs[2], ws[kGemmNB];
   gemm_fetch<MODE>(gl, 0, wsc, gsm);
   gemm_fetch<MODE>(gl, min<int64_t>(1, TS - 1), wsc, gsm + SB);
-  if constexpr (MODE == 2) {
+  if (A.tile > HQ_TILE) {
+    // factor tiles of tile / 128 units (long RHT tiles, Sec. 7.2): a tile's
+    // units accumulate into acc0 and its rescale follows its last unit, one
+    // rescale per tile / 128 units
+    const int64_t spt = (int64_t)(A.tile / HQ_TILE) / GemmMode<MODE>::U;  // stages per tile
+    for (int64_t t = 0; t < TS; t += spt) {
+      float gt[kGemmNB];
+      for (int64_t j = 0; j < spt; ++j) {
+        const int8_t* const stage = begin_stage(t + j);
+        const int8_t* const side = stage + kGemmStageA + kGemmStageB;
+        if (j == 0) gemm_side_g(side, 0, wn, lane, gt);
+        if constexpr (MODE == 2) {
+#pragma unroll
+          for (int a = 0; a < 2; ++a)
+            xs[a] = mx_scales(side + kGemmSideXs, wm * 64 + a * 32 + (lane & 31), lane);
+#pragma unroll
+          for (int b = 0; b < kGemmNB; ++b)
+            ws[b] = mx_scales(side + kGemmSideWs, wn * (kGemmN / 2) + b * 32 + (lane & 31), lane);
+          if (j == 0)
+            gemm_tile<MODE, 0, true, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+          else
+            gemm_tile<MODE, 0, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+          gemm_tile<MODE, 1, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+        } else {
+          if (j == 0)
+            gemm_tile<MODE, 0, true, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+          else
+            gemm_tile<MODE, 0, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+        }
+      }
+      gemm_rescale<MODE, 64>(0, acc0, gt, accf);
+    }
+  } else if constexpr (MODE == 2) {
     // two K tiles per stage: tile 0 into acc0 (rescaling acc1), tile 1 into acc1
     for (int64_t t = 0; t < TS; ++t) {
       const int8_t* const stage = begin_stage(t);
@@ -3569,7 +3633,7 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
       for (int b = 0; b < kGemmNB; ++b) gprev[b] = g1[b];
     }
   }
-  gemm_rescale<MODE, 64>(0, acc1, gprev, accf);  // the last tile's partials
+  if (A.tile == HQ_TILE) gemm_rescale<MODE, 64>(0, acc1, gprev, accf);  // the last tile's partials
 
 #pragma unroll
   for (int a = 0; a < 2; ++a)

@@ -116,21 +116,88 @@ def test_zero_and_nonfinite_tiles(hq, tile):
 
 
 def test_long_tiles_reject_the_128_paths(hq):
-    # the int8 / fp8 / MXFP4 casts, the GEMM, the fused GEMV and group launches are
-    # built for 128-tiles: a long-tile plan gets HQ_ERR_UNSUPPORTED
+    # the fused GEMV and the group launches are built for 128-tiles: a
+    # long-tile plan gets HQ_ERR_UNSUPPORTED
     snr = PT.op_snr("E8", 4.0)
     plan = hq.hq_plan(512, hq.HQ_E8, 0.0, 1, -1, 2048, snr_db=snr)
     s = hq.EncodedStream(plan, 4)
     x = gauss(4, 2048, 7).cuda()
     hq.hq_encode(plan, x, s)
-    for fn in (lambda: hq.hq_decode_int8(plan, s), lambda: hq.hq_decode_fp8(plan, s),
-               lambda: hq.hq_decode_gemv(plan, s, x[0].contiguous()),
-               lambda: hq.hq_encode_group([plan], [x], [hq.EncodedStream(plan, 4)]),
-               lambda: hq.hq_act_prep(plan, x), lambda: hq.hq_decode_mxfp4(plan, s),
-               lambda: hq.hq_act_prep_mxfp4(plan, x)):
+    for fn in (lambda: hq.hq_decode_gemv(plan, s, x[0].contiguous()),
+               lambda: hq.hq_encode_group([plan], [x], [hq.EncodedStream(plan, 4)])):
         with pytest.raises(hq.HQError) as e:
             fn()
         assert e.value.status == -2
+
+
+def nibbles(c):
+    c = np.asarray(c, dtype=np.uint8)
+    return (c[:, 0::2] | (c[:, 1::2] << 4)).astype(np.uint8)
+
+
+@pytest.mark.parametrize("tile", [256, 1024, 2048])
+def test_long_tile_casts_and_gemm(hq, tile):
+    """The cast paths and the block-scaled GEMM at long tiles (Sec. 7.2 with
+    Sec. 4.8 / 6.3): codes and factors, the activation prep (the longer
+    transform) bit-exact for int8, E4M3 and MXFP4, and each GEMM against the
+    oracle's product, whose factors now span `tile` columns."""
+    from paper_2606_23406_amd import workloads
+    M, N, K = 200, 160, 4096
+    snr = PT.op_snr("E8", 4.0)
+    P = PT.oracle_params(O.E8, snr, rht_seed=61 + tile, tile=tile)
+    w = gauss(N, K, 900 + tile)
+    w[:, 33] *= 20
+    a = workloads.activations(tokens=M, features=K)
+    print(f"[tiles] casts and GEMM tile={tile} M={M} N={N} K={K}", flush=True)
+    plan = PT.gpu_plan(hq, P, snr, K)
+    s = hq.EncodedStream(plan, N)
+    hq.hq_encode(plan, w.cuda(), s)
+    codes, norms, _, _ = O.frontend(P, w.float().numpy())
+    og = O.weight_factors(P, norms, N, K)
+    assert og.shape == (N, K // tile)
+    an = a.float().numpy()
+    # int8
+    c8, g8 = hq.hq_decode_int8(plan, s)
+    xq, sx = hq.hq_act_prep(plan, a.cuda())
+    out = hq.hq_gemm_int8_blockscaled(plan, xq, sx, c8, g8, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert np.array_equal(c8.cpu().numpy(), np.clip(codes, -127, 127))
+    assert np.array_equal(g8.cpu().numpy(), og)
+    oxq, osx = O.act_prep(an, tile, P.rht_seed)
+    assert np.array_equal(xq.cpu().numpy(), oxq) and np.array_equal(sx.cpu().numpy(), osx)
+    ref = O.gemm_blockscaled(codes, og, oxq, osx, tile)
+    got = out.cpu().numpy().astype(np.float64)
+    rel = np.max(np.abs(got - ref) / np.maximum(np.abs(ref), np.sqrt((ref ** 2).mean())))
+    print(f"[tiles] tile={tile} int8 GEMM: worst error {rel:.2e}", flush=True)
+    assert rel <= 1e-5
+    # E4M3
+    f8, gf = hq.hq_decode_fp8(plan, s)
+    x8, sx8 = hq.hq_act_prep_fp8(plan, a.cuda())
+    out8 = hq.hq_gemm_fp8_blockscaled(plan, x8, sx8, f8, gf, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ox8, osx8 = O.act_prep_fp8(an, tile, P.rht_seed)
+    assert np.array_equal(f8.cpu().numpy(), O.weight_codes_fp8(codes))
+    assert np.array_equal(x8.cpu().numpy(), ox8) and np.array_equal(sx8.cpu().numpy(), osx8)
+    ref8 = O.gemm_fp8_blockscaled(O.weight_codes_fp8(codes), og, ox8, osx8, tile)
+    got8 = out8.cpu().numpy().astype(np.float64)
+    rel8 = np.max(np.abs(got8 - ref8) / np.maximum(np.abs(ref8), np.sqrt((ref8 ** 2).mean())))
+    print(f"[tiles] tile={tile} fp8 GEMM: worst error {rel8:.2e}", flush=True)
+    assert rel8 <= 1e-4
+    # MXFP4
+    c4, ws4, g4 = hq.hq_decode_mxfp4(plan, s)
+    x4, xs4 = hq.hq_act_prep_mxfp4(plan, a.cuda())
+    out4 = hq.hq_gemm_mxfp4_blockscaled(plan, x4, xs4, c4, ws4, g4, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    ow4, ows4 = O.weight_codes_mxfp4(codes)
+    ox4, oxs4 = O.act_prep_mxfp4(an, tile, P.rht_seed)
+    assert np.array_equal(c4.cpu().numpy(), nibbles(ow4)) and np.array_equal(ws4.cpu().numpy(), ows4)
+    assert np.array_equal(x4.cpu().numpy(), nibbles(ox4)) and np.array_equal(xs4.cpu().numpy(), oxs4)
+    assert np.array_equal(g4.cpu().numpy(), og)
+    ref4 = O.gemm_mxfp4_blockscaled(ow4, ows4, og, ox4, oxs4, tile)
+    got4 = out4.cpu().numpy().astype(np.float64)
+    rel4 = np.max(np.abs(got4 - ref4) / np.maximum(np.abs(ref4), np.sqrt((ref4 ** 2).mean())))
+    print(f"[tiles] tile={tile} MXFP4 GEMM: worst error {rel4:.2e}", flush=True)
+    assert rel4 <= 1e-4
 
 
 @pytest.mark.parametrize("tile", TILES)

@@ -136,13 +136,15 @@ def hadamard64(n):
     return hadamard(n).astype(np.float64)
 
 
-def test_act_prep_rounds_to_nearest_within_half_a_step():
+@pytest.mark.parametrize("n", [128, 512, 2048])
+def test_act_prep_rounds_to_nearest_within_half_a_step(n):
     # Sec. 4.8 cast / Sec. 6.3, per-token symmetric int8 of the rotated row:
     # every code is the nearest multiple of s_x to y = H D a (so no code is
     # more than half a step away), the largest |y| maps to exactly +-127, and
-    # -128 never appears.  y is computed here with a dense fp64 Hadamard.
+    # -128 never appears.  y is computed here with a dense fp64 Hadamard, at
+    # the default tile and at long tiles (Sec. 7.2).
     rng = np.random.default_rng(12)
-    M, K, n, seed = 16, 512, 128, 71
+    M, K, seed = 16, 4096, 71
     a = rng.standard_normal((M, K)).astype(np.float32)
     a[:, 9] *= 30.0
     xq, sx = O.act_prep(a, n, seed)
@@ -352,16 +354,18 @@ def test_no_dither_is_biased_per_vector():
     assert np.abs(y1 - x).max() > 0
 
 
-def test_gemm_blockscaled_equals_dense_fp64():
+@pytest.mark.parametrize("n", [128, 1024])
+def test_gemm_blockscaled_equals_dense_fp64(n):
     # Sec. 4.1 / Fig. 1: the RHT cancels against the activations' RHT, so
     # sum_t g c . (H D a) equals the dense product of the decoded weights with
-    # the decoded (int8, then inverse-RHT) activations.
+    # the decoded (int8, then inverse-RHT) activations; at the default tile
+    # and a long one (Sec. 7.2), whose factors span 1024 columns.
     rng = np.random.default_rng(10)
-    N, K, M, n = 48, 512, 24, 128
+    N, K, M = 48, 2048, 24
     w = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
     a = rng.standard_normal((M, K)).astype(np.float32)
     a[:, 7] *= 30
-    P = O.Params(lattice=O.E8, alpha=O.alpha(O.E8, op_point("E8", 4.0)), rht_seed=33)
+    P = O.Params(tile=n, lattice=O.E8, alpha=O.alpha(O.E8, op_point("E8", 4.0)), rht_seed=33)
     codes, norms, _, _ = O.frontend(P, w)
     g = O.weight_factors(P, norms, N, K)
     xq, sx = O.act_prep(a, n, 33)
