@@ -3655,12 +3655,139 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
     }
 }
 
+// int8 and E4M3 at 128-deep factor tiles: the eight waves in two groups of
+// four (waves 0-3 and 4-7, so each SIMD holds one wave of each) that run
+// half a stage apart.  A wave's stage t has two phases: in V(t) it issues the
+// direct-to-LDS loads of stage t + 2, reads every fragment of stage t into
+// registers and rescales the partial sums of stage t - 1 into its fp32
+// accumulators; in M(t) it only issues MFMAs.  Group 0 runs V(t) in phase
+// 2t and M(t) in phase 2t + 1, group 1 one phase later, and every phase ends
+// at a workgroup barrier, so on each SIMD one wave's MFMAs run while the
+// other wave's LDS reads and rescale issue.  The barrier waits leave only
+// this wave's newest stage of loads in flight and no LDS read outstanding:
+// a stage is complete in LDS before either group reads it, and its slot is
+// refilled (stage t + 3, issued in phase 2t + 2) only after group 1's reads
+// of phase 2t + 1 have returned.  Every wave executes the same 2 TS + 1
+// barriers: group 1 one before its first V phase, group 0 one after its
+// last M phase.
+template <int MODE>
+__device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
+  static_assert(MODE == 0 || MODE == 1, "int8 or E4M3");
+  using acc_t = typename GemmMode<MODE>::acc_t;
+  constexpr int SB = gemm_stage_bytes<MODE>();
+  constexpr int STEPS = GemmMode<MODE>::STEPS;
+  constexpr int FW = MODE == 1 ? 2 : 1;  // 16-byte chunks per fragment
+  extern __shared__ __attribute__((aligned(16))) int8_t gsm[];
+  const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
+  const int wsc = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, in a scalar register
+  const int wm = wsc >> 1, wn = wsc & 1, grp = wsc >> 2;
+  const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
+  const int64_t TS = A.K / HQ_TILE;
+
+  float accf[2][kGemmNB][16];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < kGemmNB; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) accf[a][b][r] = 0.0f;
+  acc_t cur[2][kGemmNB];
+  float gcur[kGemmNB];
+  v4i_t fa[STEPS][2][FW], fb[STEPS][kGemmNB][FW];
+
+  const GemmLoads gl = gemm_loads<MODE>(A, m0, n0, wsc, lane);
+  constexpr int NL = 7;  // buffer loads per wave and stage
+  gemm_fetch<MODE>(gl, 0, wsc, gsm);
+  gemm_fetch<MODE>(gl, min<int64_t>(1, TS - 1), wsc, gsm + SB);
+  // a phase boundary: the waits, the barrier, and no instruction scheduled
+  // across it (the MFMAs of M(t) would otherwise rise into V(t))
+  auto phase = [&]() {
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NL) : "memory");
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  if (grp == 1) phase();  // group 1 starts one phase late
+  for (int64_t t = 0; t < TS; ++t) {
+    phase();
+    // V(t)
+    const int8_t* const stage = gsm + (t % 3) * SB;
+    gemm_fetch<MODE>(gl, min(t + 2, TS - 1), wsc, gsm + ((t + 2) % 3) * SB);
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      // int8: 32-deep step, chunk 2 s + h; E4M3: 64-deep step, chunks 4 s + 2 h and the next
+#pragma unroll
+      for (int f = 0; f < FW; ++f) {
+        const int c = MODE == 1 ? 4 * s + 2 * h + f : 2 * s + h;
+#pragma unroll
+        for (int a = 0; a < 2; ++a) fa[s][a][f] = gemm_frag(stage, wm * 64 + a * 32 + (lane & 31), c);
+#pragma unroll
+        for (int b = 0; b < kGemmNB; ++b)
+          fb[s][b][f] = gemm_frag(stage + kGemmStageA, wn * (kGemmN / 2) + b * 32 + (lane & 31), c);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // the reads issue first; the rescale runs under them
+    if (t > 0) gemm_rescale<MODE, 64>(0, cur, gcur, accf);
+    gemm_side_g(stage + kGemmStageA + kGemmStageB, 0, wn, lane, gcur);
+    phase();
+    // M(t)
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s)
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < kGemmNB; ++b) {
+          const acc_t c0 = s == 0 ? (acc_t){} : cur[a][b];
+          if constexpr (MODE == 0) {
+            cur[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[s][a][0], fb[s][b][0], c0, 0, 0, 0);
+          } else {
+            const v8i_t x = {fa[s][a][0][0], fa[s][a][0][1], fa[s][a][0][2], fa[s][a][0][3],
+                             fa[s][a][1][0], fa[s][a][1][1], fa[s][a][1][2], fa[s][a][1][3]};
+            const v8i_t y = {fb[s][b][0][0], fb[s][b][0][1], fb[s][b][0][2], fb[s][b][0][3],
+                             fb[s][b][1][0], fb[s][b][1][1], fb[s][b][1][2], fb[s][b][1][3]};
+            // cbsz = blgp = 0: both operands E4M3; scale bytes 127 (2^0)
+            cur[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(x, y, c0, 0, 0, 0, 127, 0, 127);
+          }
+        }
+  }
+  if (grp == 0) phase();  // the same barrier count in both groups
+  gemm_rescale<MODE, 64>(0, cur, gcur, accf);  // the last tile
+  // the re-fetches of the last stage land before the workgroup's LDS is freed
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t m = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (m >= A.M) continue;
+      const float sxm = A.sx[m];
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b) {
+        const int64_t n = n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31);
+        if (n >= A.N) continue;
+        const float v = sxm * accf[a][b][r];
+        if (A.out_bf16)
+          ((uint16_t*)A.out)[m * A.N + n] = (uint16_t)f32_to_bf16(v);
+        else
+          ((float*)A.out)[m * A.N + n] = v;
+      }
+    }
+}
+
 __global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_i8_kernel(hq_gemm_args A) {
   gemm_body<0>(A);
 }
 
 __global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_f8_kernel(hq_gemm_args A) {
   gemm_body<1>(A);
+}
+
+__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_i8_pp_kernel(hq_gemm_args A) {
+  gemm_body_pp<0>(A);
+}
+
+__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_f8_pp_kernel(hq_gemm_args A) {
+  gemm_body_pp<1>(A);
 }
 
 __global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_mx4_kernel(hq_gemm_args A) {
@@ -3902,6 +4029,12 @@ int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void*)hq_gemm_mx4_kernel,
                               hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<2>());
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void*)hq_gemm_i8_pp_kernel,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<0>());
+    if (e == hipSuccess)
+      e = hipFuncSetAttribute((const void*)hq_gemm_f8_pp_kernel,
+                              hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<1>());
     if (e != hipSuccess) return (int)e;
     lds_set = true;
   }
@@ -3909,8 +4042,12 @@ int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   if (a.fp8 == 2)
     hipLaunchKernelGGL(hq_gemm_mx4_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<2>(), st, a);
+  else if (a.fp8 && a.tile == HQ_TILE)
+    hipLaunchKernelGGL(hq_gemm_f8_pp_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<1>(), st, a);
   else if (a.fp8)
     hipLaunchKernelGGL(hq_gemm_f8_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<1>(), st, a);
+  else if (a.tile == HQ_TILE)
+    hipLaunchKernelGGL(hq_gemm_i8_pp_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<0>(), st, a);
   else
     hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<0>(), st, a);
   return (int)hipGetLastError();
