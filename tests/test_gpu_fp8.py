@@ -55,10 +55,11 @@ def test_act_prep_fp8(hq):
     assert np.array_equal(xq.cpu().numpy(), oxq)
 
 
-@pytest.mark.parametrize("M,N", [(128, 256), (200, 384), (64, 96)])
-def test_gemm_fp8_blockscaled(hq, M, N):
+@pytest.mark.parametrize("M,N,K", [(128, 256, 1024), (200, 384, 1024), (64, 96, 1024),
+                                   (300, 200, 512), (40, 136, 2560)])
+def test_gemm_fp8_blockscaled(hq, M, N, K):
+    # K = 512: four stages (the shortest K a plan takes); 2560: twenty, the LDS ring wrapping
     from paper_2606_23406_amd import workloads
-    K = 1024
     snr = PT.op_snr("E8", 4.0)
     P = PT.oracle_params(O.E8, snr, rht_seed=53)
     w = gauss(N, K, 63, 0.02, torch.bfloat16)
@@ -77,7 +78,7 @@ def test_gemm_fp8_blockscaled(hq, M, N):
     got = out32.cpu().numpy().astype(np.float64)
     denom = np.maximum(np.abs(ref), np.sqrt((ref ** 2).mean()))
     err = float(np.max(np.abs(got - ref) / denom))
-    print(f"[parity] gemm fp8 M={M} N={N}: worst error {err:.2e}", flush=True)
+    print(f"[parity] gemm fp8 M={M} N={N} K={K}: worst error {err:.2e}", flush=True)
     assert err <= 1e-4
     # bf16 output: the fp32 one rounded to nearest even (the fp32 tile sums
     # round, unlike the int8 path's exact int32 ones)

@@ -218,10 +218,11 @@ def test_act_prep(hq):
     assert np.array_equal(xq.cpu().numpy(), oxq)
 
 
-@pytest.mark.parametrize("M,N", [(128, 256), (200, 384), (64, 96)])
-def test_gemm_int8_blockscaled(hq, M, N):
+@pytest.mark.parametrize("M,N,K", [(128, 256, 1024), (200, 384, 1024), (64, 96, 1024),
+                                   (300, 200, 512), (40, 136, 2560)])
+def test_gemm_int8_blockscaled(hq, M, N, K):
+    # K = 512: four stages (the shortest K a plan takes); 2560: twenty, the LDS ring wrapping
     from paper_2606_23406_amd import workloads
-    K = 1024
     snr = PT.op_snr("E8", 4.0)
     P = PT.oracle_params(O.E8, snr, rht_seed=51)
     w = gauss(N, K, 61, 0.02, torch.bfloat16)
