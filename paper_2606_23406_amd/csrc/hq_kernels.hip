@@ -3259,12 +3259,13 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
 // Workgroup tile 256 (tokens) x 128 (weight rows), eight waves in 4 x 2, each
 // 64 x 64 = 2 x 2 MFMA blocks, one workgroup per CU.  An LDS stage is 128
 // bytes of every A and B row (one K tile of int8 / E4M3, two of MXFP4) plus
-// its side data (tile factors, MX block scales).  Stages are double-buffered
-// and filled straight from global memory by direct-to-LDS loads, with no
-// register staging: stage t + 1 streams in while stage t is multiplied.
-// The partial sums are double-buffered too: each K tile's MFMAs write one
-// set while the previous tile's set is rescaled by its factors on the VALU,
-// a few elements after each MFMA, so that the two pipes overlap.
+// its side data (tile factors, MX block scales), in a ring of three filled
+// straight from global memory by direct-to-LDS loads, with no register
+// staging: stage t + 2 streams in while stage t is multiplied.  int8 and
+// E4M3 run the eight waves as two groups half a stage apart (gemm_body_pp);
+// MXFP4 keeps one pipeline for all waves, with double-buffered partial sums:
+// each K tile's MFMAs write one set while the previous tile's set is
+// rescaled by its factors on the VALU, a few elements after each MFMA.
 // LDS rows are 128 bytes with the 16-byte chunk c of row r at position
 // c ^ ((r / 2) % 8): a wave's 1 KB direct load fills rows 8q .. 8q + 7 (lane
 // l at row 8q + l / 8, position l % 8), and the 16 lanes of one LDS cycle
@@ -3436,113 +3437,72 @@ __device__ __forceinline__ void gemm_rescale(int e0, const typename GemmMode<MOD
   }
 }
 
-// One 128-deep K unit (unit UNIT of the stage): its MFMAs into `cur` (from
-// zero when FRESH, the first unit of a factor tile; accumulated otherwise),
-// with the previous tile's partials `prev` rescaled by `gprev` a few
-// elements after each MFMA when RS.
-template <int MODE, int UNIT, bool FRESH = true, bool RS = true>
-__device__ __forceinline__ void gemm_tile(const int8_t* stage, int wm, int wn, int lane,
-                                          typename GemmMode<MODE>::acc_t (&cur)[2][kGemmNB],
-                                          const typename GemmMode<MODE>::acc_t (&prev)[2][kGemmNB],
-                                          const float (&gprev)[kGemmNB],
-                                          float (&accf)[2][kGemmNB][16], const uint2 (&xs)[2],
-                                          const uint2 (&ws)[kGemmNB]) {
-  using acc_t = typename GemmMode<MODE>::acc_t;
-  constexpr int STEPS = GemmMode<MODE>::STEPS;
+// MXFP4: one 128-deep K unit (unit UNIT of the stage, two 64-deep steps of
+// one MX block each): its MFMAs into `cur` (from zero when FRESH, the first
+// unit of a factor tile; accumulated otherwise), with the previous tile's
+// partials `prev` rescaled by `gprev` a few elements after each MFMA when RS.
+template <int UNIT, bool FRESH = true, bool RS = true>
+__device__ __forceinline__ void gemm_tile_mx4(const int8_t* stage, int wm, int wn, int lane,
+                                              v16f_t (&cur)[2][kGemmNB], const v16f_t (&prev)[2][kGemmNB],
+                                              const float (&gprev)[kGemmNB], float (&accf)[2][kGemmNB][16],
+                                              const uint2 (&xs)[2], const uint2 (&ws)[kGemmNB]) {
+  constexpr int STEPS = GemmMode<2>::STEPS;
   constexpr int E = 64 / (STEPS * 2 * kGemmNB);  // rescaled elements per MFMA
   const int8_t* sa = stage;
   const int8_t* sb = stage + kGemmStageA;
   const int h = lane >> 5;
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
-    if constexpr (MODE == 1) {
-      // 64-deep E4M3 step: 32 bytes a lane, chunks 4 s + 2 h and the next
-      v8i_t fa[2], fb[kGemmNB];
+    // 64-deep step ks = 2 UNIT + s, chunk 2 ks + h (32 E2M1 values, one MX block)
+    const int c = 2 * (2 * UNIT + s) + h;
+    v4i_t fa[2], fb[kGemmNB];
 #pragma unroll
-      for (int a = 0; a < 2; ++a) {
-        const int row = wm * 64 + a * 32 + (lane & 31);
-        const v4i_t lo = gemm_frag(sa, row, 4 * s + 2 * h), hi = gemm_frag(sa, row, 4 * s + 2 * h + 1);
-        fa[a] = (v8i_t){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      }
+    for (int a = 0; a < 2; ++a) fa[a] = gemm_frag(sa, wm * 64 + a * 32 + (lane & 31), c);
+#pragma unroll
+    for (int b = 0; b < kGemmNB; ++b) fb[b] = gemm_frag(sb, wn * (kGemmN / 2) + b * 32 + (lane & 31), c);
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
       for (int b = 0; b < kGemmNB; ++b) {
-        const int row = wn * (kGemmN / 2) + b * 32 + (lane & 31);
-        const v4i_t lo = gemm_frag(sb, row, 4 * s + 2 * h), hi = gemm_frag(sb, row, 4 * s + 2 * h + 1);
-        fb[b] = (v8i_t){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        // the scale byte of step ks is byte 2 (ks % 2) of word ks / 2
+        const uint32_t xa = UNIT == 0 ? xs[a].x : xs[a].y, wb = UNIT == 0 ? ws[b].x : ws[b].y;
+        const v16f_t c0 = (FRESH && s == 0) ? (v16f_t){} : cur[a][b];
+        cur[a][b] = s == 0 ? mfma_mxfp4<0>(fa[a], fb[b], c0, xa, wb) : mfma_mxfp4<2>(fa[a], fb[b], c0, xa, wb);
+        if constexpr (RS) gemm_rescale<2, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
       }
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < kGemmNB; ++b) {
-          // cbsz = blgp = 0: both operands E4M3; scale bytes 127 (2^0)
-          cur[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-              fa[a], fb[b], (FRESH && s == 0) ? (acc_t){} : cur[a][b], 0, 0, 0, 127, 0, 127);
-          if constexpr (RS) gemm_rescale<MODE, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
-        }
-    } else {
-      // int8: 32-deep step, chunk 2 s + h; MXFP4: 64-deep step ks = 2 UNIT + s,
-      // chunk 2 ks + h (32 E2M1 values, one MX block)
-      const int c = MODE == 2 ? 2 * (2 * UNIT + s) + h : 2 * s + h;
-      v4i_t fa[2], fb[kGemmNB];
-#pragma unroll
-      for (int a = 0; a < 2; ++a) fa[a] = gemm_frag(sa, wm * 64 + a * 32 + (lane & 31), c);
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b) fb[b] = gemm_frag(sb, wn * (kGemmN / 2) + b * 32 + (lane & 31), c);
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < kGemmNB; ++b) {
-          if constexpr (MODE == 0) {
-            cur[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
-                fa[a], fb[b], (FRESH && s == 0) ? (acc_t){} : cur[a][b], 0, 0, 0);
-          } else {
-            constexpr int ks = 2 * UNIT;  // + s: the scale byte of step ks is byte 2 (ks % 2) of word ks / 2
-            const uint32_t xa = UNIT == 0 ? xs[a].x : xs[a].y, wb = UNIT == 0 ? ws[b].x : ws[b].y;
-            const acc_t c0 = (FRESH && s == 0) ? (acc_t){} : cur[a][b];
-            cur[a][b] = s == 0 ? mfma_mxfp4<0>(fa[a], fb[b], c0, xa, wb)
-                               : mfma_mxfp4<2>(fa[a], fb[b], c0, xa, wb);
-            (void)ks;
-          }
-          if constexpr (RS) gemm_rescale<MODE, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
-        }
-    }
   }
   // Pin the interleave for the scheduler: a step's fragment reads, then each
-  // MFMA followed by its share of the rescale (int8: a convert and an fma per
-  // element).
-  constexpr int DSR = MODE == 1 ? 8 : 4;  // 16-byte LDS reads per step
-  constexpr int VPM = MODE == 0 ? 2 * E : E;
+  // MFMA followed by its share of the rescale.
   if constexpr (RS)
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
-    __builtin_amdgcn_sched_group_barrier(0x100, DSR, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
     for (int i = 0; i < 2 * kGemmNB; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, VPM, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, E, 0);
     }
   }
 }
 
-// MODE 0: int8, 1: fp8 (E4M3), 2: MXFP4.
-template <int MODE>
-__device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
-  using acc_t = typename GemmMode<MODE>::acc_t;
-  constexpr int SB = gemm_stage_bytes<MODE>();
+// The MXFP4 GEMM: one pipeline for all waves, two 128-deep K units per
+// 128-byte stage.
+__device__ __forceinline__ void gemm_body_mx4(const hq_gemm_args& A) {
+  constexpr int SB = gemm_stage_bytes<2>();
   extern __shared__ __attribute__((aligned(16))) int8_t gsm[];  // ring slot s at gsm + s * SB
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
-  const int64_t T = A.K / HQ_TILE;                            // 128-deep K units
-  const int64_t TS = T / GemmMode<MODE>::U;                   // LDS stages
+  const int64_t T = A.K / HQ_TILE;          // 128-deep K units
+  const int64_t TS = T / GemmMode<2>::U;    // LDS stages
 
   float accf[2][kGemmNB][16];
-  acc_t acc0[2][kGemmNB], acc1[2][kGemmNB];
+  v16f_t acc0[2][kGemmNB], acc1[2][kGemmNB];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < kGemmNB; ++b) {
-      acc1[a][b] = (acc_t){};  // the "previous tile" of the first: zero, factor 0
+      acc1[a][b] = (v16f_t){};  // the "previous tile" of the first: zero, factor 0
 #pragma unroll
       for (int r = 0; r < 16; ++r) accf[a][b][r] = 0.0f;
     }
@@ -3551,7 +3511,7 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
   for (int b = 0; b < kGemmNB; ++b) gprev[b] = 0.0f;
 
   const int wsc = __builtin_amdgcn_readfirstlane(wave);  // wave-uniform, in a scalar register
-  const GemmLoads gl = gemm_loads<MODE>(A, m0, n0, wsc, lane);
+  const GemmLoads gl = gemm_loads<2>(A, m0, n0, wsc, lane);
   // Stage t sits in ring slot t % 3.  Before it is read: this wave's loads
   // of stage t are done (only stage t + 1's, issued later, may be in
   // flight), its LDS reads of stage t - 1 have returned, and every wave has
@@ -3559,94 +3519,71 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
   // stage t + 2 (the last stage is fetched again near the end, into a slot
   // no wave reads).  A bare barrier: the loads still in flight are not
   // waited for.
-  constexpr int NL = MODE == 2 ? 9 : 7;  // buffer loads per wave and stage
+  constexpr int NL = 9;  // buffer loads per wave and stage
   auto begin_stage = [&](int64_t t) -> const int8_t* {
     asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NL) : "memory");
-    gemm_fetch<MODE>(gl, min(t + 2, TS - 1), wsc, gsm + ((t + 2) % 3) * SB);
+    gemm_fetch<2>(gl, min(t + 2, TS - 1), wsc, gsm + ((t + 2) % 3) * SB);
     return gsm + (t % 3) * SB;
   };
   uint2 xs[2], ws[kGemmNB];
-  gemm_fetch<MODE>(gl, 0, wsc, gsm);
-  gemm_fetch<MODE>(gl, min<int64_t>(1, TS - 1), wsc, gsm + SB);
+  auto scales = [&](const int8_t* side) {
+#pragma unroll
+    for (int a = 0; a < 2; ++a) xs[a] = mx_scales(side + kGemmSideXs, wm * 64 + a * 32 + (lane & 31), lane);
+#pragma unroll
+    for (int b = 0; b < kGemmNB; ++b)
+      ws[b] = mx_scales(side + kGemmSideWs, wn * (kGemmN / 2) + b * 32 + (lane & 31), lane);
+  };
+  gemm_fetch<2>(gl, 0, wsc, gsm);
+  gemm_fetch<2>(gl, min<int64_t>(1, TS - 1), wsc, gsm + SB);
   if (A.tile > HQ_TILE) {
     // factor tiles of tile / 128 units (long RHT tiles, Sec. 7.2): a tile's
     // units accumulate into acc0 and its rescale follows its last unit, one
     // rescale per tile / 128 units
-    const int64_t spt = (int64_t)(A.tile / HQ_TILE) / GemmMode<MODE>::U;  // stages per tile
+    const int64_t spt = (int64_t)(A.tile / HQ_TILE) / GemmMode<2>::U;  // stages per tile
     for (int64_t t = 0; t < TS; t += spt) {
       float gt[kGemmNB];
       for (int64_t j = 0; j < spt; ++j) {
         const int8_t* const stage = begin_stage(t + j);
         const int8_t* const side = stage + kGemmStageA + kGemmStageB;
         if (j == 0) gemm_side_g(side, 0, wn, lane, gt);
-        if constexpr (MODE == 2) {
-#pragma unroll
-          for (int a = 0; a < 2; ++a)
-            xs[a] = mx_scales(side + kGemmSideXs, wm * 64 + a * 32 + (lane & 31), lane);
-#pragma unroll
-          for (int b = 0; b < kGemmNB; ++b)
-            ws[b] = mx_scales(side + kGemmSideWs, wn * (kGemmN / 2) + b * 32 + (lane & 31), lane);
-          if (j == 0)
-            gemm_tile<MODE, 0, true, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-          else
-            gemm_tile<MODE, 0, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-          gemm_tile<MODE, 1, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-        } else {
-          if (j == 0)
-            gemm_tile<MODE, 0, true, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-          else
-            gemm_tile<MODE, 0, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-        }
+        scales(side);
+        if (j == 0)
+          gemm_tile_mx4<0, true, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+        else
+          gemm_tile_mx4<0, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+        gemm_tile_mx4<1, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
       }
-      gemm_rescale<MODE, 64>(0, acc0, gt, accf);
+      gemm_rescale<2, 64>(0, acc0, gt, accf);
     }
-  } else if constexpr (MODE == 2) {
+  } else {
     // two K tiles per stage: tile 0 into acc0 (rescaling acc1), tile 1 into acc1
     for (int64_t t = 0; t < TS; ++t) {
       const int8_t* const stage = begin_stage(t);
       const int8_t* const side = stage + kGemmStageA + kGemmStageB;
-#pragma unroll
-      for (int a = 0; a < 2; ++a) xs[a] = mx_scales(side + kGemmSideXs, wm * 64 + a * 32 + (lane & 31), lane);
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b)
-        ws[b] = mx_scales(side + kGemmSideWs, wn * (kGemmN / 2) + b * 32 + (lane & 31), lane);
+      scales(side);
       float g0[kGemmNB], g1[kGemmNB];
       gemm_side_g(side, 0, wn, lane, g0);
       gemm_side_g(side, 1, wn, lane, g1);
-      gemm_tile<MODE, 0>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-      gemm_tile<MODE, 1>(stage, wm, wn, lane, acc1, acc0, g0, accf, xs, ws);
+      gemm_tile_mx4<0>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
+      gemm_tile_mx4<1>(stage, wm, wn, lane, acc1, acc0, g0, accf, xs, ws);
 #pragma unroll
       for (int b = 0; b < kGemmNB; ++b) gprev[b] = g1[b];
     }
-  } else {
-    // one K tile per stage and an even number of stages (K is a multiple of
-    // 256): stage t into acc0, stage t + 1 into acc1
-    for (int64_t t = 0; t < TS; t += 2) {
-      float g0[kGemmNB], g1[kGemmNB];
-      const int8_t* stage = begin_stage(t);
-      gemm_side_g(stage + kGemmStageA + kGemmStageB, 0, wn, lane, g0);
-      gemm_tile<MODE, 0>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-      stage = begin_stage(t + 1);
-      gemm_side_g(stage + kGemmStageA + kGemmStageB, 0, wn, lane, g1);
-      gemm_tile<MODE, 0>(stage, wm, wn, lane, acc1, acc0, g0, accf, xs, ws);
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b) gprev[b] = g1[b];
-    }
+    gemm_rescale<2, 64>(0, acc1, gprev, accf);  // the last tile's partials
   }
-  if (A.tile == HQ_TILE) gemm_rescale<MODE, 64>(0, acc1, gprev, accf);  // the last tile's partials
 
+  // MXFP4 blocks carry their own scale: no per-token factor
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int64_t m = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (m >= A.M) continue;
-      const float sxm = MODE == 2 ? 1.0f : A.sx[m];  // MXFP4 blocks carry their own scale
 #pragma unroll
       for (int b = 0; b < kGemmNB; ++b) {
         const int64_t n = n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31);
         if (n >= A.N) continue;
-        const float v = sxm * accf[a][b][r];
+        const float v = accf[a][b][r];
         if (A.out_bf16)
           ((uint16_t*)A.out)[m * A.N + n] = (uint16_t)f32_to_bf16(v);
         else
@@ -3655,12 +3592,41 @@ __device__ __forceinline__ void gemm_body(const hq_gemm_args& A) {
     }
 }
 
-// int8 and E4M3 at 128-deep factor tiles: the eight waves in two groups of
-// four (waves 0-3 and 4-7, so each SIMD holds one wave of each) that run
-// half a stage apart.  A wave's stage t has two phases: in V(t) it issues the
+// The MFMA phase of a stage: its STEPS steps into `cur`, from zero when
+// FRESH (the first stage of a factor tile).
+template <int MODE, bool FRESH>
+__device__ __forceinline__ void gemm_mfma_pp(
+    const v4i_t (&fa)[GemmMode<MODE>::STEPS][2][MODE == 1 ? 2 : 1],
+    const v4i_t (&fb)[GemmMode<MODE>::STEPS][kGemmNB][MODE == 1 ? 2 : 1],
+    typename GemmMode<MODE>::acc_t (&cur)[2][kGemmNB]) {
+  using acc_t = typename GemmMode<MODE>::acc_t;
+#pragma unroll
+  for (int s = 0; s < GemmMode<MODE>::STEPS; ++s)
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b) {
+        const acc_t c0 = (FRESH && s == 0) ? (acc_t){} : cur[a][b];
+        if constexpr (MODE == 0) {
+          cur[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[s][a][0], fb[s][b][0], c0, 0, 0, 0);
+        } else {
+          const v8i_t x = {fa[s][a][0][0], fa[s][a][0][1], fa[s][a][0][2], fa[s][a][0][3],
+                           fa[s][a][1][0], fa[s][a][1][1], fa[s][a][1][2], fa[s][a][1][3]};
+          const v8i_t y = {fb[s][b][0][0], fb[s][b][0][1], fb[s][b][0][2], fb[s][b][0][3],
+                           fb[s][b][1][0], fb[s][b][1][1], fb[s][b][1][2], fb[s][b][1][3]};
+          // cbsz = blgp = 0: both operands E4M3; scale bytes 127 (2^0)
+          cur[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(x, y, c0, 0, 0, 0, 127, 0, 127);
+        }
+      }
+}
+
+// int8 and E4M3, any factor tile: the eight waves in two groups of four
+// (waves 0-3 and 4-7, so each SIMD holds one wave of each) that run half a
+// stage apart.  A wave's stage t has two phases: in V(t) it issues the
 // direct-to-LDS loads of stage t + 2, reads every fragment of stage t into
-// registers and rescales the partial sums of stage t - 1 into its fp32
-// accumulators; in M(t) it only issues MFMAs.  Group 0 runs V(t) in phase
+// registers and, when stage t starts a factor tile, rescales the previous
+// tile's partial sums into its fp32 accumulators; in M(t) it only issues
+// MFMAs (a long tile's stages accumulate into the same partials).  Group 0 runs V(t) in phase
 // 2t and M(t) in phase 2t + 1, group 1 one phase later, and every phase ends
 // at a workgroup barrier, so on each SIMD one wave's MFMAs run while the
 // other wave's LDS reads and rescale issue.  The barrier waits leave only
@@ -3683,6 +3649,7 @@ __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
   const int wm = wsc >> 1, wn = wsc & 1, grp = wsc >> 2;
   const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
   const int64_t TS = A.K / HQ_TILE;
+  const uint32_t tmask = (uint32_t)(A.tile / HQ_TILE) - 1u;  // stages per factor tile, less one
 
   float accf[2][kGemmNB][16];
 #pragma unroll
@@ -3726,28 +3693,19 @@ __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
       }
     }
     __builtin_amdgcn_sched_barrier(0);  // the reads issue first; the rescale runs under them
-    if (t > 0) gemm_rescale<MODE, 64>(0, cur, gcur, accf);
-    gemm_side_g(stage + kGemmStageA + kGemmStageB, 0, wn, lane, gcur);
+    // a factor tile of spt stages: its partials accumulate over its stages,
+    // and are rescaled once, in the V phase that starts the next tile
+    const bool first = ((uint32_t)t & tmask) == 0u;  // wave-uniform
+    if (first) {
+      if (t > 0) gemm_rescale<MODE, 64>(0, cur, gcur, accf);
+      gemm_side_g(stage + kGemmStageA + kGemmStageB, 0, wn, lane, gcur);
+    }
     phase();
     // M(t)
-#pragma unroll
-    for (int s = 0; s < STEPS; ++s)
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < kGemmNB; ++b) {
-          const acc_t c0 = s == 0 ? (acc_t){} : cur[a][b];
-          if constexpr (MODE == 0) {
-            cur[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[s][a][0], fb[s][b][0], c0, 0, 0, 0);
-          } else {
-            const v8i_t x = {fa[s][a][0][0], fa[s][a][0][1], fa[s][a][0][2], fa[s][a][0][3],
-                             fa[s][a][1][0], fa[s][a][1][1], fa[s][a][1][2], fa[s][a][1][3]};
-            const v8i_t y = {fb[s][b][0][0], fb[s][b][0][1], fb[s][b][0][2], fb[s][b][0][3],
-                             fb[s][b][1][0], fb[s][b][1][1], fb[s][b][1][2], fb[s][b][1][3]};
-            // cbsz = blgp = 0: both operands E4M3; scale bytes 127 (2^0)
-            cur[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(x, y, c0, 0, 0, 0, 127, 0, 127);
-          }
-        }
+    if (first)
+      gemm_mfma_pp<MODE, true>(fa, fb, cur);
+    else
+      gemm_mfma_pp<MODE, false>(fa, fb, cur);
   }
   if (grp == 0) phase();  // the same barrier count in both groups
   gemm_rescale<MODE, 64>(0, cur, gcur, accf);  // the last tile
@@ -3775,23 +3733,15 @@ __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
 }
 
 __global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_i8_kernel(hq_gemm_args A) {
-  gemm_body<0>(A);
-}
-
-__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_f8_kernel(hq_gemm_args A) {
-  gemm_body<1>(A);
-}
-
-__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_i8_pp_kernel(hq_gemm_args A) {
   gemm_body_pp<0>(A);
 }
 
-__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_f8_pp_kernel(hq_gemm_args A) {
+__global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_f8_kernel(hq_gemm_args A) {
   gemm_body_pp<1>(A);
 }
 
 __global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_mx4_kernel(hq_gemm_args A) {
-  gemm_body<2>(A);
+  gemm_body_mx4(A);
 }
 
 // ------------------------------------------------------------ utilities
@@ -4029,12 +3979,6 @@ int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
     if (e == hipSuccess)
       e = hipFuncSetAttribute((const void*)hq_gemm_mx4_kernel,
                               hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<2>());
-    if (e == hipSuccess)
-      e = hipFuncSetAttribute((const void*)hq_gemm_i8_pp_kernel,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<0>());
-    if (e == hipSuccess)
-      e = hipFuncSetAttribute((const void*)hq_gemm_f8_pp_kernel,
-                              hipFuncAttributeMaxDynamicSharedMemorySize, gemm_lds_bytes<1>());
     if (e != hipSuccess) return (int)e;
     lds_set = true;
   }
@@ -4042,12 +3986,8 @@ int hq_launch_gemm(const hq_gemm_args& a, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   if (a.fp8 == 2)
     hipLaunchKernelGGL(hq_gemm_mx4_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<2>(), st, a);
-  else if (a.fp8 && a.tile == HQ_TILE)
-    hipLaunchKernelGGL(hq_gemm_f8_pp_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<1>(), st, a);
   else if (a.fp8)
     hipLaunchKernelGGL(hq_gemm_f8_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<1>(), st, a);
-  else if (a.tile == HQ_TILE)
-    hipLaunchKernelGGL(hq_gemm_i8_pp_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<0>(), st, a);
   else
     hipLaunchKernelGGL(hq_gemm_i8_kernel, grid, dim3(kGemmThreads), gemm_lds_bytes<0>(), st, a);
   return (int)hipGetLastError();

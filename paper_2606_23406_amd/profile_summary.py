@@ -39,10 +39,8 @@ SRC = os.path.join(ROOT, "paper_2606_23406_amd", "csrc", "hq_kernels.hip")
 KERNELS = {
     "encode": "hq_encode_group_kernel<0, 0, false>",
     "decode": "hq_decode_group_kernel<0, 1, false>",
-    "gemm": "hq_gemm_i8_pp_kernel",
-    "gemm_fp8": "hq_gemm_f8_pp_kernel",
-    "gemm_long_tiles": "hq_gemm_i8_kernel",
-    "gemm_fp8_long_tiles": "hq_gemm_f8_kernel",
+    "gemm": "hq_gemm_i8_kernel",
+    "gemm_fp8": "hq_gemm_f8_kernel",
     "gemm_mxfp4": "hq_gemm_mx4_kernel",
     "decode_gemv": "hq_decode_gemv_kernel",
     "decode_gemv_rows": "hq_decode_gemv_rows_kernel",
