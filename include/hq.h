@@ -306,26 +306,29 @@ hq_status hq_gemm_fp8_blockscaled(hq_plan_t plan, const uint8_t* xq, const float
  * each element is FP4 E2M1 (magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6), the
  * nearest value to v / 2^X with ties to the even code and saturation at 6.
  * Two elements per byte, the even k in the low nibble.
- * hq_decode_mxfp4 -- as hq_decode_int8, with the lattice codes cast to MXFP4:
- *   codes device [rows, cols / 2] bytes (contiguous), scales device
- *   [rows, cols / 32] bytes, g device fp32 [rows, tiles_per_row].  Same plans
- *   and errors as hq_decode_int8.
+ * hq_decode_mxfp4 -- as hq_decode_int8, with the reconstruction cast to
+ *   MXFP4 (Sec. 4.8 Cast: the reconstruction is cast at the matmul
+ *   boundary): in the rotated coordinates, v = g[r, t] c[r, k] (the int8
+ *   path's tile factor times the lattice code, one fp32 product), cast per
+ *   32-block.  A block lies inside one tile, so the block scales carry the
+ *   tile factor and no factor array is returned.  codes device
+ *   [rows, cols / 2] bytes (contiguous), scales device [rows, cols / 32]
+ *   bytes.  Same plans and errors as hq_decode_int8.
  * hq_act_prep_mxfp4 -- activation side: per K-tile y = H D a as hq_act_prep,
  *   then the MXFP4 cast of y: xq device [M, cols / 2], scales [M, cols / 32];
  *   the block scales carry the magnitude, so there is no per-token factor.
- * hq_gemm_mxfp4_blockscaled -- out[i, r] = sum_t g[r, t] sum_{k in tile t}
- *   X[i, k] W[r, k] over the MXFP4 values (element times block scale): fp32
- *   tile sums on the gfx950 scaled matrix cores (v_mfma_scale_f32_32x32x64_
- *   f8f6f4, E2M1 operands with per-32 E8M0 scales), each rescaled by g.
- *   Operands contiguous, scale arrays 8-byte aligned; out M x N, HQ_BF16 or
- *   HQ_FP32. */
+ * hq_gemm_mxfp4_blockscaled -- out[i, r] = sum_k X[i, k] W[r, k] over the
+ *   MXFP4 values (element times block scale), accumulated in fp32 on the
+ *   gfx950 scaled matrix cores (v_mfma_scale_f32_32x32x64_f8f6f4, E2M1
+ *   operands with per-32 E8M0 scales, which carry every factor).  Operands
+ *   contiguous, scale arrays 8-byte aligned; out M x N, HQ_BF16 or HQ_FP32. */
 hq_status hq_decode_mxfp4(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows,
-                          uint8_t* codes, uint8_t* scales, float* g, void* stream);
+                          uint8_t* codes, uint8_t* scales, void* stream);
 hq_status hq_act_prep_mxfp4(hq_plan_t plan, const void* a, int64_t M, int64_t lda, uint8_t* xq,
                             uint8_t* scales, void* stream);
 hq_status hq_gemm_mxfp4_blockscaled(hq_plan_t plan, const uint8_t* xq, const uint8_t* xs, int64_t M,
-                                    const uint8_t* codes, const uint8_t* ws, const float* g,
-                                    int64_t N, void* out, int32_t ot, void* stream);
+                                    const uint8_t* codes, const uint8_t* ws, int64_t N, void* out,
+                                    int32_t ot, void* stream);
 
 /* Workspace bytes for hq_dequant_gemm_int8 with M tokens and N weight rows. */
 size_t hq_gemm_workspace_bytes(hq_plan_t plan, int64_t M, int64_t N);

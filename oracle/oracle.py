@@ -625,10 +625,16 @@ def mxfp4_value(codes, scales):
     return (c.reshape(rows, K // MX_BLOCK, MX_BLOCK) * np.ldexp(1.0, X)[:, :, None]).reshape(rows, K)
 
 
-def weight_codes_mxfp4(codes):
-    """The MXFP4 cast of the weight side: the lattice codes, 32 along K per
-    block (the per-tile factors g stay as in the int8 path)."""
-    return mxfp4_cast(np.asarray(codes, dtype=np.float64))
+def weight_codes_mxfp4(codes, g, tile):
+    """The MXFP4 cast of the weight side (Sec. 4.8 Cast: the reconstruction
+    is what is cast at the matmul boundary).  In the rotated coordinates the
+    reconstruction of coordinate k of row n is g[n, t] c[n, k], t the tile of
+    k: one fp32 product per coordinate, then the MX cast 32 along K per
+    block.  A block lies inside one tile, so its E8M0 scale carries the tile
+    factor's binade and its elements the rest."""
+    c = np.asarray(codes).astype(np.float32)
+    gk = np.repeat(np.asarray(g, dtype=np.float32), tile, axis=1)
+    return mxfp4_cast((c * gk).astype(np.float64))
 
 
 def act_prep_mxfp4(a, tile, rht_seed):
@@ -642,14 +648,9 @@ def act_prep_mxfp4(a, tile, rht_seed):
     return mxfp4_cast(y)
 
 
-def gemm_mxfp4_blockscaled(w4, ws, g, x4, xs, tile):
-    """out[m, n] = sum_t g[n, t] sum_{k in t} X[m, k] W[n, k] over the MXFP4
-    values (element times block scale), in fp64."""
-    W = mxfp4_value(w4, ws)
-    X = mxfp4_value(x4, xs)
-    N, K = W.shape
-    out = np.zeros((X.shape[0], N))
-    for t in range(K // tile):
-        ks = slice(t * tile, (t + 1) * tile)
-        out += (X[:, ks] @ W[:, ks].T) * np.asarray(g, np.float64)[:, t][None, :]
-    return out
+def gemm_mxfp4(w4, ws, x4, xs):
+    """out[m, n] = sum_k X[m, k] W[n, k] over the MXFP4 values (element times
+    block scale), in fp64: the block scales carry every factor."""
+    return mxfp4_value(x4, xs) @ mxfp4_value(w4, ws).T
+
+

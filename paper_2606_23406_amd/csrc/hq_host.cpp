@@ -789,19 +789,19 @@ hq_status hq_decode_fp8(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t r
 }
 
 hq_status hq_decode_mxfp4(hq_plan_t p, const hq_stream* s, int64_t row0, int64_t rows,
-                          uint8_t* codes, uint8_t* scales, float* g, void* stream) {
+                          uint8_t* codes, uint8_t* scales, void* stream) {
   // sub-streams of 512 (any tile: the codes carry no transform)
   if (p && p->substream != HQ_SUB) return HQ_ERR_UNSUPPORTED;
   if (!p || !s || row0 < 0 || rows < 0) return HQ_ERR_INVALID_ARG;
   if (p->lattice == HQ_A2 || p->dither || p->rotation) return HQ_ERR_UNSUPPORTED;
   if (row0 + rows > s->rows) return HQ_ERR_INVALID_ARG;
   if (rows == 0) return HQ_OK;
-  if (!codes || !scales || !g || ((uintptr_t)codes & 3u) != 0) return HQ_ERR_INVALID_ARG;
+  if (!codes || !scales || ((uintptr_t)codes & 3u) != 0) return HQ_ERR_INVALID_ARG;
   hq_decode_args a;
   fill_decode_args(p, s, row0, rows, &a);
   a.y = codes;
   a.ld = p->cols / 2;  // contiguous rows of cols / 2 bytes
-  a.g = g;
+  a.g = nullptr;       // the tile factors go into the cast
   a.mxs = scales;
   return hip_status(hq_launch_decode_mxfp4(p, a, stream));
 }
@@ -850,7 +850,7 @@ static hq_status gemm_blockscaled(hq_plan_t p, const int8_t* xq, const float* sx
   if (!p || M < 0 || N < 0) return HQ_ERR_INVALID_ARG;
   if (ot != HQ_BF16 && ot != HQ_FP32) return HQ_ERR_INVALID_ARG;
   if (M == 0 || N == 0) return HQ_OK;
-  if (!xq || (fp8 == 2 ? (!xs || !ws) : !sx) || !codes || !g || !out) return HQ_ERR_INVALID_ARG;
+  if (!xq || (fp8 == 2 ? (!xs || !ws) : (!sx || !g)) || !codes || !out) return HQ_ERR_INVALID_ARG;
   if (fp8 == 2 && (((uintptr_t)xs & 7u) != 0 || ((uintptr_t)ws & 7u) != 0)) return HQ_ERR_INVALID_ARG;
   if (!aligned16(xq) || !aligned16(codes) || !aligned16(out)) return HQ_ERR_INVALID_ARG;
   hq_gemm_args a;
@@ -886,10 +886,10 @@ hq_status hq_gemm_fp8_blockscaled(hq_plan_t p, const uint8_t* xq, const float* s
 }
 
 hq_status hq_gemm_mxfp4_blockscaled(hq_plan_t plan, const uint8_t* xq, const uint8_t* xs, int64_t M,
-                                    const uint8_t* codes, const uint8_t* ws, const float* g,
-                                    int64_t N, void* out, int32_t ot, void* stream) {
-  return gemm_blockscaled(plan, (const int8_t*)xq, nullptr, M, (const int8_t*)codes, g, N, out, ot,
-                          2, stream, xs, ws);
+                                    const uint8_t* codes, const uint8_t* ws, int64_t N, void* out,
+                                    int32_t ot, void* stream) {
+  return gemm_blockscaled(plan, (const int8_t*)xq, nullptr, M, (const int8_t*)codes, nullptr, N, out,
+                          ot, 2, stream, xs, ws);
 }
 
 size_t hq_gemm_workspace_bytes(hq_plan_t p, int64_t M, int64_t N) {

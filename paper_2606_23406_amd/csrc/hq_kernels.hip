@@ -2221,24 +2221,27 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
         A.g[(int64_t)lrow * A.tpr + (col >> __builtin_ctz((uint32_t)A.tile))] = g;
       if (clamps && A.stats) atomicAdd(&A.stats->clamps, clamps);
     } else if constexpr (MODE == 4) {
-      // the MXFP4 cast (Sec. 4.8, Sec. 6.4): blocks of 32 codes (four lanes)
-      // share X = floor(log2 amax) - 2; each code becomes E2M1(c / 2^X),
-      // two per byte (the even k in the low nibble), the scale byte X + 127
-      float am = 0.0f;
+      // the MXFP4 cast of the reconstruction (Sec. 4.8, Sec. 6.4): v = g c in
+      // the rotated coordinates (one fp32 product); blocks of 32 values (four
+      // lanes, inside one tile) share X = floor(log2 amax) - 2, and each value
+      // becomes E2M1(v / 2^X), two per byte (the even k in the low nibble),
+      // the scale byte X + 127
+      float v[8], am = 0.0f;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) am = __builtin_fmaxf(am, __builtin_fabsf((float)c[j]));
+      for (int j = 0; j < 8; ++j) {
+        v[j] = (float)c[j] * g;
+        am = __builtin_fmaxf(am, __builtin_fabsf(v[j]));
+      }
       am = __builtin_fmaxf(am, dpp_xor<1>(am));
       am = __builtin_fmaxf(am, dpp_xor<2>(am));
       const int32_t X = mx_exponent(am);
-      const float inv = __builtin_ldexpf(1.0f, -X);  // exact; c / 2^X is exact
+      const float inv = __builtin_ldexpf(1.0f, -X);  // exact: v / 2^X is exact
       uint32_t packed = 0;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) packed |= e2m1_code((float)c[j] * inv) << (4 * j);
+      for (int j = 0; j < 8; ++j) packed |= e2m1_code(v[j] * inv) << (4 * j);
       uint8_t* out = (uint8_t*)A.y + (int64_t)lrow * A.ld + (col >> 1);
       *(uint32_t*)out = packed;
       if ((lane & 3) == 0) A.mxs[(int64_t)lrow * (A.spr * (HQ_SUB / 32)) + (col >> 5)] = (uint8_t)(X + 127);
-      if ((col & (uint32_t)(A.tile - 1)) == 0)
-        A.g[(int64_t)lrow * A.tpr + (col >> __builtin_ctz((uint32_t)A.tile))] = g;
     } else if constexpr (MODE == 3) {
       // the fp8 cast (Sec. 4.8): E4M3 of each code, round to nearest even,
       // magnitudes beyond 448 saturated and counted
@@ -3251,21 +3254,19 @@ __global__ __launch_bounds__(256) void hq_act_prep_kernel(hq_actprep_args A) {
 
 
 // ------------------------------------------------------------ block-scaled GEMM
-// out[m, n] = s_x[m] * sum_t g[n, t] * P_t[m, n], P_t the sum over one
-// 128-deep K tile: exact int32 on the int8 matrix cores
-// (v_mfma_i32_32x32x32_i8), fp32 on the f8f6f4 ones for E4M3 and MXFP4
-// (v_mfma_scale_f32_32x32x64_f8f6f4; MXFP4 scales every 32-block itself and
-// has s_x = 1).
+// int8 and E4M3: out[m, n] = s_x[m] * sum_t g[n, t] * P_t[m, n], P_t the sum
+// over one factor tile of K: exact int32 on the int8 matrix cores
+// (v_mfma_i32_32x32x32_i8), fp32 on the f8f6f4 ones for E4M3
+// (v_mfma_scale_f32_32x32x64_f8f6f4 with unit scales).  MXFP4: out[m, n] =
+// sum_k X[m, k] W[n, k] over the element-times-block-scale values on the
+// same instruction, whose E8M0 scales carry every factor.
 // Workgroup tile 256 (tokens) x 128 (weight rows), eight waves in 4 x 2, each
 // 64 x 64 = 2 x 2 MFMA blocks, one workgroup per CU.  An LDS stage is 128
 // bytes of every A and B row (one K tile of int8 / E4M3, two of MXFP4) plus
 // its side data (tile factors, MX block scales), in a ring of three filled
 // straight from global memory by direct-to-LDS loads, with no register
-// staging: stage t + 2 streams in while stage t is multiplied.  int8 and
-// E4M3 run the eight waves as two groups half a stage apart (gemm_body_pp);
-// MXFP4 keeps one pipeline for all waves, with double-buffered partial sums:
-// each K tile's MFMAs write one set while the previous tile's set is
-// rescaled by its factors on the VALU, a few elements after each MFMA.
+// staging: stage t + 2 streams in while stage t is multiplied, by eight
+// waves in two groups half a stage apart (gemm_body_pp).
 // LDS rows are 128 bytes with the 16-byte chunk c of row r at position
 // c ^ ((r / 2) % 8): a wave's 1 KB direct load fills rows 8q .. 8q + 7 (lane
 // l at row 8q + l / 8, position l % 8), and the 16 lanes of one LDS cycle
@@ -3300,8 +3301,7 @@ static_assert(gemm_lds_bytes<2>() <= 160 * 1024, "the LDS ring fits one CU");
 template <bool C, class T, class F> struct gemm_pick { using type = T; };
 template <class T, class F> struct gemm_pick<false, T, F> { using type = F; };
 template <int MODE> struct GemmMode {
-  static constexpr int U = MODE == 2 ? 2 : 1;      // 128-deep K tiles per stage
-  static constexpr int STEPS = MODE == 0 ? 4 : 2;  // MFMA steps per K tile
+  static constexpr int U = MODE == 2 ? 2 : 1;  // 128-deep K units per stage
   using acc_t = typename gemm_pick<MODE == 0, v16i_t, v16f_t>::type;
 };
 
@@ -3342,7 +3342,7 @@ __device__ __forceinline__ GemmLoads gemm_loads(const hq_gemm_args& A, int64_t m
   GemmLoads L;
   L.ra = gemm_rsrc(A.xq + m0 * rb, ma * rb);
   L.rb = gemm_rsrc(A.w + n0 * rb, nb * rb);
-  L.rg = gemm_rsrc(A.g + n0 * T, nb * T * 4);
+  L.rg = gemm_rsrc(MODE != 2 ? A.g + n0 * T : nullptr, MODE != 2 ? nb * T * 4 : 0);
   L.rxs = gemm_rsrc(MODE == 2 ? A.xs + m0 * ks : nullptr, MODE == 2 ? ma * ks : 0);
   L.rws = gemm_rsrc(MODE == 2 ? A.ws + n0 * ks : nullptr, MODE == 2 ? nb * ks : 0);
   const int rr = lane >> 3;
@@ -3383,8 +3383,9 @@ __device__ __forceinline__ void gemm_fetch(const GemmLoads& L, int64_t t, int wa
     __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, (lds_void_t*)(stage + kGemmStageA + (wave * 2 + i) * 1024),
                                              16, L.b[i], so, 0, 0);
   int8_t* const side = stage + kGemmStageA + kGemmStageB;
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rg, (lds_void_t*)(side + kGemmSideG + (wave % (2 * U)) * 256),
-                                           4, L.g, (uint32_t)(((U * t) >> L.lm) * 4), 0, 0);
+  if constexpr (MODE != 2)  // MXFP4 blocks carry the tile factors in their scales
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rg, (lds_void_t*)(side + kGemmSideG + (wave % (2 * U)) * 256),
+                                             4, L.g, (uint32_t)(((U * t) >> L.lm) * 4), 0, 0);
   if constexpr (MODE == 2) {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rxs, (lds_void_t*)(side + kGemmSideXs + wave * 256), 4,
                                              L.xs, (uint32_t)(t * 8), 0, 0);
@@ -3437,171 +3438,21 @@ __device__ __forceinline__ void gemm_rescale(int e0, const typename GemmMode<MOD
   }
 }
 
-// MXFP4: one 128-deep K unit (unit UNIT of the stage, two 64-deep steps of
-// one MX block each): its MFMAs into `cur` (from zero when FRESH, the first
-// unit of a factor tile; accumulated otherwise), with the previous tile's
-// partials `prev` rescaled by `gprev` a few elements after each MFMA when RS.
-template <int UNIT, bool FRESH = true, bool RS = true>
-__device__ __forceinline__ void gemm_tile_mx4(const int8_t* stage, int wm, int wn, int lane,
-                                              v16f_t (&cur)[2][kGemmNB], const v16f_t (&prev)[2][kGemmNB],
-                                              const float (&gprev)[kGemmNB], float (&accf)[2][kGemmNB][16],
-                                              const uint2 (&xs)[2], const uint2 (&ws)[kGemmNB]) {
-  constexpr int STEPS = GemmMode<2>::STEPS;
-  constexpr int E = 64 / (STEPS * 2 * kGemmNB);  // rescaled elements per MFMA
-  const int8_t* sa = stage;
-  const int8_t* sb = stage + kGemmStageA;
-  const int h = lane >> 5;
-#pragma unroll
-  for (int s = 0; s < STEPS; ++s) {
-    // 64-deep step ks = 2 UNIT + s, chunk 2 ks + h (32 E2M1 values, one MX block)
-    const int c = 2 * (2 * UNIT + s) + h;
-    v4i_t fa[2], fb[kGemmNB];
-#pragma unroll
-    for (int a = 0; a < 2; ++a) fa[a] = gemm_frag(sa, wm * 64 + a * 32 + (lane & 31), c);
-#pragma unroll
-    for (int b = 0; b < kGemmNB; ++b) fb[b] = gemm_frag(sb, wn * (kGemmN / 2) + b * 32 + (lane & 31), c);
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b) {
-        // the scale byte of step ks is byte 2 (ks % 2) of word ks / 2
-        const uint32_t xa = UNIT == 0 ? xs[a].x : xs[a].y, wb = UNIT == 0 ? ws[b].x : ws[b].y;
-        const v16f_t c0 = (FRESH && s == 0) ? (v16f_t){} : cur[a][b];
-        cur[a][b] = s == 0 ? mfma_mxfp4<0>(fa[a], fb[b], c0, xa, wb) : mfma_mxfp4<2>(fa[a], fb[b], c0, xa, wb);
-        if constexpr (RS) gemm_rescale<2, E>(((s * 2 + a) * kGemmNB + b) * E, prev, gprev, accf);
-      }
-  }
-  // Pin the interleave for the scheduler: a step's fragment reads, then each
-  // MFMA followed by its share of the rescale.
-  if constexpr (RS)
-#pragma unroll
-  for (int s = 0; s < STEPS; ++s) {
-    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-    for (int i = 0; i < 2 * kGemmNB; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, E, 0);
-    }
-  }
-}
+// MFMA steps per stage: int8 32-deep (four), E4M3 64-deep (two), MXFP4
+// 64-deep over its two K units (four), and 16-byte chunks per fragment.
+template <int MODE> constexpr int gemm_pp_steps() { return MODE == 1 ? 2 : 4; }
+template <int MODE> constexpr int gemm_pp_fw() { return MODE == 1 ? 2 : 1; }
 
-// The MXFP4 GEMM: one pipeline for all waves, two 128-deep K units per
-// 128-byte stage.
-__device__ __forceinline__ void gemm_body_mx4(const hq_gemm_args& A) {
-  constexpr int SB = gemm_stage_bytes<2>();
-  extern __shared__ __attribute__((aligned(16))) int8_t gsm[];  // ring slot s at gsm + s * SB
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
-  const int64_t T = A.K / HQ_TILE;          // 128-deep K units
-  const int64_t TS = T / GemmMode<2>::U;    // LDS stages
-
-  float accf[2][kGemmNB][16];
-  v16f_t acc0[2][kGemmNB], acc1[2][kGemmNB];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < kGemmNB; ++b) {
-      acc1[a][b] = (v16f_t){};  // the "previous tile" of the first: zero, factor 0
-#pragma unroll
-      for (int r = 0; r < 16; ++r) accf[a][b][r] = 0.0f;
-    }
-  float gprev[kGemmNB];
-#pragma unroll
-  for (int b = 0; b < kGemmNB; ++b) gprev[b] = 0.0f;
-
-  const int wsc = __builtin_amdgcn_readfirstlane(wave);  // wave-uniform, in a scalar register
-  const GemmLoads gl = gemm_loads<2>(A, m0, n0, wsc, lane);
-  // Stage t sits in ring slot t % 3.  Before it is read: this wave's loads
-  // of stage t are done (only stage t + 1's, issued later, may be in
-  // flight), its LDS reads of stage t - 1 have returned, and every wave has
-  // got that far; then slot (t + 2) % 3, last read as stage t - 1, takes
-  // stage t + 2 (the last stage is fetched again near the end, into a slot
-  // no wave reads).  A bare barrier: the loads still in flight are not
-  // waited for.
-  constexpr int NL = 9;  // buffer loads per wave and stage
-  auto begin_stage = [&](int64_t t) -> const int8_t* {
-    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(NL) : "memory");
-    gemm_fetch<2>(gl, min(t + 2, TS - 1), wsc, gsm + ((t + 2) % 3) * SB);
-    return gsm + (t % 3) * SB;
-  };
-  uint2 xs[2], ws[kGemmNB];
-  auto scales = [&](const int8_t* side) {
-#pragma unroll
-    for (int a = 0; a < 2; ++a) xs[a] = mx_scales(side + kGemmSideXs, wm * 64 + a * 32 + (lane & 31), lane);
-#pragma unroll
-    for (int b = 0; b < kGemmNB; ++b)
-      ws[b] = mx_scales(side + kGemmSideWs, wn * (kGemmN / 2) + b * 32 + (lane & 31), lane);
-  };
-  gemm_fetch<2>(gl, 0, wsc, gsm);
-  gemm_fetch<2>(gl, min<int64_t>(1, TS - 1), wsc, gsm + SB);
-  if (A.tile > HQ_TILE) {
-    // factor tiles of tile / 128 units (long RHT tiles, Sec. 7.2): a tile's
-    // units accumulate into acc0 and its rescale follows its last unit, one
-    // rescale per tile / 128 units
-    const int64_t spt = (int64_t)(A.tile / HQ_TILE) / GemmMode<2>::U;  // stages per tile
-    for (int64_t t = 0; t < TS; t += spt) {
-      float gt[kGemmNB];
-      for (int64_t j = 0; j < spt; ++j) {
-        const int8_t* const stage = begin_stage(t + j);
-        const int8_t* const side = stage + kGemmStageA + kGemmStageB;
-        if (j == 0) gemm_side_g(side, 0, wn, lane, gt);
-        scales(side);
-        if (j == 0)
-          gemm_tile_mx4<0, true, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-        else
-          gemm_tile_mx4<0, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-        gemm_tile_mx4<1, false, false>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-      }
-      gemm_rescale<2, 64>(0, acc0, gt, accf);
-    }
-  } else {
-    // two K tiles per stage: tile 0 into acc0 (rescaling acc1), tile 1 into acc1
-    for (int64_t t = 0; t < TS; ++t) {
-      const int8_t* const stage = begin_stage(t);
-      const int8_t* const side = stage + kGemmStageA + kGemmStageB;
-      scales(side);
-      float g0[kGemmNB], g1[kGemmNB];
-      gemm_side_g(side, 0, wn, lane, g0);
-      gemm_side_g(side, 1, wn, lane, g1);
-      gemm_tile_mx4<0>(stage, wm, wn, lane, acc0, acc1, gprev, accf, xs, ws);
-      gemm_tile_mx4<1>(stage, wm, wn, lane, acc1, acc0, g0, accf, xs, ws);
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b) gprev[b] = g1[b];
-    }
-    gemm_rescale<2, 64>(0, acc1, gprev, accf);  // the last tile's partials
-  }
-
-  // MXFP4 blocks carry their own scale: no per-token factor
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t m = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      if (m >= A.M) continue;
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b) {
-        const int64_t n = n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31);
-        if (n >= A.N) continue;
-        const float v = accf[a][b][r];
-        if (A.out_bf16)
-          ((uint16_t*)A.out)[m * A.N + n] = (uint16_t)f32_to_bf16(v);
-        else
-          ((float*)A.out)[m * A.N + n] = v;
-      }
-    }
-}
-
-// The MFMA phase of a stage: its STEPS steps into `cur`, from zero when
-// FRESH (the first stage of a factor tile).
+// The MFMA phase of a stage: its steps into `cur`, from zero when FRESH (the
+// first stage of a factor tile, or of the whole product for MXFP4).
 template <int MODE, bool FRESH>
-__device__ __forceinline__ void gemm_mfma_pp(
-    const v4i_t (&fa)[GemmMode<MODE>::STEPS][2][MODE == 1 ? 2 : 1],
-    const v4i_t (&fb)[GemmMode<MODE>::STEPS][kGemmNB][MODE == 1 ? 2 : 1],
-    typename GemmMode<MODE>::acc_t (&cur)[2][kGemmNB]) {
+__device__ __forceinline__ void gemm_mfma_pp(const v4i_t (&fa)[gemm_pp_steps<MODE>()][2][gemm_pp_fw<MODE>()],
+                                             const v4i_t (&fb)[gemm_pp_steps<MODE>()][kGemmNB][gemm_pp_fw<MODE>()],
+                                             const uint2 (&xs)[2], const uint2 (&ws)[kGemmNB],
+                                             typename GemmMode<MODE>::acc_t (&cur)[2][kGemmNB]) {
   using acc_t = typename GemmMode<MODE>::acc_t;
 #pragma unroll
-  for (int s = 0; s < GemmMode<MODE>::STEPS; ++s)
+  for (int s = 0; s < gemm_pp_steps<MODE>(); ++s)
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -3609,61 +3460,71 @@ __device__ __forceinline__ void gemm_mfma_pp(
         const acc_t c0 = (FRESH && s == 0) ? (acc_t){} : cur[a][b];
         if constexpr (MODE == 0) {
           cur[a][b] = __builtin_amdgcn_mfma_i32_32x32x32_i8(fa[s][a][0], fb[s][b][0], c0, 0, 0, 0);
-        } else {
+        } else if constexpr (MODE == 1) {
           const v8i_t x = {fa[s][a][0][0], fa[s][a][0][1], fa[s][a][0][2], fa[s][a][0][3],
                            fa[s][a][1][0], fa[s][a][1][1], fa[s][a][1][2], fa[s][a][1][3]};
           const v8i_t y = {fb[s][b][0][0], fb[s][b][0][1], fb[s][b][0][2], fb[s][b][0][3],
                            fb[s][b][1][0], fb[s][b][1][1], fb[s][b][1][2], fb[s][b][1][3]};
           // cbsz = blgp = 0: both operands E4M3; scale bytes 127 (2^0)
           cur[a][b] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(x, y, c0, 0, 0, 0, 127, 0, 127);
+        } else {
+          // step s of the stage is K unit s / 2: its scale word, byte 2 (s % 2)
+          const uint32_t xa = s < 2 ? xs[a].x : xs[a].y, wb = s < 2 ? ws[b].x : ws[b].y;
+          cur[a][b] = (s & 1) ? mfma_mxfp4<2>(fa[s][a][0], fb[s][b][0], c0, xa, wb)
+                              : mfma_mxfp4<0>(fa[s][a][0], fb[s][b][0], c0, xa, wb);
         }
       }
 }
 
-// int8 and E4M3, any factor tile: the eight waves in two groups of four
-// (waves 0-3 and 4-7, so each SIMD holds one wave of each) that run half a
-// stage apart.  A wave's stage t has two phases: in V(t) it issues the
-// direct-to-LDS loads of stage t + 2, reads every fragment of stage t into
-// registers and, when stage t starts a factor tile, rescales the previous
-// tile's partial sums into its fp32 accumulators; in M(t) it only issues
-// MFMAs (a long tile's stages accumulate into the same partials).  Group 0 runs V(t) in phase
-// 2t and M(t) in phase 2t + 1, group 1 one phase later, and every phase ends
-// at a workgroup barrier, so on each SIMD one wave's MFMAs run while the
-// other wave's LDS reads and rescale issue.  The barrier waits leave only
-// this wave's newest stage of loads in flight and no LDS read outstanding:
-// a stage is complete in LDS before either group reads it, and its slot is
-// refilled (stage t + 3, issued in phase 2t + 2) only after group 1's reads
-// of phase 2t + 1 have returned.  Every wave executes the same 2 TS + 1
-// barriers: group 1 one before its first V phase, group 0 one after its
-// last M phase.
+// The block-scaled GEMM, all three operand types: the eight waves in two
+// groups of four (waves 0-3 and 4-7, so each SIMD holds one wave of each)
+// that run half a stage apart.  A wave's stage t has two phases: in V(t) it
+// issues the direct-to-LDS loads of stage t + 2, reads every fragment (and
+// for MXFP4 the block scale words) of stage t into registers and, for int8
+// and E4M3 when stage t starts a factor tile, rescales the previous tile's
+// partial sums into its fp32 accumulators; in M(t) it only issues MFMAs (a
+// long tile's stages accumulate into the same partials; MXFP4's scales
+// carry every factor, so its MFMAs accumulate the whole product).  Group 0
+// runs V(t) in phase 2t and M(t) in phase 2t + 1, group 1 one phase later,
+// and every phase ends at a workgroup barrier, so on each SIMD one wave's
+// MFMAs run while the other wave's LDS reads and rescale issue.  The barrier
+// waits leave only this wave's newest stage of loads in flight and no LDS
+// read outstanding: a stage is complete in LDS before either group reads
+// it, and its slot is refilled (stage t + 3, issued in phase 2t + 2) only
+// after group 1's reads of phase 2t + 1 have returned.  Every wave executes
+// the same 2 TS + 1 barriers: group 1 one before its first V phase, group 0
+// one after its last M phase.
 template <int MODE>
 __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
-  static_assert(MODE == 0 || MODE == 1, "int8 or E4M3");
   using acc_t = typename GemmMode<MODE>::acc_t;
+  constexpr bool RESCALE = MODE != 2;
   constexpr int SB = gemm_stage_bytes<MODE>();
-  constexpr int STEPS = GemmMode<MODE>::STEPS;
-  constexpr int FW = MODE == 1 ? 2 : 1;  // 16-byte chunks per fragment
+  constexpr int NS = gemm_pp_steps<MODE>();
+  constexpr int FW = gemm_pp_fw<MODE>();
   extern __shared__ __attribute__((aligned(16))) int8_t gsm[];
   const int tid = threadIdx.x, lane = tid & 63, h = lane >> 5;
   const int wsc = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform, in a scalar register
   const int wm = wsc >> 1, wn = wsc & 1, grp = wsc >> 2;
   const int64_t m0 = (int64_t)blockIdx.y * kGemmM, n0 = (int64_t)blockIdx.x * kGemmN;
-  const int64_t TS = A.K / HQ_TILE;
+  const int64_t TS = A.K / HQ_TILE / GemmMode<MODE>::U;  // LDS stages
   const uint32_t tmask = (uint32_t)(A.tile / HQ_TILE) - 1u;  // stages per factor tile, less one
 
   float accf[2][kGemmNB][16];
+  if constexpr (RESCALE) {
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+    for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < kGemmNB; ++b)
+      for (int b = 0; b < kGemmNB; ++b)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) accf[a][b][r] = 0.0f;
+        for (int r = 0; r < 16; ++r) accf[a][b][r] = 0.0f;
+  }
   acc_t cur[2][kGemmNB];
   float gcur[kGemmNB];
-  v4i_t fa[STEPS][2][FW], fb[STEPS][kGemmNB][FW];
+  uint2 xs[2], ws[kGemmNB];
+  v4i_t fa[NS][2][FW], fb[NS][kGemmNB][FW];
 
   const GemmLoads gl = gemm_loads<MODE>(A, m0, n0, wsc, lane);
-  constexpr int NL = 7;  // buffer loads per wave and stage
+  constexpr int NL = MODE == 2 ? 8 : 7;  // buffer loads per wave and stage
   gemm_fetch<MODE>(gl, 0, wsc, gsm);
   gemm_fetch<MODE>(gl, min<int64_t>(1, TS - 1), wsc, gsm + SB);
   // a phase boundary: the waits, the barrier, and no instruction scheduled
@@ -3678,10 +3539,13 @@ __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
     phase();
     // V(t)
     const int8_t* const stage = gsm + (t % 3) * SB;
+    const int8_t* const side = stage + kGemmStageA + kGemmStageB;
     gemm_fetch<MODE>(gl, min(t + 2, TS - 1), wsc, gsm + ((t + 2) % 3) * SB);
 #pragma unroll
-    for (int s = 0; s < STEPS; ++s) {
-      // int8: 32-deep step, chunk 2 s + h; E4M3: 64-deep step, chunks 4 s + 2 h and the next
+    for (int s = 0; s < NS; ++s) {
+      // int8: 32-deep step, chunk 2 s + h; E4M3: 64-deep step, chunks 4 s + 2 h
+      // and the next; MXFP4: 64-deep step s of the stage, chunk 2 s + h (32
+      // E2M1 values, one MX block)
 #pragma unroll
       for (int f = 0; f < FW; ++f) {
         const int c = MODE == 1 ? 4 * s + 2 * h + f : 2 * s + h;
@@ -3692,23 +3556,32 @@ __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
           fb[s][b][f] = gemm_frag(stage + kGemmStageA, wn * (kGemmN / 2) + b * 32 + (lane & 31), c);
       }
     }
+    if constexpr (MODE == 2) {
+#pragma unroll
+      for (int a = 0; a < 2; ++a) xs[a] = mx_scales(side + kGemmSideXs, wm * 64 + a * 32 + (lane & 31), lane);
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b)
+        ws[b] = mx_scales(side + kGemmSideWs, wn * (kGemmN / 2) + b * 32 + (lane & 31), lane);
+    }
     __builtin_amdgcn_sched_barrier(0);  // the reads issue first; the rescale runs under them
-    // a factor tile of spt stages: its partials accumulate over its stages,
-    // and are rescaled once, in the V phase that starts the next tile
-    const bool first = ((uint32_t)t & tmask) == 0u;  // wave-uniform
-    if (first) {
-      if (t > 0) gemm_rescale<MODE, 64>(0, cur, gcur, accf);
-      gemm_side_g(stage + kGemmStageA + kGemmStageB, 0, wn, lane, gcur);
+    // int8 / E4M3: a factor tile of tmask + 1 stages accumulates into the
+    // partials, rescaled once, in the V phase that starts the next tile
+    const bool first = RESCALE ? ((uint32_t)t & tmask) == 0u : t == 0;  // wave-uniform
+    if constexpr (RESCALE) {
+      if (first) {
+        if (t > 0) gemm_rescale<MODE, 64>(0, cur, gcur, accf);
+        gemm_side_g(side, 0, wn, lane, gcur);
+      }
     }
     phase();
     // M(t)
     if (first)
-      gemm_mfma_pp<MODE, true>(fa, fb, cur);
+      gemm_mfma_pp<MODE, true>(fa, fb, xs, ws, cur);
     else
-      gemm_mfma_pp<MODE, false>(fa, fb, cur);
+      gemm_mfma_pp<MODE, false>(fa, fb, xs, ws, cur);
   }
   if (grp == 0) phase();  // the same barrier count in both groups
-  gemm_rescale<MODE, 64>(0, cur, gcur, accf);  // the last tile
+  if constexpr (RESCALE) gemm_rescale<MODE, 64>(0, cur, gcur, accf);  // the last tile
   // the re-fetches of the last stage land before the workgroup's LDS is freed
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
@@ -3718,12 +3591,16 @@ __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
     for (int r = 0; r < 16; ++r) {
       const int64_t m = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (m >= A.M) continue;
-      const float sxm = A.sx[m];
+      const float sxm = RESCALE ? A.sx[m] : 1.0f;  // MXFP4 blocks carry their own scale
 #pragma unroll
       for (int b = 0; b < kGemmNB; ++b) {
         const int64_t n = n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31);
         if (n >= A.N) continue;
-        const float v = sxm * accf[a][b][r];
+        float v;
+        if constexpr (RESCALE)
+          v = sxm * accf[a][b][r];
+        else
+          v = cur[a][b][r];
         if (A.out_bf16)
           ((uint16_t*)A.out)[m * A.N + n] = (uint16_t)f32_to_bf16(v);
         else
@@ -3741,7 +3618,7 @@ __global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_f8_kernel(hq_gemm_arg
 }
 
 __global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_mx4_kernel(hq_gemm_args A) {
-  gemm_body_mx4(A);
+  gemm_body_pp<2>(A);
 }
 
 // ------------------------------------------------------------ utilities

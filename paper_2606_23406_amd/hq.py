@@ -104,11 +104,11 @@ def lib():
     L.hq_gemm_fp8_blockscaled.restype = i32
     L.hq_gemm_fp8_blockscaled.argtypes = [p, p, p, i64, p, p, i64, p, i32, p]
     L.hq_decode_mxfp4.restype = i32
-    L.hq_decode_mxfp4.argtypes = [p, p, i64, i64, p, p, p, p]
+    L.hq_decode_mxfp4.argtypes = [p, p, i64, i64, p, p, p]
     L.hq_act_prep_mxfp4.restype = i32
     L.hq_act_prep_mxfp4.argtypes = [p, p, i64, i64, p, p, p]
     L.hq_gemm_mxfp4_blockscaled.restype = i32
-    L.hq_gemm_mxfp4_blockscaled.argtypes = [p, p, p, i64, p, p, p, i64, p, i32, p]
+    L.hq_gemm_mxfp4_blockscaled.argtypes = [p, p, p, i64, p, p, i64, p, i32, p]
     L.hq_gemm_workspace_bytes.restype = C.c_size_t
     L.hq_gemm_workspace_bytes.argtypes = [p, i64, i64]
     L.hq_dequant_gemm_int8.restype = i32
@@ -317,17 +317,15 @@ def hq_decode_int8(plan: Plan, s: EncodedStream, row0=0, rows=None, stream=None)
 
 
 def hq_decode_mxfp4(plan: Plan, s: EncodedStream, row0=0, rows=None, stream=None):
-    """hq_decode_mxfp4: E2M1 code pairs (uint8, cols / 2 per row), E8M0 scale
-    bytes (cols / 32 per row) and the per-tile factors."""
+    """hq_decode_mxfp4: E2M1 code pairs (uint8, cols / 2 per row) and E8M0
+    scale bytes (cols / 32 per row) of the reconstruction."""
     rows = s.rows - row0 if rows is None else rows
     codes = torch.empty((rows, plan.cols // 2), dtype=torch.uint8, device=s.device)
     scales = torch.empty((rows, plan.cols // 32), dtype=torch.uint8, device=s.device)
-    g = torch.empty((rows, plan.info.tiles_per_row), dtype=torch.float32, device=s.device)
     st = lib().hq_decode_mxfp4(plan.handle, C.byref(s.c), row0, rows, C.c_void_p(codes.data_ptr()),
-                               C.c_void_p(scales.data_ptr()), C.c_void_p(g.data_ptr()),
-                               _stream_handle(stream))
+                               C.c_void_p(scales.data_ptr()), _stream_handle(stream))
     _check("hq_decode_mxfp4", st)
-    return codes, scales, g
+    return codes, scales
 
 
 def hq_act_prep_mxfp4(plan: Plan, a: torch.Tensor, stream=None):
@@ -343,16 +341,15 @@ def hq_act_prep_mxfp4(plan: Plan, a: torch.Tensor, stream=None):
     return xq, xs
 
 
-def hq_gemm_mxfp4_blockscaled(plan: Plan, xq, xs, codes, ws, g, out_dtype=torch.bfloat16,
-                              out=None, stream=None):
+def hq_gemm_mxfp4_blockscaled(plan: Plan, xq, xs, codes, ws, out_dtype=torch.bfloat16, out=None,
+                              stream=None):
     M, N = xq.shape[0], codes.shape[0]
     if out is None:
         out = torch.empty((M, N), dtype=out_dtype, device=xq.device)
     st = lib().hq_gemm_mxfp4_blockscaled(plan.handle, C.c_void_p(xq.data_ptr()),
                                          C.c_void_p(xs.data_ptr()), M, C.c_void_p(codes.data_ptr()),
-                                         C.c_void_p(ws.data_ptr()), C.c_void_p(g.data_ptr()), N,
-                                         C.c_void_p(out.data_ptr()), _dtype_code(out.dtype),
-                                         _stream_handle(stream))
+                                         C.c_void_p(ws.data_ptr()), N, C.c_void_p(out.data_ptr()),
+                                         _dtype_code(out.dtype), _stream_handle(stream))
     _check("hq_gemm_mxfp4_blockscaled", st)
     return out
 

@@ -1,10 +1,10 @@
-"""GPU parity of the MXFP4 cast path (Sec. 4.8 Cast, Sec. 6.4: the lattice
-output fed to MXFP4, OCP Microscaling blocks of 32 with E8M0 scales and E2M1
-elements) against the oracle: the decoded code nibbles, block scale bytes and
-tile factors bit for bit, the activation prep's nibbles and scales bit for
-bit, and the block-scaled GEMM on the gfx950 scaled matrix cores within 1e-4
-of max(|ref|, rms(ref)): the products of two E2M1 values times a power of two
-are exact in fp32, and only the fp32 sums across blocks and tiles round."""
+"""GPU parity of the MXFP4 cast path (Sec. 4.8 Cast, Sec. 6.4: the
+reconstruction fed to MXFP4, OCP Microscaling blocks of 32 with E8M0 scales
+and E2M1 elements) against the oracle: the decoded code nibbles and block
+scale bytes of g c bit for bit, the activation prep's nibbles and scales bit
+for bit, and the block-scaled GEMM on the gfx950 scaled matrix cores within
+1e-4 of max(|ref|, rms(ref)): the products of two E2M1 values times a power
+of two are exact in fp32, and only the fp32 sums across blocks round."""
 import numpy as np
 import pytest
 import torch
@@ -33,7 +33,7 @@ def pack_nibbles(codes):
 
 
 @pytest.mark.parametrize("lat", [O.E8, O.D4, O.Z])
-def test_decode_mxfp4_codes_scales_and_factors(hq, lat):
+def test_decode_mxfp4_codes_and_scales(hq, lat):
     snr = PT.op_snr("E8", 4.0) if lat == O.E8 else 30.0
     P = PT.oracle_params(lat, snr, rht_seed=29)
     x = gauss(40, 1024, 35, 0.02, torch.bfloat16)
@@ -41,20 +41,18 @@ def test_decode_mxfp4_codes_scales_and_factors(hq, lat):
     x[3, :] = 0.0     # an all-zero row: every block takes X = -127
     print(f"[parity] decode_mxfp4 {LAT_NAMES[lat]}", flush=True)
     plan, s = encode_gpu(hq, P, snr, x)
-    codes, scales, g = hq.hq_decode_mxfp4(plan, s)
+    codes, scales = hq.hq_decode_mxfp4(plan, s)
     torch.cuda.synchronize()
     oc, norms, _, _ = O.frontend(P, x.float().numpy())
-    o4, os_ = O.weight_codes_mxfp4(oc)
+    o4, os_ = O.weight_codes_mxfp4(oc, O.weight_factors(P, norms, 40, 1024), 128)
     assert np.array_equal(scales.cpu().numpy(), os_)
     assert np.array_equal(codes.cpu().numpy(), pack_nibbles(o4))
-    assert np.array_equal(g.cpu().numpy(), O.weight_factors(P, norms, 40, 1024))
     assert (os_[3] == 0).all()
     # a row range decodes the same bytes as the whole matrix's rows
-    c2, s2, g2 = hq.hq_decode_mxfp4(plan, s, row0=9, rows=13)
+    c2, s2 = hq.hq_decode_mxfp4(plan, s, row0=9, rows=13)
     torch.cuda.synchronize()
     assert torch.equal(c2.cpu(), codes[9:22].cpu())
     assert torch.equal(s2.cpu(), scales[9:22].cpu())
-    assert torch.equal(g2.cpu(), g[9:22].cpu())
 
 
 def test_act_prep_mxfp4(hq):
@@ -82,19 +80,20 @@ def test_gemm_mxfp4_blockscaled(hq, M, N, K):
     a = workloads.activations(tokens=M, features=K)
     print(f"[parity] gemm mxfp4 M={M} N={N} K={K}", flush=True)
     plan, s = encode_gpu(hq, P, snr, w)
-    codes, ws, g = hq.hq_decode_mxfp4(plan, s)
+    codes, ws = hq.hq_decode_mxfp4(plan, s)
     xq, xs = hq.hq_act_prep_mxfp4(plan, a.cuda())
-    out32 = hq.hq_gemm_mxfp4_blockscaled(plan, xq, xs, codes, ws, g, out_dtype=torch.float32)
-    out16 = hq.hq_gemm_mxfp4_blockscaled(plan, xq, xs, codes, ws, g, out_dtype=torch.bfloat16)
+    out32 = hq.hq_gemm_mxfp4_blockscaled(plan, xq, xs, codes, ws, out_dtype=torch.float32)
+    out16 = hq.hq_gemm_mxfp4_blockscaled(plan, xq, xs, codes, ws, out_dtype=torch.bfloat16)
     torch.cuda.synchronize()
     oc, norms, _, _ = O.frontend(P, w.float().numpy())
     og = O.weight_factors(P, norms, N, K)
-    o4, ows = O.weight_codes_mxfp4(oc)
+    o4, ows = O.weight_codes_mxfp4(oc, og, 128)
     ox4, oxs = O.act_prep_mxfp4(a.float().numpy(), 128, 59)
     # the GPU's operands are the oracle's, byte for byte, before the product
     assert np.array_equal(codes.cpu().numpy(), pack_nibbles(o4))
+    assert np.array_equal(ws.cpu().numpy(), ows)
     assert np.array_equal(xq.cpu().numpy(), pack_nibbles(ox4))
-    ref = O.gemm_mxfp4_blockscaled(o4, ows, og, ox4, oxs, 128)
+    ref = O.gemm_mxfp4(o4, ows, ox4, oxs)
     got = out32.cpu().numpy().astype(np.float64)
     denom = np.maximum(np.abs(ref), np.sqrt((ref ** 2).mean()))
     err = float(np.max(np.abs(got - ref) / denom))

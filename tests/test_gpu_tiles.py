@@ -184,16 +184,15 @@ def test_long_tile_casts_and_gemm(hq, tile):
     print(f"[tiles] tile={tile} fp8 GEMM: worst error {rel8:.2e}", flush=True)
     assert rel8 <= 1e-4
     # MXFP4
-    c4, ws4, g4 = hq.hq_decode_mxfp4(plan, s)
+    c4, ws4 = hq.hq_decode_mxfp4(plan, s)
     x4, xs4 = hq.hq_act_prep_mxfp4(plan, a.cuda())
-    out4 = hq.hq_gemm_mxfp4_blockscaled(plan, x4, xs4, c4, ws4, g4, out_dtype=torch.float32)
+    out4 = hq.hq_gemm_mxfp4_blockscaled(plan, x4, xs4, c4, ws4, out_dtype=torch.float32)
     torch.cuda.synchronize()
-    ow4, ows4 = O.weight_codes_mxfp4(codes)
+    ow4, ows4 = O.weight_codes_mxfp4(codes, og, tile)
     ox4, oxs4 = O.act_prep_mxfp4(an, tile, P.rht_seed)
     assert np.array_equal(c4.cpu().numpy(), nibbles(ow4)) and np.array_equal(ws4.cpu().numpy(), ows4)
     assert np.array_equal(x4.cpu().numpy(), nibbles(ox4)) and np.array_equal(xs4.cpu().numpy(), oxs4)
-    assert np.array_equal(g4.cpu().numpy(), og)
-    ref4 = O.gemm_mxfp4_blockscaled(ow4, ows4, og, ox4, oxs4, tile)
+    ref4 = O.gemm_mxfp4(ow4, ows4, ox4, oxs4)
     got4 = out4.cpu().numpy().astype(np.float64)
     rel4 = np.max(np.abs(got4 - ref4) / np.maximum(np.abs(ref4), np.sqrt((ref4 ** 2).mean())))
     print(f"[tiles] tile={tile} MXFP4 GEMM: worst error {rel4:.2e}", flush=True)

@@ -3,8 +3,10 @@ lattice output fed to MXFP4, 32-element blocks with power-of-two scales),
 CPU only.  The cast is pinned to the OCP Microscaling format it names: the
 E2M1 element values and codes, ties to the even code, saturation at 6, the
 E8M0 scale rule X = floor(log2 amax) - 2 at block boundaries, brute-force
-nearest values, the activation side's transform, and the GEMM against a
-dense product of the cast values."""
+nearest values, the activation side's transform, the weight side's cast of
+the reconstruction (the tile factor inside the cast: a worked example, a
+power-of-two property, the MX error bound) and the GEMM against a
+brute-force sum of the cast values."""
 import numpy as np
 import pytest
 
@@ -72,12 +74,56 @@ def test_act_prep_mxfp4_transform():
     assert np.all(np.abs(rec - y).reshape(5, 16, 32) <= (amax / 4)[:, :, None] + 1e-5)
 
 
-def test_gemm_mxfp4_matches_dense_product():
+def test_weight_cast_carries_the_tile_factor():
+    # worked example: codes 8 and 3 in one block, tile factor 0.75 -> the
+    # reconstruction 6.0 and 2.25; amax 6 -> X = 0; 6.0 is code 7 and 2.25
+    # rounds to 2 (code 4).  Casting the bare codes instead would give X = 1
+    # and 8 -> 4.0, 3 -> 1.5, i.e. 6.0 and 2.25 after the factor: the two
+    # readings differ exactly there.
+    c = np.zeros((1, 128), dtype=np.int32)
+    c[0, 0], c[0, 1] = 8, 3
+    codes, scales = O.weight_codes_mxfp4(c, np.array([[0.75]], np.float32), 128)
+    assert int(scales[0, 0]) == 127
+    assert list(codes[0, :2]) == [7, 4]
+    assert list(O.mxfp4_value(codes, scales)[0, :2]) == [6.0, 2.0]
+    assert (codes[0, 2:] == 0).all() and (scales[0, 1:] == 0).all()  # all-zero blocks: X = -127
+
+
+def test_power_of_two_factor_only_moves_the_scales():
+    # g = 2^-3 is exact in every product: the element codes are the bare
+    # codes' and each block scale is 3 binades lower
+    rng = np.random.default_rng(9)
+    c = rng.integers(-60, 61, (6, 256))
+    g = np.full((6, 2), 0.125, np.float32)
+    k1, s1 = O.weight_codes_mxfp4(c, g, 128)
+    k0, s0 = O.mxfp4_cast(c.astype(np.float64))
+    assert np.array_equal(k1, k0)
+    nz = s0 > 0
+    assert np.array_equal(s1.astype(np.int32)[nz], s0.astype(np.int32)[nz] - 3)
+
+
+def test_weight_cast_within_the_mx_bound_of_the_reconstruction():
+    rng = np.random.default_rng(10)
+    c = rng.integers(-90, 91, (8, 512))
+    g = (rng.random((8, 4)) * 0.03 + 1e-3).astype(np.float32)
+    codes, scales = O.weight_codes_mxfp4(c, g, 128)
+    v = c * np.repeat(g.astype(np.float64), 128, axis=1)
+    rec = O.mxfp4_value(codes, scales)
+    step = np.ldexp(1.0, scales.astype(np.int32) - 127)
+    # half the largest spacing of E2M1 (2 at the top binade) plus the saturation of [6, 8)
+    assert np.all(np.abs(rec - v).reshape(8, 16, 32) <= (2.0 * step)[:, :, None] + 1e-9)
+
+
+def test_gemm_mxfp4_matches_brute_force():
     rng = np.random.default_rng(7)
-    w4, ws = O.weight_codes_mxfp4(rng.integers(-40, 41, (24, 256)))
-    x4, xs = O.mxfp4_cast(rng.standard_normal((5, 256)) * 50)
-    g = rng.random((24, 2)).astype(np.float32)
-    out = O.gemm_mxfp4_blockscaled(w4, ws, g, x4, xs, 128)
-    W = O.mxfp4_value(w4, ws) * np.repeat(g.astype(np.float64), 128, axis=1)
-    ref = O.mxfp4_value(x4, xs) @ W.T
+    w4, ws = O.weight_codes_mxfp4(rng.integers(-40, 41, (6, 256)),
+                                  rng.random((6, 2)).astype(np.float32), 128)
+    x4, xs = O.mxfp4_cast(rng.standard_normal((3, 256)) * 50)
+    out = O.gemm_mxfp4(w4, ws, x4, xs)
+    ref = np.zeros((3, 6))
+    for m in range(3):
+        for n in range(6):
+            for k in range(256):
+                ref[m, n] += (float(O.e2m1_value(x4[m, k])) * 2.0 ** (int(xs[m, k // 32]) - 127) *
+                              float(O.e2m1_value(w4[n, k])) * 2.0 ** (int(ws[n, k // 32]) - 127))
     np.testing.assert_allclose(out, ref, rtol=1e-12, atol=1e-9)
