@@ -3287,9 +3287,9 @@ constexpr int kGemmM = 256, kGemmN = 128;  // the loads below assume 256 x 128 a
 constexpr int kGemmThreads = 512;           // 8 waves, 4 (m) x 2 (n)
 constexpr int kGemmNB = kGemmN / 64;        // 32 x 32 blocks per wave along n
 constexpr int kGemmStageA = kGemmM * 128, kGemmStageB = kGemmN * 128;
-// side data of a stage: the weight rows' factors (K tile h of the stage at
-// float h * 128 + column), then for MXFP4 the 8 scale bytes of each A row
-// and of each B row
+// side data of a stage: for int8 and E4M3 the weight rows' factors of the
+// stage's factor tile (float n for weight row n0 + n); for MXFP4 the 8 scale
+// bytes of each A row and of each B row
 constexpr int kGemmSideG = 0, kGemmSideXs = 1024, kGemmSideWs = 3072;
 constexpr int kGemmStages = 3;  // LDS ring: stage t + 2 loads while stage t is multiplied
 template <int MODE> constexpr int gemm_stage_bytes() {
@@ -3310,8 +3310,8 @@ template <int MODE> struct GemmMode {
 // offset within them is fixed for the whole K loop and the stage's offset is
 // a scalar.  4 A and 2 B row groups per wave (16 bytes a lane, lane l at row
 // 8q + l / 8 and K chunk (l % 8) ^ ((4q + l / 16) % 8)), then the side data
-// (4 bytes a lane): factor dword j * 64 + l = g[n0 + (j % 2) 64 + l, U t +
-// j / 2] with j = w % 2U, and for MXFP4 scale dword d = w * 64 + l of the A
+// (4 bytes a lane): for int8 and E4M3 factor dword j * 64 + l = g[n0 + 64 j +
+// l, t >> lm] with j = w % 2, for MXFP4 scale dword d = w * 64 + l of the A
 // rows and d = (w % 4) * 64 + l of the B rows (row d / 2, half d % 2).  Waves
 // with equal j (or w % 4) load the same values to the same place, so every
 // wave issues the same loads and the loop has no branch.  Rows past M or N
@@ -3358,11 +3358,8 @@ __device__ __forceinline__ GemmLoads gemm_loads(const hq_gemm_args& A, int64_t m
     const int q = wave * 2 + i;
     L.b[i] = (uint32_t)(min<int64_t>(8 * q + rr, nb - 1) * rb) + kc(q);
   }
-  const int j = wave % (2 * GemmMode<MODE>::U);
   L.lm = __builtin_ctz((uint32_t)(A.tile / HQ_TILE));
-  // a stage holds U units of one factor tile, or (128-tiles) U tiles: unit
-  // j / 2 of the stage reads its own factor only when tiles are 128 deep
-  L.g = (uint32_t)((min<int64_t>((j & 1) * 64 + lane, nb - 1) * T + (L.lm == 0 ? (j >> 1) : 0)) * 4);
+  L.g = (uint32_t)(min<int64_t>((wave & 1) * 64 + lane, nb - 1) * T * 4);
   const int d = wave * 64 + lane, e = (wave & 3) * 64 + lane;
   L.xs = (uint32_t)(min<int64_t>(d >> 1, ma - 1) * ks + (d & 1) * 4);
   L.ws = (uint32_t)(min<int64_t>(e >> 1, nb - 1) * ks + (e & 1) * 4);
@@ -3372,7 +3369,6 @@ __device__ __forceinline__ GemmLoads gemm_loads(const hq_gemm_args& A, int64_t m
 // Direct-to-LDS loads of stage t into `stage` (wave is wave-uniform).
 template <int MODE>
 __device__ __forceinline__ void gemm_fetch(const GemmLoads& L, int64_t t, int wave, int8_t* stage) {
-  constexpr int U = GemmMode<MODE>::U;
   const uint32_t so = (uint32_t)(t * 128);
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -3383,10 +3379,11 @@ __device__ __forceinline__ void gemm_fetch(const GemmLoads& L, int64_t t, int wa
     __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rb, (lds_void_t*)(stage + kGemmStageA + (wave * 2 + i) * 1024),
                                              16, L.b[i], so, 0, 0);
   int8_t* const side = stage + kGemmStageA + kGemmStageB;
-  if constexpr (MODE != 2)  // MXFP4 blocks carry the tile factors in their scales
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rg, (lds_void_t*)(side + kGemmSideG + (wave % (2 * U)) * 256),
-                                             4, L.g, (uint32_t)(((U * t) >> L.lm) * 4), 0, 0);
-  if constexpr (MODE == 2) {
+  if constexpr (MODE != 2) {
+    // the stage's factor tile; MXFP4 blocks carry the factors in their scales
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rg, (lds_void_t*)(side + kGemmSideG + (wave & 1) * 256), 4,
+                                             L.g, (uint32_t)((t >> L.lm) * 4), 0, 0);
+  } else {
     __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rxs, (lds_void_t*)(side + kGemmSideXs + wave * 256), 4,
                                              L.xs, (uint32_t)(t * 8), 0, 0);
     __builtin_amdgcn_raw_ptr_buffer_load_lds(L.rws, (lds_void_t*)(side + kGemmSideWs + (wave & 3) * 256),
@@ -3418,12 +3415,11 @@ __device__ __forceinline__ v16f_t mfma_mxfp4(v4i_t a, v4i_t b, v16f_t c, uint32_
                                                          (int)sb);
 }
 
-// A lane's factors for its kGemmNB weight columns, K tile h of the stage.
-__device__ __forceinline__ void gemm_side_g(const int8_t* side, int h, int wn, int lane,
-                                            float (&gv)[kGemmNB]) {
+// A lane's factors for its kGemmNB weight columns (int8 and E4M3).
+__device__ __forceinline__ void gemm_side_g(const int8_t* side, int wn, int lane, float (&gv)[kGemmNB]) {
 #pragma unroll
   for (int b = 0; b < kGemmNB; ++b)
-    gv[b] = ((const float*)(side + kGemmSideG))[h * 128 + wn * (kGemmN / 2) + b * 32 + (lane & 31)];
+    gv[b] = ((const float*)(side + kGemmSideG))[wn * (kGemmN / 2) + b * 32 + (lane & 31)];
 }
 
 // Rescale elements [e0, e0 + E) of a finished tile's partials (block
@@ -3570,7 +3566,7 @@ __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
     if constexpr (RESCALE) {
       if (first) {
         if (t > 0) gemm_rescale<MODE, 64>(0, cur, gcur, accf);
-        gemm_side_g(side, 0, wn, lane, gcur);
+        gemm_side_g(side, wn, lane, gcur);
       }
     }
     phase();
