@@ -3472,6 +3472,75 @@ __device__ __forceinline__ void gemm_mfma_pp(const v4i_t (&fa)[gemm_pp_steps<MOD
       }
 }
 
+// Output staging: a wave's 64 x 64 tile in LDS with rows of 64 values plus
+// 16 bytes of padding (rows 4 apart, written by the two lane halves, then
+// fall in different banks), 8 regions filling less than the stage ring.
+template <bool BF16> constexpr int gemm_out_row() { return BF16 ? 144 : 272; }
+constexpr int kGemmOutRegion = 64 * 272;
+static_assert(8 * kGemmOutRegion <= gemm_lds_bytes<0>(), "the output tiles fit the ring");
+
+// out rows r0 .. r0 + 63, columns c0 .. c0 + 63 of the wave's tile: each
+// value (s_x times the accumulator for int8 / E4M3; MXFP4's accumulator as
+// is) into LDS at its MFMA position, then 16-byte row pieces to global
+// memory (element stores at a ragged right edge).
+template <int MODE, bool BF16>
+__device__ __forceinline__ void gemm_store_tile(const hq_gemm_args& A, int8_t* tile,
+                                                const typename GemmMode<MODE>::acc_t (&cur)[2][kGemmNB],
+                                                const float (&accf)[2][kGemmNB][16], int64_t r0,
+                                                int64_t c0, int lane) {
+  constexpr bool RESCALE = MODE != 2;
+  constexpr int RS = gemm_out_row<BF16>();
+  constexpr int ES = BF16 ? 2 : 4;  // bytes per value
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const int64_t m = r0 + row;
+      const float sxm = RESCALE && m < A.M ? A.sx[m] : 1.0f;
+#pragma unroll
+      for (int b = 0; b < kGemmNB; ++b) {
+        float v;
+        if constexpr (RESCALE)
+          v = sxm * accf[a][b][r];
+        else
+          v = cur[a][b][r];
+        int8_t* const p = tile + row * RS + (b * 32 + (lane & 31)) * ES;
+        if constexpr (BF16)
+          *(uint16_t*)p = (uint16_t)f32_to_bf16(v);
+        else
+          *(float*)p = v;
+      }
+    }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  constexpr int VPL = 16 / ES;            // values per 16-byte piece
+  constexpr int LPR = 64 / VPL;           // lanes per row
+  constexpr int ROWS = 64 / LPR;          // rows per pass
+#pragma unroll
+  for (int i = 0; i < 64 / ROWS; ++i) {
+    const int row = i * ROWS + lane / LPR, col = (lane % LPR) * VPL;
+    const int64_t m = r0 + row, n = c0 + col;
+    if (m >= A.M || n >= A.N) continue;
+    const uint4 v = *(const uint4*)(tile + row * RS + col * ES);
+    char* const dst = (char*)A.out + (m * A.N + n) * ES;
+    if (n + VPL <= A.N && ((m * A.N + n) * ES) % 16 == 0) {
+      *(uint4*)dst = v;
+    } else {
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < VPL; ++e)
+        if (n + e < A.N) {
+          if constexpr (BF16)
+            ((uint16_t*)dst)[e] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
+          else
+            ((uint32_t*)dst)[e] = w[e];
+        }
+    }
+  }
+}
+
 // The block-scaled GEMM, all three operand types: the eight waves in two
 // groups of four (waves 0-3 and 4-7, so each SIMD holds one wave of each)
 // that run half a stage apart.  A wave's stage t has two phases: in V(t) it
@@ -3578,31 +3647,17 @@ __device__ __forceinline__ void gemm_body_pp(const hq_gemm_args& A) {
   }
   if (grp == 0) phase();  // the same barrier count in both groups
   if constexpr (RESCALE) gemm_rescale<MODE, 64>(0, cur, gcur, accf);  // the last tile
-  // the re-fetches of the last stage land before the workgroup's LDS is freed
+  // every wave's re-fetches of the last stage have landed: the ring is free
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
 
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int64_t m = m0 + wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      if (m >= A.M) continue;
-      const float sxm = RESCALE ? A.sx[m] : 1.0f;  // MXFP4 blocks carry their own scale
-#pragma unroll
-      for (int b = 0; b < kGemmNB; ++b) {
-        const int64_t n = n0 + wn * (kGemmN / 2) + b * 32 + (lane & 31);
-        if (n >= A.N) continue;
-        float v;
-        if constexpr (RESCALE)
-          v = sxm * accf[a][b][r];
-        else
-          v = cur[a][b][r];
-        if (A.out_bf16)
-          ((uint16_t*)A.out)[m * A.N + n] = (uint16_t)f32_to_bf16(v);
-        else
-          ((float*)A.out)[m * A.N + n] = v;
-      }
-    }
+  // The wave's 64 x 64 outputs, staged in LDS (its own region of the ring)
+  // in the MFMA layout, then written out 16 bytes a lane along whole rows.
+  int8_t* const tile = gsm + wsc * kGemmOutRegion;
+  if (A.out_bf16)
+    gemm_store_tile<MODE, true>(A, tile, cur, accf, m0 + wm * 64, n0 + wn * 64, lane);
+  else
+    gemm_store_tile<MODE, false>(A, tile, cur, accf, m0 + wm * 64, n0 + wn * 64, lane);
 }
 
 __global__ __launch_bounds__(kGemmThreads, 1) void hq_gemm_i8_kernel(hq_gemm_args A) {
