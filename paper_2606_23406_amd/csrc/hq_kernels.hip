@@ -3542,8 +3542,9 @@ __device__ __forceinline__ void gemm_store_tile(const hq_gemm_args& A, int8_t* t
 }
 
 // The block-scaled GEMM, all three operand types: the eight waves in two
-// groups of four (waves 0-3 and 4-7, so each SIMD holds one wave of each)
-// that run half a stage apart.  A wave's stage t has two phases: in V(t) it
+// groups of four (waves 0-3 and 4-7: with a workgroup's waves placed on the
+// four SIMDs in turn, each SIMD holds one wave of each group; the results
+// do not depend on the placement) that run half a stage apart.  A wave's stage t has two phases: in V(t) it
 // issues the direct-to-LDS loads of stage t + 2, reads every fragment (and
 // for MXFP4 the block scale words) of stage t into registers and, for int8
 // and E4M3 when stage t starts a factor tile, rescales the previous tile's
