@@ -71,7 +71,7 @@ def test_act_prep_mxfp4(hq):
 
 
 @pytest.mark.parametrize("M,N,K", [(128, 256, 1024), (200, 384, 1024), (64, 96, 512),
-                                   (300, 160, 2560)])
+                                   (300, 160, 2560), (70, 100, 512)])
 def test_gemm_mxfp4_blockscaled(hq, M, N, K):
     from paper_2606_23406_amd import workloads
     snr = PT.op_snr("E8", 4.0)

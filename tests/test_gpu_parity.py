@@ -219,9 +219,10 @@ def test_act_prep(hq):
 
 
 @pytest.mark.parametrize("M,N,K", [(128, 256, 1024), (200, 384, 1024), (64, 96, 1024),
-                                   (300, 200, 512), (40, 136, 2560)])
+                                   (300, 200, 512), (40, 136, 2560), (70, 100, 512)])
 def test_gemm_int8_blockscaled(hq, M, N, K):
-    # K = 512: four stages (the shortest K a plan takes); 2560: twenty, the LDS ring wrapping
+    # K = 512: four stages (the shortest K a plan takes); 2560: twenty, the LDS ring wrapping;
+    # N = 100: bf16 output rows of 200 bytes, every other one off 16-byte alignment (element stores)
     from paper_2606_23406_amd import workloads
     snr = PT.op_snr("E8", 4.0)
     P = PT.oracle_params(O.E8, snr, rht_seed=51)
