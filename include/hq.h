@@ -366,8 +366,9 @@ hq_status hq_decode_gemv(hq_plan_t plan, const hq_stream* s, int64_t row0, int64
 
 /* Workspace bytes for hq_decode_attention with `batch` sequences of at most
  * max_tokens = max_blocks * block_tokens tokens and heads_q query heads:
- * the query in coded coordinates plus one partial sum (128 values, a maximum
- * and a weight) per query head and token split; 0 for invalid arguments. */
+ * the query in coded coordinates, one score per query head and token, and
+ * per query head and token split one partial sum (128 values, a maximum and
+ * a weight) and four wave maxima; 0 for invalid arguments. */
 size_t hq_attention_workspace_bytes(hq_plan_t k_plan, int64_t batch, int32_t heads_q,
                                     int64_t max_tokens);
 

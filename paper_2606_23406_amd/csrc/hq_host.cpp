@@ -635,12 +635,20 @@ static int64_t attn_splits(int64_t max_tokens, int64_t chunk) {
   return (max_tokens + per - 1) / per;
 }
 
+// The key pass's scores, one per query head and token, rounded up to 16
+// bytes so that what follows stays aligned.
+static int64_t attn_scores_floats(int64_t heads, int64_t max_tokens) {
+  return (heads * max_tokens + 3) & ~(int64_t)3;
+}
+
 size_t hq_attention_workspace_bytes(hq_plan_t k, int64_t batch, int32_t heads_q,
                                     int64_t max_tokens) {
   if (!k || batch < 0 || heads_q <= 0 || max_tokens <= 0) return 0;
   const int64_t nx = attn_splits(max_tokens, attn_chunk(k, batch, max_tokens));
   const int64_t heads = batch * heads_q;
-  return (size_t)(heads * HQ_TILE + heads * nx * (HQ_TILE + 2)) * sizeof(float);
+  return (size_t)(heads * HQ_TILE + heads * nx * HQ_TILE + attn_scores_floats(heads, max_tokens) +
+                  heads * nx * (HQ_WAVES_PER_WG + 2)) *
+         sizeof(float);
 }
 
 hq_status hq_decode_attention(hq_plan_t pk, const hq_stream* k, hq_plan_t pv, const hq_stream* v,
@@ -689,7 +697,9 @@ hq_status hq_decode_attention(hq_plan_t pk, const hq_stream* k, hq_plan_t pv, co
   const int64_t heads = batch * heads_q;
   a.qt = (float*)workspace;
   a.part_acc = a.qt + heads * HQ_TILE;
-  a.part_m = a.part_acc + heads * nx * HQ_TILE;
+  a.scores = a.part_acc + heads * nx * HQ_TILE;
+  a.wmax = a.scores + attn_scores_floats(heads, max_tokens);
+  a.part_m = a.wmax + heads * nx * HQ_WAVES_PER_WG;
   a.part_l = a.part_m + heads * nx;
   a.batch = batch;
   a.rows = std::min(k->rows, v->rows);

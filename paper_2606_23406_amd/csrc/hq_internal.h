@@ -128,6 +128,8 @@ struct hq_attn_args {
   float* part_acc;
   float* part_m;
   float* part_l;
+  float* scores;            // key pass: [batch, spr, max tokens, 4 G] base-2 scores
+  float* wmax;              // key pass: every wave's largest score per query head
   int64_t batch;
   int64_t rows;             // rows present in both streams
   int32_t heads_q, group;   // query heads, query heads per KV head

@@ -2742,6 +2742,60 @@ __device__ __forceinline__ float row16_sum(float v) {
   return v;
 }
 
+// One step of a transposed row sum over lane bit M: of the N values a lane
+// holds, the lanes with that bit set keep the upper half and the others the
+// lower half, each adding its partner's copy of the half it keeps (N = 1:
+// a plain butterfly step).
+template <int M, int N>
+__device__ __forceinline__ void tsum_step(float* d, int lane) {
+  if constexpr (N > 1) {
+    const bool up = (lane & M) != 0;
+#pragma unroll
+    for (int h = 0; h < N / 2; ++h) {
+      const float keep = up ? d[h + N / 2] : d[h];
+      const float send = up ? d[h] : d[h + N / 2];
+      d[h] = keep + xor_lane_f<M>(send);
+    }
+  } else {
+    d[0] += xor_lane_f<M>(d[0]);
+  }
+}
+
+// Sums over the 16 lanes of a row of G per-lane values at once: lane l
+// returns the sum of value (l mod 16) / (16 / G), every lane of a run of
+// 16 / G the same bits.
+template <int G>
+__device__ __forceinline__ float row16_sums(float* d, int lane) {
+  tsum_step<8, G>(d, lane);
+  tsum_step<4, (G > 1 ? G / 2 : 1)>(d, lane);
+  tsum_step<2, (G > 3 ? G / 4 : 1)>(d, lane);
+  tsum_step<1, (G > 7 ? G / 8 : 1)>(d, lane);
+  return d[0];
+}
+
+// Value of lane N of the lane's 16-lane row (DPP row_newbcast).
+template <int N>
+__device__ __forceinline__ float row_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x150 + N, 0xF, 0xF, false));
+}
+
+// v of each of the row's G head runs (lane g (16 / G) for head g).
+template <int G>
+__device__ __forceinline__ void bcast_heads(float v, float* out) {
+  out[0] = row_bcast<0>(v);
+  if constexpr (G > 1) out[1] = row_bcast<16 / G>(v);
+  if constexpr (G > 2) {
+    out[2] = row_bcast<2 * (16 / G)>(v);
+    out[3] = row_bcast<3 * (16 / G)>(v);
+  }
+  if constexpr (G > 4) {
+    out[4] = row_bcast<8>(v);
+    out[5] = row_bcast<10>(v);
+    out[6] = row_bcast<12>(v);
+    out[7] = row_bcast<14>(v);
+  }
+}
+
 // Token count of sequence b, clamped to what its table row can hold; a bad
 // value is reported in the key stream's counters.
 __device__ __forceinline__ int64_t attn_seq_len(const hq_attn_args& A, int64_t b, bool report) {
@@ -2845,53 +2899,81 @@ __device__ __forceinline__ uint32_t lane_val(uint32_t v, uint32_t i) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, (int)i);
 }
 
-template <int LAT, int G>
-__global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
+// Two passes over the same grid and token chunks.  The key pass (VAL =
+// false) decodes each key tile and stores its G scores per KV head, base 2,
+// at scores[(b, j, t), 4 G] plus every wave's largest score per head.  The
+// value pass (VAL = true) decodes each value tile and adds p g (code - U)
+// with p = 2^(s - m), m that wave's largest score, so no sum is ever
+// rescaled inside the token loop; the four waves then rescale to their
+// common maximum and write one partial per workgroup.  Each pass holds one
+// stream's decode state: the single-pass form held both plus the value sums
+// (163 registers, three waves per SIMD).  Scores, maxima and weights are
+// per lane: lane l of a row of 16 handles query head hl = (l mod 16) /
+// (16 / G) of the row's G, and the value pass broadcasts each head's weight
+// p across the row.
+// The value pass at G <= 4 is held to 128 registers (four waves per SIMD);
+// what that moves to scratch is saved before the token loop and restored
+// after it.
+template <int LAT, int G, bool VAL>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(VAL && G <= 4 ? 4 : 1)))
+void hq_attn_kernel(hq_attn_args A) {
   extern __shared__ uint32_t smem[];
   __shared__ uint32_t s_sel[256];
   __shared__ float s_m[HQ_WAVES_PER_WG][4 * G];
   __shared__ float s_l[HQ_WAVES_PER_WG][4 * G];
-  __shared__ float4 s_q[4 * G * 32];  // the workgroup's query tiles, coded coordinates
+  __shared__ float4 s_q[VAL ? 1 : 4 * G * 32];  // key pass: the query tiles, coded coordinates
   const int tid = threadIdx.x, lane = tid & 63;
   const uint32_t wave = readfirst((uint32_t)(tid >> 6));
   const uint32_t spr = (uint32_t)A.K.spr;
   const uint32_t x = blockIdx.x % (uint32_t)A.nx;
   const uint32_t bj = blockIdx.x / (uint32_t)A.nx;
   const uint32_t b = bj / spr, j = bj - b * spr;
-  const int64_t len = attn_coded_len(A, attn_seq_len(A, b, tid == 0 && x == 0 && j == 0));
+  const int64_t len =
+      attn_coded_len(A, attn_seq_len(A, b, !VAL && tid == 0 && x == 0 && j == 0));
   const int64_t wg_t0 = (int64_t)x * HQ_WAVES_PER_WG * A.chunk;
   if (wg_t0 >= len) return;  // the whole workgroup, before any barrier
+  const hq_decode_args& S = VAL ? A.V : A.K;
   s_sel[tid] = kByteSelect.e[tid];
   // KV heads 4j .. 4j+3 read query heads (4j) G .. (4j + 4) G - 1: one block
   const int64_t hq0 = (int64_t)b * A.heads_q + (int64_t)j * 4 * G;
-  for (int i = tid; i < 4 * G * 32; i += 256) s_q[i] = ((const float4*)(A.qt + hq0 * HQ_TILE))[i];
+  if constexpr (!VAL) {
+    for (int i = tid; i < 4 * G * 32; i += 256) s_q[i] = ((const float4*)(A.qt + hq0 * HQ_TILE))[i];
+  }
   __syncthreads();
   uint32_t* buf = smem + wave * (A.lds_words + 66);
   uint32_t* starts = buf + A.lds_words + 2;
   float* comb = (float*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66));
 
   const int q4 = lane >> 4, c0 = (lane & 15) * 8;
+  const int hl = (lane & 15) / (16 / G);
+  const bool lead = (lane & (16 / G - 1)) == 0;  // first lane of its head's run
   const float4* qrow = s_q + (q4 * G) * 32 + (lane & 15) * 2;  // head g: + 32 g
-  float acc[G][8], m[G], l[G];
+  // scores of (b, j): token t's 4 G heads at + 4 G t, this lane group's at + G q4
+  float* srow =
+      A.scores + (int64_t)bj * ((int64_t)A.max_blocks * A.block_tokens) * (4 * G) + q4 * G + hl;
+  float* wmax = A.wmax + ((int64_t)blockIdx.x * HQ_WAVES_PER_WG + wave) * (4 * G) + q4 * G + hl;
+  float acc[VAL ? G : 1][8];
+  float m = -__builtin_inff(), l = 0.0f;  // head hl's
+  if constexpr (VAL) {
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
+    for (int g = 0; g < G; ++g) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) acc[g][i] = 0.0f;
-    m[g] = -__builtin_inff();
-    l[g] = 0.0f;
+      for (int i = 0; i < 8; ++i) acc[g][i] = 0.0f;
+    }
   }
 
   const int64_t t0 = wg_t0 + (int64_t)wave * A.chunk;
   const int64_t t1 = t0 + A.chunk < len ? t0 + A.chunk : len;
+  if (VAL && t0 < t1) m = *wmax;  // written by the key pass for these tokens
   const uint32_t bt = (uint32_t)A.block_tokens;
   const int32_t* trow = A.table + (int64_t)b * A.max_blocks;
   bool bad = false;
   for (int64_t tb = t0; tb < t1; tb += 64) {
-    // lane i fetches token tb + i's row and both table entries (rows past the
+    // lane i fetches token tb + i's row and table entry (rows past the
     // streams or a negative block id: row ~0u, the token is skipped)
     const uint32_t n = (uint32_t)(t1 - tb < 64 ? t1 - tb : 64);
     uint32_t rv = ~0u;
-    AttnMeta mk = {0u, 0u, 0u}, mv = {0u, 0u, 0u};
+    AttnMeta me = {0u, 0u, 0u};
     if ((uint32_t)lane < n) {
       const uint32_t t = (uint32_t)(tb + lane);
       const uint32_t bi = t / bt;
@@ -2900,68 +2982,67 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
       if (blk >= 0 && r < A.rows) {
         rv = (uint32_t)r;
         const int64_t sub = r * spr + j;
-        mk = {A.K.offsets[sub], A.K.offsets[sub + 1], A.K.kparam[sub]};
-        mv = {A.V.offsets[sub], A.V.offsets[sub + 1], A.V.kparam[sub]};
+        me = {S.offsets[sub], S.offsets[sub + 1], S.kparam[sub]};
       }
     }
-    if (__ballot(rv == ~0u && (uint32_t)lane < n) && lane == 0 && A.K.stats)
+    if (!VAL && __ballot(rv == ~0u && (uint32_t)lane < n) && lane == 0 && A.K.stats)
       atomicCAS(&A.K.stats->status, 0u, (uint32_t)HQ_ERR_INVALID_ARG);  // block id out of range
-    // token i's heads and norms, each loaded one token ahead
-    auto fetch = [&](uint32_t i, uint32_t& row, DecHead& hk, DecHead& hv, float& nk, float& nv) {
+    // token i's head, norm and (value pass) scores, each loaded one token ahead
+    auto fetch = [&](uint32_t i, uint32_t& row, DecHead& h, float& nr, float& sc) {
       row = lane_val(rv, i);
       if (row != ~0u) {
-        hk = dec_head<LAT>(A.K, true, lane_val(mk.s, i), lane_val(mk.e, i), lane_val(mk.k, i), lane);
-        hv = dec_head<LAT>(A.V, true, lane_val(mv.s, i), lane_val(mv.e, i), lane_val(mv.k, i), lane);
-        nk = attn_norm(A.K, row, j, lane);
-        nv = attn_norm(A.V, row, j, lane);
+        h = dec_head<LAT>(S, true, lane_val(me.s, i), lane_val(me.e, i), lane_val(me.k, i), lane);
+        nr = attn_norm(S, row, j, lane);
+        if constexpr (VAL) sc = srow[(tb + i) * (4 * G)];
       }
     };
     uint32_t row;
-    DecHead hk, hv;
-    float nk = 0.0f, nv = 0.0f;
-    fetch(0, row, hk, hv, nk, nv);
+    DecHead hd;
+    float nr = 0.0f, sc = 0.0f;
+    fetch(0, row, hd, nr, sc);
     for (uint32_t i = 0; i < n; ++i) {
       uint32_t nrow = ~0u;
-      DecHead nhk, nhv;
-      float nnk = 0.0f, nnv = 0.0f;
-      if (i + 1 < n) fetch(i + 1, nrow, nhk, nhv, nnk, nnv);
+      DecHead nhd;
+      float nnr = 0.0f, nsc = 0.0f;
+      if (i + 1 < n) fetch(i + 1, nrow, nhd, nnr, nsc);
       if (row != ~0u) {
         float y[8];
-        bad |= !attn_tile<LAT>(A.K, hk, lane, buf, starts, s_sel, row, j, y);
-        const float gk = nk / A.K.alpha_n;
-        float s[G];
+        bad |= !attn_tile<LAT>(S, hd, lane, buf, starts, s_sel, row, j, y);
+        const float gs = nr / S.alpha_n;
+        if constexpr (!VAL) {
+          float d[G];
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float4 qa = qrow[32 * g], qb = qrow[32 * g + 1];
-          float d = qa.x * y[0];
-          d = __builtin_fmaf(qa.y, y[1], d);
-          d = __builtin_fmaf(qa.z, y[2], d);
-          d = __builtin_fmaf(qa.w, y[3], d);
-          d = __builtin_fmaf(qb.x, y[4], d);
-          d = __builtin_fmaf(qb.y, y[5], d);
-          d = __builtin_fmaf(qb.z, y[6], d);
-          d = __builtin_fmaf(qb.w, y[7], d);
-          s[g] = gk * row16_sum(d);
-        }
-        bad |= !attn_tile<LAT>(A.V, hv, lane, buf, starts, s_sel, row, j, y);
-        const float gv = nv / A.V.alpha_n;
+          for (int g = 0; g < G; ++g) {
+            const float4 qa = qrow[32 * g], qb = qrow[32 * g + 1];
+            float e = qa.x * y[0];
+            e = __builtin_fmaf(qa.y, y[1], e);
+            e = __builtin_fmaf(qa.z, y[2], e);
+            e = __builtin_fmaf(qa.w, y[3], e);
+            e = __builtin_fmaf(qb.x, y[4], e);
+            e = __builtin_fmaf(qb.y, y[5], e);
+            e = __builtin_fmaf(qb.z, y[6], e);
+            e = __builtin_fmaf(qb.w, y[7], e);
+            d[g] = e;
+          }
+          const float sl = gs * row16_sums<G>(d, lane);
+          m = __builtin_fmaxf(m, sl);
+          if (lead) srow[(tb + i) * (4 * G)] = sl;
+        } else {
+          const float p = exp2f(sc - m);
+          l += p;
+          float pg[G];
+          bcast_heads<G>(p * gs, pg);
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float mn = __builtin_fmaxf(m[g], s[g]);
-          const float a = exp2f(m[g] - mn);  // 0 for the first token (m = -inf)
-          const float p = exp2f(s[g] - mn);
-          l[g] = __builtin_fmaf(l[g], a, p);
-          const float pg = p * gv;
+          for (int g = 0; g < G; ++g) {
 #pragma unroll
-          for (int i2 = 0; i2 < 8; ++i2) acc[g][i2] = __builtin_fmaf(acc[g][i2], a, pg * y[i2]);
-          m[g] = mn;
+            for (int i2 = 0; i2 < 8; ++i2) acc[g][i2] = __builtin_fmaf(pg[g], y[i2], acc[g][i2]);
+          }
         }
       }
       row = nrow;
-      hk = nhk;
-      hv = nhv;
-      nk = nnk;
-      nv = nnv;
+      hd = nhd;
+      nr = nnr;
+      sc = nsc;
     }
   }
   if (bad && A.K.stats) {
@@ -2971,57 +3052,61 @@ __global__ __launch_bounds__(256) void hq_attn_kernel(hq_attn_args A) {
       atomicCAS(&A.K.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
     }
   }
-
-  // the four waves' sums, rescaled to their common maximum, in wave order
-  if ((lane & 15) == 0) {
+  if constexpr (!VAL) {
+    if (t0 < t1 && lead) *wmax = m;
+    return;
+  } else {
+    // the four waves' sums, rescaled to their common maximum, in wave order
+    if (lead) s_m[wave][q4 * G + hl] = m;
+    __syncthreads();
+    float M = s_m[0][q4 * G + hl];
 #pragma unroll
-    for (int g = 0; g < G; ++g) s_m[wave][q4 * G + g] = m[g];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    float M = s_m[0][q4 * G + g];
-#pragma unroll
-    for (int w = 1; w < HQ_WAVES_PER_WG; ++w) M = __builtin_fmaxf(M, s_m[w][q4 * G + g]);
-    const float f = m[g] == -__builtin_inff() ? 0.0f : exp2f(m[g] - M);
-    l[g] *= f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) acc[g][i] *= f;
-    m[g] = M;
-  }
-  if (wave > 0) {
-    float* cw = comb + ((wave - 1) * 64 + lane) * 8 * G;
+    for (int w = 1; w < HQ_WAVES_PER_WG; ++w) M = __builtin_fmaxf(M, s_m[w][q4 * G + hl]);
+    const float f = m == -__builtin_inff() ? 0.0f : exp2f(m - M);
+    l *= f;
+    m = M;
+    float fg[G];
+    bcast_heads<G>(f, fg);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      *(float4*)(cw + 8 * g) = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
-      *(float4*)(cw + 8 * g + 4) = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
-      if ((lane & 15) == 0) s_l[wave][q4 * G + g] = l[g];
-    }
-  }
-  __syncthreads();
-  if (wave == 0) {
 #pragma unroll
-    for (int w = 1; w < HQ_WAVES_PER_WG; ++w) {
-      const float* cw = comb + ((w - 1) * 64 + lane) * 8 * G;
+      for (int i = 0; i < 8; ++i) acc[g][i] *= fg[g];
+    }
+    if (wave > 0) {
+      float* cw = comb + ((wave - 1) * 64 + lane) * 8 * G;
 #pragma unroll
       for (int g = 0; g < G; ++g) {
-        const float4 a = *(const float4*)(cw + 8 * g);
-        const float4 c = *(const float4*)(cw + 8 * g + 4);
-        acc[g][0] += a.x; acc[g][1] += a.y; acc[g][2] += a.z; acc[g][3] += a.w;
-        acc[g][4] += c.x; acc[g][5] += c.y; acc[g][6] += c.z; acc[g][7] += c.w;
-        l[g] += s_l[w][q4 * G + g];
+        *(float4*)(cw + 8 * g) = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
+        *(float4*)(cw + 8 * g + 4) = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
       }
+      if (lead) s_l[wave][q4 * G + hl] = l;
     }
-    const int64_t h0 = hq0 + (int64_t)q4 * G;
+    __syncthreads();
+    if (wave == 0) {
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const int64_t pi = (h0 + g) * A.nx + x;
-      float* o = A.part_acc + pi * HQ_TILE + c0;
-      *(float4*)o = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
-      *(float4*)(o + 4) = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
-      if ((lane & 15) == 0) {
-        A.part_m[pi] = m[g];
-        A.part_l[pi] = l[g];
+      for (int w = 1; w < HQ_WAVES_PER_WG; ++w) {
+        const float* cw = comb + ((w - 1) * 64 + lane) * 8 * G;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+          const float4 a = *(const float4*)(cw + 8 * g);
+          const float4 c = *(const float4*)(cw + 8 * g + 4);
+          acc[g][0] += a.x; acc[g][1] += a.y; acc[g][2] += a.z; acc[g][3] += a.w;
+          acc[g][4] += c.x; acc[g][5] += c.y; acc[g][6] += c.z; acc[g][7] += c.w;
+        }
+        l += s_l[w][q4 * G + hl];
+      }
+      const int64_t h0 = hq0 + (int64_t)q4 * G;
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int64_t pi = (h0 + g) * A.nx + x;
+        float* o = A.part_acc + pi * HQ_TILE + c0;
+        *(float4*)o = make_float4(acc[g][0], acc[g][1], acc[g][2], acc[g][3]);
+        *(float4*)(o + 4) = make_float4(acc[g][4], acc[g][5], acc[g][6], acc[g][7]);
+      }
+      if (lead) {
+        const int64_t pi = (h0 + hl) * A.nx + x;
+        A.part_m[pi] = m;
+        A.part_l[pi] = l;
       }
     }
   }
@@ -4032,10 +4117,11 @@ int hq_launch_decode_attention(const hq_attn_args& a, int lattice, void* stream)
   const uint32_t heads = (uint32_t)((a.batch * a.heads_q + 15) / 16);
   hipLaunchKernelGGL(hq_attn_prep_kernel, dim3(heads), dim3(256), 0, st, a);
   const uint32_t nwg = (uint32_t)(a.batch * a.K.spr * a.nx);
-  const size_t lds = ((size_t)HQ_WAVES_PER_WG * (a.lds_words + 66) +
-                      (size_t)(HQ_WAVES_PER_WG - 1) * 64 * 8 * a.group) * 4;
-#define HQ_ATTN_CASE(L, GG) \
-  hipLaunchKernelGGL((hq_attn_kernel<L, GG>), dim3(nwg), dim3(256), lds, st, a)
+  const size_t lds_k = (size_t)HQ_WAVES_PER_WG * (a.lds_words + 66) * 4;
+  const size_t lds_v = lds_k + (size_t)(HQ_WAVES_PER_WG - 1) * 64 * 8 * a.group * 4;
+#define HQ_ATTN_CASE(L, GG)                                                                  \
+  hipLaunchKernelGGL((hq_attn_kernel<L, GG, false>), dim3(nwg), dim3(256), lds_k, st, a); \
+  hipLaunchKernelGGL((hq_attn_kernel<L, GG, true>), dim3(nwg), dim3(256), lds_v, st, a)
 #define HQ_ATTN_GROUPS(L)           \
   switch (a.group) {                \
     case 1: HQ_ATTN_CASE(L, 1); break; \
