@@ -44,7 +44,8 @@ KERNELS = {
     "gemm_mxfp4": "hq_gemm_mx4_kernel",
     "decode_gemv": "hq_decode_gemv_kernel",
     "decode_gemv_rows": "hq_decode_gemv_rows_kernel",
-    "attention": "hq_attn_kernel",
+    "attention_keys": "hq_attn_kernel<0, 4, false>",
+    "attention_values": "hq_attn_kernel<0, 4, true>",
     "copy": "__amd_rocclr_copyBuffer",
 }
 CODEC = ("encode", "decode")
