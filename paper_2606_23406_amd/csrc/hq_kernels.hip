@@ -370,6 +370,54 @@ __device__ __forceinline__ float code_coord(int32_t c, int j) {
   }
 }
 
+// E8's U = b - Q(b) for a box point b in [-2, 2)^8 whose coordinates are
+// multiples of 2^-22: the point quant_e8 picks, without its roundings and
+// branches.  Every coset error is exact here: the even coset's is
+// b - 2 rint(b / 2) (rint by the 1.5 * 2^23 shift, whose low bit is k's
+// parity), the odd coset's b - sign(b) (floor(b / 2) is 0 or -1), and
+// neither is ever -0.  Each coset's parity fix moves the first coordinate of
+// largest error by 2 toward zero error's other side (e - 2 sign(e)); the
+// squared errors are summed in the same fp32 tree as quant_e8's, and U is
+// the nearer coset's error vector (the even one on a tie).
+__device__ __forceinline__ void dither_e8(const float* b, float* u) {
+  constexpr float kShift = 12582912.0f;  // 1.5 * 2^23
+  float ea[8], eb[8];
+  uint32_t pa = 0, pb = 0;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float t = b[i] * 0.5f + kShift;
+    ea[i] = __builtin_fmaf(-2.0f, t - kShift, b[i]);
+    pa ^= __float_as_uint(t);
+    const uint32_t sb = __float_as_uint(b[i]) & 0x80000000u;
+    eb[i] = b[i] - __uint_as_float(sb | 0x3F800000u);
+    pb ^= sb;
+  }
+  auto fix = [](float* e, bool odd) {
+    float m = __builtin_fabsf(e[0]);
+#pragma unroll
+    for (int i = 1; i < 8; ++i) m = __builtin_fmaxf(m, __builtin_fabsf(e[i]));
+    bool done = !odd;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const bool hit = !done && __builtin_fabsf(e[i]) == m;
+      const float two = __uint_as_float((__float_as_uint(e[i]) & 0x80000000u) | 0x40000000u);
+      e[i] = hit ? e[i] - two : e[i];
+      done = done || hit;
+    }
+  };
+  fix(ea, pa & 1u);
+  fix(eb, pb >> 31);
+  float sa[8], sq[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    sa[i] = ea[i] * ea[i];
+    sq[i] = eb[i] * eb[i];
+  }
+  const bool even = tree8(sa) <= tree8(sq);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) u[i] = even ? ea[i] : eb[i];
+}
+
 // Dither U = b - Q(b) for the lane's 8 coordinates (columns col0 .. col0+7 of
 // global row `row`, col0 a multiple of 8): b is a uniform point of a box that
 // is a fundamental domain of a sublattice ([-2, 2)^m for 2E8, D4, Z;
@@ -392,10 +440,14 @@ __device__ __forceinline__ void dither8(uint64_t seed, int64_t row, int64_t col0
       b[i] = centered * 0x1p-22f;
     }
   }
-  int32_t c[8];
-  quantize8<LAT>(b, c);
+  if constexpr (LAT == kE8) {
+    dither_e8(b, u);
+  } else {
+    int32_t c[8];
+    quantize8<LAT>(b, c);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) u[i] = b[i] - code_coord<LAT>(c[i], i);
+    for (int i = 0; i < 8; ++i) u[i] = b[i] - code_coord<LAT>(c[i], i);
+  }
 }
 
 // --------------------------------------------------------------- strip / unstrip
