@@ -375,10 +375,11 @@ __device__ __forceinline__ float code_coord(int32_t c, int j) {
 // branches.  Every coset error is exact here: the even coset's is
 // b - 2 rint(b / 2) (rint by the 1.5 * 2^23 shift, whose low bit is k's
 // parity), the odd coset's b - sign(b) (floor(b / 2) is 0 or -1), and
-// neither is ever -0.  Each coset's parity fix moves the first coordinate of
-// largest error by 2 toward zero error's other side (e - 2 sign(e)); the
-// squared errors are summed in the same fp32 tree as quant_e8's, and U is
-// the nearer coset's error vector (the even one on a tie).
+// neither is ever -0.  A coset whose parity is odd moves its first
+// coordinate of largest error to the next point on the other side, which
+// turns that error e into e - 2 sign(e); the squared errors are summed in
+// the same fp32 tree as quant_e8's, and U is the nearer coset's error vector
+// (the even one on a tie).
 __device__ __forceinline__ void dither_e8(const float* b, float* u) {
   constexpr float kShift = 12582912.0f;  // 1.5 * 2^23
   float ea[8], eb[8];
@@ -2579,6 +2580,157 @@ __global__ __launch_bounds__(256) void hq_decode_tiled_kernel(hq_decode_args A) 
   decode_wg_tiled<LAT, MODE>(A, blockIdx.x);
 }
 
+// ------------------------------------------------------------ qjl decode on the matrix cores
+// KV streams with the qjl rotation, decoded to fp32 or bf16.  S^T y is a
+// dense 128 x 128 contraction per tile, so it runs on the fp32 matrix cores
+// (v_mfma_f32_16x16x4_f32) instead of the VALU with S streamed from LDS.
+// A workgroup takes 16 consecutive sub-streams (64 tiles) per pass:
+//  1. each wave decodes its four sub-streams, undithers them and writes
+//     y = code - U into the workgroup's tile array Y in LDS (tile rows of
+//     kQjlRow floats: the 16 rows one operand load reads fall in distinct
+//     banks);
+//  2. wave w forms columns 32 w .. 32 w + 31 of Z = Y S for all 64 tiles
+//     (row z of Z is (S^T y)^T) with its 32 columns of S held in registers,
+//     then, once every wave has read Y, writes them over it;
+//  3. each wave finishes its own tiles from Z: inverse RHT, scale, signs,
+//     store.
+// The contraction sums in the matrix cores' order, so the output equals
+// the oracle's left-to-right fp32 sums to rounding, not bit for bit.
+typedef float v4f_t __attribute__((ext_vector_type(4)));
+constexpr int kQjlRow = 130;            // floats per tile row of Y
+constexpr int kQjlTiles = 64;           // tiles per workgroup pass (16 sub-streams)
+
+template <int LAT, int MODE>
+__global__ __launch_bounds__(256) void hq_decode_qjl_kernel(hq_decode_args A) {
+  extern __shared__ uint32_t smem[];
+  __shared__ uint32_t s_sel[256];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const uint32_t wave = readfirst((uint32_t)(tid >> 6));
+  uint32_t* buf = smem + wave * (A.lds_words + 66);
+  uint32_t* starts = buf + A.lds_words + 2;
+  float* const Y = (float*)(smem + HQ_WAVES_PER_WG * (A.lds_words + 66));
+  s_sel[tid] = byte_select_entry((uint32_t)tid);
+  // B operands: step s covers k = 4 s .. 4 s + 3 (lane / 16 picks k), block
+  // cb the columns n = 32 wave + 16 cb + lane % 16
+  float sb[32][2];
+#pragma unroll
+  for (int s = 0; s < 32; ++s) {
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+      sb[s][cb] = A.qjl[(4 * s + (lane >> 4)) * HQ_TILE + 32 * (int)wave + 16 * cb + (lane & 15)];
+  }
+  __syncthreads();
+  const TwSigns sg(lane);
+  const uint32_t nsub = (uint32_t)A.nsub, spr = (uint32_t)A.spr;
+  const uint32_t ngroups = (nsub + 15u) / 16u;
+  for (uint32_t grp = blockIdx.x; grp < ngroups; grp += gridDim.x) {
+    const uint32_t sub0 = grp * 16u + wave * 4u;
+    // ---- 1. decode into Y rows wave * 16 + 4 i + lane / 16
+    float gi[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t sub = sub0 + (uint32_t)i;
+      gi[i] = 0.0f;
+      if (sub >= nsub) continue;  // wave-uniform; the row's Z is never stored
+      const uint32_t o0 = readfirst(A.offsets[(uint32_t)A.first_sub + sub]);
+      const uint32_t o1 = readfirst(A.offsets[(uint32_t)A.first_sub + sub + 1]);
+      const uint32_t kb = readfirst(A.kparam[(uint32_t)A.first_sub + sub]);
+      const DecHead head = dec_head<LAT>(A, true, o0, o1, kb, lane);
+      const int64_t t = A.first_row * A.tpr + 4 * (int64_t)sub + (lane >> 4);
+      const float rs = A.norm_fp16 ? (float)((const _Float16*)A.norms)[t] : ((const float*)A.norms)[t];
+      const uint32_t lrow = sub / spr;
+      const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
+      uint32_t sym[8];
+      const bool ok = decode_symbols<LAT>(A, head, lane, buf, starts, s_sel, sym);
+      const unsigned long long bad = __ballot(!ok);
+      if (bad && A.stats && (unsigned)lane == (unsigned)__builtin_ctzll(bad)) {
+        atomicAdd(&A.stats->corrupt_substreams, 1u);
+        atomicCAS(&A.stats->status, 0u, (uint32_t)HQ_ERR_CORRUPT);
+      }
+      gi[i] = bad ? 0.0f : rs / A.alpha_n;  // a corrupt sub-stream decodes as zeros
+      int32_t c[8];
+      unstrip8<LAT>(sym, c);
+      float y[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[j] = code_coord<LAT>(c[j], j);
+      if (A.dither) {
+        float u[8];
+        dither8<LAT>(A.dither_seed, A.first_row + lrow, col, u);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = y[j] - u[j];
+      }
+      float* row = Y + (wave * 16u + 4u * (uint32_t)i + (uint32_t)(lane >> 4)) * kQjlRow + (lane & 15) * 8;
+#pragma unroll
+      for (int j = 0; j < 8; j += 2) *(float2*)(row + j) = make_float2(y[j], y[j + 1]);
+    }
+    __syncthreads();
+    // ---- 2. Z[:, 32 wave .. +31] = Y S
+    v4f_t acc[4][2];
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) acc[rb][cb] = v4f_t{0.0f, 0.0f, 0.0f, 0.0f};
+    }
+#pragma unroll  // sb is indexed by s: only a full unroll keeps it in registers
+    for (int s = 0; s < 32; ++s) {
+#pragma unroll
+      for (int rb = 0; rb < 4; ++rb) {
+        const float a = Y[(rb * 16 + (lane & 15)) * kQjlRow + 4 * s + (lane >> 4)];
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          acc[rb][cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, sb[s][cb], acc[rb][cb], 0, 0, 0);
+      }
+    }
+    __syncthreads();  // every wave has read Y
+#pragma unroll
+    for (int rb = 0; rb < 4; ++rb) {
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          Y[(rb * 16 + 4 * (lane >> 4) + r) * kQjlRow + 32 * (int)wave + 16 * cb + (lane & 15)] = acc[rb][cb][r];
+      }
+    }
+    __syncthreads();
+    // ---- 3. this wave's tiles: inverse RHT, scale, signs, store
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t sub = sub0 + (uint32_t)i;
+      if (sub >= nsub) break;
+      const uint32_t lrow = sub / spr;
+      const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
+      const float* row = Y + (wave * 16u + 4u * (uint32_t)i + (uint32_t)(lane >> 4)) * kQjlRow + (lane & 15) * 8;
+      float y[8];
+#pragma unroll
+      for (int j = 0; j < 8; j += 2) {
+        const float2 v = *(const float2*)(row + j);
+        y[j] = v.x;
+        y[j + 1] = v.y;
+      }
+      fwht128_tw(y, sg);
+      const float g_tw = xor_sign(gi[i], sg.sigma);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) y[j] = y[j] * g_tw;
+      if constexpr (MODE == 0) {
+        const uint32_t dbits = sign_bits8(A.dmask, col);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) y[j] = flip(y[j], dbits, j);
+        float4* out = (float4*)((float*)A.y + (int64_t)lrow * A.ld + col);
+        out[0] = make_float4(y[0], y[1], y[2], y[3]);
+        out[1] = make_float4(y[4], y[5], y[6], y[7]);
+      } else {
+        const uint4 sw = *(const uint4*)(A.dsign16 + (col >> 1));
+        uint4 o;
+        o.x = cvt_pk_bf16(y[0], y[1]) ^ sw.x;
+        o.y = cvt_pk_bf16(y[2], y[3]) ^ sw.y;
+        o.z = cvt_pk_bf16(y[4], y[5]) ^ sw.z;
+        o.w = cvt_pk_bf16(y[6], y[7]) ^ sw.w;
+        *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = o;
+      }
+    }
+  }
+}
+
 template <int LAT, int MODE, bool KV>
 __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
   decode_wg<LAT, MODE, KV>(A, blockIdx.x);
@@ -3980,11 +4132,39 @@ static uint32_t decode_wgs(int64_t nsub) {
   return (uint32_t)((nsub + per_wg - 1) / per_wg);
 }
 
+// qjl streams of tile 128: the matrix-core decode, a grid of workgroups
+// that each take every gridDim-th pass of 16 sub-streams.
+template <int LAT>
+int launch_decode_qjl(const hq_decode_args& a, int mode, hipStream_t st) {
+  const int64_t ngroups = (a.nsub + 15) / 16;
+  if (ngroups == 0) return 0;
+  const uint32_t nwg = (uint32_t)std::min<int64_t>(ngroups, 2048);
+  const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t) +
+                     (size_t)kQjlTiles * kQjlRow * sizeof(float);
+  static size_t granted0 = 0, granted1 = 0;
+  if (mode == 0) {
+    allow_lds((const void*)hq_decode_qjl_kernel<LAT, 0>, lds, granted0);
+    hipLaunchKernelGGL((hq_decode_qjl_kernel<LAT, 0>), dim3(nwg), dim3(256), lds, st, a);
+  } else {
+    allow_lds((const void*)hq_decode_qjl_kernel<LAT, 1>, lds, granted1);
+    hipLaunchKernelGGL((hq_decode_qjl_kernel<LAT, 1>), dim3(nwg), dim3(256), lds, st, a);
+  }
+  return (int)hipGetLastError();
+}
+
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   const int mode = (yt == HQ_FP32) ? 0 : 1;
   const bool kv = kv_variant(p);
   const uint32_t nwg = decode_wgs(a.nsub * a.mb), lw = a.lds_words;
+  if (a.qjl && p->tile == HQ_TILE && p->substream == HQ_SUB) {
+    switch (p->lattice) {
+      case HQ_E8: return launch_decode_qjl<kE8>(a, mode, st);
+      case HQ_D4: return launch_decode_qjl<kD4>(a, mode, st);
+      case HQ_A2: return launch_decode_qjl<kA2>(a, mode, st);
+      default: return launch_decode_qjl<kZ>(a, mode, st);
+    }
+  }
   if (p->tile != HQ_TILE || p->substream != HQ_SUB) {
     switch (p->lattice) {
       case HQ_E8: return launch_decode_tiled<kE8>(a, nwg, mode, st);

@@ -1,8 +1,9 @@
 """GPU parity of the qjl rotation (Sec. 4.2: encode applies a caller-supplied
 orthogonal S after the normalization, decode S^T after the undither), against
-the oracle: KV streams (dither, fp16 norms, appended in chunks) bit-exact on
-every lattice, the fused attention over qjl streams, and the entry points
-that take no qjl plan.  S is a Haar draw made on the host (QR of a seeded
+the oracle: KV streams (dither, fp16 norms, appended in chunks) with codes
+and words bit-exact on every lattice and the decode within 1e-5 of the
+lattice unit (its S^T y runs on the matrix cores), the fused attention over
+qjl streams, and the entry points that take no qjl plan.  S is a Haar draw made on the host (QR of a seeded
 Gaussian matrix with the sign fix)."""
 import numpy as np
 import pytest
