@@ -233,7 +233,9 @@ hq_status hq_encode_group(const hq_plan_t* plans, const void* const* x, int32_t 
  * for rows row0 .. row0+rows-1 of s into y (device, element type yt =
  * HQ_BF16 or HQ_FP32, row stride ld).  A sub-stream whose offsets or bits are
  * inconsistent is decoded as zeros and counted in s->stats (never read out of
- * bounds).  Errors: HQ_ERR_INVALID_ARG, HQ_ERR_HIP. */
+ * bounds).  With a qjl plan (Sec. 4.2) the product S^T y of each tile runs on
+ * the fp32 matrix cores, whose summation order differs from a left-to-right
+ * sum by rounding only.  Errors: HQ_ERR_INVALID_ARG, HQ_ERR_HIP. */
 hq_status hq_decode(hq_plan_t plan, const hq_stream* s, int64_t row0, int64_t rows, void* y,
                     int32_t yt, int64_t ld, void* stream);
 /* (A corrupt sub-stream's 512 outputs are all +-0, dithered streams too: the
