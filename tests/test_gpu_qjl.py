@@ -99,3 +99,24 @@ def test_qjl_plan_rules(hq):
     with pytest.raises(hq.HQError):  # nor the int8 codes path (rotated codes)
         hq.hq_decode_int8(plan, s)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("row0,rows", [(0, 7), (5, 33), (37, 13), (49, 1)])
+def test_qjl_partial_decodes_match_the_whole(hq, row0, rows):
+    # the matrix-core decode takes 16 sub-streams per pass; a tile's result
+    # does not depend on which tiles share its pass, so a row range decoded
+    # alone (ragged passes, row0 past the first pass) equals those rows of
+    # the whole decode bit for bit, in fp32 and in bf16
+    P = PT.oracle_params(O.E8, SNR[O.E8], rht_seed=6, rotation=2, dither=True, dither_seed=7,
+                         norm_fp16=True, qjl=haar(8))
+    x = gauss(50, 1024, 9, 1.0, torch.bfloat16)
+    plan = PT.gpu_plan(hq, P, SNR[O.E8], 1024)
+    s = hq.EncodedStream(plan, 50)
+    hq.hq_encode(plan, x.cuda(), s)
+    print(f"[qjl] partial decode rows {row0}..{row0 + rows - 1} of 50", flush=True)
+    for dt in (torch.float32, torch.bfloat16):
+        whole = hq.hq_decode(plan, s, out_dtype=dt)
+        part = hq.hq_decode(plan, s, row0=row0, rows=rows, out_dtype=dt)
+        torch.cuda.synchronize()
+        assert torch.equal(part.cpu(), whole[row0:row0 + rows].cpu()), dt
+    assert s.read_stats()["status"] == 0
