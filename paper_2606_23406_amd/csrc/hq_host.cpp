@@ -134,7 +134,7 @@ double code_norm_bound(const hq_plan_s& p) {
 }
 
 int64_t substream_word_bound(const hq_plan_s& p) {
-  const int n = p.tile, m = p.dim, S = p.substream;
+  const int n = p.tile, S = p.substream;
   const double T = (double)S / n;
   const double cn = code_norm_bound(p);
   // a sub-stream of whole tiles sums T tiles' bounds; a sub-stream inside a
@@ -305,7 +305,10 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
     delete p;
     return HQ_ERR_UNSUPPORTED;
   }
-  hipGetDevice(&p->device);
+  if (hipGetDevice(&p->device) != hipSuccess) {
+    delete p;
+    return HQ_ERR_HIP;
+  }
 
   // sign bitmasks: bit j set means the sign is -1
   const int64_t nw = (cols + 31) / 32;
@@ -345,11 +348,11 @@ hq_status hq_plan(int32_t tile, int32_t lattice, float bps, uint64_t rht_seed, i
        hipMemcpy(p->d_dsign16, ds.data(), sizeof(uint32_t) * (size_t)npairs,
                  hipMemcpyHostToDevice) == hipSuccess;
   if (!ok) {
-    if (p->d_dmask) hipFree(p->d_dmask);
-    if (p->d_smask) hipFree(p->d_smask);
-    if (p->d_dsign16) hipFree(p->d_dsign16);
-    if (p->d_qjl) hipFree(p->d_qjl);
-    if (p->d_qjlt) hipFree(p->d_qjlt);
+    // the error reported is the failed allocation or copy; the frees are
+    // best effort
+    for (void* d : {(void*)p->d_dmask, (void*)p->d_smask, (void*)p->d_dsign16, (void*)p->d_qjl,
+                    (void*)p->d_qjlt})
+      if (d) (void)hipFree(d);
     delete p;
     return HQ_ERR_HIP;
   }
@@ -377,13 +380,12 @@ hq_status hq_plan_get_info(hq_plan_t p, hq_plan_info* info) {
 
 hq_status hq_plan_destroy(hq_plan_t p) {
   if (!p) return HQ_ERR_INVALID_ARG;
-  hipFree(p->d_dmask);
-  hipFree(p->d_smask);
-  hipFree(p->d_dsign16);
-  if (p->d_qjl) hipFree(p->d_qjl);
-  if (p->d_qjlt) hipFree(p->d_qjlt);
+  bool ok = true;
+  for (void* d : {(void*)p->d_dmask, (void*)p->d_smask, (void*)p->d_dsign16, (void*)p->d_qjl,
+                  (void*)p->d_qjlt})
+    if (d) ok = hipFree(d) == hipSuccess && ok;
   delete p;
-  return HQ_OK;
+  return ok ? HQ_OK : HQ_ERR_HIP;
 }
 
 // Sub-streams per wave of an encode of nsub sub-streams: one for small

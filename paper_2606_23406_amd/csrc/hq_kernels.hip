@@ -1338,7 +1338,7 @@ __device__ __forceinline__ void encode_substream(const hq_encode_args& A, const 
   }
 
   // ---- Rice parameters (wave-uniform), quotients and the unary-length scan
-  uint32_t k0, k1, qv[8], ulen, uincl;
+  uint32_t k0, k1, qv[8], ulen, uincl = 0;  // uincl: set by the k* scan or below
   bool scanned = false;
   if constexpr (LAT == kE8 || LAT == kZ) {
     uint32_t s0 = 0;
