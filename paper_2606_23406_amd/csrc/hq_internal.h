@@ -20,6 +20,7 @@
 // a small matrix or a KV append does not leave each SIMD a single long wave.
 #define HQ_ENC_SMALL_SUBS 16384
 #define HQ_DEC_SUBS_PER_WAVE 4   // decode: consecutive sub-streams per wave
+#define HQ_DEC_SMALL 16384       // single decodes below this many sub-streams: one per wave
 #define HQ_SCAN_STATUS_OFFSET 128  // bytes before the look-back status array
 
 // Plan: immutable after hq_plan returns.

@@ -2172,7 +2172,9 @@ __device__ __forceinline__ bool decode_symbols(const hq_decode_args& A, const De
   return ok;
 }
 
-template <int LAT, int MODE, bool KV>
+// SPW consecutive sub-streams per wave: 4, or 1 for launches too small to
+// fill the chip with four per wave.
+template <int LAT, int MODE, bool KV, int SPW = HQ_DEC_SUBS_PER_WAVE>
 __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_t wgi) {
   extern __shared__ uint32_t smem[];
   __shared__ uint32_t s_sel[256];
@@ -2194,29 +2196,30 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   s_sel[tid] = byte_select_entry((uint32_t)tid);  // 256 threads, one entry each
   __syncthreads();
 
-  // this wave's sub-streams: HQ_DEC_SUBS_PER_WAVE consecutive ones; their
-  // table entries are read at once, each one's payload one sub-stream ahead
-  const uint32_t sub0 = (wgi * HQ_WAVES_PER_WG + wave) * HQ_DEC_SUBS_PER_WAVE;
+  // this wave's sub-streams: SPW consecutive ones; their table entries are
+  // read at once, each one's payload one sub-stream ahead
+  const uint32_t sub0 = (wgi * HQ_WAVES_PER_WG + wave) * SPW;
   const uint32_t nsub = (uint32_t)A.nsub;
-  uint32_t off[HQ_DEC_SUBS_PER_WAVE + 1], kbs[HQ_DEC_SUBS_PER_WAVE];
+  uint32_t off[SPW + 1], kbs[SPW];
 #pragma unroll
-  for (int i = 0; i <= HQ_DEC_SUBS_PER_WAVE; ++i) {
+  for (int i = 0; i <= SPW; ++i) {
     const uint32_t sub = sub0 + (uint32_t)i;
     off[i] = sub <= nsub ? readfirst(A.offsets[(uint32_t)A.first_sub + sub]) : 0u;
-    if (i < HQ_DEC_SUBS_PER_WAVE)
+    if (i < SPW)
       kbs[i] = sub < nsub ? readfirst(A.kparam[(uint32_t)A.first_sub + sub]) : 0u;
   }
   DecHead head = dec_head<LAT>(A, sub0 < nsub, off[0], off[1], kbs[0], lane);
   const uint32_t spr = (uint32_t)A.spr;
   const TwSigns sg(lane);
   const uint32_t sbits = use_rot ? sign_bits8(A.smask, (lane & 15) * 8) : 0u;
-  // tile factors g = r_s / (alpha n), once for the wave's 16 tiles: lane l
-  // takes sub-stream l & 3, tile l >> 4 (rows are contiguous, 4 tiles per
-  // sub-stream); sub-stream i reads them back by a quad broadcast
-  static_assert(HQ_DEC_SUBS_PER_WAVE == 4, "one sub-stream per lane of a quad");
+  // tile factors g = r_s / (alpha n), once for the wave's tiles: lane l
+  // takes sub-stream l & 3 (SPW = 4) or the one sub-stream, and tile l >> 4
+  // (rows are contiguous, 4 tiles per sub-stream); with four, sub-stream i
+  // reads them back by a quad broadcast
+  static_assert(SPW == 4 || SPW == 1, "one sub-stream per lane of a quad, or one per wave");
   float gm = 0.0f;
   {
-    const uint32_t subq = sub0 + (uint32_t)(lane & 3);
+    const uint32_t subq = sub0 + (SPW == 4 ? (uint32_t)(lane & 3) : 0u);
     if (subq < nsub) {
       // the casts (MODE >= 2) also serve long-tile weight plans: tile of the
       // 128 columns at flat position subq * 512 + 128 (lane >> 4)
@@ -2230,11 +2233,11 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
   }
 
 #pragma unroll
-  for (int i = 0; i < HQ_DEC_SUBS_PER_WAVE; ++i) {
+  for (int i = 0; i < SPW; ++i) {
     const uint32_t sub = sub0 + (uint32_t)i;
     if (sub >= nsub) break;
     DecHead next;
-    if (i + 1 < HQ_DEC_SUBS_PER_WAVE)
+    if (i + 1 < SPW)
       next = dec_head<LAT>(A, sub + 1 < nsub, off[i + 1], off[i + 2], kbs[i + 1], lane);
     const uint32_t lrow = sub / spr;
     const uint32_t col = (sub - lrow * spr) * HQ_SUB + 8u * (uint32_t)lane;
@@ -2255,7 +2258,9 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
     }
     int32_t c[8];
     unstrip8<LAT>(sym, c);
-    float g = i == 0 ? quad_bcast<0>(gm) : (i == 1 ? quad_bcast<1>(gm) : (i == 2 ? quad_bcast<2>(gm) : quad_bcast<3>(gm)));
+    float g = SPW == 1 ? gm
+                       : (i == 0 ? quad_bcast<0>(gm)
+                                 : (i == 1 ? quad_bcast<1>(gm) : (i == 2 ? quad_bcast<2>(gm) : quad_bcast<3>(gm))));
     if (bad) g = 0.0f;  // a corrupt sub-stream decodes as zeros, dither included
 
     if constexpr (MODE == 2) {
@@ -2350,7 +2355,7 @@ __device__ __forceinline__ void decode_wg(const hq_decode_args& A, const uint32_
         *(uint4*)((uint16_t*)A.y + (int64_t)lrow * A.ld + col) = o;
       }
     }
-    if (i + 1 < HQ_DEC_SUBS_PER_WAVE) head = next;
+    if (i + 1 < SPW) head = next;
   }
 }
 
@@ -2734,6 +2739,12 @@ __global__ __launch_bounds__(256) void hq_decode_qjl_kernel(hq_decode_args A) {
 template <int LAT, int MODE, bool KV>
 __global__ __launch_bounds__(256) void hq_decode_kernel(hq_decode_args A) {
   decode_wg<LAT, MODE, KV>(A, blockIdx.x);
+}
+
+// Single matrices of fewer than HQ_DEC_SMALL sub-streams: one per wave.
+template <int LAT, int MODE, bool KV>
+__global__ __launch_bounds__(256) void hq_decode_small_kernel(hq_decode_args A) {
+  decode_wg<LAT, MODE, KV, 1>(A, blockIdx.x);
 }
 
 template <int LAT, int MODE, bool KV>
@@ -4152,6 +4163,26 @@ int launch_decode_qjl(const hq_decode_args& a, int mode, hipStream_t st) {
   return (int)hipGetLastError();
 }
 
+// A single matrix of fewer than HQ_DEC_SMALL sub-streams, fp32 or bf16 out:
+// one sub-stream per wave, so that its workgroups spread over more of the
+// chip than four per wave would.
+template <int LAT>
+int launch_decode_small(const hq_decode_args& a, int mode, bool kv, hipStream_t st) {
+  const uint32_t nwg = (uint32_t)((a.nsub + HQ_WAVES_PER_WG - 1) / HQ_WAVES_PER_WG);
+  const size_t lds = (size_t)(a.lds_words + 66) * HQ_WAVES_PER_WG * sizeof(uint32_t);
+  static size_t granted[4] = {0, 0, 0, 0};
+#define HQ_SMALL_CASE(M, K, I)                                                             \
+  allow_lds((const void*)hq_decode_small_kernel<LAT, M, K>, lds, granted[I]);              \
+  hipLaunchKernelGGL((hq_decode_small_kernel<LAT, M, K>), dim3(nwg), dim3(256), lds, st, a)
+  if (mode == 0) {
+    if (kv) { HQ_SMALL_CASE(0, true, 0); } else { HQ_SMALL_CASE(0, false, 1); }
+  } else {
+    if (kv) { HQ_SMALL_CASE(1, true, 2); } else { HQ_SMALL_CASE(1, false, 3); }
+  }
+#undef HQ_SMALL_CASE
+  return (int)hipGetLastError();
+}
+
 int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* stream) {
   hipStream_t st = (hipStream_t)stream;
   const int mode = (yt == HQ_FP32) ? 0 : 1;
@@ -4163,6 +4194,15 @@ int hq_launch_decode(const hq_plan_s* p, const hq_decode_args& a, int yt, void* 
       case HQ_D4: return launch_decode_qjl<kD4>(a, mode, st);
       case HQ_A2: return launch_decode_qjl<kA2>(a, mode, st);
       default: return launch_decode_qjl<kZ>(a, mode, st);
+    }
+  }
+  if (!a.qjl && a.nsub < HQ_DEC_SMALL && p->tile == HQ_TILE && p->substream == HQ_SUB) {
+    if (a.nsub == 0) return 0;
+    switch (p->lattice) {
+      case HQ_E8: return launch_decode_small<kE8>(a, mode, kv, st);
+      case HQ_D4: return launch_decode_small<kD4>(a, mode, kv, st);
+      case HQ_A2: return launch_decode_small<kA2>(a, mode, kv, st);
+      default: return launch_decode_small<kZ>(a, mode, kv, st);
     }
   }
   if (p->tile != HQ_TILE || p->substream != HQ_SUB) {
