@@ -307,6 +307,33 @@ def test_launch_shapes_agree_at_the_small_launch_bound(hq, rows):
     assert a.read_stats() == b.read_stats()
 
 
+
+@pytest.mark.parametrize("kv", [False, True])
+def test_decode_launch_shapes_agree(hq, kv):
+    """A single decode of fewer than 16384 sub-streams runs one sub-stream per
+    wave, a larger one and every group launch four per wave: 2049 x 4096
+    (16392 sub-streams) decoded whole, in two row ranges below the bound and
+    as a group member gives the same values, fp32 and bf16."""
+    print(f"[parity] decode launch shapes kv={kv}", flush=True)
+    opts = dict(rotation=1, rot_seed=5, dither=True, dither_seed=6, norm_fp16=True) if kv else {}
+    plan = hq.hq_plan(128, O.E8, 0.0, 79, -1, 4096, snr_db=20.0, **opts)
+    rows = 2049
+    x = gauss(rows, 4096, 80, 0.02, torch.bfloat16).cuda()
+    s = hq.EncodedStream(plan, rows)
+    hq.hq_encode(plan, x, s)
+    for dt in (torch.float32, torch.bfloat16):
+        whole = hq.hq_decode(plan, s, out_dtype=dt)
+        lo = hq.hq_decode(plan, s, row0=0, rows=1024, out_dtype=dt)
+        hi = hq.hq_decode(plan, s, row0=1024, rows=rows - 1024, out_dtype=dt)
+        torch.cuda.synchronize()
+        assert torch.equal(torch.cat([lo, hi]).cpu(), whole.cpu()), dt
+        if not kv:  # the group launch checked on the weight plan
+            g = torch.empty_like(whole)
+            hq.hq_decode_group([plan], [s], [g])
+            torch.cuda.synchronize()
+            assert torch.equal(g.cpu(), whole.cpu()), dt
+    assert s.read_stats()["status"] == 0
+
 @pytest.mark.parametrize("lat", [O.E8, O.D4, O.A2, O.Z])
 def test_decode_gemv_matches_oracle(hq, lat):
     """hq_decode_gemv (the decode fused with a matrix-vector product) against
